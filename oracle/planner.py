@@ -1,0 +1,171 @@
+"""Reference planners for intermediate tensors (Sec. 5 of the paper).
+
+TEST INFRASTRUCTURE ONLY (see oracle/__init__.py).
+
+A problem is given as ``ops``: a list, in execution (topological) order, of
+``(outputs, inputs)`` tensor-id lists, plus ``sizes`` (bytes per tensor id) and
+the set of ``intermediate`` tensor ids (neither a graph input nor a graph
+output).  A result is ``(assign, objects)``: ``assign[t]`` is the shared-object
+index of intermediate tensor ``t`` and ``objects[k]`` the size of object ``k``.
+"""
+from __future__ import annotations
+
+import itertools
+
+
+def lifetimes(ops, intermediate):
+    """First op (producer) and last op (last consumer) of every intermediate
+    tensor (Sec. 5: the first and the last operator that use the tensor)."""
+    first, last = {}, {}
+    for i, (outs, ins) in enumerate(ops):
+        for t in outs:
+            if t in intermediate:
+                first.setdefault(t, i)
+                last.setdefault(t, i)
+        for t in ins:
+            if t in intermediate:
+                last[t] = i
+    return first, last
+
+
+def naive(ops, sizes, intermediate):
+    """One buffer per intermediate tensor: the paper's baseline (Sec. 5, (a))."""
+    assign, objects = {}, []
+    for outs, _ in ops:
+        for t in outs:
+            if t in intermediate:
+                assign[t] = len(objects)
+                objects.append(sizes[t])
+    return assign, objects
+
+
+def greedy(ops, sizes, intermediate):
+    """Greedy shared-object assignment (Algorithm 1), written as a plain list scan.
+
+    Operators are visited in execution order.  Each intermediate output takes
+    a new shared object when the pool of free objects is empty, otherwise the
+    free object whose size is closest to the tensor's size (absolute
+    difference; equal distances go to the lowest object index), which leaves
+    the pool and grows to the tensor's size if smaller.  Only after all outputs
+    of the operator are placed are its intermediate inputs whose last consumer
+    it is handed back to the pool, so an output never shares memory with an
+    input of the same operator.  A tensor that nothing consumes is never
+    returned to the pool.
+    """
+    consumers_left = {}
+    for outs, ins in ops:
+        for t in ins:
+            if t in intermediate:
+                consumers_left[t] = consumers_left.get(t, 0) + 1
+    last = {}
+    for i, (_, ins) in enumerate(ops):
+        for t in ins:
+            if t in intermediate:
+                last[t] = i
+    objects: list[int] = []
+    free: list[int] = []          # object indices
+    assign: dict[int, int] = {}
+    for i, (outs, ins) in enumerate(ops):
+        for t in outs:
+            if t not in intermediate:
+                continue
+            if not free:
+                k = len(objects)
+                objects.append(sizes[t])
+            else:
+                k = min(free, key=lambda j: (abs(objects[j] - sizes[t]), j))
+                free.remove(k)
+                if sizes[t] > objects[k]:
+                    objects[k] = sizes[t]
+            assign[t] = k
+        released = set()
+        for t in ins:
+            if t in intermediate and last.get(t) == i and t not in released:
+                released.add(t)
+                free.append(assign[t])
+    return assign, objects
+
+
+def total(objects):
+    return int(sum(objects))
+
+
+def check_assignment(ops, sizes, intermediate, assign, objects):
+    """Validity: every intermediate tensor has an object at least as large as
+    itself, and tensors whose lifetimes overlap never share an object."""
+    first, last = lifetimes(ops, intermediate)
+    for t in intermediate:
+        if t not in first:
+            continue
+        k = assign[t]
+        assert 0 <= k < len(objects)
+        assert objects[k] >= sizes[t]
+    ts = sorted(t for t in intermediate if t in first)
+    for a, b in itertools.combinations(ts, 2):
+        if assign[a] == assign[b]:
+            # [first, last] intervals may touch only if one ends strictly
+            # before the other is produced.
+            assert last[a] < first[b] or last[b] < first[a], (a, b)
+    return True
+
+
+def peak_live(ops, sizes, intermediate):
+    """Largest total size of tensors alive at one op: a lower bound on any plan."""
+    first, last = lifetimes(ops, intermediate)
+    best = 0
+    for i in range(len(ops)):
+        best = max(best, sum(sizes[t] for t in first if first[t] <= i <= last[t]))
+    return best
+
+
+def brute_force_optimum(ops, sizes, intermediate):
+    """Smallest total over all valid partitions of the intermediate tensors into
+    shared objects (exhaustive; only for a handful of tensors)."""
+    first, last = lifetimes(ops, intermediate)
+    ts = sorted(t for t in intermediate if t in first)
+
+    def conflict(a, b):
+        return not (last[a] < first[b] or last[b] < first[a])
+
+    best = [None]
+
+    def rec(i, groups):
+        if i == len(ts):
+            tot = sum(max(sizes[t] for t in g) for g in groups)
+            if best[0] is None or tot < best[0]:
+                best[0] = tot
+            return
+        t = ts[i]
+        for g in groups:
+            if all(not conflict(t, u) for u in g):
+                g.append(t)
+                rec(i + 1, groups)
+                g.pop()
+        groups.append([t])
+        rec(i + 1, groups)
+        groups.pop()
+
+    rec(0, [])
+    return best[0] if best[0] is not None else 0
+
+
+def graph_problem(graph, shapes, elem_bytes=2, slice_width=8, fused_nodes=None):
+    """Planner problem of a workload graph: every op is one operator, every
+    tensor except graph inputs and graph outputs is intermediate, and a
+    tensor's size is its channel-padded element count times ``elem_bytes``."""
+    from . import op_inputs
+    ops = []
+    sizes = {}
+    inter = set()
+    outputs = set(graph["outputs"])
+    for i, op in enumerate(graph["ops"]):
+        n, h, w, c = shapes[i]
+        cp = -(-c // slice_width) * slice_width
+        sizes[i] = n * h * w * cp * elem_bytes
+        if op["op"] == "input":
+            ops.append(([i], []))
+            continue
+        ops.append(([i], op_inputs(op)))
+        if i not in outputs:
+            inter.add(i)
+    return ops, sizes, inter
