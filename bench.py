@@ -1,0 +1,327 @@
+"""Throughput benchmark of the mgi engine on one MI355X.
+
+A step is one forward pass of the whole network over one batch of synthetic,
+device-resident input (launch sequence of every fused node on one stream).
+Protocol after Sec. 6 of the paper: warm-up runs are skipped, then the mean
+over the timed runs is reported.  Prints ONE JSON line on stdout.
+
+  python bench.py [--gpus 1] [--steps 100] [--warmup 10] [--workload v1_b64]
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK = 8.0e12            # bytes/s, MI355X HBM3E
+MFMA_F16_PEAK = 2516.6e12    # flop/s, dense fp16 MFMA
+RIDGE = MFMA_F16_PEAK / HBM_PEAK
+
+WORKLOADS = {
+    "dw_block": ("dw_block", 1),
+    "v1_b1": ("mobilenet_v1", 1),
+    "v2_b1": ("mobilenet_v2", 1),
+    "v1_b64": ("mobilenet_v1", 64),
+    "v2_b64": ("mobilenet_v2", 64),
+    "deeplab": ("deeplab", 1),
+}
+
+
+def eprint(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+# ---------------------------------------------------------------------------
+# HIP events through the runtime's C API
+# ---------------------------------------------------------------------------
+class Hip:
+    def __init__(self):
+        self.L = ctypes.CDLL("libamdhip64.so")
+        self.L.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.L.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                               ctypes.c_void_p]
+        self.L.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+        self.L.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+    def event(self):
+        e = ctypes.c_void_p()
+        assert self.L.hipEventCreate(ctypes.byref(e)) == 0
+        return e.value
+
+    def elapsed_ms(self, a, b):
+        f = ctypes.c_float()
+        assert self.L.hipEventSynchronize(ctypes.c_void_p(b)) == 0
+        assert self.L.hipEventElapsedTime(ctypes.byref(f), ctypes.c_void_p(a), ctypes.c_void_p(b)) == 0
+        return f.value
+
+    def destroy(self, e):
+        self.L.hipEventDestroy(ctypes.c_void_p(e))
+
+
+# ---------------------------------------------------------------------------
+# algorithmic work of each fused node
+# ---------------------------------------------------------------------------
+def tensor_shapes(desc, nodes):
+    """Shape of every graph input and every tensor a node materialises, as
+    reported by the engine."""
+    shapes = {}
+    for t, op in enumerate(desc["ops"]):
+        if op["op"] == "input":
+            shapes[t] = tuple(op["shape"])
+    for n in nodes:
+        if n["tensor"] >= 0:
+            shapes[n["tensor"]] = tuple(n["shape"])
+    return shapes
+
+
+def op_inputs(op):
+    if op["op"] == "input":
+        return []
+    if op["op"] == "add":
+        return [op["a"], op["b"]]
+    if op["op"] == "concat":
+        return list(op["ins"])
+    return [op["in"]]
+
+
+def node_work(desc, nodes, shapes, i):
+    """(flops, bytes, bound) that the method itself must do for node i:
+    activations read once and written once in fp16, weights read once."""
+    info = nodes[i]
+    kind = info["kind"]
+    t = info["tensor"]
+    materialized = {n["tensor"] for n in nodes if n["tensor"] >= 0}
+    ops = desc["ops"]
+
+    def head_of(u):
+        op = ops[u]
+        if op["op"] == "activation" and op["in"] not in materialized and ops[op["in"]]["op"] != "input":
+            return head_of(op["in"])
+        if op["op"] == "add":
+            for side in ("a", "b"):
+                v = op[side]
+                if v not in materialized and ops[v]["op"] != "input":
+                    return head_of(v)
+        return u
+
+    def elems(u):
+        n, h, w, c = shapes[u]
+        return n * h * w * c
+
+    if t < 0:
+        return 0.0, 0.0, "hbm"
+    h = head_of(t)
+    op = ops[h]
+    out_b = elems(t) * 2
+    if kind in ("conv_stem", "pw_gemm", "conv_igemm"):
+        x = op["in"]
+        cin = shapes[x][3]
+        n, oh, ow, cout = shapes[t]
+        m = n * oh * ow
+        flops = 2.0 * m * op["kh"] * op["kw"] * cin * cout
+        in_bytes = elems(x) * (4 if (kind == "conv_stem" and ops[x].get("dtype", 2) == 2) else 2)
+        byts = in_bytes + out_b + op["w"].size * 2 + op["b"].size * 4
+        if h != t:
+            byts += out_b          # fused residual operand
+    elif kind == "dw_conv":
+        flops = 2.0 * elems(t) * op["kh"] * op["kw"]
+        byts = elems(op["in"]) * 2 + out_b + op["w"].size * 4 + op["b"].size * 4
+    elif kind == "fc_gemm":
+        n = shapes[t][0]
+        flops = 2.0 * op["w"].size * n
+        byts = elems(op["in"]) * 2 + op["w"].size * 2 + op["b"].size * 4 + elems(t) * 4
+    elif kind == "global_avgpool":
+        flops = float(elems(op["in"]))
+        byts = elems(op["in"]) * 2 + out_b
+    elif kind == "softmax":
+        flops = 3.0 * elems(t)
+        byts = elems(t) * 8
+    else:
+        ins = op_inputs(op)
+        flops = float(elems(t))
+        byts = sum(elems(u) * 2 for u in ins) + out_b
+    bound = "mfma" if (flops / max(byts, 1.0)) >= RIDGE else "hbm"
+    return flops, float(byts), bound
+
+
+def roofline_entry(flops, byts, bound, seconds):
+    if bound == "mfma":
+        ach = flops / seconds / 1e12
+        return {"bound": "mfma", "achieved": round(ach, 3), "peak": MFMA_F16_PEAK / 1e12,
+                "unit": "TFLOP/s", "frac": round(ach * 1e12 / MFMA_F16_PEAK, 4)}
+    ach = byts / seconds / 1e9
+    return {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK / 1e9, "unit": "GB/s",
+            "frac": round(ach * 1e9 / HBM_PEAK, 4)}
+
+
+# ---------------------------------------------------------------------------
+def run_workload(key, steps, warmup, hip, profile_steps=20, detail=True):
+    import torch
+    import workloads
+    from paper_1907_01989_amd import _binding as B
+    from paper_1907_01989_amd import engine
+
+    net, batch = WORKLOADS[key]
+    desc = workloads.WORKLOADS[net](batch)
+    plan = engine.Plan(desc)
+    xs = plan.input_tensors()
+    outs = plan.alloc_outputs()
+    stream = torch.cuda.current_stream()
+    sh = stream.cuda_stream
+    ins = [x.data_ptr() for x in xs]
+    ops_ptrs = [o.data_ptr() for o in outs]
+    nodes = plan.nodes()
+    nn = len(nodes)
+    for _ in range(warmup):
+        B.mgi_plan_run(plan.handle, ins, ops_ptrs, sh)
+    torch.cuda.synchronize()
+
+    # per-layer pass (outside the timed region): events around every node
+    per_node = [0.0] * nn
+    if detail:
+        evs = [[hip.event() for _ in range(nn + 1)] for _ in range(profile_steps)]
+        for k in range(profile_steps):
+            B.mgi_plan_run_timed(plan.handle, ins, ops_ptrs, evs[k], sh)
+        torch.cuda.synchronize()
+        for k in range(profile_steps):
+            for i in range(nn):
+                per_node[i] += hip.elapsed_ms(evs[k][i], evs[k][i + 1]) / profile_steps
+        for row in evs:
+            for e in row:
+                hip.destroy(e)
+    dom = max(range(nn), key=lambda i: per_node[i])
+
+    # timed region: K steps; the dominant node is bracketed by HIP events
+    dev = [(hip.event(), hip.event()) for _ in range(steps)]
+    arrays = []
+    for a, b in dev:
+        ev = [None] * (nn + 1)
+        ev[dom], ev[dom + 1] = a, b
+        arrays.append(ev)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(steps):
+        B.mgi_plan_run_timed(plan.handle, ins, ops_ptrs, arrays[k], sh)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    dom_ms = sum(hip.elapsed_ms(a, b) for a, b in dev) / steps
+    for a, b in dev:
+        hip.destroy(a)
+        hip.destroy(b)
+
+    shapes = tensor_shapes(desc, nodes)
+    layers = []
+    for i, info in enumerate(nodes):
+        fl, by, bound = node_work(desc, nodes, shapes, i)
+        name = desc["ops"][info["tensor"]]["name"] if info["tensor"] >= 0 else info["kind"]
+        entry = {"node": i, "name": name, "kind": info["kind"], "us": round(per_node[i] * 1e3, 2)}
+        if per_node[i] > 0 and by > 0:
+            entry.update({k: v for k, v in roofline_entry(fl, by, bound, per_node[i] * 1e-3).items()
+                          if k in ("bound", "frac", "achieved", "unit")})
+        layers.append(entry)
+    fl, by, bound = node_work(desc, nodes, shapes, dom)
+    roof = roofline_entry(fl, by, bound, dom_ms * 1e-3)
+    roof.update({"kernel": nodes[dom]["kind"],
+                 "layer": desc["ops"][nodes[dom]["tensor"]]["name"],
+                 "algorithmic_bytes": int(by), "algorithmic_flops": int(fl),
+                 "avg_launch_us": round(dom_ms * 1e3, 3), "traffic": None})
+    total_s = t1 - t0
+    res = {"desc": desc, "batch": batch, "net": net, "ms_per_step": total_s / steps * 1e3,
+           "images_per_s": batch * steps / total_s, "roofline": roof, "layers": layers,
+           "sum_layer_us": sum(per_node) * 1e3}
+    plan.close()
+    return res
+
+
+def cpu_baseline(net, budget_s=10.0):
+    """The oracle, as it stands, on a bounded sample of the same workload:
+    whole forward passes of single images until about budget_s has elapsed."""
+    import oracle
+    import workloads
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
+    desc = workloads.WORKLOADS[net](1)
+    oracle.lib()
+    n = 0
+    t0 = time.perf_counter()
+    while True:
+        oracle.run_graph(desc, keep=desc["outputs"])
+        n += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or n >= 512:
+            break
+    return {"value": round(n / el, 4), "unit": "images/sec", "cores": threads, "kind": "oracle",
+            "sample": f"{n} single-image forward passes of {desc['name']} (float64, plain loops), "
+                      f"{el:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="v1_b64", choices=sorted(WORKLOADS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extra", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this engine runs on one GPU; --gpus {args.gpus} is not supported "
+              "(batch sharding across GPUs is described in the design notes, not built)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    if not torch.cuda.is_available():
+        eprint("bench.py: no GPU visible")
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    hip = Hip()
+    eprint(f"[bench] workload {args.workload}: warmup {args.warmup}, steps {args.steps}")
+    main_res = run_workload(args.workload, args.steps, args.warmup, hip)
+    eprint(f"[bench] {main_res['images_per_s']:.1f} images/s, {main_res['ms_per_step']:.4f} ms/step")
+    also = {}
+    if not args.no_extra:
+        for key in ("v1_b1", "v2_b1", "v1_b64", "v2_b64"):
+            if key == args.workload:
+                continue
+            r = run_workload(key, 100, 10, hip, detail=False)
+            also[key] = {"images_per_s": round(r["images_per_s"], 1),
+                         "ms_per_step": round(r["ms_per_step"], 4)}
+            eprint(f"[bench] {key}: {r['images_per_s']:.1f} images/s")
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(main_res["net"])
+        eprint(f"[bench] cpu oracle: {cpu}")
+    net, batch = WORKLOADS[args.workload]
+    out = {
+        "metric": "images/sec MobileNet-v1/v2 224 fp16 at batch 1 and 64; per-layer % roofline",
+        "value": round(main_res["images_per_s"], 2),
+        "unit": "images/sec",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(main_res["ms_per_step"], 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "fp16",
+        "data": "synthetic",
+        "config": {"workload": main_res["desc"]["name"], "network": net, "batch": batch,
+                   "input": "NHWC fp32 uniform[0,1] (fp16 values), device-resident",
+                   "weights": "He-normal seed 0, fp16", "planner": "greedy", "fused": True},
+        "roofline": main_res["roofline"],
+        "cpu_baseline": cpu,
+        "per_layer": main_res["layers"],
+        "sum_of_layer_us": round(main_res["sum_layer_us"], 2),
+        "also": also,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

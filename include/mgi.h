@@ -1,0 +1,256 @@
+/*
+ * mgi.h -- C ABI of an MI355X (gfx950) inference engine for MobileNet-class
+ * convolutional networks.
+ *
+ * The calls follow the structure of the GPU inference engine described in
+ * "On-Device Neural Net Inference with Mobile GPUs" (Lee et al., 2019):
+ *
+ *   1. the caller describes the network as a graph of operators with their
+ *      weights (Sec. 3.1, the delegate receives a graph of supported ops);
+ *   2. finalize transforms the graph: it folds padding into the operators,
+ *      fuses element-wise operators into the expensive operator that produces
+ *      their input, and specialises kernels, e.g. 1x1 convolution
+ *      (Sec. 3.2, "Shader Program Optimization");
+ *   3. finalize plans the intermediate tensors into shared objects after a
+ *      topological ordering of the graph (Sec. 5, Algorithm 1);
+ *   4. run enqueues every kernel on one stream with no host synchronisation
+ *      (Sec. 3.2, "Running Inference"), reading and writing device-resident
+ *      inputs and outputs (Sec. 6, tensors placed in GPU buffers).
+ *
+ * Conventions shared by every entry point:
+ *   - Every call returns an mgi_status; nothing throws across the ABI.  On a
+ *     failure mgi_last_error() returns a thread-local message.
+ *   - Host pointers passed to graph-building calls are read during the call
+ *     only; the library copies what it keeps.  The caller keeps ownership.
+ *   - The library never allocates device memory.  The caller allocates the
+ *     workspace, the packed-weight buffer, the inputs and the outputs, and
+ *     passes device pointers; they must stay valid while a plan uses them.
+ *   - Streams are passed as `void *` holding a hipStream_t (NULL = the null
+ *     stream).  A plan runs all of its kernels, in order, on that one stream;
+ *     its buffer sharing is valid only under that in-order execution.
+ *   - A plan is not re-entrant: at most one mgi_plan_run per plan may be in
+ *     flight on the device at a time unless the runs are ordered by the stream.
+ *   - Tensor shapes are (n, h, w, c): batch, height, width, channels.  Graph
+ *     inputs are NHWC arrays in fp32 or fp16.  Graph outputs are NHWC arrays
+ *     of fp32 values (an output of global_avgpool / fc / softmax is (n, c));
+ *     argmax outputs are int32 arrays of shape (n, h, w).
+ *   - Tensor ids are assigned in call order, starting at 0, one per
+ *     graph-building call that returns an id.
+ */
+#ifndef MGI_H_
+#define MGI_H_
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    MGI_OK = 0,
+    MGI_ERR_INVALID_ARG = 1, /* null pointer, bad id, non-positive size */
+    MGI_ERR_SHAPE = 2,       /* operand shapes that do not fit the operator */
+    MGI_ERR_UNSUPPORTED = 3, /* a valid request this engine does not implement */
+    MGI_ERR_STATE = 4,       /* call out of order (e.g. run before bind) */
+    MGI_ERR_WORKSPACE = 5,   /* a device buffer is missing or misaligned */
+    MGI_ERR_HIP = 6,         /* the HIP runtime reported an error */
+    MGI_ERR_OOM_HOST = 7     /* host allocation failed */
+} mgi_status;
+
+typedef enum { MGI_ACT_NONE = 0, MGI_ACT_RELU = 1, MGI_ACT_RELU6 = 2 } mgi_act;
+
+typedef enum {
+    MGI_DTYPE_FP16 = 0,
+    MGI_DTYPE_BF16 = 1,
+    MGI_DTYPE_FP32 = 2,
+    MGI_DTYPE_INT32 = 3
+} mgi_dtype;
+
+typedef enum {
+    MGI_PLANNER_NAIVE = 0,  /* one buffer per intermediate tensor (Sec. 5, baseline) */
+    MGI_PLANNER_GREEDY = 1  /* shared objects, Algorithm 1 (Sec. 5) */
+} mgi_planner;
+
+typedef struct mgi_graph mgi_graph;
+typedef struct mgi_plan mgi_plan;
+
+/* Convolution attributes.  Window (kh, kw), stride, dilation, explicit
+ * four-sided zero padding (a separate PAD op folded into the convolution,
+ * Sec. 3.1), output channels and the activation fused after it (Sec. 3.2).
+ * Output size: oh = (h + pad_t + pad_b - dil_h * (kh - 1) - 1) / stride_h + 1,
+ * likewise for ow.  cout is ignored by mgi_graph_add_depthwise. */
+typedef struct {
+    int kh, kw;
+    int stride_h, stride_w;
+    int dil_h, dil_w;
+    int pad_t, pad_b, pad_l, pad_r;
+    int cout;
+    int act; /* mgi_act */
+} mgi_conv_desc;
+
+/* Options of mgi_graph_finalize.  Zero-initialised options are not valid;
+ * call mgi_options_default first. */
+typedef struct {
+    int planner;         /* mgi_planner; default GREEDY */
+    int fuse;            /* 1: fuse activations / residual adds into producers (default 1) */
+    int materialize_all; /* 1: every node output keeps its own buffer so that
+                            mgi_plan_read_node works after a run (default 0) */
+    int dtype;           /* storage type of activations and weights: FP16 (default) */
+} mgi_options;
+
+/* ---------------------------------------------------------------------------
+ * errors
+ * ------------------------------------------------------------------------- */
+/* Static text naming a status code.  Never NULL. */
+const char *mgi_status_str(mgi_status s);
+/* Message of the most recent failed call on this thread ("" if none).  The
+ * pointer stays valid until the next failing call on the same thread. */
+const char *mgi_last_error(void);
+
+/* ---------------------------------------------------------------------------
+ * graph building (Sec. 3.1: the engine receives a graph of supported ops)
+ * Every add call validates its operands and writes the id of the new tensor
+ * to *out.  Shape errors are reported here; unsupported attribute
+ * combinations are reported here or by finalize.
+ * ------------------------------------------------------------------------- */
+mgi_status mgi_graph_create(mgi_graph **g);
+mgi_status mgi_graph_destroy(mgi_graph *g); /* NULL is accepted */
+
+/* A graph input: an NHWC array of `dtype` (FP32 or FP16) supplied to run. */
+mgi_status mgi_graph_add_input(mgi_graph *g, int n, int h, int w, int c, int dtype, int *out);
+
+/* 2D convolution (Sec. 4.1, convolution over a kernel_height x kernel_width
+ * window; the 1x1 case gets its own kernel, Sec. 3.2).
+ * w: cout x kh x kw x cin floats (OHWI), bias: cout floats (NULL = zeros).
+ * y = act(b + sum over window and input channels of w * x) with x zero
+ * outside the input. */
+mgi_status mgi_graph_add_conv2d(mgi_graph *g, int in, const mgi_conv_desc *d,
+                                const float *w, const float *bias, int *out);
+
+/* Depthwise convolution, channel multiplier 1: each channel is convolved with
+ * its own kh x kw filter.  w: c x kh x kw floats, bias: c floats (NULL = 0). */
+mgi_status mgi_graph_add_depthwise(mgi_graph *g, int in, const mgi_conv_desc *d,
+                                   const float *w, const float *bias, int *out);
+
+/* Element-wise y = act(a + b); a and b have equal shapes (Sec. 3.1, ADD). */
+mgi_status mgi_graph_add_add(mgi_graph *g, int a, int b, int act, int *out);
+
+/* Standalone activation; finalize fuses it into its producer when it can
+ * (Sec. 3.2: element-wise operators fused with the expensive operator). */
+mgi_status mgi_graph_add_activation(mgi_graph *g, int in, int act, int *out);
+
+/* Mean over h and w: (n, h, w, c) -> (n, 1, 1, c). */
+mgi_status mgi_graph_add_global_avgpool(mgi_graph *g, int in, int *out);
+
+/* Fully connected: input (n, h, w, c) is flattened per image to h*w*c values
+ * (h = w = 1 is required); w: cout x cin floats, bias: cout floats.
+ * Output (n, 1, 1, cout). */
+mgi_status mgi_graph_add_fc(mgi_graph *g, int in, int cout, const float *w, const float *bias,
+                            int *out);
+
+/* Softmax over the channel axis: exp(z - max z) / sum exp(z - max z). */
+mgi_status mgi_graph_add_softmax(mgi_graph *g, int in, int *out);
+
+/* Channel concatenation in the given order; all inputs share n, h, w. */
+mgi_status mgi_graph_add_concat(mgi_graph *g, const int *ins, int count, int *out);
+
+/* Bilinear resize to (oh, ow).  align_corners = 1: source coordinate
+ * d * (in - 1) / (out - 1); 0: d * in / out.  The upper neighbour is clamped
+ * to the last sample. */
+mgi_status mgi_graph_add_resize_bilinear(mgi_graph *g, int in, int oh, int ow, int align_corners,
+                                         int *out);
+
+/* Per-pixel index of the largest channel (ties: lowest index), int32. */
+mgi_status mgi_graph_add_argmax(mgi_graph *g, int in, int *out);
+
+/* Mark a tensor as a graph output (in call order: output index 0, 1, ...).
+ * Graph inputs cannot be outputs. */
+mgi_status mgi_graph_mark_output(mgi_graph *g, int id);
+
+/* ---------------------------------------------------------------------------
+ * planning (pure host code; no device call)
+ * ------------------------------------------------------------------------- */
+void mgi_options_default(mgi_options *o);
+
+/* Fuse, order, plan intermediate buffers and pack weights (Sec. 3.2, Sec. 5).
+ * The graph is not modified and may be destroyed afterwards.  The plan owns
+ * host copies of the packed weights until mgi_plan_bind uploads them. */
+mgi_status mgi_graph_finalize(const mgi_graph *g, const mgi_options *o, mgi_plan **p);
+mgi_status mgi_plan_destroy(mgi_plan *p); /* NULL is accepted */
+
+/* Bytes of device workspace (the arena holding every intermediate tensor)
+ * and of packed weights that the caller must allocate for mgi_plan_bind.
+ * Both buffers must be 256-byte aligned. */
+mgi_status mgi_plan_workspace_bytes(const mgi_plan *p, size_t *bytes);
+mgi_status mgi_plan_weight_bytes(const mgi_plan *p, size_t *bytes);
+
+/* Memory of the intermediate tensors (Sec. 5, Table 3): `naive` = one buffer
+ * per tensor, `planned` = the chosen planner's shared objects, `n_objects` =
+ * number of shared objects.  Any out pointer may be NULL. */
+mgi_status mgi_plan_memory_report(const mgi_plan *p, size_t *naive, size_t *planned,
+                                  int *n_objects);
+
+/* Graph inputs and outputs of the plan, in declaration / marking order. */
+mgi_status mgi_plan_num_io(const mgi_plan *p, int *n_inputs, int *n_outputs);
+/* Shape and element type (FP32 / FP16 for inputs, FP32 / INT32 for outputs)
+ * of input or output `index` (is_output selects which); bytes = total size. */
+mgi_status mgi_plan_io_info(const mgi_plan *p, int is_output, int index, int *n, int *h, int *w,
+                            int *c, int *dtype, size_t *bytes);
+
+/* Upload packed weights into dev_weights and adopt dev_workspace as the arena.
+ * Asynchronous on `stream`; host copies are released once the copy is done
+ * with (the call waits for the upload before returning). */
+mgi_status mgi_plan_bind(mgi_plan *p, void *dev_workspace, void *dev_weights, void *stream);
+
+/* ---------------------------------------------------------------------------
+ * running (Sec. 3.2: dispatch every program into the queue, no host sync)
+ * ------------------------------------------------------------------------- */
+/* dev_inputs[i] / dev_outputs[i]: device pointers for graph input / output i.
+ * Enqueues all kernels on `stream` and returns without synchronising. */
+mgi_status mgi_plan_run(mgi_plan *p, const void *const *dev_inputs, void *const *dev_outputs,
+                        void *stream);
+
+/* As mgi_plan_run, and records timing markers on the same stream: events[i]
+ * (a hipEvent_t, or NULL to skip) just before node i is launched, for
+ * 0 <= i < node count, and events[node count] after the last node.  The array
+ * holds node count + 1 entries and is read during the call only.  The
+ * elapsed time between events[i] and events[i + 1] is node i's duration on the
+ * device (the paper's per-program timing of Sec. 6, taken without host sync). */
+mgi_status mgi_plan_run_timed(mgi_plan *p, const void *const *dev_inputs, void *const *dev_outputs,
+                              void *stream, void *const *events);
+
+/* ---------------------------------------------------------------------------
+ * introspection, used for layer-by-layer checks
+ * ------------------------------------------------------------------------- */
+/* Number of executable nodes after fusion. */
+mgi_status mgi_plan_node_count(const mgi_plan *p, int *count);
+
+/* Node `i`: `kind` (static string such as "pw_gemm", "dw3x3"), the graph
+ * tensor id its output represents (the last operator it absorbed), the shape
+ * of that tensor, and the number of graph operators fused into it. */
+mgi_status mgi_plan_node_info(const mgi_plan *p, int i, const char **kind, int *tensor_id, int *n,
+                              int *h, int *w, int *c, int *n_fused);
+
+/* Copy node i's output, as an NHWC fp32 array (int32 for argmax), to
+ * dev_dst on `stream`.  Requires materialize_all (MGI_ERR_STATE otherwise)
+ * and a completed or stream-ordered run. */
+mgi_status mgi_plan_read_node(mgi_plan *p, int i, void *dev_dst, void *stream);
+
+/* ---------------------------------------------------------------------------
+ * stand-alone planner (Sec. 5, Algorithm 1), for planning outside a graph
+ * ------------------------------------------------------------------------- */
+/* Intermediate tensor t (0 <= t < n_tensors) has `sizes[t]` bytes, is produced
+ * by operator first_op[t] and last used by operator last_op[t]
+ * (first_op[t] <= last_op[t]; last_op[t] = -1 if nothing consumes it).
+ * Operators are numbered in execution order.  Writes the shared object of
+ * every tensor to object_of[t] and the object sizes to object_sizes[k]
+ * (capacity n_tensors); *n_objects receives the object count. */
+mgi_status mgi_planner_assign(int planner, int n_tensors, const size_t *sizes, const int *first_op,
+                              const int *last_op, int *object_of, size_t *object_sizes,
+                              int *n_objects);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MGI_H_ */

@@ -223,10 +223,51 @@ def op_inputs(op):
     return [op["in"]]
 
 
-def run_graph(graph, keep=None):
+# ops whose output the paper's engine keeps in fp16 storage (everything but
+# the fp32 logits / probabilities and the integer labels)
+FP16_STORED = {"conv2d", "depthwise", "add", "activation", "gap", "concat", "resize_bilinear"}
+
+
+def eval_op(op, operands):
+    """Evaluate one op on its operand arrays (float64 NHWC), in the order the
+    operands appear in ``op_inputs(op)``."""
+    k = op["op"]
+    if k == "input":
+        return _f64(op["data"])
+    if k == "conv2d":
+        return activation(conv2d(operands[0], op["w"], op["b"], op["stride"], op["dil"], op["pads"]),
+                          op["act"])
+    if k == "depthwise":
+        return activation(depthwise(operands[0], op["w"], op["b"], op["stride"], op["dil"],
+                                    op["pads"]), op["act"])
+    if k == "add":
+        return activation(add(operands[0], operands[1]), op["act"])
+    if k == "activation":
+        return activation(operands[0], op["act"])
+    if k == "gap":
+        return global_avgpool(operands[0])
+    if k == "fc":
+        return fc(operands[0], op["w"], op["b"])
+    if k == "softmax":
+        return softmax(operands[0])
+    if k == "concat":
+        return concat(operands)
+    if k == "resize_bilinear":
+        return resize_bilinear(operands[0], op["oh"], op["ow"], op["align_corners"])
+    if k == "argmax":
+        return argmax(operands[0])
+    raise ValueError(f"unknown op {k}")
+
+
+def run_graph(graph, keep=None, store_fp16=False):
     """Evaluate every tensor of ``graph``; returns {tensor id: float64 NHWC array}
     (argmax outputs are int32).  ``keep`` limits which tensors are returned;
-    others are dropped as soon as their last consumer has run."""
+    others are dropped as soon as their last consumer has run.
+
+    ``store_fp16`` rounds each tensor that the paper's engine stores in fp16
+    (Table 1 frames the GPU side as FP16) to the nearest fp16 value after its
+    op, everything else staying exact: it measures how much a network amplifies
+    the rounding that fp16 storage alone introduces."""
     ops = graph["ops"]
     last_use = {}
     for i, op in enumerate(ops):
@@ -235,33 +276,9 @@ def run_graph(graph, keep=None):
     want = set(range(len(ops))) if keep is None else set(keep)
     vals: dict[int, np.ndarray] = {}
     for i, op in enumerate(ops):
-        k = op["op"]
-        if k == "input":
-            y = _f64(op["data"])
-        elif k == "conv2d":
-            y = conv2d(vals[op["in"]], op["w"], op["b"], op["stride"], op["dil"], op["pads"])
-            y = activation(y, op["act"])
-        elif k == "depthwise":
-            y = depthwise(vals[op["in"]], op["w"], op["b"], op["stride"], op["dil"], op["pads"])
-            y = activation(y, op["act"])
-        elif k == "add":
-            y = activation(add(vals[op["a"]], vals[op["b"]]), op["act"])
-        elif k == "activation":
-            y = activation(vals[op["in"]], op["act"])
-        elif k == "gap":
-            y = global_avgpool(vals[op["in"]])
-        elif k == "fc":
-            y = fc(vals[op["in"]], op["w"], op["b"])
-        elif k == "softmax":
-            y = softmax(vals[op["in"]])
-        elif k == "concat":
-            y = concat([vals[t] for t in op["ins"]])
-        elif k == "resize_bilinear":
-            y = resize_bilinear(vals[op["in"]], op["oh"], op["ow"], op["align_corners"])
-        elif k == "argmax":
-            y = argmax(vals[op["in"]])
-        else:
-            raise ValueError(f"unknown op {k}")
+        y = eval_op(op, [vals[t] for t in op_inputs(op)])
+        if store_fp16 and op["op"] in FP16_STORED:
+            y = y.astype(np.float16).astype(np.float64)
         vals[i] = y
         for t in op_inputs(op):
             if last_use.get(t) == i and t not in want:

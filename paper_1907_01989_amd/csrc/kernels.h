@@ -1,0 +1,82 @@
+// Kernel parameter blocks and launchers (internal to the engine).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "../../include/mgi.h"
+
+namespace mgi {
+namespace kern {
+
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+
+// C = act2(act1(W * X + bias) + residual): MFMA GEMM over sliced activations.
+struct GemmParams {
+    const h8 *x;         // sliced input, [slices][Min] of 8 halves
+    const h8 *w;         // packed weights [nb16][ksp][16][8]
+    const float *bias;   // [nb16 * 16]
+    const h8 *res;       // sliced residual with the output's shape, or null
+    void *y;             // sliced fp16 output, or fp32 (M x cout) for FC
+    int M;               // output pixels (n * oh * ow)
+    int Min;             // input pixels (n * h * w)
+    int ksl, ksp;        // K slices, and padded to a multiple of 4
+    int nb16, ns, cout;  // output blocks of 16, output slices, channels
+    int act1, act2;
+    int mtiles, ntiles;
+    // implicit-GEMM window geometry
+    int H, W, OH, OW, sin, kw, sh, sw, dh, dw, pt, pl;
+};
+hipError_t launch_gemm(const GemmParams &p, int bm, int bn, bool taps, bool f32out,
+                       hipStream_t st);
+
+// Direct convolution of a small-channel NHWC graph input (kh*kw*c <= 32).
+struct StemParams {
+    const void *x;       // NHWC fp32 or fp16
+    const h8 *w;         // packed [nb16][4][16][8], k = (ky*kw + kx)*c + ci
+    const float *bias;
+    const h8 *res;
+    h8 *y;
+    int N, H, W, C, OH, OW, M;
+    int KW, K, sh, sw, dh, dw, pt, pl;
+    int nb16, ns, act1, act2;
+};
+hipError_t launch_stem(const StemParams &p, bool fp16_in, hipStream_t st);
+
+struct DwParams {
+    const h8 *x;
+    const float *w;      // [S][kh*kw][8]
+    const float *bias;   // [S*8]
+    h8 *y;
+    int N, H, W, S, OH, OW, KH, KW, sh, sw, dh, dw, pt, pl, act;
+};
+hipError_t launch_depthwise(const DwParams &p, hipStream_t st);
+
+hipError_t launch_add(const h8 *a, const h8 *b, h8 *y, size_t count, int act, hipStream_t st);
+hipError_t launch_act(const h8 *x, h8 *y, size_t count, int act, hipStream_t st);
+hipError_t launch_gap(const h8 *x, h8 *y, int N, int HW, int S, hipStream_t st);
+hipError_t launch_softmax(const float *z, float *y, int rows, int cols, hipStream_t st);
+
+struct ConcatParams {
+    const h8 *src[8];
+    int coff[9];
+    int nin;
+    int M, S, C;
+    h8 *y;
+};
+hipError_t launch_concat(const ConcatParams &p, hipStream_t st);
+
+struct ResizeParams {
+    const h8 *x;
+    void *y;             // sliced output, or int32 labels (argmax)
+    int N, H, W, S, C, OH, OW;
+    int align_corners;
+};
+hipError_t launch_resize(const ResizeParams &p, bool argmax, hipStream_t st);
+hipError_t launch_argmax(const h8 *x, int *y, int M, int S, int C, hipStream_t st);
+
+hipError_t launch_ingest(const void *x, bool fp16_in, h8 *y, int M, int C, hipStream_t st);
+hipError_t launch_export(const h8 *x, float *y, int M, int C, hipStream_t st);
+
+}  // namespace kern
+}  // namespace mgi

@@ -1,0 +1,628 @@
+// Graph finalisation: fusion, node list, buffer planning, weight packing.
+//
+// Pure host code: no HIP call is made here, so every step runs and is tested
+// on a machine without a GPU.
+//
+// Fusion (Sec. 3.2, first technique): an element-wise operator whose input is
+// produced by an expensive operator, and used by nothing else, becomes part of
+// that operator's epilogue:
+//   conv / depthwise / fc / add  + activation       -> act1 (or act2 after a residual)
+//   conv (any window)            + add(other)       -> residual epilogue, act2 = add's act
+//   resize_bilinear              + argmax           -> one resize-argmax pass
+// A fused node takes the place of the last operator it absorbed, so every
+// operand it reads has been produced by then.
+//
+// Kernel specialisation (Sec. 3.2, fourth technique): a 1x1 stride-1
+// convolution runs the plain pointwise GEMM; other windows run the same GEMM
+// with an implicit-im2col loader; a convolution that reads a graph input with
+// a small window (kh*kw*cin <= 32, the network stem) reads the NHWC input
+// directly and needs no layout conversion (Sec. 3.2, input conversion to the
+// sliced layout is skipped).
+#include <algorithm>
+#include <cstring>
+#include <new>
+
+#include "mgi_internal.h"
+
+namespace mgi {
+
+namespace {
+
+inline int slices(int c) { return (c + 7) / 8; }
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+uint16_t f32_to_f16_bits(float f) {
+    _Float16 h = (_Float16)f;  // round to nearest even
+    uint16_t b;
+    std::memcpy(&b, &h, 2);
+    return b;
+}
+
+struct Group {
+    int head = -1;          // heavy op
+    int last = -1;          // last absorbed op (position and output tensor)
+    int n = 1;
+    int act1 = MGI_ACT_NONE, act2 = MGI_ACT_NONE;
+    int residual_tensor = -1;
+    bool resize_argmax = false;
+};
+
+// Choose the GEMM tile for an (M x cout x K) problem: the largest tile that
+// still gives two workgroups per compute unit (256 CUs), else the smallest.
+GemmTile pick_tile(size_t M, int cout) {
+    GemmTile t;
+    int npad = ((cout + 15) / 16) * 16;
+    t.bn = npad <= 32 ? 32 : (npad <= 64 ? 64 : 128);
+    size_t ntiles = (npad + t.bn - 1) / t.bn;
+    const int bms[3] = {128, 64, 32};
+    t.bm = 32;
+    for (int bm : bms) {
+        size_t tiles = ((M + bm - 1) / bm) * ntiles;
+        if (tiles >= 512) { t.bm = bm; break; }
+    }
+    return t;
+}
+
+}  // namespace
+
+mgi_status build_plan(const mgi_graph &g, const mgi_options &o, mgi_plan &p) {
+    const int nops = (int)g.ops.size();
+    if (g.outputs.empty()) return fail(MGI_ERR_STATE, "mgi_graph_finalize: no output marked");
+    if (o.planner != MGI_PLANNER_NAIVE && o.planner != MGI_PLANNER_GREEDY)
+        return fail(MGI_ERR_UNSUPPORTED, "mgi_graph_finalize: unknown planner");
+    if (o.dtype != MGI_DTYPE_FP16)
+        return fail(MGI_ERR_UNSUPPORTED, "mgi_graph_finalize: only fp16 storage is built");
+
+    std::vector<char> is_output(nops, 0);
+    for (int t : g.outputs) is_output[t] = 1;
+    std::vector<std::vector<int>> consumers(nops);
+    for (int i = 0; i < nops; ++i)
+        for (int t : g.ops[i].in) consumers[t].push_back(i);
+
+    // ---------------------------------------------------------------- fusion
+    std::vector<int> group_of(nops, -1);
+    std::vector<Group> groups;
+    auto single_private_use = [&](int t) {
+        return consumers[t].size() == 1 && !is_output[t];
+    };
+    for (int i = 0; i < nops; ++i) {
+        const GOp &op = g.ops[i];
+        if (op.kind == OpKind::Input) continue;
+        if (o.fuse && op.kind == OpKind::Activation) {
+            int t = op.in[0];
+            int gi = group_of[t];
+            if (gi >= 0 && groups[gi].last == t && single_private_use(t)) {
+                Group &G = groups[gi];
+                OpKind hk = g.ops[G.head].kind;
+                bool ok_kind = hk == OpKind::Conv2d || hk == OpKind::Depthwise ||
+                               hk == OpKind::FC || hk == OpKind::Add;
+                int &slot = (G.residual_tensor >= 0) ? G.act2 : G.act1;
+                if (ok_kind && !G.resize_argmax && slot == MGI_ACT_NONE) {
+                    slot = op.act;
+                    G.last = i;
+                    G.n++;
+                    group_of[i] = gi;
+                    continue;
+                }
+            }
+        }
+        if (o.fuse && op.kind == OpKind::Add) {
+            bool fused = false;
+            for (int side = 0; side < 2 && !fused; ++side) {
+                int t = op.in[side], other = op.in[1 - side];
+                if (t == other) break;
+                int gi = group_of[t];
+                if (gi < 0 || groups[gi].last != t || !single_private_use(t)) continue;
+                Group &G = groups[gi];
+                if (g.ops[G.head].kind != OpKind::Conv2d || G.residual_tensor >= 0) continue;
+                G.residual_tensor = other;
+                G.act2 = op.act;
+                G.last = i;
+                G.n++;
+                group_of[i] = gi;
+                fused = true;
+            }
+            if (fused) continue;
+        }
+        if (o.fuse && op.kind == OpKind::Argmax) {
+            int t = op.in[0];
+            int gi = group_of[t];
+            if (gi >= 0 && groups[gi].last == t && single_private_use(t) &&
+                g.ops[groups[gi].head].kind == OpKind::ResizeBilinear && groups[gi].n == 1) {
+                Group &G = groups[gi];
+                G.resize_argmax = true;
+                G.last = i;
+                G.n++;
+                group_of[i] = gi;
+                continue;
+            }
+        }
+        Group G;
+        G.head = i;
+        G.last = i;
+        if (op.kind == OpKind::Conv2d || op.kind == OpKind::Depthwise || op.kind == OpKind::Add ||
+            op.kind == OpKind::Activation)
+            G.act1 = op.act;
+        group_of[i] = (int)groups.size();
+        groups.push_back(G);
+    }
+    // execution order: position of the last absorbed op
+    std::vector<int> order(groups.size());
+    for (size_t k = 0; k < groups.size(); ++k) order[k] = (int)k;
+    std::stable_sort(order.begin(), order.end(),
+                     [&](int a, int b) { return groups[a].last < groups[b].last; });
+
+    // ------------------------------------------------------- buffers, nodes
+    p.bufs.clear();
+    p.nodes.clear();
+    std::vector<int> c8_buf(nops, -1);   // graph tensor -> C8 (or other) buffer holding it
+    std::vector<int> flat_buf(nops, -1); // graph tensor -> F32 / I32 buffer
+    std::vector<int> in_buf(nops, -1);   // graph input tensor -> NHWC_IN buffer
+    std::vector<int> out_index(nops, -1);
+    for (size_t k = 0; k < g.outputs.size(); ++k) out_index[g.outputs[k]] = (int)k;
+
+    p.input_bufs.clear();
+    p.input_shapes.clear();
+    p.input_dtypes.clear();
+    for (size_t k = 0; k < g.inputs.size(); ++k) {
+        int t = g.inputs[k];
+        Buf b;
+        b.layout = Layout::NHWC_IN;
+        b.shape = g.ops[t].out;
+        b.in_dtype = g.ops[t].in_dtype;
+        b.bytes = b.shape.elems() * (b.in_dtype == MGI_DTYPE_FP16 ? 2 : 4);
+        b.loc = Loc::Input;
+        b.index = (int)k;
+        b.graph_tensor = t;
+        in_buf[t] = (int)p.bufs.size();
+        p.input_bufs.push_back(in_buf[t]);
+        p.input_shapes.push_back(b.shape);
+        p.input_dtypes.push_back(b.in_dtype);
+        p.bufs.push_back(b);
+    }
+
+    auto new_buf = [&](Layout L, const Shape &s, int tensor) {
+        Buf b;
+        b.layout = L;
+        b.shape = s;
+        if (L == Layout::C8) b.bytes = (size_t)slices(s.c) * 8 * s.pixels() * 2;
+        else b.bytes = s.elems() * 4;
+        b.graph_tensor = tensor;
+        if (tensor >= 0 && out_index[tensor] >= 0 && L != Layout::C8) {
+            b.loc = Loc::Output;
+            b.index = out_index[tensor];
+        }
+        p.bufs.push_back(b);
+        return (int)p.bufs.size() - 1;
+    };
+    auto add_node = [&](Node &&nd) {
+        p.nodes.push_back(std::move(nd));
+        return (int)p.nodes.size() - 1;
+    };
+    // a C8 view of graph tensor t, converting a graph input on first use
+    auto need_c8 = [&](int t) -> int {
+        if (c8_buf[t] >= 0) return c8_buf[t];
+        if (g.ops[t].kind == OpKind::Input) {
+            Node nd;
+            nd.kind = NodeKind::Ingest;
+            nd.kname = "ingest";
+            nd.op = t;
+            nd.out_tensor = -1;
+            nd.n_fused = 0;
+            nd.in = {in_buf[t]};
+            nd.out = new_buf(Layout::C8, g.ops[t].out, -1);
+            const int ob = nd.out;
+            add_node(std::move(nd));
+            c8_buf[t] = ob;
+            return ob;
+        }
+        return -1;
+    };
+
+    for (int gk : order) {
+        const Group &G = groups[gk];
+        const GOp &op = g.ops[G.head];
+        const Shape out_shape = g.ops[G.last].out;
+        Node nd;
+        nd.op = G.head;
+        nd.out_tensor = G.last;
+        nd.n_fused = G.n;
+        nd.act1 = G.act1;
+        nd.act2 = G.act2;
+        switch (op.kind) {
+            case OpKind::Conv2d: {
+                const Shape x = g.ops[op.in[0]].out;
+                const mgi_conv_desc &d = op.conv;
+                nd.conv = d;
+                const bool from_input = g.ops[op.in[0]].kind == OpKind::Input;
+                if (from_input && d.kh * d.kw * x.c <= 32 && d.cout <= 64) {
+                    nd.kind = NodeKind::Stem;
+                    nd.kname = "conv_stem";
+                    nd.in = {in_buf[op.in[0]]};
+                    nd.ksl = 4;
+                    nd.ksp = 4;
+                } else {
+                    int xb = need_c8(op.in[0]);
+                    if (xb < 0) return fail(MGI_ERR_UNSUPPORTED, "conv2d input has no sliced form");
+                    nd.kind = NodeKind::Gemm;
+                    nd.in = {xb};
+                    nd.taps = !(d.kh == 1 && d.kw == 1 && d.stride_h == 1 && d.stride_w == 1 &&
+                                d.pad_t == 0 && d.pad_b == 0 && d.pad_l == 0 && d.pad_r == 0);
+                    nd.kname = nd.taps ? "conv_igemm" : "pw_gemm";
+                    nd.ksl = d.kh * d.kw * slices(x.c);
+                    nd.ksp = (nd.ksl + 3) / 4 * 4;
+                }
+                nd.nb16 = (d.cout + 15) / 16;
+                nd.tile = pick_tile(out_shape.pixels(), d.cout);
+                if (G.residual_tensor >= 0) {
+                    int rb = need_c8(G.residual_tensor);
+                    if (rb < 0) rb = c8_buf[G.residual_tensor];
+                    if (rb < 0) return fail(MGI_ERR_UNSUPPORTED, "residual operand has no sliced form");
+                    nd.residual = rb;
+                }
+                nd.out = new_buf(Layout::C8, out_shape, G.last);
+                c8_buf[G.last] = nd.out;
+                break;
+            }
+            case OpKind::Depthwise: {
+                int xb = need_c8(op.in[0]);
+                if (xb < 0) return fail(MGI_ERR_UNSUPPORTED, "depthwise input has no sliced form");
+                nd.kind = NodeKind::Depthwise;
+                nd.kname = "dw_conv";
+                nd.conv = op.conv;
+                nd.in = {xb};
+                nd.out = new_buf(Layout::C8, out_shape, G.last);
+                c8_buf[G.last] = nd.out;
+                break;
+            }
+            case OpKind::Add:
+            case OpKind::Activation: {
+                nd.kind = op.kind == OpKind::Add ? NodeKind::Add : NodeKind::Act;
+                nd.kname = op.kind == OpKind::Add ? "add" : "activation";
+                for (int t : op.in) {
+                    int b = need_c8(t);
+                    if (b < 0) b = c8_buf[t];
+                    if (b < 0) return fail(MGI_ERR_UNSUPPORTED, "element-wise operand is not sliced");
+                    nd.in.push_back(b);
+                }
+                nd.out = new_buf(Layout::C8, out_shape, G.last);
+                c8_buf[G.last] = nd.out;
+                break;
+            }
+            case OpKind::GlobalAvgPool: {
+                int xb = need_c8(op.in[0]);
+                if (xb < 0) xb = c8_buf[op.in[0]];
+                if (xb < 0) return fail(MGI_ERR_UNSUPPORTED, "pool input is not sliced");
+                nd.kind = NodeKind::Gap;
+                nd.kname = "global_avgpool";
+                nd.in = {xb};
+                nd.out = new_buf(Layout::C8, out_shape, G.last);
+                c8_buf[G.last] = nd.out;
+                break;
+            }
+            case OpKind::FC: {
+                int xb = need_c8(op.in[0]);
+                if (xb < 0) xb = c8_buf[op.in[0]];
+                if (xb < 0)
+                    return fail(MGI_ERR_UNSUPPORTED, "fc input must come from a sliced tensor");
+                const Shape x = g.ops[op.in[0]].out;
+                nd.kind = NodeKind::FC;
+                nd.kname = "fc_gemm";
+                nd.in = {xb};
+                nd.ksl = slices(x.c);
+                nd.ksp = (nd.ksl + 3) / 4 * 4;
+                nd.nb16 = (op.cout + 15) / 16;
+                nd.conv.cout = op.cout;
+                nd.tile = pick_tile(out_shape.pixels(), op.cout);
+                nd.out = new_buf(Layout::F32, out_shape, G.last);
+                flat_buf[G.last] = nd.out;
+                break;
+            }
+            case OpKind::Softmax: {
+                int t = op.in[0];
+                int xb = flat_buf[t];
+                if (xb < 0) {
+                    int cb = need_c8(t);
+                    if (cb < 0) cb = c8_buf[t];
+                    if (cb < 0) return fail(MGI_ERR_UNSUPPORTED, "softmax input unavailable");
+                    Node ex;
+                    ex.kind = NodeKind::Export;
+                    ex.kname = "export";
+                    ex.out_tensor = -1;
+                    ex.n_fused = 0;
+                    ex.in = {cb};
+                    ex.out = new_buf(Layout::F32, g.ops[t].out, -1);
+                    xb = ex.out;
+                    add_node(std::move(ex));
+                }
+                nd.kind = NodeKind::Softmax;
+                nd.kname = "softmax";
+                nd.in = {xb};
+                nd.out = new_buf(Layout::F32, out_shape, G.last);
+                flat_buf[G.last] = nd.out;
+                break;
+            }
+            case OpKind::Concat: {
+                nd.kind = NodeKind::Concat;
+                nd.kname = "concat";
+                for (int t : op.in) {
+                    int b = need_c8(t);
+                    if (b < 0) b = c8_buf[t];
+                    if (b < 0) return fail(MGI_ERR_UNSUPPORTED, "concat operand is not sliced");
+                    nd.in.push_back(b);
+                }
+                nd.out = new_buf(Layout::C8, out_shape, G.last);
+                c8_buf[G.last] = nd.out;
+                break;
+            }
+            case OpKind::ResizeBilinear: {
+                int xb = need_c8(op.in[0]);
+                if (xb < 0) xb = c8_buf[op.in[0]];
+                if (xb < 0) return fail(MGI_ERR_UNSUPPORTED, "resize input is not sliced");
+                nd.in = {xb};
+                nd.align_corners = op.align_corners;
+                if (G.resize_argmax) {
+                    nd.kind = NodeKind::ResizeArgmax;
+                    nd.kname = "resize_argmax";
+                    nd.out = new_buf(Layout::I32, out_shape, G.last);
+                    flat_buf[G.last] = nd.out;
+                } else {
+                    nd.kind = NodeKind::Resize;
+                    nd.kname = "resize_bilinear";
+                    nd.out = new_buf(Layout::C8, out_shape, G.last);
+                    c8_buf[G.last] = nd.out;
+                }
+                break;
+            }
+            case OpKind::Argmax: {
+                int xb = need_c8(op.in[0]);
+                if (xb < 0) xb = c8_buf[op.in[0]];
+                if (xb < 0) return fail(MGI_ERR_UNSUPPORTED, "argmax input is not sliced");
+                nd.kind = NodeKind::Argmax;
+                nd.kname = "argmax";
+                nd.in = {xb};
+                nd.out = new_buf(Layout::I32, out_shape, G.last);
+                flat_buf[G.last] = nd.out;
+                break;
+            }
+            case OpKind::Input:
+                break;
+        }
+        add_node(std::move(nd));
+        // a sliced tensor that is a graph output is exported right away
+        const int t = G.last;
+        if (out_index[t] >= 0 && c8_buf[t] >= 0 && p.bufs[c8_buf[t]].layout == Layout::C8 &&
+            flat_buf[t] < 0) {
+            Node ex;
+            ex.kind = NodeKind::Export;
+            ex.kname = "export";
+            ex.out_tensor = -1;
+            ex.n_fused = 0;
+            ex.in = {c8_buf[t]};
+            Buf b;
+            b.layout = Layout::F32;
+            b.shape = g.ops[t].out;
+            b.bytes = b.shape.elems() * 4;
+            b.loc = Loc::Output;
+            b.index = out_index[t];
+            b.graph_tensor = t;
+            p.bufs.push_back(b);
+            ex.out = (int)p.bufs.size() - 1;
+            flat_buf[t] = ex.out;
+            add_node(std::move(ex));
+        }
+    }
+
+    // outputs
+    p.output_bufs.assign(g.outputs.size(), -1);
+    p.output_tensor = g.outputs;
+    p.output_shapes.clear();
+    p.output_dtypes.clear();
+    for (size_t k = 0; k < g.outputs.size(); ++k) {
+        int t = g.outputs[k];
+        int b = flat_buf[t];
+        if (b < 0 || p.bufs[b].loc != Loc::Output)
+            return fail(MGI_ERR_UNSUPPORTED, "output tensor " + std::to_string(t) +
+                                                 " was fused away or cannot be exported");
+        p.output_bufs[k] = b;
+        Shape s = g.ops[t].out;
+        p.output_shapes.push_back(s);
+        p.output_dtypes.push_back(p.bufs[b].layout == Layout::I32 ? MGI_DTYPE_INT32 : MGI_DTYPE_FP32);
+    }
+
+    // ------------------------------------------------------------ lifetimes
+    for (size_t i = 0; i < p.nodes.size(); ++i) {
+        Node &nd = p.nodes[i];
+        p.bufs[nd.out].producer = (int)i;
+        for (int b : nd.in) p.bufs[b].last_use = (int)i;
+        if (nd.residual >= 0) p.bufs[nd.residual].last_use = (int)i;
+    }
+
+    // -------------------------------------------------------------- planning
+    std::vector<int> arena;
+    std::vector<size_t> sizes;
+    std::vector<int> first, last;
+    for (size_t b = 0; b < p.bufs.size(); ++b) {
+        if (p.bufs[b].loc != Loc::Arena) continue;
+        arena.push_back((int)b);
+        sizes.push_back(p.bufs[b].bytes);
+        first.push_back(p.bufs[b].producer);
+        last.push_back(p.bufs[b].last_use);
+    }
+    PlanResult naive = plan_naive(sizes);
+    PlanResult pr = (o.planner == MGI_PLANNER_GREEDY && !o.materialize_all)
+                        ? plan_greedy(sizes, first, last)
+                        : naive;
+    p.mem_naive = 0;
+    for (size_t s : sizes) p.mem_naive += s;
+    p.mem_planned = 0;
+    std::vector<size_t> obj_off(pr.object_size.size());
+    size_t off = 0;
+    for (size_t k = 0; k < pr.object_size.size(); ++k) {
+        p.mem_planned += pr.object_size[k];
+        obj_off[k] = off;
+        off = align256(off + pr.object_size[k]);
+    }
+    p.n_objects = (int)pr.object_size.size();
+    p.workspace_bytes = std::max<size_t>(off, 256);
+    for (size_t i = 0; i < arena.size(); ++i) p.bufs[arena[i]].offset = obj_off[pr.object_of[i]];
+
+    // --------------------------------------------------------------- packing
+    // GEMM weights (A operand of v_mfma_f32_16x16x32_f16): for output block nb
+    // (16 channels) and K slice ks (8 inputs), 16 rows x 8 halves, contiguous:
+    //   packed[((nb * ksp + ks) * 16 + row) * 8 + j] = W[nb*16 + row][k(ks, j)]
+    // so one wave's fragment for (nb, four slices) is 1 KiB of consecutive
+    // 16-byte lane loads.  K order for an implicit GEMM: tap-major
+    // (ky, kx), then input channel slices; for the stem: k = (ky*kw + kx)*cin + ci.
+    std::vector<uint8_t> &blob = p.weights;
+    blob.clear();
+    auto reserve = [&](size_t bytes) {
+        size_t o2 = align256(blob.size());
+        blob.resize(o2 + align256(bytes), 0);
+        return o2;
+    };
+    for (Node &nd : p.nodes) {
+        const GOp &op = g.ops[nd.op >= 0 ? nd.op : 0];
+        if (nd.kind == NodeKind::Gemm || nd.kind == NodeKind::Stem || nd.kind == NodeKind::FC) {
+            const Shape x = g.ops[op.in[0]].out;
+            const int cin = x.c;
+            const int cout = nd.kind == NodeKind::FC ? op.cout : op.conv.cout;
+            const int kh = nd.kind == NodeKind::FC ? 1 : op.conv.kh;
+            const int kw = nd.kind == NodeKind::FC ? 1 : op.conv.kw;
+            const int sin = slices(cin);
+            nd.w_bytes = (size_t)nd.nb16 * nd.ksp * 16 * 8 * 2;
+            nd.w_off = reserve(nd.w_bytes);
+            uint16_t *wp = reinterpret_cast<uint16_t *>(blob.data() + nd.w_off);
+            for (int co = 0; co < cout; ++co) {
+                const int nb = co / 16, row = co % 16;
+                for (int ky = 0; ky < kh; ++ky)
+                    for (int kx = 0; kx < kw; ++kx)
+                        for (int ci = 0; ci < cin; ++ci) {
+                            int ks, j;
+                            if (nd.kind == NodeKind::Stem) {
+                                int k = (ky * kw + kx) * cin + ci;
+                                ks = k / 8;
+                                j = k % 8;
+                            } else {
+                                ks = (ky * kw + kx) * sin + ci / 8;
+                                j = ci % 8;
+                            }
+                            float v = op.w[(((size_t)co * kh + ky) * kw + kx) * cin + ci];
+                            wp[(((size_t)nb * nd.ksp + ks) * 16 + row) * 8 + j] = f32_to_f16_bits(v);
+                        }
+            }
+            nd.b_bytes = (size_t)nd.nb16 * 16 * 4;
+            nd.b_off = reserve(nd.b_bytes);
+            float *bp = reinterpret_cast<float *>(blob.data() + nd.b_off);
+            for (int co = 0; co < cout; ++co) bp[co] = op.b[co];
+        } else if (nd.kind == NodeKind::Depthwise) {
+            // fp32 taps per slice: [S][kh*kw][8], bias [S*8]; padded channels 0
+            const int c = op.out.c, S = slices(c), taps = op.conv.kh * op.conv.kw;
+            nd.w_bytes = (size_t)S * taps * 8 * 4;
+            nd.w_off = reserve(nd.w_bytes);
+            float *wp = reinterpret_cast<float *>(blob.data() + nd.w_off);
+            for (int ch = 0; ch < c; ++ch)
+                for (int t = 0; t < taps; ++t)
+                    wp[((size_t)(ch / 8) * taps + t) * 8 + ch % 8] = op.w[(size_t)ch * taps + t];
+            nd.b_bytes = (size_t)S * 8 * 4;
+            nd.b_off = reserve(nd.b_bytes);
+            float *bp = reinterpret_cast<float *>(blob.data() + nd.b_off);
+            for (int ch = 0; ch < c; ++ch) bp[ch] = op.b[ch];
+        }
+    }
+    p.weight_bytes = std::max<size_t>(blob.size(), 256);
+    p.opt = o;
+    return MGI_OK;
+}
+
+}  // namespace mgi
+
+using namespace mgi;
+
+extern "C" mgi_status mgi_graph_finalize(const mgi_graph *g, const mgi_options *o, mgi_plan **p) {
+    if (!g || !o || !p) return fail(MGI_ERR_INVALID_ARG, "mgi_graph_finalize: null pointer");
+    *p = nullptr;
+    mgi_plan *plan = new (std::nothrow) mgi_plan();
+    if (!plan) return fail(MGI_ERR_OOM_HOST, "mgi_graph_finalize: out of host memory");
+    mgi_status s;
+    try {
+        s = build_plan(*g, *o, *plan);
+    } catch (const std::bad_alloc &) {
+        s = fail(MGI_ERR_OOM_HOST, "mgi_graph_finalize: out of host memory");
+    }
+    if (s != MGI_OK) {
+        delete plan;
+        return s;
+    }
+    *p = plan;
+    return MGI_OK;
+}
+
+extern "C" mgi_status mgi_plan_workspace_bytes(const mgi_plan *p, size_t *bytes) {
+    if (!p || !bytes) return fail(MGI_ERR_INVALID_ARG, "mgi_plan_workspace_bytes: null pointer");
+    *bytes = p->workspace_bytes;
+    return MGI_OK;
+}
+
+extern "C" mgi_status mgi_plan_weight_bytes(const mgi_plan *p, size_t *bytes) {
+    if (!p || !bytes) return fail(MGI_ERR_INVALID_ARG, "mgi_plan_weight_bytes: null pointer");
+    *bytes = p->weight_bytes;
+    return MGI_OK;
+}
+
+extern "C" mgi_status mgi_plan_memory_report(const mgi_plan *p, size_t *naive, size_t *planned,
+                                             int *n_objects) {
+    if (!p) return fail(MGI_ERR_INVALID_ARG, "mgi_plan_memory_report: null plan");
+    if (naive) *naive = p->mem_naive;
+    if (planned) *planned = p->mem_planned;
+    if (n_objects) *n_objects = p->n_objects;
+    return MGI_OK;
+}
+
+extern "C" mgi_status mgi_plan_num_io(const mgi_plan *p, int *n_inputs, int *n_outputs) {
+    if (!p) return fail(MGI_ERR_INVALID_ARG, "mgi_plan_num_io: null plan");
+    if (n_inputs) *n_inputs = (int)p->input_bufs.size();
+    if (n_outputs) *n_outputs = (int)p->output_bufs.size();
+    return MGI_OK;
+}
+
+extern "C" mgi_status mgi_plan_io_info(const mgi_plan *p, int is_output, int index, int *n, int *h,
+                                       int *w, int *c, int *dtype, size_t *bytes) {
+    if (!p) return fail(MGI_ERR_INVALID_ARG, "mgi_plan_io_info: null plan");
+    const auto &shapes = is_output ? p->output_shapes : p->input_shapes;
+    const auto &types = is_output ? p->output_dtypes : p->input_dtypes;
+    if (index < 0 || index >= (int)shapes.size())
+        return fail(MGI_ERR_INVALID_ARG, "mgi_plan_io_info: index out of range");
+    const Shape s = shapes[index];
+    if (n) *n = s.n;
+    if (h) *h = s.h;
+    if (w) *w = s.w;
+    if (c) *c = s.c;
+    if (dtype) *dtype = types[index];
+    if (bytes) *bytes = s.elems() * (types[index] == MGI_DTYPE_FP16 ? 2 : 4);
+    return MGI_OK;
+}
+
+extern "C" mgi_status mgi_plan_node_count(const mgi_plan *p, int *count) {
+    if (!p || !count) return fail(MGI_ERR_INVALID_ARG, "mgi_plan_node_count: null pointer");
+    *count = (int)p->nodes.size();
+    return MGI_OK;
+}
+
+extern "C" mgi_status mgi_plan_node_info(const mgi_plan *p, int i, const char **kind,
+                                         int *tensor_id, int *n, int *h, int *w, int *c,
+                                         int *n_fused) {
+    if (!p) return fail(MGI_ERR_INVALID_ARG, "mgi_plan_node_info: null plan");
+    if (i < 0 || i >= (int)p->nodes.size())
+        return fail(MGI_ERR_INVALID_ARG, "mgi_plan_node_info: node index out of range");
+    const Node &nd = p->nodes[i];
+    const Shape s = p->bufs[nd.out].shape;
+    if (kind) *kind = nd.kname;
+    if (tensor_id) *tensor_id = nd.out_tensor;
+    if (n) *n = s.n;
+    if (h) *h = s.h;
+    if (w) *w = s.w;
+    if (c) *c = s.c;
+    if (n_fused) *n_fused = nd.n_fused;
+    return MGI_OK;
+}

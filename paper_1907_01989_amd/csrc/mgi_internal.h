@@ -1,0 +1,145 @@
+// Internal data structures of the mgi engine (host side).
+//
+// Activation storage ("C8 layout"): a tensor (n, h, w, c) is split into
+// S = ceil(c / 8) slices of 8 channels; slice s of all n*h*w pixels is stored
+// contiguously, pixel-major, 8 fp16 values (16 bytes) per pixel:
+//     element (n, y, x, ch) at  ((ch / 8) * M + (n * h + y) * w + x) * 8 + ch % 8
+// with M = n * h * w.  Channels c..8S-1 of the last slice are kept at zero.
+// This is the channel-sliced layout of the paper (Sec. 4, PHWC4) widened to
+// 8 channels so that one lane moves 16 bytes and 8 neighbouring lanes fill a
+// 128-byte line; with n = 1 it is exactly PHWC8.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "../../include/mgi.h"
+
+namespace mgi {
+
+enum class OpKind {
+    Input, Conv2d, Depthwise, Add, Activation, GlobalAvgPool, FC, Softmax, Concat,
+    ResizeBilinear, Argmax
+};
+
+struct Shape {
+    int n = 0, h = 0, w = 0, c = 0;
+    size_t pixels() const { return (size_t)n * h * w; }
+    size_t elems() const { return pixels() * c; }
+};
+
+// One graph operator; its output is tensor id == its index in Graph::ops.
+struct GOp {
+    OpKind kind;
+    std::vector<int> in;
+    Shape out;
+    mgi_conv_desc conv{};       // Conv2d / Depthwise
+    int act = MGI_ACT_NONE;     // Conv2d / Depthwise / Add / Activation
+    int in_dtype = MGI_DTYPE_FP32;  // Input
+    int oh = 0, ow = 0, align_corners = 1;  // ResizeBilinear
+    int cout = 0;               // FC
+    std::vector<float> w, b;    // weights as given (OHWI / CHW / COUT x CIN), bias
+};
+
+}  // namespace mgi
+
+struct mgi_graph {
+    std::vector<mgi::GOp> ops;
+    std::vector<int> outputs;
+    std::vector<int> inputs;  // tensor ids of Input ops, in declaration order
+};
+
+namespace mgi {
+
+// Storage classes of materialised tensors.
+enum class Layout { C8, F32, I32, NHWC_IN };
+enum class Loc { Arena, Input, Output };
+
+struct Buf {
+    Layout layout = Layout::C8;
+    Shape shape;
+    size_t bytes = 0;
+    Loc loc = Loc::Arena;
+    int index = -1;          // input / output index for Loc::Input / Loc::Output
+    size_t offset = 0;       // arena offset for Loc::Arena
+    int producer = -1;       // node index (-1: graph input)
+    int last_use = -1;       // last node index that reads it (-1: none)
+    int graph_tensor = -1;   // graph tensor id it holds (-1: internal)
+    int in_dtype = MGI_DTYPE_FP32;  // element type of a NHWC_IN buffer
+};
+
+enum class NodeKind {
+    Ingest, Stem, Gemm, Depthwise, Add, Act, Gap, FC, Softmax, Concat, Resize, Argmax,
+    ResizeArgmax, Export
+};
+
+// Tile shape of the MFMA GEMM (pointwise, implicit-GEMM convolution, FC).
+struct GemmTile {
+    int bm = 64, bn = 64;
+};
+
+struct Node {
+    NodeKind kind;
+    const char *kname = "";
+    int op = -1;            // heavy graph op (first absorbed)
+    int out_tensor = -1;    // graph tensor represented by the output
+    int n_fused = 1;        // graph ops absorbed
+    std::vector<int> in;    // buffer ids
+    int out = -1;           // buffer id
+    int residual = -1;      // buffer id (Gemm / Stem epilogue), -1 = none
+    int act1 = MGI_ACT_NONE, act2 = MGI_ACT_NONE;
+    // weights in the packed blob
+    size_t w_off = 0, w_bytes = 0, b_off = 0, b_bytes = 0;
+    // GEMM geometry
+    int ksl = 0;            // K slices (8 wide) before padding
+    int ksp = 0;            // K slices padded to a multiple of 4
+    int nb16 = 0;           // output channel blocks of 16
+    bool taps = false;      // implicit GEMM over a kh x kw window
+    GemmTile tile;
+    mgi_conv_desc conv{};
+    int align_corners = 1;
+};
+
+}  // namespace mgi
+
+struct mgi_plan {
+    std::vector<mgi::Node> nodes;
+    std::vector<mgi::Buf> bufs;
+    std::vector<int> input_bufs;   // graph input i -> buffer id
+    std::vector<int> output_bufs;  // graph output i -> buffer id
+    std::vector<int> output_tensor;
+    std::vector<mgi::Shape> input_shapes, output_shapes;
+    std::vector<int> input_dtypes, output_dtypes;
+    std::vector<uint8_t> weights;  // packed host copy (released after bind)
+    size_t weight_bytes = 0;
+    size_t workspace_bytes = 0;
+    size_t mem_naive = 0, mem_planned = 0;
+    int n_objects = 0;
+    mgi_options opt{};
+    void *dev_ws = nullptr;
+    void *dev_w = nullptr;
+    bool bound = false;
+    std::vector<void *> last_outputs;  // output pointers of the latest run
+};
+
+namespace mgi {
+
+// error reporting (thread-local last error)
+mgi_status fail(mgi_status s, const std::string &msg);
+
+// planner (Sec. 5).  Tensors are given by size and lifetime [first, last]
+// in node order (last = -1: never consumed).
+struct PlanResult {
+    std::vector<int> object_of;
+    std::vector<size_t> object_size;
+};
+PlanResult plan_naive(const std::vector<size_t> &sizes);
+PlanResult plan_greedy(const std::vector<size_t> &sizes, const std::vector<int> &first,
+                       const std::vector<int> &last);
+
+// finalize steps
+mgi_status build_plan(const mgi_graph &g, const mgi_options &o, mgi_plan &p);
+
+}  // namespace mgi

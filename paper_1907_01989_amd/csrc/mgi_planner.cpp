@@ -1,0 +1,120 @@
+// Intermediate-tensor planner (Sec. 5 of the paper).
+//
+// Greedy shared objects (Algorithm 1): operators are visited in execution
+// order.  Each intermediate output of an operator takes a new shared object if
+// the pool of free objects is empty, otherwise the free object closest in size
+// to the tensor (absolute difference), which grows to the tensor's size when
+// smaller.  After all outputs of the operator are placed, every intermediate
+// input whose last consumer is this operator returns its object to the pool.
+// Placing outputs before freeing inputs keeps an operator's output from
+// sharing memory with its own input.
+//
+// The pool is an ordered multimap keyed by object size (the binary search tree
+// of the paper) so "closest size" is a lower_bound plus one step back:
+// O(n log n) over n tensors.  Equal distances go to the lower object index;
+// the set of live objects needs no explicit container because an object is
+// either in the pool or attached to a live tensor.
+#include <algorithm>
+#include <cstdint>
+#include <map>
+
+#include "mgi_internal.h"
+
+namespace mgi {
+
+PlanResult plan_naive(const std::vector<size_t> &sizes) {
+    PlanResult r;
+    r.object_of.resize(sizes.size());
+    for (size_t t = 0; t < sizes.size(); ++t) {
+        r.object_of[t] = (int)t;
+        r.object_size.push_back(sizes[t]);
+    }
+    return r;
+}
+
+PlanResult plan_greedy(const std::vector<size_t> &sizes, const std::vector<int> &first,
+                       const std::vector<int> &last) {
+    const int n = (int)sizes.size();
+    PlanResult r;
+    r.object_of.assign(n, -1);
+    int max_op = -1;
+    for (int t = 0; t < n; ++t) max_op = std::max(max_op, std::max(first[t], last[t]));
+    // tensors produced / released at each operator, in tensor order
+    std::vector<std::vector<int>> produced(max_op + 1), released(max_op + 1);
+    for (int t = 0; t < n; ++t) {
+        produced[first[t]].push_back(t);
+        if (last[t] >= 0) released[last[t]].push_back(t);
+    }
+    // pool of free objects: size -> object index (ordered by size, then index)
+    std::multimap<size_t, int> pool;
+    auto pool_erase = [&](std::multimap<size_t, int>::iterator it) { pool.erase(it); };
+    for (int op = 0; op <= max_op; ++op) {
+        for (int t : produced[op]) {
+            const size_t sz = sizes[t];
+            int k;
+            if (pool.empty()) {
+                k = (int)r.object_size.size();
+                r.object_size.push_back(sz);
+            } else {
+                // candidates: the smallest object >= sz and the largest object < sz;
+                // among equal sizes the multimap keeps insertion order, so scan the
+                // run of equal keys for the lowest index.
+                auto hi = pool.lower_bound(sz);
+                std::multimap<size_t, int>::iterator best = pool.end();
+                auto better = [&](std::multimap<size_t, int>::iterator c) {
+                    if (best == pool.end()) return true;
+                    size_t dc = c->first > sz ? c->first - sz : sz - c->first;
+                    size_t db = best->first > sz ? best->first - sz : sz - best->first;
+                    return dc < db || (dc == db && c->second < best->second);
+                };
+                if (hi != pool.end()) {
+                    for (auto it = hi; it != pool.end() && it->first == hi->first; ++it)
+                        if (better(it)) best = it;
+                }
+                if (hi != pool.begin()) {
+                    auto lo = std::prev(hi);
+                    const size_t key = lo->first;
+                    for (auto it = pool.lower_bound(key); it != pool.end() && it->first == key; ++it)
+                        if (better(it)) best = it;
+                }
+                k = best->second;
+                pool_erase(best);
+                if (sz > r.object_size[k]) r.object_size[k] = sz;
+            }
+            r.object_of[t] = k;
+        }
+        for (int t : released[op]) {
+            const int k = r.object_of[t];
+            pool.emplace(r.object_size[k], k);
+        }
+    }
+    return r;
+}
+
+}  // namespace mgi
+
+using namespace mgi;
+
+extern "C" mgi_status mgi_planner_assign(int planner, int n_tensors, const size_t *sizes,
+                                         const int *first_op, const int *last_op, int *object_of,
+                                         size_t *object_sizes, int *n_objects) {
+    if (n_tensors < 0) return fail(MGI_ERR_INVALID_ARG, "mgi_planner_assign: n_tensors < 0");
+    if (n_tensors > 0 && (!sizes || !first_op || !last_op || !object_of || !object_sizes))
+        return fail(MGI_ERR_INVALID_ARG, "mgi_planner_assign: null pointer");
+    if (!n_objects) return fail(MGI_ERR_INVALID_ARG, "mgi_planner_assign: null n_objects");
+    std::vector<size_t> sz(sizes, sizes + n_tensors);
+    std::vector<int> fi(first_op, first_op + n_tensors), la(last_op, last_op + n_tensors);
+    for (int t = 0; t < n_tensors; ++t) {
+        if (fi[t] < 0 || (la[t] >= 0 && la[t] < fi[t]))
+            return fail(MGI_ERR_INVALID_ARG, "mgi_planner_assign: tensor " + std::to_string(t) +
+                                                 " has an invalid lifetime");
+    }
+    PlanResult r;
+    if (planner == MGI_PLANNER_NAIVE) r = plan_naive(sz);
+    else if (planner == MGI_PLANNER_GREEDY) r = plan_greedy(sz, fi, la);
+    else return fail(MGI_ERR_UNSUPPORTED, "mgi_planner_assign: unknown planner");
+    for (int t = 0; t < n_tensors; ++t) object_of[t] = r.object_of[t];
+    for (size_t k = 0; k < r.object_size.size(); ++k) object_sizes[k] = r.object_size[k];
+    *n_objects = (int)r.object_size.size();
+    return MGI_OK;
+}

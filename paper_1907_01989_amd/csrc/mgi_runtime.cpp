@@ -1,0 +1,264 @@
+// Binding and running a plan.
+//
+// mgi_plan_run enqueues every node's kernel on the caller's stream and
+// returns without synchronising (Sec. 3.2: programs are inserted into the
+// command queue and the GPU drains it with no CPU/GPU synchronisation).  All
+// operands are resolved from three bases: the arena, the caller's inputs and
+// the caller's outputs.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstring>
+
+#include "kernels.h"
+#include "mgi_internal.h"
+
+using namespace mgi;
+using namespace mgi::kern;
+
+namespace {
+
+mgi_status hip_fail(hipError_t e, const char *what) {
+    return fail(MGI_ERR_HIP, std::string(what) + ": " + hipGetErrorName(e) + " (" +
+                                 hipGetErrorString(e) + ")");
+}
+
+struct Bases {
+    char *ws;
+    const void *const *ins;
+    void *const *outs;
+};
+
+void *buf_ptr(const mgi_plan &p, int b, const Bases &B) {
+    const Buf &f = p.bufs[b];
+    switch (f.loc) {
+        case Loc::Arena: return B.ws + f.offset;
+        case Loc::Input: return const_cast<void *>(B.ins[f.index]);
+        case Loc::Output: return B.outs[f.index];
+    }
+    return nullptr;
+}
+
+inline int slices(int c) { return (c + 7) / 8; }
+
+hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStream_t st) {
+    const char *wbase = static_cast<const char *>(p.dev_w);
+    const Buf &ob = p.bufs[nd.out];
+    const Shape os = ob.shape;
+    void *y = buf_ptr(p, nd.out, B);
+    switch (nd.kind) {
+        case NodeKind::Ingest: {
+            const Buf &ib = p.bufs[nd.in[0]];
+            return launch_ingest(buf_ptr(p, nd.in[0], B), ib.in_dtype == MGI_DTYPE_FP16, (h8 *)y,
+                                 (int)ib.shape.pixels(), ib.shape.c, st);
+        }
+        case NodeKind::Stem: {
+            const Buf &ib = p.bufs[nd.in[0]];
+            StemParams q{};
+            q.x = buf_ptr(p, nd.in[0], B);
+            q.w = (const h8 *)(wbase + nd.w_off);
+            q.bias = (const float *)(wbase + nd.b_off);
+            q.res = nd.residual >= 0 ? (const h8 *)buf_ptr(p, nd.residual, B) : nullptr;
+            q.y = (h8 *)y;
+            q.N = ib.shape.n; q.H = ib.shape.h; q.W = ib.shape.w; q.C = ib.shape.c;
+            q.OH = os.h; q.OW = os.w; q.M = (int)os.pixels();
+            q.KW = nd.conv.kw; q.K = nd.conv.kh * nd.conv.kw * ib.shape.c;
+            q.sh = nd.conv.stride_h; q.sw = nd.conv.stride_w;
+            q.dh = nd.conv.dil_h; q.dw = nd.conv.dil_w;
+            q.pt = nd.conv.pad_t; q.pl = nd.conv.pad_l;
+            q.nb16 = nd.nb16; q.ns = slices(os.c);
+            q.act1 = nd.act1; q.act2 = nd.act2;
+            return launch_stem(q, ib.in_dtype == MGI_DTYPE_FP16, st);
+        }
+        case NodeKind::Gemm:
+        case NodeKind::FC: {
+            const Buf &ib = p.bufs[nd.in[0]];
+            GemmParams q{};
+            q.x = (const h8 *)buf_ptr(p, nd.in[0], B);
+            q.w = (const h8 *)(wbase + nd.w_off);
+            q.bias = (const float *)(wbase + nd.b_off);
+            q.res = nd.residual >= 0 ? (const h8 *)buf_ptr(p, nd.residual, B) : nullptr;
+            q.y = y;
+            q.M = (int)os.pixels();
+            q.Min = (int)ib.shape.pixels();
+            q.ksl = nd.ksl; q.ksp = nd.ksp;
+            q.nb16 = nd.nb16; q.ns = slices(os.c); q.cout = os.c;
+            q.act1 = nd.act1; q.act2 = nd.act2;
+            q.H = ib.shape.h; q.W = ib.shape.w; q.OH = os.h; q.OW = os.w;
+            q.sin = slices(ib.shape.c); q.kw = nd.conv.kw;
+            q.sh = nd.conv.stride_h; q.sw = nd.conv.stride_w;
+            q.dh = nd.conv.dil_h; q.dw = nd.conv.dil_w;
+            q.pt = nd.conv.pad_t; q.pl = nd.conv.pad_l;
+            return launch_gemm(q, nd.tile.bm, nd.tile.bn, nd.taps, nd.kind == NodeKind::FC, st);
+        }
+        case NodeKind::Depthwise: {
+            const Buf &ib = p.bufs[nd.in[0]];
+            DwParams q{};
+            q.x = (const h8 *)buf_ptr(p, nd.in[0], B);
+            q.w = (const float *)(wbase + nd.w_off);
+            q.bias = (const float *)(wbase + nd.b_off);
+            q.y = (h8 *)y;
+            q.N = ib.shape.n; q.H = ib.shape.h; q.W = ib.shape.w; q.S = slices(ib.shape.c);
+            q.OH = os.h; q.OW = os.w; q.KH = nd.conv.kh; q.KW = nd.conv.kw;
+            q.sh = nd.conv.stride_h; q.sw = nd.conv.stride_w;
+            q.dh = nd.conv.dil_h; q.dw = nd.conv.dil_w;
+            q.pt = nd.conv.pad_t; q.pl = nd.conv.pad_l;
+            q.act = nd.act1;
+            return launch_depthwise(q, st);
+        }
+        case NodeKind::Add:
+            return launch_add((const h8 *)buf_ptr(p, nd.in[0], B), (const h8 *)buf_ptr(p, nd.in[1], B),
+                              (h8 *)y, (size_t)slices(os.c) * os.pixels(), nd.act1, st);
+        case NodeKind::Act:
+            return launch_act((const h8 *)buf_ptr(p, nd.in[0], B), (h8 *)y,
+                              (size_t)slices(os.c) * os.pixels(), nd.act1, st);
+        case NodeKind::Gap: {
+            const Buf &ib = p.bufs[nd.in[0]];
+            return launch_gap((const h8 *)buf_ptr(p, nd.in[0], B), (h8 *)y, ib.shape.n,
+                              ib.shape.h * ib.shape.w, slices(ib.shape.c), st);
+        }
+        case NodeKind::Softmax:
+            return launch_softmax((const float *)buf_ptr(p, nd.in[0], B), (float *)y,
+                                  (int)os.pixels(), os.c, st);
+        case NodeKind::Concat: {
+            ConcatParams q{};
+            q.nin = (int)nd.in.size();
+            int off = 0;
+            for (int k = 0; k < q.nin; ++k) {
+                q.src[k] = (const h8 *)buf_ptr(p, nd.in[k], B);
+                q.coff[k] = off;
+                off += p.bufs[nd.in[k]].shape.c;
+            }
+            q.coff[q.nin] = off;
+            q.M = (int)os.pixels(); q.S = slices(os.c); q.C = os.c;
+            q.y = (h8 *)y;
+            return launch_concat(q, st);
+        }
+        case NodeKind::Resize:
+        case NodeKind::ResizeArgmax: {
+            const Buf &ib = p.bufs[nd.in[0]];
+            ResizeParams q{};
+            q.x = (const h8 *)buf_ptr(p, nd.in[0], B);
+            q.y = y;
+            q.N = ib.shape.n; q.H = ib.shape.h; q.W = ib.shape.w;
+            q.S = slices(ib.shape.c); q.C = ib.shape.c;
+            q.OH = os.h; q.OW = os.w;
+            q.align_corners = nd.align_corners;
+            return launch_resize(q, nd.kind == NodeKind::ResizeArgmax, st);
+        }
+        case NodeKind::Argmax: {
+            const Buf &ib = p.bufs[nd.in[0]];
+            return launch_argmax((const h8 *)buf_ptr(p, nd.in[0], B), (int *)y,
+                                 (int)ib.shape.pixels(), slices(ib.shape.c), ib.shape.c, st);
+        }
+        case NodeKind::Export: {
+            const Buf &ib = p.bufs[nd.in[0]];
+            return launch_export((const h8 *)buf_ptr(p, nd.in[0], B), (float *)y,
+                                 (int)ib.shape.pixels(), ib.shape.c, st);
+        }
+    }
+    return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+extern "C" mgi_status mgi_plan_destroy(mgi_plan *p) {
+    delete p;
+    return MGI_OK;
+}
+
+extern "C" mgi_status mgi_plan_bind(mgi_plan *p, void *dev_workspace, void *dev_weights,
+                                    void *stream) {
+    if (!p) return fail(MGI_ERR_INVALID_ARG, "mgi_plan_bind: null plan");
+    if (!dev_workspace || !dev_weights)
+        return fail(MGI_ERR_WORKSPACE, "mgi_plan_bind: workspace and weight buffers are required");
+    if (((uintptr_t)dev_workspace & 255) || ((uintptr_t)dev_weights & 255))
+        return fail(MGI_ERR_WORKSPACE, "mgi_plan_bind: buffers must be 256-byte aligned");
+    if (p->bound && p->weights.empty())
+        return fail(MGI_ERR_STATE, "mgi_plan_bind: plan already bound");
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (!p->weights.empty()) {
+        hipError_t e = hipMemcpyAsync(dev_weights, p->weights.data(), p->weights.size(),
+                                      hipMemcpyHostToDevice, st);
+        if (e != hipSuccess) return hip_fail(e, "mgi_plan_bind: weight upload");
+        e = hipStreamSynchronize(st);
+        if (e != hipSuccess) return hip_fail(e, "mgi_plan_bind: weight upload");
+    }
+    std::vector<uint8_t>().swap(p->weights);
+    p->dev_ws = dev_workspace;
+    p->dev_w = dev_weights;
+    p->bound = true;
+    return MGI_OK;
+}
+
+namespace {
+
+mgi_status run_plan(mgi_plan *p, const void *const *dev_inputs, void *const *dev_outputs,
+                    void *stream, void *const *events, const char *who) {
+    if (!p) return fail(MGI_ERR_INVALID_ARG, std::string(who) + ": null plan");
+    if (!p->bound) return fail(MGI_ERR_STATE, std::string(who) + ": plan is not bound");
+    if (!p->input_bufs.empty() && !dev_inputs)
+        return fail(MGI_ERR_INVALID_ARG, std::string(who) + ": null input array");
+    if (!dev_outputs) return fail(MGI_ERR_INVALID_ARG, std::string(who) + ": null output array");
+    for (size_t i = 0; i < p->input_bufs.size(); ++i)
+        if (!dev_inputs[i]) return fail(MGI_ERR_INVALID_ARG, std::string(who) + ": null input pointer");
+    for (size_t i = 0; i < p->output_bufs.size(); ++i)
+        if (!dev_outputs[i]) return fail(MGI_ERR_INVALID_ARG, std::string(who) + ": null output pointer");
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    Bases B{static_cast<char *>(p->dev_ws), dev_inputs, dev_outputs};
+    const size_t nn = p->nodes.size();
+    for (size_t i = 0; i < nn; ++i) {
+        if (events && events[i]) {
+            hipError_t e = hipEventRecord(static_cast<hipEvent_t>(events[i]), st);
+            if (e != hipSuccess) return hip_fail(e, (std::string(who) + ": event record").c_str());
+        }
+        hipError_t e = launch_node(*p, p->nodes[i], B, st);
+        if (e != hipSuccess)
+            return hip_fail(e, (std::string(who) + ": node " + std::to_string(i) + " (" +
+                                p->nodes[i].kname + ")").c_str());
+    }
+    if (events && events[nn]) {
+        hipError_t e = hipEventRecord(static_cast<hipEvent_t>(events[nn]), st);
+        if (e != hipSuccess) return hip_fail(e, (std::string(who) + ": event record").c_str());
+    }
+    p->last_outputs.assign(dev_outputs, dev_outputs + p->output_bufs.size());
+    return MGI_OK;
+}
+
+}  // namespace
+
+extern "C" mgi_status mgi_plan_run(mgi_plan *p, const void *const *dev_inputs,
+                                   void *const *dev_outputs, void *stream) {
+    return run_plan(p, dev_inputs, dev_outputs, stream, nullptr, "mgi_plan_run");
+}
+
+extern "C" mgi_status mgi_plan_run_timed(mgi_plan *p, const void *const *dev_inputs,
+                                         void *const *dev_outputs, void *stream,
+                                         void *const *events) {
+    if (!events) return fail(MGI_ERR_INVALID_ARG, "mgi_plan_run_timed: null event array");
+    return run_plan(p, dev_inputs, dev_outputs, stream, events, "mgi_plan_run_timed");
+}
+
+extern "C" mgi_status mgi_plan_read_node(mgi_plan *p, int i, void *dev_dst, void *stream) {
+    if (!p || !dev_dst) return fail(MGI_ERR_INVALID_ARG, "mgi_plan_read_node: null pointer");
+    if (i < 0 || i >= (int)p->nodes.size())
+        return fail(MGI_ERR_INVALID_ARG, "mgi_plan_read_node: node index out of range");
+    if (!p->opt.materialize_all)
+        return fail(MGI_ERR_STATE, "mgi_plan_read_node: plan was finalized without materialize_all");
+    if (!p->bound || p->last_outputs.size() != p->output_bufs.size())
+        return fail(MGI_ERR_STATE, "mgi_plan_read_node: no run has been enqueued");
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const Node &nd = p->nodes[i];
+    const Buf &b = p->bufs[nd.out];
+    Bases B{static_cast<char *>(p->dev_ws), nullptr, p->last_outputs.data()};
+    if (b.loc == Loc::Input) return fail(MGI_ERR_STATE, "mgi_plan_read_node: input buffer");
+    void *src = buf_ptr(*p, nd.out, B);
+    hipError_t e;
+    if (b.layout == Layout::C8) {
+        e = launch_export((const h8 *)src, (float *)dev_dst, (int)b.shape.pixels(), b.shape.c, st);
+    } else {
+        e = hipMemcpyAsync(dev_dst, src, b.bytes, hipMemcpyDeviceToDevice, st);
+    }
+    if (e != hipSuccess) return hip_fail(e, "mgi_plan_read_node");
+    return MGI_OK;
+}

@@ -1,0 +1,167 @@
+"""Thin Python front end: builds an mgi graph from a network description
+(a list of operator dicts, see the workload generators), finalises it, and
+binds it to torch-allocated device memory.  torch supplies device memory and
+streams only; every step of the forward pass runs in libmgi's kernels.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from . import _binding as B
+
+
+def _stream_handle(stream):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+def build_graph(desc):
+    """Create an mgi graph from ``desc`` (dict with "ops" and "outputs").
+    Returns the graph handle; tensor ids equal op indices."""
+    g = B.mgi_graph_create()
+    try:
+        for i, op in enumerate(desc["ops"]):
+            k = op["op"]
+            if k == "input":
+                n, h, w, c = op["shape"]
+                t = B.mgi_graph_add_input(g, n, h, w, c, op.get("dtype", B.DTYPE_FP32))
+            elif k == "conv2d":
+                d = B.conv_desc(op["kh"], op["kw"], op["stride"], op["dil"], op["pads"],
+                                op["cout"], op["act"])
+                t = B.mgi_graph_add_conv2d(g, op["in"], d, op["w"], op["b"])
+            elif k == "depthwise":
+                d = B.conv_desc(op["kh"], op["kw"], op["stride"], op["dil"], op["pads"], 0,
+                                op["act"])
+                t = B.mgi_graph_add_depthwise(g, op["in"], d, op["w"], op["b"])
+            elif k == "add":
+                t = B.mgi_graph_add_add(g, op["a"], op["b"], op["act"])
+            elif k == "activation":
+                t = B.mgi_graph_add_activation(g, op["in"], op["act"])
+            elif k == "gap":
+                t = B.mgi_graph_add_global_avgpool(g, op["in"])
+            elif k == "fc":
+                t = B.mgi_graph_add_fc(g, op["in"], op["cout"], op["w"], op["b"])
+            elif k == "softmax":
+                t = B.mgi_graph_add_softmax(g, op["in"])
+            elif k == "concat":
+                t = B.mgi_graph_add_concat(g, op["ins"])
+            elif k == "resize_bilinear":
+                t = B.mgi_graph_add_resize_bilinear(g, op["in"], op["oh"], op["ow"],
+                                                    op["align_corners"])
+            elif k == "argmax":
+                t = B.mgi_graph_add_argmax(g, op["in"])
+            else:
+                raise ValueError(f"unknown op {k}")
+            if t != i:
+                raise RuntimeError(f"tensor id {t} != op index {i}")
+        for t in desc["outputs"]:
+            B.mgi_graph_mark_output(g, t)
+    except Exception:
+        B.mgi_graph_destroy(g)
+        raise
+    return g
+
+
+def options(planner=B.PLANNER_GREEDY, fuse=True, materialize_all=False):
+    o = B.mgi_options_default()
+    o.planner = planner
+    o.fuse = int(fuse)
+    o.materialize_all = int(materialize_all)
+    return o
+
+
+class Plan:
+    """A finalised, device-bound network."""
+
+    def __init__(self, desc, planner=B.PLANNER_GREEDY, fuse=True, materialize_all=False,
+                 device="cuda:0", bind=True):
+        self.desc = desc
+        g = build_graph(desc)
+        try:
+            self.handle = B.mgi_graph_finalize(g, options(planner, fuse, materialize_all))
+        finally:
+            B.mgi_graph_destroy(g)
+        self.device = device
+        self.n_inputs, self.n_outputs = B.mgi_plan_num_io(self.handle)
+        self.inputs_info = [B.mgi_plan_io_info(self.handle, 0, i) for i in range(self.n_inputs)]
+        self.outputs_info = [B.mgi_plan_io_info(self.handle, 1, i) for i in range(self.n_outputs)]
+        self.workspace_bytes = B.mgi_plan_workspace_bytes(self.handle)
+        self.weight_bytes = B.mgi_plan_weight_bytes(self.handle)
+        self.bound = False
+        if bind:
+            self.bind()
+
+    # ---------------------------------------------------------------- device
+    def bind(self, stream=None):
+        import torch
+        self.ws = torch.empty(self.workspace_bytes + 256, dtype=torch.uint8, device=self.device)
+        self.wts = torch.empty(self.weight_bytes + 256, dtype=torch.uint8, device=self.device)
+        self._ws_ptr = (self.ws.data_ptr() + 255) & ~255
+        self._w_ptr = (self.wts.data_ptr() + 255) & ~255
+        B.mgi_plan_bind(self.handle, self._ws_ptr, self._w_ptr, _stream_handle(stream))
+        self.bound = True
+
+    def alloc_outputs(self):
+        import torch
+        outs = []
+        for shape, dt, _ in self.outputs_info:
+            n, h, w, c = shape
+            tdt = torch.int32 if dt == B.DTYPE_INT32 else torch.float32
+            if dt == B.DTYPE_INT32:
+                outs.append(torch.empty((n, h, w), dtype=tdt, device=self.device))
+            elif h == 1 and w == 1:
+                outs.append(torch.empty((n, c), dtype=tdt, device=self.device))
+            else:
+                outs.append(torch.empty((n, h, w, c), dtype=tdt, device=self.device))
+        return outs
+
+    def run(self, inputs, outputs=None, stream=None):
+        """Enqueue one forward pass; returns the output tensors (not synchronised)."""
+        if outputs is None:
+            outputs = self.alloc_outputs()
+        for x, (shape, dt, nbytes) in zip(inputs, self.inputs_info):
+            if x.numel() * x.element_size() != nbytes or not x.is_contiguous():
+                raise ValueError(f"input must be a contiguous NHWC tensor of {nbytes} bytes")
+        B.mgi_plan_run(self.handle, [x.data_ptr() for x in inputs],
+                       [y.data_ptr() for y in outputs], _stream_handle(stream))
+        return outputs
+
+    def input_tensors(self):
+        """Device copies of the description's input arrays."""
+        import torch
+        xs = []
+        for op in self.desc["ops"]:
+            if op["op"] == "input":
+                dt = torch.float16 if op.get("dtype", B.DTYPE_FP32) == B.DTYPE_FP16 else torch.float32
+                xs.append(torch.from_numpy(np.ascontiguousarray(op["data"])).to(self.device, dt))
+        return xs
+
+    # --------------------------------------------------------- introspection
+    def nodes(self):
+        return [B.mgi_plan_node_info(self.handle, i) for i in range(B.mgi_plan_node_count(self.handle))]
+
+    def read_node(self, i, stream=None):
+        import torch
+        info = B.mgi_plan_node_info(self.handle, i)
+        n, h, w, c = info["shape"]
+        if info["kind"] in ("argmax", "resize_argmax"):
+            dst = torch.empty((n, h, w, 1), dtype=torch.int32, device=self.device)
+        else:
+            dst = torch.empty((n, h, w, c), dtype=torch.float32, device=self.device)
+        B.mgi_plan_read_node(self.handle, i, dst.data_ptr(), _stream_handle(stream))
+        return info, dst
+
+    def memory_report(self):
+        return B.mgi_plan_memory_report(self.handle)
+
+    def close(self):
+        if getattr(self, "handle", None):
+            B.mgi_plan_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,198 @@
+"""Host-side tests of the C ABI (no GPU call is made).
+
+The library is loaded, its exports are checked against include/mgi.h, and the
+pure-host entry points (graph building, validation, fusion, planning) are run
+and compared with the oracle planner.
+"""
+import ctypes
+import os
+import random
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from oracle import planner as oplan
+from paper_1907_01989_amd import _binding as B
+from paper_1907_01989_amd import engine
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def header_functions():
+    text = open(os.path.join(ROOT, "include", "mgi.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(mgi_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = header_functions()
+    assert len(names) >= 30
+    L = ctypes.CDLL(B.LIB_PATH)
+    for n in names:
+        assert hasattr(L, n), f"{n} declared in mgi.h but not exported"
+    assert set(names) == set(B._SIGS), "binding and header disagree"
+
+
+def test_status_strings():
+    assert B.mgi_status_str(0) == "MGI_OK"
+    assert B.mgi_status_str(3) == "MGI_ERR_UNSUPPORTED"
+    assert B.mgi_status_str(99) == "MGI_ERR_UNKNOWN"
+
+
+def err(fn, *a, **k):
+    with pytest.raises(B.MgiError) as e:
+        fn(*a, **k)
+    return e.value.status
+
+
+def test_graph_validation_errors():
+    L = B.lib()
+    g = B.mgi_graph_create()
+    try:
+        assert err(B.mgi_graph_add_input, g, 0, 4, 4, 3) == 1
+        assert err(B.mgi_graph_add_input, g, 1, 4, 4, 3, B.DTYPE_INT32) == 3
+        x = B.mgi_graph_add_input(g, 1, 4, 4, 8)
+        w = np.zeros((8, 3, 3, 8), np.float32)
+        # bad stride, window larger than padded input, bad tensor id, bad activation
+        assert err(B.mgi_graph_add_conv2d, g, x, B.conv_desc(3, 3, (0, 1), cout=8), w) == 1
+        assert err(B.mgi_graph_add_conv2d, g, x, B.conv_desc(7, 7, cout=8), np.zeros((8, 7, 7, 8), np.float32)) == 2
+        assert err(B.mgi_graph_add_conv2d, g, 5, B.conv_desc(3, 3, cout=8), w) == 1
+        assert err(B.mgi_graph_add_conv2d, g, x, B.conv_desc(3, 3, cout=8, act=7), w) == 1
+        y = B.mgi_graph_add_conv2d(g, x, B.conv_desc(3, 3, pads=(1, 1, 1, 1), cout=8), w)
+        z = B.mgi_graph_add_input(g, 1, 4, 4, 16)
+        assert err(B.mgi_graph_add_add, g, y, z) == 2
+        assert err(B.mgi_graph_add_fc, g, y, 10, np.zeros((10, 128), np.float32)) == 3
+        other = B.mgi_graph_add_input(g, 2, 4, 4, 8)
+        assert err(B.mgi_graph_add_concat, g, [y, other]) == 2
+        assert err(B.mgi_graph_mark_output, g, x) == 3
+        B.mgi_graph_mark_output(g, y)
+        assert err(B.mgi_graph_mark_output, g, y) == 1
+        # null pointers straight through the C ABI
+        assert L.mgi_graph_add_input(g, 1, 1, 1, 1, 2, None) == 1
+        assert L.mgi_graph_add_conv2d(g, x, None, None, None, None) == 1
+        assert L.mgi_graph_finalize(None, None, None) == 1
+        assert "null" in B.mgi_last_error()
+    finally:
+        B.mgi_graph_destroy(g)
+    assert B.lib().mgi_graph_destroy(None) == 0
+    assert B.lib().mgi_plan_destroy(None) == 0
+
+
+def test_finalize_state_errors_and_run_before_bind():
+    g = B.mgi_graph_create()
+    try:
+        x = B.mgi_graph_add_input(g, 1, 4, 4, 8)
+        y = B.mgi_graph_add_activation(g, x, B.ACT_RELU)
+        assert err(B.mgi_graph_finalize, g) == 4          # no output marked
+        B.mgi_graph_mark_output(g, y)
+        o = B.mgi_options_default()
+        o.planner = 9
+        assert err(B.mgi_graph_finalize, g, o) == 3
+        p = B.mgi_graph_finalize(g)
+    finally:
+        B.mgi_graph_destroy(g)
+    try:
+        assert err(B.mgi_plan_run, p, [1], [1]) == 4        # not bound
+        assert err(B.mgi_plan_bind, p, 0, 0) == 5           # no buffers
+        assert err(B.mgi_plan_bind, p, 0x1001, 0x2000) == 5  # misaligned
+        assert err(B.mgi_plan_read_node, p, 0, 0x1000) == 4  # not materialized
+        assert err(B.mgi_plan_node_info, p, 99) == 1
+    finally:
+        B.mgi_plan_destroy(p)
+
+
+def test_fusion_structure():
+    v1 = engine.Plan(workloads.mobilenet_v1(1), bind=False)
+    kinds = [n["kind"] for n in v1.nodes()]
+    assert kinds[0] == "conv_stem" and kinds.count("dw_conv") == 13 and kinds.count("pw_gemm") == 13
+    assert kinds[-3:] == ["global_avgpool", "fc_gemm", "softmax"]
+    assert len(kinds) == 30
+    v2 = engine.Plan(workloads.mobilenet_v2(1), bind=False)
+    nodes = v2.nodes()
+    assert sum(1 for n in nodes if n["n_fused"] == 2) == 10      # residual adds absorbed
+    assert not any(n["kind"] == "add" for n in nodes)
+    v2u = engine.Plan(workloads.mobilenet_v2(1), fuse=False, bind=False)
+    assert sum(1 for n in v2u.nodes() if n["kind"] == "add") == 10
+    dl = engine.Plan(workloads.deeplab_v2_os16(1), bind=False)
+    assert dl.nodes()[-1]["kind"] == "resize_argmax"
+
+
+def test_standalone_activation_and_add_fusion():
+    g = workloads.NetBuilder(0)
+    x = g.input(1, 8, 8, 64, -1, 1)
+    c = g.conv(x, 16, 1, act=workloads.ACT_NONE)
+    a = g.activation(c, workloads.ACT_RELU6)
+    d = g.conv(a, 16, 1, act=workloads.ACT_NONE)
+    s = g.add(d, a, act=workloads.ACT_RELU)
+    g.mark_output(s)
+    p = engine.Plan(g.graph("t"), bind=False)
+    nodes = p.nodes()
+    assert [n["kind"] for n in nodes] == ["ingest", "pw_gemm", "pw_gemm", "export"]
+    assert [n["n_fused"] for n in nodes[1:3]] == [2, 2]
+    pu = engine.Plan(g.graph("t"), fuse=False, bind=False)
+    assert [n["kind"] for n in pu.nodes()] == ["ingest", "pw_gemm", "activation", "pw_gemm", "add",
+                                                "export"]
+
+
+@pytest.mark.parametrize("net,key", [("mobilenet_v1", "MobileNet"), ("mobilenet_v2", "MobileNetV2")])
+@pytest.mark.parametrize("fuse", [True, False])
+def test_library_memory_report_reproduces_table3(net, key, fuse):
+    t3 = {"MobileNet": (9.6, 2.3), "MobileNetV2": (13.2, 4.0)}[key]
+    d = workloads.WORKLOADS[net](1, logits_output=False)
+    naive, planned, nobj = engine.Plan(d, fuse=fuse, bind=False).memory_report()
+    ops, sizes, inter = oplan.graph_problem(d, oracle.tensor_shapes(d))
+    _, ref = oplan.greedy(ops, sizes, inter)
+    assert planned == oplan.total(ref)
+    assert round(planned / 2 ** 20, 1) == t3[1]
+    if not fuse:
+        assert round(naive / 2 ** 20, 1) == t3[0]
+    materialized = engine.Plan(d, fuse=fuse, materialize_all=True, bind=False).memory_report()
+    assert materialized[1] == materialized[0] == naive
+
+
+def to_lifetimes(ops, sizes, inter):
+    first, last = oplan.lifetimes(ops, inter)
+    consumed = {t for _, ins in ops for t in ins}
+    ts = sorted(t for t in inter if t in first)
+    return (ts, [sizes[t] for t in ts], [first[t] for t in ts],
+            [last[t] if t in consumed else -1 for t in ts])
+
+
+def test_library_planner_equals_oracle_on_random_dags():
+    rng = random.Random(77)
+    for _ in range(400):
+        n = rng.randint(3, 14)
+        ops = [([0], [])]
+        for i in range(1, n):
+            ops.append(([i], rng.sample(range(i), rng.randint(1, min(3, i)))))
+        sizes = {i: rng.choice([16, 32, 48, 64, 100, 128, 256]) for i in range(n)}
+        inter = set(range(1, n - 1))
+        ts, sz, fi, la = to_lifetimes(ops, sizes, inter)
+        obj, osz = B.mgi_planner_assign(B.PLANNER_GREEDY, sz, fi, la)
+        ref_assign, ref_obj = oplan.greedy(ops, sizes, inter)
+        assert osz == ref_obj
+        assert obj == [ref_assign[t] for t in ts]
+        nobj, nsz = B.mgi_planner_assign(B.PLANNER_NAIVE, sz, fi, la)
+        assert nobj == list(range(len(ts))) and nsz == sz
+
+
+def test_library_planner_fig5(golden_dir):
+    import json
+    with open(os.path.join(golden_dir, "fig5_planner_example.json")) as f:
+        gd = json.load(f)
+    ops = [(o[0], o[1]) for o in gd["graph"]["ops"]]
+    sizes = dict(enumerate(gd["graph"]["sizes"]))
+    ts, sz, fi, la = to_lifetimes(ops, sizes, set(sizes))
+    obj, osz = B.mgi_planner_assign(B.PLANNER_GREEDY, sz, fi, la)
+    assert sum(osz) == gd["greedy"]["total"]
+    for a, b in gd["greedy"]["reuse"]:
+        assert obj[ts.index(a)] == obj[ts.index(b)]
+
+
+def test_planner_assign_rejects_bad_lifetimes():
+    assert err(B.mgi_planner_assign, B.PLANNER_GREEDY, [4, 4], [0, 3], [2, 1]) == 1
+    assert err(B.mgi_planner_assign, 7, [4], [0], [1]) == 3
+    assert B.mgi_planner_assign(B.PLANNER_GREEDY, [], [], []) == ([], [])

@@ -310,3 +310,21 @@ def test_seeded_draws_are_fp16_values_and_he_scaled():
     assert abs(w.std() - math.sqrt(2 / 1024)) < 0.02 * math.sqrt(2 / 1024)
     g2 = workloads.mobilenet_v1(1)
     np.testing.assert_array_equal(g2["ops"][3]["w"], g["ops"][3]["w"])
+
+
+def test_store_fp16_rounds_stored_tensors_only():
+    g = workloads.NetBuilder(3)
+    x = g.input(1, 6, 6, 8, -1, 1)
+    c = g.conv(x, 16, 3, 1, act=workloads.ACT_NONE)
+    p = g.gap(c)
+    z = g.fc(p, 5)
+    g.mark_output(z)
+    d = g.graph("t")
+    exact = oracle.run_graph(d)
+    r16 = oracle.run_graph(d, store_fp16=True)
+    np.testing.assert_array_equal(r16[c], exact[c].astype(np.float16).astype(np.float64))
+    assert not np.array_equal(r16[c], exact[c])
+    pooled = r16[c].mean(axis=(1, 2), keepdims=True)
+    np.testing.assert_allclose(r16[p], pooled.astype(np.float16).astype(np.float64), rtol=0, atol=0)
+    # logits are kept in fp32 by the engine: not rounded, computed from the rounded pool
+    np.testing.assert_allclose(r16[z], oracle.fc(r16[p], d["ops"][z]["w"], d["ops"][z]["b"]), rtol=1e-15)
