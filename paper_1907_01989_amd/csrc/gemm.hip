@@ -17,6 +17,8 @@
 // Weight and activation tiles for four K slices (32 channels) per step are
 // staged through LDS, double-buffered with one barrier per step, the next
 // step's global loads issued before the current step's MFMAs.
+#include <cmath>
+
 #include "kernels.h"
 
 namespace mgi {
@@ -24,10 +26,13 @@ namespace kern {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 
+// Activation as one clamp (v_med3_f32): [lo, hi] = (-inf, inf) for none,
+// (0, inf) for ReLU, (0, 6) for ReLU6; act is uniform, so lo and hi are
+// computed once per kernel.
 __device__ __forceinline__ float act_apply(float v, int act) {
-    if (act == MGI_ACT_RELU) return fmaxf(v, 0.0f);
-    if (act == MGI_ACT_RELU6) return fminf(fmaxf(v, 0.0f), 6.0f);
-    return v;
+    const float lo = act == MGI_ACT_NONE ? -INFINITY : 0.0f;
+    const float hi = act == MGI_ACT_RELU6 ? 6.0f : INFINITY;
+    return __builtin_amdgcn_fmed3f(v, lo, hi);
 }
 
 __device__ __forceinline__ h8 zero_h8() {
@@ -225,6 +230,184 @@ hipError_t launch_gemm(const GemmParams &p, int bm, int bn, bool taps, bool f32o
     MGI_GEMM_CASE(128, 64)
     MGI_GEMM_CASE(128, 128)
 #undef MGI_GEMM_CASE
+    return hipErrorInvalidValue;
+}
+
+// ---------------------------------------------------------------------------
+// Coalesced epilogue.  An MFMA accumulator gives a lane 4 channels of one
+// pixel (half of a 16-byte sliced element, the other half in lane l+16);
+// storing that directly makes every quarter-wave write half-masked 64-byte
+// pieces, which costs several times the bandwidth of whole lines.  Instead
+// each wave parks act1(acc + bias) in its own LDS tile
+// [2*FN slices][16*FM pixels][8] fp32, then re-reads it so that consecutive
+// lanes own consecutive pixels of one slice: residual reads and output writes
+// are whole 16-byte elements, 1 KiB per wave instruction.  No barrier: a wave
+// reads back only what it wrote.
+// ---------------------------------------------------------------------------
+template <int FM, int FN>
+__device__ __forceinline__ void store_tile_c8(const GemmParams &p, const f4 (&acc)[FN][FM], int m0,
+                                              int nb0, float *stage, int lane) {
+    constexpr int NPIX = 16 * FM, NSL = 2 * FN;
+#pragma unroll
+    for (int i = 0; i < FN; ++i) {
+        const int nbase = (nb0 + i) * 16 + 4 * (lane >> 4);
+        float bv[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) bv[r] = p.bias[min(nbase, p.nb16 * 16 - 4) + r];
+        const int sl = 2 * i + ((lane >> 4) >> 1), half = 4 * ((lane >> 4) & 1);
+#pragma unroll
+        for (int j = 0; j < FM; ++j) {
+            f4 v;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) v[r] = act_apply(acc[i][j][r] + bv[r], p.act1);
+            *(f4 *)(stage + ((sl * NPIX) + j * 16 + (lane & 15)) * 8 + half) = v;
+        }
+    }
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int t = 0; t < (NSL * NPIX) / 64; ++t) {
+        const int e = lane + 64 * t;
+        const int sl = e / NPIX, px = e - sl * NPIX;
+        const int os = nb0 * 2 + sl, m = m0 + px;
+        if (os >= p.ns || m >= p.M) continue;
+        const f4 lo = *(const f4 *)(stage + e * 8), hi = *(const f4 *)(stage + e * 8 + 4);
+        float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        const size_t off = (size_t)os * p.M + m;
+        if (p.res) {
+            const h8 rv = p.res[off];
+#pragma unroll
+            for (int r = 0; r < 8; ++r) v[r] = act_apply(v[r] + (float)rv[r], p.act2);
+        }
+        h8 o;
+#pragma unroll
+        for (int r = 0; r < 8; ++r) o[r] = (_Float16)v[r];
+        ((h8 *)p.y)[off] = o;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Pointwise GEMM, weight-slab variant.  The tile's whole weight slab
+// (BN channels x all K, at most 64 KiB) is loaded into LDS once, behind one
+// barrier; each of the 4 waves then owns WM pixels and all BN channels, and
+// streams its activation fragments straight from the sliced layout into
+// registers, PF K-steps ahead of their use (a ring of PF register sets indexed
+// statically by unrolling the K loop by PF).  The K loop has no barrier and no
+// load other than the activation stream, so the in-order load counter lets
+// PF steps of loads stay in flight.
+// ---------------------------------------------------------------------------
+template <int WM, int BN, int PF>
+__global__ __launch_bounds__(256) void gemm_xs_kernel(GemmParams p) {
+    constexpr int FM = WM / 16, FN = BN / 16, BM = 4 * WM;
+    extern __shared__ h8 wsm[];                  // [FN][ksp][16]
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tile = xcd_tile(blockIdx.x, gridDim.x);
+    const int mt = tile / p.ntiles, nt = tile - mt * p.ntiles;
+    const int m0 = mt * BM + wave * WM, nb0 = nt * FN;
+    const int ksteps = p.ksp >> 2;
+
+    // Loads are branch-free (a load under a lane condition becomes an
+    // exec-masked branch followed by a wait): a row past the end reads the
+    // last row (its results are never stored); a K slice past the end (K not
+    // a multiple of 32) reads the last real slice, whose products meet the
+    // zero-padded weights of those K positions (exact for finite activations).
+    int xm[FM], xmc[FM];
+#pragma unroll
+    for (int j = 0; j < FM; ++j) {
+        xm[j] = m0 + j * 16 + (lane & 15);
+        xmc[j] = xm[j] < p.M ? xm[j] : p.M - 1;
+    }
+    const int xsl = lane >> 4;
+    h8 xq[PF][FM];
+    auto xload = [&](int kk, h8 *dst) {
+        const int ks = min(kk * 4 + xsl, p.ksl - 1);
+        const h8 *src = p.x + (size_t)ks * p.M;
+#pragma unroll
+        for (int j = 0; j < FM; ++j) dst[j] = src[xmc[j]];
+    };
+#pragma unroll
+    for (int u = 0; u < PF; ++u)
+        if (u < ksteps) xload(u, xq[u]);
+
+    // weight slab: FN blocks x ksp slices x 16 rows (blocks past the end are
+    // clamped; their accumulators are never stored)
+    const int slab = FN * p.ksp * 16;
+    for (int e = tid; e < slab; e += 256) {
+        const int f = e / (p.ksp * 16);
+        const int r = e - f * p.ksp * 16;
+        const int nb = min(nb0 + f, p.nb16 - 1);
+        wsm[e] = p.w[(size_t)nb * p.ksp * 16 + r];
+    }
+    __syncthreads();
+
+    f4 acc[FN][FM];
+#pragma unroll
+    for (int i = 0; i < FN; ++i)
+#pragma unroll
+        for (int j = 0; j < FM; ++j) acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+
+    auto step = [&](int kk, const h8 *b) {
+        h8 a[FN];
+#pragma unroll
+        for (int i = 0; i < FN; ++i) a[i] = wsm[(i * p.ksp + kk * 4) * 16 + lane];
+#pragma unroll
+        for (int i = 0; i < FN; ++i)
+#pragma unroll
+            for (int j = 0; j < FM; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[i], b[j], acc[i][j], 0, 0, 0);
+    };
+    // Main loop over whole groups of PF steps: every step issues exactly FM
+    // loads (the prefetch index is clamped instead of skipped), so the wait
+    // before each step's MFMAs can leave the newer PF-1 steps in flight.
+    int kk0 = 0;
+    for (; kk0 + PF <= ksteps; kk0 += PF) {
+#pragma unroll
+        for (int u = 0; u < PF; ++u) {
+            step(kk0 + u, xq[u]);
+            xload(min(kk0 + u + PF, ksteps - 1), xq[u]);
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < PF - 1; ++u)
+        if (kk0 + u < ksteps) step(kk0 + u, xq[u]);
+
+    // per-wave epilogue tile after the weight slab
+    float *stage = (float *)(wsm + FN * p.ksp * 16) + wave * (FN * FM * 256);
+    store_tile_c8<FM, FN>(p, acc, m0, nb0, stage, lane);
+}
+
+// LDS bytes of the weight slab for a bn-wide tile
+static size_t xs_stage_bytes(int wm, int bn) { return (size_t)4 * (wm / 16) * (bn / 16) * 256 * 4; }
+size_t gemm_xs_lds_bytes(int ksp, int wm, int bn) {
+    return (size_t)(bn / 16) * ksp * 256 + xs_stage_bytes(wm, bn);
+}
+
+template <int WM, int BN, int PF>
+static hipError_t launch_xs(const GemmParams &p, hipStream_t st) {
+    GemmParams q = p;
+    constexpr int BM = 4 * WM, FN = BN / 16;
+    q.mtiles = (p.M + BM - 1) / BM;
+    q.ntiles = (p.nb16 + FN - 1) / FN;
+    const size_t lds = gemm_xs_lds_bytes(p.ksp, WM, BN);
+    if (lds > 65536) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((gemm_xs_kernel<WM, BN, PF>), dim3(q.mtiles * q.ntiles), dim3(256), lds, st, q);
+    return hipGetLastError();
+}
+
+hipError_t launch_gemm_xs(const GemmParams &p, int wm, int bn, int pf, hipStream_t st) {
+    if (p.M <= 0) return hipSuccess;
+#define MGI_XS_CASE(WM_, BN_, PF_) \
+    if (wm == WM_ && bn == BN_ && pf == PF_) return launch_xs<WM_, BN_, PF_>(p, st);
+#define MGI_XS_PF(WM_, BN_) MGI_XS_CASE(WM_, BN_, 1) MGI_XS_CASE(WM_, BN_, 2) MGI_XS_CASE(WM_, BN_, 4)
+    MGI_XS_PF(16, 32)
+    MGI_XS_PF(16, 64)
+    MGI_XS_PF(16, 128)
+    MGI_XS_PF(32, 32)
+    MGI_XS_PF(32, 64)
+    MGI_XS_PF(32, 128)
+    MGI_XS_PF(64, 32)
+    MGI_XS_PF(64, 64)
+#undef MGI_XS_PF
+#undef MGI_XS_CASE
     return hipErrorInvalidValue;
 }
 

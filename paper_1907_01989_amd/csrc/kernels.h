@@ -29,6 +29,12 @@ struct GemmParams {
 };
 hipError_t launch_gemm(const GemmParams &p, int bm, int bn, bool taps, bool f32out,
                        hipStream_t st);
+// pointwise (1x1, stride 1) GEMM with fp16 sliced output: the tile's weight
+// slab in LDS, activations streamed to registers; tile (4 * wm) pixels x bn
+// channels, pf K steps of activation prefetch.  Needs
+// gemm_xs_lds_bytes(ksp, wm, bn) <= 64 KiB and zero weights for padded K.
+hipError_t launch_gemm_xs(const GemmParams &p, int wm, int bn, int pf, hipStream_t st);
+size_t gemm_xs_lds_bytes(int ksp, int wm, int bn);
 
 // Direct convolution of a small-channel NHWC graph input (kh*kw*c <= 32).
 struct StemParams {
@@ -45,8 +51,9 @@ hipError_t launch_stem(const StemParams &p, bool fp16_in, hipStream_t st);
 
 struct DwParams {
     const h8 *x;
-    const float *w;      // [S][kh*kw][8]
+    const h8 *w;         // fp16 taps [S][kh*kw][8]
     const float *bias;   // [S*8]
+    const h8 *zero;      // one zeroed 16-byte element (read for taps outside the input)
     h8 *y;
     int N, H, W, S, OH, OW, KH, KW, sh, sw, dh, dw, pt, pl, act;
 };

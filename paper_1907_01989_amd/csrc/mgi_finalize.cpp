@@ -254,6 +254,19 @@ mgi_status build_plan(const mgi_graph &g, const mgi_options &o, mgi_plan &p) {
                 }
                 nd.nb16 = (d.cout + 15) / 16;
                 nd.tile = pick_tile(out_shape.pixels(), d.cout);
+                if (nd.kind == NodeKind::Gemm && !nd.taps) {
+                    // weight-slab kernel: 128 x 32 tiles, two K steps of
+                    // prefetch when there are at least two; the slab (32
+                    // channels x all K) plus the epilogue tiles fit 64 KiB
+                    // up to K = 768
+                    const size_t slab = (size_t)2 * nd.ksp * 256 + 16384;
+                    if (slab <= 65536) {
+                        nd.tile.slab = true;
+                        nd.tile.wm = 32;
+                        nd.tile.bn = 32;
+                        nd.tile.pf = nd.ksp >= 8 ? 2 : 1;
+                    }
+                }
                 if (G.residual_tensor >= 0) {
                     int rb = need_c8(G.residual_tensor);
                     if (rb < 0) rb = c8_buf[G.residual_tensor];
@@ -481,6 +494,7 @@ mgi_status build_plan(const mgi_graph &g, const mgi_options &o, mgi_plan &p) {
         blob.resize(o2 + align256(bytes), 0);
         return o2;
     };
+    p.zero_off = reserve(256);  // zeroed block read by kernels for out-of-range taps
     for (Node &nd : p.nodes) {
         const GOp &op = g.ops[nd.op >= 0 ? nd.op : 0];
         if (nd.kind == NodeKind::Gemm || nd.kind == NodeKind::Stem || nd.kind == NodeKind::FC) {
@@ -516,14 +530,15 @@ mgi_status build_plan(const mgi_graph &g, const mgi_options &o, mgi_plan &p) {
             float *bp = reinterpret_cast<float *>(blob.data() + nd.b_off);
             for (int co = 0; co < cout; ++co) bp[co] = op.b[co];
         } else if (nd.kind == NodeKind::Depthwise) {
-            // fp32 taps per slice: [S][kh*kw][8], bias [S*8]; padded channels 0
+            // fp16 taps per slice: [S][kh*kw][8], bias fp32 [S*8]; padded channels 0
             const int c = op.out.c, S = slices(c), taps = op.conv.kh * op.conv.kw;
-            nd.w_bytes = (size_t)S * taps * 8 * 4;
+            nd.w_bytes = (size_t)S * taps * 8 * 2;
             nd.w_off = reserve(nd.w_bytes);
-            float *wp = reinterpret_cast<float *>(blob.data() + nd.w_off);
+            uint16_t *wp = reinterpret_cast<uint16_t *>(blob.data() + nd.w_off);
             for (int ch = 0; ch < c; ++ch)
                 for (int t = 0; t < taps; ++t)
-                    wp[((size_t)(ch / 8) * taps + t) * 8 + ch % 8] = op.w[(size_t)ch * taps + t];
+                    wp[((size_t)(ch / 8) * taps + t) * 8 + ch % 8] =
+                        f32_to_f16_bits(op.w[(size_t)ch * taps + t]);
             nd.b_bytes = (size_t)S * 8 * 4;
             nd.b_off = reserve(nd.b_bytes);
             float *bp = reinterpret_cast<float *>(blob.data() + nd.b_off);

@@ -76,8 +76,13 @@ enum class NodeKind {
 };
 
 // Tile shape of the MFMA GEMM (pointwise, implicit-GEMM convolution, FC).
+// slab = true selects the weight-slab pointwise kernel with (4 * wm) x bn
+// tiles and pf K steps of activation prefetch; otherwise the LDS-staged
+// kernel with bm x bn tiles.
 struct GemmTile {
     int bm = 64, bn = 64;
+    bool slab = false;
+    int wm = 32, pf = 1;
 };
 
 struct Node {
@@ -114,6 +119,7 @@ struct mgi_plan {
     std::vector<int> input_dtypes, output_dtypes;
     std::vector<uint8_t> weights;  // packed host copy (released after bind)
     size_t weight_bytes = 0;
+    size_t zero_off = 0;           // offset of a zeroed 256-byte block in the weight blob
     size_t workspace_bytes = 0;
     size_t mem_naive = 0, mem_planned = 0;
     int n_objects = 0;

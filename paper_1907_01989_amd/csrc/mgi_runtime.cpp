@@ -89,14 +89,16 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
             q.sh = nd.conv.stride_h; q.sw = nd.conv.stride_w;
             q.dh = nd.conv.dil_h; q.dw = nd.conv.dil_w;
             q.pt = nd.conv.pad_t; q.pl = nd.conv.pad_l;
+            if (nd.tile.slab) return launch_gemm_xs(q, nd.tile.wm, nd.tile.bn, nd.tile.pf, st);
             return launch_gemm(q, nd.tile.bm, nd.tile.bn, nd.taps, nd.kind == NodeKind::FC, st);
         }
         case NodeKind::Depthwise: {
             const Buf &ib = p.bufs[nd.in[0]];
             DwParams q{};
             q.x = (const h8 *)buf_ptr(p, nd.in[0], B);
-            q.w = (const float *)(wbase + nd.w_off);
+            q.w = (const h8 *)(wbase + nd.w_off);
             q.bias = (const float *)(wbase + nd.b_off);
+            q.zero = (const h8 *)(wbase + p.zero_off);
             q.y = (h8 *)y;
             q.N = ib.shape.n; q.H = ib.shape.h; q.W = ib.shape.w; q.S = slices(ib.shape.c);
             q.OH = os.h; q.OW = os.w; q.KH = nd.conv.kh; q.KW = nd.conv.kw;

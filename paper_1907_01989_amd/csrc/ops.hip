@@ -8,16 +8,21 @@
 // consecutive pixels of one 8-channel slice, so a wave's 16-byte loads cover
 // 1 KiB of contiguous memory.
 #include <cfloat>
+#include <cmath>
+#include <cstdint>
 
 #include "kernels.h"
 
 namespace mgi {
 namespace kern {
 
+// Activation as one clamp (v_med3_f32): [lo, hi] = (-inf, inf) for none,
+// (0, inf) for ReLU, (0, 6) for ReLU6; act is uniform, so lo and hi are
+// computed once per kernel.
 __device__ __forceinline__ float act_apply(float v, int act) {
-    if (act == MGI_ACT_RELU) return fmaxf(v, 0.0f);
-    if (act == MGI_ACT_RELU6) return fminf(fmaxf(v, 0.0f), 6.0f);
-    return v;
+    const float lo = act == MGI_ACT_NONE ? -INFINITY : 0.0f;
+    const float hi = act == MGI_ACT_RELU6 ? 6.0f : INFINITY;
+    return __builtin_amdgcn_fmed3f(v, lo, hi);
 }
 
 __device__ __forceinline__ h8 zero_h8() {
@@ -30,11 +35,108 @@ __device__ __forceinline__ h8 zero_h8() {
 static inline unsigned blocks_for(size_t n, int per) { return (unsigned)((n + per - 1) / per); }
 
 // ---------------------------------------------------------------------------
-// depthwise convolution: one thread per output pixel of one slice (8
-// channels), fp32 accumulation over the kh x kw window, bias + activation
-// epilogue.  The launch is 1-D: block b covers pixels [256*(b % tpp), +256) of
-// plane b / tpp, a plane being one (slice, image) pair.
+// Depthwise 3x3 convolution, column strips.  A thread owns one output column
+// of one 8-channel slice of one image and R consecutive output rows: it reads
+// the (R-1)*S + 2*D + 1 input rows of its three input columns once (16 bytes
+// each), and every input value feeds all the outputs whose window covers it,
+// accumulating in fp32 with fp16 taps (exact products).  Consecutive lanes
+// take consecutive columns, so each load instruction of a wave covers a
+// contiguous run of one row.  Taps outside the input read a zeroed 16-byte
+// element instead of branching, so all loads are issued unconditionally.
+// Launch: 1-D, thread g -> column g % OW, strip (g / OW) % nstrips, plane
+// g / (OW * nstrips) (plane = slice * N + image).
 // ---------------------------------------------------------------------------
+// v_fma_mix_f32: fp32 acc += fp16 a * fp16 b, both halves taken from the same
+// position (low or high) of a packed pair; the product of two fp16 values is
+// exact in fp32, so this equals fmaf((float)a, (float)b, acc) with no
+// conversion instructions.
+template <int HI>
+__device__ __forceinline__ void fma_mix(float &acc, uint32_t a, uint32_t b) {
+    if (HI)
+        asm volatile("v_fma_mix_f32 %0, %1, %2, %0 op_sel:[1,1,0] op_sel_hi:[1,1,0]"
+                     : "+v"(acc) : "v"(a), "v"(b));
+    else
+        asm volatile("v_fma_mix_f32 %0, %1, %2, %0 op_sel:[0,0,0] op_sel_hi:[1,1,0]"
+                     : "+v"(acc) : "v"(a), "v"(b));
+}
+
+typedef uint32_t u4x __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ u4x as_u4(h8 v) { return __builtin_bit_cast(u4x, v); }
+
+// acc[0..7] += w * v channel-wise, w and v fp16 x 8
+__device__ __forceinline__ void fma8(float *acc, u4x w, u4x v) {
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+        fma_mix<0>(acc[2 * d], w[d], v[d]);
+        fma_mix<1>(acc[2 * d + 1], w[d], v[d]);
+    }
+}
+
+template <int S_, int D_, int R>
+__global__ __launch_bounds__(256) void dw3_kernel(DwParams p, int nstrips) {
+    constexpr int NR = (R - 1) * S_ + 2 * D_ + 1;
+    const int g = blockIdx.x * 256 + threadIdx.x;
+    const int ox = g % p.OW;
+    const int rest = g / p.OW;
+    const int strip = rest % nstrips;
+    const int plane = rest / nstrips;
+    if (plane >= p.S * p.N) return;
+    const int s = plane / p.N;
+    const int oy0 = strip * R;
+    const h8 *xin = p.x + (size_t)plane * p.H * p.W;
+    const h8 *wp = p.w + (size_t)s * 9;
+    u4x w[9];
+#pragma unroll
+    for (int t = 0; t < 9; ++t) w[t] = as_u4(wp[t]);
+    const int iy0 = oy0 * S_ - p.pt, ix0 = ox * S_ - p.pl;
+    int cx[3];
+    bool cv[3];
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+        cx[k] = ix0 + k * D_;
+        cv[k] = cx[k] >= 0 && cx[k] < p.W;
+    }
+    u4x v[NR][3];
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+        const int iy = iy0 + r;
+        const bool rv = iy >= 0 && iy < p.H;
+#pragma unroll
+        for (int k = 0; k < 3; ++k)
+            v[r][k] = as_u4(*((rv && cv[k]) ? xin + (size_t)iy * p.W + cx[k] : p.zero));
+    }
+    float acc[R][8];
+#pragma unroll
+    for (int o = 0; o < R; ++o)
+#pragma unroll
+        for (int c = 0; c < 8; ++c) acc[o][c] = p.bias[s * 8 + c];
+#pragma unroll
+    for (int r = 0; r < NR; ++r)
+#pragma unroll
+        for (int ky = 0; ky < 3; ++ky) {
+            const int t = r - ky * D_;
+            if (t >= 0 && t % S_ == 0 && t / S_ < R) {
+#pragma unroll
+                for (int k = 0; k < 3; ++k) fma8(acc[t / S_], w[ky * 3 + k], v[r][k]);
+            }
+        }
+    // activation as one clamp: [lo, hi] = (-inf, inf), (0, inf) or (0, 6)
+    const float lo = p.act == MGI_ACT_NONE ? -INFINITY : 0.0f;
+    const float hi = p.act == MGI_ACT_RELU6 ? 6.0f : INFINITY;
+    h8 *yout = p.y + (size_t)plane * p.OH * p.OW + ox;
+#pragma unroll
+    for (int o = 0; o < R; ++o) {
+        if (oy0 + o >= p.OH) break;
+        h8 q;
+#pragma unroll
+        for (int c = 0; c < 8; ++c) q[c] = (_Float16)__builtin_amdgcn_fmed3f(acc[o][c], lo, hi);
+        yout[(size_t)(oy0 + o) * p.OW] = q;
+    }
+}
+
+// Any window size: one thread per output pixel of one slice, fp32
+// accumulation over the kh x kw window.
 __global__ __launch_bounds__(256) void dw_kernel(DwParams p, int tpp) {
     const int plane = blockIdx.x / tpp;
     const int pix = (blockIdx.x - plane * tpp) * 256 + threadIdx.x;
@@ -43,7 +145,7 @@ __global__ __launch_bounds__(256) void dw_kernel(DwParams p, int tpp) {
     const int s = plane / p.N;
     const int oy = pix / p.OW, ox = pix - oy * p.OW;
     const h8 *xin = p.x + (size_t)plane * p.H * p.W;
-    const float *wt = p.w + (size_t)s * p.KH * p.KW * 8;
+    const h8 *wt = p.w + (size_t)s * p.KH * p.KW;
     float acc[8];
 #pragma unroll
     for (int c = 0; c < 8; ++c) acc[c] = p.bias[s * 8 + c];
@@ -54,9 +156,9 @@ __global__ __launch_bounds__(256) void dw_kernel(DwParams p, int tpp) {
             const int ix = ox * p.sw + kx * p.dw - p.pl;
             if (ix < 0 || ix >= p.W) continue;
             const h8 v = xin[(size_t)iy * p.W + ix];
-            const float *wk = wt + (ky * p.KW + kx) * 8;
+            const h8 wk = wt[ky * p.KW + kx];
 #pragma unroll
-            for (int c = 0; c < 8; ++c) acc[c] = fmaf(wk[c], (float)v[c], acc[c]);
+            for (int c = 0; c < 8; ++c) acc[c] = fmaf((float)wk[c], (float)v[c], acc[c]);
         }
     }
     h8 o;
@@ -65,9 +167,25 @@ __global__ __launch_bounds__(256) void dw_kernel(DwParams p, int tpp) {
     p.y[(size_t)plane * ohw + pix] = o;
 }
 
+template <int S_, int D_, int R>
+static hipError_t launch_dw3(const DwParams &p, hipStream_t st) {
+    const int nstrips = (p.OH + R - 1) / R;
+    const size_t threads = (size_t)p.OW * nstrips * p.S * p.N;
+    if (threads > 0x7fffffffull) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((dw3_kernel<S_, D_, R>), dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, st,
+                       p, nstrips);
+    return hipGetLastError();
+}
+
 hipError_t launch_depthwise(const DwParams &p, hipStream_t st) {
     const int ohw = p.OH * p.OW;
     if (ohw <= 0 || p.N <= 0 || p.S <= 0) return hipSuccess;
+    if (p.KH == 3 && p.KW == 3 && p.sh == p.sw && p.dh == p.dw) {
+        if (p.sh == 1 && p.dh == 1) return launch_dw3<1, 1, 4>(p, st);
+        if (p.sh == 2 && p.dh == 1) return launch_dw3<2, 1, 2>(p, st);
+        if (p.sh == 1 && p.dh == 2) return launch_dw3<1, 2, 4>(p, st);
+        if (p.sh == 2 && p.dh == 2) return launch_dw3<2, 2, 2>(p, st);
+    }
     const int tpp = (ohw + 255) / 256;
     const size_t nblk = (size_t)tpp * p.S * p.N;
     if (nblk > 0x7fffffffu) return hipErrorInvalidValue;
