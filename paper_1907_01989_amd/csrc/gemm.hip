@@ -412,71 +412,165 @@ hipError_t launch_gemm_xs(const GemmParams &p, int wm, int bn, int pf, hipStream
 }
 
 // ---------------------------------------------------------------------------
-// Stem: a convolution that reads the NHWC graph input directly.  The whole
-// window (kh*kw*c <= 32 values) is one K step: lane l gathers im2col entries
-// k = 8*(l/16) .. +7 of pixel l%16, converted to fp16, as its B fragment.
-// Each wave covers 4 x 16 pixels and all output blocks (NB <= 4).
+// Fully-connected layer (1x1 spatial input, fp32 logits out).  M (images) is
+// small and K long, so a workgroup takes 16 output channels for up to 16*FM
+// images and splits K over its 4 waves; each wave loads B K-steps of weight
+// and activation fragments at once, straight from global memory, and the four
+// fp32 partial tiles are summed through LDS in a fixed wave order.
+// ---------------------------------------------------------------------------
+template <int FM, int B>
+__global__ __launch_bounds__(256) void fc_kernel(GemmParams p) {
+    __shared__ f4 red[4][FM][64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int nb = blockIdx.x % p.nb16, mt = blockIdx.x / p.nb16;
+    const int m0 = mt * 16 * FM;
+    const int ksteps = p.ksp >> 2;
+    const int per = (ksteps + 3) >> 2;
+    const int s0 = min(wave * per, ksteps), s1 = min(s0 + per, ksteps);
+    int xmc[FM];
+#pragma unroll
+    for (int j = 0; j < FM; ++j) xmc[j] = min(m0 + j * 16 + (lane & 15), p.M - 1);
+    const h8 *wrow = p.w + (size_t)nb * p.ksp * 16 + lane;
+    f4 acc[FM];
+#pragma unroll
+    for (int j = 0; j < FM; ++j) acc[j] = f4{0.f, 0.f, 0.f, 0.f};
+    for (int s = s0; s < s1; s += B) {
+        h8 xa[B][FM], wa[B];
+#pragma unroll
+        for (int b = 0; b < B; ++b) {
+            const int kk = min(s + b, s1 - 1);
+            const int ks = min(kk * 4 + (lane >> 4), p.ksl - 1);
+#pragma unroll
+            for (int j = 0; j < FM; ++j) xa[b][j] = p.x[(size_t)ks * p.M + xmc[j]];
+            wa[b] = wrow[(size_t)kk * 64];
+        }
+#pragma unroll
+        for (int b = 0; b < B; ++b)
+            if (s + b < s1) {
+#pragma unroll
+                for (int j = 0; j < FM; ++j)
+                    acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wa[b], xa[b][j], acc[j], 0, 0, 0);
+            }
+    }
+#pragma unroll
+    for (int j = 0; j < FM; ++j) red[wave][j][lane] = acc[j];
+    __syncthreads();
+    for (int j = wave; j < FM; j += 4) {
+        const f4 v = red[0][j][lane] + red[1][j][lane] + red[2][j][lane] + red[3][j][lane];
+        const int m = m0 + j * 16 + (lane & 15);
+        if (m >= p.M) continue;
+        const int nbase = nb * 16 + 4 * (lane >> 4);
+        float *y = (float *)p.y + (size_t)m * p.cout;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+            if (nbase + r < p.cout) y[nbase + r] = act_apply(v[r] + p.bias[nbase + r], p.act1);
+    }
+}
+
+hipError_t launch_fc(const GemmParams &p, hipStream_t st) {
+    if (p.M <= 0) return hipSuccess;
+    const int fm = p.M <= 16 ? 1 : (p.M <= 32 ? 2 : 4);
+    const int mtiles = (p.M + 16 * fm - 1) / (16 * fm);
+    const dim3 grid(mtiles * p.nb16), block(256);
+    if (fm == 1) hipLaunchKernelGGL((fc_kernel<1, 4>), grid, block, 0, st, p);
+    else if (fm == 2) hipLaunchKernelGGL((fc_kernel<2, 4>), grid, block, 0, st, p);
+    else hipLaunchKernelGGL((fc_kernel<4, 4>), grid, block, 0, st, p);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Stem: a convolution that reads the NHWC graph input directly (no layout
+// conversion of the input, Sec. 3.2), for windows with kh*kw*c <= 32 so the
+// whole window is one MFMA K step.  A workgroup owns one image and a band of
+// th output rows: it first stages the input rows of the band into LDS as
+// fp16 (coalesced loads of whole input rows; rows outside the image and the
+// padding columns are written as zeros), then each lane builds its B
+// fragment -- im2col entries k = 8*(l/16) .. +7 of pixel l%16 -- from LDS and
+// runs one MFMA per output block of 16 channels.  Entries k >= kh*kw*c read
+// any staged value: their weights are zero.
 // ---------------------------------------------------------------------------
 template <typename TIN, int NB>
-__global__ __launch_bounds__(256) void stem_kernel(StemParams p) {
-    constexpr int FM = 4;
+__global__ __launch_bounds__(256) void stem_kernel(StemParams p, int th, int rs, int nrows) {
+    extern __shared__ _Float16 band[];           // [nrows][rs] fp16
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int mbase = (blockIdx.x * 4 + wave) * (FM * 16);
+    const int bands = (p.OH + th - 1) / th;
+    const int n = blockIdx.x / bands, oy0 = (blockIdx.x - n * bands) * th;
+    const int iy0 = oy0 * p.sh - p.pt;
     const TIN *x = (const TIN *)p.x;
-
-    int dy[8], dx[8], ci[8];
-    bool kv[8];
+    const int rowlen = p.W * p.C;                // elements of one NHWC input row
+    const int lead = p.pl * p.C;                 // zero columns before the data
+    // zero the band, then copy the rows that exist (16-byte vectors when the
+    // input rows and their place in LDS are 16-byte aligned)
+    for (int e = tid * 8; e < nrows * rs; e += 256 * 8) {
+        if (e + 8 <= nrows * rs) *(h8 *)(band + e) = zero_h8();
+        else for (int q = e; q < nrows * rs; ++q) band[q] = (_Float16)0.0f;
+    }
+    __syncthreads();
+    constexpr int VEC = 16 / sizeof(TIN);        // elements per 16-byte load
+    const bool vec = (rowlen % 8) == 0 && (lead % 8) == 0 && (rs % 8) == 0;
+    for (int r = 0; r < nrows; ++r) {
+        const int iy = iy0 + r;
+        if (iy < 0 || iy >= p.H) continue;       // uniform: the band row stays zero
+        const TIN *src = x + ((size_t)n * p.H + iy) * rowlen;
+        _Float16 *dst = band + r * rs + lead;
+        if (vec) {
+            for (int c = tid * VEC; c < rowlen; c += 256 * VEC) {
+                if (VEC == 8) {
+                    *(h8 *)(dst + c) = *(const h8 *)(src + c);
+                } else {
+                    const float4 f = *(const float4 *)(src + c);
+                    h4 hv;
+                    hv[0] = (_Float16)f.x; hv[1] = (_Float16)f.y; hv[2] = (_Float16)f.z; hv[3] = (_Float16)f.w;
+                    *(h4 *)(dst + c) = hv;
+                }
+            }
+        } else {
+            for (int c = tid; c < rowlen; c += 256) dst[c] = (_Float16)(float)src[c];
+        }
+    }
+    // per-lane offsets of its 8 im2col entries inside a window
+    int koff[8];
 #pragma unroll
     for (int t = 0; t < 8; ++t) {
         const int k = 8 * (lane >> 4) + t;
-        kv[t] = k < p.K;
-        const int kk = kv[t] ? k : 0;
-        const int tap = kk / p.C;
-        ci[t] = kk - tap * p.C;
-        const int ky = tap / p.KW, kx = tap - ky * p.KW;
-        dy[t] = ky * p.dh - p.pt;
-        dx[t] = kx * p.dw - p.pl;
+        int off = 0;
+        if (k < p.K) {
+            const int tap = k / p.C, ci = k - tap * p.C;
+            const int ky = tap / p.KW, kx = tap - ky * p.KW;
+            off = ky * p.dh * rs + kx * p.dw * p.C + ci;
+        }
+        koff[t] = off;
     }
     h8 a[NB];
 #pragma unroll
     for (int i = 0; i < NB; ++i) a[i] = p.w[(size_t)i * 64 + lane];
-    const int hw = p.OH * p.OW;
-    f4 acc[NB][FM];
+    float bv[NB][4];
 #pragma unroll
-    for (int j = 0; j < FM; ++j) {
-        const int m = mbase + j * 16 + (lane & 15);
-        h8 b = zero_h8();
-        if (m < p.M) {
-            const int n = m / hw, r = m - n * hw;
-            const int oy = r / p.OW, ox = r - oy * p.OW;
-            const int iy0 = oy * p.sh, ix0 = ox * p.sw;
+    for (int i = 0; i < NB; ++i)
 #pragma unroll
-            for (int t = 0; t < 8; ++t) {
-                const int iy = iy0 + dy[t], ix = ix0 + dx[t];
-                if (kv[t] && iy >= 0 && iy < p.H && ix >= 0 && ix < p.W)
-                    b[t] = (_Float16)(float)x[(((size_t)n * p.H + iy) * p.W + ix) * p.C + ci[t]];
-            }
-        }
+        for (int r = 0; r < 4; ++r) bv[i][r] = p.bias[i * 16 + 4 * (lane >> 4) + r];
+    __syncthreads();
+
+    const int fpr = (p.OW + 15) >> 4;            // 16-pixel fragments per output row
+    const int nfr = min(th, p.OH - oy0) * fpr;
+    for (int f = wave; f < nfr; f += 4) {
+        const int oyl = f / fpr;
+        const int ox = (f - oyl * fpr) * 16 + (lane & 15);
+        const int base = oyl * p.sh * rs + min(ox, p.OW - 1) * p.sw * p.C;
+        h8 b;
 #pragma unroll
-        for (int i = 0; i < NB; ++i)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[i], b, f4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
-    }
+        for (int t = 0; t < 8; ++t) b[t] = band[base + koff[t]];
+        const int m = (n * p.OH + oy0 + oyl) * p.OW + ox;
 #pragma unroll
-    for (int i = 0; i < NB; ++i) {
-        const int nbase = i * 16 + 4 * (lane >> 4);
-        const int os = nbase >> 3, hoff = nbase & 7;
-        if (os >= p.ns) continue;
-        float bv[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) bv[r] = p.bias[nbase + r];
-#pragma unroll
-        for (int j = 0; j < FM; ++j) {
-            const int m = mbase + j * 16 + (lane & 15);
-            if (m >= p.M) continue;
+        for (int i = 0; i < NB; ++i) {
+            const f4 acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[i], b, f4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+            const int nbase = i * 16 + 4 * (lane >> 4);
+            const int os = nbase >> 3, hoff = nbase & 7;
+            if (ox >= p.OW || os >= p.ns) continue;
             const size_t off = ((size_t)os * p.M + m) * 8 + hoff;
             float v[4];
 #pragma unroll
-            for (int r = 0; r < 4; ++r) v[r] = act_apply(acc[i][j][r] + bv[r], p.act1);
+            for (int r = 0; r < 4; ++r) v[r] = act_apply(acc[r] + bv[i][r], p.act1);
             if (p.res) {
                 const h4 rv = *(const h4 *)((const _Float16 *)p.res + off);
 #pragma unroll
@@ -490,14 +584,36 @@ __global__ __launch_bounds__(256) void stem_kernel(StemParams p) {
     }
 }
 
+static int stem_row_stride(int c, int w, int ow, int sw, int kw, int dw, int pl) {
+    int rs = ((ow - 1) * sw + (kw - 1) * dw + 1) * c;
+    rs = rs > (w + pl) * c ? rs : (w + pl) * c;
+    return (rs + 7) & ~7;
+}
+
+size_t stem_band_bytes(int th, int kh, int kw, int c, int w, int ow, int sh, int sw, int dh, int dw,
+                       int pl) {
+    const int nrows = (th - 1) * sh + (kh - 1) * dh + 1;
+    return (size_t)nrows * stem_row_stride(c, w, ow, sw, kw, dw, pl) * 2;
+}
+
 template <typename TIN>
 static hipError_t launch_stem_t(const StemParams &p, hipStream_t st) {
-    const dim3 grid((p.M + 255) / 256), block(256);
+    // band of th output rows: enough workgroups to fill the chip when possible
+    // and a band that fits 64 KiB of LDS
+    int th = 4;
+    while (th > 1 && (size_t)p.N * ((p.OH + th - 1) / th) < 1024) th >>= 1;
+    while (th > 1 && stem_band_bytes(th, p.KH, p.KW, p.C, p.W, p.OW, p.sh, p.sw, p.dh, p.dw, p.pl) > 65536)
+        th >>= 1;
+    const int nrows = (th - 1) * p.sh + (p.KH - 1) * p.dh + 1;
+    const int rs = stem_row_stride(p.C, p.W, p.OW, p.sw, p.KW, p.dw, p.pl);
+    const size_t lds = (size_t)nrows * rs * 2;
+    if (lds > 65536) return hipErrorInvalidValue;
+    const dim3 grid(p.N * ((p.OH + th - 1) / th)), block(256);
     switch (p.nb16) {
-        case 1: hipLaunchKernelGGL((stem_kernel<TIN, 1>), grid, block, 0, st, p); break;
-        case 2: hipLaunchKernelGGL((stem_kernel<TIN, 2>), grid, block, 0, st, p); break;
-        case 3: hipLaunchKernelGGL((stem_kernel<TIN, 3>), grid, block, 0, st, p); break;
-        case 4: hipLaunchKernelGGL((stem_kernel<TIN, 4>), grid, block, 0, st, p); break;
+        case 1: hipLaunchKernelGGL((stem_kernel<TIN, 1>), grid, block, lds, st, p, th, rs, nrows); break;
+        case 2: hipLaunchKernelGGL((stem_kernel<TIN, 2>), grid, block, lds, st, p, th, rs, nrows); break;
+        case 3: hipLaunchKernelGGL((stem_kernel<TIN, 3>), grid, block, lds, st, p, th, rs, nrows); break;
+        case 4: hipLaunchKernelGGL((stem_kernel<TIN, 4>), grid, block, lds, st, p, th, rs, nrows); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

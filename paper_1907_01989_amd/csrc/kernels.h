@@ -34,6 +34,8 @@ hipError_t launch_gemm(const GemmParams &p, int bm, int bn, bool taps, bool f32o
 // channels, pf K steps of activation prefetch.  Needs
 // gemm_xs_lds_bytes(ksp, wm, bn) <= 64 KiB and zero weights for padded K.
 hipError_t launch_gemm_xs(const GemmParams &p, int wm, int bn, int pf, hipStream_t st);
+// fully-connected layer, fp32 (M x cout) output; K split over the waves
+hipError_t launch_fc(const GemmParams &p, hipStream_t st);
 size_t gemm_xs_lds_bytes(int ksp, int wm, int bn);
 
 // Direct convolution of a small-channel NHWC graph input (kh*kw*c <= 32).
@@ -44,10 +46,13 @@ struct StemParams {
     const h8 *res;
     h8 *y;
     int N, H, W, C, OH, OW, M;
-    int KW, K, sh, sw, dh, dw, pt, pl;
+    int KH, KW, K, sh, sw, dh, dw, pt, pl;
     int nb16, ns, act1, act2;
 };
 hipError_t launch_stem(const StemParams &p, bool fp16_in, hipStream_t st);
+// LDS bytes the stem kernel stages for a band of th output rows
+size_t stem_band_bytes(int th, int kh, int kw, int c, int w, int ow, int sh, int sw, int dh, int dw,
+                       int pl);
 
 struct DwParams {
     const h8 *x;
@@ -61,7 +66,7 @@ hipError_t launch_depthwise(const DwParams &p, hipStream_t st);
 
 hipError_t launch_add(const h8 *a, const h8 *b, h8 *y, size_t count, int act, hipStream_t st);
 hipError_t launch_act(const h8 *x, h8 *y, size_t count, int act, hipStream_t st);
-hipError_t launch_gap(const h8 *x, h8 *y, int N, int HW, int S, hipStream_t st);
+hipError_t launch_gap(const h8 *x, h8 *y, const h8 *zero, int N, int HW, int S, hipStream_t st);
 hipError_t launch_softmax(const float *z, float *y, int rows, int cols, hipStream_t st);
 
 struct ConcatParams {

@@ -62,7 +62,7 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
             q.y = (h8 *)y;
             q.N = ib.shape.n; q.H = ib.shape.h; q.W = ib.shape.w; q.C = ib.shape.c;
             q.OH = os.h; q.OW = os.w; q.M = (int)os.pixels();
-            q.KW = nd.conv.kw; q.K = nd.conv.kh * nd.conv.kw * ib.shape.c;
+            q.KH = nd.conv.kh; q.KW = nd.conv.kw; q.K = nd.conv.kh * nd.conv.kw * ib.shape.c;
             q.sh = nd.conv.stride_h; q.sw = nd.conv.stride_w;
             q.dh = nd.conv.dil_h; q.dw = nd.conv.dil_w;
             q.pt = nd.conv.pad_t; q.pl = nd.conv.pad_l;
@@ -89,6 +89,7 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
             q.sh = nd.conv.stride_h; q.sw = nd.conv.stride_w;
             q.dh = nd.conv.dil_h; q.dw = nd.conv.dil_w;
             q.pt = nd.conv.pad_t; q.pl = nd.conv.pad_l;
+            if (nd.kind == NodeKind::FC) return launch_fc(q, st);
             if (nd.tile.slab) return launch_gemm_xs(q, nd.tile.wm, nd.tile.bn, nd.tile.pf, st);
             return launch_gemm(q, nd.tile.bm, nd.tile.bn, nd.taps, nd.kind == NodeKind::FC, st);
         }
@@ -116,7 +117,8 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
                               (size_t)slices(os.c) * os.pixels(), nd.act1, st);
         case NodeKind::Gap: {
             const Buf &ib = p.bufs[nd.in[0]];
-            return launch_gap((const h8 *)buf_ptr(p, nd.in[0], B), (h8 *)y, ib.shape.n,
+            return launch_gap((const h8 *)buf_ptr(p, nd.in[0], B), (h8 *)y,
+                              (const h8 *)(wbase + p.zero_off), ib.shape.n,
                               ib.shape.h * ib.shape.w, slices(ib.shape.c), st);
         }
         case NodeKind::Softmax:

@@ -259,53 +259,110 @@ __global__ __launch_bounds__(256) void gap_kernel(const h8 *x, h8 *y, int N, int
     }
 }
 
-hipError_t launch_gap(const h8 *x, h8 *y, int N, int HW, int S, hipStream_t st) {
-    const size_t waves = (size_t)S * N;
-    if (!waves) return hipSuccess;
-    hipLaunchKernelGGL(gap_kernel, dim3(blocks_for(waves, 4)), dim3(256), 0, st, x, y, N, HW, S);
+// Small planes (up to 64 pixels): 8 lanes per (slice, image); lane j sums
+// pixels j, j+8, ... with all loads issued at once (pixels past the end read
+// the zero element instead of branching), then a 3-step butterfly inside the
+// 8-lane group.  Fixed order, so deterministic.
+__global__ __launch_bounds__(256) void gap_small_kernel(const h8 *x, h8 *y, const h8 *zero,
+                                                        int planes, int HW) {
+    const int t = blockIdx.x * 256 + threadIdx.x;
+    const int idx = t >> 3, j = t & 7;
+    const bool live = idx < planes;
+    const h8 *xin = x + (size_t)(live ? idx : 0) * HW;
+    h8 v[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const int px = j + 8 * i;
+        v[i] = *((live && px < HW) ? xin + px : zero);
+    }
+    float acc[8];
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+        float a = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) a += (float)v[i][c];
+        acc[c] = a;
+    }
+#pragma unroll
+    for (int off = 4; off >= 1; off >>= 1)
+#pragma unroll
+        for (int c = 0; c < 8; ++c) acc[c] += __shfl_xor(acc[c], off, 8);
+    if (live && j == 0) {
+        const float inv = 1.0f / (float)HW;
+        h8 o;
+#pragma unroll
+        for (int c = 0; c < 8; ++c) o[c] = (_Float16)(acc[c] * inv);
+        y[idx] = o;
+    }
+}
+
+hipError_t launch_gap(const h8 *x, h8 *y, const h8 *zero, int N, int HW, int S, hipStream_t st) {
+    const size_t planes = (size_t)S * N;
+    if (!planes) return hipSuccess;
+    if (HW <= 64) {
+        hipLaunchKernelGGL(gap_small_kernel, dim3(blocks_for(planes * 8, 256)), dim3(256), 0, st, x, y,
+                           zero, (int)planes, HW);
+    } else {
+        hipLaunchKernelGGL(gap_kernel, dim3(blocks_for(planes, 4)), dim3(256), 0, st, x, y, N, HW, S);
+    }
     return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
-// softmax over rows of an fp32 (rows x cols) array; one workgroup per row.
+// softmax over rows of an fp32 (rows x cols) array; one wave per row.  The
+// row is held in registers (up to 16 values per lane, all loads issued at
+// once; columns past the end repeat the last column, which leaves the max
+// unchanged and is masked out of the sum); max and sum use a fixed butterfly.
+// Longer rows take a looped path.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ float block_reduce(float v, bool is_max, float *red) {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-        const float o = __shfl_xor(v, off, 64);
-        v = is_max ? fmaxf(v, o) : v + o;
-    }
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    __syncthreads();
-    if (lane == 0) red[wave] = v;
-    __syncthreads();
-    float r = red[0];
-#pragma unroll
-    for (int w = 1; w < 4; ++w) r = is_max ? fmaxf(r, red[w]) : r + red[w];
-    return r;
-}
-
-__global__ __launch_bounds__(256) void softmax_kernel(const float *z, float *y, int cols) {
-    __shared__ float red[4];
-    const float *zr = z + (size_t)blockIdx.x * cols;
-    float *yr = y + (size_t)blockIdx.x * cols;
+__global__ __launch_bounds__(256) void softmax_kernel(const float *z, float *y, int rows, int cols) {
+    constexpr int PER = 16;
+    const int lane = threadIdx.x & 63;
+    const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= rows) return;  // whole wave
+    const float *zr = z + (size_t)row * cols;
+    float *yr = y + (size_t)row * cols;
     float m = -FLT_MAX;
-    for (int j = threadIdx.x; j < cols; j += 256) m = fmaxf(m, zr[j]);
-    m = block_reduce(m, true, red);
+    if (cols <= 64 * PER) {
+        float v[PER];
+#pragma unroll
+        for (int i = 0; i < PER; ++i) v[i] = zr[min(lane + 64 * i, cols - 1)];
+#pragma unroll
+        for (int i = 0; i < PER; ++i) m = fmaxf(m, v[i]);
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, 64));
+        float s = 0.0f;
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            v[i] = expf(v[i] - m);
+            s += lane + 64 * i < cols ? v[i] : 0.0f;
+        }
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
+        const float inv = 1.0f / s;
+#pragma unroll
+        for (int i = 0; i < PER; ++i)
+            if (lane + 64 * i < cols) yr[lane + 64 * i] = v[i] * inv;
+        return;
+    }
+    for (int j = lane; j < cols; j += 64) m = fmaxf(m, zr[j]);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, 64));
     float s = 0.0f;
-    for (int j = threadIdx.x; j < cols; j += 256) {
+    for (int j = lane; j < cols; j += 64) {
         const float e = expf(zr[j] - m);
         yr[j] = e;
         s += e;
     }
-    s = block_reduce(s, false, red);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
     const float inv = 1.0f / s;
-    for (int j = threadIdx.x; j < cols; j += 256) yr[j] *= inv;
+    for (int j = lane; j < cols; j += 64) yr[j] *= inv;
 }
 
 hipError_t launch_softmax(const float *z, float *y, int rows, int cols, hipStream_t st) {
     if (rows <= 0 || cols <= 0) return hipSuccess;
-    hipLaunchKernelGGL(softmax_kernel, dim3(rows), dim3(256), 0, st, z, y, cols);
+    hipLaunchKernelGGL(softmax_kernel, dim3(blocks_for(rows, 4)), dim3(256), 0, st, z, y, rows, cols);
     return hipGetLastError();
 }
 

@@ -94,9 +94,7 @@ STEM_CASES = [
 @pytest.mark.parametrize("n,h,w,c,cout,k,s,fp16", STEM_CASES)
 def test_stem(n, h, w, c, cout, k, s, fp16):
     g = NetBuilder(seed=7)
-    x = g.input(n, h, w, c, 0, 1)
-    if fp16:
-        g.ops[x]["dtype"] = 0
+    x = g.input(n, h, w, c, 0, 1, dtype=workloads.DTYPE_FP16 if fp16 else workloads.DTYPE_FP32)
     y = g.conv(x, cout, k, s, act=ACT_RELU6)
     g.mark_output(y)
     outs, nodes, ref = run_case(f"stem_{n}x{h}x{w}x{c}->{cout}_k{k}s{s}_f16{int(fp16)}", g, y)

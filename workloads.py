@@ -24,6 +24,7 @@ from __future__ import annotations
 import numpy as np
 
 ACT_NONE, ACT_RELU, ACT_RELU6 = 0, 1, 2
+DTYPE_FP16, DTYPE_FP32 = 0, 2     # element types of graph inputs
 
 
 # ----------------------------------------------------------------------------
@@ -87,9 +88,12 @@ class NetBuilder:
     def hwc(self, t):
         return self._hwc[t]
 
-    def input(self, n, h, w, c, lo, hi, name="input"):
+    def input(self, n, h, w, c, lo, hi, name="input", dtype=DTYPE_FP16):
+        """A graph input of fp16-representable values, handed to the engine
+        as fp16 (``dtype`` 0) or fp32 (2) NHWC."""
         x = make_input((n, h, w, c), lo, hi, self.seed)
-        return self._push({"op": "input", "name": name, "shape": (n, h, w, c), "data": x}, (h, w, c))
+        return self._push({"op": "input", "name": name, "shape": (n, h, w, c), "data": x,
+                           "dtype": dtype}, (h, w, c))
 
     def conv(self, x, cout, k=1, s=1, d=1, act=ACT_RELU6, name=None, pads=None):
         h, w, cin = self._hwc[x]
