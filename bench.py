@@ -150,6 +150,34 @@ def node_work(desc, nodes, shapes, i):
     return flops, float(byts), bound
 
 
+def kernel_sources_hash():
+    """Hash of the kernel sources; a counter-based traffic figure is used only
+    while the kernels it was measured on are unchanged."""
+    import hashlib
+    h = hashlib.sha1()
+    for f in ("gemm.hip", "ops.hip", "kernels.h"):
+        with open(os.path.join(ROOT, "paper_1907_01989_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel, layer):
+    """HBM bytes per launch of (kernel, layer) from the committed rocprofv3
+    FETCH_SIZE / WRITE_SIZE summary, scaled by the copy calibration there;
+    None when absent or measured on other kernel sources."""
+    path = os.path.join(ROOT, "profiles", "mobilenet_v1_224_b64_traffic.md")
+    if not os.path.exists(path):
+        return None
+    cur = kernel_sources_hash()
+    with open(path) as f:
+        for line in f:
+            if line.startswith("traffic_bytes_per_launch:"):
+                _, k, l, nbytes, _, h = line.split()
+                if k == kernel and l == layer and h == cur:
+                    return int(nbytes)
+    return None
+
+
 def roofline_entry(flops, byts, bound, seconds):
     if bound == "mfma":
         ach = flops / seconds / 1e12
@@ -182,32 +210,35 @@ def run_workload(key, steps, warmup, hip, profile_steps=20, detail=True):
         B.mgi_plan_run(plan.handle, ins, ops_ptrs, sh)
     torch.cuda.synchronize()
 
-    # per-layer pass (outside the timed region): events around every node
+    # per-layer pass (outside the timed region): every node's kernel
+    # timestamped at its start and end on the device
     per_node = [0.0] * nn
     if detail:
-        evs = [[hip.event() for _ in range(nn + 1)] for _ in range(profile_steps)]
+        evs = [([hip.event() for _ in range(nn)], [hip.event() for _ in range(nn)])
+               for _ in range(profile_steps)]
         for k in range(profile_steps):
-            B.mgi_plan_run_timed(plan.handle, ins, ops_ptrs, evs[k], sh)
+            B.mgi_plan_run_timed(plan.handle, ins, ops_ptrs, evs[k][0], evs[k][1], sh)
         torch.cuda.synchronize()
         for k in range(profile_steps):
             for i in range(nn):
-                per_node[i] += hip.elapsed_ms(evs[k][i], evs[k][i + 1]) / profile_steps
-        for row in evs:
-            for e in row:
+                per_node[i] += hip.elapsed_ms(evs[k][0][i], evs[k][1][i]) / profile_steps
+        for a, b in evs:
+            for e in a + b:
                 hip.destroy(e)
     dom = max(range(nn), key=lambda i: per_node[i])
 
-    # timed region: K steps; the dominant node is bracketed by HIP events
+    # timed region: K steps; the dominant node's kernel is timestamped at its
+    # start and end in every step
     dev = [(hip.event(), hip.event()) for _ in range(steps)]
     arrays = []
     for a, b in dev:
-        ev = [None] * (nn + 1)
-        ev[dom], ev[dom + 1] = a, b
-        arrays.append(ev)
+        e0, e1 = [None] * nn, [None] * nn
+        e0[dom], e1[dom] = a, b
+        arrays.append((e0, e1))
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(steps):
-        B.mgi_plan_run_timed(plan.handle, ins, ops_ptrs, arrays[k], sh)
+        B.mgi_plan_run_timed(plan.handle, ins, ops_ptrs, arrays[k][0], arrays[k][1], sh)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     dom_ms = sum(hip.elapsed_ms(a, b) for a, b in dev) / steps
@@ -230,7 +261,8 @@ def run_workload(key, steps, warmup, hip, profile_steps=20, detail=True):
     roof.update({"kernel": nodes[dom]["kind"],
                  "layer": desc["ops"][nodes[dom]["tensor"]]["name"],
                  "algorithmic_bytes": int(by), "algorithmic_flops": int(fl),
-                 "avg_launch_us": round(dom_ms * 1e3, 3), "traffic": None})
+                 "avg_launch_us": round(dom_ms * 1e3, 3),
+                 "traffic": measured_traffic(nodes[dom]["kind"], desc["ops"][nodes[dom]["tensor"]]["name"])})
     total_s = t1 - t0
     res = {"desc": desc, "batch": batch, "net": net, "ms_per_step": total_s / steps * 1e3,
            "images_per_s": batch * steps / total_s, "roofline": roof, "layers": layers,
@@ -268,6 +300,9 @@ def main():
     ap.add_argument("--workload", default="v1_b64", choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true")
+    ap.add_argument("--copy-only", type=int, default=0, metavar="MIB",
+                    help="only run a plain device-to-device copy of MIB MiB, 20 times (the "
+                         "reference kernel for scaling HBM traffic counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this engine runs on one GPU; --gpus {args.gpus} is not supported "
@@ -280,6 +315,15 @@ def main():
         eprint("bench.py: no GPU visible")
         sys.exit(1)
     torch.cuda.set_device(0)
+    if args.copy_only:
+        n = args.copy_only * 1024 * 1024
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(20):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": n, "launches": 20}), flush=True)
+        return
     hip = Hip()
     eprint(f"[bench] workload {args.workload}: warmup {args.warmup}, steps {args.steps}")
     main_res = run_workload(args.workload, args.steps, args.warmup, hip)

@@ -210,14 +210,15 @@ mgi_status mgi_plan_bind(mgi_plan *p, void *dev_workspace, void *dev_weights, vo
 mgi_status mgi_plan_run(mgi_plan *p, const void *const *dev_inputs, void *const *dev_outputs,
                         void *stream);
 
-/* As mgi_plan_run, and records timing markers on the same stream: events[i]
- * (a hipEvent_t, or NULL to skip) just before node i is launched, for
- * 0 <= i < node count, and events[node count] after the last node.  The array
- * holds node count + 1 entries and is read during the call only.  The
- * elapsed time between events[i] and events[i + 1] is node i's duration on the
- * device (the paper's per-program timing of Sec. 6, taken without host sync). */
+/* As mgi_plan_run, and timestamps node kernels: node i's kernel is launched
+ * so that start_events[i] is recorded when it begins executing on the device
+ * and stop_events[i] when it ends (hipEvent_t values; NULL entries are not
+ * recorded).  Both arrays hold node-count entries and are read during the
+ * call only.  hipEventElapsedTime(start_events[i], stop_events[i]) is then
+ * node i's kernel duration, with no host synchronisation in the run (the
+ * paper's per-program timing of Sec. 6). */
 mgi_status mgi_plan_run_timed(mgi_plan *p, const void *const *dev_inputs, void *const *dev_outputs,
-                              void *stream, void *const *events);
+                              void *stream, void *const *start_events, void *const *stop_events);
 
 /* ---------------------------------------------------------------------------
  * introspection, used for layer-by-layer checks

@@ -206,11 +206,11 @@ static hipError_t launch_bm_bn(const GemmParams &p, bool taps, bool f32out, hipS
     const dim3 grid(q.mtiles * q.ntiles), block(256);
     if (f32out) {
         if (taps) return hipErrorInvalidValue;
-        hipLaunchKernelGGL((gemm_kernel<BM, BN, false, true>), grid, block, 0, st, q);
+        launch((gemm_kernel<BM, BN, false, true>), grid, block, 0, st, q);
     } else if (taps) {
-        hipLaunchKernelGGL((gemm_kernel<BM, BN, true, false>), grid, block, 0, st, q);
+        launch((gemm_kernel<BM, BN, true, false>), grid, block, 0, st, q);
     } else {
-        hipLaunchKernelGGL((gemm_kernel<BM, BN, false, false>), grid, block, 0, st, q);
+        launch((gemm_kernel<BM, BN, false, false>), grid, block, 0, st, q);
     }
     return hipGetLastError();
 }
@@ -389,7 +389,7 @@ static hipError_t launch_xs(const GemmParams &p, hipStream_t st) {
     q.ntiles = (p.nb16 + FN - 1) / FN;
     const size_t lds = gemm_xs_lds_bytes(p.ksp, WM, BN);
     if (lds > 65536) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((gemm_xs_kernel<WM, BN, PF>), dim3(q.mtiles * q.ntiles), dim3(256), lds, st, q);
+    launch((gemm_xs_kernel<WM, BN, PF>), dim3(q.mtiles * q.ntiles), dim3(256), lds, st, q);
     return hipGetLastError();
 }
 
@@ -472,9 +472,9 @@ hipError_t launch_fc(const GemmParams &p, hipStream_t st) {
     const int fm = p.M <= 16 ? 1 : (p.M <= 32 ? 2 : 4);
     const int mtiles = (p.M + 16 * fm - 1) / (16 * fm);
     const dim3 grid(mtiles * p.nb16), block(256);
-    if (fm == 1) hipLaunchKernelGGL((fc_kernel<1, 4>), grid, block, 0, st, p);
-    else if (fm == 2) hipLaunchKernelGGL((fc_kernel<2, 4>), grid, block, 0, st, p);
-    else hipLaunchKernelGGL((fc_kernel<4, 4>), grid, block, 0, st, p);
+    if (fm == 1) launch((fc_kernel<1, 4>), grid, block, 0, st, p);
+    else if (fm == 2) launch((fc_kernel<2, 4>), grid, block, 0, st, p);
+    else launch((fc_kernel<4, 4>), grid, block, 0, st, p);
     return hipGetLastError();
 }
 
@@ -610,10 +610,10 @@ static hipError_t launch_stem_t(const StemParams &p, hipStream_t st) {
     if (lds > 65536) return hipErrorInvalidValue;
     const dim3 grid(p.N * ((p.OH + th - 1) / th)), block(256);
     switch (p.nb16) {
-        case 1: hipLaunchKernelGGL((stem_kernel<TIN, 1>), grid, block, lds, st, p, th, rs, nrows); break;
-        case 2: hipLaunchKernelGGL((stem_kernel<TIN, 2>), grid, block, lds, st, p, th, rs, nrows); break;
-        case 3: hipLaunchKernelGGL((stem_kernel<TIN, 3>), grid, block, lds, st, p, th, rs, nrows); break;
-        case 4: hipLaunchKernelGGL((stem_kernel<TIN, 4>), grid, block, lds, st, p, th, rs, nrows); break;
+        case 1: launch((stem_kernel<TIN, 1>), grid, block, lds, st, p, th, rs, nrows); break;
+        case 2: launch((stem_kernel<TIN, 2>), grid, block, lds, st, p, th, rs, nrows); break;
+        case 3: launch((stem_kernel<TIN, 3>), grid, block, lds, st, p, th, rs, nrows); break;
+        case 4: launch((stem_kernel<TIN, 4>), grid, block, lds, st, p, th, rs, nrows); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

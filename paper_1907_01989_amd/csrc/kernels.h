@@ -1,12 +1,30 @@
 // Kernel parameter blocks and launchers (internal to the engine).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include "../../include/mgi.h"
 
 namespace mgi {
 namespace kern {
+
+// Optional timestamps for the next kernel launch on this thread: when set,
+// launches go through hipExtLaunchKernelGGL, which records `start` when the
+// kernel begins and `stop` when it ends on the device.
+struct LaunchEvents {
+    hipEvent_t start = nullptr, stop = nullptr;
+};
+LaunchEvents &launch_events();
+
+template <typename F, typename... Args>
+inline void launch(F kernel, dim3 grid, dim3 block, unsigned lds, hipStream_t st, Args... args) {
+    const LaunchEvents &ev = launch_events();
+    if (ev.start || ev.stop)
+        hipExtLaunchKernelGGL(kernel, grid, block, lds, st, ev.start, ev.stop, 0, args...);
+    else
+        hipLaunchKernelGGL(kernel, grid, block, lds, st, args...);
+}
 
 typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 typedef _Float16 h4 __attribute__((ext_vector_type(4)));

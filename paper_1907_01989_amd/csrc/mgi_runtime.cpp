@@ -198,7 +198,7 @@ extern "C" mgi_status mgi_plan_bind(mgi_plan *p, void *dev_workspace, void *dev_
 namespace {
 
 mgi_status run_plan(mgi_plan *p, const void *const *dev_inputs, void *const *dev_outputs,
-                    void *stream, void *const *events, const char *who) {
+                    void *stream, void *const *start_ev, void *const *stop_ev, const char *who) {
     if (!p) return fail(MGI_ERR_INVALID_ARG, std::string(who) + ": null plan");
     if (!p->bound) return fail(MGI_ERR_STATE, std::string(who) + ": plan is not bound");
     if (!p->input_bufs.empty() && !dev_inputs)
@@ -210,20 +210,15 @@ mgi_status run_plan(mgi_plan *p, const void *const *dev_inputs, void *const *dev
         if (!dev_outputs[i]) return fail(MGI_ERR_INVALID_ARG, std::string(who) + ": null output pointer");
     hipStream_t st = static_cast<hipStream_t>(stream);
     Bases B{static_cast<char *>(p->dev_ws), dev_inputs, dev_outputs};
-    const size_t nn = p->nodes.size();
-    for (size_t i = 0; i < nn; ++i) {
-        if (events && events[i]) {
-            hipError_t e = hipEventRecord(static_cast<hipEvent_t>(events[i]), st);
-            if (e != hipSuccess) return hip_fail(e, (std::string(who) + ": event record").c_str());
-        }
+    LaunchEvents &ev = launch_events();
+    for (size_t i = 0; i < p->nodes.size(); ++i) {
+        ev.start = start_ev ? static_cast<hipEvent_t>(start_ev[i]) : nullptr;
+        ev.stop = stop_ev ? static_cast<hipEvent_t>(stop_ev[i]) : nullptr;
         hipError_t e = launch_node(*p, p->nodes[i], B, st);
+        ev.start = ev.stop = nullptr;
         if (e != hipSuccess)
             return hip_fail(e, (std::string(who) + ": node " + std::to_string(i) + " (" +
                                 p->nodes[i].kname + ")").c_str());
-    }
-    if (events && events[nn]) {
-        hipError_t e = hipEventRecord(static_cast<hipEvent_t>(events[nn]), st);
-        if (e != hipSuccess) return hip_fail(e, (std::string(who) + ": event record").c_str());
     }
     p->last_outputs.assign(dev_outputs, dev_outputs + p->output_bufs.size());
     return MGI_OK;
@@ -233,14 +228,16 @@ mgi_status run_plan(mgi_plan *p, const void *const *dev_inputs, void *const *dev
 
 extern "C" mgi_status mgi_plan_run(mgi_plan *p, const void *const *dev_inputs,
                                    void *const *dev_outputs, void *stream) {
-    return run_plan(p, dev_inputs, dev_outputs, stream, nullptr, "mgi_plan_run");
+    return run_plan(p, dev_inputs, dev_outputs, stream, nullptr, nullptr, "mgi_plan_run");
 }
 
 extern "C" mgi_status mgi_plan_run_timed(mgi_plan *p, const void *const *dev_inputs,
                                          void *const *dev_outputs, void *stream,
-                                         void *const *events) {
-    if (!events) return fail(MGI_ERR_INVALID_ARG, "mgi_plan_run_timed: null event array");
-    return run_plan(p, dev_inputs, dev_outputs, stream, events, "mgi_plan_run_timed");
+                                         void *const *start_events, void *const *stop_events) {
+    if (!start_events || !stop_events)
+        return fail(MGI_ERR_INVALID_ARG, "mgi_plan_run_timed: null event array");
+    return run_plan(p, dev_inputs, dev_outputs, stream, start_events, stop_events,
+                    "mgi_plan_run_timed");
 }
 
 extern "C" mgi_status mgi_plan_read_node(mgi_plan *p, int i, void *dev_dst, void *stream) {

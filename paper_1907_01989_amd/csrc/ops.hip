@@ -34,6 +34,11 @@ __device__ __forceinline__ h8 zero_h8() {
 
 static inline unsigned blocks_for(size_t n, int per) { return (unsigned)((n + per - 1) / per); }
 
+LaunchEvents &launch_events() {
+    static thread_local LaunchEvents ev;
+    return ev;
+}
+
 // ---------------------------------------------------------------------------
 // Depthwise 3x3 convolution, column strips.  A thread owns one output column
 // of one 8-channel slice of one image and R consecutive output rows: it reads
@@ -172,7 +177,7 @@ static hipError_t launch_dw3(const DwParams &p, hipStream_t st) {
     const int nstrips = (p.OH + R - 1) / R;
     const size_t threads = (size_t)p.OW * nstrips * p.S * p.N;
     if (threads > 0x7fffffffull) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((dw3_kernel<S_, D_, R>), dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, st,
+    launch((dw3_kernel<S_, D_, R>), dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, st,
                        p, nstrips);
     return hipGetLastError();
 }
@@ -189,7 +194,7 @@ hipError_t launch_depthwise(const DwParams &p, hipStream_t st) {
     const int tpp = (ohw + 255) / 256;
     const size_t nblk = (size_t)tpp * p.S * p.N;
     if (nblk > 0x7fffffffu) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(dw_kernel, dim3((unsigned)nblk), dim3(256), 0, st, p, tpp);
+    launch(dw_kernel, dim3((unsigned)nblk), dim3(256), 0, st, p, tpp);
     return hipGetLastError();
 }
 
@@ -208,7 +213,7 @@ __global__ __launch_bounds__(256) void add_kernel(const h8 *a, const h8 *b, h8 *
 
 hipError_t launch_add(const h8 *a, const h8 *b, h8 *y, size_t count, int act, hipStream_t st) {
     if (!count) return hipSuccess;
-    hipLaunchKernelGGL(add_kernel, dim3(blocks_for(count, 256)), dim3(256), 0, st, a, b, y, count, act);
+    launch(add_kernel, dim3(blocks_for(count, 256)), dim3(256), 0, st, a, b, y, count, act);
     return hipGetLastError();
 }
 
@@ -224,7 +229,7 @@ __global__ __launch_bounds__(256) void act_kernel(const h8 *x, h8 *y, size_t n, 
 
 hipError_t launch_act(const h8 *x, h8 *y, size_t count, int act, hipStream_t st) {
     if (!count) return hipSuccess;
-    hipLaunchKernelGGL(act_kernel, dim3(blocks_for(count, 256)), dim3(256), 0, st, x, y, count, act);
+    launch(act_kernel, dim3(blocks_for(count, 256)), dim3(256), 0, st, x, y, count, act);
     return hipGetLastError();
 }
 
@@ -300,10 +305,10 @@ hipError_t launch_gap(const h8 *x, h8 *y, const h8 *zero, int N, int HW, int S, 
     const size_t planes = (size_t)S * N;
     if (!planes) return hipSuccess;
     if (HW <= 64) {
-        hipLaunchKernelGGL(gap_small_kernel, dim3(blocks_for(planes * 8, 256)), dim3(256), 0, st, x, y,
+        launch(gap_small_kernel, dim3(blocks_for(planes * 8, 256)), dim3(256), 0, st, x, y,
                            zero, (int)planes, HW);
     } else {
-        hipLaunchKernelGGL(gap_kernel, dim3(blocks_for(planes, 4)), dim3(256), 0, st, x, y, N, HW, S);
+        launch(gap_kernel, dim3(blocks_for(planes, 4)), dim3(256), 0, st, x, y, N, HW, S);
     }
     return hipGetLastError();
 }
@@ -362,7 +367,7 @@ __global__ __launch_bounds__(256) void softmax_kernel(const float *z, float *y, 
 
 hipError_t launch_softmax(const float *z, float *y, int rows, int cols, hipStream_t st) {
     if (rows <= 0 || cols <= 0) return hipSuccess;
-    hipLaunchKernelGGL(softmax_kernel, dim3(blocks_for(rows, 4)), dim3(256), 0, st, z, y, rows, cols);
+    launch(softmax_kernel, dim3(blocks_for(rows, 4)), dim3(256), 0, st, z, y, rows, cols);
     return hipGetLastError();
 }
 
@@ -390,7 +395,7 @@ __global__ __launch_bounds__(256) void concat_kernel(ConcatParams p) {
 hipError_t launch_concat(const ConcatParams &p, hipStream_t st) {
     const size_t n = (size_t)p.S * p.M;
     if (!n) return hipSuccess;
-    hipLaunchKernelGGL(concat_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, st, p);
+    launch(concat_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, st, p);
     return hipGetLastError();
 }
 
@@ -471,9 +476,9 @@ hipError_t launch_resize(const ResizeParams &p, bool argmax, hipStream_t st) {
     const size_t opix = (size_t)p.N * p.OH * p.OW;
     if (!opix) return hipSuccess;
     if (argmax) {
-        hipLaunchKernelGGL(resize_argmax_kernel, dim3(blocks_for(opix, 256)), dim3(256), 0, st, p);
+        launch(resize_argmax_kernel, dim3(blocks_for(opix, 256)), dim3(256), 0, st, p);
     } else {
-        hipLaunchKernelGGL(resize_kernel, dim3(blocks_for(opix * p.S, 256)), dim3(256), 0, st, p);
+        launch(resize_kernel, dim3(blocks_for(opix * p.S, 256)), dim3(256), 0, st, p);
     }
     return hipGetLastError();
 }
@@ -501,7 +506,7 @@ __global__ __launch_bounds__(256) void argmax_kernel(const h8 *x, int *y, int M,
 
 hipError_t launch_argmax(const h8 *x, int *y, int M, int S, int C, hipStream_t st) {
     if (M <= 0) return hipSuccess;
-    hipLaunchKernelGGL(argmax_kernel, dim3(blocks_for(M, 256)), dim3(256), 0, st, x, y, M, S, C);
+    launch(argmax_kernel, dim3(blocks_for(M, 256)), dim3(256), 0, st, x, y, M, S, C);
     return hipGetLastError();
 }
 
@@ -528,10 +533,10 @@ hipError_t launch_ingest(const void *x, bool fp16_in, h8 *y, int M, int C, hipSt
     const size_t n = (size_t)M * S;
     if (!n) return hipSuccess;
     if (fp16_in)
-        hipLaunchKernelGGL((ingest_kernel<_Float16>), dim3(blocks_for(n, 256)), dim3(256), 0, st,
+        launch((ingest_kernel<_Float16>), dim3(blocks_for(n, 256)), dim3(256), 0, st,
                            (const _Float16 *)x, y, M, C, S);
     else
-        hipLaunchKernelGGL((ingest_kernel<float>), dim3(blocks_for(n, 256)), dim3(256), 0, st,
+        launch((ingest_kernel<float>), dim3(blocks_for(n, 256)), dim3(256), 0, st,
                            (const float *)x, y, M, C, S);
     return hipGetLastError();
 }
@@ -551,7 +556,7 @@ hipError_t launch_export(const h8 *x, float *y, int M, int C, hipStream_t st) {
     const int S = (C + 7) / 8;
     const size_t n = (size_t)M * S;
     if (!n) return hipSuccess;
-    hipLaunchKernelGGL(export_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, st, x, y, M, C, S);
+    launch(export_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, st, x, y, M, C, S);
     return hipGetLastError();
 }
 
