@@ -412,6 +412,147 @@ hipError_t launch_gemm_xs(const GemmParams &p, int wm, int bn, int pf, hipStream
 }
 
 // ---------------------------------------------------------------------------
+// Pointwise GEMM, pipelined variant for mid and long K.  Re-reading the
+// activations for every 32-channel output block (the weight-slab kernel) costs
+// more L2->CU traffic than the per-CU load path delivers once K and the number
+// of output channels grow; here a workgroup owns a BM-pixel x BN-channel tile
+// (2 x 2 waves of BM/2 x BN/2), so activations are read cout/BN times and
+// weights M/BM times.  Both operands go through a ring of NST LDS stages of
+// 4 K-slices each, filled by direct global->LDS loads (16 bytes per lane, no
+// register staging): a stage's 64 consecutive sliced elements are one wave
+// load, and its weight fragments keep the packed per-lane order.  Each
+// iteration waits for its own stage (the newer NST-2 stages stay in flight),
+// meets the other waves at a barrier, issues the load of the stage NST-1
+// ahead into the slot freed by the previous iteration, and runs its MFMAs.
+// The loop is unrolled by NST so every slot is a compile-time choice.
+// ---------------------------------------------------------------------------
+// 16 bytes per lane from global memory straight into LDS: lane l writes
+// lds + 16*l, so the LDS side is one contiguous KiB per wave.  Issued as
+// inline asm so that the compiler does not track it: it would otherwise
+// conservatively wait for every such load before any LDS read it cannot
+// prove independent (at loop heads it cannot), serialising the ring.  The
+// loads are ordered by explicit s_waitcnt + s_barrier instead.
+__device__ __forceinline__ void load_lds16(const h8 *src, const h8 *lds) {
+    const unsigned la = (unsigned)(size_t)(__attribute__((address_space(3))) const void *)lds;
+    asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(la) : "memory");
+}
+
+// wait until at most N vector-memory instructions of this wave are in flight
+// and all of its LDS reads have returned (expcnt left at its maximum)
+template <int N>
+__device__ __forceinline__ void wait_vm_lds() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4));
+}
+
+template <int BM, int BN>
+struct PipeTile {
+    static constexpr int KS = 4, NST = 4;
+    static constexpr int XE = BM * KS, WE = BN * KS;    // 16-byte elements per stage
+    static constexpr int XL = XE / 256, WL = WE / 256;  // wave loads per wave per stage
+    static constexpr int LPW = XL + WL;
+    static_assert(XE % 256 == 0 && WE % 256 == 0, "tile must be a multiple of 64 both ways");
+};
+
+template <int BM, int BN>
+__device__ __forceinline__ void pipe_issue(const GemmParams &p, int kk, h8 *st, int m0, int nb0,
+                                           int wave, int lane) {
+    using T = PipeTile<BM, BN>;
+    const int k0 = kk * T::KS;
+#pragma unroll
+    for (int i = 0; i < T::XL; ++i) {
+        const int q = wave * T::XL + i;                  // wave load within the stage
+        const int e0 = q * 64, sl = e0 / BM, px = e0 - sl * BM;
+        const int ks = min(k0 + sl, p.ksl - 1);          // K tail meets zero weights
+        const int m = min(m0 + px + lane, p.M - 1);      // rows past M are never stored
+        load_lds16(p.x + (size_t)ks * p.M + m, st + e0);
+    }
+#pragma unroll
+    for (int i = 0; i < T::WL; ++i) {
+        const int q = wave * T::WL + i;                  // output block within the tile
+        const int nb = min(nb0 + q, p.nb16 - 1);
+        load_lds16(p.w + ((size_t)nb * p.ksp + k0) * 16 + lane, st + T::XE + q * 64);
+    }
+}
+
+template <int BM, int BN>
+__global__ __launch_bounds__(256) void gemm_pipe_kernel(GemmParams p) {
+    using T = PipeTile<BM, BN>;
+    constexpr int WMP = BM / 2, WNC = BN / 2, FM = WMP / 16, FN = WNC / 16;
+    static_assert(WMP * WNC * 4 <= (T::XE + T::WE) * 16, "epilogue tile must fit one stage");
+    __shared__ h8 st0[T::XE + T::WE], st1[T::XE + T::WE], st2[T::XE + T::WE], st3[T::XE + T::WE];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave & 1, wn = wave >> 1;
+    const int tile = xcd_tile(blockIdx.x, gridDim.x);
+    const int mt = tile / p.ntiles, nt = tile - mt * p.ntiles;
+    const int m0 = mt * BM, nb0 = nt * (BN / 16);
+    const int nk = p.ksp / T::KS;
+
+    f4 acc[FN][FM];
+#pragma unroll
+    for (int i = 0; i < FN; ++i)
+#pragma unroll
+        for (int j = 0; j < FM; ++j) acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+
+    pipe_issue<BM, BN>(p, 0, st0, m0, nb0, wave, lane);
+    if (nk > 1) pipe_issue<BM, BN>(p, 1, st1, m0, nb0, wave, lane);
+    if (nk > 2) pipe_issue<BM, BN>(p, 2, st2, m0, nb0, wave, lane);
+
+    auto body = [&](int kk, const h8 *cur, h8 *nxt) {
+        // stage kk has landed once at most min(2, nk-1-kk) newer stages are
+        // pending; this wave's reads of the previous slot have returned, so
+        // after the barrier no wave still reads the slot refilled below
+        const int newer = min(2, nk - 1 - kk);
+        if (newer >= 2) wait_vm_lds<2 * T::LPW>();
+        else if (newer == 1) wait_vm_lds<T::LPW>();
+        else wait_vm_lds<0>();
+        __builtin_amdgcn_s_barrier();
+        if (kk + 3 < nk) pipe_issue<BM, BN>(p, kk + 3, nxt, m0, nb0, wave, lane);
+        h8 a[FN], b[FM];
+#pragma unroll
+        for (int i = 0; i < FN; ++i) a[i] = cur[T::XE + (wn * FN + i) * 64 + lane];
+#pragma unroll
+        for (int j = 0; j < FM; ++j) b[j] = cur[(lane >> 4) * BM + wm * WMP + j * 16 + (lane & 15)];
+#pragma unroll
+        for (int i = 0; i < FN; ++i)
+#pragma unroll
+            for (int j = 0; j < FM; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[i], b[j], acc[i][j], 0, 0, 0);
+    };
+    for (int kk = 0; kk < nk; kk += 4) {
+        body(kk, st0, st3);
+        if (kk + 1 < nk) body(kk + 1, st1, st0);
+        if (kk + 2 < nk) body(kk + 2, st2, st1);
+        if (kk + 3 < nk) body(kk + 3, st3, st2);
+    }
+
+    __syncthreads();
+    h8 *stage = wave == 0 ? st0 : wave == 1 ? st1 : wave == 2 ? st2 : st3;
+    store_tile_c8<FM, FN>(p, acc, m0 + wm * WMP, nb0 + wn * FN, (float *)stage, lane);
+}
+
+template <int BM, int BN>
+static hipError_t launch_pipe_t(const GemmParams &p, hipStream_t st) {
+    GemmParams q = p;
+    q.mtiles = (p.M + BM - 1) / BM;
+    q.ntiles = (p.nb16 * 16 + BN - 1) / BN;
+    launch((gemm_pipe_kernel<BM, BN>), dim3(q.mtiles * q.ntiles), dim3(256), 0, st, q);
+    return hipGetLastError();
+}
+
+hipError_t launch_gemm_pipe(const GemmParams &p, int bm, int bn, hipStream_t st) {
+    if (p.M <= 0) return hipSuccess;
+    if (p.ksp % 4 != 0 || p.Min != p.M) return hipErrorInvalidValue;
+    if (bm == 64 && bn == 64) return launch_pipe_t<64, 64>(p, st);
+    if (bm == 64 && bn == 128) return launch_pipe_t<64, 128>(p, st);
+    if (bm == 128 && bn == 64) return launch_pipe_t<128, 64>(p, st);
+    if (bm == 128 && bn == 128) return launch_pipe_t<128, 128>(p, st);
+    return hipErrorInvalidValue;
+}
+
+// ---------------------------------------------------------------------------
 // Fully-connected layer (1x1 spatial input, fp32 logits out).  M (images) is
 // small and K long, so a workgroup takes 16 output channels for up to 16*FM
 // images and splits K over its 4 waves; each wave loads B K-steps of weight

@@ -52,6 +52,9 @@ hipError_t launch_gemm(const GemmParams &p, int bm, int bn, bool taps, bool f32o
 // channels, pf K steps of activation prefetch.  Needs
 // gemm_xs_lds_bytes(ksp, wm, bn) <= 64 KiB and zero weights for padded K.
 hipError_t launch_gemm_xs(const GemmParams &p, int wm, int bn, int pf, hipStream_t st);
+// pointwise GEMM with both operands in a 4-stage LDS ring fed by direct
+// global->LDS loads; tile bm pixels x bn channels, bm, bn in {64, 128}
+hipError_t launch_gemm_pipe(const GemmParams &p, int bm, int bn, hipStream_t st);
 // fully-connected layer, fp32 (M x cout) output; K split over the waves
 hipError_t launch_fc(const GemmParams &p, hipStream_t st);
 size_t gemm_xs_lds_bytes(int ksp, int wm, int bn);

@@ -63,6 +63,28 @@ GemmTile pick_tile(size_t M, int cout) {
     return t;
 }
 
+// Pipelined pointwise kernel (K >= 64, at least 64 output channels): a
+// 128 x 128 tile when there are at least 512 channels, else 128 x 64, as long
+// as that still gives 384 workgroups (1.5 per CU); otherwise the shape with
+// the most workgroups.  Measured on the MobileNet shapes: 128-channel tiles
+// pay off only when many channels share one activation read.
+void pick_pipe_tile(GemmTile &t, size_t M, int npad) {
+    const int cand[3][2] = {{128, 128}, {128, 64}, {64, 64}};
+    size_t best_tiles = 0;
+    int best = 2;
+    for (int c = 0; c < 3; ++c) {
+        const int bm = cand[c][0], bn = cand[c][1];
+        if (bn == 128 && npad < 512) continue;
+        const size_t tiles = ((M + bm - 1) / bm) * (size_t)((npad + bn - 1) / bn);
+        if (tiles >= 384) { best = c; break; }
+        if (tiles > best_tiles) { best_tiles = tiles; best = c; }
+    }
+    t.pipe = true;
+    t.slab = false;
+    t.bm = cand[best][0];
+    t.bn = cand[best][1];
+}
+
 }  // namespace
 
 mgi_status build_plan(const mgi_graph &g, const mgi_options &o, mgi_plan &p) {
@@ -260,7 +282,9 @@ mgi_status build_plan(const mgi_graph &g, const mgi_options &o, mgi_plan &p) {
                 }
                 nd.nb16 = (d.cout + 15) / 16;
                 nd.tile = pick_tile(out_shape.pixels(), d.cout);
-                if (nd.kind == NodeKind::Gemm && !nd.taps) {
+                if (nd.kind == NodeKind::Gemm && !nd.taps && nd.ksl >= 8 && nd.nb16 * 16 >= 64) {
+                    pick_pipe_tile(nd.tile, out_shape.pixels(), nd.nb16 * 16);
+                } else if (nd.kind == NodeKind::Gemm && !nd.taps) {
                     // weight-slab kernel: 128 x 32 tiles, two K steps of
                     // prefetch when there are at least two; the slab (32
                     // channels x all K) plus the epilogue tiles fit 64 KiB

@@ -76,11 +76,13 @@ enum class NodeKind {
 };
 
 // Tile shape of the MFMA GEMM (pointwise, implicit-GEMM convolution, FC).
-// slab = true selects the weight-slab pointwise kernel with (4 * wm) x bn
-// tiles and pf K steps of activation prefetch; otherwise the LDS-staged
-// kernel with bm x bn tiles.
+// pipe = true selects the pipelined pointwise kernel with bm x bn tiles;
+// slab = true the weight-slab pointwise kernel with (4 * wm) x bn tiles and
+// pf K steps of activation prefetch; otherwise the LDS-staged kernel with
+// bm x bn tiles.
 struct GemmTile {
     int bm = 64, bn = 64;
+    bool pipe = false;
     bool slab = false;
     int wm = 32, pf = 1;
 };

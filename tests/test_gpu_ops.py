@@ -43,6 +43,11 @@ PW_CASES = [
     (4, 9, 9, 24, 144, ACT_RELU6, False),
     (2, 7, 7, 160, 160, ACT_NONE, True),
     (64, 7, 7, 64, 200, ACT_RELU6, False),
+    # pipelined kernel: K not a multiple of 32, ragged pixel and channel tails,
+    # a 128 x 128 tile with a residual epilogue, long K with 64 x 64 tiles
+    (1, 13, 13, 200, 72, ACT_RELU6, False),
+    (64, 14, 14, 96, 576, ACT_RELU6, True),
+    (8, 14, 14, 512, 1024, ACT_RELU, True),
 ]
 
 
