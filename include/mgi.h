@@ -68,7 +68,10 @@ typedef enum {
 
 typedef enum {
     MGI_PLANNER_NAIVE = 0,  /* one buffer per intermediate tensor (Sec. 5, baseline) */
-    MGI_PLANNER_GREEDY = 1  /* shared objects, Algorithm 1 (Sec. 5) */
+    MGI_PLANNER_GREEDY = 1, /* shared objects, Algorithm 1 (Sec. 5) */
+    MGI_PLANNER_MCFP = 2    /* shared objects from a minimum-cost flow (Sec. 5, flow network
+                               solved by successive shortest paths with SPFA); a tensor that
+                               nothing consumes is free right after its producer */
 } mgi_planner;
 
 typedef struct mgi_graph mgi_graph;
@@ -238,7 +241,8 @@ mgi_status mgi_plan_node_info(const mgi_plan *p, int i, const char **kind, int *
 mgi_status mgi_plan_read_node(mgi_plan *p, int i, void *dev_dst, void *stream);
 
 /* ---------------------------------------------------------------------------
- * stand-alone planner (Sec. 5, Algorithm 1), for planning outside a graph
+ * stand-alone planner (Sec. 5: Algorithm 1 or the minimum-cost flow), for
+ * planning outside a graph
  * ------------------------------------------------------------------------- */
 /* Intermediate tensor t (0 <= t < n_tensors) has `sizes[t]` bytes, is produced
  * by operator first_op[t] and last used by operator last_op[t]

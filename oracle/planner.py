@@ -86,6 +86,104 @@ def greedy(ops, sizes, intermediate):
     return assign, objects
 
 
+def mcfp(ops, sizes, intermediate):
+    """Minimum-cost-flow shared objects (Sec. 5, the flow-network paragraph).
+
+    The network has a source s, a sink t and two vertices l_x, r_x per
+    intermediate tensor x, and four kinds of unit-capacity edges:
+      1. s -> r_x, cost size_x (x gets a new shared object);
+      2. l_x -> r_y, cost max(0, size_y - size_x), when the object of x can be
+         reused for y, i.e. x's last consumer runs before y's producer;
+      3. s -> l_x, cost 0;
+      4. r_x -> t, cost 0.
+    A flow of value N (one unit through every r_x) of minimum cost is found by
+    successive shortest augmenting paths, each found with Bellman-Ford over
+    the residual network (the paper names SPFA, a queue-driven Bellman-Ford;
+    the plain form relaxes every edge each pass).  A saturated edge of kind 1
+    opens a new object for x; a saturated edge of kind 2 hands x's object to
+    y.  Object sizes are the largest tensor placed in them.  Returns
+    ``(assign, objects, flow_cost)``.
+    """
+    first, last = lifetimes(ops, intermediate)
+    ts = sorted((t for t in intermediate if t in first), key=lambda t: (first[t], t))
+    n = len(ts)
+    S, T = 0, 1
+    L = lambda i: 2 + 2 * i          # noqa: E731
+    R = lambda i: 3 + 2 * i          # noqa: E731
+    nv = 2 + 2 * n
+    edges = []                       # [from, to, residual capacity, cost]; edge e^1 is e's reverse
+
+    def add(u, v, cost):
+        edges.append([u, v, 1, cost])
+        edges.append([v, u, 0, -cost])
+        return len(edges) - 2
+
+    new_edge = [add(S, R(i), sizes[ts[i]]) for i in range(n)]                      # kind 1
+    reuse_edge = {}
+    for i in range(n):
+        for j in range(n):
+            if last[ts[i]] < first[ts[j]]:
+                reuse_edge[(i, j)] = add(L(i), R(j), max(0, sizes[ts[j]] - sizes[ts[i]]))  # kind 2
+    for i in range(n):
+        add(S, L(i), 0)                                                          # kind 3
+    for i in range(n):
+        add(R(i), T, 0)                                                          # kind 4
+
+    cost = 0
+    for _ in range(n):
+        inf = float("inf")
+        dist = [inf] * nv
+        pred = [-1] * nv
+        dist[S] = 0
+        for _ in range(nv - 1):
+            changed = False
+            for e, (u, v, cap, c) in enumerate(edges):
+                if cap > 0 and dist[u] + c < dist[v]:
+                    dist[v] = dist[u] + c
+                    pred[v] = e
+                    changed = True
+            if not changed:
+                break
+        assert dist[T] < inf, "the network always admits a flow of value N"
+        v = T
+        while v != S:
+            e = pred[v]
+            edges[e][2] -= 1
+            edges[e ^ 1][2] += 1
+            v = edges[e][0]
+        cost += dist[T]
+
+    assign, objects = {}, []
+    for j in range(n):
+        y = ts[j]
+        if edges[new_edge[j]][2] == 0:
+            assign[y] = len(objects)
+            objects.append(sizes[y])
+            continue
+        src = [i for i in range(n) if (i, j) in reuse_edge and edges[reuse_edge[(i, j)]][2] == 0]
+        assert len(src) == 1
+        k = assign[ts[src[0]]]
+        assign[y] = k
+        objects[k] = max(objects[k], sizes[y])
+    return assign, objects, cost
+
+
+def chain_cost(ops, sizes, intermediate, assign):
+    """The flow-network cost of an assignment: per object, the size of its
+    first tensor plus every increase from one tensor to the next (kinds 1
+    and 2 of the network); equals the minimum-cost flow for an MCFP plan."""
+    first, _ = lifetimes(ops, intermediate)
+    by_obj = {}
+    for t in sorted((t for t in intermediate if t in first), key=lambda t: (first[t], t)):
+        by_obj.setdefault(assign[t], []).append(t)
+    c = 0
+    for chain in by_obj.values():
+        c += sizes[chain[0]]
+        for a, b in zip(chain, chain[1:]):
+            c += max(0, sizes[b] - sizes[a])
+    return c
+
+
 def total(objects):
     return int(sum(objects))
 

@@ -16,7 +16,7 @@ STATUS = {0: "MGI_OK", 1: "MGI_ERR_INVALID_ARG", 2: "MGI_ERR_SHAPE", 3: "MGI_ERR
           4: "MGI_ERR_STATE", 5: "MGI_ERR_WORKSPACE", 6: "MGI_ERR_HIP", 7: "MGI_ERR_OOM_HOST"}
 ACT_NONE, ACT_RELU, ACT_RELU6 = 0, 1, 2
 DTYPE_FP16, DTYPE_BF16, DTYPE_FP32, DTYPE_INT32 = 0, 1, 2, 3
-PLANNER_NAIVE, PLANNER_GREEDY = 0, 1
+PLANNER_NAIVE, PLANNER_GREEDY, PLANNER_MCFP = 0, 1, 2
 
 
 class MgiError(RuntimeError):

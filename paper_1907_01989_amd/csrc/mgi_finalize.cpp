@@ -90,7 +90,7 @@ void pick_pipe_tile(GemmTile &t, size_t M, int npad) {
 mgi_status build_plan(const mgi_graph &g, const mgi_options &o, mgi_plan &p) {
     const int nops = (int)g.ops.size();
     if (g.outputs.empty()) return fail(MGI_ERR_STATE, "mgi_graph_finalize: no output marked");
-    if (o.planner != MGI_PLANNER_NAIVE && o.planner != MGI_PLANNER_GREEDY)
+    if (o.planner != MGI_PLANNER_NAIVE && o.planner != MGI_PLANNER_GREEDY && o.planner != MGI_PLANNER_MCFP)
         return fail(MGI_ERR_UNSUPPORTED, "mgi_graph_finalize: unknown planner");
     if (o.dtype != MGI_DTYPE_FP16)
         return fail(MGI_ERR_UNSUPPORTED, "mgi_graph_finalize: only fp16 storage is built");
@@ -493,9 +493,10 @@ mgi_status build_plan(const mgi_graph &g, const mgi_options &o, mgi_plan &p) {
         last.push_back(p.bufs[b].last_use);
     }
     PlanResult naive = plan_naive(sizes);
-    PlanResult pr = (o.planner == MGI_PLANNER_GREEDY && !o.materialize_all)
-                        ? plan_greedy(sizes, first, last)
-                        : naive;
+    PlanResult pr = o.materialize_all                   ? naive
+                    : o.planner == MGI_PLANNER_GREEDY ? plan_greedy(sizes, first, last)
+                    : o.planner == MGI_PLANNER_MCFP   ? plan_mcfp(sizes, first, last)
+                                                      : naive;
     p.mem_naive = 0;
     for (size_t s : sizes) p.mem_naive += s;
     p.mem_planned = 0;

@@ -146,6 +146,8 @@ struct PlanResult {
 PlanResult plan_naive(const std::vector<size_t> &sizes);
 PlanResult plan_greedy(const std::vector<size_t> &sizes, const std::vector<int> &first,
                        const std::vector<int> &last);
+PlanResult plan_mcfp(const std::vector<size_t> &sizes, const std::vector<int> &first,
+                     const std::vector<int> &last);
 
 // finalize steps
 mgi_status build_plan(const mgi_graph &g, const mgi_options &o, mgi_plan &p);

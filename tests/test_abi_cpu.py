@@ -192,6 +192,53 @@ def test_library_planner_fig5(golden_dir):
         assert obj[ts.index(a)] == obj[ts.index(b)]
 
 
+@pytest.mark.parametrize("net,key,mib", [("mobilenet_v1", "MobileNet", 2.7), ("mobilenet_v2", "MobileNetV2", 3.8)])
+def test_library_mcfp_reproduces_table3(net, key, mib):
+    # Table 3 counts the graph's tensors as given (fusion off); fusing the
+    # residual adds of v2 into the projections removes tensors and changes
+    # the flow solution, which must stay no larger than the unfused one
+    d = workloads.WORKLOADS[net](1, logits_output=False)
+    naive, planned, nobj = engine.Plan(d, planner=B.PLANNER_MCFP, fuse=False, bind=False).memory_report()
+    ops, sizes, inter = oplan.graph_problem(d, oracle.tensor_shapes(d))
+    _, ref, _ = oplan.mcfp(ops, sizes, inter)
+    assert round(planned / 2 ** 20, 1) == mib
+    assert planned == oplan.total(ref) and nobj == len(ref)
+    fused = engine.Plan(d, planner=B.PLANNER_MCFP, fuse=True, bind=False).memory_report()
+    assert fused[1] <= planned
+
+
+def test_library_mcfp_matches_oracle_on_random_dags():
+    rng = random.Random(99)
+    for _ in range(300):
+        n = rng.randint(3, 14)
+        ops = [([0], [])]
+        for i in range(1, n):
+            ops.append(([i], rng.sample(range(i), rng.randint(1, min(3, i)))))
+        sizes = {i: rng.choice([16, 32, 48, 64, 100, 128, 256]) for i in range(n)}
+        inter = set(range(1, n - 1))
+        ts, sz, fi, la = to_lifetimes(ops, sizes, inter)
+        obj, osz = B.mgi_planner_assign(B.PLANNER_MCFP, sz, fi, la)
+        assign = {t: obj[i] for i, t in enumerate(ts)}
+        oplan.check_assignment(ops, sizes, inter, assign, osz)
+        for k, size in enumerate(osz):
+            assert size == max(sizes[t] for t in ts if assign[t] == k)
+        _, _, ref_cost = oplan.mcfp(ops, sizes, inter)
+        assert oplan.chain_cost(ops, sizes, inter, assign) == ref_cost
+
+
+def test_library_mcfp_fig5(golden_dir):
+    import json
+    with open(os.path.join(golden_dir, "fig5_planner_example.json")) as f:
+        gd = json.load(f)
+    ops = [(o[0], o[1]) for o in gd["graph"]["ops"]]
+    sizes = dict(enumerate(gd["graph"]["sizes"]))
+    ts, sz, fi, la = to_lifetimes(ops, sizes, set(sizes))
+    obj, osz = B.mgi_planner_assign(B.PLANNER_MCFP, sz, fi, la)
+    assert sum(osz) == gd["mcfp"]["total"]
+    for a, b in gd["mcfp"]["reuse"]:
+        assert obj[ts.index(a)] == obj[ts.index(b)]
+
+
 def test_planner_assign_rejects_bad_lifetimes():
     assert err(B.mgi_planner_assign, B.PLANNER_GREEDY, [4, 4], [0, 3], [2, 1]) == 1
     assert err(B.mgi_planner_assign, 7, [4], [0], [1]) == 3

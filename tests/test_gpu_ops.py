@@ -232,3 +232,17 @@ def test_greedy_and_materialized_runs_agree():
     _, outs_b, _ = run_gpu(desc, materialize_all=True)
     for a, b in zip(outs_a, outs_b):
         np.testing.assert_array_equal(a, b)
+
+
+@pytest.mark.parametrize("net,batch", [("mobilenet_v2", 2), ("deeplab", 1)])
+def test_mcfp_arena_runs_agree_with_greedy(net, batch):
+    # the minimum-cost-flow plan places tensors differently (Sec. 5); the
+    # kernels and their inputs are the same, so the outputs are bit-identical
+    from paper_1907_01989_amd import _binding as B
+    desc = workloads.WORKLOADS[net](batch)
+    log(f"[case] {net} b{batch} mcfp vs greedy arena")
+    plan_m, outs_m, _ = run_gpu(desc, materialize_all=False, planner=B.PLANNER_MCFP)
+    plan_g, outs_g, _ = run_gpu(desc, materialize_all=False, planner=B.PLANNER_GREEDY)
+    assert plan_m.memory_report()[1] != plan_g.memory_report()[1]
+    for a, b in zip(outs_m, outs_g):
+        np.testing.assert_array_equal(a, b)
