@@ -48,6 +48,7 @@ class Hip:
                                                ctypes.c_void_p]
         self.L.hipEventSynchronize.argtypes = [ctypes.c_void_p]
         self.L.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.L.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
 
     def event(self):
         e = ctypes.c_void_p()
@@ -62,6 +63,15 @@ class Hip:
 
     def destroy(self, e):
         self.L.hipEventDestroy(ctypes.c_void_p(e))
+
+    def record(self, e, stream):
+        assert self.L.hipEventRecord(ctypes.c_void_p(e), ctypes.c_void_p(stream)) == 0
+
+
+def percentiles(xs):
+    ys = sorted(xs)
+    pick = lambda q: ys[min(len(ys) - 1, int(q * len(ys)))]   # noqa: E731
+    return {"mean": sum(ys) / len(ys), "p50": pick(0.5), "p90": pick(0.9)}
 
 
 # ---------------------------------------------------------------------------
@@ -235,13 +245,19 @@ def run_workload(key, steps, warmup, hip, profile_steps=20, detail=True):
         e0, e1 = [None] * nn, [None] * nn
         e0[dom], e1[dom] = a, b
         arrays.append((e0, e1))
+    marks = [hip.event() for _ in range(steps + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(steps):
+        hip.record(marks[k], sh)
         B.mgi_plan_run_timed(plan.handle, ins, ops_ptrs, arrays[k][0], arrays[k][1], sh)
+    hip.record(marks[steps], sh)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     dom_ms = sum(hip.elapsed_ms(a, b) for a, b in dev) / steps
+    step_ms = percentiles([hip.elapsed_ms(marks[k], marks[k + 1]) for k in range(steps)])
+    for e in marks:
+        hip.destroy(e)
     for a, b in dev:
         hip.destroy(a)
         hip.destroy(b)
@@ -266,9 +282,43 @@ def run_workload(key, steps, warmup, hip, profile_steps=20, detail=True):
     total_s = t1 - t0
     res = {"desc": desc, "batch": batch, "net": net, "ms_per_step": total_s / steps * 1e3,
            "images_per_s": batch * steps / total_s, "roofline": roof, "layers": layers,
-           "sum_layer_us": sum(per_node) * 1e3}
+           "sum_layer_us": sum(per_node) * 1e3,
+           "step_ms_device": {k: round(v, 5) for k, v in step_ms.items()}}
     plan.close()
     return res
+
+
+def run_graph_replay(key, steps, warmup, hip):
+    """The same workload with the launch list captured once as a HIP graph and
+    replayed per step (mgi_plan_capture / mgi_plan_replay)."""
+    import torch
+    import workloads
+    from paper_1907_01989_amd import engine
+
+    net, batch = WORKLOADS[key]
+    desc = workloads.WORKLOADS[net](batch)
+    plan = engine.Plan(desc)
+    xs = plan.input_tensors()
+    plan.capture(xs)
+    sh = torch.cuda.current_stream().cuda_stream
+    for _ in range(warmup):
+        plan.replay(sh)
+    marks = [hip.event() for _ in range(steps + 1)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(steps):
+        hip.record(marks[k], sh)
+        plan.replay(sh)
+    hip.record(marks[steps], sh)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    step_ms = percentiles([hip.elapsed_ms(marks[k], marks[k + 1]) for k in range(steps)])
+    for e in marks:
+        hip.destroy(e)
+    plan.close()
+    total_s = t1 - t0
+    return {"images_per_s": batch * steps / total_s, "ms_per_step": total_s / steps * 1e3,
+            "step_ms_device": {k: round(v, 5) for k, v in step_ms.items()}}
 
 
 def cpu_baseline(net, budget_s=10.0):
@@ -335,8 +385,15 @@ def main():
                 continue
             r = run_workload(key, 100, 10, hip, detail=False)
             also[key] = {"images_per_s": round(r["images_per_s"], 1),
-                         "ms_per_step": round(r["ms_per_step"], 4)}
+                         "ms_per_step": round(r["ms_per_step"], 4),
+                         "step_ms_device": r["step_ms_device"]}
             eprint(f"[bench] {key}: {r['images_per_s']:.1f} images/s")
+        for key in ("v1_b1", "v2_b1", "v1_b64", "v2_b64"):
+            r = run_graph_replay(key, 100, 10, hip)
+            also[key + "_graph"] = {"images_per_s": round(r["images_per_s"], 1),
+                                    "ms_per_step": round(r["ms_per_step"], 4),
+                                    "step_ms_device": r["step_ms_device"]}
+            eprint(f"[bench] {key} graph replay: {r['images_per_s']:.1f} images/s")
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(main_res["net"])
@@ -350,13 +407,14 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(main_res["ms_per_step"], 5),
+        "step_ms_device": main_res["step_ms_device"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "fp16",
         "data": "synthetic",
         "config": {"workload": main_res["desc"]["name"], "network": net, "batch": batch,
-                   "input": "NHWC fp32 uniform[0,1] (fp16 values), device-resident",
+                   "input": "NHWC fp16 uniform[0,1], device-resident",
                    "weights": "He-normal seed 0, fp16", "planner": "greedy", "fused": True},
         "roofline": main_res["roofline"],
         "cpu_baseline": cpu,

@@ -240,6 +240,21 @@ mgi_status mgi_plan_node_info(const mgi_plan *p, int i, const char **kind, int *
  * and a completed or stream-ordered run. */
 mgi_status mgi_plan_read_node(mgi_plan *p, int i, void *dev_dst, void *stream);
 
+/* Record one run with these device inputs and outputs (same arguments and
+ * checks as mgi_plan_run) as a HIP graph held by the plan, replacing any
+ * earlier one.  Extends the no-synchronisation dispatch of Sec. 3.2: the
+ * whole launch list becomes one graph launch.  The recorded pointers are
+ * baked in: the caller keeps those buffers alive and unchanged in size, and
+ * refreshes their contents before each replay.  Nothing is executed by the
+ * capture itself.  Errors: MGI_ERR_STATE before mgi_plan_bind; the run's
+ * argument errors; MGI_ERR_HIP if capture or instantiation fails. */
+mgi_status mgi_plan_capture(mgi_plan *p, const void *const *dev_inputs, void *const *dev_outputs);
+
+/* Launch the captured graph on `stream` (asynchronous, like mgi_plan_run;
+ * one replay at a time per plan, since replays share the plan's arena).
+ * MGI_ERR_STATE if nothing has been captured. */
+mgi_status mgi_plan_replay(mgi_plan *p, void *stream);
+
 /* ---------------------------------------------------------------------------
  * stand-alone planner (Sec. 5: Algorithm 1 or the minimum-cost flow), for
  * planning outside a graph

@@ -71,6 +71,8 @@ _SIGS = {
     "mgi_plan_run": ([P, ctypes.POINTER(P), ctypes.POINTER(P), P], I),
     "mgi_plan_run_timed": ([P, ctypes.POINTER(P), ctypes.POINTER(P), P, ctypes.POINTER(P),
                             ctypes.POINTER(P)], I),
+    "mgi_plan_capture": ([P, ctypes.POINTER(P), ctypes.POINTER(P)], I),
+    "mgi_plan_replay": ([P, P], I),
     "mgi_plan_node_count": ([P, IP], I),
     "mgi_plan_node_info": ([P, I, ctypes.POINTER(ctypes.c_char_p), IP, IP, IP, IP, IP, IP], I),
     "mgi_plan_read_node": ([P, I, P, P], I),
@@ -261,6 +263,16 @@ def mgi_plan_run_timed(p, in_ptrs, out_ptrs, start_events, stop_events, stream=N
     ev0 = (P * max(1, len(start_events)))(*[e or None for e in start_events])
     ev1 = (P * max(1, len(stop_events)))(*[e or None for e in stop_events])
     _check(lib().mgi_plan_run_timed(p, ins, outs, P(stream or 0), ev0, ev1))
+
+
+def mgi_plan_capture(p, in_ptrs, out_ptrs):
+    ins = (P * max(1, len(in_ptrs)))(*in_ptrs)
+    outs = (P * max(1, len(out_ptrs)))(*out_ptrs)
+    _check(lib().mgi_plan_capture(p, ins, outs))
+
+
+def mgi_plan_replay(p, stream=None):
+    _check(lib().mgi_plan_replay(p, P(stream or 0)))
 
 
 def mgi_plan_node_count(p):

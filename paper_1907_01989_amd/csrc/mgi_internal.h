@@ -130,6 +130,10 @@ struct mgi_plan {
     void *dev_w = nullptr;
     bool bound = false;
     std::vector<void *> last_outputs;  // output pointers of the latest run
+    void *graph = nullptr;             // hipGraph_t of the captured launch list
+    void *graph_exec = nullptr;        // hipGraphExec_t
+    std::vector<void *> graph_outputs; // output pointers baked into the graph
+    ~mgi_plan();
 };
 
 namespace mgi {

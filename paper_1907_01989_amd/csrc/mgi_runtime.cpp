@@ -167,6 +167,20 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
 
 }  // namespace
 
+namespace {
+
+void release_graph(mgi_plan &p) {
+    if (p.graph_exec) hipGraphExecDestroy(static_cast<hipGraphExec_t>(p.graph_exec));
+    if (p.graph) hipGraphDestroy(static_cast<hipGraph_t>(p.graph));
+    p.graph_exec = nullptr;
+    p.graph = nullptr;
+    p.graph_outputs.clear();
+}
+
+}  // namespace
+
+mgi_plan::~mgi_plan() { release_graph(*this); }
+
 extern "C" mgi_status mgi_plan_destroy(mgi_plan *p) {
     delete p;
     return MGI_OK;
@@ -239,6 +253,56 @@ extern "C" mgi_status mgi_plan_run_timed(mgi_plan *p, const void *const *dev_inp
         return fail(MGI_ERR_INVALID_ARG, "mgi_plan_run_timed: null event array");
     return run_plan(p, dev_inputs, dev_outputs, stream, start_events, stop_events,
                     "mgi_plan_run_timed");
+}
+
+// The launch list of one run is recorded once through stream capture on a
+// stream of the library's own (the caller's stream may be the null stream,
+// which cannot be captured), instantiated, and then replayed with a single
+// graph launch: the per-kernel launch cost of the eager loop, which dominates
+// at batch 1, is paid once at capture.  No node issues a memset or copy, so
+// the graph holds kernel nodes only.
+extern "C" mgi_status mgi_plan_capture(mgi_plan *p, const void *const *dev_inputs,
+                                       void *const *dev_outputs) {
+    if (!p) return fail(MGI_ERR_INVALID_ARG, "mgi_plan_capture: null plan");
+    if (!p->bound) return fail(MGI_ERR_STATE, "mgi_plan_capture: plan is not bound");
+    release_graph(*p);
+    hipStream_t cs = nullptr;
+    hipError_t e = hipStreamCreateWithFlags(&cs, hipStreamNonBlocking);
+    if (e != hipSuccess) return hip_fail(e, "mgi_plan_capture: stream");
+    e = hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal);
+    if (e != hipSuccess) {
+        hipStreamDestroy(cs);
+        return hip_fail(e, "mgi_plan_capture: begin capture");
+    }
+    const mgi_status st = run_plan(p, dev_inputs, dev_outputs, cs, nullptr, nullptr, "mgi_plan_capture");
+    hipGraph_t g = nullptr;
+    e = hipStreamEndCapture(cs, &g);
+    hipStreamDestroy(cs);
+    if (st != MGI_OK) {
+        if (g) hipGraphDestroy(g);
+        return st;
+    }
+    if (e != hipSuccess) return hip_fail(e, "mgi_plan_capture: end capture");
+    hipGraphExec_t ge = nullptr;
+    e = hipGraphInstantiate(&ge, g, nullptr, nullptr, 0);
+    if (e != hipSuccess) {
+        hipGraphDestroy(g);
+        return hip_fail(e, "mgi_plan_capture: instantiate");
+    }
+    p->graph = g;
+    p->graph_exec = ge;
+    p->graph_outputs.assign(dev_outputs, dev_outputs + p->output_bufs.size());
+    return MGI_OK;
+}
+
+extern "C" mgi_status mgi_plan_replay(mgi_plan *p, void *stream) {
+    if (!p) return fail(MGI_ERR_INVALID_ARG, "mgi_plan_replay: null plan");
+    if (!p->graph_exec) return fail(MGI_ERR_STATE, "mgi_plan_replay: nothing captured");
+    hipError_t e = hipGraphLaunch(static_cast<hipGraphExec_t>(p->graph_exec),
+                                  static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "mgi_plan_replay");
+    p->last_outputs = p->graph_outputs;
+    return MGI_OK;
 }
 
 extern "C" mgi_status mgi_plan_read_node(mgi_plan *p, int i, void *dev_dst, void *stream) {

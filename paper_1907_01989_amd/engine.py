@@ -11,6 +11,9 @@ from . import _binding as B
 
 
 def _stream_handle(stream):
+    """A torch stream, a raw hipStream_t (int), or None for torch's current stream."""
+    if isinstance(stream, int):
+        return stream
     import torch
     s = stream if stream is not None else torch.cuda.current_stream()
     return s.cuda_stream
@@ -126,6 +129,23 @@ class Plan:
         B.mgi_plan_run(self.handle, [x.data_ptr() for x in inputs],
                        [y.data_ptr() for y in outputs], _stream_handle(stream))
         return outputs
+
+    def capture(self, inputs, outputs=None):
+        """Record one run over these tensors as a HIP graph (see replay); the
+        tensors stay referenced by the plan so that their memory outlives it."""
+        if outputs is None:
+            outputs = self.alloc_outputs()
+        for x, (shape, dt, nbytes) in zip(inputs, self.inputs_info):
+            if x.numel() * x.element_size() != nbytes or not x.is_contiguous():
+                raise ValueError(f"input must be a contiguous NHWC tensor of {nbytes} bytes")
+        B.mgi_plan_capture(self.handle, [x.data_ptr() for x in inputs], [y.data_ptr() for y in outputs])
+        self._graph_io = (list(inputs), list(outputs))
+        return outputs
+
+    def replay(self, stream=None):
+        """Enqueue the captured run; returns its output tensors (not synchronised)."""
+        B.mgi_plan_replay(self.handle, _stream_handle(stream))
+        return self._graph_io[1]
 
     def input_tensors(self):
         """Device copies of the description's input arrays."""

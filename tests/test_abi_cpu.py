@@ -96,6 +96,8 @@ def test_finalize_state_errors_and_run_before_bind():
         B.mgi_graph_destroy(g)
     try:
         assert err(B.mgi_plan_run, p, [1], [1]) == 4        # not bound
+        assert err(B.mgi_plan_capture, p, [1], [1]) == 4    # not bound
+        assert err(B.mgi_plan_replay, p) == 4               # nothing captured
         assert err(B.mgi_plan_bind, p, 0, 0) == 5           # no buffers
         assert err(B.mgi_plan_bind, p, 0x1001, 0x2000) == 5  # misaligned
         assert err(B.mgi_plan_read_node, p, 0, 0x1000) == 4  # not materialized
