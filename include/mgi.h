@@ -139,8 +139,18 @@ mgi_status mgi_graph_add_depthwise(mgi_graph *g, int in, const mgi_conv_desc *d,
 mgi_status mgi_graph_add_add(mgi_graph *g, int a, int b, int act, int *out);
 
 /* Standalone activation; finalize fuses it into its producer when it can
- * (Sec. 3.2: element-wise operators fused with the expensive operator). */
+ * (Sec. 3.2: element-wise operators fused with the expensive operator).
+ * With fusion on, an activation NONE whose input is not a graph input and
+ * whose output is not a graph output is an identity and is removed (Sec. 3.1:
+ * graph transformations drop identity operations). */
 mgi_status mgi_graph_add_activation(mgi_graph *g, int in, int act, int *out);
+
+/* Spatial zero padding: output (n, h + pad_t + pad_b, w + pad_l + pad_r, c).
+ * With fusion on, a PAD whose consumers are all conv2d / depthwise ops is
+ * merged into their padding (Sec. 3.1); otherwise it runs as its own kernel.
+ * Pads must be non-negative (MGI_ERR_INVALID_ARG). */
+mgi_status mgi_graph_add_pad(mgi_graph *g, int in, int pad_t, int pad_b, int pad_l, int pad_r,
+                             int *out);
 
 /* Mean over h and w: (n, h, w, c) -> (n, 1, 1, c). */
 mgi_status mgi_graph_add_global_avgpool(mgi_graph *g, int in, int *out);
@@ -154,12 +164,14 @@ mgi_status mgi_graph_add_fc(mgi_graph *g, int in, int cout, const float *w, cons
 /* Softmax over the channel axis: exp(z - max z) / sum exp(z - max z). */
 mgi_status mgi_graph_add_softmax(mgi_graph *g, int in, int *out);
 
-/* Channel concatenation in the given order; all inputs share n, h, w. */
+/* Channel concatenation in the given order; all inputs share n, h, w.  A
+ * single-input concatenation is an identity (removed like activation NONE). */
 mgi_status mgi_graph_add_concat(mgi_graph *g, const int *ins, int count, int *out);
 
 /* Bilinear resize to (oh, ow).  align_corners = 1: source coordinate
  * d * (in - 1) / (out - 1); 0: d * in / out.  The upper neighbour is clamped
- * to the last sample. */
+ * to the last sample.  A resize to the input's own size is an identity
+ * (removed like activation NONE). */
 mgi_status mgi_graph_add_resize_bilinear(mgi_graph *g, int in, int oh, int ow, int align_corners,
                                          int *out);
 

@@ -109,6 +109,19 @@ def activation(x, act):
     return y
 
 
+def zero_pad(x, pads):
+    """Spatial zero padding (Sec. 3.1, PAD): the input is placed at row pt,
+    column pl of an all-zero (n, h + pt + pb, w + pl + pr, c) tensor."""
+    x = _f64(x)
+    pt, pb, pl, pr = pads
+    n, h, w, c = x.shape
+    y = np.zeros((n, h + pt + pb, w + pl + pr, c))
+    for yy in range(h):
+        for xx in range(w):
+            y[:, pt + yy, pl + xx, :] = x[:, yy, xx, :]
+    return y
+
+
 def add(a, b):
     a = _f64(a); b = _f64(b)
     assert a.shape == b.shape
@@ -193,6 +206,10 @@ def tensor_shapes(graph):
             shapes.append(shapes[op["a"]])
         elif k in ("activation", "softmax"):
             shapes.append(shapes[op["in"]])
+        elif k == "pad":
+            n, h, w, c = shapes[op["in"]]
+            pt, pb, pl, pr = op["pads"]
+            shapes.append((n, h + pt + pb, w + pl + pr, c))
         elif k == "gap":
             n, h, w, c = shapes[op["in"]]
             shapes.append((n, 1, 1, c))
@@ -225,7 +242,7 @@ def op_inputs(op):
 
 # ops whose output the paper's engine keeps in fp16 storage (everything but
 # the fp32 logits / probabilities and the integer labels)
-FP16_STORED = {"conv2d", "depthwise", "add", "activation", "gap", "concat", "resize_bilinear"}
+FP16_STORED = {"conv2d", "depthwise", "add", "activation", "gap", "concat", "resize_bilinear", "pad"}
 
 
 def eval_op(op, operands):
@@ -244,6 +261,8 @@ def eval_op(op, operands):
         return activation(add(operands[0], operands[1]), op["act"])
     if k == "activation":
         return activation(operands[0], op["act"])
+    if k == "pad":
+        return zero_pad(operands[0], op["pads"])
     if k == "gap":
         return global_avgpool(operands[0])
     if k == "fc":

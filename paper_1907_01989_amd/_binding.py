@@ -52,6 +52,7 @@ _SIGS = {
     "mgi_graph_add_depthwise": ([P, I, ctypes.POINTER(ConvDesc), FP, FP, IP], I),
     "mgi_graph_add_add": ([P, I, I, I, IP], I),
     "mgi_graph_add_activation": ([P, I, I, IP], I),
+    "mgi_graph_add_pad": ([P, I, I, I, I, I, IP], I),
     "mgi_graph_add_global_avgpool": ([P, I, IP], I),
     "mgi_graph_add_fc": ([P, I, I, FP, FP, IP], I),
     "mgi_graph_add_softmax": ([P, I, IP], I),
@@ -163,6 +164,10 @@ def mgi_graph_add_add(g, a, b, act=ACT_NONE):
 
 def mgi_graph_add_activation(g, x, act):
     return _out(lib().mgi_graph_add_activation, g, x, act)
+
+
+def mgi_graph_add_pad(g, x, pt, pb, pl, pr):
+    return _out(lib().mgi_graph_add_pad, g, x, pt, pb, pl, pr)
 
 
 def mgi_graph_add_global_avgpool(g, x):

@@ -86,6 +86,10 @@ struct DwParams {
 hipError_t launch_depthwise(const DwParams &p, hipStream_t st);
 
 hipError_t launch_add(const h8 *a, const h8 *b, h8 *y, size_t count, int act, hipStream_t st);
+// zero padding of a sliced tensor: (N, H, W) planes of S slices -> (N, OH, OW),
+// input placed at row pt, column pl
+hipError_t launch_pad(const h8 *x, h8 *y, int N, int S, int H, int W, int OH, int OW, int pt, int pl,
+                      hipStream_t st);
 hipError_t launch_act(const h8 *x, h8 *y, size_t count, int act, hipStream_t st);
 hipError_t launch_gap(const h8 *x, h8 *y, const h8 *zero, int N, int HW, int S, hipStream_t st);
 hipError_t launch_softmax(const float *z, float *y, int rows, int cols, hipStream_t st);

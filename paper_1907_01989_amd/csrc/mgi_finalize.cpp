@@ -87,7 +87,91 @@ void pick_pipe_tile(GemmTile &t, size_t M, int npad) {
 
 }  // namespace
 
+namespace {
+
+// Graph transformations before fusion (Sec. 3.1), on a copy of the graph:
+//  - identity removal: an activation NONE, a one-input concatenation or a
+//    resize to the input's own size forwards its input to its consumers.
+//    Identities applied directly to a graph input are kept: they are where the
+//    input is converted to the sliced layout;
+//  - PAD merge: a zero PAD whose consumers are all convolutions (full or
+//    depthwise) is folded into their padding: a convolution over a zero-padded
+//    tensor equals the convolution with the pads added.
+// Graph outputs are never rewritten away.  Tensor ids are unchanged; ops left
+// without consumers are dropped afterwards as dead.
+void clean_graph(mgi_graph &g) {
+    const int nops = (int)g.ops.size();
+    std::vector<char> is_output(nops, 0);
+    for (int t : g.outputs) is_output[t] = 1;
+    std::vector<int> alias(nops);
+    for (int i = 0; i < nops; ++i) alias[i] = i;
+    for (int i = 0; i < nops; ++i) {
+        GOp &op = g.ops[i];
+        for (int &t : op.in) t = alias[t];
+        if (is_output[i] || op.in.empty() || g.ops[op.in[0]].kind == OpKind::Input) continue;
+        const Shape &x = g.ops[op.in[0]].out;
+        const bool identity =
+            (op.kind == OpKind::Activation && op.act == MGI_ACT_NONE) ||
+            (op.kind == OpKind::Concat && op.in.size() == 1) ||
+            (op.kind == OpKind::ResizeBilinear && op.oh == x.h && op.ow == x.w) ||
+            (op.kind == OpKind::Pad && op.pads[0] == 0 && op.pads[1] == 0 && op.pads[2] == 0 &&
+             op.pads[3] == 0);
+        if (identity) alias[i] = op.in[0];
+    }
+    std::vector<std::vector<int>> consumers(nops);
+    for (int i = 0; i < nops; ++i)
+        if (alias[i] == i)
+            for (int t : g.ops[i].in) consumers[t].push_back(i);
+    for (int i = 0; i < nops; ++i) {
+        const GOp &pd = g.ops[i];
+        if (pd.kind != OpKind::Pad || alias[i] != i || is_output[i] || consumers[i].empty()) continue;
+        bool all_conv = true;
+        for (int c : consumers[i]) {
+            const OpKind k = g.ops[c].kind;
+            all_conv = all_conv && (k == OpKind::Conv2d || k == OpKind::Depthwise);
+        }
+        if (!all_conv) continue;
+        for (int c : consumers[i]) {
+            GOp &cv = g.ops[c];
+            cv.conv.pad_t += pd.pads[0];
+            cv.conv.pad_b += pd.pads[1];
+            cv.conv.pad_l += pd.pads[2];
+            cv.conv.pad_r += pd.pads[3];
+            cv.in[0] = pd.in[0];
+        }
+    }
+}
+
+// Ops that some graph output depends on; graph inputs are always kept.
+std::vector<char> live_ops(const mgi_graph &g) {
+    std::vector<char> live(g.ops.size(), 0);
+    std::vector<int> stack(g.outputs.begin(), g.outputs.end());
+    while (!stack.empty()) {
+        const int t = stack.back();
+        stack.pop_back();
+        if (live[t]) continue;
+        live[t] = 1;
+        for (int u : g.ops[t].in) stack.push_back(u);
+    }
+    for (int t : g.inputs) live[t] = 1;
+    return live;
+}
+
+mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p);
+
+}  // namespace
+
 mgi_status build_plan(const mgi_graph &g, const mgi_options &o, mgi_plan &p) {
+    if (g.outputs.empty()) return fail(MGI_ERR_STATE, "mgi_graph_finalize: no output marked");
+    if (!o.fuse) return build_plan_impl(g, o, p);
+    mgi_graph gc = g;
+    clean_graph(gc);
+    return build_plan_impl(gc, o, p);
+}
+
+namespace {
+
+mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p) {
     const int nops = (int)g.ops.size();
     if (g.outputs.empty()) return fail(MGI_ERR_STATE, "mgi_graph_finalize: no output marked");
     if (o.planner != MGI_PLANNER_NAIVE && o.planner != MGI_PLANNER_GREEDY && o.planner != MGI_PLANNER_MCFP)
@@ -95,11 +179,13 @@ mgi_status build_plan(const mgi_graph &g, const mgi_options &o, mgi_plan &p) {
     if (o.dtype != MGI_DTYPE_FP16)
         return fail(MGI_ERR_UNSUPPORTED, "mgi_graph_finalize: only fp16 storage is built");
 
+    const std::vector<char> live = live_ops(g);
     std::vector<char> is_output(nops, 0);
     for (int t : g.outputs) is_output[t] = 1;
     std::vector<std::vector<int>> consumers(nops);
     for (int i = 0; i < nops; ++i)
-        for (int t : g.ops[i].in) consumers[t].push_back(i);
+        if (live[i])
+            for (int t : g.ops[i].in) consumers[t].push_back(i);
 
     // ---------------------------------------------------------------- fusion
     std::vector<int> group_of(nops, -1);
@@ -109,7 +195,7 @@ mgi_status build_plan(const mgi_graph &g, const mgi_options &o, mgi_plan &p) {
     };
     for (int i = 0; i < nops; ++i) {
         const GOp &op = g.ops[i];
-        if (op.kind == OpKind::Input) continue;
+        if (op.kind == OpKind::Input || !live[i]) continue;
         if (o.fuse && op.kind == OpKind::Activation) {
             int t = op.in[0];
             int gi = group_of[t];
@@ -428,6 +514,19 @@ mgi_status build_plan(const mgi_graph &g, const mgi_options &o, mgi_plan &p) {
                 flat_buf[G.last] = nd.out;
                 break;
             }
+            case OpKind::Pad: {
+                int xb = need_c8(op.in[0]);
+                if (xb < 0) xb = c8_buf[op.in[0]];
+                if (xb < 0) return fail(MGI_ERR_UNSUPPORTED, "pad input is not sliced");
+                nd.kind = NodeKind::Pad;
+                nd.kname = "pad";
+                nd.in = {xb};
+                nd.conv.pad_t = op.pads[0];
+                nd.conv.pad_l = op.pads[2];
+                nd.out = new_buf(Layout::C8, out_shape, G.last);
+                c8_buf[G.last] = nd.out;
+                break;
+            }
             case OpKind::Input:
                 break;
         }
@@ -580,6 +679,8 @@ mgi_status build_plan(const mgi_graph &g, const mgi_options &o, mgi_plan &p) {
     p.opt = o;
     return MGI_OK;
 }
+
+}  // namespace
 
 }  // namespace mgi
 

@@ -191,6 +191,26 @@ extern "C" mgi_status mgi_graph_add_activation(mgi_graph *g, int in, int act, in
     return push(g, std::move(op), out);
 }
 
+extern "C" mgi_status mgi_graph_add_pad(mgi_graph *g, int in, int pad_t, int pad_b, int pad_l,
+                                        int pad_r, int *out) {
+    mgi_status s = check_tensor(g, in, "mgi_graph_add_pad");
+    if (s) return s;
+    if (!out) return fail(MGI_ERR_INVALID_ARG, "mgi_graph_add_pad: null pointer");
+    if (pad_t < 0 || pad_b < 0 || pad_l < 0 || pad_r < 0)
+        return fail(MGI_ERR_INVALID_ARG, "mgi_graph_add_pad: pads must be non-negative");
+    GOp op;
+    op.kind = OpKind::Pad;
+    op.in = {in};
+    op.pads[0] = pad_t;
+    op.pads[1] = pad_b;
+    op.pads[2] = pad_l;
+    op.pads[3] = pad_r;
+    op.out = g->ops[in].out;
+    op.out.h += pad_t + pad_b;
+    op.out.w += pad_l + pad_r;
+    return push(g, std::move(op), out);
+}
+
 extern "C" mgi_status mgi_graph_add_global_avgpool(mgi_graph *g, int in, int *out) {
     mgi_status s = check_tensor(g, in, "mgi_graph_add_global_avgpool");
     if (s) return s;

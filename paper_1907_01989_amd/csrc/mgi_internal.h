@@ -21,7 +21,7 @@ namespace mgi {
 
 enum class OpKind {
     Input, Conv2d, Depthwise, Add, Activation, GlobalAvgPool, FC, Softmax, Concat,
-    ResizeBilinear, Argmax
+    ResizeBilinear, Argmax, Pad
 };
 
 struct Shape {
@@ -40,6 +40,7 @@ struct GOp {
     int in_dtype = MGI_DTYPE_FP32;  // Input
     int oh = 0, ow = 0, align_corners = 1;  // ResizeBilinear
     int cout = 0;               // FC
+    int pads[4] = {0, 0, 0, 0}; // Pad: top, bottom, left, right
     std::vector<float> w, b;    // weights as given (OHWI / CHW / COUT x CIN), bias
 };
 
@@ -72,7 +73,7 @@ struct Buf {
 
 enum class NodeKind {
     Ingest, Stem, Gemm, Depthwise, Add, Act, Gap, FC, Softmax, Concat, Resize, Argmax,
-    ResizeArgmax, Export
+    ResizeArgmax, Export, Pad
 };
 
 // Tile shape of the MFMA GEMM (pointwise, implicit-GEMM convolution, FC).

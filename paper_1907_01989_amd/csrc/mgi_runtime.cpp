@@ -125,6 +125,12 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
         case NodeKind::Softmax:
             return launch_softmax((const float *)buf_ptr(p, nd.in[0], B), (float *)y,
                                   (int)os.pixels(), os.c, st);
+        case NodeKind::Pad: {
+            const Buf &ib = p.bufs[nd.in[0]];
+            return launch_pad((const h8 *)buf_ptr(p, nd.in[0], B), (h8 *)y, ib.shape.n,
+                              slices(ib.shape.c), ib.shape.h, ib.shape.w, os.h, os.w, nd.conv.pad_t,
+                              nd.conv.pad_l, st);
+        }
         case NodeKind::Concat: {
             ConcatParams q{};
             q.nin = (int)nd.in.size();

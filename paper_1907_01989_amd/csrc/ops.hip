@@ -199,6 +199,37 @@ hipError_t launch_depthwise(const DwParams &p, hipStream_t st) {
 }
 
 // ---------------------------------------------------------------------------
+// Spatial zero padding of a sliced tensor (a PAD that could not be merged into
+// a convolution): one thread per output element of 16 bytes.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void pad_kernel(const h8 *x, h8 *y, int N, int H, int W, int OH,
+                                                  int OW, int pt, int pl, size_t total) {
+    const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= total) return;
+    const size_t plane = i / ((size_t)OH * OW);
+    const int r = (int)(i - plane * OH * OW);
+    const int oy = r / OW, ox = r - oy * OW;
+    const int iy = oy - pt, ix = ox - pl;
+    h8 v;
+    if (iy >= 0 && iy < H && ix >= 0 && ix < W) {
+        v = x[(plane * H + iy) * W + ix];
+    } else {
+#pragma unroll
+        for (int c = 0; c < 8; ++c) v[c] = (_Float16)0.0f;
+    }
+    y[i] = v;
+}
+
+hipError_t launch_pad(const h8 *x, h8 *y, int N, int S, int H, int W, int OH, int OW, int pt, int pl,
+                      hipStream_t st) {
+    const size_t total = (size_t)S * N * OH * OW;
+    if (!total) return hipSuccess;
+    launch(pad_kernel, dim3(blocks_for(total, 256)), dim3(256), 0, st, x, y, N, H, W, OH, OW, pt, pl,
+           total);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 // element-wise
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void add_kernel(const h8 *a, const h8 *b, h8 *y, size_t n, int act) {

@@ -41,6 +41,8 @@ def build_graph(desc):
                 t = B.mgi_graph_add_add(g, op["a"], op["b"], op["act"])
             elif k == "activation":
                 t = B.mgi_graph_add_activation(g, op["in"], op["act"])
+            elif k == "pad":
+                t = B.mgi_graph_add_pad(g, op["in"], *op["pads"])
             elif k == "gap":
                 t = B.mgi_graph_add_global_avgpool(g, op["in"])
             elif k == "fc":

@@ -15,6 +15,7 @@ import pytest
 import oracle
 import workloads
 from oracle import planner as oplan
+from workloads import ACT_NONE, NetBuilder
 from paper_1907_01989_amd import _binding as B
 from paper_1907_01989_amd import engine
 
@@ -137,6 +138,51 @@ def test_standalone_activation_and_add_fusion():
     pu = engine.Plan(g.graph("t"), fuse=False, bind=False)
     assert [n["kind"] for n in pu.nodes()] == ["ingest", "pw_gemm", "activation", "pw_gemm", "add",
                                                 "export"]
+
+
+def _kinds(desc, **kw):
+    return [n["kind"] for n in engine.Plan(desc, bind=False, **kw).nodes()]
+
+
+def test_identity_removal_and_pad_merge():
+    g = NetBuilder(seed=3)
+    x = g.activation(g.input(2, 9, 9, 16, -1, 1), ACT_NONE)       # kept: the input's layout conversion
+    a = g.conv(x, 32, 1)
+    i1 = g.activation(a, ACT_NONE)                                # a has two consumers: not fusable
+    i2 = g.concat([i1])                                            # one-input concat
+    i3 = g.resize(i2, 9, 9, True)                                  # resize to its own size
+    p1 = g.pad(i3, (0, 1, 0, 1))                                   # TF-style stride-2 padding
+    c1 = g.conv(p1, 24, 3, s=2, pads=(0, 0, 0, 0))
+    p2 = g.pad(a, (1, 1, 1, 1))
+    d1 = g.dw(p2, 3, s=1, pads=(0, 0, 0, 0))
+    y = g.add(g.gap(c1), g.gap(g.conv(g.gap(d1), 24, 1)))
+    g.gap(d1)                                                      # dead: reaches no output
+    g.mark_output(y)
+    desc = g.graph("cleanup")
+    fused = _kinds(desc)
+    assert "pad" not in fused and "concat" not in fused
+    assert fused.count("activation") == 1                          # only the one on the graph input
+    assert "resize_bilinear" not in fused
+    assert fused.count("global_avgpool") == 3                      # the dead pool has no node
+    assert fused.count("conv_igemm") == 1 and fused.count("dw_conv") == 1
+    unfused = _kinds(desc, fuse=False)
+    assert unfused.count("pad") == 2 and "concat" in unfused and "resize_bilinear" in unfused
+    # merged pads leave the convolutions' output shapes unchanged
+    sh = {n["tensor"]: n["shape"] for n in engine.Plan(desc, bind=False).nodes()}
+    ref = oracle.tensor_shapes(desc)
+    for t in (c1, d1):
+        assert sh[t] == tuple(ref[t])
+
+
+def test_pad_that_cannot_merge_runs_as_a_node():
+    g = NetBuilder(seed=4)
+    x = g.activation(g.input(1, 5, 6, 8, -1, 1), ACT_NONE)
+    p = g.pad(x, (1, 2, 0, 3))
+    y = g.add(p, g.pad(x, (1, 2, 0, 3)))
+    g.mark_output(y)
+    kinds = _kinds(g.graph("pad_add"))
+    assert kinds.count("pad") == 2
+    assert err(B.mgi_graph_add_pad, B.mgi_graph_create(), 0, 0, 0, 0, 0) == 1   # no tensor 0
 
 
 @pytest.mark.parametrize("net,key", [("mobilenet_v1", "MobileNet"), ("mobilenet_v2", "MobileNetV2")])

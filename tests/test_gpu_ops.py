@@ -14,7 +14,7 @@ import oracle
 import workloads
 from workloads import ACT_NONE, ACT_RELU, ACT_RELU6, NetBuilder
 
-from gpu_util import check_isolated, labels_check, log, run_gpu
+from gpu_util import check_isolated, check_layer, isolated_reference, labels_check, log, run_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -223,6 +223,48 @@ def test_resize_argmax_fused():
     assert bad == 0 and covered > 0.9, (bad, covered, raw)
     # grid points are exact copies of the input pixels: labels equal the input argmax
     np.testing.assert_array_equal(outs[0][0, ::16, ::16], ref[x].argmax(-1)[0])
+
+
+def test_graph_cleanup_matches_oracle():
+    # identities (activation NONE on a shared tensor, one-input concat,
+    # same-size resize) are removed and both PADs fold into the convolutions
+    # that consume them (Sec. 3.1); results follow the oracle on the graph as
+    # written
+    g = NetBuilder(seed=3)
+    x = sliced(g, g.input(2, 9, 9, 16, -1, 1))
+    a = g.conv(x, 32, 1)
+    i3 = g.resize(g.concat([g.activation(a, ACT_NONE)]), 9, 9, True)
+    c1 = g.conv(g.pad(i3, (0, 1, 0, 1)), 24, 3, s=2, pads=(0, 0, 0, 0))
+    d1 = g.dw(g.pad(a, (1, 1, 1, 1)), 3, s=1, pads=(0, 0, 0, 0))
+    y = g.add(g.gap(c1), g.gap(g.conv(g.gap(d1), 24, 1)))
+    g.mark_output(y)
+    desc = g.graph("cleanup")
+    log("[case] graph cleanup")
+    _, outs, nodes = run_gpu(desc, materialize_all=True)
+    ref = oracle.run_graph(desc)
+    kinds = [n["kind"] for n in __import__("paper_1907_01989_amd.engine", fromlist=["x"]).Plan(desc, bind=False).nodes()]
+    assert "pad" not in kinds and "concat" not in kinds
+    for t in (c1, d1):
+        check_isolated(f"node {t}", nodes[t], isolated_reference(desc, t, nodes))
+    ok, msg = check_layer("output", outs[0], ref[y].reshape(outs[0].shape))
+    assert ok, msg
+
+
+def test_pad_merged_into_stem_and_standalone_pad():
+    g = NetBuilder(seed=11)
+    x = g.input(1, 34, 34, 3, 0, 1, dtype=workloads.DTYPE_FP16)
+    st = g.conv(g.pad(x, (0, 1, 0, 1)), 32, 3, s=2, pads=(0, 0, 0, 0))
+    xs = sliced(g, g.input(2, 5, 6, 12, -1, 1, name="input2"))
+    q = g.add(g.pad(xs, (1, 2, 0, 3)), g.pad(xs, (2, 1, 3, 0)), act=ACT_RELU)
+    g.mark_output(st)
+    g.mark_output(q)
+    desc = g.graph("pads")
+    log("[case] pad into stem + standalone pads")
+    _, outs, nodes = run_gpu(desc, materialize_all=True)
+    ref = oracle.run_graph(desc)
+    check_isolated("stem", nodes[st], ref[st])
+    check_isolated("pad add", nodes[q], ref[q])
+    check_isolated("pad add out", outs[1], ref[q].reshape(outs[1].shape))
 
 
 def test_greedy_and_materialized_runs_agree():

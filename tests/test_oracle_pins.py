@@ -171,6 +171,28 @@ def test_conv_matches_im2col(s, d, pads):
 # ----------------------------------------------------------------------------
 # element-wise, pooling and head operators
 # ----------------------------------------------------------------------------
+def test_zero_pad_hand_values():
+    x = np.array([[1.0, 2.0], [3.0, 4.0]]).reshape(1, 2, 2, 1)
+    y = oracle.zero_pad(x, (1, 0, 0, 2))[0, :, :, 0]
+    np.testing.assert_array_equal(y, [[0, 0, 0, 0], [1, 2, 0, 0], [3, 4, 0, 0]])
+
+
+@pytest.mark.parametrize("pads,s,d", [((1, 1, 1, 1), 1, 1), ((0, 1, 0, 1), 2, 1), ((2, 2, 2, 2), 1, 2),
+                                      ((3, 0, 1, 2), 2, 1)])
+def test_conv_of_zero_padded_input_equals_padded_conv(pads, s, d):
+    # PAD folded into a convolution (Sec. 3.1) is exact: a convolution over a
+    # zero-padded tensor equals the convolution with the pads added
+    x = rnd((2, 7, 6, 5), 31)
+    w = rnd((4, 3, 3, 5), 32)
+    b = rnd(4, 33)
+    direct = oracle.conv2d(x, w, b, (s, s), (d, d), pads)
+    folded = oracle.conv2d(oracle.zero_pad(x, pads), w, b, (s, s), (d, d), (0, 0, 0, 0))
+    np.testing.assert_allclose(folded, direct, rtol=0, atol=1e-12)
+    wd = rnd((5, 3, 3), 34)
+    np.testing.assert_allclose(oracle.depthwise(oracle.zero_pad(x, pads), wd, None, (s, s), (d, d), (0, 0, 0, 0)),
+                               oracle.depthwise(x, wd, None, (s, s), (d, d), pads), rtol=0, atol=1e-12)
+
+
 def test_relu_relu6_hand_values():
     v = np.array([-1.0, 0.0, 3.0, 6.0, 7.5, -0.0, 5.999])
     np.testing.assert_array_equal(oracle.activation(v, 0), v)

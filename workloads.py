@@ -113,11 +113,16 @@ class NetBuilder:
               "act": act, "w": wt, "b": b}
         return self._push(op, (oh, ow, cout))
 
-    def dw(self, x, k=3, s=1, d=1, act=ACT_RELU6, name=None):
+    def dw(self, x, k=3, s=1, d=1, act=ACT_RELU6, name=None, pads=None):
         h, w, c = self._hwc[x]
         idx = len(self.ops)
-        pt, pb, oh = same_pads(h, k, s, d)
-        pl, pr, ow = same_pads(w, k, s, d)
+        if pads is None:
+            pt, pb, oh = same_pads(h, k, s, d)
+            pl, pr, ow = same_pads(w, k, s, d)
+        else:
+            pt, pb, pl, pr = pads
+            oh = (h + pt + pb - d * (k - 1) - 1) // s + 1
+            ow = (w + pl + pr - d * (k - 1) - 1) // s + 1
         rng = rng_for(self.seed, idx)
         wt = he_normal(rng, (c, k, k), k * k)
         b = bias_normal(rng, c)
@@ -133,6 +138,13 @@ class NetBuilder:
     def activation(self, x, act, name=None):
         return self._push({"op": "activation", "name": name or f"act{len(self.ops)}", "in": x,
                            "act": act}, self._hwc[x])
+
+    def pad(self, x, pads, name=None):
+        """Zero padding (top, bottom, left, right) of the spatial dimensions."""
+        h, w, c = self._hwc[x]
+        pt, pb, pl, pr = pads
+        return self._push({"op": "pad", "name": name or f"pad{len(self.ops)}", "in": x,
+                           "pads": tuple(pads)}, (h + pt + pb, w + pl + pr, c))
 
     def gap(self, x, name=None):
         _, _, c = self._hwc[x]
