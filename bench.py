@@ -199,7 +199,7 @@ def roofline_entry(flops, byts, bound, seconds):
 
 
 # ---------------------------------------------------------------------------
-def run_workload(key, steps, warmup, hip, profile_steps=20, detail=True):
+def run_workload(key, steps, warmup, hip, profile_steps=20, detail=True, tune=True):
     import torch
     import workloads
     from paper_1907_01989_amd import _binding as B
@@ -216,6 +216,11 @@ def run_workload(key, steps, warmup, hip, profile_steps=20, detail=True):
     ops_ptrs = [o.data_ptr() for o in outs]
     nodes = plan.nodes()
     nn = len(nodes)
+    if tune:
+        # plan-time tuning of kernel configurations (mgi_plan_autotune), as an
+        # application would do once after loading the model
+        plan.autotune(xs, outs, reps=5, stream=sh)
+    configs = [name for _, _, name in plan.node_configs()]
     for _ in range(warmup):
         B.mgi_plan_run(plan.handle, ins, ops_ptrs, sh)
     torch.cuda.synchronize()
@@ -267,7 +272,8 @@ def run_workload(key, steps, warmup, hip, profile_steps=20, detail=True):
     for i, info in enumerate(nodes):
         fl, by, bound = node_work(desc, nodes, shapes, i)
         name = desc["ops"][info["tensor"]]["name"] if info["tensor"] >= 0 else info["kind"]
-        entry = {"node": i, "name": name, "kind": info["kind"], "us": round(per_node[i] * 1e3, 2)}
+        entry = {"node": i, "name": name, "kind": info["kind"], "config": configs[i],
+                 "us": round(per_node[i] * 1e3, 2)}
         if per_node[i] > 0 and by > 0:
             entry.update({k: v for k, v in roofline_entry(fl, by, bound, per_node[i] * 1e-3).items()
                           if k in ("bound", "frac", "achieved", "unit")})
@@ -288,7 +294,7 @@ def run_workload(key, steps, warmup, hip, profile_steps=20, detail=True):
     return res
 
 
-def run_graph_replay(key, steps, warmup, hip):
+def run_graph_replay(key, steps, warmup, hip, tune=True):
     """The same workload with the launch list captured once as a HIP graph and
     replayed per step (mgi_plan_capture / mgi_plan_replay)."""
     import torch
@@ -299,8 +305,10 @@ def run_graph_replay(key, steps, warmup, hip):
     desc = workloads.WORKLOADS[net](batch)
     plan = engine.Plan(desc)
     xs = plan.input_tensors()
-    plan.capture(xs)
     sh = torch.cuda.current_stream().cuda_stream
+    if tune:
+        plan.autotune(xs, reps=5, stream=sh)
+    plan.capture(xs)
     for _ in range(warmup):
         plan.replay(sh)
     marks = [hip.event() for _ in range(steps + 1)]
@@ -350,6 +358,8 @@ def main():
     ap.add_argument("--workload", default="v1_b64", choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true")
+    ap.add_argument("--no-autotune", action="store_true",
+                    help="keep the finalize-time kernel configurations")
     ap.add_argument("--copy-only", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB, 20 times (the "
                          "reference kernel for scaling HBM traffic counters)")
@@ -376,20 +386,21 @@ def main():
         return
     hip = Hip()
     eprint(f"[bench] workload {args.workload}: warmup {args.warmup}, steps {args.steps}")
-    main_res = run_workload(args.workload, args.steps, args.warmup, hip)
+    tune = not args.no_autotune
+    main_res = run_workload(args.workload, args.steps, args.warmup, hip, tune=tune)
     eprint(f"[bench] {main_res['images_per_s']:.1f} images/s, {main_res['ms_per_step']:.4f} ms/step")
     also = {}
     if not args.no_extra:
         for key in ("v1_b1", "v2_b1", "v1_b64", "v2_b64"):
             if key == args.workload:
                 continue
-            r = run_workload(key, 100, 10, hip, detail=False)
+            r = run_workload(key, 100, 10, hip, detail=False, tune=tune)
             also[key] = {"images_per_s": round(r["images_per_s"], 1),
                          "ms_per_step": round(r["ms_per_step"], 4),
                          "step_ms_device": r["step_ms_device"]}
             eprint(f"[bench] {key}: {r['images_per_s']:.1f} images/s")
         for key in ("v1_b1", "v2_b1", "v1_b64", "v2_b64"):
-            r = run_graph_replay(key, 100, 10, hip)
+            r = run_graph_replay(key, 100, 10, hip, tune=tune)
             also[key + "_graph"] = {"images_per_s": round(r["images_per_s"], 1),
                                     "ms_per_step": round(r["ms_per_step"], 4),
                                     "step_ms_device": r["step_ms_device"]}
@@ -415,7 +426,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": main_res["desc"]["name"], "network": net, "batch": batch,
                    "input": "NHWC fp16 uniform[0,1], device-resident",
-                   "weights": "He-normal seed 0, fp16", "planner": "greedy", "fused": True},
+                   "weights": "He-normal seed 0, fp16", "planner": "greedy", "fused": True,
+                   "autotuned": tune},
         "roofline": main_res["roofline"],
         "cpu_baseline": cpu,
         "per_layer": main_res["layers"],

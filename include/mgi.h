@@ -252,6 +252,31 @@ mgi_status mgi_plan_node_info(const mgi_plan *p, int i, const char **kind, int *
  * and a completed or stream-ordered run. */
 mgi_status mgi_plan_read_node(mgi_plan *p, int i, void *dev_dst, void *stream);
 
+/* Plan-time tuning (after Sec. 4.2, where work-group sizes are chosen by
+ * measurement): runs the plan once with these device buffers (same
+ * arguments and checks as mgi_plan_run), then times every candidate kernel
+ * configuration of each pointwise / implicit-GEMM and depthwise node with
+ * `reps` device-timestamped launches (plus one warm-up) on the plan's own
+ * buffers and keeps the fastest.  All candidates produce bit-identical
+ * results.  Synchronises `stream`; releases a captured graph (capture again
+ * afterwards).  The output buffers hold no defined result afterwards: run the
+ * plan again.  Errors: MGI_ERR_INVALID_ARG for reps outside 1..1000; run
+ * errors; MGI_ERR_HIP if timing fails. */
+mgi_status mgi_plan_autotune(mgi_plan *p, const void *const *dev_inputs, void *const *dev_outputs,
+                             void *stream, int reps);
+
+/* Configuration in use by node i: its index among the node's candidates
+ * (0 = the finalize-time choice), the number of candidates (1 for nodes
+ * without alternatives) and a short name such as "pipe128x64" or "rows4"
+ * (valid while the plan lives). */
+mgi_status mgi_plan_node_config(const mgi_plan *p, int i, int *config, int *n_configs,
+                                const char **name);
+
+/* Use candidate `config` (0 <= config < n_configs) for node i from now on, as
+ * a tuned choice would be; releases a captured graph.  For callers that
+ * tune elsewhere or replay a stored tuning. */
+mgi_status mgi_plan_set_node_config(mgi_plan *p, int i, int config);
+
 /* Record one run with these device inputs and outputs (same arguments and
  * checks as mgi_plan_run) as a HIP graph held by the plan, replacing any
  * earlier one.  Extends the no-synchronisation dispatch of Sec. 3.2: the

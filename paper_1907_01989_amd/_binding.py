@@ -73,6 +73,9 @@ _SIGS = {
     "mgi_plan_run_timed": ([P, ctypes.POINTER(P), ctypes.POINTER(P), P, ctypes.POINTER(P),
                             ctypes.POINTER(P)], I),
     "mgi_plan_capture": ([P, ctypes.POINTER(P), ctypes.POINTER(P)], I),
+    "mgi_plan_autotune": ([P, ctypes.POINTER(P), ctypes.POINTER(P), P, I], I),
+    "mgi_plan_node_config": ([P, I, IP, IP, ctypes.POINTER(ctypes.c_char_p)], I),
+    "mgi_plan_set_node_config": ([P, I, I], I),
     "mgi_plan_replay": ([P, P], I),
     "mgi_plan_node_count": ([P, IP], I),
     "mgi_plan_node_info": ([P, I, ctypes.POINTER(ctypes.c_char_p), IP, IP, IP, IP, IP, IP], I),
@@ -274,6 +277,23 @@ def mgi_plan_capture(p, in_ptrs, out_ptrs):
     ins = (P * max(1, len(in_ptrs)))(*in_ptrs)
     outs = (P * max(1, len(out_ptrs)))(*out_ptrs)
     _check(lib().mgi_plan_capture(p, ins, outs))
+
+
+def mgi_plan_autotune(p, in_ptrs, out_ptrs, stream=None, reps=5):
+    ins = (P * max(1, len(in_ptrs)))(*in_ptrs)
+    outs = (P * max(1, len(out_ptrs)))(*out_ptrs)
+    _check(lib().mgi_plan_autotune(p, ins, outs, P(stream or 0), reps))
+
+
+def mgi_plan_node_config(p, i):
+    cfg, n = ctypes.c_int(), ctypes.c_int()
+    name = ctypes.c_char_p()
+    _check(lib().mgi_plan_node_config(p, i, ctypes.byref(cfg), ctypes.byref(n), ctypes.byref(name)))
+    return cfg.value, n.value, name.value.decode()
+
+
+def mgi_plan_set_node_config(p, i, config):
+    _check(lib().mgi_plan_set_node_config(p, i, config))
 
 
 def mgi_plan_replay(p, stream=None):

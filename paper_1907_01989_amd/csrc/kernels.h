@@ -83,7 +83,8 @@ struct DwParams {
     h8 *y;
     int N, H, W, S, OH, OW, KH, KW, sh, sw, dh, dw, pt, pl, act;
 };
-hipError_t launch_depthwise(const DwParams &p, hipStream_t st);
+// rows: output rows per thread of the 3x3 kernel (1, 2, 4 or 8; 0 = default)
+hipError_t launch_depthwise(const DwParams &p, int rows, hipStream_t st);
 
 hipError_t launch_add(const h8 *a, const h8 *b, h8 *y, size_t count, int act, hipStream_t st);
 // zero padding of a sliced tensor: (N, H, W) planes of S slices -> (N, OH, OW),

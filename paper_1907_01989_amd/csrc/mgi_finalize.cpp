@@ -68,6 +68,70 @@ GemmTile pick_tile(size_t M, int cout) {
 // as that still gives 384 workgroups (1.5 per CU); otherwise the shape with
 // the most workgroups.  Measured on the MobileNet shapes: 128-channel tiles
 // pay off only when many channels share one activation read.
+// Candidate kernel configurations of a node for the autotuner; the first is
+// the configuration finalize picked.  Every candidate accumulates each output
+// in the same order (K ascending in steps of 32 for the GEMMs, taps in window
+// order for depthwise), so they differ in speed only.
+std::string tile_name(const GemmTile &t) {
+    if (t.pipe) return "pipe" + std::to_string(t.bm) + "x" + std::to_string(t.bn);
+    if (t.slab)
+        return "slab" + std::to_string(4 * t.wm) + "x" + std::to_string(t.bn) + "p" + std::to_string(t.pf);
+    return "lds" + std::to_string(t.bm) + "x" + std::to_string(t.bn);
+}
+
+void add_configs(Node &nd, size_t M) {
+    auto push = [&](const GemmTile &t) {
+        for (const Node::Config &c : nd.cfgs)
+            if (c.tile.pipe == t.pipe && c.tile.slab == t.slab && c.tile.bm == t.bm &&
+                c.tile.bn == t.bn && c.tile.wm == t.wm && c.tile.pf == t.pf)
+                return;
+        nd.cfgs.push_back({t, 0, tile_name(t)});
+    };
+    if (nd.kind == NodeKind::Gemm) {
+        push(nd.tile);
+        const int npad = nd.nb16 * 16;
+        if (!nd.taps) {
+            const int pipes[4][2] = {{128, 128}, {128, 64}, {64, 128}, {64, 64}};
+            for (auto &pb : pipes) {
+                if (pb[1] > 64 && npad <= 64) continue;
+                GemmTile t;
+                t.pipe = true;
+                t.bm = pb[0];
+                t.bn = pb[1];
+                push(t);
+            }
+            const int slabs[4][2] = {{32, 32}, {16, 32}, {32, 64}, {16, 64}};
+            for (auto &sb : slabs) {
+                if (sb[1] > 32 && npad <= 32) continue;
+                const size_t lds = (size_t)(sb[1] / 16) * nd.ksp * 256 +
+                                   (size_t)4 * (sb[0] / 16) * (sb[1] / 16) * 1024;
+                if (lds > 65536) continue;
+                GemmTile t;
+                t.slab = true;
+                t.wm = sb[0];
+                t.bn = sb[1];
+                t.pf = nd.ksp >= 8 ? 2 : 1;
+                push(t);
+            }
+        }
+        const int ldss[5][2] = {{128, 128}, {64, 128}, {32, 128}, {64, 64}, {128, 64}};
+        for (auto &lb : ldss) {
+            if (lb[1] > 64 && npad <= 64) continue;
+            GemmTile t;
+            t.bm = lb[0];
+            t.bn = lb[1];
+            push(t);
+        }
+    } else if (nd.kind == NodeKind::Depthwise && nd.conv.kh == 3 && nd.conv.kw == 3 &&
+               nd.conv.stride_h == nd.conv.stride_w && nd.conv.dil_h == nd.conv.dil_w &&
+               nd.conv.stride_h <= 2 && nd.conv.dil_h <= 2) {
+        const int rows[2][3] = {{4, 2, 8}, {2, 1, 4}};
+        for (int r : rows[nd.conv.stride_h - 1]) nd.cfgs.push_back({GemmTile{}, r, "rows" + std::to_string(r)});
+        nd.dw_rows = nd.cfgs[0].dw_rows;
+    }
+    (void)M;
+}
+
 void pick_pipe_tile(GemmTile &t, size_t M, int npad) {
     const int cand[3][2] = {{128, 128}, {128, 64}, {64, 64}};
     size_t best_tiles = 0;
@@ -571,6 +635,8 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
         p.output_shapes.push_back(s);
         p.output_dtypes.push_back(p.bufs[b].layout == Layout::I32 ? MGI_DTYPE_INT32 : MGI_DTYPE_FP32);
     }
+
+    for (Node &nd : p.nodes) add_configs(nd, p.bufs[nd.out].shape.pixels());
 
     // ------------------------------------------------------------ lifetimes
     for (size_t i = 0; i < p.nodes.size(); ++i) {

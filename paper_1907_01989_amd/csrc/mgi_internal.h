@@ -108,6 +108,16 @@ struct Node {
     GemmTile tile;
     mgi_conv_desc conv{};
     int align_corners = 1;
+    int dw_rows = 0;        // depthwise 3x3: output rows per thread (0 = kernel default)
+    // kernel configurations the autotuner may choose from (index 0 = the
+    // finalize-time choice); `cfg` is the one in use
+    struct Config {
+        GemmTile tile;
+        int dw_rows = 0;
+        std::string name;
+    };
+    std::vector<Config> cfgs;
+    int cfg = 0;
 };
 
 }  // namespace mgi

@@ -10,6 +10,8 @@
 #include <cstdint>
 #include <cstring>
 
+#include <algorithm>
+
 #include "kernels.h"
 #include "mgi_internal.h"
 
@@ -108,7 +110,7 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
             q.dh = nd.conv.dil_h; q.dw = nd.conv.dil_w;
             q.pt = nd.conv.pad_t; q.pl = nd.conv.pad_l;
             q.act = nd.act1;
-            return launch_depthwise(q, st);
+            return launch_depthwise(q, nd.dw_rows, st);
         }
         case NodeKind::Add:
             return launch_add((const h8 *)buf_ptr(p, nd.in[0], B), (const h8 *)buf_ptr(p, nd.in[1], B),
@@ -308,6 +310,102 @@ extern "C" mgi_status mgi_plan_replay(mgi_plan *p, void *stream) {
                                   static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "mgi_plan_replay");
     p->last_outputs = p->graph_outputs;
+    return MGI_OK;
+}
+
+// Plan-time tuning, the counterpart of choosing work-group sizes by
+// measurement (Sec. 4.2): every node with more than one candidate
+// configuration is launched reps + 1 times per candidate on the plan's own
+// buffers (after one full run has filled them), each launch timestamped on the
+// device; the fastest (minimum over the timed launches, the first launch being
+// a warm-up) is kept.  Candidates compute identical results, so tuning changes
+// speed only.  A captured graph holds the old configurations and is released.
+extern "C" mgi_status mgi_plan_autotune(mgi_plan *p, const void *const *dev_inputs,
+                                        void *const *dev_outputs, void *stream, int reps) {
+    if (!p) return fail(MGI_ERR_INVALID_ARG, "mgi_plan_autotune: null plan");
+    if (reps < 1 || reps > 1000) return fail(MGI_ERR_INVALID_ARG, "mgi_plan_autotune: reps in 1..1000");
+    mgi_status s = run_plan(p, dev_inputs, dev_outputs, stream, nullptr, nullptr, "mgi_plan_autotune");
+    if (s != MGI_OK) return s;
+    release_graph(*p);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    hipError_t e = hipEventCreate(&e0);
+    if (e == hipSuccess) e = hipEventCreate(&e1);
+    if (e != hipSuccess) {
+        if (e0) hipEventDestroy(e0);
+        return hip_fail(e, "mgi_plan_autotune: events");
+    }
+    Bases B{static_cast<char *>(p->dev_ws), dev_inputs, dev_outputs};
+    LaunchEvents &ev = launch_events();
+    mgi_status result = MGI_OK;
+    for (Node &nd : p->nodes) {
+        if (nd.cfgs.size() < 2) continue;
+        int best = 0;
+        float best_ms = 3.0e38f;
+        for (size_t c = 0; c < nd.cfgs.size() && result == MGI_OK; ++c) {
+            nd.tile = nd.cfgs[c].tile;
+            nd.dw_rows = nd.cfgs[c].dw_rows;
+            float tmin = 3.0e38f;
+            bool usable = true;
+            for (int r = 0; r <= reps; ++r) {
+                ev.start = e0;
+                ev.stop = e1;
+                e = launch_node(*p, nd, B, st);
+                ev.start = ev.stop = nullptr;
+                if (e != hipSuccess) {
+                    usable = false;   // configuration not launchable for this shape
+                    break;
+                }
+                float ms = 0.0f;
+                e = hipEventSynchronize(e1);
+                if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
+                if (e != hipSuccess) {
+                    result = hip_fail(e, "mgi_plan_autotune: timing");
+                    break;
+                }
+                if (r > 0) tmin = std::min(tmin, ms);
+            }
+            if (usable && tmin < best_ms) {
+                best_ms = tmin;
+                best = (int)c;
+            }
+        }
+        nd.cfg = best;
+        nd.tile = nd.cfgs[best].tile;
+        nd.dw_rows = nd.cfgs[best].dw_rows;
+        if (result != MGI_OK) break;
+    }
+    hipEventDestroy(e0);
+    hipEventDestroy(e1);
+    return result;
+}
+
+extern "C" mgi_status mgi_plan_node_config(const mgi_plan *p, int i, int *config, int *n_configs,
+                                           const char **name) {
+    if (!p) return fail(MGI_ERR_INVALID_ARG, "mgi_plan_node_config: null plan");
+    if (i < 0 || i >= (int)p->nodes.size())
+        return fail(MGI_ERR_INVALID_ARG, "mgi_plan_node_config: node index out of range");
+    const Node &nd = p->nodes[i];
+    if (config) *config = nd.cfgs.empty() ? 0 : nd.cfg;
+    if (n_configs) *n_configs = nd.cfgs.empty() ? 1 : (int)nd.cfgs.size();
+    if (name) *name = nd.cfgs.empty() ? nd.kname : nd.cfgs[nd.cfg].name.c_str();
+    return MGI_OK;
+}
+
+extern "C" mgi_status mgi_plan_set_node_config(mgi_plan *p, int i, int config) {
+    if (!p) return fail(MGI_ERR_INVALID_ARG, "mgi_plan_set_node_config: null plan");
+    if (i < 0 || i >= (int)p->nodes.size())
+        return fail(MGI_ERR_INVALID_ARG, "mgi_plan_set_node_config: node index out of range");
+    Node &nd = p->nodes[i];
+    const int n = nd.cfgs.empty() ? 1 : (int)nd.cfgs.size();
+    if (config < 0 || config >= n)
+        return fail(MGI_ERR_INVALID_ARG, "mgi_plan_set_node_config: configuration out of range");
+    if (!nd.cfgs.empty()) {
+        nd.cfg = config;
+        nd.tile = nd.cfgs[config].tile;
+        nd.dw_rows = nd.cfgs[config].dw_rows;
+    }
+    release_graph(*p);
     return MGI_OK;
 }
 

@@ -182,14 +182,20 @@ static hipError_t launch_dw3(const DwParams &p, hipStream_t st) {
     return hipGetLastError();
 }
 
-hipError_t launch_depthwise(const DwParams &p, hipStream_t st) {
+hipError_t launch_depthwise(const DwParams &p, int rows, hipStream_t st) {
     const int ohw = p.OH * p.OW;
     if (ohw <= 0 || p.N <= 0 || p.S <= 0) return hipSuccess;
     if (p.KH == 3 && p.KW == 3 && p.sh == p.sw && p.dh == p.dw) {
-        if (p.sh == 1 && p.dh == 1) return launch_dw3<1, 1, 4>(p, st);
-        if (p.sh == 2 && p.dh == 1) return launch_dw3<2, 1, 2>(p, st);
-        if (p.sh == 1 && p.dh == 2) return launch_dw3<1, 2, 4>(p, st);
-        if (p.sh == 2 && p.dh == 2) return launch_dw3<2, 2, 2>(p, st);
+        // output rows per thread: 4 at stride 1, 2 at stride 2 unless chosen
+        const int R = rows > 0 ? rows : (p.sh == 1 ? 4 : 2);
+#define MGI_DW_CASE(S_, D_, R_) \
+        if (p.sh == S_ && p.dh == D_ && R == R_) return launch_dw3<S_, D_, R_>(p, st);
+        MGI_DW_CASE(1, 1, 2) MGI_DW_CASE(1, 1, 4) MGI_DW_CASE(1, 1, 8)
+        MGI_DW_CASE(2, 1, 1) MGI_DW_CASE(2, 1, 2) MGI_DW_CASE(2, 1, 4)
+        MGI_DW_CASE(1, 2, 2) MGI_DW_CASE(1, 2, 4) MGI_DW_CASE(1, 2, 8)
+        MGI_DW_CASE(2, 2, 1) MGI_DW_CASE(2, 2, 2) MGI_DW_CASE(2, 2, 4)
+#undef MGI_DW_CASE
+        if (rows > 0) return hipErrorInvalidValue;
     }
     const int tpp = (ohw + 255) / 256;
     const size_t nblk = (size_t)tpp * p.S * p.N;

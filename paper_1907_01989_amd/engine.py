@@ -132,6 +132,18 @@ class Plan:
                        [y.data_ptr() for y in outputs], _stream_handle(stream))
         return outputs
 
+    def autotune(self, inputs, outputs=None, reps=5, stream=None):
+        """Time every candidate kernel configuration per node on these buffers
+        and keep the fastest (see mgi_plan_autotune); synchronises."""
+        if outputs is None:
+            outputs = self.alloc_outputs()
+        B.mgi_plan_autotune(self.handle, [x.data_ptr() for x in inputs], [y.data_ptr() for y in outputs],
+                            _stream_handle(stream), reps)
+        self._graph_io = None
+
+    def node_configs(self):
+        return [B.mgi_plan_node_config(self.handle, i) for i in range(B.mgi_plan_node_count(self.handle))]
+
     def capture(self, inputs, outputs=None):
         """Record one run over these tensors as a HIP graph (see replay); the
         tensors stay referenced by the plan so that their memory outlives it."""

@@ -98,6 +98,8 @@ def test_finalize_state_errors_and_run_before_bind():
     try:
         assert err(B.mgi_plan_run, p, [1], [1]) == 4        # not bound
         assert err(B.mgi_plan_capture, p, [1], [1]) == 4    # not bound
+        assert err(B.mgi_plan_autotune, p, [1], [1], None, 0) == 1   # reps out of range
+        assert err(B.mgi_plan_autotune, p, [1], [1], None, 3) == 4   # not bound
         assert err(B.mgi_plan_replay, p) == 4               # nothing captured
         assert err(B.mgi_plan_bind, p, 0, 0) == 5           # no buffers
         assert err(B.mgi_plan_bind, p, 0x1001, 0x2000) == 5  # misaligned
@@ -172,6 +174,28 @@ def test_identity_removal_and_pad_merge():
     ref = oracle.tensor_shapes(desc)
     for t in (c1, d1):
         assert sh[t] == tuple(ref[t])
+
+
+def test_node_configuration_candidates():
+    # every pointwise GEMM and 3x3 depthwise node offers several kernel
+    # configurations; index 0 is the finalize-time choice
+    d = workloads.WORKLOADS["mobilenet_v2"](2)
+    pl = engine.Plan(d, bind=False)
+    nodes = pl.nodes()
+    cfgs = pl.node_configs()
+    for n, (c, k, name) in zip(nodes, cfgs):
+        assert c == 0
+        if n["kind"] == "pw_gemm":
+            assert k >= 5 and name.startswith(("pipe", "slab", "lds"))
+        elif n["kind"] == "dw_conv":
+            assert k == 3 and name.startswith("rows")
+        else:
+            assert k == 1
+    i = next(j for j, n in enumerate(nodes) if n["kind"] == "pw_gemm")
+    B.mgi_plan_set_node_config(pl.handle, i, 2)
+    assert pl.node_configs()[i][0] == 2
+    assert err(B.mgi_plan_set_node_config, pl.handle, i, 99) == 1
+    assert err(B.mgi_plan_set_node_config, pl.handle, 9999, 0) == 1
 
 
 def test_pad_that_cannot_merge_runs_as_a_node():
