@@ -139,6 +139,19 @@ def node_work(desc, nodes, shapes, i):
         byts = in_bytes + out_b + op["w"].size * 2 + op["b"].size * 4
         if h != t:
             byts += out_b          # fused residual operand
+    elif kind == "dw_pw":
+        # depthwise input in, pointwise output out; the intermediate tensor
+        # never reaches memory
+        d = head_of(op["in"])
+        dop = ops[d]
+        n, oh, ow, cout = shapes[t]
+        m = n * oh * ow
+        cin = op["w"].shape[-1]
+        flops = 2.0 * m * cin * cout + 2.0 * m * cin * dop["kh"] * dop["kw"]
+        byts = (elems(dop["in"]) * 2 + out_b + op["w"].size * 2 + op["b"].size * 4 +
+                dop["w"].size * 2 + dop["b"].size * 4)
+        if h != t:
+            byts += out_b          # fused residual operand
     elif kind == "dw_conv":
         flops = 2.0 * elems(t) * op["kh"] * op["kw"]
         byts = elems(op["in"]) * 2 + out_b + op["w"].size * 4 + op["b"].size * 4
@@ -165,7 +178,7 @@ def kernel_sources_hash():
     while the kernels it was measured on are unchanged."""
     import hashlib
     h = hashlib.sha1()
-    for f in ("gemm.hip", "ops.hip", "kernels.h"):
+    for f in ("gemm.hip", "ops.hip", "dwpw.hip", "device.h", "kernels.h"):
         with open(os.path.join(ROOT, "paper_1907_01989_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -199,7 +212,7 @@ def roofline_entry(flops, byts, bound, seconds):
 
 
 # ---------------------------------------------------------------------------
-def run_workload(key, steps, warmup, hip, profile_steps=20, detail=True, tune=True):
+def run_workload(key, steps, warmup, hip, profile_steps=20, detail=True, tune=True, fuse_dwpw=False):
     import torch
     import workloads
     from paper_1907_01989_amd import _binding as B
@@ -207,7 +220,7 @@ def run_workload(key, steps, warmup, hip, profile_steps=20, detail=True, tune=Tr
 
     net, batch = WORKLOADS[key]
     desc = workloads.WORKLOADS[net](batch)
-    plan = engine.Plan(desc)
+    plan = engine.Plan(desc, fuse_dwpw=fuse_dwpw)
     xs = plan.input_tensors()
     outs = plan.alloc_outputs()
     stream = torch.cuda.current_stream()
@@ -358,6 +371,9 @@ def main():
     ap.add_argument("--workload", default="v1_b64", choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true")
+    ap.add_argument("--fuse-dwpw", action="store_true",
+                    help="fuse 3x3 depthwise convolutions into the pointwise convolutions "
+                         "that consume them (mgi_options.fuse_dwpw)")
     ap.add_argument("--no-autotune", action="store_true",
                     help="keep the finalize-time kernel configurations")
     ap.add_argument("--copy-only", type=int, default=0, metavar="MIB",
@@ -387,7 +403,8 @@ def main():
     hip = Hip()
     eprint(f"[bench] workload {args.workload}: warmup {args.warmup}, steps {args.steps}")
     tune = not args.no_autotune
-    main_res = run_workload(args.workload, args.steps, args.warmup, hip, tune=tune)
+    main_res = run_workload(args.workload, args.steps, args.warmup, hip, tune=tune,
+                            fuse_dwpw=args.fuse_dwpw)
     eprint(f"[bench] {main_res['images_per_s']:.1f} images/s, {main_res['ms_per_step']:.4f} ms/step")
     also = {}
     if not args.no_extra:
@@ -427,7 +444,7 @@ def main():
         "config": {"workload": main_res["desc"]["name"], "network": net, "batch": batch,
                    "input": "NHWC fp16 uniform[0,1], device-resident",
                    "weights": "He-normal seed 0, fp16", "planner": "greedy", "fused": True,
-                   "autotuned": tune},
+                   "autotuned": tune, "dw_pw_fused": args.fuse_dwpw},
         "roofline": main_res["roofline"],
         "cpu_baseline": cpu,
         "per_layer": main_res["layers"],

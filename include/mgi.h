@@ -99,6 +99,11 @@ typedef struct {
     int materialize_all; /* 1: every node output keeps its own buffer so that
                             mgi_plan_read_node works after a run (default 0) */
     int dtype;           /* storage type of activations and weights: FP16 (default) */
+    int fuse_dwpw;       /* 1: run a 3x3 depthwise convolution (stride 1 or 2, no dilation)
+                            inside the pointwise convolution that alone consumes it, when
+                            that convolution has at most 320 output channels and enough
+                            pixels to fill the GPU; the depthwise output then never reaches
+                            memory (default 0; needs fuse = 1) */
 } mgi_options;
 
 /* ---------------------------------------------------------------------------

@@ -32,7 +32,8 @@ class ConvDesc(ctypes.Structure):
 
 class Options(ctypes.Structure):
     _fields_ = [("planner", ctypes.c_int), ("fuse", ctypes.c_int),
-                ("materialize_all", ctypes.c_int), ("dtype", ctypes.c_int)]
+                ("materialize_all", ctypes.c_int), ("dtype", ctypes.c_int),
+                ("fuse_dwpw", ctypes.c_int)]
 
 
 _lib = None
@@ -92,6 +93,15 @@ def lib():
         if not os.path.exists(LIB_PATH):
             raise ImportError(f"{LIB_PATH} is missing: build it with "
                               "`python -m paper_1907_01989_amd.build_lib`")
+        # One HIP runtime per process: PyTorch-ROCm carries its own copy of
+        # the HIP runtime, and the device buffers and streams handed to the
+        # library come from it.  Loading the library first would bind it to
+        # the system copy and give the process two runtimes, in which the
+        # library's calls find no device.
+        try:
+            import torch  # noqa: F401
+        except ImportError:
+            pass
         L = ctypes.CDLL(LIB_PATH)
         for name, (args, res) in _SIGS.items():
             f = getattr(L, name)

@@ -19,37 +19,11 @@
 // step's global loads issued before the current step's MFMAs.
 #include <cmath>
 
-#include "kernels.h"
+#include "device.h"
 
 namespace mgi {
 namespace kern {
 
-typedef float f4 __attribute__((ext_vector_type(4)));
-
-// Activation as one clamp (v_med3_f32): [lo, hi] = (-inf, inf) for none,
-// (0, inf) for ReLU, (0, 6) for ReLU6; act is uniform, so lo and hi are
-// computed once per kernel.
-__device__ __forceinline__ float act_apply(float v, int act) {
-    const float lo = act == MGI_ACT_NONE ? -INFINITY : 0.0f;
-    const float hi = act == MGI_ACT_RELU6 ? 6.0f : INFINITY;
-    return __builtin_amdgcn_fmed3f(v, lo, hi);
-}
-
-__device__ __forceinline__ h8 zero_h8() {
-    h8 z;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) z[i] = (_Float16)0.0f;
-    return z;
-}
-
-// Workgroups are dispatched to the 8 XCDs round-robin (block b -> XCD b % 8).
-// Give every XCD a contiguous range of tiles so that tiles sharing input rows
-// (same pixel block, neighbouring channel blocks) meet in the same L2.
-__device__ __forceinline__ int xcd_tile(int bid, int nblocks) {
-    const int xcd = bid & 7, idx = bid >> 3;
-    const int per = nblocks >> 3, rem = nblocks & 7;
-    return xcd * per + min(xcd, rem) + idx;
-}
 
 template <int BM, int BN, bool TAPS, bool F32OUT>
 __global__ __launch_bounds__(256) void gemm_kernel(GemmParams p) {
@@ -234,58 +208,6 @@ hipError_t launch_gemm(const GemmParams &p, int bm, int bn, bool taps, bool f32o
 }
 
 // ---------------------------------------------------------------------------
-// Coalesced epilogue.  An MFMA accumulator gives a lane 4 channels of one
-// pixel (half of a 16-byte sliced element, the other half in lane l+16);
-// storing that directly makes every quarter-wave write half-masked 64-byte
-// pieces, which costs several times the bandwidth of whole lines.  Instead
-// each wave parks act1(acc + bias) in its own LDS tile
-// [2*FN slices][16*FM pixels][8] fp32, then re-reads it so that consecutive
-// lanes own consecutive pixels of one slice: residual reads and output writes
-// are whole 16-byte elements, 1 KiB per wave instruction.  No barrier: a wave
-// reads back only what it wrote.
-// ---------------------------------------------------------------------------
-template <int FM, int FN>
-__device__ __forceinline__ void store_tile_c8(const GemmParams &p, const f4 (&acc)[FN][FM], int m0,
-                                              int nb0, float *stage, int lane) {
-    constexpr int NPIX = 16 * FM, NSL = 2 * FN;
-#pragma unroll
-    for (int i = 0; i < FN; ++i) {
-        const int nbase = (nb0 + i) * 16 + 4 * (lane >> 4);
-        float bv[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) bv[r] = p.bias[min(nbase, p.nb16 * 16 - 4) + r];
-        const int sl = 2 * i + ((lane >> 4) >> 1), half = 4 * ((lane >> 4) & 1);
-#pragma unroll
-        for (int j = 0; j < FM; ++j) {
-            f4 v;
-#pragma unroll
-            for (int r = 0; r < 4; ++r) v[r] = act_apply(acc[i][j][r] + bv[r], p.act1);
-            *(f4 *)(stage + ((sl * NPIX) + j * 16 + (lane & 15)) * 8 + half) = v;
-        }
-    }
-    __builtin_amdgcn_wave_barrier();
-#pragma unroll
-    for (int t = 0; t < (NSL * NPIX) / 64; ++t) {
-        const int e = lane + 64 * t;
-        const int sl = e / NPIX, px = e - sl * NPIX;
-        const int os = nb0 * 2 + sl, m = m0 + px;
-        if (os >= p.ns || m >= p.M) continue;
-        const f4 lo = *(const f4 *)(stage + e * 8), hi = *(const f4 *)(stage + e * 8 + 4);
-        float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-        const size_t off = (size_t)os * p.M + m;
-        if (p.res) {
-            const h8 rv = p.res[off];
-#pragma unroll
-            for (int r = 0; r < 8; ++r) v[r] = act_apply(v[r] + (float)rv[r], p.act2);
-        }
-        h8 o;
-#pragma unroll
-        for (int r = 0; r < 8; ++r) o[r] = (_Float16)v[r];
-        ((h8 *)p.y)[off] = o;
-    }
-}
-
-// ---------------------------------------------------------------------------
 // Pointwise GEMM, weight-slab variant.  The tile's whole weight slab
 // (BN channels x all K, at most 64 KiB) is loaded into LDS once, behind one
 // barrier; each of the 4 waves then owns WM pixels and all BN channels, and
@@ -426,25 +348,6 @@ hipError_t launch_gemm_xs(const GemmParams &p, int wm, int bn, int pf, hipStream
 // ahead into the slot freed by the previous iteration, and runs its MFMAs.
 // The loop is unrolled by NST so every slot is a compile-time choice.
 // ---------------------------------------------------------------------------
-// 16 bytes per lane from global memory straight into LDS: lane l writes
-// lds + 16*l, so the LDS side is one contiguous KiB per wave.  Issued as
-// inline asm so that the compiler does not track it: it would otherwise
-// conservatively wait for every such load before any LDS read it cannot
-// prove independent (at loop heads it cannot), serialising the ring.  The
-// loads are ordered by explicit s_waitcnt + s_barrier instead.
-__device__ __forceinline__ void load_lds16(const h8 *src, const h8 *lds) {
-    const unsigned la = (unsigned)(size_t)(__attribute__((address_space(3))) const void *)lds;
-    asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(la) : "memory");
-}
-
-// wait until at most N vector-memory instructions of this wave are in flight
-// and all of its LDS reads have returned (expcnt left at its maximum)
-template <int N>
-__device__ __forceinline__ void wait_vm_lds() {
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4));
-}
-
 template <int BM, int BN>
 struct PipeTile {
     static constexpr int KS = 4, NST = 4;

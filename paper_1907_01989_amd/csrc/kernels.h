@@ -59,6 +59,22 @@ hipError_t launch_gemm_pipe(const GemmParams &p, int bm, int bn, hipStream_t st)
 hipError_t launch_fc(const GemmParams &p, hipStream_t st);
 size_t gemm_xs_lds_bytes(int ksp, int wm, int bn);
 
+// Depthwise 3x3 (stride 1 or 2, dilation 1) fused into the pointwise GEMM
+// that consumes it: x is the depthwise input (sliced, N*H*W pixels per
+// slice, K = g.ksl slices), g describes the pointwise GEMM (g.x unused).
+struct DwPwParams {
+    const h8 *x;
+    const h8 *dww;       // fp16 taps [ksl][9][8]
+    const float *dwb;    // [ksl * 8]
+    const h8 *zero;      // one zeroed element
+    int N, H, W, OH, OW, sh, sw, pt, pl, act;
+    GemmParams g;
+};
+// bm: 64 or 128 pixels per workgroup; g.nb16 <= 20
+hipError_t launch_dwpw(const DwPwParams &p, int bm, hipStream_t st);
+// channel blocks the kernel instance computes for nb16 output blocks (0: too many)
+int dwpw_blocks(int nb16);
+
 // Direct convolution of a small-channel NHWC graph input (kh*kw*c <= 32).
 struct StemParams {
     const void *x;       // NHWC fp32 or fp16

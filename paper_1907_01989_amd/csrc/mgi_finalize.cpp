@@ -22,6 +22,7 @@
 #include <cstring>
 #include <new>
 
+#include "kernels.h"
 #include "mgi_internal.h"
 
 namespace mgi {
@@ -122,6 +123,14 @@ void add_configs(Node &nd, size_t M) {
             t.bn = lb[1];
             push(t);
         }
+    } else if (nd.kind == NodeKind::DwPw) {
+        for (int bm : {nd.tile.bm, 128, 64}) {
+            GemmTile t;
+            t.bm = bm;
+            bool dup = false;
+            for (const Node::Config &c : nd.cfgs) dup = dup || c.tile.bm == bm;
+            if (!dup) nd.cfgs.push_back({t, 0, "dwpw" + std::to_string(bm)});
+        }
     } else if (nd.kind == NodeKind::Depthwise && nd.conv.kh == 3 && nd.conv.kw == 3 &&
                nd.conv.stride_h == nd.conv.stride_w && nd.conv.dil_h == nd.conv.dil_w &&
                nd.conv.stride_h <= 2 && nd.conv.dil_h <= 2) {
@@ -130,6 +139,51 @@ void add_configs(Node &nd, size_t M) {
         nd.dw_rows = nd.cfgs[0].dw_rows;
     }
     (void)M;
+}
+
+// Depthwise -> pointwise fusion (Sec. 3.2's fusion extended to the
+// depthwise-separable pair): a 3x3 depthwise node (stride 1 or 2, dilation 1)
+// whose output only feeds one pointwise GEMM with at most 320 output channels
+// becomes part of that GEMM's node, when the GEMM's pixels still give at least
+// 256 workgroups of 64 (or 512 of 128); the intermediate buffer is dropped.
+void fuse_dw_into_pw(mgi_plan &p) {
+    std::vector<int> readers(p.bufs.size(), 0), producer(p.bufs.size(), -1);
+    for (size_t i = 0; i < p.nodes.size(); ++i) {
+        const Node &nd = p.nodes[i];
+        for (int b : nd.in) readers[b]++;
+        if (nd.residual >= 0) readers[nd.residual]++;
+        producer[nd.out] = (int)i;
+    }
+    std::vector<char> drop(p.nodes.size(), 0);
+    for (Node &pw : p.nodes) {
+        if (pw.kind != NodeKind::Gemm || pw.taps || pw.in.empty()) continue;
+        const int mid = pw.in[0];
+        if (readers[mid] != 1 || p.bufs[mid].loc != Loc::Arena || producer[mid] < 0) continue;
+        Node &dw = p.nodes[producer[mid]];
+        const mgi_conv_desc &c = dw.conv;
+        if (dw.kind != NodeKind::Depthwise || c.kh != 3 || c.kw != 3 || c.stride_h != c.stride_w ||
+            c.stride_h > 2 || c.dil_h != 1 || c.dil_w != 1)
+            continue;
+        if (kern::dwpw_blocks(pw.nb16) == 0) continue;
+        const size_t M = p.bufs[pw.out].shape.pixels();
+        const int bm = M / 128 >= 512 ? 128 : (M / 64 >= 256 ? 64 : 0);
+        if (!bm) continue;
+        pw.kind = NodeKind::DwPw;
+        pw.kname = "dw_pw";
+        pw.dw_op = dw.op;
+        pw.dw_conv = dw.conv;
+        pw.dw_act = dw.act1;
+        pw.in[0] = dw.in[0];
+        pw.n_fused += dw.n_fused;
+        pw.tile = GemmTile{};
+        pw.tile.bm = bm;
+        p.bufs[mid].dead = true;
+        drop[producer[mid]] = 1;
+    }
+    std::vector<Node> kept;
+    for (size_t i = 0; i < p.nodes.size(); ++i)
+        if (!drop[i]) kept.push_back(std::move(p.nodes[i]));
+    p.nodes.swap(kept);
 }
 
 void pick_pipe_tile(GemmTile &t, size_t M, int npad) {
@@ -636,6 +690,7 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
         p.output_dtypes.push_back(p.bufs[b].layout == Layout::I32 ? MGI_DTYPE_INT32 : MGI_DTYPE_FP32);
     }
 
+    if (o.fuse && o.fuse_dwpw) fuse_dw_into_pw(p);
     for (Node &nd : p.nodes) add_configs(nd, p.bufs[nd.out].shape.pixels());
 
     // ------------------------------------------------------------ lifetimes
@@ -651,7 +706,7 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
     std::vector<size_t> sizes;
     std::vector<int> first, last;
     for (size_t b = 0; b < p.bufs.size(); ++b) {
-        if (p.bufs[b].loc != Loc::Arena) continue;
+        if (p.bufs[b].loc != Loc::Arena || p.bufs[b].dead) continue;
         arena.push_back((int)b);
         sizes.push_back(p.bufs[b].bytes);
         first.push_back(p.bufs[b].producer);
@@ -693,7 +748,21 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
     p.zero_off = reserve(256);  // zeroed block read by kernels for out-of-range taps
     for (Node &nd : p.nodes) {
         const GOp &op = g.ops[nd.op >= 0 ? nd.op : 0];
-        if (nd.kind == NodeKind::Gemm || nd.kind == NodeKind::Stem || nd.kind == NodeKind::FC) {
+        if (nd.kind == NodeKind::DwPw) {
+            // depthwise taps of the absorbed op, laid out as for a depthwise node
+            const GOp &dop = g.ops[nd.dw_op];
+            const int c = dop.out.c, S = slices(c);
+            nd.dw_w_off = reserve((size_t)S * 9 * 8 * 2);
+            uint16_t *wp = reinterpret_cast<uint16_t *>(blob.data() + nd.dw_w_off);
+            for (int ch = 0; ch < c; ++ch)
+                for (int t = 0; t < 9; ++t)
+                    wp[((size_t)(ch / 8) * 9 + t) * 8 + ch % 8] = f32_to_f16_bits(dop.w[(size_t)ch * 9 + t]);
+            nd.dw_b_off = reserve((size_t)S * 8 * 4);
+            float *bp = reinterpret_cast<float *>(blob.data() + nd.dw_b_off);
+            for (int ch = 0; ch < c; ++ch) bp[ch] = dop.b[ch];
+        }
+        if (nd.kind == NodeKind::Gemm || nd.kind == NodeKind::Stem || nd.kind == NodeKind::FC ||
+            nd.kind == NodeKind::DwPw) {
             const Shape x = g.ops[op.in[0]].out;
             const int cin = x.c;
             const int cout = nd.kind == NodeKind::FC ? op.cout : op.conv.cout;

@@ -68,12 +68,13 @@ struct Buf {
     int producer = -1;       // node index (-1: graph input)
     int last_use = -1;       // last node index that reads it (-1: none)
     int graph_tensor = -1;   // graph tensor id it holds (-1: internal)
+    bool dead = false;       // no longer produced or read (fused away); not planned
     int in_dtype = MGI_DTYPE_FP32;  // element type of a NHWC_IN buffer
 };
 
 enum class NodeKind {
     Ingest, Stem, Gemm, Depthwise, Add, Act, Gap, FC, Softmax, Concat, Resize, Argmax,
-    ResizeArgmax, Export, Pad
+    ResizeArgmax, Export, Pad, DwPw
 };
 
 // Tile shape of the MFMA GEMM (pointwise, implicit-GEMM convolution, FC).
@@ -109,6 +110,11 @@ struct Node {
     mgi_conv_desc conv{};
     int align_corners = 1;
     int dw_rows = 0;        // depthwise 3x3: output rows per thread (0 = kernel default)
+    // DwPw: the absorbed depthwise op, its window, activation and packed taps
+    int dw_op = -1;
+    mgi_conv_desc dw_conv{};
+    int dw_act = MGI_ACT_NONE;
+    size_t dw_w_off = 0, dw_b_off = 0;
     // kernel configurations the autotuner may choose from (index 0 = the
     // finalize-time choice); `cfg` is the one in use
     struct Config {

@@ -96,6 +96,28 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
             if (nd.tile.slab) return launch_gemm_xs(q, nd.tile.wm, nd.tile.bn, nd.tile.pf, st);
             return launch_gemm(q, nd.tile.bm, nd.tile.bn, nd.taps, nd.kind == NodeKind::FC, st);
         }
+        case NodeKind::DwPw: {
+            const Buf &ib = p.bufs[nd.in[0]];
+            DwPwParams q{};
+            q.x = (const h8 *)buf_ptr(p, nd.in[0], B);
+            q.dww = (const h8 *)(wbase + nd.dw_w_off);
+            q.dwb = (const float *)(wbase + nd.dw_b_off);
+            q.zero = (const h8 *)(wbase + p.zero_off);
+            q.N = ib.shape.n; q.H = ib.shape.h; q.W = ib.shape.w; q.OH = os.h; q.OW = os.w;
+            q.sh = nd.dw_conv.stride_h; q.sw = nd.dw_conv.stride_w;
+            q.pt = nd.dw_conv.pad_t; q.pl = nd.dw_conv.pad_l; q.act = nd.dw_act;
+            GemmParams &g = q.g;
+            g.w = (const h8 *)(wbase + nd.w_off);
+            g.bias = (const float *)(wbase + nd.b_off);
+            g.res = nd.residual >= 0 ? (const h8 *)buf_ptr(p, nd.residual, B) : nullptr;
+            g.y = y;
+            g.M = (int)os.pixels();
+            g.Min = g.M;
+            g.ksl = nd.ksl; g.ksp = nd.ksp;
+            g.nb16 = nd.nb16; g.ns = slices(os.c); g.cout = os.c;
+            g.act1 = nd.act1; g.act2 = nd.act2;
+            return launch_dwpw(q, nd.tile.bm, st);
+        }
         case NodeKind::Depthwise: {
             const Buf &ib = p.bufs[nd.in[0]];
             DwParams q{};

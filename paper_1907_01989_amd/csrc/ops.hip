@@ -11,26 +11,10 @@
 #include <cmath>
 #include <cstdint>
 
-#include "kernels.h"
+#include "device.h"
 
 namespace mgi {
 namespace kern {
-
-// Activation as one clamp (v_med3_f32): [lo, hi] = (-inf, inf) for none,
-// (0, inf) for ReLU, (0, 6) for ReLU6; act is uniform, so lo and hi are
-// computed once per kernel.
-__device__ __forceinline__ float act_apply(float v, int act) {
-    const float lo = act == MGI_ACT_NONE ? -INFINITY : 0.0f;
-    const float hi = act == MGI_ACT_RELU6 ? 6.0f : INFINITY;
-    return __builtin_amdgcn_fmed3f(v, lo, hi);
-}
-
-__device__ __forceinline__ h8 zero_h8() {
-    h8 z;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) z[i] = (_Float16)0.0f;
-    return z;
-}
 
 static inline unsigned blocks_for(size_t n, int per) { return (unsigned)((n + per - 1) / per); }
 
@@ -51,33 +35,6 @@ LaunchEvents &launch_events() {
 // Launch: 1-D, thread g -> column g % OW, strip (g / OW) % nstrips, plane
 // g / (OW * nstrips) (plane = slice * N + image).
 // ---------------------------------------------------------------------------
-// v_fma_mix_f32: fp32 acc += fp16 a * fp16 b, both halves taken from the same
-// position (low or high) of a packed pair; the product of two fp16 values is
-// exact in fp32, so this equals fmaf((float)a, (float)b, acc) with no
-// conversion instructions.
-template <int HI>
-__device__ __forceinline__ void fma_mix(float &acc, uint32_t a, uint32_t b) {
-    if (HI)
-        asm volatile("v_fma_mix_f32 %0, %1, %2, %0 op_sel:[1,1,0] op_sel_hi:[1,1,0]"
-                     : "+v"(acc) : "v"(a), "v"(b));
-    else
-        asm volatile("v_fma_mix_f32 %0, %1, %2, %0 op_sel:[0,0,0] op_sel_hi:[1,1,0]"
-                     : "+v"(acc) : "v"(a), "v"(b));
-}
-
-typedef uint32_t u4x __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ u4x as_u4(h8 v) { return __builtin_bit_cast(u4x, v); }
-
-// acc[0..7] += w * v channel-wise, w and v fp16 x 8
-__device__ __forceinline__ void fma8(float *acc, u4x w, u4x v) {
-#pragma unroll
-    for (int d = 0; d < 4; ++d) {
-        fma_mix<0>(acc[2 * d], w[d], v[d]);
-        fma_mix<1>(acc[2 * d + 1], w[d], v[d]);
-    }
-}
-
 template <int S_, int D_, int R>
 __global__ __launch_bounds__(256) void dw3_kernel(DwParams p, int nstrips) {
     constexpr int NR = (R - 1) * S_ + 2 * D_ + 1;

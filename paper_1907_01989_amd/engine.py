@@ -68,11 +68,12 @@ def build_graph(desc):
     return g
 
 
-def options(planner=B.PLANNER_GREEDY, fuse=True, materialize_all=False):
+def options(planner=B.PLANNER_GREEDY, fuse=True, materialize_all=False, fuse_dwpw=False):
     o = B.mgi_options_default()
     o.planner = planner
     o.fuse = int(fuse)
     o.materialize_all = int(materialize_all)
+    o.fuse_dwpw = int(fuse_dwpw)
     return o
 
 
@@ -80,11 +81,11 @@ class Plan:
     """A finalised, device-bound network."""
 
     def __init__(self, desc, planner=B.PLANNER_GREEDY, fuse=True, materialize_all=False,
-                 device="cuda:0", bind=True):
+                 device="cuda:0", bind=True, fuse_dwpw=False):
         self.desc = desc
         g = build_graph(desc)
         try:
-            self.handle = B.mgi_graph_finalize(g, options(planner, fuse, materialize_all))
+            self.handle = B.mgi_graph_finalize(g, options(planner, fuse, materialize_all, fuse_dwpw))
         finally:
             B.mgi_graph_destroy(g)
         self.device = device

@@ -29,11 +29,13 @@ def to_numpy(t):
     return t.detach().cpu().numpy()
 
 
-def run_gpu(desc, materialize_all=True, fuse=True, planner=None):
+def run_gpu(desc, materialize_all=True, fuse=True, planner=None, fuse_dwpw=False):
     """Run ``desc`` once; returns (plan, outputs as numpy, {tensor id: node output})."""
     import torch
     from paper_1907_01989_amd import engine, _binding as B
-    kw = {} if planner is None else {"planner": planner}
+    kw = {"fuse_dwpw": fuse_dwpw}
+    if planner is not None:
+        kw["planner"] = planner
     plan = engine.Plan(desc, fuse=fuse, materialize_all=materialize_all, **kw)
     xs = plan.input_tensors()
     outs = plan.run(xs)
