@@ -93,10 +93,12 @@ __device__ __forceinline__ void wait_vm_lds() {
 // are whole 16-byte elements, 1 KiB per wave instruction.  No barrier: a wave
 // reads back only what it wrote.
 // ---------------------------------------------------------------------------
+// mlim: pixels at or past it are not stored (default: p.M).
 template <int FM, int FN>
 __device__ __forceinline__ void store_tile_c8(const GemmParams &p, const f4 (&acc)[FN][FM], int m0,
-                                              int nb0, float *stage, int lane) {
+                                              int nb0, float *stage, int lane, int mlim = -1) {
     constexpr int NPIX = 16 * FM, NSL = 2 * FN;
+    const int lim = mlim < 0 ? p.M : mlim;
 #pragma unroll
     for (int i = 0; i < FN; ++i) {
         const int nbase = (nb0 + i) * 16 + 4 * (lane >> 4);
@@ -119,7 +121,7 @@ __device__ __forceinline__ void store_tile_c8(const GemmParams &p, const f4 (&ac
         if ((NSL * NPIX) % 64 != 0 && e >= NSL * NPIX) break;   // a single 16x16 block: half a wave
         const int sl = e / NPIX, px = e - sl * NPIX;
         const int os = nb0 * 2 + sl, m = m0 + px;
-        if (os >= p.ns || m >= p.M) continue;
+        if (os >= p.ns || m >= lim) continue;
         const f4 lo = *(const f4 *)(stage + e * 8), hi = *(const f4 *)(stage + e * 8 + 4);
         float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
         const size_t off = (size_t)os * p.M + m;

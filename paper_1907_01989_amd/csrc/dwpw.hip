@@ -4,61 +4,75 @@
 //
 // The unfused pair writes the depthwise output to HBM and reads it straight
 // back; in the early MobileNet layers that round trip is a third of the
-// layer's bytes.  Here a workgroup owns BM consecutive output pixels and all
-// FN*16 output channels of the pointwise convolution, and walks K (the
-// depthwise channels) in chunks of four slices: for each chunk it computes
-// the depthwise outputs of its pixels (same tap order, fp32 accumulation,
-// activation and fp16 rounding as the standalone depthwise kernel) straight
-// into an LDS B tile, stages the chunk's packed weights next to it, and runs
-// the MFMAs (v_mfma_f32_16x16x32_f16, K ascending as in the GEMM kernels).
-// The result is therefore bit-identical to the unfused pair.  Loads for
-// chunk k+1 are issued before the MFMAs of chunk k; LDS is double-buffered
-// with one barrier per chunk.  The four waves split the pixels (BM/64
-// fragments of 16 each) and each holds all FN channel blocks.
+// layer's bytes.  Here a workgroup owns RB whole output rows of one image
+// (RB * OW <= 64 * FMW pixels) and all FN*16 output channels of the
+// pointwise convolution, and walks K (the depthwise channels) in chunks of
+// four slices.  For each chunk it
+//   1. stages the input rows its outputs need (with the zero padding written
+//      out as zeros) in LDS, each element loaded once;
+//   2. computes the depthwise outputs from LDS (same tap order, fp32
+//      accumulation, activation and fp16 rounding as the standalone kernel)
+//      into an LDS B tile;
+//   3. runs the MFMAs (v_mfma_f32_16x16x32_f16, K ascending as in the GEMM
+//      kernels) against the chunk's packed weights, staged next to it.
+// The result is bit-identical to the unfused pair.  The next chunk's band
+// and weights are loaded into registers while the current chunk computes.
+// The four waves split the pixel fragments; each holds all FN channel blocks.
 #include "device.h"
 
 namespace mgi {
 namespace kern {
 
-template <int BM, int FN, int S_>
-__global__ __launch_bounds__(256) void dwpw_kernel(DwPwParams p) {
-    constexpr int FMW = BM / 64;                 // pixel fragments per wave
-    constexpr int PPT = BM / 64;                 // (pixel, slice) pairs per thread and chunk
-    constexpr int BT = 4 * BM, AT = FN * 64;     // B tile and A chunk, in 16-byte elements
-    constexpr int BUF = BT + AT;
-    constexpr int WPT = (AT + 255) / 256;        // weight elements per thread and chunk
-    constexpr int STAGE = 4 * 4 * FMW * 256;     // epilogue floats (4 waves, 4 blocks per pass)
-    constexpr int LDS_H8 = 2 * BUF > STAGE / 4 ? 2 * BUF : STAGE / 4;
-    __shared__ h8 lds[LDS_H8];
+__device__ __forceinline__ int fdiv_exact(int a, float inv) { return (int)(((float)a + 0.5f) * inv); }
+
+template <int FMW, int FN, int S_>
+__global__ __launch_bounds__(256) void dwpw_kernel(DwPwParams p, DwPwTile t) {
+    constexpr int BM = 64 * FMW;                 // pixels computed per workgroup
+    constexpr int BT = 4 * BM, AT = FN * 64;     // B tile and A chunk, 16-byte elements
+    constexpr int EPT = (kDwPwBandMax + 255) / 256;
+    constexpr int WPT = (AT + 255) / 256;
+    constexpr int PPT = (4 * BM + 255) / 256;    // depthwise (pixel, slice) pairs per thread
+    constexpr int STAGE_H8 = 4 * 4 * FMW * 256 / 4;
+    constexpr int MAIN_H8 = kDwPwBandMax + BT + AT;
+    __shared__ h8 lds[MAIN_H8 > STAGE_H8 ? MAIN_H8 : STAGE_H8];
+    h8 *band = lds, *btile = lds + kDwPwBandMax, *atile = lds + kDwPwBandMax + BT;
     const GemmParams &g = p.g;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int m0 = blockIdx.x * BM;
+    const int n = blockIdx.x / t.nbands, oy0 = (blockIdx.x - n * t.nbands) * t.RB;
+    const int m0 = (n * p.OH + oy0) * p.OW;
+    const int valid = t.RB * p.OW;
     const int nk = g.ksp >> 2;
+    const int per = t.NRB * t.WP, E = 4 * per;
+    const int min_px = p.N * p.H * p.W;
 
-    // this thread's pixel (fixed over K) and the element offsets of its taps
-    const int px = tid % BM;
-    const int ohw = p.OH * p.OW;
-    const int mc = min(m0 + px, g.M - 1);        // pixels past M are computed, never stored
-    const int n = mc / ohw, r = mc - n * ohw;
-    const int oy = r / p.OW, ox = r - oy * p.OW;
-    int off[9];
+    // band element e of this thread: slice-in-chunk and spatial offset (fixed over K)
+    int bsl[EPT], boff[EPT];
 #pragma unroll
-    for (int ky = 0; ky < 3; ++ky)
+    for (int i = 0; i < EPT; ++i) {
+        const int e = tid + 256 * i;
+        const int sl = fdiv_exact(e, t.inv_per), rem = e - sl * per;
+        const int r = fdiv_exact(rem, t.inv_wp), c = rem - r * t.WP;
+        const int iy = oy0 * S_ - p.pt + r, ix = c - p.pl;
+        bsl[i] = sl;
+        boff[i] = (e < E && iy >= 0 && iy < p.H && ix >= 0 && ix < p.W) ? (n * p.H + iy) * p.W + ix : -1;
+    }
+    // depthwise outputs of this thread: slice-in-chunk, pixel, LDS base of its window
+    int dsl[PPT], dpx[PPT], dbase[PPT];
 #pragma unroll
-        for (int kx = 0; kx < 3; ++kx) {
-            const int iy = oy * S_ - p.pt + ky, ix = ox * S_ - p.pl + kx;
-            off[ky * 3 + kx] = (iy >= 0 && iy < p.H && ix >= 0 && ix < p.W) ? (n * p.H + iy) * p.W + ix : -1;
-        }
-    const int min_px = p.N * p.H * p.W;          // pixels per slice of the depthwise input
+    for (int j = 0; j < PPT; ++j) {
+        const int q = tid + 256 * j;
+        dsl[j] = q / BM;
+        dpx[j] = q - dsl[j] * BM;
+        const int r = fdiv_exact(dpx[j], t.inv_ow), x = dpx[j] - r * p.OW;
+        dbase[j] = (dsl[j] * t.NRB + r * S_) * t.WP + x * S_;
+    }
 
-    h8 v[PPT][9], wr[WPT];
+    h8 bv[EPT], wr[WPT];
     auto gload = [&](int kc) {
 #pragma unroll
-        for (int j = 0; j < PPT; ++j) {
-            const int s = min(kc * 4 + tid / BM + j * (256 / BM), g.ksl - 1);   // K tail: zero weights
-            const h8 *base = p.x + (size_t)s * min_px;
-#pragma unroll
-            for (int t = 0; t < 9; ++t) v[j][t] = *(off[t] >= 0 ? base + off[t] : p.zero);
+        for (int i = 0; i < EPT; ++i) {
+            const int s = min(kc * 4 + bsl[i], g.ksl - 1);   // K tail: its weights are zero
+            bv[i] = *(boff[i] >= 0 ? p.x + (size_t)s * min_px + boff[i] : p.zero);
         }
 #pragma unroll
         for (int i = 0; i < WPT; ++i) {
@@ -69,28 +83,6 @@ __global__ __launch_bounds__(256) void dwpw_kernel(DwPwParams p) {
     };
     const float lo = p.act == MGI_ACT_NONE ? -INFINITY : 0.0f;
     const float hi = p.act == MGI_ACT_RELU6 ? 6.0f : INFINITY;
-    auto lstore = [&](int kc, h8 *buf) {
-#pragma unroll
-        for (int j = 0; j < PPT; ++j) {
-            const int sl = tid / BM + j * (256 / BM);
-            const int s = min(kc * 4 + sl, g.ksl - 1);
-            const h8 *wt = p.dww + (size_t)s * 9;
-            float acc[8];
-#pragma unroll
-            for (int c = 0; c < 8; ++c) acc[c] = p.dwb[s * 8 + c];
-#pragma unroll
-            for (int t = 0; t < 9; ++t) fma8(acc, as_u4(wt[t]), as_u4(v[j][t]));
-            h8 o;
-#pragma unroll
-            for (int c = 0; c < 8; ++c) o[c] = (_Float16)__builtin_amdgcn_fmed3f(acc[c], lo, hi);
-            buf[sl * BM + px] = o;
-        }
-#pragma unroll
-        for (int i = 0; i < WPT; ++i) {
-            const int e = tid + 256 * i;
-            if (AT % 256 == 0 || e < AT) buf[BT + e] = wr[i];
-        }
-    };
 
     f4 acc[FN][FMW];
 #pragma unroll
@@ -99,46 +91,73 @@ __global__ __launch_bounds__(256) void dwpw_kernel(DwPwParams p) {
         for (int j = 0; j < FMW; ++j) acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
 
     gload(0);
-    lstore(0, lds);
-    __syncthreads();
     for (int kc = 0; kc < nk; ++kc) {
-        const h8 *cur = lds + (kc & 1) * BUF;
+        __syncthreads();                         // the previous chunk is done with LDS
+#pragma unroll
+        for (int i = 0; i < EPT; ++i)
+            if (tid + 256 * i < E) band[tid + 256 * i] = bv[i];
+#pragma unroll
+        for (int i = 0; i < WPT; ++i) {
+            const int e = tid + 256 * i;
+            if (AT % 256 == 0 || e < AT) atile[e] = wr[i];
+        }
+        __syncthreads();
         if (kc + 1 < nk) gload(kc + 1);
+#pragma unroll
+        for (int j = 0; j < PPT; ++j) {
+            if (dpx[j] >= valid || dsl[j] >= 4) continue;   // padding pixels: never stored
+            const int s = min(kc * 4 + dsl[j], g.ksl - 1);
+            const h8 *wt = p.dww + (size_t)s * 9;
+            float a8[8];
+#pragma unroll
+            for (int c = 0; c < 8; ++c) a8[c] = p.dwb[s * 8 + c];
+#pragma unroll
+            for (int ky = 0; ky < 3; ++ky)
+#pragma unroll
+                for (int kx = 0; kx < 3; ++kx)
+                    fma8(a8, as_u4(wt[ky * 3 + kx]), as_u4(band[dbase[j] + ky * t.WP + kx]));
+            h8 o;
+#pragma unroll
+            for (int c = 0; c < 8; ++c) o[c] = (_Float16)__builtin_amdgcn_fmed3f(a8[c], lo, hi);
+            btile[dsl[j] * BM + dpx[j]] = o;
+        }
+        __syncthreads();
         h8 b[FMW];
 #pragma unroll
-        for (int j = 0; j < FMW; ++j) b[j] = cur[(lane >> 4) * BM + (wave * FMW + j) * 16 + (lane & 15)];
+        for (int j = 0; j < FMW; ++j) b[j] = btile[(lane >> 4) * BM + (wave * FMW + j) * 16 + (lane & 15)];
 #pragma unroll
         for (int i = 0; i < FN; ++i) {
-            const h8 a = cur[BT + i * 64 + lane];
+            const h8 a = atile[i * 64 + lane];
 #pragma unroll
             for (int j = 0; j < FMW; ++j)
                 acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b[j], acc[i][j], 0, 0, 0);
         }
-        if (kc + 1 < nk) lstore(kc + 1, lds + ((kc + 1) & 1) * BUF);
-        __syncthreads();
     }
+    __syncthreads();
 
-    // epilogue in passes of four channel blocks through a per-wave stage
+    // epilogue in passes of four channel blocks through a per-wave stage;
+    // pixels past this band's rows belong to the next band and are not stored
     float *stage = (float *)lds + wave * (4 * FMW * 256);
-    const int mw = m0 + wave * FMW * 16;
+    const int mw = m0 + wave * FMW * 16, mlim = m0 + valid;
 #pragma unroll
     for (int g4 = 0; g4 < FN; g4 += 4) {
         constexpr int REM = FN % 4 == 0 ? 4 : FN % 4;
         if (g4 + 4 <= FN) {
-            store_tile_c8<FMW, 4>(g, *reinterpret_cast<const f4(*)[4][FMW]>(&acc[g4]), mw, g4, stage, lane);
+            store_tile_c8<FMW, 4>(g, *reinterpret_cast<const f4(*)[4][FMW]>(&acc[g4]), mw, g4, stage, lane,
+                                  mlim);
         } else {
             store_tile_c8<FMW, REM>(g, *reinterpret_cast<const f4(*)[REM][FMW]>(&acc[g4]), mw, g4, stage,
-                                    lane);
+                                    lane, mlim);
         }
         __builtin_amdgcn_wave_barrier();
     }
 }
 
-template <int BM, int FN>
-static hipError_t launch_dwpw_fn(const DwPwParams &p, hipStream_t st) {
-    const unsigned blocks = (unsigned)((p.g.M + BM - 1) / BM);
-    if (p.sh == 1) launch((dwpw_kernel<BM, FN, 1>), dim3(blocks), dim3(256), 0, st, p);
-    else launch((dwpw_kernel<BM, FN, 2>), dim3(blocks), dim3(256), 0, st, p);
+template <int FMW, int FN>
+static hipError_t launch_dwpw_fn(const DwPwParams &p, const DwPwTile &t, hipStream_t st) {
+    const unsigned blocks = (unsigned)(p.N * t.nbands);
+    if (p.sh == 1) launch((dwpw_kernel<FMW, FN, 1>), dim3(blocks), dim3(256), 0, st, p, t);
+    else launch((dwpw_kernel<FMW, FN, 2>), dim3(blocks), dim3(256), 0, st, p, t);
     return hipGetLastError();
 }
 
@@ -149,16 +168,36 @@ int dwpw_blocks(int nb16) {
     return 0;
 }
 
-hipError_t launch_dwpw(const DwPwParams &p, int bm, hipStream_t st) {
+bool dwpw_tile(int OH, int OW, int S, int N, DwPwTile &t, int max_px) {
+    int rb = 0;
+    for (int r = 1; r <= OH; ++r)
+        if (OH % r == 0 && r * OW <= max_px) rb = r;
+    if (!rb) return false;
+    t.RB = rb;
+    t.nbands = OH / rb;
+    t.NRB = (rb - 1) * S + 3;
+    t.WP = (OW - 1) * S + 3;
+    if (4 * t.NRB * t.WP > kDwPwBandMax) return false;
+    t.fmw = rb * OW <= 64 ? 1 : 2;
+    t.inv_per = 1.0f / (float)(t.NRB * t.WP);
+    t.inv_wp = 1.0f / (float)t.WP;
+    t.inv_ow = 1.0f / (float)OW;
+    (void)N;
+    return true;
+}
+
+hipError_t launch_dwpw(const DwPwParams &p, const DwPwTile &t, hipStream_t st) {
     if (p.g.M <= 0) return hipSuccess;
     if (p.sh != p.sw || (p.sh != 1 && p.sh != 2)) return hipErrorInvalidValue;
+    if (t.RB <= 0 || p.OH % t.RB != 0 || t.RB * p.OW > 64 * t.fmw || 4 * t.NRB * t.WP > kDwPwBandMax)
+        return hipErrorInvalidValue;
     const int fn = dwpw_blocks(p.g.nb16);
-#define MGI_DWPW_CASE(BM_, FN_) \
-    if (bm == BM_ && fn == FN_) return launch_dwpw_fn<BM_, FN_>(p, st);
-    MGI_DWPW_CASE(64, 1) MGI_DWPW_CASE(64, 2) MGI_DWPW_CASE(64, 4) MGI_DWPW_CASE(64, 8)
-    MGI_DWPW_CASE(64, 12) MGI_DWPW_CASE(64, 16) MGI_DWPW_CASE(64, 20)
-    MGI_DWPW_CASE(128, 1) MGI_DWPW_CASE(128, 2) MGI_DWPW_CASE(128, 4) MGI_DWPW_CASE(128, 8)
-    MGI_DWPW_CASE(128, 12) MGI_DWPW_CASE(128, 16) MGI_DWPW_CASE(128, 20)
+#define MGI_DWPW_CASE(FMW_, FN_) \
+    if (t.fmw == FMW_ && fn == FN_) return launch_dwpw_fn<FMW_, FN_>(p, t, st);
+    MGI_DWPW_CASE(1, 1) MGI_DWPW_CASE(1, 2) MGI_DWPW_CASE(1, 4) MGI_DWPW_CASE(1, 8)
+    MGI_DWPW_CASE(1, 12) MGI_DWPW_CASE(1, 16) MGI_DWPW_CASE(1, 20)
+    MGI_DWPW_CASE(2, 1) MGI_DWPW_CASE(2, 2) MGI_DWPW_CASE(2, 4) MGI_DWPW_CASE(2, 8)
+    MGI_DWPW_CASE(2, 12) MGI_DWPW_CASE(2, 16) MGI_DWPW_CASE(2, 20)
 #undef MGI_DWPW_CASE
     return hipErrorInvalidValue;
 }

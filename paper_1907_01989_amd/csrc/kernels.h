@@ -70,8 +70,17 @@ struct DwPwParams {
     int N, H, W, OH, OW, sh, sw, pt, pl, act;
     GemmParams g;
 };
-// bm: 64 or 128 pixels per workgroup; g.nb16 <= 20
-hipError_t launch_dwpw(const DwPwParams &p, int bm, hipStream_t st);
+// Workgroup tile: RB whole output rows of one image (RB divides OH,
+// RB * OW <= 64 * fmw); the input band of a chunk is NRB rows of WP elements
+// for each of four slices, at most kDwPwBandMax elements.
+constexpr int kDwPwBandMax = 2304;
+struct DwPwTile {
+    int RB = 0, nbands = 0, NRB = 0, WP = 0, fmw = 2;
+    float inv_per = 0, inv_wp = 0, inv_ow = 0;
+};
+// band of at most max_px (64 or 128) pixels; false when no band fits
+bool dwpw_tile(int OH, int OW, int S, int N, DwPwTile &t, int max_px = 128);
+hipError_t launch_dwpw(const DwPwParams &p, const DwPwTile &t, hipStream_t st);
 // channel blocks the kernel instance computes for nb16 output blocks (0: too many)
 int dwpw_blocks(int nb16);
 

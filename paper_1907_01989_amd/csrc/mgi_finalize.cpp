@@ -124,12 +124,12 @@ void add_configs(Node &nd, size_t M) {
             push(t);
         }
     } else if (nd.kind == NodeKind::DwPw) {
-        for (int bm : {nd.tile.bm, 128, 64}) {
+        // band heights for the fused depthwise + pointwise kernel: up to 128
+        // or up to 64 pixels per workgroup
+        for (int px : {128, 64}) {
             GemmTile t;
-            t.bm = bm;
-            bool dup = false;
-            for (const Node::Config &c : nd.cfgs) dup = dup || c.tile.bm == bm;
-            if (!dup) nd.cfgs.push_back({t, 0, "dwpw" + std::to_string(bm)});
+            t.bm = px;
+            nd.cfgs.push_back({t, 0, "band" + std::to_string(px)});
         }
     } else if (nd.kind == NodeKind::Depthwise && nd.conv.kh == 3 && nd.conv.kw == 3 &&
                nd.conv.stride_h == nd.conv.stride_w && nd.conv.dil_h == nd.conv.dil_w &&
@@ -144,8 +144,9 @@ void add_configs(Node &nd, size_t M) {
 // Depthwise -> pointwise fusion (Sec. 3.2's fusion extended to the
 // depthwise-separable pair): a 3x3 depthwise node (stride 1 or 2, dilation 1)
 // whose output only feeds one pointwise GEMM with at most 320 output channels
-// becomes part of that GEMM's node, when the GEMM's pixels still give at least
-// 256 workgroups of 64 (or 512 of 128); the intermediate buffer is dropped.
+// becomes part of that GEMM's node, when whole output rows tile the image
+// (a band of rows of at most 128 pixels) into at least 256 workgroups; the
+// intermediate buffer is dropped.
 void fuse_dw_into_pw(mgi_plan &p) {
     std::vector<int> readers(p.bufs.size(), 0), producer(p.bufs.size(), -1);
     for (size_t i = 0; i < p.nodes.size(); ++i) {
@@ -165,9 +166,9 @@ void fuse_dw_into_pw(mgi_plan &p) {
             c.stride_h > 2 || c.dil_h != 1 || c.dil_w != 1)
             continue;
         if (kern::dwpw_blocks(pw.nb16) == 0) continue;
-        const size_t M = p.bufs[pw.out].shape.pixels();
-        const int bm = M / 128 >= 512 ? 128 : (M / 64 >= 256 ? 64 : 0);
-        if (!bm) continue;
+        const Shape os = p.bufs[pw.out].shape;
+        kern::DwPwTile t;
+        if (!kern::dwpw_tile(os.h, os.w, c.stride_h, os.n, t) || (size_t)os.n * t.nbands < 256) continue;
         pw.kind = NodeKind::DwPw;
         pw.kname = "dw_pw";
         pw.dw_op = dw.op;
@@ -176,7 +177,7 @@ void fuse_dw_into_pw(mgi_plan &p) {
         pw.in[0] = dw.in[0];
         pw.n_fused += dw.n_fused;
         pw.tile = GemmTile{};
-        pw.tile.bm = bm;
+        pw.tile.bm = 128;
         p.bufs[mid].dead = true;
         drop[producer[mid]] = 1;
     }

@@ -116,7 +116,10 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
             g.ksl = nd.ksl; g.ksp = nd.ksp;
             g.nb16 = nd.nb16; g.ns = slices(os.c); g.cout = os.c;
             g.act1 = nd.act1; g.act2 = nd.act2;
-            return launch_dwpw(q, nd.tile.bm, st);
+            DwPwTile t;
+            if (!dwpw_tile(os.h, os.w, q.sh, os.n, t, nd.tile.bm > 0 ? nd.tile.bm : 128))
+                return hipErrorInvalidValue;
+            return launch_dwpw(q, t, st);
         }
         case NodeKind::Depthwise: {
             const Buf &ib = p.bufs[nd.in[0]];

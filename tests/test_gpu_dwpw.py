@@ -23,7 +23,7 @@ pytestmark = pytest.mark.gpu
 CASES = [
     # n, h, w, c (depthwise channels = K), stride, N (pointwise outputs), residual
     (64, 28, 28, 72, 1, 40, False),      # 64-pixel tiles, K tail
-    (32, 56, 56, 32, 2, 24, True),       # stride 2, residual
+    (48, 56, 56, 32, 2, 24, True),       # stride 2, residual
     (128, 14, 14, 96, 1, 160, False),    # 12 blocks for 10
     (17, 57, 55, 20, 1, 320, True),      # odd sizes, 20 blocks, ragged everything
     (64, 112, 112, 32, 1, 64, False),    # 128-pixel tiles (v1 layer 1 shape)
