@@ -98,7 +98,9 @@ typedef struct {
     int fuse;            /* 1: fuse activations / residual adds into producers (default 1) */
     int materialize_all; /* 1: every node output keeps its own buffer so that
                             mgi_plan_read_node works after a run (default 0) */
-    int dtype;           /* storage type of activations and weights: FP16 (default) */
+    int dtype;           /* storage type of activations and weights: FP16 (default) or
+                            BF16 (round to nearest even; MFMA and accumulation in fp32
+                            either way); other values give MGI_ERR_UNSUPPORTED */
     int fuse_dwpw;       /* 1: run a 3x3 depthwise convolution (stride 1 or 2, no dilation)
                             inside the pointwise convolution that alone consumes it, when
                             that convolution has at most 320 output channels and enough

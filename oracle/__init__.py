@@ -278,7 +278,15 @@ def eval_op(op, operands):
     raise ValueError(f"unknown op {k}")
 
 
-def run_graph(graph, keep=None, store_fp16=False):
+def _round_bf16(y):
+    """Nearest bf16 value (ties to even) of each element, via the float32 bit
+    pattern: bf16 keeps the upper 16 bits of a float32."""
+    u = np.asarray(y, dtype=np.float64).astype(np.float32).view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) >> 16 << 16
+    return u.astype(np.uint32).view(np.float32).astype(np.float64).reshape(np.shape(y))
+
+
+def run_graph(graph, keep=None, store_fp16=False, store_bf16=False):
     """Evaluate every tensor of ``graph``; returns {tensor id: float64 NHWC array}
     (argmax outputs are int32).  ``keep`` limits which tensors are returned;
     others are dropped as soon as their last consumer has run.
@@ -286,7 +294,8 @@ def run_graph(graph, keep=None, store_fp16=False):
     ``store_fp16`` rounds each tensor that the paper's engine stores in fp16
     (Table 1 frames the GPU side as FP16) to the nearest fp16 value after its
     op, everything else staying exact: it measures how much a network amplifies
-    the rounding that fp16 storage alone introduces."""
+    the rounding that fp16 storage alone introduces.  ``store_bf16`` does the
+    same for bf16 storage."""
     ops = graph["ops"]
     last_use = {}
     for i, op in enumerate(ops):
@@ -298,6 +307,8 @@ def run_graph(graph, keep=None, store_fp16=False):
         y = eval_op(op, [vals[t] for t in op_inputs(op)])
         if store_fp16 and op["op"] in FP16_STORED:
             y = y.astype(np.float16).astype(np.float64)
+        if store_bf16 and op["op"] in FP16_STORED:
+            y = _round_bf16(y)
         vals[i] = y
         for t in op_inputs(op):
             if last_use.get(t) == i and t not in want:

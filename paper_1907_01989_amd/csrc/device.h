@@ -63,6 +63,67 @@ __device__ __forceinline__ void fma8(float *acc, u4x w, u4x v) {
     }
 }
 
+// Storage element traits.  Activations and weights are stored as 16-bit
+// floats, 8 per 16-byte element, either fp16 or bf16 (mgi_options.dtype);
+// kernels move elements as raw 16-byte values and only convert at these
+// points.  Products of two 16-bit values are exact in fp32 for both types.
+typedef __bf16 bh8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bh4 __attribute__((ext_vector_type(4)));
+typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
+typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
+
+struct F16 {
+    static constexpr bool bf = false;
+    __device__ static float get(h8 v, int i) { return (float)v[i]; }
+    __device__ static h8 pack(const float *v) {
+        h8 o;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) o[i] = (_Float16)v[i];
+        return o;
+    }
+    __device__ static f4 mma(h8 a, h8 b, f4 c) { return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0); }
+    __device__ static void fma8(float *acc, h8 w, h8 v) { kern::fma8(acc, as_u4(w), as_u4(v)); }
+    __device__ static float get4(h4 v, int i) { return (float)v[i]; }
+    __device__ static h4 pack4(const float *v) {
+        h4 o;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[i] = (_Float16)v[i];
+        return o;
+    }
+    __device__ static uint16_t bits(float f) { return __builtin_bit_cast(uint16_t, (_Float16)f); }
+};
+
+struct BF16 {
+    static constexpr bool bf = true;
+    __device__ static float get(h8 v, int i) {
+        return __uint_as_float((uint32_t)__builtin_bit_cast(u16x8, v)[i] << 16);
+    }
+    __device__ static h8 pack(const float *v) {
+        bh8 o;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) o[i] = (__bf16)v[i];
+        return __builtin_bit_cast(h8, o);
+    }
+    __device__ static f4 mma(h8 a, h8 b, f4 c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bh8, a), __builtin_bit_cast(bh8, b), c,
+                                                      0, 0, 0);
+    }
+    __device__ static void fma8(float *acc, h8 w, h8 v) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[i] = fmaf(get(w, i), get(v, i), acc[i]);
+    }
+    __device__ static float get4(h4 v, int i) {
+        return __uint_as_float((uint32_t)__builtin_bit_cast(u16x4, v)[i] << 16);
+    }
+    __device__ static h4 pack4(const float *v) {
+        bh4 o;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[i] = (__bf16)v[i];
+        return __builtin_bit_cast(h4, o);
+    }
+    __device__ static uint16_t bits(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
+};
+
 // 16 bytes per lane from global memory straight into LDS: lane l writes
 // lds + 16*l, so the LDS side is one contiguous KiB per wave.  Issued as
 // inline asm so that the compiler does not track it: it would otherwise
@@ -94,7 +155,7 @@ __device__ __forceinline__ void wait_vm_lds() {
 // reads back only what it wrote.
 // ---------------------------------------------------------------------------
 // mlim: pixels at or past it are not stored (default: p.M).
-template <int FM, int FN>
+template <typename E, int FM, int FN>
 __device__ __forceinline__ void store_tile_c8(const GemmParams &p, const f4 (&acc)[FN][FM], int m0,
                                               int nb0, float *stage, int lane, int mlim = -1) {
     constexpr int NPIX = 16 * FM, NSL = 2 * FN;
@@ -128,12 +189,9 @@ __device__ __forceinline__ void store_tile_c8(const GemmParams &p, const f4 (&ac
         if (p.res) {
             const h8 rv = p.res[off];
 #pragma unroll
-            for (int r = 0; r < 8; ++r) v[r] = act_apply(v[r] + (float)rv[r], p.act2);
+            for (int r = 0; r < 8; ++r) v[r] = act_apply(v[r] + E::get(rv, r), p.act2);
         }
-        h8 o;
-#pragma unroll
-        for (int r = 0; r < 8; ++r) o[r] = (_Float16)v[r];
-        ((h8 *)p.y)[off] = o;
+        ((h8 *)p.y)[off] = E::pack(v);
     }
 }
 

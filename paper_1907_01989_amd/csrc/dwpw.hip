@@ -25,7 +25,7 @@ namespace kern {
 
 __device__ __forceinline__ int fdiv_exact(int a, float inv) { return (int)(((float)a + 0.5f) * inv); }
 
-template <int FMW, int FN, int S_>
+template <typename E, int FMW, int FN, int S_>
 __global__ __launch_bounds__(256) void dwpw_kernel(DwPwParams p, DwPwTile t) {
     constexpr int BM = 64 * FMW;                 // pixels computed per workgroup
     constexpr int BT = 4 * BM, AT = FN * 64;     // B tile and A chunk, 16-byte elements
@@ -42,7 +42,7 @@ __global__ __launch_bounds__(256) void dwpw_kernel(DwPwParams p, DwPwTile t) {
     const int m0 = (n * p.OH + oy0) * p.OW;
     const int valid = t.RB * p.OW;
     const int nk = g.ksp >> 2;
-    const int per = t.NRB * t.WP, E = 4 * per;
+    const int per = t.NRB * t.WP, band_n = 4 * per;
     const int min_px = p.N * p.H * p.W;
 
     // band element e of this thread: slice-in-chunk and spatial offset (fixed over K)
@@ -54,7 +54,7 @@ __global__ __launch_bounds__(256) void dwpw_kernel(DwPwParams p, DwPwTile t) {
         const int r = fdiv_exact(rem, t.inv_wp), c = rem - r * t.WP;
         const int iy = oy0 * S_ - p.pt + r, ix = c - p.pl;
         bsl[i] = sl;
-        boff[i] = (e < E && iy >= 0 && iy < p.H && ix >= 0 && ix < p.W) ? (n * p.H + iy) * p.W + ix : -1;
+        boff[i] = (e < band_n && iy >= 0 && iy < p.H && ix >= 0 && ix < p.W) ? (n * p.H + iy) * p.W + ix : -1;
     }
     // depthwise outputs of this thread: slice-in-chunk, pixel, LDS base of its window
     int dsl[PPT], dpx[PPT], dbase[PPT];
@@ -95,7 +95,7 @@ __global__ __launch_bounds__(256) void dwpw_kernel(DwPwParams p, DwPwTile t) {
         __syncthreads();                         // the previous chunk is done with LDS
 #pragma unroll
         for (int i = 0; i < EPT; ++i)
-            if (tid + 256 * i < E) band[tid + 256 * i] = bv[i];
+            if (tid + 256 * i < band_n) band[tid + 256 * i] = bv[i];
 #pragma unroll
         for (int i = 0; i < WPT; ++i) {
             const int e = tid + 256 * i;
@@ -115,11 +115,10 @@ __global__ __launch_bounds__(256) void dwpw_kernel(DwPwParams p, DwPwTile t) {
             for (int ky = 0; ky < 3; ++ky)
 #pragma unroll
                 for (int kx = 0; kx < 3; ++kx)
-                    fma8(a8, as_u4(wt[ky * 3 + kx]), as_u4(band[dbase[j] + ky * t.WP + kx]));
-            h8 o;
+                    E::fma8(a8, wt[ky * 3 + kx], band[dbase[j] + ky * t.WP + kx]);
 #pragma unroll
-            for (int c = 0; c < 8; ++c) o[c] = (_Float16)__builtin_amdgcn_fmed3f(a8[c], lo, hi);
-            btile[dsl[j] * BM + dpx[j]] = o;
+            for (int c = 0; c < 8; ++c) a8[c] = __builtin_amdgcn_fmed3f(a8[c], lo, hi);
+            btile[dsl[j] * BM + dpx[j]] = E::pack(a8);
         }
         __syncthreads();
         h8 b[FMW];
@@ -130,7 +129,7 @@ __global__ __launch_bounds__(256) void dwpw_kernel(DwPwParams p, DwPwTile t) {
             const h8 a = atile[i * 64 + lane];
 #pragma unroll
             for (int j = 0; j < FMW; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b[j], acc[i][j], 0, 0, 0);
+                acc[i][j] = E::mma(a, b[j], acc[i][j]);
         }
     }
     __syncthreads();
@@ -143,10 +142,10 @@ __global__ __launch_bounds__(256) void dwpw_kernel(DwPwParams p, DwPwTile t) {
     for (int g4 = 0; g4 < FN; g4 += 4) {
         constexpr int REM = FN % 4 == 0 ? 4 : FN % 4;
         if (g4 + 4 <= FN) {
-            store_tile_c8<FMW, 4>(g, *reinterpret_cast<const f4(*)[4][FMW]>(&acc[g4]), mw, g4, stage, lane,
+            store_tile_c8<E, FMW, 4>(g, *reinterpret_cast<const f4(*)[4][FMW]>(&acc[g4]), mw, g4, stage, lane,
                                   mlim);
         } else {
-            store_tile_c8<FMW, REM>(g, *reinterpret_cast<const f4(*)[REM][FMW]>(&acc[g4]), mw, g4, stage,
+            store_tile_c8<E, FMW, REM>(g, *reinterpret_cast<const f4(*)[REM][FMW]>(&acc[g4]), mw, g4, stage,
                                     lane, mlim);
         }
         __builtin_amdgcn_wave_barrier();
@@ -156,8 +155,13 @@ __global__ __launch_bounds__(256) void dwpw_kernel(DwPwParams p, DwPwTile t) {
 template <int FMW, int FN>
 static hipError_t launch_dwpw_fn(const DwPwParams &p, const DwPwTile &t, hipStream_t st) {
     const unsigned blocks = (unsigned)(p.N * t.nbands);
-    if (p.sh == 1) launch((dwpw_kernel<FMW, FN, 1>), dim3(blocks), dim3(256), 0, st, p, t);
-    else launch((dwpw_kernel<FMW, FN, 2>), dim3(blocks), dim3(256), 0, st, p, t);
+    if (p.g.bf16) {
+        if (p.sh == 1) launch((dwpw_kernel<BF16, FMW, FN, 1>), dim3(blocks), dim3(256), 0, st, p, t);
+        else launch((dwpw_kernel<BF16, FMW, FN, 2>), dim3(blocks), dim3(256), 0, st, p, t);
+    } else {
+        if (p.sh == 1) launch((dwpw_kernel<F16, FMW, FN, 1>), dim3(blocks), dim3(256), 0, st, p, t);
+        else launch((dwpw_kernel<F16, FMW, FN, 2>), dim3(blocks), dim3(256), 0, st, p, t);
+    }
     return hipGetLastError();
 }
 

@@ -25,7 +25,7 @@ namespace mgi {
 namespace kern {
 
 
-template <int BM, int BN, bool TAPS, bool F32OUT>
+template <typename E, int BM, int BN, bool TAPS, bool F32OUT>
 __global__ __launch_bounds__(256) void gemm_kernel(GemmParams p) {
     constexpr int WM = BM / 2, WN = BN / 2;      // 2 x 2 waves
     constexpr int FM = WM / 16, FN = WN / 16;    // fragments per wave
@@ -128,7 +128,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmParams p) {
         for (int i = 0; i < FN; ++i)
 #pragma unroll
             for (int j = 0; j < FM; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[i], b[j], acc[i][j], 0, 0, 0);
+                acc[i][j] = E::mma(a[i], b[j], acc[i][j]);
         if (more) lstore(cur ^ 1);
         __syncthreads();
     }
@@ -161,18 +161,15 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmParams p) {
                 if (p.res) {
                     const h4 rv = *(const h4 *)((const _Float16 *)p.res + off);
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) v[r] = act_apply(v[r] + (float)rv[r], p.act2);
+                    for (int r = 0; r < 4; ++r) v[r] = act_apply(v[r] + E::get4(rv, r), p.act2);
                 }
-                h4 o;
-#pragma unroll
-                for (int r = 0; r < 4; ++r) o[r] = (_Float16)v[r];
-                *(h4 *)((_Float16 *)p.y + off) = o;
+                *(h4 *)((_Float16 *)p.y + off) = E::pack4(v);
             }
         }
     }
 }
 
-template <int BM, int BN>
+template <typename E, int BM, int BN>
 static hipError_t launch_bm_bn(const GemmParams &p, bool taps, bool f32out, hipStream_t st) {
     GemmParams q = p;
     q.mtiles = (p.M + BM - 1) / BM;
@@ -180,11 +177,11 @@ static hipError_t launch_bm_bn(const GemmParams &p, bool taps, bool f32out, hipS
     const dim3 grid(q.mtiles * q.ntiles), block(256);
     if (f32out) {
         if (taps) return hipErrorInvalidValue;
-        launch((gemm_kernel<BM, BN, false, true>), grid, block, 0, st, q);
+        launch((gemm_kernel<E, BM, BN, false, true>), grid, block, 0, st, q);
     } else if (taps) {
-        launch((gemm_kernel<BM, BN, true, false>), grid, block, 0, st, q);
+        launch((gemm_kernel<E, BM, BN, true, false>), grid, block, 0, st, q);
     } else {
-        launch((gemm_kernel<BM, BN, false, false>), grid, block, 0, st, q);
+        launch((gemm_kernel<E, BM, BN, false, false>), grid, block, 0, st, q);
     }
     return hipGetLastError();
 }
@@ -193,7 +190,8 @@ hipError_t launch_gemm(const GemmParams &p, int bm, int bn, bool taps, bool f32o
                        hipStream_t st) {
     if (p.M <= 0) return hipSuccess;
 #define MGI_GEMM_CASE(BM_, BN_) \
-    if (bm == BM_ && bn == BN_) return launch_bm_bn<BM_, BN_>(p, taps, f32out, st);
+    if (bm == BM_ && bn == BN_)     \
+        return p.bf16 ? launch_bm_bn<BF16, BM_, BN_>(p, taps, f32out, st) : launch_bm_bn<F16, BM_, BN_>(p, taps, f32out, st);
     MGI_GEMM_CASE(32, 32)
     MGI_GEMM_CASE(32, 64)
     MGI_GEMM_CASE(32, 128)
@@ -217,7 +215,7 @@ hipError_t launch_gemm(const GemmParams &p, int bm, int bn, bool taps, bool f32o
 // load other than the activation stream, so the in-order load counter lets
 // PF steps of loads stay in flight.
 // ---------------------------------------------------------------------------
-template <int WM, int BN, int PF>
+template <typename E, int WM, int BN, int PF>
 __global__ __launch_bounds__(256) void gemm_xs_kernel(GemmParams p) {
     constexpr int FM = WM / 16, FN = BN / 16, BM = 4 * WM;
     extern __shared__ h8 wsm[];                  // [FN][ksp][16]
@@ -275,7 +273,7 @@ __global__ __launch_bounds__(256) void gemm_xs_kernel(GemmParams p) {
         for (int i = 0; i < FN; ++i)
 #pragma unroll
             for (int j = 0; j < FM; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[i], b[j], acc[i][j], 0, 0, 0);
+                acc[i][j] = E::mma(a[i], b[j], acc[i][j]);
     };
     // Main loop over whole groups of PF steps: every step issues exactly FM
     // loads (the prefetch index is clamped instead of skipped), so the wait
@@ -294,7 +292,7 @@ __global__ __launch_bounds__(256) void gemm_xs_kernel(GemmParams p) {
 
     // per-wave epilogue tile after the weight slab
     float *stage = (float *)(wsm + FN * p.ksp * 16) + wave * (FN * FM * 256);
-    store_tile_c8<FM, FN>(p, acc, m0, nb0, stage, lane);
+    store_tile_c8<E, FM, FN>(p, acc, m0, nb0, stage, lane);
 }
 
 // LDS bytes of the weight slab for a bn-wide tile
@@ -303,7 +301,7 @@ size_t gemm_xs_lds_bytes(int ksp, int wm, int bn) {
     return (size_t)(bn / 16) * ksp * 256 + xs_stage_bytes(wm, bn);
 }
 
-template <int WM, int BN, int PF>
+template <typename E, int WM, int BN, int PF>
 static hipError_t launch_xs(const GemmParams &p, hipStream_t st) {
     GemmParams q = p;
     constexpr int BM = 4 * WM, FN = BN / 16;
@@ -311,14 +309,15 @@ static hipError_t launch_xs(const GemmParams &p, hipStream_t st) {
     q.ntiles = (p.nb16 + FN - 1) / FN;
     const size_t lds = gemm_xs_lds_bytes(p.ksp, WM, BN);
     if (lds > 65536) return hipErrorInvalidValue;
-    launch((gemm_xs_kernel<WM, BN, PF>), dim3(q.mtiles * q.ntiles), dim3(256), lds, st, q);
+    launch((gemm_xs_kernel<E, WM, BN, PF>), dim3(q.mtiles * q.ntiles), dim3(256), lds, st, q);
     return hipGetLastError();
 }
 
 hipError_t launch_gemm_xs(const GemmParams &p, int wm, int bn, int pf, hipStream_t st) {
     if (p.M <= 0) return hipSuccess;
 #define MGI_XS_CASE(WM_, BN_, PF_) \
-    if (wm == WM_ && bn == BN_ && pf == PF_) return launch_xs<WM_, BN_, PF_>(p, st);
+    if (wm == WM_ && bn == BN_ && pf == PF_) \
+        return p.bf16 ? launch_xs<BF16, WM_, BN_, PF_>(p, st) : launch_xs<F16, WM_, BN_, PF_>(p, st);
 #define MGI_XS_PF(WM_, BN_) MGI_XS_CASE(WM_, BN_, 1) MGI_XS_CASE(WM_, BN_, 2) MGI_XS_CASE(WM_, BN_, 4)
     MGI_XS_PF(16, 32)
     MGI_XS_PF(16, 64)
@@ -378,7 +377,7 @@ __device__ __forceinline__ void pipe_issue(const GemmParams &p, int kk, h8 *st, 
     }
 }
 
-template <int BM, int BN>
+template <typename E, int BM, int BN>
 __global__ __launch_bounds__(256) void gemm_pipe_kernel(GemmParams p) {
     using T = PipeTile<BM, BN>;
     constexpr int WMP = BM / 2, WNC = BN / 2, FM = WMP / 16, FN = WNC / 16;
@@ -422,7 +421,7 @@ __global__ __launch_bounds__(256) void gemm_pipe_kernel(GemmParams p) {
         for (int i = 0; i < FN; ++i)
 #pragma unroll
             for (int j = 0; j < FM; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[i], b[j], acc[i][j], 0, 0, 0);
+                acc[i][j] = E::mma(a[i], b[j], acc[i][j]);
     };
     for (int kk = 0; kk < nk; kk += 4) {
         body(kk, st0, st3);
@@ -433,25 +432,25 @@ __global__ __launch_bounds__(256) void gemm_pipe_kernel(GemmParams p) {
 
     __syncthreads();
     h8 *stage = wave == 0 ? st0 : wave == 1 ? st1 : wave == 2 ? st2 : st3;
-    store_tile_c8<FM, FN>(p, acc, m0 + wm * WMP, nb0 + wn * FN, (float *)stage, lane);
+    store_tile_c8<E, FM, FN>(p, acc, m0 + wm * WMP, nb0 + wn * FN, (float *)stage, lane);
 }
 
-template <int BM, int BN>
+template <typename E, int BM, int BN>
 static hipError_t launch_pipe_t(const GemmParams &p, hipStream_t st) {
     GemmParams q = p;
     q.mtiles = (p.M + BM - 1) / BM;
     q.ntiles = (p.nb16 * 16 + BN - 1) / BN;
-    launch((gemm_pipe_kernel<BM, BN>), dim3(q.mtiles * q.ntiles), dim3(256), 0, st, q);
+    launch((gemm_pipe_kernel<E, BM, BN>), dim3(q.mtiles * q.ntiles), dim3(256), 0, st, q);
     return hipGetLastError();
 }
 
 hipError_t launch_gemm_pipe(const GemmParams &p, int bm, int bn, hipStream_t st) {
     if (p.M <= 0) return hipSuccess;
     if (p.ksp % 4 != 0 || p.Min != p.M) return hipErrorInvalidValue;
-    if (bm == 64 && bn == 64) return launch_pipe_t<64, 64>(p, st);
-    if (bm == 64 && bn == 128) return launch_pipe_t<64, 128>(p, st);
-    if (bm == 128 && bn == 64) return launch_pipe_t<128, 64>(p, st);
-    if (bm == 128 && bn == 128) return launch_pipe_t<128, 128>(p, st);
+    if (bm == 64 && bn == 64) return p.bf16 ? launch_pipe_t<BF16, 64, 64>(p, st) : launch_pipe_t<F16, 64, 64>(p, st);
+    if (bm == 64 && bn == 128) return p.bf16 ? launch_pipe_t<BF16, 64, 128>(p, st) : launch_pipe_t<F16, 64, 128>(p, st);
+    if (bm == 128 && bn == 64) return p.bf16 ? launch_pipe_t<BF16, 128, 64>(p, st) : launch_pipe_t<F16, 128, 64>(p, st);
+    if (bm == 128 && bn == 128) return p.bf16 ? launch_pipe_t<BF16, 128, 128>(p, st) : launch_pipe_t<F16, 128, 128>(p, st);
     return hipErrorInvalidValue;
 }
 
@@ -462,7 +461,7 @@ hipError_t launch_gemm_pipe(const GemmParams &p, int bm, int bn, hipStream_t st)
 // and activation fragments at once, straight from global memory, and the four
 // fp32 partial tiles are summed through LDS in a fixed wave order.
 // ---------------------------------------------------------------------------
-template <int FM, int B>
+template <typename E, int FM, int B>
 __global__ __launch_bounds__(256) void fc_kernel(GemmParams p) {
     __shared__ f4 red[4][FM][64];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -493,7 +492,7 @@ __global__ __launch_bounds__(256) void fc_kernel(GemmParams p) {
             if (s + b < s1) {
 #pragma unroll
                 for (int j = 0; j < FM; ++j)
-                    acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wa[b], xa[b][j], acc[j], 0, 0, 0);
+                    acc[j] = E::mma(wa[b], xa[b][j], acc[j]);
             }
     }
 #pragma unroll
@@ -516,9 +515,15 @@ hipError_t launch_fc(const GemmParams &p, hipStream_t st) {
     const int fm = p.M <= 16 ? 1 : (p.M <= 32 ? 2 : 4);
     const int mtiles = (p.M + 16 * fm - 1) / (16 * fm);
     const dim3 grid(mtiles * p.nb16), block(256);
-    if (fm == 1) launch((fc_kernel<1, 4>), grid, block, 0, st, p);
-    else if (fm == 2) launch((fc_kernel<2, 4>), grid, block, 0, st, p);
-    else launch((fc_kernel<4, 4>), grid, block, 0, st, p);
+    if (p.bf16) {
+        if (fm == 1) launch((fc_kernel<BF16, 1, 4>), grid, block, 0, st, p);
+        else if (fm == 2) launch((fc_kernel<BF16, 2, 4>), grid, block, 0, st, p);
+        else launch((fc_kernel<BF16, 4, 4>), grid, block, 0, st, p);
+    } else {
+        if (fm == 1) launch((fc_kernel<F16, 1, 4>), grid, block, 0, st, p);
+        else if (fm == 2) launch((fc_kernel<F16, 2, 4>), grid, block, 0, st, p);
+        else launch((fc_kernel<F16, 4, 4>), grid, block, 0, st, p);
+    }
     return hipGetLastError();
 }
 
@@ -533,9 +538,9 @@ hipError_t launch_fc(const GemmParams &p, hipStream_t st) {
 // runs one MFMA per output block of 16 channels.  Entries k >= kh*kw*c read
 // any staged value: their weights are zero.
 // ---------------------------------------------------------------------------
-template <typename TIN, int NB>
+template <typename E, typename TIN, int NB>
 __global__ __launch_bounds__(256) void stem_kernel(StemParams p, int th, int rs, int nrows) {
-    extern __shared__ _Float16 band[];           // [nrows][rs] fp16
+    extern __shared__ _Float16 band[];           // [nrows][rs] 16-bit storage values
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int bands = (p.OH + th - 1) / th;
     const int n = blockIdx.x / bands, oy0 = (blockIdx.x - n * bands) * th;
@@ -559,17 +564,23 @@ __global__ __launch_bounds__(256) void stem_kernel(StemParams p, int th, int rs,
         _Float16 *dst = band + r * rs + lead;
         if (vec) {
             for (int c = tid * VEC; c < rowlen; c += 256 * VEC) {
-                if (VEC == 8) {
+                if (VEC == 8 && !E::bf) {
                     *(h8 *)(dst + c) = *(const h8 *)(src + c);
+                } else if (VEC == 8) {
+                    const h8 hv = *(const h8 *)(src + c);
+                    float f[8];
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) f[i] = (float)hv[i];
+                    *(h8 *)(dst + c) = E::pack(f);
                 } else {
                     const float4 f = *(const float4 *)(src + c);
-                    h4 hv;
-                    hv[0] = (_Float16)f.x; hv[1] = (_Float16)f.y; hv[2] = (_Float16)f.z; hv[3] = (_Float16)f.w;
-                    *(h4 *)(dst + c) = hv;
+                    const float fv[4] = {f.x, f.y, f.z, f.w};
+                    *(h4 *)(dst + c) = E::pack4(fv);
                 }
             }
         } else {
-            for (int c = tid; c < rowlen; c += 256) dst[c] = (_Float16)(float)src[c];
+            uint16_t *d16 = (uint16_t *)dst;
+            for (int c = tid; c < rowlen; c += 256) d16[c] = E::bits((float)src[c]);
         }
     }
     // per-lane offsets of its 8 im2col entries inside a window
@@ -607,7 +618,7 @@ __global__ __launch_bounds__(256) void stem_kernel(StemParams p, int th, int rs,
         const int m = (n * p.OH + oy0 + oyl) * p.OW + ox;
 #pragma unroll
         for (int i = 0; i < NB; ++i) {
-            const f4 acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[i], b, f4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+            const f4 acc = E::mma(a[i], b, f4{0.f, 0.f, 0.f, 0.f});
             const int nbase = i * 16 + 4 * (lane >> 4);
             const int os = nbase >> 3, hoff = nbase & 7;
             if (ox >= p.OW || os >= p.ns) continue;
@@ -618,12 +629,9 @@ __global__ __launch_bounds__(256) void stem_kernel(StemParams p, int th, int rs,
             if (p.res) {
                 const h4 rv = *(const h4 *)((const _Float16 *)p.res + off);
 #pragma unroll
-                for (int r = 0; r < 4; ++r) v[r] = act_apply(v[r] + (float)rv[r], p.act2);
+                for (int r = 0; r < 4; ++r) v[r] = act_apply(v[r] + E::get4(rv, r), p.act2);
             }
-            h4 o;
-#pragma unroll
-            for (int r = 0; r < 4; ++r) o[r] = (_Float16)v[r];
-            *(h4 *)((_Float16 *)p.y + off) = o;
+            *(h4 *)((_Float16 *)p.y + off) = E::pack4(v);
         }
     }
 }
@@ -640,7 +648,7 @@ size_t stem_band_bytes(int th, int kh, int kw, int c, int w, int ow, int sh, int
     return (size_t)nrows * stem_row_stride(c, w, ow, sw, kw, dw, pl) * 2;
 }
 
-template <typename TIN>
+template <typename E, typename TIN>
 static hipError_t launch_stem_t(const StemParams &p, hipStream_t st) {
     // band of th output rows: enough workgroups to fill the chip when possible
     // and a band that fits 64 KiB of LDS
@@ -654,10 +662,10 @@ static hipError_t launch_stem_t(const StemParams &p, hipStream_t st) {
     if (lds > 65536) return hipErrorInvalidValue;
     const dim3 grid(p.N * ((p.OH + th - 1) / th)), block(256);
     switch (p.nb16) {
-        case 1: launch((stem_kernel<TIN, 1>), grid, block, lds, st, p, th, rs, nrows); break;
-        case 2: launch((stem_kernel<TIN, 2>), grid, block, lds, st, p, th, rs, nrows); break;
-        case 3: launch((stem_kernel<TIN, 3>), grid, block, lds, st, p, th, rs, nrows); break;
-        case 4: launch((stem_kernel<TIN, 4>), grid, block, lds, st, p, th, rs, nrows); break;
+        case 1: launch((stem_kernel<E, TIN, 1>), grid, block, lds, st, p, th, rs, nrows); break;
+        case 2: launch((stem_kernel<E, TIN, 2>), grid, block, lds, st, p, th, rs, nrows); break;
+        case 3: launch((stem_kernel<E, TIN, 3>), grid, block, lds, st, p, th, rs, nrows); break;
+        case 4: launch((stem_kernel<E, TIN, 4>), grid, block, lds, st, p, th, rs, nrows); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -665,7 +673,8 @@ static hipError_t launch_stem_t(const StemParams &p, hipStream_t st) {
 
 hipError_t launch_stem(const StemParams &p, bool fp16_in, hipStream_t st) {
     if (p.M <= 0) return hipSuccess;
-    return fp16_in ? launch_stem_t<_Float16>(p, st) : launch_stem_t<float>(p, st);
+    if (p.bf16) return fp16_in ? launch_stem_t<BF16, _Float16>(p, st) : launch_stem_t<BF16, float>(p, st);
+    return fp16_in ? launch_stem_t<F16, _Float16>(p, st) : launch_stem_t<F16, float>(p, st);
 }
 
 }  // namespace kern

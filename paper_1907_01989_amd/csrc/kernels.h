@@ -42,6 +42,7 @@ struct GemmParams {
     int nb16, ns, cout;  // output blocks of 16, output slices, channels
     int act1, act2;
     int mtiles, ntiles;
+    int bf16;            // storage type: 0 fp16, 1 bf16
     // implicit-GEMM window geometry
     int H, W, OH, OW, sin, kw, sh, sw, dh, dw, pt, pl;
 };
@@ -94,6 +95,7 @@ struct StemParams {
     int N, H, W, C, OH, OW, M;
     int KH, KW, K, sh, sw, dh, dw, pt, pl;
     int nb16, ns, act1, act2;
+    int bf16;            // storage type: 0 fp16, 1 bf16
 };
 hipError_t launch_stem(const StemParams &p, bool fp16_in, hipStream_t st);
 // LDS bytes the stem kernel stages for a band of th output rows
@@ -107,17 +109,19 @@ struct DwParams {
     const h8 *zero;      // one zeroed 16-byte element (read for taps outside the input)
     h8 *y;
     int N, H, W, S, OH, OW, KH, KW, sh, sw, dh, dw, pt, pl, act;
+    int bf16;            // storage type: 0 fp16, 1 bf16
 };
 // rows: output rows per thread of the 3x3 kernel (1, 2, 4 or 8; 0 = default)
 hipError_t launch_depthwise(const DwParams &p, int rows, hipStream_t st);
 
-hipError_t launch_add(const h8 *a, const h8 *b, h8 *y, size_t count, int act, hipStream_t st);
+hipError_t launch_add(const h8 *a, const h8 *b, h8 *y, size_t count, int act, bool bf16, hipStream_t st);
 // zero padding of a sliced tensor: (N, H, W) planes of S slices -> (N, OH, OW),
 // input placed at row pt, column pl
 hipError_t launch_pad(const h8 *x, h8 *y, int N, int S, int H, int W, int OH, int OW, int pt, int pl,
                       hipStream_t st);
-hipError_t launch_act(const h8 *x, h8 *y, size_t count, int act, hipStream_t st);
-hipError_t launch_gap(const h8 *x, h8 *y, const h8 *zero, int N, int HW, int S, hipStream_t st);
+hipError_t launch_act(const h8 *x, h8 *y, size_t count, int act, bool bf16, hipStream_t st);
+hipError_t launch_gap(const h8 *x, h8 *y, const h8 *zero, int N, int HW, int S, bool bf16,
+                      hipStream_t st);
 hipError_t launch_softmax(const float *z, float *y, int rows, int cols, hipStream_t st);
 
 struct ConcatParams {
@@ -134,12 +138,13 @@ struct ResizeParams {
     void *y;             // sliced output, or int32 labels (argmax)
     int N, H, W, S, C, OH, OW;
     int align_corners;
+    int bf16;            // storage type: 0 fp16, 1 bf16
 };
 hipError_t launch_resize(const ResizeParams &p, bool argmax, hipStream_t st);
-hipError_t launch_argmax(const h8 *x, int *y, int M, int S, int C, hipStream_t st);
+hipError_t launch_argmax(const h8 *x, int *y, int M, int S, int C, bool bf16, hipStream_t st);
 
-hipError_t launch_ingest(const void *x, bool fp16_in, h8 *y, int M, int C, hipStream_t st);
-hipError_t launch_export(const h8 *x, float *y, int M, int C, hipStream_t st);
+hipError_t launch_ingest(const void *x, bool fp16_in, h8 *y, int M, int C, bool bf16, hipStream_t st);
+hipError_t launch_export(const h8 *x, float *y, int M, int C, bool bf16, hipStream_t st);
 
 }  // namespace kern
 }  // namespace mgi

@@ -39,6 +39,16 @@ uint16_t f32_to_f16_bits(float f) {
     return b;
 }
 
+// bf16: the upper half of the fp32 pattern, rounded to nearest even (NaN
+// kept quiet)
+uint16_t f32_to_bf16_bits(float f) {
+    uint32_t u;
+    std::memcpy(&u, &f, 4);
+    if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return (uint16_t)((u >> 16) | 0x40);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
 struct Group {
     int head = -1;          // heavy op
     int last = -1;          // last absorbed op (position and output tensor)
@@ -295,8 +305,9 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
     if (g.outputs.empty()) return fail(MGI_ERR_STATE, "mgi_graph_finalize: no output marked");
     if (o.planner != MGI_PLANNER_NAIVE && o.planner != MGI_PLANNER_GREEDY && o.planner != MGI_PLANNER_MCFP)
         return fail(MGI_ERR_UNSUPPORTED, "mgi_graph_finalize: unknown planner");
-    if (o.dtype != MGI_DTYPE_FP16)
-        return fail(MGI_ERR_UNSUPPORTED, "mgi_graph_finalize: only fp16 storage is built");
+    if (o.dtype != MGI_DTYPE_FP16 && o.dtype != MGI_DTYPE_BF16)
+        return fail(MGI_ERR_UNSUPPORTED, "mgi_graph_finalize: storage is fp16 or bf16");
+    auto to_bits = o.dtype == MGI_DTYPE_BF16 ? f32_to_bf16_bits : f32_to_f16_bits;
 
     const std::vector<char> live = live_ops(g);
     std::vector<char> is_output(nops, 0);
@@ -757,7 +768,7 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
             uint16_t *wp = reinterpret_cast<uint16_t *>(blob.data() + nd.dw_w_off);
             for (int ch = 0; ch < c; ++ch)
                 for (int t = 0; t < 9; ++t)
-                    wp[((size_t)(ch / 8) * 9 + t) * 8 + ch % 8] = f32_to_f16_bits(dop.w[(size_t)ch * 9 + t]);
+                    wp[((size_t)(ch / 8) * 9 + t) * 8 + ch % 8] = to_bits(dop.w[(size_t)ch * 9 + t]);
             nd.dw_b_off = reserve((size_t)S * 8 * 4);
             float *bp = reinterpret_cast<float *>(blob.data() + nd.dw_b_off);
             for (int ch = 0; ch < c; ++ch) bp[ch] = dop.b[ch];
@@ -788,7 +799,7 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
                                 j = ci % 8;
                             }
                             float v = op.w[(((size_t)co * kh + ky) * kw + kx) * cin + ci];
-                            wp[(((size_t)nb * nd.ksp + ks) * 16 + row) * 8 + j] = f32_to_f16_bits(v);
+                            wp[(((size_t)nb * nd.ksp + ks) * 16 + row) * 8 + j] = to_bits(v);
                         }
             }
             nd.b_bytes = (size_t)nd.nb16 * 16 * 4;
@@ -804,7 +815,7 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
             for (int ch = 0; ch < c; ++ch)
                 for (int t = 0; t < taps; ++t)
                     wp[((size_t)(ch / 8) * taps + t) * 8 + ch % 8] =
-                        f32_to_f16_bits(op.w[(size_t)ch * taps + t]);
+                        to_bits(op.w[(size_t)ch * taps + t]);
             nd.b_bytes = (size_t)S * 8 * 4;
             nd.b_off = reserve(nd.b_bytes);
             float *bp = reinterpret_cast<float *>(blob.data() + nd.b_off);

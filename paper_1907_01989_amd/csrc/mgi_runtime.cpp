@@ -48,15 +48,17 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
     const Buf &ob = p.bufs[nd.out];
     const Shape os = ob.shape;
     void *y = buf_ptr(p, nd.out, B);
+    const bool bf = p.opt.dtype == MGI_DTYPE_BF16;
     switch (nd.kind) {
         case NodeKind::Ingest: {
             const Buf &ib = p.bufs[nd.in[0]];
             return launch_ingest(buf_ptr(p, nd.in[0], B), ib.in_dtype == MGI_DTYPE_FP16, (h8 *)y,
-                                 (int)ib.shape.pixels(), ib.shape.c, st);
+                                 (int)ib.shape.pixels(), ib.shape.c, bf, st);
         }
         case NodeKind::Stem: {
             const Buf &ib = p.bufs[nd.in[0]];
             StemParams q{};
+            q.bf16 = bf;
             q.x = buf_ptr(p, nd.in[0], B);
             q.w = (const h8 *)(wbase + nd.w_off);
             q.bias = (const float *)(wbase + nd.b_off);
@@ -76,6 +78,7 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
         case NodeKind::FC: {
             const Buf &ib = p.bufs[nd.in[0]];
             GemmParams q{};
+            q.bf16 = bf;
             q.x = (const h8 *)buf_ptr(p, nd.in[0], B);
             q.w = (const h8 *)(wbase + nd.w_off);
             q.bias = (const float *)(wbase + nd.b_off);
@@ -107,6 +110,7 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
             q.sh = nd.dw_conv.stride_h; q.sw = nd.dw_conv.stride_w;
             q.pt = nd.dw_conv.pad_t; q.pl = nd.dw_conv.pad_l; q.act = nd.dw_act;
             GemmParams &g = q.g;
+            g.bf16 = bf;
             g.w = (const h8 *)(wbase + nd.w_off);
             g.bias = (const float *)(wbase + nd.b_off);
             g.res = nd.residual >= 0 ? (const h8 *)buf_ptr(p, nd.residual, B) : nullptr;
@@ -124,6 +128,7 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
         case NodeKind::Depthwise: {
             const Buf &ib = p.bufs[nd.in[0]];
             DwParams q{};
+            q.bf16 = bf;
             q.x = (const h8 *)buf_ptr(p, nd.in[0], B);
             q.w = (const h8 *)(wbase + nd.w_off);
             q.bias = (const float *)(wbase + nd.b_off);
@@ -139,15 +144,15 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
         }
         case NodeKind::Add:
             return launch_add((const h8 *)buf_ptr(p, nd.in[0], B), (const h8 *)buf_ptr(p, nd.in[1], B),
-                              (h8 *)y, (size_t)slices(os.c) * os.pixels(), nd.act1, st);
+                              (h8 *)y, (size_t)slices(os.c) * os.pixels(), nd.act1, bf, st);
         case NodeKind::Act:
             return launch_act((const h8 *)buf_ptr(p, nd.in[0], B), (h8 *)y,
-                              (size_t)slices(os.c) * os.pixels(), nd.act1, st);
+                              (size_t)slices(os.c) * os.pixels(), nd.act1, bf, st);
         case NodeKind::Gap: {
             const Buf &ib = p.bufs[nd.in[0]];
             return launch_gap((const h8 *)buf_ptr(p, nd.in[0], B), (h8 *)y,
                               (const h8 *)(wbase + p.zero_off), ib.shape.n,
-                              ib.shape.h * ib.shape.w, slices(ib.shape.c), st);
+                              ib.shape.h * ib.shape.w, slices(ib.shape.c), bf, st);
         }
         case NodeKind::Softmax:
             return launch_softmax((const float *)buf_ptr(p, nd.in[0], B), (float *)y,
@@ -182,17 +187,18 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
             q.S = slices(ib.shape.c); q.C = ib.shape.c;
             q.OH = os.h; q.OW = os.w;
             q.align_corners = nd.align_corners;
+            q.bf16 = bf;
             return launch_resize(q, nd.kind == NodeKind::ResizeArgmax, st);
         }
         case NodeKind::Argmax: {
             const Buf &ib = p.bufs[nd.in[0]];
             return launch_argmax((const h8 *)buf_ptr(p, nd.in[0], B), (int *)y,
-                                 (int)ib.shape.pixels(), slices(ib.shape.c), ib.shape.c, st);
+                                 (int)ib.shape.pixels(), slices(ib.shape.c), ib.shape.c, bf, st);
         }
         case NodeKind::Export: {
             const Buf &ib = p.bufs[nd.in[0]];
             return launch_export((const h8 *)buf_ptr(p, nd.in[0], B), (float *)y,
-                                 (int)ib.shape.pixels(), ib.shape.c, st);
+                                 (int)ib.shape.pixels(), ib.shape.c, bf, st);
         }
     }
     return hipErrorInvalidValue;
@@ -450,7 +456,8 @@ extern "C" mgi_status mgi_plan_read_node(mgi_plan *p, int i, void *dev_dst, void
     void *src = buf_ptr(*p, nd.out, B);
     hipError_t e;
     if (b.layout == Layout::C8) {
-        e = launch_export((const h8 *)src, (float *)dev_dst, (int)b.shape.pixels(), b.shape.c, st);
+        e = launch_export((const h8 *)src, (float *)dev_dst, (int)b.shape.pixels(), b.shape.c,
+                          p->opt.dtype == MGI_DTYPE_BF16, st);
     } else {
         e = hipMemcpyAsync(dev_dst, src, b.bytes, hipMemcpyDeviceToDevice, st);
     }

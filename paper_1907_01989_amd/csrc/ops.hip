@@ -35,7 +35,7 @@ LaunchEvents &launch_events() {
 // Launch: 1-D, thread g -> column g % OW, strip (g / OW) % nstrips, plane
 // g / (OW * nstrips) (plane = slice * N + image).
 // ---------------------------------------------------------------------------
-template <int S_, int D_, int R>
+template <typename E, int S_, int D_, int R>
 __global__ __launch_bounds__(256) void dw3_kernel(DwParams p, int nstrips) {
     constexpr int NR = (R - 1) * S_ + 2 * D_ + 1;
     const int g = blockIdx.x * 256 + threadIdx.x;
@@ -48,9 +48,9 @@ __global__ __launch_bounds__(256) void dw3_kernel(DwParams p, int nstrips) {
     const int oy0 = strip * R;
     const h8 *xin = p.x + (size_t)plane * p.H * p.W;
     const h8 *wp = p.w + (size_t)s * 9;
-    u4x w[9];
+    h8 w[9];
 #pragma unroll
-    for (int t = 0; t < 9; ++t) w[t] = as_u4(wp[t]);
+    for (int t = 0; t < 9; ++t) w[t] = wp[t];
     const int iy0 = oy0 * S_ - p.pt, ix0 = ox * S_ - p.pl;
     int cx[3];
     bool cv[3];
@@ -59,14 +59,14 @@ __global__ __launch_bounds__(256) void dw3_kernel(DwParams p, int nstrips) {
         cx[k] = ix0 + k * D_;
         cv[k] = cx[k] >= 0 && cx[k] < p.W;
     }
-    u4x v[NR][3];
+    h8 v[NR][3];
 #pragma unroll
     for (int r = 0; r < NR; ++r) {
         const int iy = iy0 + r;
         const bool rv = iy >= 0 && iy < p.H;
 #pragma unroll
         for (int k = 0; k < 3; ++k)
-            v[r][k] = as_u4(*((rv && cv[k]) ? xin + (size_t)iy * p.W + cx[k] : p.zero));
+            v[r][k] = *((rv && cv[k]) ? xin + (size_t)iy * p.W + cx[k] : p.zero);
     }
     float acc[R][8];
 #pragma unroll
@@ -80,7 +80,7 @@ __global__ __launch_bounds__(256) void dw3_kernel(DwParams p, int nstrips) {
             const int t = r - ky * D_;
             if (t >= 0 && t % S_ == 0 && t / S_ < R) {
 #pragma unroll
-                for (int k = 0; k < 3; ++k) fma8(acc[t / S_], w[ky * 3 + k], v[r][k]);
+                for (int k = 0; k < 3; ++k) E::fma8(acc[t / S_], w[ky * 3 + k], v[r][k]);
             }
         }
     // activation as one clamp: [lo, hi] = (-inf, inf), (0, inf) or (0, 6)
@@ -90,15 +90,16 @@ __global__ __launch_bounds__(256) void dw3_kernel(DwParams p, int nstrips) {
 #pragma unroll
     for (int o = 0; o < R; ++o) {
         if (oy0 + o >= p.OH) break;
-        h8 q;
+        float q[8];
 #pragma unroll
-        for (int c = 0; c < 8; ++c) q[c] = (_Float16)__builtin_amdgcn_fmed3f(acc[o][c], lo, hi);
-        yout[(size_t)(oy0 + o) * p.OW] = q;
+        for (int c = 0; c < 8; ++c) q[c] = __builtin_amdgcn_fmed3f(acc[o][c], lo, hi);
+        yout[(size_t)(oy0 + o) * p.OW] = E::pack(q);
     }
 }
 
 // Any window size: one thread per output pixel of one slice, fp32
 // accumulation over the kh x kw window.
+template <typename E>
 __global__ __launch_bounds__(256) void dw_kernel(DwParams p, int tpp) {
     const int plane = blockIdx.x / tpp;
     const int pix = (blockIdx.x - plane * tpp) * 256 + threadIdx.x;
@@ -120,21 +121,20 @@ __global__ __launch_bounds__(256) void dw_kernel(DwParams p, int tpp) {
             const h8 v = xin[(size_t)iy * p.W + ix];
             const h8 wk = wt[ky * p.KW + kx];
 #pragma unroll
-            for (int c = 0; c < 8; ++c) acc[c] = fmaf((float)wk[c], (float)v[c], acc[c]);
+            for (int c = 0; c < 8; ++c) acc[c] = fmaf(E::get(wk, c), E::get(v, c), acc[c]);
         }
     }
-    h8 o;
 #pragma unroll
-    for (int c = 0; c < 8; ++c) o[c] = (_Float16)act_apply(acc[c], p.act);
-    p.y[(size_t)plane * ohw + pix] = o;
+    for (int c = 0; c < 8; ++c) acc[c] = act_apply(acc[c], p.act);
+    p.y[(size_t)plane * ohw + pix] = E::pack(acc);
 }
 
-template <int S_, int D_, int R>
+template <typename E, int S_, int D_, int R>
 static hipError_t launch_dw3(const DwParams &p, hipStream_t st) {
     const int nstrips = (p.OH + R - 1) / R;
     const size_t threads = (size_t)p.OW * nstrips * p.S * p.N;
     if (threads > 0x7fffffffull) return hipErrorInvalidValue;
-    launch((dw3_kernel<S_, D_, R>), dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, st,
+    launch((dw3_kernel<E, S_, D_, R>), dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, st,
                        p, nstrips);
     return hipGetLastError();
 }
@@ -146,7 +146,8 @@ hipError_t launch_depthwise(const DwParams &p, int rows, hipStream_t st) {
         // output rows per thread: 4 at stride 1, 2 at stride 2 unless chosen
         const int R = rows > 0 ? rows : (p.sh == 1 ? 4 : 2);
 #define MGI_DW_CASE(S_, D_, R_) \
-        if (p.sh == S_ && p.dh == D_ && R == R_) return launch_dw3<S_, D_, R_>(p, st);
+        if (p.sh == S_ && p.dh == D_ && R == R_) \
+            return p.bf16 ? launch_dw3<BF16, S_, D_, R_>(p, st) : launch_dw3<F16, S_, D_, R_>(p, st);
         MGI_DW_CASE(1, 1, 2) MGI_DW_CASE(1, 1, 4) MGI_DW_CASE(1, 1, 8)
         MGI_DW_CASE(2, 1, 1) MGI_DW_CASE(2, 1, 2) MGI_DW_CASE(2, 1, 4)
         MGI_DW_CASE(1, 2, 2) MGI_DW_CASE(1, 2, 4) MGI_DW_CASE(1, 2, 8)
@@ -157,7 +158,8 @@ hipError_t launch_depthwise(const DwParams &p, int rows, hipStream_t st) {
     const int tpp = (ohw + 255) / 256;
     const size_t nblk = (size_t)tpp * p.S * p.N;
     if (nblk > 0x7fffffffu) return hipErrorInvalidValue;
-    launch(dw_kernel, dim3((unsigned)nblk), dim3(256), 0, st, p, tpp);
+    if (p.bf16) launch(dw_kernel<BF16>, dim3((unsigned)nblk), dim3(256), 0, st, p, tpp);
+    else launch(dw_kernel<F16>, dim3((unsigned)nblk), dim3(256), 0, st, p, tpp);
     return hipGetLastError();
 }
 
@@ -195,35 +197,39 @@ hipError_t launch_pad(const h8 *x, h8 *y, int N, int S, int H, int W, int OH, in
 // ---------------------------------------------------------------------------
 // element-wise
 // ---------------------------------------------------------------------------
+template <typename E>
 __global__ __launch_bounds__(256) void add_kernel(const h8 *a, const h8 *b, h8 *y, size_t n, int act) {
     const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
     if (i >= n) return;
     const h8 u = a[i], v = b[i];
-    h8 o;
+    float o[8];
 #pragma unroll
-    for (int c = 0; c < 8; ++c) o[c] = (_Float16)act_apply((float)u[c] + (float)v[c], act);
-    y[i] = o;
+    for (int c = 0; c < 8; ++c) o[c] = act_apply(E::get(u, c) + E::get(v, c), act);
+    y[i] = E::pack(o);
 }
 
-hipError_t launch_add(const h8 *a, const h8 *b, h8 *y, size_t count, int act, hipStream_t st) {
+hipError_t launch_add(const h8 *a, const h8 *b, h8 *y, size_t count, int act, bool bf16, hipStream_t st) {
     if (!count) return hipSuccess;
-    launch(add_kernel, dim3(blocks_for(count, 256)), dim3(256), 0, st, a, b, y, count, act);
+    if (bf16) launch(add_kernel<BF16>, dim3(blocks_for(count, 256)), dim3(256), 0, st, a, b, y, count, act);
+    else launch(add_kernel<F16>, dim3(blocks_for(count, 256)), dim3(256), 0, st, a, b, y, count, act);
     return hipGetLastError();
 }
 
+template <typename E>
 __global__ __launch_bounds__(256) void act_kernel(const h8 *x, h8 *y, size_t n, int act) {
     const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
     if (i >= n) return;
     const h8 u = x[i];
-    h8 o;
+    float o[8];
 #pragma unroll
-    for (int c = 0; c < 8; ++c) o[c] = (_Float16)act_apply((float)u[c], act);
-    y[i] = o;
+    for (int c = 0; c < 8; ++c) o[c] = act_apply(E::get(u, c), act);
+    y[i] = E::pack(o);
 }
 
-hipError_t launch_act(const h8 *x, h8 *y, size_t count, int act, hipStream_t st) {
+hipError_t launch_act(const h8 *x, h8 *y, size_t count, int act, bool bf16, hipStream_t st) {
     if (!count) return hipSuccess;
-    launch(act_kernel, dim3(blocks_for(count, 256)), dim3(256), 0, st, x, y, count, act);
+    if (bf16) launch(act_kernel<BF16>, dim3(blocks_for(count, 256)), dim3(256), 0, st, x, y, count, act);
+    else launch(act_kernel<F16>, dim3(blocks_for(count, 256)), dim3(256), 0, st, x, y, count, act);
     return hipGetLastError();
 }
 
@@ -232,6 +238,7 @@ hipError_t launch_act(const h8 *x, h8 *y, size_t count, int act, hipStream_t st)
 // pixels, then a fixed butterfly reduction (deterministic).  Output is the
 // sliced (n, 1, 1, c) tensor in fp16.
 // ---------------------------------------------------------------------------
+template <typename E>
 __global__ __launch_bounds__(256) void gap_kernel(const h8 *x, h8 *y, int N, int HW, int S) {
     const int lane = threadIdx.x & 63;
     const int idx = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -243,7 +250,7 @@ __global__ __launch_bounds__(256) void gap_kernel(const h8 *x, h8 *y, int N, int
     for (int p = lane; p < HW; p += 64) {
         const h8 v = xin[p];
 #pragma unroll
-        for (int c = 0; c < 8; ++c) acc[c] += (float)v[c];
+        for (int c = 0; c < 8; ++c) acc[c] += E::get(v, c);
     }
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1)
@@ -251,10 +258,9 @@ __global__ __launch_bounds__(256) void gap_kernel(const h8 *x, h8 *y, int N, int
         for (int c = 0; c < 8; ++c) acc[c] += __shfl_xor(acc[c], off, 64);
     if (lane == 0) {
         const float inv = 1.0f / (float)HW;
-        h8 o;
 #pragma unroll
-        for (int c = 0; c < 8; ++c) o[c] = (_Float16)(acc[c] * inv);
-        y[idx] = o;
+        for (int c = 0; c < 8; ++c) acc[c] *= inv;
+        y[idx] = E::pack(acc);
     }
 }
 
@@ -262,6 +268,7 @@ __global__ __launch_bounds__(256) void gap_kernel(const h8 *x, h8 *y, int N, int
 // pixels j, j+8, ... with all loads issued at once (pixels past the end read
 // the zero element instead of branching), then a 3-step butterfly inside the
 // 8-lane group.  Fixed order, so deterministic.
+template <typename E>
 __global__ __launch_bounds__(256) void gap_small_kernel(const h8 *x, h8 *y, const h8 *zero,
                                                         int planes, int HW) {
     const int t = blockIdx.x * 256 + threadIdx.x;
@@ -279,7 +286,7 @@ __global__ __launch_bounds__(256) void gap_small_kernel(const h8 *x, h8 *y, cons
     for (int c = 0; c < 8; ++c) {
         float a = 0.0f;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) a += (float)v[i][c];
+        for (int i = 0; i < 8; ++i) a += E::get(v[i], c);
         acc[c] = a;
     }
 #pragma unroll
@@ -288,21 +295,26 @@ __global__ __launch_bounds__(256) void gap_small_kernel(const h8 *x, h8 *y, cons
         for (int c = 0; c < 8; ++c) acc[c] += __shfl_xor(acc[c], off, 8);
     if (live && j == 0) {
         const float inv = 1.0f / (float)HW;
-        h8 o;
 #pragma unroll
-        for (int c = 0; c < 8; ++c) o[c] = (_Float16)(acc[c] * inv);
-        y[idx] = o;
+        for (int c = 0; c < 8; ++c) acc[c] *= inv;
+        y[idx] = E::pack(acc);
     }
 }
 
-hipError_t launch_gap(const h8 *x, h8 *y, const h8 *zero, int N, int HW, int S, hipStream_t st) {
+hipError_t launch_gap(const h8 *x, h8 *y, const h8 *zero, int N, int HW, int S, bool bf16,
+                      hipStream_t st) {
     const size_t planes = (size_t)S * N;
     if (!planes) return hipSuccess;
     if (HW <= 64) {
-        launch(gap_small_kernel, dim3(blocks_for(planes * 8, 256)), dim3(256), 0, st, x, y,
-                           zero, (int)planes, HW);
+        if (bf16)
+            launch(gap_small_kernel<BF16>, dim3(blocks_for(planes * 8, 256)), dim3(256), 0, st, x, y, zero,
+                   (int)planes, HW);
+        else
+            launch(gap_small_kernel<F16>, dim3(blocks_for(planes * 8, 256)), dim3(256), 0, st, x, y, zero,
+                   (int)planes, HW);
     } else {
-        launch(gap_kernel, dim3(blocks_for(planes, 4)), dim3(256), 0, st, x, y, N, HW, S);
+        if (bf16) launch(gap_kernel<BF16>, dim3(blocks_for(planes, 4)), dim3(256), 0, st, x, y, N, HW, S);
+        else launch(gap_kernel<F16>, dim3(blocks_for(planes, 4)), dim3(256), 0, st, x, y, N, HW, S);
     }
     return hipGetLastError();
 }
@@ -373,7 +385,8 @@ __global__ __launch_bounds__(256) void concat_kernel(ConcatParams p) {
     if (i >= (size_t)p.S * p.M) return;
     const int s = (int)(i / p.M);
     const int m = (int)(i - (size_t)s * p.M);
-    h8 o = zero_h8();
+    // 16-bit values are moved as raw bits (the same for fp16 and bf16 storage)
+    u16x8 o = {0, 0, 0, 0, 0, 0, 0, 0};
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
         const int c = s * 8 + j;
@@ -381,9 +394,9 @@ __global__ __launch_bounds__(256) void concat_kernel(ConcatParams p) {
         int k = 0;
         while (k + 1 < p.nin && c >= p.coff[k + 1]) ++k;
         const int cc = c - p.coff[k];
-        o[j] = ((const _Float16 *)p.src[k])[((size_t)(cc >> 3) * p.M + m) * 8 + (cc & 7)];
+        o[j] = ((const uint16_t *)p.src[k])[((size_t)(cc >> 3) * p.M + m) * 8 + (cc & 7)];
     }
-    p.y[i] = o;
+    p.y[i] = __builtin_bit_cast(h8, o);
 }
 
 hipError_t launch_concat(const ConcatParams &p, hipStream_t st) {
@@ -411,6 +424,7 @@ __device__ __forceinline__ Lerp lerp_coord(int d, int in, int out, int align_cor
     return Lerp{i0, i1, src - (float)i0};
 }
 
+template <typename E>
 __global__ __launch_bounds__(256) void resize_kernel(ResizeParams p) {
     const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
     const size_t opix = (size_t)p.N * p.OH * p.OW;
@@ -425,16 +439,17 @@ __global__ __launch_bounds__(256) void resize_kernel(ResizeParams p) {
     const h8 *plane = p.x + ((size_t)s * p.N + n) * p.H * p.W;
     const h8 v00 = plane[(size_t)ly.i0 * p.W + lx.i0], v01 = plane[(size_t)ly.i0 * p.W + lx.i1];
     const h8 v10 = plane[(size_t)ly.i1 * p.W + lx.i0], v11 = plane[(size_t)ly.i1 * p.W + lx.i1];
-    h8 o;
+    float o[8];
 #pragma unroll
     for (int c = 0; c < 8; ++c) {
-        const float top = (1.0f - lx.f) * (float)v00[c] + lx.f * (float)v01[c];
-        const float bot = (1.0f - lx.f) * (float)v10[c] + lx.f * (float)v11[c];
-        o[c] = (_Float16)((1.0f - ly.f) * top + ly.f * bot);
+        const float top = (1.0f - lx.f) * E::get(v00, c) + lx.f * E::get(v01, c);
+        const float bot = (1.0f - lx.f) * E::get(v10, c) + lx.f * E::get(v11, c);
+        o[c] = (1.0f - ly.f) * top + ly.f * bot;
     }
-    ((h8 *)p.y)[i] = o;
+    ((h8 *)p.y)[i] = E::pack(o);
 }
 
+template <typename E>
 __global__ __launch_bounds__(256) void resize_argmax_kernel(ResizeParams p) {
     const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
     const size_t opix = (size_t)p.N * p.OH * p.OW;
@@ -454,8 +469,8 @@ __global__ __launch_bounds__(256) void resize_argmax_kernel(ResizeParams p) {
         for (int c = 0; c < 8; ++c) {
             const int ch = s * 8 + c;
             if (ch >= p.C) break;
-            const float top = (1.0f - lx.f) * (float)v00[c] + lx.f * (float)v01[c];
-            const float bot = (1.0f - lx.f) * (float)v10[c] + lx.f * (float)v11[c];
+            const float top = (1.0f - lx.f) * E::get(v00, c) + lx.f * E::get(v01, c);
+            const float bot = (1.0f - lx.f) * E::get(v10, c) + lx.f * E::get(v11, c);
             const float v = (1.0f - ly.f) * top + ly.f * bot;
             if (ch == 0 || v > best) {
                 best = v;
@@ -470,13 +485,16 @@ hipError_t launch_resize(const ResizeParams &p, bool argmax, hipStream_t st) {
     const size_t opix = (size_t)p.N * p.OH * p.OW;
     if (!opix) return hipSuccess;
     if (argmax) {
-        launch(resize_argmax_kernel, dim3(blocks_for(opix, 256)), dim3(256), 0, st, p);
+        if (p.bf16) launch(resize_argmax_kernel<BF16>, dim3(blocks_for(opix, 256)), dim3(256), 0, st, p);
+        else launch(resize_argmax_kernel<F16>, dim3(blocks_for(opix, 256)), dim3(256), 0, st, p);
     } else {
-        launch(resize_kernel, dim3(blocks_for(opix * p.S, 256)), dim3(256), 0, st, p);
+        if (p.bf16) launch(resize_kernel<BF16>, dim3(blocks_for(opix * p.S, 256)), dim3(256), 0, st, p);
+        else launch(resize_kernel<F16>, dim3(blocks_for(opix * p.S, 256)), dim3(256), 0, st, p);
     }
     return hipGetLastError();
 }
 
+template <typename E>
 __global__ __launch_bounds__(256) void argmax_kernel(const h8 *x, int *y, int M, int S, int C) {
     const int m = blockIdx.x * 256 + threadIdx.x;
     if (m >= M) return;
@@ -488,7 +506,7 @@ __global__ __launch_bounds__(256) void argmax_kernel(const h8 *x, int *y, int M,
         for (int c = 0; c < 8; ++c) {
             const int ch = s * 8 + c;
             if (ch >= C) break;
-            const float f = (float)v[c];
+            const float f = E::get(v, c);
             if (ch == 0 || f > best) {
                 best = f;
                 arg = ch;
@@ -498,9 +516,10 @@ __global__ __launch_bounds__(256) void argmax_kernel(const h8 *x, int *y, int M,
     y[m] = arg;
 }
 
-hipError_t launch_argmax(const h8 *x, int *y, int M, int S, int C, hipStream_t st) {
+hipError_t launch_argmax(const h8 *x, int *y, int M, int S, int C, bool bf16, hipStream_t st) {
     if (M <= 0) return hipSuccess;
-    launch(argmax_kernel, dim3(blocks_for(M, 256)), dim3(256), 0, st, x, y, M, S, C);
+    if (bf16) launch(argmax_kernel<BF16>, dim3(blocks_for(M, 256)), dim3(256), 0, st, x, y, M, S, C);
+    else launch(argmax_kernel<F16>, dim3(blocks_for(M, 256)), dim3(256), 0, st, x, y, M, S, C);
     return hipGetLastError();
 }
 
@@ -509,32 +528,37 @@ hipError_t launch_argmax(const h8 *x, int *y, int M, int S, int C, hipStream_t s
 // per (pixel, slice) with the slice index fastest, so a wave reads one
 // contiguous run of NHWC memory.
 // ---------------------------------------------------------------------------
-template <typename TIN>
+template <typename E, typename TIN>
 __global__ __launch_bounds__(256) void ingest_kernel(const TIN *x, h8 *y, int M, int C, int S) {
     const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
     if (i >= (size_t)M * S) return;
     const int m = (int)(i / S), s = (int)(i - (size_t)m * S);
     const TIN *src = x + (size_t)m * C + s * 8;
-    h8 o = zero_h8();
+    float o[8];
 #pragma unroll
-    for (int c = 0; c < 8; ++c)
-        if (s * 8 + c < C) o[c] = (_Float16)(float)src[c];
-    y[(size_t)s * M + m] = o;
+    for (int c = 0; c < 8; ++c) o[c] = s * 8 + c < C ? (float)src[c] : 0.0f;
+    y[(size_t)s * M + m] = E::pack(o);
 }
 
-hipError_t launch_ingest(const void *x, bool fp16_in, h8 *y, int M, int C, hipStream_t st) {
+template <typename E>
+static hipError_t launch_ingest_e(const void *x, bool fp16_in, h8 *y, int M, int C, hipStream_t st) {
     const int S = (C + 7) / 8;
     const size_t n = (size_t)M * S;
     if (!n) return hipSuccess;
     if (fp16_in)
-        launch((ingest_kernel<_Float16>), dim3(blocks_for(n, 256)), dim3(256), 0, st,
+        launch((ingest_kernel<E, _Float16>), dim3(blocks_for(n, 256)), dim3(256), 0, st,
                            (const _Float16 *)x, y, M, C, S);
     else
-        launch((ingest_kernel<float>), dim3(blocks_for(n, 256)), dim3(256), 0, st,
+        launch((ingest_kernel<E, float>), dim3(blocks_for(n, 256)), dim3(256), 0, st,
                            (const float *)x, y, M, C, S);
     return hipGetLastError();
 }
 
+hipError_t launch_ingest(const void *x, bool fp16_in, h8 *y, int M, int C, bool bf16, hipStream_t st) {
+    return bf16 ? launch_ingest_e<BF16>(x, fp16_in, y, M, C, st) : launch_ingest_e<F16>(x, fp16_in, y, M, C, st);
+}
+
+template <typename E>
 __global__ __launch_bounds__(256) void export_kernel(const h8 *x, float *y, int M, int C, int S) {
     const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
     if (i >= (size_t)M * S) return;
@@ -543,14 +567,15 @@ __global__ __launch_bounds__(256) void export_kernel(const h8 *x, float *y, int 
     float *dst = y + (size_t)m * C + s * 8;
 #pragma unroll
     for (int c = 0; c < 8; ++c)
-        if (s * 8 + c < C) dst[c] = (float)v[c];
+        if (s * 8 + c < C) dst[c] = E::get(v, c);
 }
 
-hipError_t launch_export(const h8 *x, float *y, int M, int C, hipStream_t st) {
+hipError_t launch_export(const h8 *x, float *y, int M, int C, bool bf16, hipStream_t st) {
     const int S = (C + 7) / 8;
     const size_t n = (size_t)M * S;
     if (!n) return hipSuccess;
-    launch(export_kernel, dim3(blocks_for(n, 256)), dim3(256), 0, st, x, y, M, C, S);
+    if (bf16) launch(export_kernel<BF16>, dim3(blocks_for(n, 256)), dim3(256), 0, st, x, y, M, C, S);
+    else launch(export_kernel<F16>, dim3(blocks_for(n, 256)), dim3(256), 0, st, x, y, M, C, S);
     return hipGetLastError();
 }
 

@@ -68,8 +68,10 @@ def build_graph(desc):
     return g
 
 
-def options(planner=B.PLANNER_GREEDY, fuse=True, materialize_all=False, fuse_dwpw=False):
+def options(planner=B.PLANNER_GREEDY, fuse=True, materialize_all=False, fuse_dwpw=False,
+            dtype=B.DTYPE_FP16):
     o = B.mgi_options_default()
+    o.dtype = dtype
     o.planner = planner
     o.fuse = int(fuse)
     o.materialize_all = int(materialize_all)
@@ -81,11 +83,11 @@ class Plan:
     """A finalised, device-bound network."""
 
     def __init__(self, desc, planner=B.PLANNER_GREEDY, fuse=True, materialize_all=False,
-                 device="cuda:0", bind=True, fuse_dwpw=False):
+                 device="cuda:0", bind=True, fuse_dwpw=False, dtype=B.DTYPE_FP16):
         self.desc = desc
         g = build_graph(desc)
         try:
-            self.handle = B.mgi_graph_finalize(g, options(planner, fuse, materialize_all, fuse_dwpw))
+            self.handle = B.mgi_graph_finalize(g, options(planner, fuse, materialize_all, fuse_dwpw, dtype))
         finally:
             B.mgi_graph_destroy(g)
         self.device = device

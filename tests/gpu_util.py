@@ -29,11 +29,11 @@ def to_numpy(t):
     return t.detach().cpu().numpy()
 
 
-def run_gpu(desc, materialize_all=True, fuse=True, planner=None, fuse_dwpw=False):
+def run_gpu(desc, materialize_all=True, fuse=True, planner=None, fuse_dwpw=False, dtype=0):
     """Run ``desc`` once; returns (plan, outputs as numpy, {tensor id: node output})."""
     import torch
     from paper_1907_01989_amd import engine, _binding as B
-    kw = {"fuse_dwpw": fuse_dwpw}
+    kw = {"fuse_dwpw": fuse_dwpw, "dtype": dtype}
     if planner is not None:
         kw["planner"] = planner
     plan = engine.Plan(desc, fuse=fuse, materialize_all=materialize_all, **kw)
@@ -67,11 +67,15 @@ def check_layer(name, g, r, tol=LAYER_TOL):
     return ok, f"{name}: max|diff|={err:.3e} max|ref|={denom:.3e} ratio={err / max(denom, 1e-30):.3e}"
 
 
-def check_isolated(name, g, r):
+# bf16 storage: 8 significand bits, half an ulp is 2^-9 relative
+ISO_RTOL_BF16 = 2.0 ** -8
+
+
+def check_isolated(name, g, r, rtol=ISO_RTOL):
     g = np.asarray(g, np.float64)
     r = np.asarray(r, np.float64)
     assert g.shape == r.shape, (name, g.shape, r.shape)
-    bound = ISO_RTOL * np.abs(r) + ISO_ATOL_FRAC * max(float(np.abs(r).max()), 1e-30)
+    bound = rtol * np.abs(r) + ISO_ATOL_FRAC * max(float(np.abs(r).max()), 1e-30)
     bad = np.abs(g - r) > bound
     assert not bad.any(), (f"{name}: {int(bad.sum())} of {bad.size} elements out of bound; "
                            f"worst |diff|={float(np.abs(g - r).max()):.3e}")

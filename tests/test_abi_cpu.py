@@ -176,6 +176,19 @@ def test_identity_removal_and_pad_merge():
         assert sh[t] == tuple(ref[t])
 
 
+def test_storage_types():
+    d = workloads.WORKLOADS["mobilenet_v1"](1)
+    f16 = engine.Plan(d, bind=False)
+    bf = engine.Plan(d, bind=False, dtype=B.DTYPE_BF16)
+    assert bf.weight_bytes == f16.weight_bytes and bf.workspace_bytes == f16.workspace_bytes
+    g = engine.build_graph(d)
+    try:
+        o = engine.options(dtype=B.DTYPE_FP32)
+        assert err(B.mgi_graph_finalize, g, o) == 3
+    finally:
+        B.mgi_graph_destroy(g)
+
+
 def test_node_configuration_candidates():
     # every pointwise GEMM and 3x3 depthwise node offers several kernel
     # configurations; index 0 is the finalize-time choice

@@ -350,3 +350,18 @@ def test_store_fp16_rounds_stored_tensors_only():
     np.testing.assert_allclose(r16[p], pooled.astype(np.float16).astype(np.float64), rtol=0, atol=0)
     # logits are kept in fp32 by the engine: not rounded, computed from the rounded pool
     np.testing.assert_allclose(r16[z], oracle.fc(r16[p], d["ops"][z]["w"], d["ops"][z]["b"]), rtol=1e-15)
+
+
+def test_bf16_storage_rounding_matches_library():
+    # the oracle's bf16 storage emulation is round-to-nearest-even on the
+    # float32 pattern; torch's bfloat16 conversion is an independent route
+    torch = pytest.importorskip("torch")
+    x = np.concatenate([rnd(4000, 77) * 10.0 ** np.arange(-3, 5).repeat(500),
+                        np.array([1.0, 1.00390625, 1.01171875, -0.0, 3.3895314e38])])
+    ref = torch.tensor(x.astype(np.float32)).to(torch.bfloat16).float().numpy().astype(np.float64)
+    np.testing.assert_array_equal(oracle._round_bf16(x), ref)
+    g = workloads.NetBuilder(seed=1)
+    t = g.conv(g.input(1, 3, 3, 8, -1, 1), 8, 1)
+    g.mark_output(t)
+    out = oracle.run_graph(g.graph("b"), store_bf16=True)[t]
+    np.testing.assert_array_equal(out, oracle._round_bf16(out))

@@ -298,6 +298,28 @@ WORKLOADS = {
 }
 
 
+def bf16_round(a):
+    """Nearest bf16 value (ties to even) of each element, as float32."""
+    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) >> 16 << 16
+    return u.astype(np.uint32).view(np.float32).reshape(np.shape(a))
+
+
+def as_bf16_graph(graph):
+    """The same network with its input data and weights rounded to bf16 values
+    (biases stay fp32), so that a bf16-storage engine and the oracle consume
+    identical numbers."""
+    ops = []
+    for op in graph["ops"]:
+        op = dict(op)
+        if op["op"] == "input":
+            op["data"] = bf16_round(op["data"])
+        if "w" in op:
+            op["w"] = bf16_round(op["w"])
+        ops.append(op)
+    return {"name": graph["name"] + "_bf16", "ops": ops, "outputs": list(graph["outputs"])}
+
+
 def subset_batch(graph, images):
     """The same network applied to a subset of the batch images (batch entries
     are independent, so a sampled check can run the oracle on them alone)."""
