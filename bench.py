@@ -152,6 +152,16 @@ def node_work(desc, nodes, shapes, i):
                 dop["w"].size * 2 + dop["b"].size * 4)
         if h != t:
             byts += out_b          # fused residual operand
+    elif kind == "pw_dw":
+        # pointwise input in, depthwise output out; the pointwise output
+        # never reaches memory
+        p = head_of(op["in"])
+        pop = ops[p]
+        n, h_, w_, cin = shapes[pop["in"]]        # 1x1 stride 1: same plane
+        cmid = pop["cout"]
+        flops = 2.0 * n * h_ * w_ * cin * cmid + 2.0 * elems(t) * op["kh"] * op["kw"]
+        byts = (elems(pop["in"]) * 2 + out_b + pop["w"].size * 2 + pop["b"].size * 4 +
+                op["w"].size * 2 + op["b"].size * 4)
     elif kind == "dw_conv":
         flops = 2.0 * elems(t) * op["kh"] * op["kw"]
         byts = elems(op["in"]) * 2 + out_b + op["w"].size * 4 + op["b"].size * 4
@@ -178,7 +188,7 @@ def kernel_sources_hash():
     while the kernels it was measured on are unchanged."""
     import hashlib
     h = hashlib.sha1()
-    for f in ("gemm.hip", "ops.hip", "dwpw.hip", "device.h", "kernels.h"):
+    for f in ("gemm.hip", "ops.hip", "dwpw.hip", "pwdw.hip", "device.h", "kernels.h"):
         with open(os.path.join(ROOT, "paper_1907_01989_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -212,7 +222,8 @@ def roofline_entry(flops, byts, bound, seconds):
 
 
 # ---------------------------------------------------------------------------
-def run_workload(key, steps, warmup, hip, profile_steps=20, detail=True, tune=True, fuse_dwpw=False):
+def run_workload(key, steps, warmup, hip, profile_steps=20, detail=True, tune=True, fuse_dwpw=False,
+                 fuse_pwdw=True):
     import torch
     import workloads
     from paper_1907_01989_amd import _binding as B
@@ -220,7 +231,7 @@ def run_workload(key, steps, warmup, hip, profile_steps=20, detail=True, tune=Tr
 
     net, batch = WORKLOADS[key]
     desc = workloads.WORKLOADS[net](batch)
-    plan = engine.Plan(desc, fuse_dwpw=fuse_dwpw)
+    plan = engine.Plan(desc, fuse_dwpw=fuse_dwpw, fuse_pwdw=fuse_pwdw)
     xs = plan.input_tensors()
     outs = plan.alloc_outputs()
     stream = torch.cuda.current_stream()
@@ -374,6 +385,9 @@ def main():
     ap.add_argument("--fuse-dwpw", action="store_true",
                     help="fuse 3x3 depthwise convolutions into the pointwise convolutions "
                          "that consume them (mgi_options.fuse_dwpw)")
+    ap.add_argument("--no-fuse-pwdw", action="store_true",
+                    help="keep pointwise convolutions and the 3x3 depthwise convolutions "
+                         "that read them as separate kernels (mgi_options.fuse_pwdw = 0)")
     ap.add_argument("--no-autotune", action="store_true",
                     help="keep the finalize-time kernel configurations")
     ap.add_argument("--copy-only", type=int, default=0, metavar="MIB",
@@ -404,7 +418,7 @@ def main():
     eprint(f"[bench] workload {args.workload}: warmup {args.warmup}, steps {args.steps}")
     tune = not args.no_autotune
     main_res = run_workload(args.workload, args.steps, args.warmup, hip, tune=tune,
-                            fuse_dwpw=args.fuse_dwpw)
+                            fuse_dwpw=args.fuse_dwpw, fuse_pwdw=not args.no_fuse_pwdw)
     eprint(f"[bench] {main_res['images_per_s']:.1f} images/s, {main_res['ms_per_step']:.4f} ms/step")
     also = {}
     if not args.no_extra:
@@ -444,7 +458,8 @@ def main():
         "config": {"workload": main_res["desc"]["name"], "network": net, "batch": batch,
                    "input": "NHWC fp16 uniform[0,1], device-resident",
                    "weights": "He-normal seed 0, fp16", "planner": "greedy", "fused": True,
-                   "autotuned": tune, "dw_pw_fused": args.fuse_dwpw},
+                   "autotuned": tune, "dw_pw_fused": args.fuse_dwpw,
+                   "pw_dw_fused": not args.no_fuse_pwdw},
         "roofline": main_res["roofline"],
         "cpu_baseline": cpu,
         "per_layer": main_res["layers"],

@@ -106,6 +106,15 @@ typedef struct {
                             that convolution has at most 320 output channels and enough
                             pixels to fill the GPU; the depthwise output then never reaches
                             memory (default 0; needs fuse = 1) */
+    int fuse_pwdw;       /* run a 3x3 depthwise convolution (stride 1 or 2, no dilation, top
+                            and left padding of at most one) inside the pointwise convolution
+                            that produces its input, when that output feeds nothing else,
+                            planes are at most 16 x 16 and the channel count is a multiple of
+                            64; the pointwise output then never reaches memory (Sec. 3.2's
+                            fusion extended to the pointwise -> depthwise pair).  0: never;
+                            1 (default): when the fused kernel gets at least 128 workgroups
+                            (images per tile x channel tiles; below that the separate kernels
+                            are faster); 2: whenever the shapes allow.  Needs fuse = 1. */
 } mgi_options;
 
 /* ---------------------------------------------------------------------------

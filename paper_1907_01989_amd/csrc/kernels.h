@@ -114,6 +114,28 @@ struct DwParams {
 // rows: output rows per thread of the 3x3 kernel (1, 2, 4 or 8; 0 = default)
 hipError_t launch_depthwise(const DwParams &p, int rows, hipStream_t st);
 
+// Pointwise convolution fused with the depthwise 3x3 convolution (dilation 1,
+// stride 1 or 2) that consumes its output: a workgroup owns ipt whole images
+// and 16*NBT output channels, so the depthwise step needs no halo.
+struct PwDwParams {
+    const h8 *x;         // pointwise input, sliced [ksl][M]
+    const h8 *w;         // packed pointwise weights [nb16][ksp][16][8]
+    const float *bias;   // [nb16 * 16]
+    int M, ksl, ksp, nb16, act1;
+    const h4 *dw_t;      // depthwise taps per channel and kernel row, (w0, w1, w2, 0): [16 * nb16][3]
+    const float *dw_b;   // [16 * nb16]
+    h8 *y;               // depthwise output, sliced [2 * nb16][N * OH * OW]
+    int N, H, W, OH, OW, S, pt, pl, act2;
+    int ipt;             // images per tile
+    int ntiles;          // channel tiles (nb16 / NBT)
+    int bf16;            // storage type: 0 fp16, 1 bf16
+};
+// cfg selects the channels per tile (0: 128, 1: 64).  pwdw_supported tells
+// whether a shape is covered and gives the images per tile; launch_pwdw
+// returns hipErrorInvalidValue for anything else.
+bool pwdw_supported(int H, int W, int OH, int OW, int S, int pt, int pl, int nb16, int ksp, int cfg, int *ipt);
+hipError_t launch_pwdw(const PwDwParams &p, int cfg, hipStream_t st);
+
 hipError_t launch_add(const h8 *a, const h8 *b, h8 *y, size_t count, int act, bool bf16, hipStream_t st);
 // zero padding of a sliced tensor: (N, H, W) planes of S slices -> (N, OH, OW),
 // input placed at row pt, column pl

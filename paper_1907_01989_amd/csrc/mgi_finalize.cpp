@@ -133,6 +133,18 @@ void add_configs(Node &nd, size_t M) {
             t.bn = lb[1];
             push(t);
         }
+    } else if (nd.kind == NodeKind::PwDw) {
+        // channels per workgroup of the fused pointwise + depthwise kernel
+        for (int bn : {64, 128}) {
+            const Shape &s = nd.dw_in;
+            if (!kern::pwdw_supported(s.h, s.w, nd.dw_out.h, nd.dw_out.w, nd.dw_conv.stride_h, nd.dw_conv.pad_t,
+                                      nd.dw_conv.pad_l, nd.nb16, nd.ksp, bn == 128 ? 0 : 1, nullptr))
+                continue;
+            GemmTile t;
+            t.bn = bn;
+            nd.cfgs.push_back({t, 0, "img" + std::to_string(bn)});
+        }
+        nd.tile = nd.cfgs[0].tile;
     } else if (nd.kind == NodeKind::DwPw) {
         // band heights for the fused depthwise + pointwise kernel: up to 128
         // or up to 64 pixels per workgroup
@@ -190,6 +202,61 @@ void fuse_dw_into_pw(mgi_plan &p) {
         pw.tile.bm = 128;
         p.bufs[mid].dead = true;
         drop[producer[mid]] = 1;
+    }
+    std::vector<Node> kept;
+    for (size_t i = 0; i < p.nodes.size(); ++i)
+        if (!drop[i]) kept.push_back(std::move(p.nodes[i]));
+    p.nodes.swap(kept);
+}
+
+// Pointwise -> depthwise fusion (Sec. 3.2's fusion of a cheap operator into
+// the expensive one, extended to the pair inside a MobileNet stage): a 1x1
+// pointwise GEMM node without residual whose output only feeds one 3x3
+// depthwise node (dilation 1, stride 1 or 2) becomes a single node producing
+// the depthwise output, when the planes fit the fused kernel's whole-image
+// tiles (pwdw_supported) and, unless `always`, give at least 128 workgroups;
+// the intermediate buffer is dropped.
+void fuse_pw_into_dw(mgi_plan &p, bool always) {
+    std::vector<int> readers(p.bufs.size(), 0), producer(p.bufs.size(), -1);
+    for (size_t i = 0; i < p.nodes.size(); ++i) {
+        const Node &nd = p.nodes[i];
+        for (int b : nd.in) readers[b]++;
+        if (nd.residual >= 0) readers[nd.residual]++;
+        producer[nd.out] = (int)i;
+    }
+    std::vector<char> drop(p.nodes.size(), 0);
+    for (size_t i = 0; i < p.nodes.size(); ++i) {
+        const Node &dw = p.nodes[i];
+        const mgi_conv_desc &c = dw.conv;
+        if (dw.kind != NodeKind::Depthwise || dw.in.size() != 1 || c.kh != 3 || c.kw != 3 ||
+            c.stride_h != c.stride_w || c.stride_h > 2 || c.dil_h != 1 || c.dil_w != 1)
+            continue;
+        const int mid = dw.in[0];
+        if (readers[mid] != 1 || p.bufs[mid].loc != Loc::Arena || producer[mid] < 0) continue;
+        Node &pw = p.nodes[producer[mid]];
+        if (pw.kind != NodeKind::Gemm || pw.taps || pw.residual >= 0 || pw.in.size() != 1) continue;
+        const Shape in = p.bufs[mid].shape, out = p.bufs[dw.out].shape;
+        int ipt = 0;
+        if (!kern::pwdw_supported(in.h, in.w, out.h, out.w, c.stride_h, c.pad_t, c.pad_l, pw.nb16, pw.ksp, 1,
+                                  &ipt))
+            continue;
+        // a workgroup runs a whole tile's K loop and depthwise step alone; with
+        // fewer than half as many tiles as compute units the separate kernels,
+        // which split the work finer, finish first
+        if (!always && (size_t)(in.n + ipt - 1) / ipt * (pw.nb16 / 4) < 128) continue;
+        pw.kind = NodeKind::PwDw;
+        pw.kname = "pw_dw";
+        pw.dw_op = dw.op;
+        pw.dw_conv = dw.conv;
+        pw.dw_act = dw.act1;
+        pw.dw_in = in;
+        pw.dw_out = out;
+        pw.out = dw.out;
+        pw.out_tensor = dw.out_tensor;
+        pw.n_fused += dw.n_fused;
+        pw.tile = GemmTile{};
+        p.bufs[mid].dead = true;
+        drop[i] = 1;
     }
     std::vector<Node> kept;
     for (size_t i = 0; i < p.nodes.size(); ++i)
@@ -307,6 +374,8 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
         return fail(MGI_ERR_UNSUPPORTED, "mgi_graph_finalize: unknown planner");
     if (o.dtype != MGI_DTYPE_FP16 && o.dtype != MGI_DTYPE_BF16)
         return fail(MGI_ERR_UNSUPPORTED, "mgi_graph_finalize: storage is fp16 or bf16");
+    if (o.fuse_pwdw < 0 || o.fuse_pwdw > 2)
+        return fail(MGI_ERR_INVALID_ARG, "mgi_graph_finalize: fuse_pwdw is 0, 1 or 2");
     auto to_bits = o.dtype == MGI_DTYPE_BF16 ? f32_to_bf16_bits : f32_to_f16_bits;
 
     const std::vector<char> live = live_ops(g);
@@ -702,6 +771,7 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
         p.output_dtypes.push_back(p.bufs[b].layout == Layout::I32 ? MGI_DTYPE_INT32 : MGI_DTYPE_FP32);
     }
 
+    if (o.fuse && o.fuse_pwdw) fuse_pw_into_dw(p, o.fuse_pwdw == 2);
     if (o.fuse && o.fuse_dwpw) fuse_dw_into_pw(p);
     for (Node &nd : p.nodes) add_configs(nd, p.bufs[nd.out].shape.pixels());
 
@@ -773,8 +843,24 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
             float *bp = reinterpret_cast<float *>(blob.data() + nd.dw_b_off);
             for (int ch = 0; ch < c; ++ch) bp[ch] = dop.b[ch];
         }
+        if (nd.kind == NodeKind::PwDw) {
+            // depthwise taps of the absorbed op per channel and kernel row,
+            // (w0, w1, w2, 0) (the B operand source of the matrix-core
+            // depthwise step), biases fp32; channels past c are zero
+            const GOp &dop = g.ops[nd.dw_op];
+            const int c = dop.out.c, cp = nd.nb16 * 16;
+            nd.dw_w_off = reserve((size_t)cp * 3 * 4 * 2);
+            uint16_t *wp = reinterpret_cast<uint16_t *>(blob.data() + nd.dw_w_off);
+            for (int ch = 0; ch < c; ++ch)
+                for (int ky = 0; ky < 3; ++ky)
+                    for (int kx = 0; kx < 3; ++kx)
+                        wp[((size_t)ch * 3 + ky) * 4 + kx] = to_bits(dop.w[(size_t)ch * 9 + ky * 3 + kx]);
+            nd.dw_b_off = reserve((size_t)cp * 4);
+            float *bp = reinterpret_cast<float *>(blob.data() + nd.dw_b_off);
+            for (int ch = 0; ch < c; ++ch) bp[ch] = dop.b[ch];
+        }
         if (nd.kind == NodeKind::Gemm || nd.kind == NodeKind::Stem || nd.kind == NodeKind::FC ||
-            nd.kind == NodeKind::DwPw) {
+            nd.kind == NodeKind::DwPw || nd.kind == NodeKind::PwDw) {
             const Shape x = g.ops[op.in[0]].out;
             const int cin = x.c;
             const int cout = nd.kind == NodeKind::FC ? op.cout : op.conv.cout;

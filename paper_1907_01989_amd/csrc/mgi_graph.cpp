@@ -327,4 +327,5 @@ extern "C" void mgi_options_default(mgi_options *o) {
     o->materialize_all = 0;
     o->dtype = MGI_DTYPE_FP16;
     o->fuse_dwpw = 0;
+    o->fuse_pwdw = 1;
 }

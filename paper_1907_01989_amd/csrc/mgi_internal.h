@@ -74,7 +74,7 @@ struct Buf {
 
 enum class NodeKind {
     Ingest, Stem, Gemm, Depthwise, Add, Act, Gap, FC, Softmax, Concat, Resize, Argmax,
-    ResizeArgmax, Export, Pad, DwPw
+    ResizeArgmax, Export, Pad, DwPw, PwDw
 };
 
 // Tile shape of the MFMA GEMM (pointwise, implicit-GEMM convolution, FC).
@@ -110,11 +110,14 @@ struct Node {
     mgi_conv_desc conv{};
     int align_corners = 1;
     int dw_rows = 0;        // depthwise 3x3: output rows per thread (0 = kernel default)
-    // DwPw: the absorbed depthwise op, its window, activation and packed taps
+    // DwPw / PwDw: the absorbed depthwise op (the pointwise input's producer,
+    // or the pointwise output's consumer), its window, activation and packed
+    // taps; for PwDw tile.bn is the fused kernel's channels per tile
     int dw_op = -1;
     mgi_conv_desc dw_conv{};
     int dw_act = MGI_ACT_NONE;
     size_t dw_w_off = 0, dw_b_off = 0;
+    Shape dw_in, dw_out;    // PwDw: shapes of the depthwise input (the pointwise output) and output
     // kernel configurations the autotuner may choose from (index 0 = the
     // finalize-time choice); `cfg` is the one in use
     struct Config {

@@ -125,6 +125,26 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
                 return hipErrorInvalidValue;
             return launch_dwpw(q, t, st);
         }
+        case NodeKind::PwDw: {
+            PwDwParams q{};
+            q.bf16 = bf;
+            q.x = (const h8 *)buf_ptr(p, nd.in[0], B);
+            q.w = (const h8 *)(wbase + nd.w_off);
+            q.bias = (const float *)(wbase + nd.b_off);
+            q.M = (int)nd.dw_in.pixels();
+            q.ksl = nd.ksl; q.ksp = nd.ksp; q.nb16 = nd.nb16; q.act1 = nd.act1;
+            q.dw_t = (const h4 *)(wbase + nd.dw_w_off);
+            q.dw_b = (const float *)(wbase + nd.dw_b_off);
+            q.y = (h8 *)y;
+            q.N = nd.dw_in.n; q.H = nd.dw_in.h; q.W = nd.dw_in.w; q.OH = os.h; q.OW = os.w;
+            q.S = nd.dw_conv.stride_h; q.pt = nd.dw_conv.pad_t; q.pl = nd.dw_conv.pad_l;
+            q.act2 = nd.dw_act;
+            const int cfg = nd.tile.bn == 128 ? 0 : 1;
+            if (!pwdw_supported(q.H, q.W, q.OH, q.OW, q.S, q.pt, q.pl, q.nb16, q.ksp, cfg, &q.ipt))
+                return hipErrorInvalidValue;
+            q.ntiles = q.nb16 / (cfg == 0 ? 8 : 4);
+            return launch_pwdw(q, cfg, st);
+        }
         case NodeKind::Depthwise: {
             const Buf &ib = p.bufs[nd.in[0]];
             DwParams q{};

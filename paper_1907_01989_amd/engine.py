@@ -69,13 +69,14 @@ def build_graph(desc):
 
 
 def options(planner=B.PLANNER_GREEDY, fuse=True, materialize_all=False, fuse_dwpw=False,
-            dtype=B.DTYPE_FP16):
+            dtype=B.DTYPE_FP16, fuse_pwdw=True):
     o = B.mgi_options_default()
     o.dtype = dtype
     o.planner = planner
     o.fuse = int(fuse)
     o.materialize_all = int(materialize_all)
     o.fuse_dwpw = int(fuse_dwpw)
+    o.fuse_pwdw = int(fuse_pwdw)     # False/True or 2 (fuse regardless of workgroup count)
     return o
 
 
@@ -83,11 +84,12 @@ class Plan:
     """A finalised, device-bound network."""
 
     def __init__(self, desc, planner=B.PLANNER_GREEDY, fuse=True, materialize_all=False,
-                 device="cuda:0", bind=True, fuse_dwpw=False, dtype=B.DTYPE_FP16):
+                 device="cuda:0", bind=True, fuse_dwpw=False, dtype=B.DTYPE_FP16, fuse_pwdw=True):
         self.desc = desc
         g = build_graph(desc)
         try:
-            self.handle = B.mgi_graph_finalize(g, options(planner, fuse, materialize_all, fuse_dwpw, dtype))
+            self.handle = B.mgi_graph_finalize(
+                g, options(planner, fuse, materialize_all, fuse_dwpw, dtype, fuse_pwdw))
         finally:
             B.mgi_graph_destroy(g)
         self.device = device

@@ -29,14 +29,18 @@ def to_numpy(t):
     return t.detach().cpu().numpy()
 
 
-def run_gpu(desc, materialize_all=True, fuse=True, planner=None, fuse_dwpw=False, dtype=0):
-    """Run ``desc`` once; returns (plan, outputs as numpy, {tensor id: node output})."""
+def run_gpu(desc, materialize_all=True, fuse=True, planner=None, fuse_dwpw=False, dtype=0,
+            fuse_pwdw=True, configs=None):
+    """Run ``desc`` once; returns (plan, outputs as numpy, {tensor id: node output}).
+    ``configs``: {node index: kernel configuration} set before the run."""
     import torch
     from paper_1907_01989_amd import engine, _binding as B
-    kw = {"fuse_dwpw": fuse_dwpw, "dtype": dtype}
+    kw = {"fuse_dwpw": fuse_dwpw, "dtype": dtype, "fuse_pwdw": fuse_pwdw}
     if planner is not None:
         kw["planner"] = planner
     plan = engine.Plan(desc, fuse=fuse, materialize_all=materialize_all, **kw)
+    for i, c in (configs or {}).items():
+        B.mgi_plan_set_node_config(plan.handle, i, c)
     xs = plan.input_tensors()
     outs = plan.run(xs)
     nodes = {}

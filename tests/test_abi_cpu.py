@@ -110,12 +110,12 @@ def test_finalize_state_errors_and_run_before_bind():
 
 
 def test_fusion_structure():
-    v1 = engine.Plan(workloads.mobilenet_v1(1), bind=False)
+    v1 = engine.Plan(workloads.mobilenet_v1(1), bind=False, fuse_pwdw=False)
     kinds = [n["kind"] for n in v1.nodes()]
     assert kinds[0] == "conv_stem" and kinds.count("dw_conv") == 13 and kinds.count("pw_gemm") == 13
     assert kinds[-3:] == ["global_avgpool", "fc_gemm", "softmax"]
     assert len(kinds) == 30
-    v2 = engine.Plan(workloads.mobilenet_v2(1), bind=False)
+    v2 = engine.Plan(workloads.mobilenet_v2(1), bind=False, fuse_pwdw=False)
     nodes = v2.nodes()
     assert sum(1 for n in nodes if n["n_fused"] == 2) == 10      # residual adds absorbed
     assert not any(n["kind"] == "add" for n in nodes)
@@ -123,6 +123,42 @@ def test_fusion_structure():
     assert sum(1 for n in v2u.nodes() if n["kind"] == "add") == 10
     dl = engine.Plan(workloads.deeplab_v2_os16(1), bind=False)
     assert dl.nodes()[-1]["kind"] == "resize_argmax"
+
+
+def test_pointwise_depthwise_fusion_structure():
+    # v1: pw6..pw12 feed depthwise convolutions on 14x14 (pw11 -> dw12 at
+    # stride 2) and 7x7 planes; pw1..pw5 (planes of 28 and more) and pw13 stay
+    v1 = engine.Plan(workloads.mobilenet_v1(64), bind=False)
+    nodes = v1.nodes()
+    kinds = [n["kind"] for n in nodes]
+    assert kinds.count("pw_dw") == 7 and kinds.count("dw_conv") == 6 and kinds.count("pw_gemm") == 6
+    assert len(kinds) == 23
+    for n in nodes:
+        if n["kind"] == "pw_dw":
+            assert n["n_fused"] == 2 and n["shape"][1] in (14, 7)
+    # the fused node's output is the depthwise tensor
+    desc = workloads.mobilenet_v1(64)
+    fused_tensors = [n["tensor"] for n in nodes if n["kind"] == "pw_dw"]
+    assert all(desc["ops"][t]["op"] == "depthwise" for t in fused_tensors)
+    # v2: the expansions feeding 14x14 / 7x7 depthwise convolutions (ten blocks)
+    v2 = engine.Plan(workloads.mobilenet_v2(64), bind=False)
+    k2 = [n["kind"] for n in v2.nodes()]
+    assert k2.count("pw_dw") == 10
+    # the planner holds fewer tensors once the pointwise outputs vanish
+    v1u = engine.Plan(workloads.mobilenet_v1(64), bind=False, fuse_pwdw=False)
+    assert v1.memory_report()[1] <= v1u.memory_report()[1]
+    # at batch 1 the fused kernel would get 8..16 workgroups: not fused by
+    # default, fused when asked for regardless (fuse_pwdw = 2)
+    b1 = [n["kind"] for n in engine.Plan(workloads.mobilenet_v1(1), bind=False).nodes()]
+    assert b1.count("pw_dw") == 0 and len(b1) == 30
+    b1f = [n["kind"] for n in engine.Plan(workloads.mobilenet_v1(1), bind=False, fuse_pwdw=2).nodes()]
+    assert b1f.count("pw_dw") == 7
+    o = engine.options(fuse_pwdw=3)
+    g = engine.build_graph(workloads.mobilenet_v1(1))
+    try:
+        assert err(B.mgi_graph_finalize, g, o) == 1
+    finally:
+        B.mgi_graph_destroy(g)
 
 
 def test_standalone_activation_and_add_fusion():
@@ -202,6 +238,8 @@ def test_node_configuration_candidates():
             assert k >= 5 and name.startswith(("pipe", "slab", "lds"))
         elif n["kind"] == "dw_conv":
             assert k == 3 and name.startswith("rows")
+        elif n["kind"] == "pw_dw":
+            assert 1 <= k <= 2 and name.startswith("img")
         else:
             assert k == 1
     i = next(j for j, n in enumerate(nodes) if n["kind"] == "pw_gemm")
