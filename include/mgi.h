@@ -270,11 +270,12 @@ mgi_status mgi_plan_read_node(mgi_plan *p, int i, void *dev_dst, void *stream);
 
 /* Plan-time tuning (after Sec. 4.2, where work-group sizes are chosen by
  * measurement): runs the plan once with these device buffers (same
- * arguments and checks as mgi_plan_run), then times every candidate kernel
- * configuration of each pointwise / implicit-GEMM and depthwise node with
- * `reps` device-timestamped launches (plus one warm-up) on the plan's own
- * buffers and keeps the fastest.  All candidates produce bit-identical
- * results.  Synchronises `stream`; releases a captured graph (capture again
+ * arguments and checks as mgi_plan_run), then, node by node in run order,
+ * times every candidate kernel configuration of each node that has several
+ * (pointwise / implicit-GEMM, depthwise, fused pointwise -> depthwise) inside
+ * `reps` whole runs of the plan (plus one warm-up; only the node's kernels
+ * are timestamped, so it meets its input as in a run) and keeps the fastest.
+ * All candidates produce bit-identical results.  Synchronises `stream`; releases a captured graph (capture again
  * afterwards).  The output buffers hold no defined result afterwards: run the
  * plan again.  Errors: MGI_ERR_INVALID_ARG for reps outside 1..1000; run
  * errors; MGI_ERR_HIP if timing fails. */

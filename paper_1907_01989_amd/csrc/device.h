@@ -71,7 +71,6 @@ typedef __bf16 bh8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bh4 __attribute__((ext_vector_type(4)));
 typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
 typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
-typedef short s16x4 __attribute__((ext_vector_type(4)));
 
 struct F16 {
     static constexpr bool bf = false;
@@ -83,7 +82,6 @@ struct F16 {
         return o;
     }
     __device__ static f4 mma(h8 a, h8 b, f4 c) { return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0); }
-    __device__ static f4 mma16(h4 a, h4 b, f4 c) { return __builtin_amdgcn_mfma_f32_16x16x16f16(a, b, c, 0, 0, 0); }
     __device__ static void fma8(float *acc, h8 w, h8 v) { kern::fma8(acc, as_u4(w), as_u4(v)); }
     __device__ static float get4(h4 v, int i) { return (float)v[i]; }
     __device__ static h4 pack4(const float *v) {
@@ -109,10 +107,6 @@ struct BF16 {
     __device__ static f4 mma(h8 a, h8 b, f4 c) {
         return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bh8, a), __builtin_bit_cast(bh8, b), c,
                                                       0, 0, 0);
-    }
-    __device__ static f4 mma16(h4 a, h4 b, f4 c) {
-        return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4, a), __builtin_bit_cast(s16x4, b), c,
-                                                        0, 0, 0);
     }
     __device__ static void fma8(float *acc, h8 w, h8 v) {
 #pragma unroll

@@ -122,7 +122,7 @@ struct PwDwParams {
     const h8 *w;         // packed pointwise weights [nb16][ksp][16][8]
     const float *bias;   // [nb16 * 16]
     int M, ksl, ksp, nb16, act1;
-    const h4 *dw_t;      // depthwise taps per channel and kernel row, (w0, w1, w2, 0): [16 * nb16][3]
+    const h8 *dw_w;      // depthwise taps [2 * nb16][9][8]
     const float *dw_b;   // [16 * nb16]
     h8 *y;               // depthwise output, sliced [2 * nb16][N * OH * OW]
     int N, H, W, OH, OW, S, pt, pl, act2;

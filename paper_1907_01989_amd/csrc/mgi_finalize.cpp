@@ -90,6 +90,8 @@ std::string tile_name(const GemmTile &t) {
     return "lds" + std::to_string(t.bm) + "x" + std::to_string(t.bn);
 }
 
+void pick_pipe_tile(GemmTile &t, size_t M, int npad);
+
 void add_configs(Node &nd, size_t M) {
     auto push = [&](const GemmTile &t) {
         for (const Node::Config &c : nd.cfgs)
@@ -134,7 +136,10 @@ void add_configs(Node &nd, size_t M) {
             push(t);
         }
     } else if (nd.kind == NodeKind::PwDw) {
-        // channels per workgroup of the fused pointwise + depthwise kernel
+        // channels per workgroup of the fused pointwise + depthwise kernel, and
+        // the two separate kernels through the scratch tensor (pipelined GEMM
+        // tile by the pointwise rule, depthwise rows by the depthwise rule);
+        // the split form first when the fused kernel would not fill the GPU
         for (int bn : {64, 128}) {
             const Shape &s = nd.dw_in;
             if (!kern::pwdw_supported(s.h, s.w, nd.dw_out.h, nd.dw_out.w, nd.dw_conv.stride_h, nd.dw_conv.pad_t,
@@ -142,9 +147,13 @@ void add_configs(Node &nd, size_t M) {
                 continue;
             GemmTile t;
             t.bn = bn;
-            nd.cfgs.push_back({t, 0, "img" + std::to_string(bn)});
+            nd.cfgs.push_back({t, 0, "img" + std::to_string(bn), false});
         }
-        nd.tile = nd.cfgs[0].tile;
+        GemmTile t;
+        pick_pipe_tile(t, nd.dw_in.pixels(), nd.nb16 * 16);
+        const Node::Config split{t, nd.dw_conv.stride_h == 1 ? 4 : 2, "split_" + tile_name(t), true};
+        nd.cfgs.insert(nd.fused_default ? nd.cfgs.end() : nd.cfgs.begin(), split);
+        nd.apply(0);
     } else if (nd.kind == NodeKind::DwPw) {
         // band heights for the fused depthwise + pointwise kernel: up to 128
         // or up to 64 pixels per workgroup
@@ -214,8 +223,11 @@ void fuse_dw_into_pw(mgi_plan &p) {
 // pointwise GEMM node without residual whose output only feeds one 3x3
 // depthwise node (dilation 1, stride 1 or 2) becomes a single node producing
 // the depthwise output, when the planes fit the fused kernel's whole-image
-// tiles (pwdw_supported) and, unless `always`, give at least 128 workgroups;
-// the intermediate buffer is dropped.
+// tiles (pwdw_supported).  The intermediate tensor stays planned as the
+// node's scratch, so the node can also run as the two separate kernels; the
+// fused kernel is its default configuration when it gets at least 128
+// workgroups (or `always`): with fewer, the separate kernels, which split
+// the work finer, finish first.
 void fuse_pw_into_dw(mgi_plan &p, bool always) {
     std::vector<int> readers(p.bufs.size(), 0), producer(p.bufs.size(), -1);
     for (size_t i = 0; i < p.nodes.size(); ++i) {
@@ -240,10 +252,7 @@ void fuse_pw_into_dw(mgi_plan &p, bool always) {
         if (!kern::pwdw_supported(in.h, in.w, out.h, out.w, c.stride_h, c.pad_t, c.pad_l, pw.nb16, pw.ksp, 1,
                                   &ipt))
             continue;
-        // a workgroup runs a whole tile's K loop and depthwise step alone; with
-        // fewer than half as many tiles as compute units the separate kernels,
-        // which split the work finer, finish first
-        if (!always && (size_t)(in.n + ipt - 1) / ipt * (pw.nb16 / 4) < 128) continue;
+        pw.fused_default = always || (size_t)(in.n + ipt - 1) / ipt * (pw.nb16 / 4) >= 128;
         pw.kind = NodeKind::PwDw;
         pw.kname = "pw_dw";
         pw.dw_op = dw.op;
@@ -255,7 +264,7 @@ void fuse_pw_into_dw(mgi_plan &p, bool always) {
         pw.out_tensor = dw.out_tensor;
         pw.n_fused += dw.n_fused;
         pw.tile = GemmTile{};
-        p.bufs[mid].dead = true;
+        pw.scratch = mid;
         drop[i] = 1;
     }
     std::vector<Node> kept;
@@ -781,6 +790,7 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
         p.bufs[nd.out].producer = (int)i;
         for (int b : nd.in) p.bufs[b].last_use = (int)i;
         if (nd.residual >= 0) p.bufs[nd.residual].last_use = (int)i;
+        if (nd.scratch >= 0) p.bufs[nd.scratch].producer = p.bufs[nd.scratch].last_use = (int)i;
     }
 
     // -------------------------------------------------------------- planning
@@ -844,17 +854,15 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
             for (int ch = 0; ch < c; ++ch) bp[ch] = dop.b[ch];
         }
         if (nd.kind == NodeKind::PwDw) {
-            // depthwise taps of the absorbed op per channel and kernel row,
-            // (w0, w1, w2, 0) (the B operand source of the matrix-core
-            // depthwise step), biases fp32; channels past c are zero
+            // depthwise taps of the absorbed op laid out as for a depthwise
+            // node, [S][9][8], biases fp32; channels past c are zero
             const GOp &dop = g.ops[nd.dw_op];
             const int c = dop.out.c, cp = nd.nb16 * 16;
-            nd.dw_w_off = reserve((size_t)cp * 3 * 4 * 2);
+            nd.dw_w_off = reserve((size_t)(cp / 8) * 9 * 8 * 2);
             uint16_t *wp = reinterpret_cast<uint16_t *>(blob.data() + nd.dw_w_off);
             for (int ch = 0; ch < c; ++ch)
-                for (int ky = 0; ky < 3; ++ky)
-                    for (int kx = 0; kx < 3; ++kx)
-                        wp[((size_t)ch * 3 + ky) * 4 + kx] = to_bits(dop.w[(size_t)ch * 9 + ky * 3 + kx]);
+                for (int t = 0; t < 9; ++t)
+                    wp[((size_t)(ch / 8) * 9 + t) * 8 + ch % 8] = to_bits(dop.w[(size_t)ch * 9 + t]);
             nd.dw_b_off = reserve((size_t)cp * 4);
             float *bp = reinterpret_cast<float *>(blob.data() + nd.dw_b_off);
             for (int ch = 0; ch < c; ++ch) bp[ch] = dop.b[ch];

@@ -120,13 +120,26 @@ struct Node {
     Shape dw_in, dw_out;    // PwDw: shapes of the depthwise input (the pointwise output) and output
     // kernel configurations the autotuner may choose from (index 0 = the
     // finalize-time choice); `cfg` is the one in use
+    // PwDw: the pointwise output kept as a planned scratch tensor, so that the
+    // node can also run as the two separate kernels (split); whether the
+    // fused kernel is the default configuration
+    int scratch = -1;
+    bool split = false;
+    bool fused_default = true;
     struct Config {
         GemmTile tile;
         int dw_rows = 0;
         std::string name;
+        bool split = false;
     };
     std::vector<Config> cfgs;
     int cfg = 0;
+    void apply(int c) {
+        cfg = c;
+        tile = cfgs[c].tile;
+        dw_rows = cfgs[c].dw_rows;
+        split = cfgs[c].split;
+    }
 };
 
 }  // namespace mgi

@@ -126,6 +126,47 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
             return launch_dwpw(q, t, st);
         }
         case NodeKind::PwDw: {
+            if (nd.split) {
+                // the pointwise GEMM into the scratch tensor, then the depthwise
+                // kernel; a timed run stamps the first kernel's start and the
+                // second one's end
+                LaunchEvents &ev = launch_events();
+                const LaunchEvents saved = ev;
+                const Shape mid = nd.dw_in;
+                void *sp = buf_ptr(p, nd.scratch, B);
+                GemmParams g{};
+                g.bf16 = bf;
+                g.x = (const h8 *)buf_ptr(p, nd.in[0], B);
+                g.w = (const h8 *)(wbase + nd.w_off);
+                g.bias = (const float *)(wbase + nd.b_off);
+                g.y = sp;
+                g.M = g.Min = (int)mid.pixels();
+                g.ksl = nd.ksl; g.ksp = nd.ksp;
+                g.nb16 = nd.nb16; g.ns = slices(mid.c); g.cout = mid.c;
+                g.act1 = nd.act1; g.act2 = MGI_ACT_NONE;
+                ev.stop = nullptr;
+                hipError_t e = launch_gemm_pipe(g, nd.tile.bm, nd.tile.bn, st);
+                ev.start = nullptr;
+                ev.stop = saved.stop;
+                if (e == hipSuccess) {
+                    DwParams q{};
+                    q.bf16 = bf;
+                    q.x = (const h8 *)sp;
+                    q.w = (const h8 *)(wbase + nd.dw_w_off);
+                    q.bias = (const float *)(wbase + nd.dw_b_off);
+                    q.zero = (const h8 *)(wbase + p.zero_off);
+                    q.y = (h8 *)y;
+                    q.N = mid.n; q.H = mid.h; q.W = mid.w; q.S = slices(mid.c);
+                    q.OH = os.h; q.OW = os.w; q.KH = q.KW = 3;
+                    q.sh = q.sw = nd.dw_conv.stride_h;
+                    q.dh = q.dw = 1;
+                    q.pt = nd.dw_conv.pad_t; q.pl = nd.dw_conv.pad_l;
+                    q.act = nd.dw_act;
+                    e = launch_depthwise(q, nd.dw_rows, st);
+                }
+                ev = saved;
+                return e;
+            }
             PwDwParams q{};
             q.bf16 = bf;
             q.x = (const h8 *)buf_ptr(p, nd.in[0], B);
@@ -133,7 +174,7 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
             q.bias = (const float *)(wbase + nd.b_off);
             q.M = (int)nd.dw_in.pixels();
             q.ksl = nd.ksl; q.ksp = nd.ksp; q.nb16 = nd.nb16; q.act1 = nd.act1;
-            q.dw_t = (const h4 *)(wbase + nd.dw_w_off);
+            q.dw_w = (const h8 *)(wbase + nd.dw_w_off);
             q.dw_b = (const float *)(wbase + nd.dw_b_off);
             q.y = (h8 *)y;
             q.N = nd.dw_in.n; q.H = nd.dw_in.h; q.W = nd.dw_in.w; q.OH = os.h; q.OW = os.w;
@@ -389,21 +430,32 @@ extern "C" mgi_status mgi_plan_autotune(mgi_plan *p, const void *const *dev_inpu
     Bases B{static_cast<char *>(p->dev_ws), dev_inputs, dev_outputs};
     LaunchEvents &ev = launch_events();
     mgi_status result = MGI_OK;
-    for (Node &nd : p->nodes) {
+    for (size_t ni = 0; ni < p->nodes.size() && result == MGI_OK; ++ni) {
+        Node &nd = p->nodes[ni];
         if (nd.cfgs.size() < 2) continue;
         int best = 0;
         float best_ms = 3.0e38f;
         for (size_t c = 0; c < nd.cfgs.size() && result == MGI_OK; ++c) {
-            nd.tile = nd.cfgs[c].tile;
-            nd.dw_rows = nd.cfgs[c].dw_rows;
+            nd.apply((int)c);
             float tmin = 3.0e38f;
             bool usable = true;
             for (int r = 0; r <= reps; ++r) {
-                ev.start = e0;
-                ev.stop = e1;
-                e = launch_node(*p, nd, B, st);
-                ev.start = ev.stop = nullptr;
+                // the whole plan runs, so that the node meets its input as it
+                // does in a run (just written by its producer), and only the
+                // node's kernels are timestamped
+                for (size_t j = 0; j < p->nodes.size() && e == hipSuccess; ++j) {
+                    ev.start = j == ni ? e0 : nullptr;
+                    ev.stop = j == ni ? e1 : nullptr;
+                    e = launch_node(*p, p->nodes[j], B, st);
+                    ev.start = ev.stop = nullptr;
+                    if (e != hipSuccess && j != ni) {
+                        result = hip_fail(e, "mgi_plan_autotune: run");
+                        break;
+                    }
+                }
+                if (result != MGI_OK) break;
                 if (e != hipSuccess) {
+                    e = hipSuccess;
                     usable = false;   // configuration not launchable for this shape
                     break;
                 }
@@ -421,9 +473,7 @@ extern "C" mgi_status mgi_plan_autotune(mgi_plan *p, const void *const *dev_inpu
                 best = (int)c;
             }
         }
-        nd.cfg = best;
-        nd.tile = nd.cfgs[best].tile;
-        nd.dw_rows = nd.cfgs[best].dw_rows;
+        nd.apply(best);
         if (result != MGI_OK) break;
     }
     hipEventDestroy(e0);
@@ -451,11 +501,7 @@ extern "C" mgi_status mgi_plan_set_node_config(mgi_plan *p, int i, int config) {
     const int n = nd.cfgs.empty() ? 1 : (int)nd.cfgs.size();
     if (config < 0 || config >= n)
         return fail(MGI_ERR_INVALID_ARG, "mgi_plan_set_node_config: configuration out of range");
-    if (!nd.cfgs.empty()) {
-        nd.cfg = config;
-        nd.tile = nd.cfgs[config].tile;
-        nd.dw_rows = nd.cfgs[config].dw_rows;
-    }
+    if (!nd.cfgs.empty()) nd.apply(config);
     release_graph(*p);
     return MGI_OK;
 }

@@ -19,36 +19,38 @@
 //      chunk, or streaming them through a two-chunk ring, measured no faster:
 //      the loop is bound by the L2->CU transfer of activations and weights,
 //      about 324 KiB per workgroup at v1's 14x14 stage);
-//   3. bias and activation are applied, and the 16-bit pointwise output is
-//      parked in LDS channel-planar: one zero-bordered plane per channel and
-//      image, in place of the slab;
-//   4. the depthwise convolution runs on the matrix cores.  For one channel and
-//      one kernel row ky, the output plane (at most 16 x 16) is
-//         out[oy][ox] += sum_ix in[oy*S + ky - pt][ix] * T[ix][ox],
-//      T[ix][ox] = w[ky][ix - ox*S + pl] (zero off the three-tap band), one
-//      v_mfma_f32_16x16x16: the A operand is four input columns of a row read
-//      from the plane, the B operand is T, built per lane from the row's three
-//      taps by a byte permute.  Three MFMAs per channel accumulate the kernel
-//      rows; zero rows and columns of the plane are the zero padding.
-// The pointwise part is bit-identical to the GEMM kernels; the depthwise sums
-// are formed by the matrix core (fp32 accumulation) instead of nine
-// sequential fp32 FMAs, so results agree with the separate depthwise kernel to
-// fp32 rounding before the final 16-bit rounding.
+//   3. bias and activation are applied and the 16-bit pointwise output tile
+//      is parked in LDS, slice-major, in place of the weights;
+//   4. the depthwise convolution runs from LDS: one lane per output column, a
+//      row of lanes per (image, slice, strip of R output rows); the left and
+//      right input columns come from the neighbouring lanes by wave-wide DPP
+//      shifts (lanes past the last column hold zeros, which is the zero
+//      padding).
+// Accumulation order, rounding points and activations are those of the
+// separate GEMM and depthwise kernels, so the result is bit-identical to the
+// unfused pair (and to the node's split form, which runs those kernels).
 #include "device.h"
 
 namespace mgi {
 namespace kern {
 
-typedef uint32_t u2x __attribute__((ext_vector_type(2)));
+// whole-wave lane shift of a 16-byte value: kWaveShr1 gives lane l the value
+// of lane l-1 (lane 0 gets zero), kWaveShl1 that of lane l+1 (lane 63 gets zero)
+constexpr int kWaveShl1 = 0x130, kWaveShr1 = 0x138;
+template <int CTRL>
+__device__ __forceinline__ h8 wave_shift(h8 v) {
+    const u4x u = as_u4(v);
+    u4x r;
+#pragma unroll
+    for (int d = 0; d < 4; ++d)
+        r[d] = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)u[d], CTRL, 0xf, 0xf, false);
+    return __builtin_bit_cast(h8, r);
+}
 
 constexpr int kPwDwPixels = 256;   // pixel capacity of a tile (16 fragments)
-constexpr int kPwDwRow = 20;       // halves per plane row: 16 columns + bank padding
 constexpr int kPwDwLds = 160 * 1024;
 
-// halves per channel plane of an H-row input: a zero row above and below
-__host__ __device__ constexpr int pwdw_plane(int H) { return (H + 2) * kPwDwRow + 4; }
-
-template <typename E, int NW, int FMW, int NBT, int S_, int PF>
+template <typename E, int NW, int FMW, int NBT, int S_, int R, int LPR, int PF>
 __global__ __launch_bounds__(NW * 64) void pwdw_kernel(PwDwParams p) {
     constexpr int PMAX = 16 * NW * FMW;
     constexpr int NCH = 16 * NBT;                 // output channels of the tile
@@ -58,7 +60,8 @@ __global__ __launch_bounds__(NW * 64) void pwdw_kernel(PwDwParams p) {
     constexpr int SQ = NBT * CK;                  // 64-element wave loads per chunk
     static_assert(SQ % NW == 0, "weight chunk split");
     constexpr int DPW = SQ / NW;                  // ... per wave
-    constexpr int kTapQ = (NCH * 3 / 2 + 63) / 64, kTapH8 = 64 * kTapQ;   // (w0,w1,w2,0) rows, whole wave loads
+    constexpr int GPI = NW * 64 / LPR;            // lane rows per pass of the depthwise step
+    constexpr int kTapQ = (NSL * 9 + 63) / 64, kTapH8 = 64 * kTapQ;   // taps [NSL][9], whole wave loads
     constexpr int kBiasQ = (NCH / 4 + 63) / 64;
     extern __shared__ h8 lds[];
 
@@ -73,11 +76,10 @@ __global__ __launch_bounds__(NW * 64) void pwdw_kernel(PwDwParams p) {
     const int m0 = img0 * hw;
     const int nb0 = ct * NBT;
     const int ksp = p.ksp, nk = ksp >> 2;
-    const int pstr = pwdw_plane(p.H);
     const int nchunks = (nk + CK - 1) / CK;
-    const int main_h8 = max(nchunks * SQ * 64, (p.ipt * NCH * pstr + 7) / 8);
-    const h4 *taps = (const h4 *)(lds + main_h8);                 // [NCH][3]
-    const float *dwb = (const float *)(lds + main_h8 + kTapH8);  // [NCH]
+    const int main_h8 = max(nchunks * SQ * 64, NSL * PMAX);
+    const h8 *taps = lds + main_h8;                               // [NSL][9]
+    const float *dwb = (const float *)(lds + main_h8 + kTapH8);  // [NSL][8]
 
     // 1. weights -> LDS in K order, chunk c = K-steps [c*CK, c*CK + CK) of the
     // NBT channel blocks, layout [chunk][NBT][CK][64]; wave load q of a chunk
@@ -92,11 +94,11 @@ __global__ __launch_bounds__(NW * 64) void pwdw_kernel(PwDwParams p) {
                 load_lds16(p.w + ((size_t)(nb0 + i) * ksp + kk * 4) * 16 + lane, lds + (c * SQ + q) * 64);
             }
         }
-        const h8 *tsrc = (const h8 *)(p.dw_t + (size_t)nb0 * 16 * 3);
+        const h8 *tsrc = p.dw_w + (size_t)nb0 * 2 * 9;
         const h8 *bsrc = (const h8 *)(p.dw_b + nb0 * 16);
         for (int q = wave; q < kTapQ + kBiasQ; q += NW) {
             const int e = (q < kTapQ ? q : q - kTapQ) * 64 + lane;
-            if (q < kTapQ) load_lds16(tsrc + min(e, NCH * 3 / 2 - 1), lds + main_h8 + e);
+            if (q < kTapQ) load_lds16(tsrc + min(e, NSL * 9 - 1), lds + main_h8 + e);
             else load_lds16(bsrc + min(e, NCH / 4 - 1), lds + main_h8 + kTapH8 + e);
         }
     }
@@ -155,116 +157,119 @@ __global__ __launch_bounds__(NW * 64) void pwdw_kernel(PwDwParams p) {
         }
     }
 
-    // 3. pointwise epilogue into channel planes [ipt][NCH][H + 2 rows][kPwDwRow]
-    // (16-bit), zeroed first so that the border rows and the columns past W
-    // read as zeros
-    __syncthreads();
-    _Float16 *planes = (_Float16 *)lds;
-    {
-        const int n4 = p.ipt * NCH * pstr / 4;
-        h4 z;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) z[i] = (_Float16)0.0f;
-        for (int e = tid; e < n4; e += NW * 64) ((h4 *)planes)[e] = z;
-    }
+    // 3. pointwise epilogue into LDS: tile [NSL][PMAX] of sliced elements
     __syncthreads();
 #pragma unroll
-    for (int j = 0; j < FMW; ++j) {
-        const int px = (wave + j * NW) * 16 + (lane & 15);
-        if (!fj[j] || px >= P) continue;
-        const int t = px / hw, rem = px - t * hw;
-        const int y = rem / p.W, x = rem - y * p.W;
-        _Float16 *dst = planes + t * NCH * pstr + (y + 1) * kPwDwRow + x;
+    for (int i = 0; i < NBT; ++i) {
+        const int c = i * 16 + 4 * (lane >> 4);       // channel within the tile
+        float bv[4];
 #pragma unroll
-        for (int i = 0; i < NBT; ++i) {
-            const int c = i * 16 + 4 * (lane >> 4);   // channel within the tile
+        for (int r = 0; r < 4; ++r) bv[r] = p.bias[nb0 * 16 + c + r];
+#pragma unroll
+        for (int j = 0; j < FMW; ++j) {
+            const int px = (wave + j * NW) * 16 + (lane & 15);
+            if (!fj[j] || px >= P) continue;
             float v[4];
 #pragma unroll
-            for (int r = 0; r < 4; ++r) v[r] = act_apply(acc[i][j][r] + p.bias[nb0 * 16 + c + r], p.act1);
-            const h4 pv = E::pack4(v);
-#pragma unroll
-            for (int r = 0; r < 4; ++r) dst[(c + r) * pstr] = pv[r];
+            for (int r = 0; r < 4; ++r) v[r] = act_apply(acc[i][j][r] + bv[r], p.act1);
+            *(h4 *)((_Float16 *)(lds + (c >> 3) * PMAX + px) + (c & 7)) = E::pack4(v);
         }
     }
     __syncthreads();
 
-    // 4. depthwise 3x3 on the matrix cores, one (image, slice) per wave at a time
-    const int q4 = lane >> 4, ln = lane & 15;
-    // B operand selectors: half i of this lane is T[4*q4 + i][ln], the tap
-    // d = 4*q4 + i - ln*S + pl of the row, or zero (selector byte 0x0c)
-    uint32_t sel[2];
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-        sel[h] = 0;
-#pragma unroll
-        for (int b2 = 0; b2 < 2; ++b2) {
-            const int d = 4 * q4 + 2 * h + b2 - ln * S_ + p.pl;
-            const uint32_t pair = (d >= 0 && d <= 2) ? (uint32_t)(2 * d) | (uint32_t)(2 * d + 1) << 8 : 0x0c0cu;
-            sel[h] |= pair << (16 * b2);
-        }
-    }
-    const int prow = p.H + 1;                        // last plane row (a zero row)
+    // 4. depthwise 3x3 from LDS, taps and accumulation order of the separate
+    // depthwise kernel
+    constexpr int NR = (R - 1) * S_ + 3;          // input rows of a strip
+    constexpr int NC = S_;                        // input columns loaded per lane
+    const int nstrips = (p.OH + R - 1) / R;
+    const int ngroups = nimg * NSL * nstrips;
+    const int ox = tid % LPR;
     const float lo = p.act2 == MGI_ACT_NONE ? -INFINITY : 0.0f;
     const float hi = p.act2 == MGI_ACT_RELU6 ? 6.0f : INFINITY;
-    const int units = nimg * NSL;
-    for (int u = wave; u < units; u += NW) {
-        const int t = u / NSL, sl = u - t * NSL;
-        const _Float16 *plane = planes + (t * NCH + sl * 8) * pstr + 4 * q4;
-        u2x tw[8][3];
+    const int passes = (ngroups + GPI - 1) / GPI;
+    for (int pass = 0; pass < passes; ++pass) {     // same count in every lane (DPP below)
+        const int g = pass * GPI + tid / LPR;
+        const bool gv = g < ngroups;
+        const int gg = gv ? g : 0;
+        const int strip = gg % nstrips, rest = gg / nstrips;
+        const int sl = rest % NSL, t = rest / NSL;
+        const int oy0 = strip * R, iy0 = oy0 * S_ - p.pt;
+        const h8 *plane = lds + sl * PMAX + t * hw;
+        h8 w[9];
 #pragma unroll
-        for (int ch = 0; ch < 8; ++ch)
+        for (int k = 0; k < 9; ++k) w[k] = taps[sl * 9 + k];
+        int cx[NC];
+        bool cv[NC];
 #pragma unroll
-            for (int ky = 0; ky < 3; ++ky) tw[ch][ky] = __builtin_bit_cast(u2x, taps[(sl * 8 + ch) * 3 + ky]);
-        f4 dacc[8];
+        for (int k = 0; k < NC; ++k) {
+            cx[k] = ox * S_ + k;
+            cv[k] = gv && cx[k] < p.W;
+        }
+        float acc2[R][8];
 #pragma unroll
-        for (int ch = 0; ch < 8; ++ch) dacc[ch] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+        for (int o = 0; o < R; ++o)
 #pragma unroll
-        for (int ky = 0; ky < 3; ++ky) {
-            // plane row of input row ln*S + ky - pt (rows of outputs past OH
-            // are clamped; their results are never stored)
-            const int rr = min(ln * S_ + ky - p.pt + 1, prow);
-            h4 a[8];
+            for (int c = 0; c < 8; ++c) acc2[o][c] = dwb[sl * 8 + c];
 #pragma unroll
-            for (int ch = 0; ch < 8; ++ch) a[ch] = *(const h4 *)(plane + ch * pstr + rr * kPwDwRow);
+        for (int r = 0; r < NR; ++r) {
+            const int iy = iy0 + r;
+            const bool rv = iy >= 0 && iy < p.H;
+            h8 v[NC];
 #pragma unroll
-            for (int ch = 0; ch < 8; ++ch) {
-                u2x bw;
-                bw[0] = __builtin_amdgcn_perm(tw[ch][ky][1], tw[ch][ky][0], sel[0]);
-                bw[1] = __builtin_amdgcn_perm(tw[ch][ky][1], tw[ch][ky][0], sel[1]);
-                dacc[ch] = E::mma16(a[ch], __builtin_bit_cast(h4, bw), dacc[ch]);
+            for (int k = 0; k < NC; ++k) v[k] = (rv && cv[k]) ? plane[iy * p.W + cx[k]] : zero_h8();
+            h8 t3[3];
+            if (S_ == 1) {          // columns ox-1, ox, ox+1 (left padding 1)
+                t3[0] = wave_shift<kWaveShr1>(v[0]);
+                t3[1] = v[0];
+                t3[2] = wave_shift<kWaveShl1>(v[0]);
+            } else if (p.pl == 0) { // columns 2ox, 2ox+1, 2ox+2
+                t3[0] = v[0];
+                t3[1] = v[NC - 1];
+                t3[2] = wave_shift<kWaveShl1>(v[0]);
+            } else {                // columns 2ox-1, 2ox, 2ox+1
+                t3[0] = wave_shift<kWaveShr1>(v[NC - 1]);
+                t3[1] = v[0];
+                t3[2] = v[NC - 1];
+            }
+#pragma unroll
+            for (int ky = 0; ky < 3; ++ky) {
+                const int tt = r - ky;
+                if (tt >= 0 && tt % S_ == 0 && tt / S_ < R) {
+#pragma unroll
+                    for (int k = 0; k < 3; ++k) E::fma8(acc2[tt / S_], w[ky * 3 + k], t3[k]);
+                }
             }
         }
-        // lane holds output column ln of rows 4*q4 .. 4*q4+3 for the 8 channels
-        const int gs = nb0 * 2 + sl;
-        h8 *yout = p.y + ((size_t)gs * p.N + img0 + t) * p.OH * p.OW;
-        float bch[8];
+        if (gv && ox < p.OW) {
+            const int gs = nb0 * 2 + sl;                 // global slice
+            h8 *yout = p.y + ((size_t)gs * p.N + img0 + t) * p.OH * p.OW + ox;
 #pragma unroll
-        for (int ch = 0; ch < 8; ++ch) bch[ch] = dwb[sl * 8 + ch];
+            for (int o = 0; o < R; ++o) {
+                if (oy0 + o >= p.OH) break;
+                float q[8];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int oy = 4 * q4 + r;
-            if (oy >= p.OH || ln >= p.OW) continue;
-            float v[8];
-#pragma unroll
-            for (int ch = 0; ch < 8; ++ch) v[ch] = __builtin_amdgcn_fmed3f(dacc[ch][r] + bch[ch], lo, hi);
-            yout[oy * p.OW + ln] = E::pack(v);
+                for (int c = 0; c < 8; ++c) q[c] = __builtin_amdgcn_fmed3f(acc2[o][c], lo, hi);
+                yout[(size_t)(oy0 + o) * p.OW] = E::pack(q);
+            }
         }
     }
 }
 
 namespace {
-constexpr int kPwDwNW = 8, kPwDwFMW = 2, kPwDwPF = 4;
+constexpr int kPwDwNW = 8, kPwDwFMW = 2, kPwDwPF = 4, kPwDwR = 7;
 
 int pwdw_nbt(int cfg) { return cfg == 0 ? 8 : 4; }
 
+int pwdw_lpr(int OW) { return OW < 8 ? 8 : OW < 16 ? 16 : 0; }
+
 size_t tail_bytes(int nbt) {   // taps and biases behind the main region
-    const size_t nch = 16 * (size_t)nbt;
-    return (64 * ((nch * 3 / 2 + 63) / 64) + 64 * ((nch / 4 + 63) / 64)) * 16;
+    const size_t nsl = 2 * (size_t)nbt;
+    return (64 * ((nsl * 9 + 63) / 64) + 64 * ((nsl * 2 + 63) / 64)) * 16;
 }
 
-template <typename E, int NBT, int S_>
+template <typename E, int NBT, int S_, int LPR>
 hipError_t launch_pwdw_t(const PwDwParams &p, size_t lds, hipStream_t st) {
-    auto kern = pwdw_kernel<E, kPwDwNW, kPwDwFMW, NBT, S_, kPwDwPF>;
+    auto kern = pwdw_kernel<E, kPwDwNW, kPwDwFMW, NBT, S_, kPwDwR, LPR, kPwDwPF>;
     static const hipError_t attr =
         hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, kPwDwLds);
     if (attr != hipSuccess) return attr;
@@ -273,28 +278,37 @@ hipError_t launch_pwdw_t(const PwDwParams &p, size_t lds, hipStream_t st) {
     return hipGetLastError();
 }
 
-size_t lds_bytes(int ksp, int H, int ipt, int nbt) {
+size_t lds_bytes(int ksp, int nbt) {
     const size_t nk = (size_t)ksp / 4, nchunks = (nk + kPwDwPF - 1) / kPwDwPF;
     const size_t slab = nchunks * nbt * kPwDwPF * 64 * 16;   // weights, whole K in chunks
-    const size_t planes = ((size_t)ipt * 16 * nbt * pwdw_plane(H) + 7) / 8 * 16;
-    return (slab > planes ? slab : planes) + tail_bytes(nbt);
+    const size_t otile = (size_t)2 * nbt * kPwDwPixels * 16;  // pointwise output tile
+    return (slab > otile ? slab : otile) + tail_bytes(nbt);
+}
+
+template <typename E, int NBT>
+hipError_t launch_pwdw_e(const PwDwParams &p, size_t lds, hipStream_t st) {
+    const int lpr = pwdw_lpr(p.OW);
+    if (p.S == 1) return lpr == 8 ? launch_pwdw_t<E, NBT, 1, 8>(p, lds, st) : launch_pwdw_t<E, NBT, 1, 16>(p, lds, st);
+    return lpr == 8 ? launch_pwdw_t<E, NBT, 2, 8>(p, lds, st) : launch_pwdw_t<E, NBT, 2, 16>(p, lds, st);
 }
 }  // namespace
 
 bool pwdw_supported(int H, int W, int OH, int OW, int S, int pt, int pl, int nb16, int ksp, int cfg, int *ipt) {
     if (cfg < 0 || cfg > 1 || H <= 0 || W <= 0 || OH <= 0 || OW <= 0 || (S != 1 && S != 2)) return false;
     const int hw = H * W;
-    // input and output planes of at most 16 x 16 (the MFMA tile); input
-    // columns outside [0, 16) are padding (W <= 16) and drop out of the sum;
-    // input rows read lie in [-1, H], the plane's zero border rows
-    if (H > 16 || W > 16 || OH > 16 || OW > 16 || hw > kPwDwPixels) return false;
-    if (pt < 0 || pt > 1 || pl < 0 || pl > 2 || (OH - 1) * S + 2 - pt > H) return false;
+    // whole images of at most 256 pixels per tile; an output row fits a row
+    // of 8 or 16 lanes with a lane to spare, and every input column a lane
+    // needs from a neighbour is held by a lane of the same row or is padding
+    // (the neighbour past the row's end holds zeros): stride 1 with left
+    // padding 1 and W < lanes, stride 2 with left padding 0 or 1 and
+    // W <= 2 * lanes - 1
+    const int lpr = pwdw_lpr(OW);
+    if (hw > kPwDwPixels || lpr == 0 || pt < 0) return false;
+    if (S == 1 ? (pl != 1 || W >= lpr) : ((pl != 0 && pl != 1) || W > 2 * lpr - 1)) return false;
     const int nbt = pwdw_nbt(cfg);
     if (nb16 % nbt != 0 || ksp % 4 != 0) return false;
-    int n = kPwDwPixels / hw;
-    while (n > 0 && lds_bytes(ksp, H, n, nbt) > (size_t)kPwDwLds) --n;
-    if (n == 0) return false;
-    if (ipt) *ipt = n;
+    if (lds_bytes(ksp, nbt) > (size_t)kPwDwLds) return false;
+    if (ipt) *ipt = kPwDwPixels / hw;
     return true;
 }
 
@@ -304,13 +318,9 @@ hipError_t launch_pwdw(const PwDwParams &p, int cfg, hipStream_t st) {
         p.ipt > ipt || p.ntiles * pwdw_nbt(cfg) != p.nb16 || p.M != p.N * p.H * p.W)
         return hipErrorInvalidValue;
     if (p.N <= 0) return hipSuccess;
-    const size_t lds = lds_bytes(p.ksp, p.H, p.ipt, pwdw_nbt(cfg));
-    if (cfg == 0) {
-        if (p.S == 1) return p.bf16 ? launch_pwdw_t<BF16, 8, 1>(p, lds, st) : launch_pwdw_t<F16, 8, 1>(p, lds, st);
-        return p.bf16 ? launch_pwdw_t<BF16, 8, 2>(p, lds, st) : launch_pwdw_t<F16, 8, 2>(p, lds, st);
-    }
-    if (p.S == 1) return p.bf16 ? launch_pwdw_t<BF16, 4, 1>(p, lds, st) : launch_pwdw_t<F16, 4, 1>(p, lds, st);
-    return p.bf16 ? launch_pwdw_t<BF16, 4, 2>(p, lds, st) : launch_pwdw_t<F16, 4, 2>(p, lds, st);
+    const size_t lds = lds_bytes(p.ksp, pwdw_nbt(cfg));
+    if (cfg == 0) return p.bf16 ? launch_pwdw_e<BF16, 8>(p, lds, st) : launch_pwdw_e<F16, 8>(p, lds, st);
+    return p.bf16 ? launch_pwdw_e<BF16, 4>(p, lds, st) : launch_pwdw_e<F16, 4>(p, lds, st);
 }
 
 }  // namespace kern

@@ -144,15 +144,16 @@ def test_pointwise_depthwise_fusion_structure():
     v2 = engine.Plan(workloads.mobilenet_v2(64), bind=False)
     k2 = [n["kind"] for n in v2.nodes()]
     assert k2.count("pw_dw") == 10
-    # the planner holds fewer tensors once the pointwise outputs vanish
-    v1u = engine.Plan(workloads.mobilenet_v1(64), bind=False, fuse_pwdw=False)
-    assert v1.memory_report()[1] <= v1u.memory_report()[1]
-    # at batch 1 the fused kernel would get 8..16 workgroups: not fused by
-    # default, fused when asked for regardless (fuse_pwdw = 2)
-    b1 = [n["kind"] for n in engine.Plan(workloads.mobilenet_v1(1), bind=False).nodes()]
-    assert b1.count("pw_dw") == 0 and len(b1) == 30
-    b1f = [n["kind"] for n in engine.Plan(workloads.mobilenet_v1(1), bind=False, fuse_pwdw=2).nodes()]
-    assert b1f.count("pw_dw") == 7
+    cf = [c for n, c in zip(nodes, v1.node_configs()) if n["kind"] == "pw_dw"]
+    assert all(name.startswith("img") and k == 3 for _, k, name in cf)   # img64, img128, split
+    # at batch 1 the fused kernel would get 8..16 workgroups: the node runs as
+    # the two separate kernels by default, fused when asked for (fuse_pwdw = 2)
+    b1 = engine.Plan(workloads.mobilenet_v1(1), bind=False)
+    b1c = [c for n, c in zip(b1.nodes(), b1.node_configs()) if n["kind"] == "pw_dw"]
+    assert len(b1c) == 7 and all(name.startswith("split") for _, _, name in b1c)
+    b1f = engine.Plan(workloads.mobilenet_v1(1), bind=False, fuse_pwdw=2)
+    b1fc = [c for n, c in zip(b1f.nodes(), b1f.node_configs()) if n["kind"] == "pw_dw"]
+    assert len(b1fc) == 7 and all(name.startswith("img") for _, _, name in b1fc)
     o = engine.options(fuse_pwdw=3)
     g = engine.build_graph(workloads.mobilenet_v1(1))
     try:
@@ -239,7 +240,7 @@ def test_node_configuration_candidates():
         elif n["kind"] == "dw_conv":
             assert k == 3 and name.startswith("rows")
         elif n["kind"] == "pw_dw":
-            assert 1 <= k <= 2 and name.startswith("img")
+            assert 2 <= k <= 3 and name.startswith(("img", "split"))
         else:
             assert k == 1
     i = next(j for j, n in enumerate(nodes) if n["kind"] == "pw_gemm")
@@ -265,7 +266,9 @@ def test_pad_that_cannot_merge_runs_as_a_node():
 def test_library_memory_report_reproduces_table3(net, key, fuse):
     t3 = {"MobileNet": (9.6, 2.3), "MobileNetV2": (13.2, 4.0)}[key]
     d = workloads.WORKLOADS[net](1, logits_output=False)
-    naive, planned, nobj = engine.Plan(d, fuse=fuse, bind=False).memory_report()
+    # Algorithm 1 on the model graph: the pointwise -> depthwise fusion (which keeps
+    # the pointwise output as a node scratch tensor) is left out
+    naive, planned, nobj = engine.Plan(d, fuse=fuse, bind=False, fuse_pwdw=False).memory_report()
     ops, sizes, inter = oplan.graph_problem(d, oracle.tensor_shapes(d))
     _, ref = oplan.greedy(ops, sizes, inter)
     assert planned == oplan.total(ref)
@@ -319,14 +322,16 @@ def test_library_planner_fig5(golden_dir):
 def test_library_mcfp_reproduces_table3(net, key, mib):
     # Table 3 counts the graph's tensors as given (fusion off); fusing the
     # residual adds of v2 into the projections removes tensors and changes
-    # the flow solution, which must stay no larger than the unfused one
+    # the flow solution, which must stay no larger than the unfused one (the
+    # pointwise -> depthwise fusion adds a scratch tensor per fused node and
+    # is left out here)
     d = workloads.WORKLOADS[net](1, logits_output=False)
     naive, planned, nobj = engine.Plan(d, planner=B.PLANNER_MCFP, fuse=False, bind=False).memory_report()
     ops, sizes, inter = oplan.graph_problem(d, oracle.tensor_shapes(d))
     _, ref, _ = oplan.mcfp(ops, sizes, inter)
     assert round(planned / 2 ** 20, 1) == mib
     assert planned == oplan.total(ref) and nobj == len(ref)
-    fused = engine.Plan(d, planner=B.PLANNER_MCFP, fuse=True, bind=False).memory_report()
+    fused = engine.Plan(d, planner=B.PLANNER_MCFP, fuse=True, bind=False, fuse_pwdw=False).memory_report()
     assert fused[1] <= planned
 
 

@@ -1,15 +1,15 @@
 """Pointwise convolution fused with the depthwise 3x3 convolution that reads
 its output (whole-image tiles, depthwise step on the matrix cores).
 
-The pointwise part accumulates K in the GEMM kernels' order, so the fused
-node differs from the unfused pair only by the depthwise sums, which the
-matrix core forms in fp32 in its own order: fused and unfused outputs agree to
-one unit of the final 16-bit rounding.  Both tile widths (64 and 128 channels)
-compute every output identically and must agree bit for bit.  Every case is
-also held to the oracle at the chained-layer bound.  Shapes cover both
-strides, TF-SAME and symmetric padding, 16 x 16 planes (the largest the kernel
-takes), several images per tile with a ragged last tile, K tails and single
-slices, and batch 1.
+The fused kernel accumulates K in the GEMM kernels' order and each depthwise
+output with the depthwise kernel's tap order, rounding and activation, so
+every configuration of the node -- both tile widths (64 and 128 channels) and
+the split form (the two separate kernels through a scratch tensor) -- and
+the unfused plan must agree bit for bit.  Every case is also held to the
+oracle at the chained-layer bound.  Shapes cover both strides, TF-SAME and
+symmetric padding, the widest rows the kernel takes (15 at stride 1, 16 at
+stride 2), several images per tile with a ragged last tile, K tails and
+single slices, and batch 1.
 """
 import numpy as np
 import pytest
@@ -18,7 +18,7 @@ import oracle
 import workloads
 from workloads import ACT_NONE, ACT_RELU, ACT_RELU6, NetBuilder
 
-from gpu_util import check_layer, log, logits_check, run_gpu, LOGITS_RELL2
+from gpu_util import check_layer, log, run_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -30,7 +30,7 @@ CASES = [
     (3, 13, 15, 40, 64, 1, None, ACT_NONE),         # ragged plane, K tail, linear
     (5, 9, 11, 24, 128, 2, None, ACT_RELU),         # odd sizes at stride 2 (pt 1)
     (2, 16, 16, 64, 64, 2, (1, 1, 1, 1), ACT_RELU6),  # symmetric padding at stride 2
-    (1, 16, 16, 8, 64, 1, None, ACT_RELU6),         # 16 x 16, one K slice, batch 1
+    (1, 15, 15, 8, 64, 1, None, ACT_RELU6),         # 15 x 15 (widest row at stride 1), one K slice, batch 1
     (7, 4, 4, 32, 192, 1, None, ACT_RELU6),         # 16 images per tile
 ]
 
@@ -50,24 +50,28 @@ def fused_nodes(plan):
 
 @pytest.mark.parametrize("n,h,w,K,C,s,pads,act", CASES)
 def test_fused_pair(n, h, w, K, C, s, pads, act):
-    from paper_1907_01989_amd import engine
+    from paper_1907_01989_amd import engine, _binding as B
     desc, y = pair_graph(n, h, w, K, C, s, pads, act)
     plan = engine.Plan(desc, bind=False, fuse_pwdw=2)
     idx = fused_nodes(plan)
     assert len(idx) == 1 and "dw_conv" not in [k["kind"] for k in plan.nodes()]
     ncfg = plan.node_configs()[idx[0]][1]
-    log(f"[case] {desc['name']} ({ncfg} tile widths)")
+    log(f"[case] {desc['name']} ({ncfg} configurations)")
     outs = []
     for c in range(ncfg):
         _, o, _ = run_gpu(desc, materialize_all=False, configs={idx[0]: c}, fuse_pwdw=2)
         outs.append(o[0])
-    for o in outs[1:]:
-        np.testing.assert_array_equal(o, outs[0])
+    names = []
+    for c in range(ncfg):
+        B.mgi_plan_set_node_config(plan.handle, idx[0], c)
+        names.append(plan.node_configs()[idx[0]][2])
+    fused_outs = [o for o, n in zip(outs, names) if n.startswith("img")]
+    split_outs = [o for o, n in zip(outs, names) if n.startswith("split")]
+    assert len(fused_outs) >= 1 and len(split_outs) == 1, names
     _, plain, _ = run_gpu(desc, materialize_all=False, fuse_pwdw=False)
-    fused = outs[0]
-    diff = np.abs(fused.astype(np.float64) - plain[0].astype(np.float64))
-    scale = float(np.abs(plain[0]).max())
-    assert diff.max() <= 2.0 ** -10 * max(scale, 1e-30), (diff.max(), scale)
+    for o in fused_outs + split_outs:
+        np.testing.assert_array_equal(o, plain[0])
+    fused = fused_outs[0]
     ref = oracle.run_graph(desc, keep=[y])[y]
     ok, msg = check_layer("fused output", fused, ref.reshape(fused.shape))
     assert ok, msg
@@ -80,8 +84,7 @@ def test_fused_pair_bf16():
     bdesc = workloads.as_bf16_graph(desc)
     _, fused, _ = run_gpu(bdesc, materialize_all=False, dtype=B.DTYPE_BF16, fuse_pwdw=2)
     _, plain, _ = run_gpu(bdesc, materialize_all=False, dtype=B.DTYPE_BF16, fuse_pwdw=False)
-    diff = np.abs(fused[0].astype(np.float64) - plain[0].astype(np.float64))
-    assert diff.max() <= 2.0 ** -7 * float(np.abs(plain[0]).max())
+    np.testing.assert_array_equal(fused[0], plain[0])
     ref = oracle.run_graph(bdesc, keep=[y], store_bf16=True)[y]
     ok, msg = check_layer("fused bf16 output", fused[0], ref.reshape(fused[0].shape))
     assert ok, msg
@@ -96,9 +99,5 @@ def test_fused_network(net):
     log(f"[case] {net} b64 pointwise->depthwise fused vs unfused")
     _, fused, _ = run_gpu(desc, materialize_all=False)
     _, plain, _ = run_gpu(desc, materialize_all=False, fuse_pwdw=False)
-    # logits (pre-softmax output is not exported; compare the probabilities
-    # and their ranking): both paths see the same network to rounding
-    pf, pp = fused[0].reshape(64, -1), plain[0].reshape(64, -1)
-    rel = np.linalg.norm(pf - pp, axis=1) / np.linalg.norm(pp, axis=1)
-    assert rel.max() <= LOGITS_RELL2, rel.max()
-    assert (pf.argmax(1) == pp.argmax(1)).mean() >= 0.95
+    for a, b in zip(fused, plain):
+        np.testing.assert_array_equal(a, b)
