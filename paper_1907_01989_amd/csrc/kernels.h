@@ -115,8 +115,9 @@ struct DwParams {
 hipError_t launch_depthwise(const DwParams &p, int rows, hipStream_t st);
 
 // Pointwise convolution fused with the depthwise 3x3 convolution (dilation 1,
-// stride 1 or 2) that consumes its output: a workgroup owns ipt whole images
-// and 16*NBT output channels, so the depthwise step needs no halo.
+// stride 1 or 2) that consumes its output: a workgroup owns a channel tile and
+// whole images or a band of output rows (with the input rows they read), so
+// the depthwise step needs no data from other workgroups.
 struct PwDwParams {
     const h8 *x;         // pointwise input, sliced [ksl][M]
     const h8 *w;         // packed pointwise weights [nb16][ksp][16][8]
@@ -126,14 +127,19 @@ struct PwDwParams {
     const float *dw_b;   // [16 * nb16]
     h8 *y;               // depthwise output, sliced [2 * nb16][N * OH * OW]
     int N, H, W, OH, OW, S, pt, pl, act2;
-    int ipt;             // images per tile
-    int ntiles;          // channel tiles (nb16 / NBT)
+    int ipt, nbands, ntiles;   // set by launch_pwdw from the configuration
     int bf16;            // storage type: 0 fp16, 1 bf16
 };
-// cfg selects the channels per tile (0: 128, 1: 64).  pwdw_supported tells
-// whether a shape is covered and gives the images per tile; launch_pwdw
-// returns hipErrorInvalidValue for anything else.
-bool pwdw_supported(int H, int W, int OH, int OW, int S, int pt, int pl, int nb16, int ksp, int cfg, int *ipt);
+// Tiling of one configuration: images per tile (whole-image tiles) or bands
+// per image, tile groups, channel blocks per tile, LDS bytes.
+struct PwDwGeom {
+    int ipt, nbands, groups, nbt;
+    size_t lds;
+};
+// Number of fused-kernel configurations that cover a shape (0: none); for
+// 0 <= cfg < that number, its geometry and name.
+int pwdw_configs(int N, int H, int W, int OH, int OW, int S, int pt, int pl, int ksp, int cfg,
+                 PwDwGeom *g, const char **name);
 hipError_t launch_pwdw(const PwDwParams &p, int cfg, hipStream_t st);
 
 hipError_t launch_add(const h8 *a, const h8 *b, h8 *y, size_t count, int act, bool bf16, hipStream_t st);

@@ -140,19 +140,20 @@ void add_configs(Node &nd, size_t M) {
         // the two separate kernels through the scratch tensor (pipelined GEMM
         // tile by the pointwise rule, depthwise rows by the depthwise rule);
         // the split form first when the fused kernel would not fill the GPU
-        for (int bn : {64, 128}) {
-            const Shape &s = nd.dw_in;
-            if (!kern::pwdw_supported(s.h, s.w, nd.dw_out.h, nd.dw_out.w, nd.dw_conv.stride_h, nd.dw_conv.pad_t,
-                                      nd.dw_conv.pad_l, nd.nb16, nd.ksp, bn == 128 ? 0 : 1, nullptr))
-                continue;
-            GemmTile t;
-            t.bn = bn;
-            nd.cfgs.push_back({t, 0, "img" + std::to_string(bn), false});
+        const Shape &s = nd.dw_in;
+        const int nf = kern::pwdw_configs(s.n, s.h, s.w, nd.dw_out.h, nd.dw_out.w, nd.dw_conv.stride_h,
+                                          nd.dw_conv.pad_t, nd.dw_conv.pad_l, nd.ksp, -1, nullptr, nullptr);
+        for (int c = 0; c < nf; ++c) {
+            const char *name = "";
+            kern::pwdw_configs(s.n, s.h, s.w, nd.dw_out.h, nd.dw_out.w, nd.dw_conv.stride_h, nd.dw_conv.pad_t,
+                               nd.dw_conv.pad_l, nd.ksp, c, nullptr, &name);
+            Node::Config fc{GemmTile{}, 0, name, false, c};
+            nd.cfgs.push_back(fc);
         }
         GemmTile t;
         pick_pipe_tile(t, nd.dw_in.pixels(), nd.nb16 * 16);
-        const Node::Config split{t, nd.dw_conv.stride_h == 1 ? 4 : 2, "split_" + tile_name(t), true};
-        nd.cfgs.insert(nd.fused_default ? nd.cfgs.end() : nd.cfgs.begin(), split);
+        const Node::Config split{t, nd.dw_conv.stride_h == 1 ? 4 : 2, "split_" + tile_name(t), true, 0};
+        nd.cfgs.insert(nd.fused_default ? nd.cfgs.end() : nd.cfgs.begin(), Node::Config(split));
         nd.apply(0);
     } else if (nd.kind == NodeKind::DwPw) {
         // band heights for the fused depthwise + pointwise kernel: up to 128
@@ -223,7 +224,7 @@ void fuse_dw_into_pw(mgi_plan &p) {
 // pointwise GEMM node without residual whose output only feeds one 3x3
 // depthwise node (dilation 1, stride 1 or 2) becomes a single node producing
 // the depthwise output, when the planes fit the fused kernel's whole-image
-// tiles (pwdw_supported).  The intermediate tensor stays planned as the
+// tiles or bands (pwdw_configs).  The intermediate tensor stays planned as the
 // node's scratch, so the node can also run as the two separate kernels; the
 // fused kernel is its default configuration when it gets at least 128
 // workgroups (or `always`): with fewer, the separate kernels, which split
@@ -248,11 +249,11 @@ void fuse_pw_into_dw(mgi_plan &p, bool always) {
         Node &pw = p.nodes[producer[mid]];
         if (pw.kind != NodeKind::Gemm || pw.taps || pw.residual >= 0 || pw.in.size() != 1) continue;
         const Shape in = p.bufs[mid].shape, out = p.bufs[dw.out].shape;
-        int ipt = 0;
-        if (!kern::pwdw_supported(in.h, in.w, out.h, out.w, c.stride_h, c.pad_t, c.pad_l, pw.nb16, pw.ksp, 1,
-                                  &ipt))
+        kern::PwDwGeom geo{};
+        if (kern::pwdw_configs(in.n, in.h, in.w, out.h, out.w, c.stride_h, c.pad_t, c.pad_l, pw.ksp, 0, &geo,
+                               nullptr) == 0)
             continue;
-        pw.fused_default = always || (size_t)(in.n + ipt - 1) / ipt * (pw.nb16 / 4) >= 128;
+        pw.fused_default = always || (size_t)geo.groups * ((pw.nb16 + geo.nbt - 1) / geo.nbt) >= 128;
         pw.kind = NodeKind::PwDw;
         pw.kname = "pw_dw";
         pw.dw_op = dw.op;

@@ -112,7 +112,7 @@ struct Node {
     int dw_rows = 0;        // depthwise 3x3: output rows per thread (0 = kernel default)
     // DwPw / PwDw: the absorbed depthwise op (the pointwise input's producer,
     // or the pointwise output's consumer), its window, activation and packed
-    // taps; for PwDw tile.bn is the fused kernel's channels per tile
+    // taps
     int dw_op = -1;
     mgi_conv_desc dw_conv{};
     int dw_act = MGI_ACT_NONE;
@@ -126,11 +126,13 @@ struct Node {
     int scratch = -1;
     bool split = false;
     bool fused_default = true;
+    int pwdw_cfg = 0;       // PwDw: configuration of the fused kernel (pwdw_configs)
     struct Config {
         GemmTile tile;
         int dw_rows = 0;
         std::string name;
         bool split = false;
+        int pwdw_cfg = 0;
     };
     std::vector<Config> cfgs;
     int cfg = 0;
@@ -139,6 +141,7 @@ struct Node {
         tile = cfgs[c].tile;
         dw_rows = cfgs[c].dw_rows;
         split = cfgs[c].split;
+        pwdw_cfg = cfgs[c].pwdw_cfg;
     }
 };
 

@@ -180,11 +180,7 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
             q.N = nd.dw_in.n; q.H = nd.dw_in.h; q.W = nd.dw_in.w; q.OH = os.h; q.OW = os.w;
             q.S = nd.dw_conv.stride_h; q.pt = nd.dw_conv.pad_t; q.pl = nd.dw_conv.pad_l;
             q.act2 = nd.dw_act;
-            const int cfg = nd.tile.bn == 128 ? 0 : 1;
-            if (!pwdw_supported(q.H, q.W, q.OH, q.OW, q.S, q.pt, q.pl, q.nb16, q.ksp, cfg, &q.ipt))
-                return hipErrorInvalidValue;
-            q.ntiles = q.nb16 / (cfg == 0 ? 8 : 4);
-            return launch_pwdw(q, cfg, st);
+            return launch_pwdw(q, nd.pwdw_cfg, st);
         }
         case NodeKind::Depthwise: {
             const Buf &ib = p.bufs[nd.in[0]];

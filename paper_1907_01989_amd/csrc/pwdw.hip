@@ -4,27 +4,26 @@
 // MobileNet stage).
 //
 // Unfused, the pointwise output is written to memory and read straight back by
-// the depthwise kernel, and each of the two kernels pays its own launch and
-// ramp.  Here a workgroup owns `ipt` whole images (at most 256 pixels, planes of
-// at most 16 x 16) and 16*NBT output channels of the pointwise convolution, so
-// the depthwise step over those channels needs no halo from other workgroups:
-//   1. the depthwise taps and biases are copied into LDS by direct
-//      global->LDS loads;
+// the depthwise kernel (on the 112 x 112 and 56 x 56 planes of a batch of 64
+// that round trip is hundreds of MB), and each of the two kernels pays its own
+// launch and ramp.  Here a workgroup owns 16*NBT output channels of the
+// pointwise convolution (a channel tile; the last one may be partial) and
+// either `ipt` whole images (at most 16*NW*FMW pixels) or a band of R output
+// rows of one image together with the input rows those need (the halo rows
+// are computed by both neighbouring bands), so the depthwise step over its
+// channels needs nothing from other workgroups:
+//   1. the weights (NBT channel blocks x all of K), the depthwise taps and
+//      biases are copied into LDS by direct global->LDS loads;
 //   2. each wave owns FMW fragments of 16 pixels and all NBT channel blocks;
 //      its activation fragments stream from the sliced layout into registers
 //      PF K-steps ahead of use, and the MFMAs (v_mfma_f32_16x16x32, K
-//      ascending, as in the GEMM kernels) read the weight fragments from LDS.
-//      The weights (NBT channel blocks x all of K) are copied into LDS by
-//      direct global->LDS loads before the K loop.  (Waiting for them chunk by
-//      chunk, or streaming them through a two-chunk ring, measured no faster:
-//      the loop is bound by the L2->CU transfer of activations and weights,
-//      about 324 KiB per workgroup at v1's 14x14 stage);
+//      ascending, as in the GEMM kernels) read the weight fragments from LDS;
 //   3. bias and activation are applied and the 16-bit pointwise output tile
 //      is parked in LDS, slice-major, in place of the weights;
 //   4. the depthwise convolution runs from LDS: one lane per output column, a
-//      row of lanes per (image, slice, strip of R output rows); the left and
-//      right input columns come from the neighbouring lanes by wave-wide DPP
-//      shifts (lanes past the last column hold zeros, which is the zero
+//      row of LPR lanes per (image, slice, strip of R output rows); the left
+//      and right input columns come from the neighbouring lanes by wave-wide
+//      DPP shifts (lanes past the row's end hold zeros, which is the zero
 //      padding).
 // Accumulation order, rounding points and activations are those of the
 // separate GEMM and depthwise kernels, so the result is bit-identical to the
@@ -47,59 +46,76 @@ __device__ __forceinline__ h8 wave_shift(h8 v) {
     return __builtin_bit_cast(h8, r);
 }
 
-constexpr int kPwDwPixels = 256;   // pixel capacity of a tile (16 fragments)
+constexpr int kPwDwNW = 8;         // waves per workgroup
 constexpr int kPwDwLds = 160 * 1024;
 
-template <typename E, int NW, int FMW, int NBT, int S_, int R, int LPR, int PF>
-__global__ __launch_bounds__(NW * 64) void pwdw_kernel(PwDwParams p) {
-    constexpr int PMAX = 16 * NW * FMW;
-    constexpr int NCH = 16 * NBT;                 // output channels of the tile
+template <typename E, int FMW, int NBT, int S_, int R, int LPR, int PF>
+__global__ __launch_bounds__(kPwDwNW * 64) void pwdw_kernel(PwDwParams p) {
+    constexpr int NW = kPwDwNW;
+    constexpr int PMAX = 16 * NW * FMW;           // pixel capacity of a tile
+    constexpr int NCH = 16 * NBT;                 // output channels of a tile
     constexpr int NSL = 2 * NBT;                  // ... in sliced elements
-    static_assert(PMAX == kPwDwPixels, "tile capacity");
+    constexpr int GPI = NW * 64 / LPR;            // lane rows per pass of the depthwise step
     constexpr int CK = PF;                        // K-steps per weight chunk
     constexpr int SQ = NBT * CK;                  // 64-element wave loads per chunk
-    static_assert(SQ % NW == 0, "weight chunk split");
-    constexpr int DPW = SQ / NW;                  // ... per wave
-    constexpr int GPI = NW * 64 / LPR;            // lane rows per pass of the depthwise step
     constexpr int kTapQ = (NSL * 9 + 63) / 64, kTapH8 = 64 * kTapQ;   // taps [NSL][9], whole wave loads
     constexpr int kBiasQ = (NCH / 4 + 63) / 64;
+    static_assert(LPR <= 64 && 64 % LPR == 0, "a lane row lies in one wave");
     extern __shared__ h8 lds[];
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int tile = xcd_tile(blockIdx.x, gridDim.x);
     const int grp = tile / p.ntiles, ct = tile - grp * p.ntiles;
-    const int hw = p.H * p.W;
-    const int img0 = grp * p.ipt;
-    const int nimg = min(p.ipt, p.N - img0);
-    const int P = nimg * hw;                      // valid pixels of the tile
-    const int m0 = img0 * hw;
     const int nb0 = ct * NBT;
+    const int nbv = min(NBT, p.nb16 - nb0);       // channel blocks of this tile
+    // pixels of the tile: whole images img0 .. img0+nimg-1, or the input rows
+    // [ir0, ir1) of image img0 that output rows [oy_lo, oy_hi) read
+    int img0, nimg, oy_lo, oy_hi, ir0, ir1;
+    if (p.nbands) {
+        img0 = grp / p.nbands;
+        nimg = 1;
+        oy_lo = (grp - img0 * p.nbands) * R;
+        oy_hi = min(p.OH, oy_lo + R);
+        ir0 = max(0, oy_lo * S_ - p.pt);
+        ir1 = min(p.H, (oy_hi - 1) * S_ - p.pt + 3);
+    } else {
+        img0 = grp * p.ipt;
+        nimg = min(p.ipt, p.N - img0);
+        oy_lo = 0;
+        oy_hi = p.OH;
+        ir0 = 0;
+        ir1 = p.H;
+    }
+    const int thw = (ir1 - ir0) * p.W;            // tile pixels per image
+    const int P = nimg * thw;                     // valid pixels of the tile
+    const int m0 = (img0 * p.H + ir0) * p.W;
     const int ksp = p.ksp, nk = ksp >> 2;
     const int nchunks = (nk + CK - 1) / CK;
     const int main_h8 = max(nchunks * SQ * 64, NSL * PMAX);
     const h8 *taps = lds + main_h8;                               // [NSL][9]
-    const float *dwb = (const float *)(lds + main_h8 + kTapH8);  // [NSL][8]
+    const float *dwb = (const float *)(lds + main_h8 + kTapH8);  // [NCH]
 
     // 1. weights -> LDS in K order, chunk c = K-steps [c*CK, c*CK + CK) of the
     // NBT channel blocks, layout [chunk][NBT][CK][64]; wave load q of a chunk
-    // is channel block q / CK, K-step q % CK (steps past K read the last one);
-    // then the taps and depthwise biases (sources clamped to their last
-    // element; the copies past the end land in padding)
+    // is channel block q / CK, K-step q % CK (steps past K read the last one,
+    // blocks past the tile's last read the last valid one: their results are
+    // never stored); then the taps and depthwise biases (sources clamped to
+    // their last element; the copies past the end land in padding)
     {
         for (int c = 0; c < nchunks; ++c) {
-#pragma unroll
-            for (int r = 0; r < DPW; ++r) {
-                const int q = wave + NW * r, i = q / CK, kk = min(c * CK + q % CK, nk - 1);
+            for (int q = wave; q < SQ; q += NW) {
+                const int i = min(q / CK, nbv - 1), kk = min(c * CK + q % CK, nk - 1);
                 load_lds16(p.w + ((size_t)(nb0 + i) * ksp + kk * 4) * 16 + lane, lds + (c * SQ + q) * 64);
             }
         }
         const h8 *tsrc = p.dw_w + (size_t)nb0 * 2 * 9;
         const h8 *bsrc = (const h8 *)(p.dw_b + nb0 * 16);
+        const int tn = nbv * 2 * 9, bn = nbv * 4;
         for (int q = wave; q < kTapQ + kBiasQ; q += NW) {
             const int e = (q < kTapQ ? q : q - kTapQ) * 64 + lane;
-            if (q < kTapQ) load_lds16(tsrc + min(e, NSL * 9 - 1), lds + main_h8 + e);
-            else load_lds16(bsrc + min(e, NCH / 4 - 1), lds + main_h8 + kTapH8 + e);
+            if (q < kTapQ) load_lds16(tsrc + min(e, tn - 1), lds + main_h8 + e);
+            else load_lds16(bsrc + min(e, bn - 1), lds + main_h8 + kTapH8 + e);
         }
     }
 
@@ -161,6 +177,7 @@ __global__ __launch_bounds__(NW * 64) void pwdw_kernel(PwDwParams p) {
     __syncthreads();
 #pragma unroll
     for (int i = 0; i < NBT; ++i) {
+        if (i >= nbv) break;
         const int c = i * 16 + 4 * (lane >> 4);       // channel within the tile
         float bv[4];
 #pragma unroll
@@ -181,8 +198,9 @@ __global__ __launch_bounds__(NW * 64) void pwdw_kernel(PwDwParams p) {
     // depthwise kernel
     constexpr int NR = (R - 1) * S_ + 3;          // input rows of a strip
     constexpr int NC = S_;                        // input columns loaded per lane
-    const int nstrips = (p.OH + R - 1) / R;
-    const int ngroups = nimg * NSL * nstrips;
+    const int nsl = 2 * nbv;
+    const int nstrips = p.nbands ? 1 : (p.OH + R - 1) / R;
+    const int ngroups = nimg * nsl * nstrips;
     const int ox = tid % LPR;
     const float lo = p.act2 == MGI_ACT_NONE ? -INFINITY : 0.0f;
     const float hi = p.act2 == MGI_ACT_RELU6 ? 6.0f : INFINITY;
@@ -192,9 +210,9 @@ __global__ __launch_bounds__(NW * 64) void pwdw_kernel(PwDwParams p) {
         const bool gv = g < ngroups;
         const int gg = gv ? g : 0;
         const int strip = gg % nstrips, rest = gg / nstrips;
-        const int sl = rest % NSL, t = rest / NSL;
-        const int oy0 = strip * R, iy0 = oy0 * S_ - p.pt;
-        const h8 *plane = lds + sl * PMAX + t * hw;
+        const int sl = rest % nsl, t = rest / nsl;
+        const int oy0 = oy_lo + strip * R, iy0 = oy0 * S_ - p.pt;
+        const h8 *plane = lds + sl * PMAX + t * thw;
         h8 w[9];
 #pragma unroll
         for (int k = 0; k < 9; ++k) w[k] = taps[sl * 9 + k];
@@ -213,10 +231,10 @@ __global__ __launch_bounds__(NW * 64) void pwdw_kernel(PwDwParams p) {
 #pragma unroll
         for (int r = 0; r < NR; ++r) {
             const int iy = iy0 + r;
-            const bool rv = iy >= 0 && iy < p.H;
+            const bool rv = iy >= ir0 && iy < ir1;
             h8 v[NC];
 #pragma unroll
-            for (int k = 0; k < NC; ++k) v[k] = (rv && cv[k]) ? plane[iy * p.W + cx[k]] : zero_h8();
+            for (int k = 0; k < NC; ++k) v[k] = (rv && cv[k]) ? plane[(iy - ir0) * p.W + cx[k]] : zero_h8();
             h8 t3[3];
             if (S_ == 1) {          // columns ox-1, ox, ox+1 (left padding 1)
                 t3[0] = wave_shift<kWaveShr1>(v[0]);
@@ -245,7 +263,7 @@ __global__ __launch_bounds__(NW * 64) void pwdw_kernel(PwDwParams p) {
             h8 *yout = p.y + ((size_t)gs * p.N + img0 + t) * p.OH * p.OW + ox;
 #pragma unroll
             for (int o = 0; o < R; ++o) {
-                if (oy0 + o >= p.OH) break;
+                if (oy0 + o >= oy_hi) break;
                 float q[8];
 #pragma unroll
                 for (int c = 0; c < 8; ++c) q[c] = __builtin_amdgcn_fmed3f(acc2[o][c], lo, hi);
@@ -255,72 +273,141 @@ __global__ __launch_bounds__(NW * 64) void pwdw_kernel(PwDwParams p) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// Instances.  A whole-image instance takes images of at most 16*8*FMW pixels
+// whose output rows fit a lane row (OW < LPR); a band instance takes R output
+// rows per workgroup.  Each instance covers one stride and one lane-row width.
+// ---------------------------------------------------------------------------
 namespace {
-constexpr int kPwDwNW = 8, kPwDwFMW = 2, kPwDwPF = 4, kPwDwR = 7;
 
-int pwdw_nbt(int cfg) { return cfg == 0 ? 8 : 4; }
+struct Inst {
+    bool band;
+    int fmw, nbt, s, r, lpr, pf;
+    const char *name;
+};
 
-int pwdw_lpr(int OW) { return OW < 8 ? 8 : OW < 16 ? 16 : 0; }
+// the candidates, in preference order for a shape
+const Inst kInsts[] = {
+    {false, 2, 4, 1, 7, 16, 4, "img64"},   {false, 2, 8, 1, 7, 16, 4, "img128"},
+    {false, 2, 4, 1, 7, 8, 4, "img64"},    {false, 2, 8, 1, 7, 8, 4, "img128"},
+    {false, 2, 4, 2, 7, 16, 4, "img64"},   {false, 2, 8, 2, 7, 16, 4, "img128"},
+    {false, 2, 4, 2, 7, 8, 4, "img64"},    {false, 2, 8, 2, 7, 8, 4, "img128"},
+    {true, 2, 8, 2, 4, 16, 4, "band4x128"},                                   // 28 -> 14 at stride 2
+    {true, 2, 8, 1, 4, 32, 4, "band4x128"},                                   // 28 x 28
+    {true, 4, 8, 2, 4, 32, 4, "band4x128"},                                   // 56 -> 28
+    {true, 3, 8, 1, 4, 64, 2, "band4x128"},                                   // 56 x 56
+    {true, 8, 4, 2, 4, 64, 2, "band4x64"},                                    // 112 -> 56
+    {true, 4, 4, 1, 4, 64, 2, "band4x64"},                                    // 56 x 56, 64 channels
+};
+constexpr int kNumInsts = sizeof(kInsts) / sizeof(kInsts[0]);
+
+int lanes_for(int OW) { return OW < 8 ? 8 : OW < 16 ? 16 : OW < 32 ? 32 : OW < 64 ? 64 : 0; }
 
 size_t tail_bytes(int nbt) {   // taps and biases behind the main region
-    const size_t nsl = 2 * (size_t)nbt;
-    return (64 * ((nsl * 9 + 63) / 64) + 64 * ((nsl * 2 + 63) / 64)) * 16;
+    const size_t nsl = 2 * (size_t)nbt, nch = 16 * (size_t)nbt;
+    return (64 * ((nsl * 9 + 63) / 64) + 64 * ((nch / 4 + 63) / 64)) * 16;
 }
 
-template <typename E, int NBT, int S_, int LPR>
-hipError_t launch_pwdw_t(const PwDwParams &p, size_t lds, hipStream_t st) {
-    auto kern = pwdw_kernel<E, kPwDwNW, kPwDwFMW, NBT, S_, kPwDwR, LPR, kPwDwPF>;
+size_t lds_bytes(const Inst &in, int ksp) {
+    const size_t nk = (size_t)ksp / 4, nchunks = (nk + in.pf - 1) / in.pf;
+    const size_t slab = nchunks * in.nbt * in.pf * 64 * 16;                // weights, all of K
+    const size_t otile = (size_t)2 * in.nbt * 16 * kPwDwNW * in.fmw * 16;  // pointwise output tile
+    return (slab > otile ? slab : otile) + tail_bytes(in.nbt);
+}
+
+// geometry of instance `in` for a shape, or false if it does not apply
+bool fits(const Inst &in, int N, int H, int W, int OH, int OW, int S, int pt, int pl, int ksp,
+          PwDwGeom *g) {
+    if (S != in.s || lanes_for(OW) != in.lpr || pt < 0) return false;
+    // every input column a lane needs from a neighbour is held by a lane of the
+    // same row, or is padding (the neighbour past the row's end holds zeros)
+    if (S == 1 ? (pl != 1 || W >= in.lpr) : ((pl != 0 && pl != 1) || W > 2 * in.lpr - 1)) return false;
+    if (lds_bytes(in, ksp) > (size_t)kPwDwLds) return false;
+    const int pmax = 16 * kPwDwNW * in.fmw;
+    if (!in.band) {
+        if (H * W > pmax) return false;
+        g->ipt = pmax / (H * W);
+        g->nbands = 0;
+        g->groups = (N + g->ipt - 1) / g->ipt;
+    } else {
+        // a band's input rows: (R - 1) * S + 3 at most
+        if (((in.r - 1) * S + 3) * W > pmax) return false;
+        g->ipt = 1;
+        g->nbands = (OH + in.r - 1) / in.r;
+        g->groups = N * g->nbands;
+    }
+    g->nbt = in.nbt;
+    g->lds = lds_bytes(in, ksp);
+    return true;
+}
+
+template <typename E, int FMW, int NBT, int S_, int R, int LPR, int PF>
+hipError_t launch_t(const PwDwParams &p, size_t lds, hipStream_t st) {
+    auto kern = pwdw_kernel<E, FMW, NBT, S_, R, LPR, PF>;
     static const hipError_t attr =
         hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, kPwDwLds);
     if (attr != hipSuccess) return attr;
-    const int groups = (p.N + p.ipt - 1) / p.ipt;
+    const int groups = p.nbands ? p.N * p.nbands : (p.N + p.ipt - 1) / p.ipt;
     launch(kern, dim3(groups * p.ntiles), dim3(kPwDwNW * 64), (unsigned)lds, st, p);
     return hipGetLastError();
 }
 
-size_t lds_bytes(int ksp, int nbt) {
-    const size_t nk = (size_t)ksp / 4, nchunks = (nk + kPwDwPF - 1) / kPwDwPF;
-    const size_t slab = nchunks * nbt * kPwDwPF * 64 * 16;   // weights, whole K in chunks
-    const size_t otile = (size_t)2 * nbt * kPwDwPixels * 16;  // pointwise output tile
-    return (slab > otile ? slab : otile) + tail_bytes(nbt);
+template <typename E>
+hipError_t launch_inst(int k, const PwDwParams &p, size_t lds, hipStream_t st) {
+    switch (k) {
+#define MGI_PWDW(K_, FMW_, NBT_, S_, R_, LPR_, PF_) \
+    case K_: return launch_t<E, FMW_, NBT_, S_, R_, LPR_, PF_>(p, lds, st);
+        MGI_PWDW(0, 2, 4, 1, 7, 16, 4) MGI_PWDW(1, 2, 8, 1, 7, 16, 4)
+        MGI_PWDW(2, 2, 4, 1, 7, 8, 4) MGI_PWDW(3, 2, 8, 1, 7, 8, 4)
+        MGI_PWDW(4, 2, 4, 2, 7, 16, 4) MGI_PWDW(5, 2, 8, 2, 7, 16, 4)
+        MGI_PWDW(6, 2, 4, 2, 7, 8, 4) MGI_PWDW(7, 2, 8, 2, 7, 8, 4)
+        MGI_PWDW(8, 2, 8, 2, 4, 16, 4) MGI_PWDW(9, 2, 8, 1, 4, 32, 4)
+        MGI_PWDW(10, 4, 8, 2, 4, 32, 4) MGI_PWDW(11, 3, 8, 1, 4, 64, 2)
+        MGI_PWDW(12, 8, 4, 2, 4, 64, 2) MGI_PWDW(13, 4, 4, 1, 4, 64, 2)
+#undef MGI_PWDW
+    }
+    return hipErrorInvalidValue;
 }
 
-template <typename E, int NBT>
-hipError_t launch_pwdw_e(const PwDwParams &p, size_t lds, hipStream_t st) {
-    const int lpr = pwdw_lpr(p.OW);
-    if (p.S == 1) return lpr == 8 ? launch_pwdw_t<E, NBT, 1, 8>(p, lds, st) : launch_pwdw_t<E, NBT, 1, 16>(p, lds, st);
-    return lpr == 8 ? launch_pwdw_t<E, NBT, 2, 8>(p, lds, st) : launch_pwdw_t<E, NBT, 2, 16>(p, lds, st);
+// the applicable instances of a shape, in table order
+int applicable(int N, int H, int W, int OH, int OW, int S, int pt, int pl, int ksp, int *idx,
+               PwDwGeom *geo) {
+    int n = 0;
+    for (int k = 0; k < kNumInsts; ++k) {
+        PwDwGeom g{};
+        if (!fits(kInsts[k], N, H, W, OH, OW, S, pt, pl, ksp, &g)) continue;
+        if (idx) idx[n] = k;
+        if (geo) geo[n] = g;
+        ++n;
+    }
+    return n;
 }
 }  // namespace
 
-bool pwdw_supported(int H, int W, int OH, int OW, int S, int pt, int pl, int nb16, int ksp, int cfg, int *ipt) {
-    if (cfg < 0 || cfg > 1 || H <= 0 || W <= 0 || OH <= 0 || OW <= 0 || (S != 1 && S != 2)) return false;
-    const int hw = H * W;
-    // whole images of at most 256 pixels per tile; an output row fits a row
-    // of 8 or 16 lanes with a lane to spare, and every input column a lane
-    // needs from a neighbour is held by a lane of the same row or is padding
-    // (the neighbour past the row's end holds zeros): stride 1 with left
-    // padding 1 and W < lanes, stride 2 with left padding 0 or 1 and
-    // W <= 2 * lanes - 1
-    const int lpr = pwdw_lpr(OW);
-    if (hw > kPwDwPixels || lpr == 0 || pt < 0) return false;
-    if (S == 1 ? (pl != 1 || W >= lpr) : ((pl != 0 && pl != 1) || W > 2 * lpr - 1)) return false;
-    const int nbt = pwdw_nbt(cfg);
-    if (nb16 % nbt != 0 || ksp % 4 != 0) return false;
-    if (lds_bytes(ksp, nbt) > (size_t)kPwDwLds) return false;
-    if (ipt) *ipt = kPwDwPixels / hw;
-    return true;
+int pwdw_configs(int N, int H, int W, int OH, int OW, int S, int pt, int pl, int ksp, int cfg,
+                 PwDwGeom *g, const char **name) {
+    int idx[kNumInsts];
+    PwDwGeom geo[kNumInsts];
+    const int n = applicable(N, H, W, OH, OW, S, pt, pl, ksp, idx, geo);
+    if (cfg >= 0 && cfg < n) {
+        if (g) *g = geo[cfg];
+        if (name) *name = kInsts[idx[cfg]].name;
+    }
+    return n;
 }
 
 hipError_t launch_pwdw(const PwDwParams &p, int cfg, hipStream_t st) {
-    int ipt = 0;
-    if (!pwdw_supported(p.H, p.W, p.OH, p.OW, p.S, p.pt, p.pl, p.nb16, p.ksp, cfg, &ipt) || p.ipt < 1 ||
-        p.ipt > ipt || p.ntiles * pwdw_nbt(cfg) != p.nb16 || p.M != p.N * p.H * p.W)
-        return hipErrorInvalidValue;
+    int idx[kNumInsts];
+    PwDwGeom geo[kNumInsts];
+    const int n = applicable(p.N, p.H, p.W, p.OH, p.OW, p.S, p.pt, p.pl, p.ksp, idx, geo);
+    if (cfg < 0 || cfg >= n || p.M != p.N * p.H * p.W || p.ksp % 4 != 0 || p.nb16 <= 0) return hipErrorInvalidValue;
+    const PwDwGeom &g = geo[cfg];
+    PwDwParams q = p;
+    q.ipt = g.ipt;
+    q.nbands = g.nbands;
+    q.ntiles = (p.nb16 + g.nbt - 1) / g.nbt;
     if (p.N <= 0) return hipSuccess;
-    const size_t lds = lds_bytes(p.ksp, pwdw_nbt(cfg));
-    if (cfg == 0) return p.bf16 ? launch_pwdw_e<BF16, 8>(p, lds, st) : launch_pwdw_e<F16, 8>(p, lds, st);
-    return p.bf16 ? launch_pwdw_e<BF16, 4>(p, lds, st) : launch_pwdw_e<F16, 4>(p, lds, st);
+    return p.bf16 ? launch_inst<BF16>(idx[cfg], q, g.lds, st) : launch_inst<F16>(idx[cfg], q, g.lds, st);
 }
 
 }  // namespace kern

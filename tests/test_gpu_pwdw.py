@@ -7,9 +7,10 @@ every configuration of the node -- both tile widths (64 and 128 channels) and
 the split form (the two separate kernels through a scratch tensor) -- and
 the unfused plan must agree bit for bit.  Every case is also held to the
 oracle at the chained-layer bound.  Shapes cover both strides, TF-SAME and
-symmetric padding, the widest rows the kernel takes (15 at stride 1, 16 at
-stride 2), several images per tile with a ragged last tile, K tails and
-single slices, and batch 1.
+symmetric padding, whole-image tiles (several images per tile, ragged last
+tile) and row bands (every v1 band shape, odd planes with a short last band),
+partial channel tiles (v2's 96 and 144 channels), K tails and single
+slices, and batch 1.
 """
 import numpy as np
 import pytest
@@ -32,6 +33,16 @@ CASES = [
     (2, 16, 16, 64, 64, 2, (1, 1, 1, 1), ACT_RELU6),  # symmetric padding at stride 2
     (1, 15, 15, 8, 64, 1, None, ACT_RELU6),         # 15 x 15 (widest row at stride 1), one K slice, batch 1
     (7, 4, 4, 32, 192, 1, None, ACT_RELU6),         # 16 images per tile
+    # row bands (a halo row computed by both neighbouring bands)
+    (3, 112, 112, 32, 64, 2, None, ACT_RELU6),      # v1 pw1 -> dw2
+    (2, 56, 56, 64, 128, 1, None, ACT_RELU6),       # v1 pw2 -> dw3
+    (2, 56, 56, 128, 128, 2, None, ACT_RELU6),      # v1 pw3 -> dw4
+    (3, 28, 28, 128, 256, 1, None, ACT_RELU6),      # v1 pw4 -> dw5
+    (3, 28, 28, 256, 256, 2, None, ACT_RELU6),      # v1 pw5 -> dw6
+    (2, 56, 56, 24, 144, 1, None, ACT_RELU6),       # v2 expansion, partial channel tile (9 blocks)
+    (2, 112, 112, 16, 96, 2, None, ACT_RELU6),      # v2 expansion at 112, 6 blocks
+    (2, 27, 29, 40, 80, 1, None, ACT_NONE),         # odd plane, last band short, K tail
+    (2, 55, 53, 24, 64, 2, (1, 1, 1, 1), ACT_RELU6),  # odd plane at stride 2, symmetric padding
 ]
 
 
@@ -65,7 +76,7 @@ def test_fused_pair(n, h, w, K, C, s, pads, act):
     for c in range(ncfg):
         B.mgi_plan_set_node_config(plan.handle, idx[0], c)
         names.append(plan.node_configs()[idx[0]][2])
-    fused_outs = [o for o, n in zip(outs, names) if n.startswith("img")]
+    fused_outs = [o for o, n in zip(outs, names) if n.startswith(("img", "band"))]
     split_outs = [o for o, n in zip(outs, names) if n.startswith("split")]
     assert len(fused_outs) >= 1 and len(split_outs) == 1, names
     _, plain, _ = run_gpu(desc, materialize_all=False, fuse_pwdw=False)
