@@ -128,12 +128,13 @@ struct PwDwParams {
     h8 *y;               // depthwise output, sliced [2 * nb16][N * OH * OW]
     int N, H, W, OH, OW, S, pt, pl, act2;
     int ipt, nbands, ntiles;   // set by launch_pwdw from the configuration
+    int pstride;         // ... pixel stride of the LDS output tile
     int bf16;            // storage type: 0 fp16, 1 bf16
 };
 // Tiling of one configuration: images per tile (whole-image tiles) or bands
 // per image, tile groups, channel blocks per tile, LDS bytes.
 struct PwDwGeom {
-    int ipt, nbands, groups, nbt;
+    int ipt, nbands, groups, nbt, pstride;
     size_t lds;
 };
 // Number of fused-kernel configurations that cover a shape (0: none); for

@@ -14,7 +14,8 @@
 // channels needs nothing from other workgroups:
 //   1. the weights (NBT channel blocks x all of K), the depthwise taps and
 //      biases are copied into LDS by direct global->LDS loads;
-//   2. each wave owns FMW fragments of 16 pixels and all NBT channel blocks;
+//   2. each of the NW waves owns FMW fragments of 16 pixels and all NBT
+//      channel blocks;
 //      its activation fragments stream from the sliced layout into registers
 //      PF K-steps ahead of use, and the MFMAs (v_mfma_f32_16x16x32, K
 //      ascending, as in the GEMM kernels) read the weight fragments from LDS;
@@ -28,6 +29,8 @@
 // Accumulation order, rounding points and activations are those of the
 // separate GEMM and depthwise kernels, so the result is bit-identical to the
 // unfused pair (and to the node's split form, which runs those kernels).
+#include <algorithm>
+
 #include "device.h"
 
 namespace mgi {
@@ -46,13 +49,11 @@ __device__ __forceinline__ h8 wave_shift(h8 v) {
     return __builtin_bit_cast(h8, r);
 }
 
-constexpr int kPwDwNW = 8;         // waves per workgroup
 constexpr int kPwDwLds = 160 * 1024;
 
-template <typename E, int FMW, int NBT, int S_, int R, int LPR, int PF>
-__global__ __launch_bounds__(kPwDwNW * 64) void pwdw_kernel(PwDwParams p) {
-    constexpr int NW = kPwDwNW;
-    constexpr int PMAX = 16 * NW * FMW;           // pixel capacity of a tile
+template <typename E, int NW, int FMW, int NBT, int S_, int R, int LPR, int PF>
+__global__ __launch_bounds__(NW * 64, 2) void pwdw_kernel(PwDwParams p) {   // >= 2 waves per SIMD: <= 256 VGPRs
+    const int PMAX = p.pstride;                   // pixel stride of the LDS output tile (>= a tile's pixels)
     constexpr int NCH = 16 * NBT;                 // output channels of a tile
     constexpr int NSL = 2 * NBT;                  // ... in sliced elements
     constexpr int GPI = NW * 64 / LPR;            // lane rows per pass of the depthwise step
@@ -61,6 +62,7 @@ __global__ __launch_bounds__(kPwDwNW * 64) void pwdw_kernel(PwDwParams p) {
     constexpr int kTapQ = (NSL * 9 + 63) / 64, kTapH8 = 64 * kTapQ;   // taps [NSL][9], whole wave loads
     constexpr int kBiasQ = (NCH / 4 + 63) / 64;
     static_assert(LPR <= 64 && 64 % LPR == 0, "a lane row lies in one wave");
+    static_assert(NW == 4 || NW == 8, "waves per workgroup");
     extern __shared__ h8 lds[];
 
     const int tid = threadIdx.x, lane = tid & 63;
@@ -274,7 +276,7 @@ __global__ __launch_bounds__(kPwDwNW * 64) void pwdw_kernel(PwDwParams p) {
 }
 
 // ---------------------------------------------------------------------------
-// Instances.  A whole-image instance takes images of at most 16*8*FMW pixels
+// Instances.  A whole-image instance takes images of at most 16*NW*FMW pixels
 // whose output rows fit a lane row (OW < LPR); a band instance takes R output
 // rows per workgroup.  Each instance covers one stride and one lane-row width.
 // ---------------------------------------------------------------------------
@@ -282,22 +284,24 @@ namespace {
 
 struct Inst {
     bool band;
-    int fmw, nbt, s, r, lpr, pf;
+    int nw, fmw, nbt, s, r, lpr, pf;
     const char *name;
 };
 
 // the candidates, in preference order for a shape
 const Inst kInsts[] = {
-    {false, 2, 4, 1, 7, 16, 4, "img64"},   {false, 2, 8, 1, 7, 16, 4, "img128"},
-    {false, 2, 4, 1, 7, 8, 4, "img64"},    {false, 2, 8, 1, 7, 8, 4, "img128"},
-    {false, 2, 4, 2, 7, 16, 4, "img64"},   {false, 2, 8, 2, 7, 16, 4, "img128"},
-    {false, 2, 4, 2, 7, 8, 4, "img64"},    {false, 2, 8, 2, 7, 8, 4, "img128"},
-    {true, 2, 8, 2, 4, 16, 4, "band4x128"},                                   // 28 -> 14 at stride 2
-    {true, 2, 8, 1, 4, 32, 4, "band4x128"},                                   // 28 x 28
-    {true, 4, 8, 2, 4, 32, 4, "band4x128"},                                   // 56 -> 28
-    {true, 3, 8, 1, 4, 64, 2, "band4x128"},                                   // 56 x 56
-    {true, 8, 4, 2, 4, 64, 2, "band4x64"},                                    // 112 -> 56
-    {true, 4, 4, 1, 4, 64, 2, "band4x64"},                                    // 56 x 56, 64 channels
+    {false, 8, 2, 4, 1, 7, 16, 4, "img64"},   {false, 8, 2, 8, 1, 7, 16, 4, "img128"},
+    {false, 8, 2, 4, 1, 7, 8, 4, "img64"},    {false, 8, 2, 8, 1, 7, 8, 4, "img128"},
+    {false, 8, 2, 4, 2, 7, 16, 4, "img64"},   {false, 8, 2, 8, 2, 7, 16, 4, "img128"},
+    {false, 8, 2, 4, 2, 7, 8, 4, "img64"},    {false, 8, 2, 8, 2, 7, 8, 4, "img128"},
+    // row bands: 8 waves and 4-row bands, or 4 waves and 2-row bands (small
+    // enough in LDS for two workgroups per compute unit)
+    {true, 8, 2, 8, 2, 4, 16, 4, "band4x128"},  {true, 4, 3, 8, 2, 2, 16, 4, "band2x128w4"},  // 28 -> 14
+    {true, 8, 2, 8, 1, 4, 32, 4, "band4x128"},  {true, 4, 3, 8, 1, 4, 32, 4, "band4x128w4"},  // 28 x 28
+    {true, 8, 4, 8, 2, 4, 32, 4, "band4x128"},  {true, 4, 5, 8, 2, 2, 32, 2, "band2x128w4"},  // 56 -> 28
+    {true, 8, 3, 8, 1, 4, 64, 2, "band4x128"},  {true, 4, 4, 8, 1, 2, 64, 2, "band2x128w4"},  // 56 x 56
+    {true, 8, 8, 4, 2, 4, 64, 2, "band4x64"},   {true, 4, 9, 4, 2, 2, 64, 1, "band2x64w4"},   // 112 -> 56
+    {true, 8, 4, 4, 1, 4, 64, 2, "band4x64"},   {true, 4, 4, 4, 1, 2, 64, 2, "band2x64w4"},   // 56 x 56, 64 channels
 };
 constexpr int kNumInsts = sizeof(kInsts) / sizeof(kInsts[0]);
 
@@ -308,10 +312,10 @@ size_t tail_bytes(int nbt) {   // taps and biases behind the main region
     return (64 * ((nsl * 9 + 63) / 64) + 64 * ((nch / 4 + 63) / 64)) * 16;
 }
 
-size_t lds_bytes(const Inst &in, int ksp) {
+size_t lds_bytes(const Inst &in, int ksp, int pstride) {
     const size_t nk = (size_t)ksp / 4, nchunks = (nk + in.pf - 1) / in.pf;
     const size_t slab = nchunks * in.nbt * in.pf * 64 * 16;                // weights, all of K
-    const size_t otile = (size_t)2 * in.nbt * 16 * kPwDwNW * in.fmw * 16;  // pointwise output tile
+    const size_t otile = (size_t)2 * in.nbt * pstride * 16;                // pointwise output tile
     return (slab > otile ? slab : otile) + tail_bytes(in.nbt);
 }
 
@@ -322,48 +326,53 @@ bool fits(const Inst &in, int N, int H, int W, int OH, int OW, int S, int pt, in
     // every input column a lane needs from a neighbour is held by a lane of the
     // same row, or is padding (the neighbour past the row's end holds zeros)
     if (S == 1 ? (pl != 1 || W >= in.lpr) : ((pl != 0 && pl != 1) || W > 2 * in.lpr - 1)) return false;
-    if (lds_bytes(in, ksp) > (size_t)kPwDwLds) return false;
-    const int pmax = 16 * kPwDwNW * in.fmw;
+    const int pmax = 16 * in.nw * in.fmw;
     if (!in.band) {
         if (H * W > pmax) return false;
         g->ipt = pmax / (H * W);
         g->nbands = 0;
         g->groups = (N + g->ipt - 1) / g->ipt;
+        g->pstride = g->ipt * H * W;
     } else {
         // a band's input rows: (R - 1) * S + 3 at most
-        if (((in.r - 1) * S + 3) * W > pmax) return false;
+        const int rows = std::min((in.r - 1) * S + 3, H);
+        if (rows * W > pmax) return false;
         g->ipt = 1;
         g->nbands = (OH + in.r - 1) / in.r;
         g->groups = N * g->nbands;
+        g->pstride = rows * W;
     }
     g->nbt = in.nbt;
-    g->lds = lds_bytes(in, ksp);
-    return true;
+    g->lds = lds_bytes(in, ksp, g->pstride);
+    return g->lds <= (size_t)kPwDwLds;
 }
 
-template <typename E, int FMW, int NBT, int S_, int R, int LPR, int PF>
+template <typename E, int NW, int FMW, int NBT, int S_, int R, int LPR, int PF>
 hipError_t launch_t(const PwDwParams &p, size_t lds, hipStream_t st) {
-    auto kern = pwdw_kernel<E, FMW, NBT, S_, R, LPR, PF>;
+    auto kern = pwdw_kernel<E, NW, FMW, NBT, S_, R, LPR, PF>;
     static const hipError_t attr =
         hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, kPwDwLds);
     if (attr != hipSuccess) return attr;
     const int groups = p.nbands ? p.N * p.nbands : (p.N + p.ipt - 1) / p.ipt;
-    launch(kern, dim3(groups * p.ntiles), dim3(kPwDwNW * 64), (unsigned)lds, st, p);
+    launch(kern, dim3(groups * p.ntiles), dim3(NW * 64), (unsigned)lds, st, p);
     return hipGetLastError();
 }
 
 template <typename E>
 hipError_t launch_inst(int k, const PwDwParams &p, size_t lds, hipStream_t st) {
     switch (k) {
-#define MGI_PWDW(K_, FMW_, NBT_, S_, R_, LPR_, PF_) \
-    case K_: return launch_t<E, FMW_, NBT_, S_, R_, LPR_, PF_>(p, lds, st);
-        MGI_PWDW(0, 2, 4, 1, 7, 16, 4) MGI_PWDW(1, 2, 8, 1, 7, 16, 4)
-        MGI_PWDW(2, 2, 4, 1, 7, 8, 4) MGI_PWDW(3, 2, 8, 1, 7, 8, 4)
-        MGI_PWDW(4, 2, 4, 2, 7, 16, 4) MGI_PWDW(5, 2, 8, 2, 7, 16, 4)
-        MGI_PWDW(6, 2, 4, 2, 7, 8, 4) MGI_PWDW(7, 2, 8, 2, 7, 8, 4)
-        MGI_PWDW(8, 2, 8, 2, 4, 16, 4) MGI_PWDW(9, 2, 8, 1, 4, 32, 4)
-        MGI_PWDW(10, 4, 8, 2, 4, 32, 4) MGI_PWDW(11, 3, 8, 1, 4, 64, 2)
-        MGI_PWDW(12, 8, 4, 2, 4, 64, 2) MGI_PWDW(13, 4, 4, 1, 4, 64, 2)
+#define MGI_PWDW(K_, NW_, FMW_, NBT_, S_, R_, LPR_, PF_) \
+    case K_: return launch_t<E, NW_, FMW_, NBT_, S_, R_, LPR_, PF_>(p, lds, st);
+        MGI_PWDW(0, 8, 2, 4, 1, 7, 16, 4) MGI_PWDW(1, 8, 2, 8, 1, 7, 16, 4)
+        MGI_PWDW(2, 8, 2, 4, 1, 7, 8, 4) MGI_PWDW(3, 8, 2, 8, 1, 7, 8, 4)
+        MGI_PWDW(4, 8, 2, 4, 2, 7, 16, 4) MGI_PWDW(5, 8, 2, 8, 2, 7, 16, 4)
+        MGI_PWDW(6, 8, 2, 4, 2, 7, 8, 4) MGI_PWDW(7, 8, 2, 8, 2, 7, 8, 4)
+        MGI_PWDW(8, 8, 2, 8, 2, 4, 16, 4) MGI_PWDW(9, 4, 3, 8, 2, 2, 16, 4)
+        MGI_PWDW(10, 8, 2, 8, 1, 4, 32, 4) MGI_PWDW(11, 4, 3, 8, 1, 4, 32, 4)
+        MGI_PWDW(12, 8, 4, 8, 2, 4, 32, 4) MGI_PWDW(13, 4, 5, 8, 2, 2, 32, 2)
+        MGI_PWDW(14, 8, 3, 8, 1, 4, 64, 2) MGI_PWDW(15, 4, 4, 8, 1, 2, 64, 2)
+        MGI_PWDW(16, 8, 8, 4, 2, 4, 64, 2) MGI_PWDW(17, 4, 9, 4, 2, 2, 64, 1)
+        MGI_PWDW(18, 8, 4, 4, 1, 4, 64, 2) MGI_PWDW(19, 4, 4, 4, 1, 2, 64, 2)
 #undef MGI_PWDW
     }
     return hipErrorInvalidValue;
@@ -405,6 +414,7 @@ hipError_t launch_pwdw(const PwDwParams &p, int cfg, hipStream_t st) {
     PwDwParams q = p;
     q.ipt = g.ipt;
     q.nbands = g.nbands;
+    q.pstride = g.pstride;
     q.ntiles = (p.nb16 + g.nbt - 1) / g.nbt;
     if (p.N <= 0) return hipSuccess;
     return p.bf16 ? launch_inst<BF16>(idx[cfg], q, g.lds, st) : launch_inst<F16>(idx[cfg], q, g.lds, st);

@@ -241,7 +241,7 @@ def test_node_configuration_candidates():
         elif n["kind"] == "dw_conv":
             assert k == 3 and name.startswith("rows")
         elif n["kind"] == "pw_dw":
-            assert 2 <= k <= 4 and name.startswith(("img", "band", "split"))
+            assert 2 <= k <= 6 and name.startswith(("img", "band", "split"))
         else:
             assert k == 1
     i = next(j for j, n in enumerate(nodes) if n["kind"] == "pw_gemm")
