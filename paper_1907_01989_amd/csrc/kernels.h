@@ -139,7 +139,7 @@ struct PwDwGeom {
 };
 // Number of fused-kernel configurations that cover a shape (0: none); for
 // 0 <= cfg < that number, its geometry and name.
-int pwdw_configs(int N, int H, int W, int OH, int OW, int S, int pt, int pl, int ksp, int cfg,
+int pwdw_configs(int N, int H, int W, int OH, int OW, int S, int pt, int pl, int ksp, int nb16, int cfg,
                  PwDwGeom *g, const char **name);
 hipError_t launch_pwdw(const PwDwParams &p, int cfg, hipStream_t st);
 

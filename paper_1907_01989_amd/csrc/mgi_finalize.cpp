@@ -142,11 +142,11 @@ void add_configs(Node &nd, size_t M) {
         // the split form first when the fused kernel would not fill the GPU
         const Shape &s = nd.dw_in;
         const int nf = kern::pwdw_configs(s.n, s.h, s.w, nd.dw_out.h, nd.dw_out.w, nd.dw_conv.stride_h,
-                                          nd.dw_conv.pad_t, nd.dw_conv.pad_l, nd.ksp, -1, nullptr, nullptr);
+                                          nd.dw_conv.pad_t, nd.dw_conv.pad_l, nd.ksp, nd.nb16, -1, nullptr, nullptr);
         for (int c = 0; c < nf; ++c) {
             const char *name = "";
             kern::pwdw_configs(s.n, s.h, s.w, nd.dw_out.h, nd.dw_out.w, nd.dw_conv.stride_h, nd.dw_conv.pad_t,
-                               nd.dw_conv.pad_l, nd.ksp, c, nullptr, &name);
+                               nd.dw_conv.pad_l, nd.ksp, nd.nb16, c, nullptr, &name);
             Node::Config fc{GemmTile{}, 0, name, false, c};
             nd.cfgs.push_back(fc);
         }
@@ -250,7 +250,7 @@ void fuse_pw_into_dw(mgi_plan &p, bool always) {
         if (pw.kind != NodeKind::Gemm || pw.taps || pw.residual >= 0 || pw.in.size() != 1) continue;
         const Shape in = p.bufs[mid].shape, out = p.bufs[dw.out].shape;
         kern::PwDwGeom geo{};
-        if (kern::pwdw_configs(in.n, in.h, in.w, out.h, out.w, c.stride_h, c.pad_t, c.pad_l, pw.ksp, 0, &geo,
+        if (kern::pwdw_configs(in.n, in.h, in.w, out.h, out.w, c.stride_h, c.pad_t, c.pad_l, pw.ksp, pw.nb16, 0, &geo,
                                nullptr) == 0)
             continue;
         pw.fused_default = always || (size_t)geo.groups * ((pw.nb16 + geo.nbt - 1) / geo.nbt) >= 128;

@@ -13,7 +13,8 @@
 // are computed by both neighbouring bands), so the depthwise step over its
 // channels needs nothing from other workgroups:
 //   1. the weights (NBT channel blocks x all of K), the depthwise taps and
-//      biases are copied into LDS by direct global->LDS loads;
+//      biases are copied into LDS by direct global->LDS loads (taps past the
+//      input read a zero element kept in LDS);
 //   2. each of the NW waves owns FMW fragments of 16 pixels and all NBT
 //      channel blocks;
 //      its activation fragments stream from the sliced layout into registers
@@ -37,15 +38,15 @@ namespace mgi {
 namespace kern {
 
 // whole-wave lane shift of a 16-byte value: kWaveShr1 gives lane l the value
-// of lane l-1 (lane 0 gets zero), kWaveShl1 that of lane l+1 (lane 63 gets zero)
+// of lane l-1, kWaveShl1 that of lane l+1; the lane with no source gets zero
+// (DPP bound control)
 constexpr int kWaveShl1 = 0x130, kWaveShr1 = 0x138;
 template <int CTRL>
 __device__ __forceinline__ h8 wave_shift(h8 v) {
     const u4x u = as_u4(v);
     u4x r;
 #pragma unroll
-    for (int d = 0; d < 4; ++d)
-        r[d] = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)u[d], CTRL, 0xf, 0xf, false);
+    for (int d = 0; d < 4; ++d) r[d] = (uint32_t)__builtin_amdgcn_mov_dpp((int)u[d], CTRL, 0xf, 0xf, true);
     return __builtin_bit_cast(h8, r);
 }
 
@@ -97,6 +98,7 @@ __global__ __launch_bounds__(NW * 64, 2) void pwdw_kernel(PwDwParams p) {   // >
     const int main_h8 = max(nchunks * SQ * 64, NSL * PMAX);
     const h8 *taps = lds + main_h8;                               // [NSL][9]
     const float *dwb = (const float *)(lds + main_h8 + kTapH8);  // [NCH]
+    h8 *zslot = lds + main_h8 + kTapH8 + 64 * kBiasQ;             // one zero element
 
     // 1. weights -> LDS in K order, chunk c = K-steps [c*CK, c*CK + CK) of the
     // NBT channel blocks, layout [chunk][NBT][CK][64]; wave load q of a chunk
@@ -144,6 +146,7 @@ __global__ __launch_bounds__(NW * 64, 2) void pwdw_kernel(PwDwParams p) {   // >
 #pragma unroll
     for (int u = 0; u < PF; ++u)
         if (u < nk) xload(u, xq[u]);
+    if (tid == 0) *zslot = zero_h8();
     wait_vm_lds<0>();                 // this wave's share of the weights has landed
     __builtin_amdgcn_s_barrier();     // ... and every other wave's
 
@@ -200,6 +203,9 @@ __global__ __launch_bounds__(NW * 64, 2) void pwdw_kernel(PwDwParams p) {   // >
     // depthwise kernel
     constexpr int NR = (R - 1) * S_ + 3;          // input rows of a strip
     constexpr int NC = S_;                        // input columns loaded per lane
+    // stride 2: lane ox loads columns 2*ox - pl and 2*ox - pl + 1; its third
+    // tap column is its right neighbour's first
+    const int cx0 = S_ == 2 ? -p.pl : 0;
     const int nsl = 2 * nbv;
     const int nstrips = p.nbands ? 1 : (p.OH + R - 1) / R;
     const int ngroups = nimg * nsl * nstrips;
@@ -222,8 +228,8 @@ __global__ __launch_bounds__(NW * 64, 2) void pwdw_kernel(PwDwParams p) {   // >
         bool cv[NC];
 #pragma unroll
         for (int k = 0; k < NC; ++k) {
-            cx[k] = ox * S_ + k;
-            cv[k] = gv && cx[k] < p.W;
+            cx[k] = ox * S_ + cx0 + k;
+            cv[k] = gv && cx[k] >= 0 && cx[k] < p.W;
         }
         float acc2[R][8];
 #pragma unroll
@@ -236,20 +242,16 @@ __global__ __launch_bounds__(NW * 64, 2) void pwdw_kernel(PwDwParams p) {   // >
             const bool rv = iy >= ir0 && iy < ir1;
             h8 v[NC];
 #pragma unroll
-            for (int k = 0; k < NC; ++k) v[k] = (rv && cv[k]) ? plane[(iy - ir0) * p.W + cx[k]] : zero_h8();
+            for (int k = 0; k < NC; ++k) v[k] = *((rv && cv[k]) ? plane + (iy - ir0) * p.W + cx[k] : zslot);
             h8 t3[3];
             if (S_ == 1) {          // columns ox-1, ox, ox+1 (left padding 1)
                 t3[0] = wave_shift<kWaveShr1>(v[0]);
                 t3[1] = v[0];
                 t3[2] = wave_shift<kWaveShl1>(v[0]);
-            } else if (p.pl == 0) { // columns 2ox, 2ox+1, 2ox+2
+            } else {                // columns 2ox-pl, 2ox-pl+1, 2ox-pl+2
                 t3[0] = v[0];
                 t3[1] = v[NC - 1];
                 t3[2] = wave_shift<kWaveShl1>(v[0]);
-            } else {                // columns 2ox-1, 2ox, 2ox+1
-                t3[0] = wave_shift<kWaveShr1>(v[NC - 1]);
-                t3[1] = v[0];
-                t3[2] = v[NC - 1];
             }
 #pragma unroll
             for (int ky = 0; ky < 3; ++ky) {
@@ -307,9 +309,9 @@ constexpr int kNumInsts = sizeof(kInsts) / sizeof(kInsts[0]);
 
 int lanes_for(int OW) { return OW < 8 ? 8 : OW < 16 ? 16 : OW < 32 ? 32 : OW < 64 ? 64 : 0; }
 
-size_t tail_bytes(int nbt) {   // taps and biases behind the main region
+size_t tail_bytes(int nbt) {   // taps, biases and a zero element behind the main region
     const size_t nsl = 2 * (size_t)nbt, nch = 16 * (size_t)nbt;
-    return (64 * ((nsl * 9 + 63) / 64) + 64 * ((nch / 4 + 63) / 64)) * 16;
+    return (64 * ((nsl * 9 + 63) / 64) + 64 * ((nch / 4 + 63) / 64) + 1) * 16;
 }
 
 size_t lds_bytes(const Inst &in, int ksp, int pstride) {
@@ -393,8 +395,9 @@ int applicable(int N, int H, int W, int OH, int OW, int S, int pt, int pl, int k
 }
 }  // namespace
 
-int pwdw_configs(int N, int H, int W, int OH, int OW, int S, int pt, int pl, int ksp, int cfg,
+int pwdw_configs(int N, int H, int W, int OH, int OW, int S, int pt, int pl, int ksp, int nb16, int cfg,
                  PwDwGeom *g, const char **name) {
+    (void)nb16;
     int idx[kNumInsts];
     PwDwGeom geo[kNumInsts];
     const int n = applicable(N, H, W, OH, OW, S, pt, pl, ksp, idx, geo);
