@@ -194,10 +194,11 @@ def kernel_sources_hash():
     return h.hexdigest()[:16]
 
 
-def measured_traffic(kernel, layer):
-    """HBM bytes per launch of (kernel, layer) from the committed rocprofv3
-    FETCH_SIZE / WRITE_SIZE summary, scaled by the copy calibration there;
-    None when absent or measured on other kernel sources."""
+def measured_traffic(kernel, layer, config):
+    """HBM bytes per launch of (node kind, layer, configuration) from the
+    committed rocprofv3 FETCH_SIZE / WRITE_SIZE summary, scaled by the copy
+    calibration there; None when absent, measured on other kernel sources or
+    on another configuration of the layer."""
     path = os.path.join(ROOT, "profiles", "mobilenet_v1_224_b64_traffic.md")
     if not os.path.exists(path):
         return None
@@ -205,9 +206,9 @@ def measured_traffic(kernel, layer):
     with open(path) as f:
         for line in f:
             if line.startswith("traffic_bytes_per_launch:"):
-                _, k, l, nbytes, _, h = line.split()
-                if k == kernel and l == layer and h == cur:
-                    return int(nbytes)
+                f = line.split()
+                if len(f) == 7 and f[1:4] == [kernel, layer, config] and f[6] == cur:
+                    return int(f[4])
     return None
 
 
@@ -304,11 +305,11 @@ def run_workload(key, steps, warmup, hip, profile_steps=20, detail=True, tune=Tr
         layers.append(entry)
     fl, by, bound = node_work(desc, nodes, shapes, dom)
     roof = roofline_entry(fl, by, bound, dom_ms * 1e-3)
-    roof.update({"kernel": nodes[dom]["kind"],
-                 "layer": desc["ops"][nodes[dom]["tensor"]]["name"],
+    dom_layer = desc["ops"][nodes[dom]["tensor"]]["name"]
+    roof.update({"kernel": nodes[dom]["kind"], "layer": dom_layer, "config": configs[dom],
                  "algorithmic_bytes": int(by), "algorithmic_flops": int(fl),
                  "avg_launch_us": round(dom_ms * 1e3, 3),
-                 "traffic": measured_traffic(nodes[dom]["kind"], desc["ops"][nodes[dom]["tensor"]]["name"])})
+                 "traffic": measured_traffic(nodes[dom]["kind"], dom_layer, configs[dom])})
     total_s = t1 - t0
     res = {"desc": desc, "batch": batch, "net": net, "ms_per_step": total_s / steps * 1e3,
            "images_per_s": batch * steps / total_s, "roofline": roof, "layers": layers,
@@ -316,6 +317,44 @@ def run_workload(key, steps, warmup, hip, profile_steps=20, detail=True, tune=Tr
            "step_ms_device": {k: round(v, 5) for k, v in step_ms.items()}}
     plan.close()
     return res
+
+
+def config_sweep(key, reps):
+    """Every candidate kernel configuration of every node, one node at a time
+    (the others on their finalize-time choice), each run `reps` whole-plan
+    times; prints the run order as JSON.  The HBM traffic counters are taken
+    over this sequence so that every (layer, configuration) pair the
+    autotuner may pick has its own figure."""
+    import torch
+    import workloads
+    from paper_1907_01989_amd import _binding as B
+    from paper_1907_01989_amd import engine
+
+    net, batch = WORKLOADS[key]
+    desc = workloads.WORKLOADS[net](batch)
+    plan = engine.Plan(desc)
+    xs = plan.input_tensors()
+    outs = plan.alloc_outputs()
+    sh = torch.cuda.current_stream().cuda_stream
+    ins = [x.data_ptr() for x in xs]
+    ops_ptrs = [o.data_ptr() for o in outs]
+    nodes = plan.nodes()
+    runs = []
+    for i in range(len(nodes)):
+        c0, n, _ = plan.node_configs()[i]
+        for c in range(n):
+            B.mgi_plan_set_node_config(plan.handle, i, c)
+            for _ in range(reps):
+                B.mgi_plan_run(plan.handle, ins, ops_ptrs, sh)
+            runs.append({"node": i, "configs": [name for _, _, name in plan.node_configs()]})
+        B.mgi_plan_set_node_config(plan.handle, i, c0)
+    torch.cuda.synchronize()
+    layers = [{"node": i, "kind": nd["kind"],
+               "name": desc["ops"][nd["tensor"]]["name"] if nd["tensor"] >= 0 else nd["kind"]}
+              for i, nd in enumerate(nodes)]
+    print(json.dumps({"config_sweep": runs, "reps": reps, "layers": layers,
+                      "kernel_sources": kernel_sources_hash()}), flush=True)
+    plan.close()
 
 
 def run_graph_replay(key, steps, warmup, hip, tune=True):
@@ -393,6 +432,10 @@ def main():
     ap.add_argument("--copy-only", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB, 20 times (the "
                          "reference kernel for scaling HBM traffic counters)")
+    ap.add_argument("--config-sweep", type=int, default=0, metavar="REPS",
+                    help="only run every candidate configuration of every node of the workload "
+                         "REPS times, one node at a time (the sequence the HBM traffic counters "
+                         "are collected over), and print the order as JSON")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this engine runs on one GPU; --gpus {args.gpus} is not supported "
@@ -413,6 +456,9 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes": n, "launches": 20}), flush=True)
+        return
+    if args.config_sweep:
+        config_sweep(args.workload, args.config_sweep)
         return
     hip = Hip()
     eprint(f"[bench] workload {args.workload}: warmup {args.warmup}, steps {args.steps}")
