@@ -150,12 +150,10 @@ __global__ __launch_bounds__(NW * 64, 2) void pwdw_kernel(PwDwParams p) {   // >
     wait_vm_lds<0>();                 // this wave's share of the weights has landed
     __builtin_amdgcn_s_barrier();     // ... and every other wave's
 
+    // (the first K-step takes a zero accumulator as an operand instead of
+    // zeroing the accumulators: same sums, no initialisation instructions)
     f4 acc[NBT][FMW];
-#pragma unroll
-    for (int i = 0; i < NBT; ++i)
-#pragma unroll
-        for (int j = 0; j < FMW; ++j) acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
-    auto step = [&](int kk, const h8 *b) {
+    auto step = [&](int kk, const h8 *b, bool first) {
         const h8 *buf = lds + (kk / CK) * SQ * 64 + (kk % CK) * 64 + lane;
         h8 a[NBT];
 #pragma unroll
@@ -164,22 +162,30 @@ __global__ __launch_bounds__(NW * 64, 2) void pwdw_kernel(PwDwParams p) {   // >
         for (int j = 0; j < FMW; ++j)
             if (fj[j]) {
 #pragma unroll
-                for (int i = 0; i < NBT; ++i) acc[i][j] = E::mma(a[i], b[j], acc[i][j]);
+                for (int i = 0; i < NBT; ++i)
+                    acc[i][j] = E::mma(a[i], b[j], first ? f4{0.0f, 0.0f, 0.0f, 0.0f} : acc[i][j]);
             }
     };
+    step(0, xq[0], true);
+    xload(min(PF, nk - 1), xq[0]);
     for (int c = 0; c < nchunks; ++c) {
 #pragma unroll
         for (int u = 0; u < CK; ++u) {
             const int kk = c * CK + u;
-            if (kk < nk) {
-                step(kk, xq[u]);
+            if (kk > 0 && kk < nk) {
+                step(kk, xq[u], false);
                 xload(min(kk + PF, nk - 1), xq[u]);
             }
         }
     }
 
     // 3. pointwise epilogue into LDS: tile [NSL][PMAX] of sliced elements
+    // (lanes past the tile's last pixel computed that pixel again: they store
+    // the same value to its place, so no store is under a lane mask)
     __syncthreads();
+    int pxc[FMW];
+#pragma unroll
+    for (int j = 0; j < FMW; ++j) pxc[j] = min((wave + j * NW) * 16 + (lane & 15), P - 1);
 #pragma unroll
     for (int i = 0; i < NBT; ++i) {
         if (i >= nbv) break;
@@ -187,14 +193,14 @@ __global__ __launch_bounds__(NW * 64, 2) void pwdw_kernel(PwDwParams p) {   // >
         float bv[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) bv[r] = p.bias[nb0 * 16 + c + r];
+        _Float16 *row = (_Float16 *)(lds + (c >> 3) * PMAX) + (c & 7);
 #pragma unroll
         for (int j = 0; j < FMW; ++j) {
-            const int px = (wave + j * NW) * 16 + (lane & 15);
-            if (!fj[j] || px >= P) continue;
+            if (!fj[j]) continue;
             float v[4];
 #pragma unroll
             for (int r = 0; r < 4; ++r) v[r] = act_apply(acc[i][j][r] + bv[r], p.act1);
-            *(h4 *)((_Float16 *)(lds + (c >> 3) * PMAX + px) + (c & 7)) = E::pack4(v);
+            *(h4 *)(row + pxc[j] * 8) = E::pack4(v);
         }
     }
     __syncthreads();
