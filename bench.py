@@ -244,7 +244,7 @@ def run_workload(key, steps, warmup, hip, profile_steps=20, detail=True, tune=Tr
     if tune:
         # plan-time tuning of kernel configurations (mgi_plan_autotune), as an
         # application would do once after loading the model
-        plan.autotune(xs, outs, reps=5, stream=sh)
+        plan.autotune(xs, outs, reps=10, stream=sh)
     configs = [name for _, _, name in plan.node_configs()]
     for _ in range(warmup):
         B.mgi_plan_run(plan.handle, ins, ops_ptrs, sh)
@@ -370,7 +370,7 @@ def run_graph_replay(key, steps, warmup, hip, tune=True):
     xs = plan.input_tensors()
     sh = torch.cuda.current_stream().cuda_stream
     if tune:
-        plan.autotune(xs, reps=5, stream=sh)
+        plan.autotune(xs, reps=10, stream=sh)
     plan.capture(xs)
     for _ in range(warmup):
         plan.replay(sh)

@@ -273,10 +273,11 @@ mgi_status mgi_plan_read_node(mgi_plan *p, int i, void *dev_dst, void *stream);
  * arguments and checks as mgi_plan_run), then, node by node in run order,
  * times every candidate kernel configuration of each node that has several
  * (pointwise / implicit-GEMM, depthwise, fused pointwise -> depthwise) inside
- * `reps` whole runs of the plan (plus one warm-up; only the node's kernels
- * are timestamped, so it meets its input as in a run) and keeps the fastest.
- * All candidates produce bit-identical results.  Synchronises `stream`; releases a captured graph (capture again
- * afterwards).  The output buffers hold no defined result afterwards: run the
+ * `reps` whole runs of the plan, queued back to back (plus one warm-up run;
+ * only the node's kernels are timestamped, so it meets its input as in a
+ * run), and keeps the one with the lowest median time.  All candidates
+ * produce bit-identical results.  Synchronises `stream` once per candidate;
+ * releases a captured graph (capture again afterwards).  The output buffers hold no defined result afterwards: run the
  * plan again.  Errors: MGI_ERR_INVALID_ARG for reps outside 1..1000; run
  * errors; MGI_ERR_HIP if timing fails. */
 mgi_status mgi_plan_autotune(mgi_plan *p, const void *const *dev_inputs, void *const *dev_outputs,

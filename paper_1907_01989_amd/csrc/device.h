@@ -148,13 +148,23 @@ __device__ __forceinline__ void wait_vm_lds() {
 // pixel (half of a 16-byte sliced element, the other half in lane l+16);
 // storing that directly makes every quarter-wave write half-masked 64-byte
 // pieces, which costs several times the bandwidth of whole lines.  Instead
-// each wave parks act1(acc + bias) in its own LDS tile
+// each wave parks act1(acc) (the accumulators include the bias) in its own LDS tile
 // [2*FN slices][16*FM pixels][8] fp32, then re-reads it so that consecutive
 // lanes own consecutive pixels of one slice: residual reads and output writes
 // are whole 16-byte elements, 1 KiB per wave instruction.  No barrier: a wave
 // reads back only what it wrote.
 // ---------------------------------------------------------------------------
 // mlim: pixels at or past it are not stored (default: p.M).
+// Bias of the four channels a lane holds in a 16x16 accumulator tile of
+// output block nb (blocks past the last are clamped: never stored).  Every
+// pointwise GEMM kernel starts its accumulators from this value, so the bias
+// enters the sum first, in the same place in every kernel.
+__device__ __forceinline__ f4 bias_frag(const float *bias, int nb, int nb16, int lane) {
+    const float *b = bias + min(nb, nb16 - 1) * 16 + 4 * (lane >> 4);
+    return f4{b[0], b[1], b[2], b[3]};
+}
+
+// accumulators (bias included) -> act1 -> (+ residual -> act2) -> sliced store
 template <typename E, int FM, int FN>
 __device__ __forceinline__ void store_tile_c8(const GemmParams &p, const f4 (&acc)[FN][FM], int m0,
                                               int nb0, float *stage, int lane, int mlim = -1) {
@@ -162,16 +172,12 @@ __device__ __forceinline__ void store_tile_c8(const GemmParams &p, const f4 (&ac
     const int lim = mlim < 0 ? p.M : mlim;
 #pragma unroll
     for (int i = 0; i < FN; ++i) {
-        const int nbase = (nb0 + i) * 16 + 4 * (lane >> 4);
-        float bv[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) bv[r] = p.bias[min(nbase, p.nb16 * 16 - 4) + r];
         const int sl = 2 * i + ((lane >> 4) >> 1), half = 4 * ((lane >> 4) & 1);
 #pragma unroll
         for (int j = 0; j < FM; ++j) {
             f4 v;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) v[r] = act_apply(acc[i][j][r] + bv[r], p.act1);
+            for (int r = 0; r < 4; ++r) v[r] = act_apply(acc[i][j][r], p.act1);
             *(f4 *)(stage + ((sl * NPIX) + j * 16 + (lane & 15)) * 8 + half) = v;
         }
     }

@@ -86,9 +86,11 @@ __global__ __launch_bounds__(256) void dwpw_kernel(DwPwParams p, DwPwTile t) {
 
     f4 acc[FN][FMW];
 #pragma unroll
-    for (int i = 0; i < FN; ++i)
+    for (int i = 0; i < FN; ++i) {
+        const f4 b0 = bias_frag(g.bias, i, g.nb16, lane);
 #pragma unroll
-        for (int j = 0; j < FMW; ++j) acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+        for (int j = 0; j < FMW; ++j) acc[i][j] = b0;
+    }
 
     gload(0);
     for (int kc = 0; kc < nk; ++kc) {

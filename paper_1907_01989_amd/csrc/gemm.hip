@@ -12,8 +12,10 @@
 //     pixel l%16 and channel slice l/16, i.e. exactly one 16-byte sliced
 //     element, so fragments are read straight from the sliced layout;
 //   - the accumulator gives lane l four consecutive output channels
-//     4*(l/16)+r of pixel l%16, half a sliced element: the epilogue adds bias,
-//     applies the activation(s) and the residual and writes 8 bytes per lane.
+//     4*(l/16)+r of pixel l%16, half a sliced element; it starts from the
+//     bias (in every pointwise kernel, so all of them round alike), and the
+//     epilogue applies the activation(s) and the residual and writes 8 bytes
+//     per lane.
 // Weight and activation tiles for four K slices (32 channels) per step are
 // staged through LDS, double-buffered with one barrier per step, the next
 // step's global loads issued before the current step's MFMAs.
@@ -108,9 +110,11 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmParams p) {
 
     f4 acc[FN][FM];
 #pragma unroll
-    for (int i = 0; i < FN; ++i)
+    for (int i = 0; i < FN; ++i) {
+        const f4 b0 = bias_frag(p.bias, nb0 + wn * FN + i, p.nb16, lane);
 #pragma unroll
-        for (int j = 0; j < FM; ++j) acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+        for (int j = 0; j < FM; ++j) acc[i][j] = b0;
+    }
 
     gload(0);
     lstore(0);
@@ -139,16 +143,13 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmParams p) {
         const int nb = nb0 + wn * FN + i;
         if (nb >= p.nb16) continue;
         const int nbase = nb * 16 + 4 * (lane >> 4);
-        float bv[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) bv[r] = p.bias[nbase + r];
 #pragma unroll
         for (int j = 0; j < FM; ++j) {
             const int m = m0 + wm * WM + j * 16 + (lane & 15);
             if (m >= p.M) continue;
             float v[4];
 #pragma unroll
-            for (int r = 0; r < 4; ++r) v[r] = act_apply(acc[i][j][r] + bv[r], p.act1);
+            for (int r = 0; r < 4; ++r) v[r] = act_apply(acc[i][j][r], p.act1);
             if (F32OUT) {
                 float *y = (float *)p.y + (size_t)m * p.cout;
 #pragma unroll
@@ -248,6 +249,16 @@ __global__ __launch_bounds__(256) void gemm_xs_kernel(GemmParams p) {
     for (int u = 0; u < PF; ++u)
         if (u < ksteps) xload(u, xq[u]);
 
+    // accumulators start from the bias (loaded before the weight slab, whose
+    // barrier then covers it)
+    f4 acc[FN][FM];
+#pragma unroll
+    for (int i = 0; i < FN; ++i) {
+        const f4 b0 = bias_frag(p.bias, nb0 + i, p.nb16, lane);
+#pragma unroll
+        for (int j = 0; j < FM; ++j) acc[i][j] = b0;
+    }
+
     // weight slab: FN blocks x ksp slices x 16 rows (blocks past the end are
     // clamped; their accumulators are never stored)
     const int slab = FN * p.ksp * 16;
@@ -258,12 +269,6 @@ __global__ __launch_bounds__(256) void gemm_xs_kernel(GemmParams p) {
         wsm[e] = p.w[(size_t)nb * p.ksp * 16 + r];
     }
     __syncthreads();
-
-    f4 acc[FN][FM];
-#pragma unroll
-    for (int i = 0; i < FN; ++i)
-#pragma unroll
-        for (int j = 0; j < FM; ++j) acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
 
     auto step = [&](int kk, const h8 *b) {
         h8 a[FN];
@@ -394,9 +399,11 @@ __global__ __launch_bounds__(256) void gemm_pipe_kernel(GemmParams p) {
 
     f4 acc[FN][FM];
 #pragma unroll
-    for (int i = 0; i < FN; ++i)
+    for (int i = 0; i < FN; ++i) {
+        const f4 b0 = bias_frag(p.bias, nb0 + wn * FN + i, p.nb16, lane);
 #pragma unroll
-        for (int j = 0; j < FM; ++j) acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+        for (int j = 0; j < FM; ++j) acc[i][j] = b0;
+    }
 
     pipe_issue<BM, BN>(p, 0, st0, m0, nb0, wave, lane);
     if (nk > 1) pipe_issue<BM, BN>(p, 1, st1, m0, nb0, wave, lane);

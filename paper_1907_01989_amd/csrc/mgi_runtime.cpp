@@ -416,16 +416,23 @@ extern "C" mgi_status mgi_plan_autotune(mgi_plan *p, const void *const *dev_inpu
     if (s != MGI_OK) return s;
     release_graph(*p);
     hipStream_t st = static_cast<hipStream_t>(stream);
-    hipEvent_t e0 = nullptr, e1 = nullptr;
-    hipError_t e = hipEventCreate(&e0);
-    if (e == hipSuccess) e = hipEventCreate(&e1);
+    // one start/stop pair per run, so that a candidate's runs go back to
+    // back (as in steady operation) and are read after one synchronisation
+    std::vector<hipEvent_t> evs(2 * (size_t)(reps + 1), nullptr);
+    hipError_t e = hipSuccess;
+    for (size_t k = 0; k < evs.size() && e == hipSuccess; ++k) e = hipEventCreate(&evs[k]);
+    auto destroy = [&]() {
+        for (hipEvent_t x : evs)
+            if (x) hipEventDestroy(x);
+    };
     if (e != hipSuccess) {
-        if (e0) hipEventDestroy(e0);
+        destroy();
         return hip_fail(e, "mgi_plan_autotune: events");
     }
     Bases B{static_cast<char *>(p->dev_ws), dev_inputs, dev_outputs};
     LaunchEvents &ev = launch_events();
     mgi_status result = MGI_OK;
+    std::vector<float> times;
     for (size_t ni = 0; ni < p->nodes.size() && result == MGI_OK; ++ni) {
         Node &nd = p->nodes[ni];
         if (nd.cfgs.size() < 2) continue;
@@ -433,47 +440,52 @@ extern "C" mgi_status mgi_plan_autotune(mgi_plan *p, const void *const *dev_inpu
         float best_ms = 3.0e38f;
         for (size_t c = 0; c < nd.cfgs.size() && result == MGI_OK; ++c) {
             nd.apply((int)c);
-            float tmin = 3.0e38f;
             bool usable = true;
-            for (int r = 0; r <= reps; ++r) {
+            for (int r = 0; r <= reps && usable && result == MGI_OK; ++r) {
                 // the whole plan runs, so that the node meets its input as it
                 // does in a run (just written by its producer), and only the
                 // node's kernels are timestamped
-                for (size_t j = 0; j < p->nodes.size() && e == hipSuccess; ++j) {
-                    ev.start = j == ni ? e0 : nullptr;
-                    ev.stop = j == ni ? e1 : nullptr;
+                for (size_t j = 0; j < p->nodes.size(); ++j) {
+                    ev.start = j == ni ? evs[2 * r] : nullptr;
+                    ev.stop = j == ni ? evs[2 * r + 1] : nullptr;
                     e = launch_node(*p, p->nodes[j], B, st);
                     ev.start = ev.stop = nullptr;
-                    if (e != hipSuccess && j != ni) {
-                        result = hip_fail(e, "mgi_plan_autotune: run");
-                        break;
-                    }
-                }
-                if (result != MGI_OK) break;
-                if (e != hipSuccess) {
+                    if (e == hipSuccess) continue;
+                    if (j != ni) result = hip_fail(e, "mgi_plan_autotune: run");
+                    else usable = false;   // configuration not launchable for this shape
                     e = hipSuccess;
-                    usable = false;   // configuration not launchable for this shape
                     break;
                 }
-                float ms = 0.0f;
-                e = hipEventSynchronize(e1);
-                if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
-                if (e != hipSuccess) {
-                    result = hip_fail(e, "mgi_plan_autotune: timing");
-                    break;
-                }
-                if (r > 0) tmin = std::min(tmin, ms);
             }
-            if (usable && tmin < best_ms) {
-                best_ms = tmin;
+            if (result != MGI_OK) break;
+            // drain what was queued (also after an unusable configuration)
+            e = hipStreamSynchronize(st);
+            if (e != hipSuccess) {
+                result = hip_fail(e, "mgi_plan_autotune: run");
+                break;
+            }
+            if (!usable) continue;
+            times.clear();
+            for (int r = 1; r <= reps && e == hipSuccess; ++r) {
+                float ms = 0.0f;
+                e = hipEventElapsedTime(&ms, evs[2 * r], evs[2 * r + 1]);
+                times.push_back(ms);
+            }
+            if (e != hipSuccess) {
+                result = hip_fail(e, "mgi_plan_autotune: timing");
+                break;
+            }
+            // median of the runs after the first (which meets cold caches)
+            std::sort(times.begin(), times.end());
+            const float med = times[times.size() / 2];
+            if (med < best_ms) {
+                best_ms = med;
                 best = (int)c;
             }
         }
         nd.apply(best);
-        if (result != MGI_OK) break;
     }
-    hipEventDestroy(e0);
-    hipEventDestroy(e1);
+    destroy();
     return result;
 }
 

@@ -98,14 +98,15 @@ __global__ __launch_bounds__(NW * 64, 2) void pwdw_kernel(PwDwParams p) {   // >
     const int main_h8 = max(nchunks * SQ * 64, NSL * PMAX);
     const h8 *taps = lds + main_h8;                               // [NSL][9]
     const float *dwb = (const float *)(lds + main_h8 + kTapH8);  // [NCH]
-    h8 *zslot = lds + main_h8 + kTapH8 + 64 * kBiasQ;             // one zero element
+    const f4 *pwb = (const f4 *)(lds + main_h8 + kTapH8 + 64 * kBiasQ);   // pointwise bias [NCH]
+    h8 *zslot = lds + main_h8 + kTapH8 + 128 * kBiasQ;            // one zero element
 
     // 1. weights -> LDS in K order, chunk c = K-steps [c*CK, c*CK + CK) of the
     // NBT channel blocks, layout [chunk][NBT][CK][64]; wave load q of a chunk
     // is channel block q / CK, K-step q % CK (steps past K read the last one,
     // blocks past the tile's last read the last valid one: their results are
-    // never stored); then the taps and depthwise biases (sources clamped to
-    // their last element; the copies past the end land in padding)
+    // never stored); then the taps, depthwise and pointwise biases (sources
+    // clamped to their last element; the copies past the end land in padding)
     {
         for (int c = 0; c < nchunks; ++c) {
             for (int q = wave; q < SQ; q += NW) {
@@ -114,12 +115,19 @@ __global__ __launch_bounds__(NW * 64, 2) void pwdw_kernel(PwDwParams p) {   // >
             }
         }
         const h8 *tsrc = p.dw_w + (size_t)nb0 * 2 * 9;
-        const h8 *bsrc = (const h8 *)(p.dw_b + nb0 * 16);
+        const h8 *bsrc = (const h8 *)(p.dw_b + nb0 * 16), *psrc = (const h8 *)(p.bias + nb0 * 16);
         const int tn = nbv * 2 * 9, bn = nbv * 4;
-        for (int q = wave; q < kTapQ + kBiasQ; q += NW) {
-            const int e = (q < kTapQ ? q : q - kTapQ) * 64 + lane;
-            if (q < kTapQ) load_lds16(tsrc + min(e, tn - 1), lds + main_h8 + e);
-            else load_lds16(bsrc + min(e, bn - 1), lds + main_h8 + kTapH8 + e);
+        for (int q = wave; q < kTapQ + 2 * kBiasQ; q += NW) {
+            if (q < kTapQ) {
+                const int e = q * 64 + lane;
+                load_lds16(tsrc + min(e, tn - 1), lds + main_h8 + e);
+            } else if (q < kTapQ + kBiasQ) {
+                const int e = (q - kTapQ) * 64 + lane;
+                load_lds16(bsrc + min(e, bn - 1), lds + main_h8 + kTapH8 + e);
+            } else {
+                const int e = (q - kTapQ - kBiasQ) * 64 + lane;
+                load_lds16(psrc + min(e, bn - 1), lds + main_h8 + kTapH8 + 64 * kBiasQ + e);
+            }
         }
     }
 
@@ -150,20 +158,30 @@ __global__ __launch_bounds__(NW * 64, 2) void pwdw_kernel(PwDwParams p) {   // >
     wait_vm_lds<0>();                 // this wave's share of the weights has landed
     __builtin_amdgcn_s_barrier();     // ... and every other wave's
 
-    // (the first K-step takes a zero accumulator as an operand instead of
-    // zeroing the accumulators: same sums, no initialisation instructions)
+    // (accumulators start from the bias, as in every pointwise GEMM kernel;
+    // the first K-step takes it from LDS as an operand, one channel block at
+    // a time, so nothing is initialised and few registers hold it)
     f4 acc[NBT][FMW];
     auto step = [&](int kk, const h8 *b, bool first) {
         const h8 *buf = lds + (kk / CK) * SQ * 64 + (kk % CK) * 64 + lane;
         h8 a[NBT];
 #pragma unroll
         for (int i = 0; i < NBT; ++i) a[i] = buf[i * CK * 64];
+        if (first) {
+#pragma unroll
+            for (int i = 0; i < NBT; ++i) {
+                const f4 c0 = pwb[i * 4 + (lane >> 4)];
+#pragma unroll
+                for (int j = 0; j < FMW; ++j)
+                    if (fj[j]) acc[i][j] = E::mma(a[i], b[j], c0);
+            }
+            return;
+        }
 #pragma unroll
         for (int j = 0; j < FMW; ++j)
             if (fj[j]) {
 #pragma unroll
-                for (int i = 0; i < NBT; ++i)
-                    acc[i][j] = E::mma(a[i], b[j], first ? f4{0.0f, 0.0f, 0.0f, 0.0f} : acc[i][j]);
+                for (int i = 0; i < NBT; ++i) acc[i][j] = E::mma(a[i], b[j], acc[i][j]);
             }
     };
     step(0, xq[0], true);
@@ -190,16 +208,13 @@ __global__ __launch_bounds__(NW * 64, 2) void pwdw_kernel(PwDwParams p) {   // >
     for (int i = 0; i < NBT; ++i) {
         if (i >= nbv) break;
         const int c = i * 16 + 4 * (lane >> 4);       // channel within the tile
-        float bv[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) bv[r] = p.bias[nb0 * 16 + c + r];
         _Float16 *row = (_Float16 *)(lds + (c >> 3) * PMAX) + (c & 7);
 #pragma unroll
         for (int j = 0; j < FMW; ++j) {
             if (!fj[j]) continue;
             float v[4];
 #pragma unroll
-            for (int r = 0; r < 4; ++r) v[r] = act_apply(acc[i][j][r] + bv[r], p.act1);
+            for (int r = 0; r < 4; ++r) v[r] = act_apply(acc[i][j][r], p.act1);
             *(h4 *)(row + pxc[j] * 8) = E::pack4(v);
         }
     }
@@ -315,9 +330,9 @@ constexpr int kNumInsts = sizeof(kInsts) / sizeof(kInsts[0]);
 
 int lanes_for(int OW) { return OW < 8 ? 8 : OW < 16 ? 16 : OW < 32 ? 32 : OW < 64 ? 64 : 0; }
 
-size_t tail_bytes(int nbt) {   // taps, biases and a zero element behind the main region
+size_t tail_bytes(int nbt) {   // taps, two biases and a zero element behind the main region
     const size_t nsl = 2 * (size_t)nbt, nch = 16 * (size_t)nbt;
-    return (64 * ((nsl * 9 + 63) / 64) + 64 * ((nch / 4 + 63) / 64) + 1) * 16;
+    return (64 * ((nsl * 9 + 63) / 64) + 128 * ((nch / 4 + 63) / 64) + 1) * 16;
 }
 
 size_t lds_bytes(const Inst &in, int ksp, int pstride) {
