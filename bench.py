@@ -162,6 +162,19 @@ def node_work(desc, nodes, shapes, i):
         flops = 2.0 * n * h_ * w_ * cin * cmid + 2.0 * elems(t) * op["kh"] * op["kw"]
         byts = (elems(pop["in"]) * 2 + out_b + pop["w"].size * 2 + pop["b"].size * 4 +
                 op["w"].size * 2 + op["b"].size * 4)
+    elif kind == "stem_dw":
+        # graph input in, depthwise output out; the stem output never
+        # reaches memory
+        sop = ops[head_of(op["in"])]
+        x = sop["in"]
+        cin = shapes[x][3]
+        sn, sh_, sw_ = shapes[x][0], (shapes[t][1]), (shapes[t][2])   # stride-1 depthwise: same plane
+        cmid = sop["cout"]
+        flops = (2.0 * sn * sh_ * sw_ * sop["kh"] * sop["kw"] * cin * cmid +
+                 2.0 * elems(t) * op["kh"] * op["kw"])
+        in_bytes = elems(x) * (4 if ops[x].get("dtype", 2) == 2 else 2)
+        byts = (in_bytes + out_b + sop["w"].size * 2 + sop["b"].size * 4 +
+                op["w"].size * 2 + op["b"].size * 4)
     elif kind == "dw_conv":
         flops = 2.0 * elems(t) * op["kh"] * op["kw"]
         byts = elems(op["in"]) * 2 + out_b + op["w"].size * 4 + op["b"].size * 4
@@ -188,7 +201,7 @@ def kernel_sources_hash():
     while the kernels it was measured on are unchanged."""
     import hashlib
     h = hashlib.sha1()
-    for f in ("gemm.hip", "ops.hip", "dwpw.hip", "pwdw.hip", "device.h", "kernels.h"):
+    for f in ("gemm.hip", "ops.hip", "dwpw.hip", "pwdw.hip", "stemdw.hip", "device.h", "kernels.h"):
         with open(os.path.join(ROOT, "paper_1907_01989_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -224,7 +237,7 @@ def roofline_entry(flops, byts, bound, seconds):
 
 # ---------------------------------------------------------------------------
 def run_workload(key, steps, warmup, hip, profile_steps=20, detail=True, tune=True, fuse_dwpw=False,
-                 fuse_pwdw=True):
+                 fuse_pwdw=True, fuse_stemdw=True):
     import torch
     import workloads
     from paper_1907_01989_amd import _binding as B
@@ -232,7 +245,7 @@ def run_workload(key, steps, warmup, hip, profile_steps=20, detail=True, tune=Tr
 
     net, batch = WORKLOADS[key]
     desc = workloads.WORKLOADS[net](batch)
-    plan = engine.Plan(desc, fuse_dwpw=fuse_dwpw, fuse_pwdw=fuse_pwdw)
+    plan = engine.Plan(desc, fuse_dwpw=fuse_dwpw, fuse_pwdw=fuse_pwdw, fuse_stemdw=fuse_stemdw)
     xs = plan.input_tensors()
     outs = plan.alloc_outputs()
     stream = torch.cuda.current_stream()
@@ -427,6 +440,9 @@ def main():
     ap.add_argument("--no-fuse-pwdw", action="store_true",
                     help="keep pointwise convolutions and the 3x3 depthwise convolutions "
                          "that read them as separate kernels (mgi_options.fuse_pwdw = 0)")
+    ap.add_argument("--no-fuse-stemdw", action="store_true",
+                    help="keep the stem and the depthwise convolution that reads it as separate "
+                         "kernels (mgi_options.fuse_stemdw = 0)")
     ap.add_argument("--no-autotune", action="store_true",
                     help="keep the finalize-time kernel configurations")
     ap.add_argument("--copy-only", type=int, default=0, metavar="MIB",
@@ -464,7 +480,8 @@ def main():
     eprint(f"[bench] workload {args.workload}: warmup {args.warmup}, steps {args.steps}")
     tune = not args.no_autotune
     main_res = run_workload(args.workload, args.steps, args.warmup, hip, tune=tune,
-                            fuse_dwpw=args.fuse_dwpw, fuse_pwdw=not args.no_fuse_pwdw)
+                            fuse_dwpw=args.fuse_dwpw, fuse_pwdw=not args.no_fuse_pwdw,
+                            fuse_stemdw=not args.no_fuse_stemdw)
     eprint(f"[bench] {main_res['images_per_s']:.1f} images/s, {main_res['ms_per_step']:.4f} ms/step")
     also = {}
     if not args.no_extra:
@@ -505,7 +522,7 @@ def main():
                    "input": "NHWC fp16 uniform[0,1], device-resident",
                    "weights": "He-normal seed 0, fp16", "planner": "greedy", "fused": True,
                    "autotuned": tune, "dw_pw_fused": args.fuse_dwpw,
-                   "pw_dw_fused": not args.no_fuse_pwdw},
+                   "pw_dw_fused": not args.no_fuse_pwdw, "stem_dw_fused": not args.no_fuse_stemdw},
         "roofline": main_res["roofline"],
         "cpu_baseline": cpu,
         "per_layer": main_res["layers"],

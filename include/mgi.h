@@ -107,14 +107,19 @@ typedef struct {
                             pixels to fill the GPU; the depthwise output then never reaches
                             memory (default 0; needs fuse = 1) */
     int fuse_pwdw;       /* run a 3x3 depthwise convolution (stride 1 or 2, no dilation, top
-                            and left padding of at most one) inside the pointwise convolution
-                            that produces its input, when that output feeds nothing else,
-                            planes are at most 16 x 16 and the channel count is a multiple of
-                            64; the pointwise output then never reaches memory (Sec. 3.2's
-                            fusion extended to the pointwise -> depthwise pair).  0: never;
-                            1 (default): when the fused kernel gets at least 128 workgroups
-                            (images per tile x channel tiles; below that the separate kernels
-                            are faster); 2: whenever the shapes allow.  Needs fuse = 1. */
+                            and left padding of at most one, planes up to 112 wide) inside
+                            the pointwise convolution that produces its input, when that
+                            output feeds nothing else; the pointwise output then never
+                            reaches memory (Sec. 3.2's fusion extended to the pointwise ->
+                            depthwise pair).  0: never; 1 (default): the fused kernel is the
+                            default configuration when it gets at least 128 workgroups (tiles
+                            x channel tiles; below that the separate kernels are), the other
+                            one an autotune candidate; 2: the fused kernel is the default
+                            whenever the shapes allow.  Needs fuse = 1. */
+    int fuse_stemdw;     /* the same for the stem (a convolution over the graph input with
+                            kh*kw*c <= 32 and at most 64 output channels) and a 3x3 depthwise
+                            convolution at stride 1 that alone reads its output: 0, 1
+                            (default) or 2 as for fuse_pwdw.  Needs fuse = 1. */
 } mgi_options;
 
 /* ---------------------------------------------------------------------------

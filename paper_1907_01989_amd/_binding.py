@@ -34,7 +34,8 @@ class Options(ctypes.Structure):
     _fields_ = [("planner", ctypes.c_int), ("fuse", ctypes.c_int),
                 ("materialize_all", ctypes.c_int), ("dtype", ctypes.c_int),
                 ("fuse_dwpw", ctypes.c_int),
-                ("fuse_pwdw", ctypes.c_int)]
+                ("fuse_pwdw", ctypes.c_int),
+                ("fuse_stemdw", ctypes.c_int)]
 
 
 _lib = None

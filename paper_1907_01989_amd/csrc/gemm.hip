@@ -604,13 +604,12 @@ __global__ __launch_bounds__(256) void stem_kernel(StemParams p, int th, int rs,
         koff[t] = off;
     }
     h8 a[NB];
+    f4 c0[NB];                                   // accumulators start from the bias
 #pragma unroll
-    for (int i = 0; i < NB; ++i) a[i] = p.w[(size_t)i * 64 + lane];
-    float bv[NB][4];
-#pragma unroll
-    for (int i = 0; i < NB; ++i)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) bv[i][r] = p.bias[i * 16 + 4 * (lane >> 4) + r];
+    for (int i = 0; i < NB; ++i) {
+        a[i] = p.w[(size_t)i * 64 + lane];
+        c0[i] = bias_frag(p.bias, i, p.nb16, lane);
+    }
     __syncthreads();
 
     const int fpr = (p.OW + 15) >> 4;            // 16-pixel fragments per output row
@@ -625,14 +624,14 @@ __global__ __launch_bounds__(256) void stem_kernel(StemParams p, int th, int rs,
         const int m = (n * p.OH + oy0 + oyl) * p.OW + ox;
 #pragma unroll
         for (int i = 0; i < NB; ++i) {
-            const f4 acc = E::mma(a[i], b, f4{0.f, 0.f, 0.f, 0.f});
+            const f4 acc = E::mma(a[i], b, c0[i]);
             const int nbase = i * 16 + 4 * (lane >> 4);
             const int os = nbase >> 3, hoff = nbase & 7;
             if (ox >= p.OW || os >= p.ns) continue;
             const size_t off = ((size_t)os * p.M + m) * 8 + hoff;
             float v[4];
 #pragma unroll
-            for (int r = 0; r < 4; ++r) v[r] = act_apply(acc[r] + bv[i][r], p.act1);
+            for (int r = 0; r < 4; ++r) v[r] = act_apply(acc[r], p.act1);
             if (p.res) {
                 const h4 rv = *(const h4 *)((const _Float16 *)p.res + off);
 #pragma unroll

@@ -102,6 +102,31 @@ hipError_t launch_stem(const StemParams &p, bool fp16_in, hipStream_t st);
 size_t stem_band_bytes(int th, int kh, int kw, int c, int w, int ow, int sh, int sw, int dh, int dw,
                        int pl);
 
+// Stem convolution fused with the depthwise 3x3 convolution (stride 1,
+// dilation 1) that reads its output: a workgroup owns R output rows of one
+// image and computes the stem rows they read into LDS.
+struct StemDwParams {
+    const void *x;       // NHWC graph input, fp32 or fp16
+    const h8 *w;         // stem weights [nb16][4][16][8], k = (ky*kw + kx)*c + ci
+    const float *bias;   // [nb16 * 16]
+    int N, H, W, C, SH, SW;          // input size and stem output size
+    int KH, KW, K, sh, sw, dh, dw, pt, pl, nb16, act1;
+    const h8 *dw_w;      // depthwise taps [2 * nb16][9][8]
+    const float *dw_b;   // [16 * nb16]
+    h8 *y;               // depthwise output, sliced [ns][N * OH * OW]
+    int OH, OW, S, dpt, dpl, ns, act2;
+    int nbands, rs, pstride, band_h8; // set by launch_stemdw from the configuration
+    int bf16;            // storage type: 0 fp16, 1 bf16
+};
+struct StemDwGeom {
+    int rows, nbands, rs, pstride, band_h8;
+    size_t lds;
+};
+// Number of fused configurations (band heights) that fit a shape (0: none);
+// for 0 <= cfg < that number, its geometry and name.
+int stemdw_configs(const StemDwParams &p, int cfg, StemDwGeom *g, const char **name);
+hipError_t launch_stemdw(const StemDwParams &p, int cfg, bool fp16_in, hipStream_t st);
+
 struct DwParams {
     const h8 *x;
     const h8 *w;         // fp16 taps [S][kh*kw][8]

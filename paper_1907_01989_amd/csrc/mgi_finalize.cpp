@@ -27,6 +27,20 @@
 
 namespace mgi {
 
+void stemdw_shape(const mgi_plan &p, const Node &nd, kern::StemDwParams &q) {
+    const Shape x = p.bufs[nd.in[0]].shape;
+    const mgi_conv_desc &c = nd.conv, &d = nd.dw_conv;
+    q.N = x.n; q.H = x.h; q.W = x.w; q.C = x.c;
+    q.SH = nd.dw_in.h; q.SW = nd.dw_in.w;
+    q.KH = c.kh; q.KW = c.kw; q.K = c.kh * c.kw * x.c;
+    q.sh = c.stride_h; q.sw = c.stride_w; q.dh = c.dil_h; q.dw = c.dil_w;
+    q.pt = c.pad_t; q.pl = c.pad_l;
+    q.nb16 = nd.nb16; q.act1 = nd.act1;
+    q.OH = nd.dw_out.h; q.OW = nd.dw_out.w; q.S = d.stride_h;
+    q.dpt = d.pad_t; q.dpl = d.pad_l;
+    q.ns = (nd.dw_out.c + 7) / 8; q.act2 = nd.dw_act;
+}
+
 namespace {
 
 inline int slices(int c) { return (c + 7) / 8; }
@@ -92,7 +106,7 @@ std::string tile_name(const GemmTile &t) {
 
 void pick_pipe_tile(GemmTile &t, size_t M, int npad);
 
-void add_configs(Node &nd, size_t M) {
+void add_configs(const mgi_plan &p, Node &nd, size_t M) {
     auto push = [&](const GemmTile &t) {
         for (const Node::Config &c : nd.cfgs)
             if (c.tile.pipe == t.pipe && c.tile.slab == t.slab && c.tile.bm == t.bm &&
@@ -153,6 +167,21 @@ void add_configs(Node &nd, size_t M) {
         GemmTile t;
         pick_pipe_tile(t, nd.dw_in.pixels(), nd.nb16 * 16);
         const Node::Config split{t, nd.dw_conv.stride_h == 1 ? 4 : 2, "split_" + tile_name(t), true, 0};
+        nd.cfgs.insert(nd.fused_default ? nd.cfgs.end() : nd.cfgs.begin(), Node::Config(split));
+        nd.apply(0);
+    } else if (nd.kind == NodeKind::StemDw) {
+        // band heights of the fused stem + depthwise kernel, and the two
+        // separate kernels through the scratch tensor (first when the fused
+        // kernel would not fill the GPU)
+        kern::StemDwParams q{};
+        stemdw_shape(p, nd, q);
+        const int nf = kern::stemdw_configs(q, -1, nullptr, nullptr);
+        for (int c = 0; c < nf; ++c) {
+            const char *name = "";
+            kern::stemdw_configs(q, c, nullptr, &name);
+            nd.cfgs.push_back(Node::Config{GemmTile{}, 0, name, false, c});
+        }
+        const Node::Config split{GemmTile{}, 4, "split", true, 0};
         nd.cfgs.insert(nd.fused_default ? nd.cfgs.end() : nd.cfgs.begin(), Node::Config(split));
         nd.apply(0);
     } else if (nd.kind == NodeKind::DwPw) {
@@ -274,6 +303,55 @@ void fuse_pw_into_dw(mgi_plan &p, bool always) {
     p.nodes.swap(kept);
 }
 
+// The stem and a 3x3 depthwise convolution at stride 1 that alone reads its
+// output become one node (kernel in stemdw.hip), the same pattern as above
+// for the network's first layer pair; the stem output stays a planned scratch
+// tensor for the split configuration.
+void fuse_stem_into_dw(mgi_plan &p, bool always) {
+    std::vector<int> readers(p.bufs.size(), 0), producer(p.bufs.size(), -1);
+    for (size_t i = 0; i < p.nodes.size(); ++i) {
+        const Node &nd = p.nodes[i];
+        for (int b : nd.in) readers[b]++;
+        if (nd.residual >= 0) readers[nd.residual]++;
+        producer[nd.out] = (int)i;
+    }
+    std::vector<char> drop(p.nodes.size(), 0);
+    for (size_t i = 0; i < p.nodes.size(); ++i) {
+        const Node &dw = p.nodes[i];
+        const mgi_conv_desc &c = dw.conv;
+        if (dw.kind != NodeKind::Depthwise || dw.in.size() != 1 || c.kh != 3 || c.kw != 3 ||
+            c.stride_h != 1 || c.stride_w != 1 || c.dil_h != 1 || c.dil_w != 1)
+            continue;
+        const int mid = dw.in[0];
+        if (readers[mid] != 1 || p.bufs[mid].loc != Loc::Arena || producer[mid] < 0) continue;
+        Node &sn = p.nodes[producer[mid]];
+        if (sn.kind != NodeKind::Stem || sn.residual >= 0 || sn.in.size() != 1) continue;
+        Node t = sn;
+        t.kind = NodeKind::StemDw;
+        t.dw_conv = dw.conv;
+        t.dw_act = dw.act1;
+        t.dw_in = p.bufs[mid].shape;
+        t.dw_out = p.bufs[dw.out].shape;
+        kern::StemDwParams q{};
+        stemdw_shape(p, t, q);
+        kern::StemDwGeom geo{};
+        if (kern::stemdw_configs(q, 0, &geo, nullptr) == 0) continue;
+        t.fused_default = always || (size_t)q.N * geo.nbands >= 128;
+        t.kname = "stem_dw";
+        t.dw_op = dw.op;
+        t.out = dw.out;
+        t.out_tensor = dw.out_tensor;
+        t.n_fused += dw.n_fused;
+        t.scratch = mid;
+        sn = std::move(t);
+        drop[i] = 1;
+    }
+    std::vector<Node> kept;
+    for (size_t i = 0; i < p.nodes.size(); ++i)
+        if (!drop[i]) kept.push_back(std::move(p.nodes[i]));
+    p.nodes.swap(kept);
+}
+
 void pick_pipe_tile(GemmTile &t, size_t M, int npad) {
     const int cand[3][2] = {{128, 128}, {128, 64}, {64, 64}};
     size_t best_tiles = 0;
@@ -363,6 +441,7 @@ std::vector<char> live_ops(const mgi_graph &g) {
     return live;
 }
 
+
 mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p);
 
 }  // namespace
@@ -386,6 +465,8 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
         return fail(MGI_ERR_UNSUPPORTED, "mgi_graph_finalize: storage is fp16 or bf16");
     if (o.fuse_pwdw < 0 || o.fuse_pwdw > 2)
         return fail(MGI_ERR_INVALID_ARG, "mgi_graph_finalize: fuse_pwdw is 0, 1 or 2");
+    if (o.fuse_stemdw < 0 || o.fuse_stemdw > 2)
+        return fail(MGI_ERR_INVALID_ARG, "mgi_graph_finalize: fuse_stemdw is 0, 1 or 2");
     auto to_bits = o.dtype == MGI_DTYPE_BF16 ? f32_to_bf16_bits : f32_to_f16_bits;
 
     const std::vector<char> live = live_ops(g);
@@ -782,8 +863,9 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
     }
 
     if (o.fuse && o.fuse_pwdw) fuse_pw_into_dw(p, o.fuse_pwdw == 2);
+    if (o.fuse && o.fuse_stemdw) fuse_stem_into_dw(p, o.fuse_stemdw == 2);
     if (o.fuse && o.fuse_dwpw) fuse_dw_into_pw(p);
-    for (Node &nd : p.nodes) add_configs(nd, p.bufs[nd.out].shape.pixels());
+    for (Node &nd : p.nodes) add_configs(p, nd, p.bufs[nd.out].shape.pixels());
 
     // ------------------------------------------------------------ lifetimes
     for (size_t i = 0; i < p.nodes.size(); ++i) {
@@ -854,7 +936,7 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
             float *bp = reinterpret_cast<float *>(blob.data() + nd.dw_b_off);
             for (int ch = 0; ch < c; ++ch) bp[ch] = dop.b[ch];
         }
-        if (nd.kind == NodeKind::PwDw) {
+        if (nd.kind == NodeKind::PwDw || nd.kind == NodeKind::StemDw) {
             // depthwise taps of the absorbed op laid out as for a depthwise
             // node, [S][9][8], biases fp32; channels past c are zero
             const GOp &dop = g.ops[nd.dw_op];
@@ -869,7 +951,7 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
             for (int ch = 0; ch < c; ++ch) bp[ch] = dop.b[ch];
         }
         if (nd.kind == NodeKind::Gemm || nd.kind == NodeKind::Stem || nd.kind == NodeKind::FC ||
-            nd.kind == NodeKind::DwPw || nd.kind == NodeKind::PwDw) {
+            nd.kind == NodeKind::DwPw || nd.kind == NodeKind::PwDw || nd.kind == NodeKind::StemDw) {
             const Shape x = g.ops[op.in[0]].out;
             const int cin = x.c;
             const int cout = nd.kind == NodeKind::FC ? op.cout : op.conv.cout;
@@ -885,7 +967,7 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
                     for (int kx = 0; kx < kw; ++kx)
                         for (int ci = 0; ci < cin; ++ci) {
                             int ks, j;
-                            if (nd.kind == NodeKind::Stem) {
+                            if (nd.kind == NodeKind::Stem || nd.kind == NodeKind::StemDw) {
                                 int k = (ky * kw + kx) * cin + ci;
                                 ks = k / 8;
                                 j = k % 8;

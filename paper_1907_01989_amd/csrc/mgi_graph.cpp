@@ -328,4 +328,5 @@ extern "C" void mgi_options_default(mgi_options *o) {
     o->dtype = MGI_DTYPE_FP16;
     o->fuse_dwpw = 0;
     o->fuse_pwdw = 1;
+    o->fuse_stemdw = 1;
 }

@@ -74,7 +74,7 @@ struct Buf {
 
 enum class NodeKind {
     Ingest, Stem, Gemm, Depthwise, Add, Act, Gap, FC, Softmax, Concat, Resize, Argmax,
-    ResizeArgmax, Export, Pad, DwPw, PwDw
+    ResizeArgmax, Export, Pad, DwPw, PwDw, StemDw
 };
 
 // Tile shape of the MFMA GEMM (pointwise, implicit-GEMM convolution, FC).
@@ -117,16 +117,17 @@ struct Node {
     mgi_conv_desc dw_conv{};
     int dw_act = MGI_ACT_NONE;
     size_t dw_w_off = 0, dw_b_off = 0;
-    Shape dw_in, dw_out;    // PwDw: shapes of the depthwise input (the pointwise output) and output
+    Shape dw_in, dw_out;    // PwDw / StemDw: shapes of the depthwise input (the first op's output) and output
     // kernel configurations the autotuner may choose from (index 0 = the
     // finalize-time choice); `cfg` is the one in use
-    // PwDw: the pointwise output kept as a planned scratch tensor, so that the
-    // node can also run as the two separate kernels (split); whether the
-    // fused kernel is the default configuration
+    // PwDw / StemDw: the first op's output kept as a planned scratch tensor,
+    // so that the node can also run as the two separate kernels (split);
+    // whether the fused kernel is the default configuration
     int scratch = -1;
     bool split = false;
     bool fused_default = true;
-    int pwdw_cfg = 0;       // PwDw: configuration of the fused kernel (pwdw_configs)
+    int pwdw_cfg = 0;       // PwDw / StemDw: configuration of the fused kernel (pwdw_configs,
+                            // stemdw_configs)
     struct Config {
         GemmTile tile;
         int dw_rows = 0;
@@ -191,5 +192,12 @@ PlanResult plan_mcfp(const std::vector<size_t> &sizes, const std::vector<int> &f
 
 // finalize steps
 mgi_status build_plan(const mgi_graph &g, const mgi_options &o, mgi_plan &p);
+
+namespace kern {
+struct StemDwParams;
+}
+// shape fields of the fused stem -> depthwise kernel's parameters for a
+// StemDw node (pointers and storage type left to the caller)
+void stemdw_shape(const mgi_plan &p, const Node &nd, kern::StemDwParams &q);
 
 }  // namespace mgi

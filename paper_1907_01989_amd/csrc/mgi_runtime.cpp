@@ -43,6 +43,26 @@ void *buf_ptr(const mgi_plan &p, int b, const Bases &B) {
 
 inline int slices(int c) { return (c + 7) / 8; }
 
+// The depthwise half of a split fused node: the 3x3 depthwise kernel from the
+// node's scratch tensor (the first half's output) to its output.
+hipError_t launch_split_dw(const mgi_plan &p, const Node &nd, const void *sp, void *y, bool bf, hipStream_t st) {
+    const Shape mid = nd.dw_in, os = nd.dw_out;
+    DwParams q{};
+    q.bf16 = bf;
+    q.x = (const h8 *)sp;
+    q.w = (const h8 *)(static_cast<const char *>(p.dev_w) + nd.dw_w_off);
+    q.bias = (const float *)(static_cast<const char *>(p.dev_w) + nd.dw_b_off);
+    q.zero = (const h8 *)(static_cast<const char *>(p.dev_w) + p.zero_off);
+    q.y = (h8 *)y;
+    q.N = mid.n; q.H = mid.h; q.W = mid.w; q.S = slices(mid.c);
+    q.OH = os.h; q.OW = os.w; q.KH = q.KW = 3;
+    q.sh = q.sw = nd.dw_conv.stride_h;
+    q.dh = q.dw = 1;
+    q.pt = nd.dw_conv.pad_t; q.pl = nd.dw_conv.pad_l;
+    q.act = nd.dw_act;
+    return launch_depthwise(q, nd.dw_rows, st);
+}
+
 hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStream_t st) {
     const char *wbase = static_cast<const char *>(p.dev_w);
     const Buf &ob = p.bufs[nd.out];
@@ -148,22 +168,7 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
                 hipError_t e = launch_gemm_pipe(g, nd.tile.bm, nd.tile.bn, st);
                 ev.start = nullptr;
                 ev.stop = saved.stop;
-                if (e == hipSuccess) {
-                    DwParams q{};
-                    q.bf16 = bf;
-                    q.x = (const h8 *)sp;
-                    q.w = (const h8 *)(wbase + nd.dw_w_off);
-                    q.bias = (const float *)(wbase + nd.dw_b_off);
-                    q.zero = (const h8 *)(wbase + p.zero_off);
-                    q.y = (h8 *)y;
-                    q.N = mid.n; q.H = mid.h; q.W = mid.w; q.S = slices(mid.c);
-                    q.OH = os.h; q.OW = os.w; q.KH = q.KW = 3;
-                    q.sh = q.sw = nd.dw_conv.stride_h;
-                    q.dh = q.dw = 1;
-                    q.pt = nd.dw_conv.pad_t; q.pl = nd.dw_conv.pad_l;
-                    q.act = nd.dw_act;
-                    e = launch_depthwise(q, nd.dw_rows, st);
-                }
+                if (e == hipSuccess) e = launch_split_dw(p, nd, sp, y, bf, st);
                 ev = saved;
                 return e;
             }
@@ -181,6 +186,50 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
             q.S = nd.dw_conv.stride_h; q.pt = nd.dw_conv.pad_t; q.pl = nd.dw_conv.pad_l;
             q.act2 = nd.dw_act;
             return launch_pwdw(q, nd.pwdw_cfg, st);
+        }
+        case NodeKind::StemDw: {
+            const Buf &ib = p.bufs[nd.in[0]];
+            const bool fp16_in = ib.in_dtype == MGI_DTYPE_FP16;
+            if (nd.split) {
+                // the stem kernel into the scratch tensor, then the depthwise
+                // kernel (timed as one: first kernel's start, second's end)
+                LaunchEvents &ev = launch_events();
+                const LaunchEvents saved = ev;
+                const Shape mid = nd.dw_in;
+                void *sp = buf_ptr(p, nd.scratch, B);
+                StemParams q{};
+                q.bf16 = bf;
+                q.x = buf_ptr(p, nd.in[0], B);
+                q.w = (const h8 *)(wbase + nd.w_off);
+                q.bias = (const float *)(wbase + nd.b_off);
+                q.res = nullptr;
+                q.y = (h8 *)sp;
+                q.N = ib.shape.n; q.H = ib.shape.h; q.W = ib.shape.w; q.C = ib.shape.c;
+                q.OH = mid.h; q.OW = mid.w; q.M = (int)mid.pixels();
+                q.KH = nd.conv.kh; q.KW = nd.conv.kw; q.K = nd.conv.kh * nd.conv.kw * ib.shape.c;
+                q.sh = nd.conv.stride_h; q.sw = nd.conv.stride_w;
+                q.dh = nd.conv.dil_h; q.dw = nd.conv.dil_w;
+                q.pt = nd.conv.pad_t; q.pl = nd.conv.pad_l;
+                q.nb16 = nd.nb16; q.ns = slices(mid.c);
+                q.act1 = nd.act1; q.act2 = MGI_ACT_NONE;
+                ev.stop = nullptr;
+                hipError_t e = launch_stem(q, fp16_in, st);
+                ev.start = nullptr;
+                ev.stop = saved.stop;
+                if (e == hipSuccess) e = launch_split_dw(p, nd, sp, y, bf, st);
+                ev = saved;
+                return e;
+            }
+            StemDwParams q{};
+            stemdw_shape(p, nd, q);
+            q.bf16 = bf;
+            q.x = buf_ptr(p, nd.in[0], B);
+            q.w = (const h8 *)(wbase + nd.w_off);
+            q.bias = (const float *)(wbase + nd.b_off);
+            q.dw_w = (const h8 *)(wbase + nd.dw_w_off);
+            q.dw_b = (const float *)(wbase + nd.dw_b_off);
+            q.y = (h8 *)y;
+            return launch_stemdw(q, nd.pwdw_cfg, fp16_in, st);
         }
         case NodeKind::Depthwise: {
             const Buf &ib = p.bufs[nd.in[0]];

@@ -160,7 +160,10 @@ __global__ __launch_bounds__(NW * 64, 2) void pwdw_kernel(PwDwParams p) {   // >
 
     // (accumulators start from the bias, as in every pointwise GEMM kernel;
     // the first K-step takes it from LDS as an operand, one channel block at
-    // a time, so nothing is initialised and few registers hold it)
+    // a time, so nothing is initialised and few registers hold it).  The
+    // weight fragments are read right before their MFMAs: reading the next
+    // step's ahead costs registers, and past 128 (or 168) registers a compute
+    // unit holds fewer waves, which cost more than the overlap gained.
     f4 acc[NBT][FMW];
     auto step = [&](int kk, const h8 *b, bool first) {
         const h8 *buf = lds + (kk / CK) * SQ * 64 + (kk % CK) * 64 + lane;
@@ -325,6 +328,11 @@ const Inst kInsts[] = {
     {true, 8, 3, 8, 1, 4, 64, 2, "band4x128"},  {true, 4, 4, 8, 1, 2, 64, 2, "band2x128w4"},  // 56 x 56
     {true, 8, 8, 4, 2, 4, 64, 2, "band4x64"},   {true, 4, 9, 4, 2, 2, 64, 1, "band2x64w4"},   // 112 -> 56
     {true, 8, 4, 4, 1, 4, 64, 2, "band4x64"},   {true, 4, 4, 4, 1, 2, 64, 2, "band2x64w4"},   // 56 x 56, 64 channels
+    // 32-channel tiles: half the LDS of the 64-channel ones, so more
+    // workgroups share a compute unit (on the 112 and 56 planes, where K is
+    // small, this pays for reading the activations twice as often; measured
+    // slower on the deeper band layers, as were 16-channel tiles)
+    {true, 4, 9, 2, 2, 2, 64, 1, "band2x32w4"},  {true, 4, 4, 2, 1, 2, 64, 2, "band2x32w4"},   // 112 -> 56, 56 x 56
 };
 constexpr int kNumInsts = sizeof(kInsts) / sizeof(kInsts[0]);
 
@@ -396,6 +404,7 @@ hipError_t launch_inst(int k, const PwDwParams &p, size_t lds, hipStream_t st) {
         MGI_PWDW(14, 8, 3, 8, 1, 4, 64, 2) MGI_PWDW(15, 4, 4, 8, 1, 2, 64, 2)
         MGI_PWDW(16, 8, 8, 4, 2, 4, 64, 2) MGI_PWDW(17, 4, 9, 4, 2, 2, 64, 1)
         MGI_PWDW(18, 8, 4, 4, 1, 4, 64, 2) MGI_PWDW(19, 4, 4, 4, 1, 2, 64, 2)
+        MGI_PWDW(20, 4, 9, 2, 2, 2, 64, 1) MGI_PWDW(21, 4, 4, 2, 1, 2, 64, 2)
 #undef MGI_PWDW
     }
     return hipErrorInvalidValue;

@@ -69,7 +69,7 @@ def build_graph(desc):
 
 
 def options(planner=B.PLANNER_GREEDY, fuse=True, materialize_all=False, fuse_dwpw=False,
-            dtype=B.DTYPE_FP16, fuse_pwdw=True):
+            dtype=B.DTYPE_FP16, fuse_pwdw=True, fuse_stemdw=True):
     o = B.mgi_options_default()
     o.dtype = dtype
     o.planner = planner
@@ -77,6 +77,7 @@ def options(planner=B.PLANNER_GREEDY, fuse=True, materialize_all=False, fuse_dwp
     o.materialize_all = int(materialize_all)
     o.fuse_dwpw = int(fuse_dwpw)
     o.fuse_pwdw = int(fuse_pwdw)     # False/True or 2 (fuse regardless of workgroup count)
+    o.fuse_stemdw = int(fuse_stemdw)  # likewise
     return o
 
 
@@ -84,12 +85,13 @@ class Plan:
     """A finalised, device-bound network."""
 
     def __init__(self, desc, planner=B.PLANNER_GREEDY, fuse=True, materialize_all=False,
-                 device="cuda:0", bind=True, fuse_dwpw=False, dtype=B.DTYPE_FP16, fuse_pwdw=True):
+                 device="cuda:0", bind=True, fuse_dwpw=False, dtype=B.DTYPE_FP16, fuse_pwdw=True,
+                 fuse_stemdw=True):
         self.desc = desc
         g = build_graph(desc)
         try:
             self.handle = B.mgi_graph_finalize(
-                g, options(planner, fuse, materialize_all, fuse_dwpw, dtype, fuse_pwdw))
+                g, options(planner, fuse, materialize_all, fuse_dwpw, dtype, fuse_pwdw, fuse_stemdw))
         finally:
             B.mgi_graph_destroy(g)
         self.device = device

@@ -110,12 +110,12 @@ def test_finalize_state_errors_and_run_before_bind():
 
 
 def test_fusion_structure():
-    v1 = engine.Plan(workloads.mobilenet_v1(1), bind=False, fuse_pwdw=False)
+    v1 = engine.Plan(workloads.mobilenet_v1(1), bind=False, fuse_pwdw=False, fuse_stemdw=False)
     kinds = [n["kind"] for n in v1.nodes()]
     assert kinds[0] == "conv_stem" and kinds.count("dw_conv") == 13 and kinds.count("pw_gemm") == 13
     assert kinds[-3:] == ["global_avgpool", "fc_gemm", "softmax"]
     assert len(kinds) == 30
-    v2 = engine.Plan(workloads.mobilenet_v2(1), bind=False, fuse_pwdw=False)
+    v2 = engine.Plan(workloads.mobilenet_v2(1), bind=False, fuse_pwdw=False, fuse_stemdw=False)
     nodes = v2.nodes()
     assert sum(1 for n in nodes if n["n_fused"] == 2) == 10      # residual adds absorbed
     assert not any(n["kind"] == "add" for n in nodes)
@@ -127,13 +127,16 @@ def test_fusion_structure():
 
 def test_pointwise_depthwise_fusion_structure():
     # v1: pw1..pw12 each feed one depthwise convolution (whole-image tiles on
-    # 14x14 and 7x7 planes, row bands on 112..28); dw1 reads the stem, pw13
-    # feeds the pooling
+    # 14x14 and 7x7 planes, row bands on 112..28); dw1 reads the stem (fused
+    # with it), pw13 feeds the pooling
     v1 = engine.Plan(workloads.mobilenet_v1(64), bind=False)
     nodes = v1.nodes()
     kinds = [n["kind"] for n in nodes]
-    assert kinds.count("pw_dw") == 12 and kinds.count("dw_conv") == 1 and kinds.count("pw_gemm") == 1
-    assert len(kinds) == 18
+    assert kinds.count("pw_dw") == 12 and kinds.count("stem_dw") == 1 and kinds.count("pw_gemm") == 1
+    assert kinds[0] == "stem_dw" and "dw_conv" not in kinds and "conv_stem" not in kinds
+    assert len(kinds) == 17
+    k_nostem = [n["kind"] for n in engine.Plan(workloads.mobilenet_v1(64), bind=False, fuse_stemdw=False).nodes()]
+    assert k_nostem[:2] == ["conv_stem", "dw_conv"] and len(k_nostem) == 18
     for n in nodes:
         if n["kind"] == "pw_dw":
             assert n["n_fused"] == 2
@@ -155,12 +158,39 @@ def test_pointwise_depthwise_fusion_structure():
     b1f = engine.Plan(workloads.mobilenet_v1(1), bind=False, fuse_pwdw=2)
     b1fc = [c for n, c in zip(b1f.nodes(), b1f.node_configs()) if n["kind"] == "pw_dw"]
     assert len(b1fc) == 12 and all(name.startswith(("img", "band")) for _, _, name in b1fc)
-    o = engine.options(fuse_pwdw=3)
-    g = engine.build_graph(workloads.mobilenet_v1(1))
-    try:
-        assert err(B.mgi_graph_finalize, g, o) == 1
-    finally:
-        B.mgi_graph_destroy(g)
+    for o in (engine.options(fuse_pwdw=3), engine.options(fuse_stemdw=3), engine.options(fuse_stemdw=-1)):
+        g = engine.build_graph(workloads.mobilenet_v1(1))
+        try:
+            assert err(B.mgi_graph_finalize, g, o) == 1
+        finally:
+            B.mgi_graph_destroy(g)
+
+
+def test_stem_depthwise_fusion_structure():
+    # the stem node absorbs dw1: at batch 64 the fused kernel (4- or 2-row
+    # bands) is the default and the split pair a candidate; at batch 1 (28
+    # bands) the split pair is the default unless asked for (fuse_stemdw = 2)
+    for net in (workloads.mobilenet_v1, workloads.mobilenet_v2):
+        p = engine.Plan(net(64), bind=False)
+        n0 = p.nodes()[0]
+        assert n0["kind"] == "stem_dw" and n0["n_fused"] == 2 and tuple(n0["shape"]) == (64, 112, 112, 32)
+        cfg, k, name = p.node_configs()[0]
+        assert name == "band4" and k == 3
+        names = []
+        for c in range(k):
+            B.mgi_plan_set_node_config(p.handle, 0, c)
+            names.append(p.node_configs()[0][2])
+        assert names == ["band4", "band2", "split"]
+    assert engine.Plan(workloads.mobilenet_v1(1), bind=False).node_configs()[0][2] == "split"
+    assert engine.Plan(workloads.mobilenet_v1(1), bind=False, fuse_stemdw=2).node_configs()[0][2] == "band4"
+    # a stride-2 depthwise after the stem is not fused
+    g = workloads.NetBuilder(0)
+    x = g.input(2, 64, 64, 3, 0, 1)
+    s = g.conv(x, 32, 3, s=2)
+    y = g.dw(s, 3, s=2)
+    g.mark_output(y)
+    kinds = [n["kind"] for n in engine.Plan(g.graph("s2"), bind=False).nodes()]
+    assert kinds[:2] == ["conv_stem", "dw_conv"] and "stem_dw" not in kinds, kinds
 
 
 def test_standalone_activation_and_add_fusion():
@@ -242,6 +272,8 @@ def test_node_configuration_candidates():
             assert k == 3 and name.startswith("rows")
         elif n["kind"] == "pw_dw":
             assert 2 <= k <= 6 and name.startswith(("img", "band", "split"))
+        elif n["kind"] == "stem_dw":
+            assert k == 3 and name.startswith(("band", "split"))
         else:
             assert k == 1
     i = next(j for j, n in enumerate(nodes) if n["kind"] == "pw_gemm")

@@ -62,12 +62,14 @@ def test_fused_pair_matches_unfused(n, h, w, c, s, N, res):
 @pytest.mark.parametrize("net", ["mobilenet_v1", "mobilenet_v2"])
 def test_fused_network_matches_unfused(net):
     from paper_1907_01989_amd import engine
-    # (with the pointwise -> depthwise fusion off, which would take the pairs)
+    # (with the pointwise -> depthwise and stem -> depthwise fusions off, which
+    # would take the depthwise layers first)
     desc = workloads.WORKLOADS[net](64)
-    kinds = [k["kind"] for k in engine.Plan(desc, bind=False, fuse_dwpw=True, fuse_pwdw=False).nodes()]
+    off = {"fuse_pwdw": False, "fuse_stemdw": False}
+    kinds = [k["kind"] for k in engine.Plan(desc, bind=False, fuse_dwpw=True, **off).nodes()]
     assert kinds.count("dw_pw") >= 5
     log(f"[case] {net} b64 fused vs unfused")
-    _, fused, _ = run_gpu(desc, materialize_all=False, fuse_dwpw=True, fuse_pwdw=False)
-    _, plain, _ = run_gpu(desc, materialize_all=False, fuse_dwpw=False, fuse_pwdw=False)
+    _, fused, _ = run_gpu(desc, materialize_all=False, fuse_dwpw=True, **off)
+    _, plain, _ = run_gpu(desc, materialize_all=False, fuse_dwpw=False, **off)
     for a, b in zip(fused, plain):
         np.testing.assert_array_equal(a, b)
