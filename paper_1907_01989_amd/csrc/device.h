@@ -144,6 +144,91 @@ __device__ __forceinline__ void wait_vm_lds() {
 }
 
 // ---------------------------------------------------------------------------
+// Input band of a convolution over an NHWC graph input: rows [iy0, iy0 +
+// nrows) of image n, row r of the band at band + r * rs (16-bit storage
+// values, the data from column lead on).  The padding cells (rows outside
+// the image, columns before and after the data) are zeroed, then the rows
+// are copied with each thread loading NV units (16-byte vectors, or single
+// elements when rows are not 16-byte aligned) before storing any, so that a
+// workgroup's loads are in flight together.  A thread's place in a row is
+// found with one division; rows shorter than the workgroup are copied
+// several per pass.  The caller synchronises before reading the band.
+// ---------------------------------------------------------------------------
+template <typename E, typename TIN, int NT, int NV>
+__device__ __forceinline__ void stage_input_band(_Float16 *band, const TIN *x, int n, int H, int W, int C,
+                                                 int iy0, int nrows, int rs, int lead, int tid) {
+    constexpr int VEC = 16 / sizeof(TIN);
+    typedef TIN tv __attribute__((ext_vector_type(VEC)));
+    const int rowlen = W * C;
+    const int r_lo = max(0, -iy0), r_hi = min(nrows, H - iy0);   // band rows inside the image
+    const TIN *src0 = x + ((size_t)n * H + iy0) * rowlen;
+    const bool vec = (rowlen % 8) == 0 && (lead % 8) == 0 && (rs % 8) == 0;
+    const int upr = vec ? rowlen / VEC : rowlen;                  // load units per row
+    uint16_t *b16 = (uint16_t *)band;
+    const int tail = rs - lead - rowlen;                         // zero columns after the data
+    for (int r = 0; r < nrows; ++r) {
+        if (r >= r_lo && r < r_hi) {
+            for (int c = tid; c < lead + tail; c += NT) b16[r * rs + (c < lead ? c : rowlen + c)] = 0;
+        } else {
+            for (int c = tid; c < rs; c += NT) b16[r * rs + c] = 0;
+        }
+    }
+    auto copy_unit = [&](int r, int c, const tv &v, TIN e) {
+        if (vec) {
+            _Float16 *dst = band + r * rs + lead + c * VEC;
+            float f[VEC];
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) f[i] = (float)v[i];
+            if (VEC == 8 && !E::bf) *(tv *)dst = v;                  // fp16 input, fp16 storage
+            else if (VEC == 8) *(h8 *)dst = E::pack(f);
+            else *(h4 *)dst = E::pack4(f);
+        } else {
+            b16[r * rs + lead + c] = E::bits((float)e);
+        }
+    };
+    tv bv[NV];
+    TIN bs[NV];
+    if (upr <= NT) {
+        const int P = NT / upr;                                   // rows per pass
+        const int rq = tid / upr, cq = tid - rq * upr;
+        const int npass = (r_hi - r_lo + P - 1) / P;
+        for (int p0 = 0; p0 < npass; p0 += NV) {
+#pragma unroll
+            for (int u = 0; u < NV; ++u) {
+                const int r = r_lo + (p0 + u) * P + rq;
+                if (rq < P && r < r_hi) {
+                    if (vec) bv[u] = *(const tv *)(src0 + (size_t)r * rowlen + cq * VEC);
+                    else bs[u] = src0[(size_t)r * rowlen + cq];
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < NV; ++u) {
+                const int r = r_lo + (p0 + u) * P + rq;
+                if (rq < P && r < r_hi) copy_unit(r, cq, bv[u], bs[u]);
+            }
+        }
+    } else {
+        for (int r = r_lo; r < r_hi; ++r) {                       // rows longer than the workgroup
+            for (int c0 = 0; c0 < upr; c0 += NT * NV) {
+#pragma unroll
+                for (int u = 0; u < NV; ++u) {
+                    const int c = c0 + u * NT + tid;
+                    if (c < upr) {
+                        if (vec) bv[u] = *(const tv *)(src0 + (size_t)r * rowlen + c * VEC);
+                        else bs[u] = src0[(size_t)r * rowlen + c];
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < NV; ++u) {
+                    const int c = c0 + u * NT + tid;
+                    if (c < upr) copy_unit(r, c, bv[u], bs[u]);
+                }
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Coalesced epilogue.  An MFMA accumulator gives a lane 4 channels of one
 // pixel (half of a 16-byte sliced element, the other half in lane l+16);
 // storing that directly makes every quarter-wave write half-masked 64-byte

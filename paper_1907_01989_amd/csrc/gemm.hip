@@ -548,61 +548,13 @@ hipError_t launch_fc(const GemmParams &p, hipStream_t st) {
 template <typename E, typename TIN, int NB>
 __global__ __launch_bounds__(256) void stem_kernel(StemParams p, int th, int rs, int nrows) {
     extern __shared__ _Float16 band[];           // [nrows][rs] 16-bit storage values
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int bands = (p.OH + th - 1) / th;
     const int n = blockIdx.x / bands, oy0 = (blockIdx.x - n * bands) * th;
     const int iy0 = oy0 * p.sh - p.pt;
-    const TIN *x = (const TIN *)p.x;
-    const int rowlen = p.W * p.C;                // elements of one NHWC input row
-    const int lead = p.pl * p.C;                 // zero columns before the data
-    // zero the band, then copy the rows that exist (16-byte vectors when the
-    // input rows and their place in LDS are 16-byte aligned)
-    for (int e = tid * 8; e < nrows * rs; e += 256 * 8) {
-        if (e + 8 <= nrows * rs) *(h8 *)(band + e) = zero_h8();
-        else for (int q = e; q < nrows * rs; ++q) band[q] = (_Float16)0.0f;
-    }
-    __syncthreads();
-    constexpr int VEC = 16 / sizeof(TIN);        // elements per 16-byte load
-    const bool vec = (rowlen % 8) == 0 && (lead % 8) == 0 && (rs % 8) == 0;
-    for (int r = 0; r < nrows; ++r) {
-        const int iy = iy0 + r;
-        if (iy < 0 || iy >= p.H) continue;       // uniform: the band row stays zero
-        const TIN *src = x + ((size_t)n * p.H + iy) * rowlen;
-        _Float16 *dst = band + r * rs + lead;
-        if (vec) {
-            for (int c = tid * VEC; c < rowlen; c += 256 * VEC) {
-                if (VEC == 8 && !E::bf) {
-                    *(h8 *)(dst + c) = *(const h8 *)(src + c);
-                } else if (VEC == 8) {
-                    const h8 hv = *(const h8 *)(src + c);
-                    float f[8];
-#pragma unroll
-                    for (int i = 0; i < 8; ++i) f[i] = (float)hv[i];
-                    *(h8 *)(dst + c) = E::pack(f);
-                } else {
-                    const float4 f = *(const float4 *)(src + c);
-                    const float fv[4] = {f.x, f.y, f.z, f.w};
-                    *(h4 *)(dst + c) = E::pack4(fv);
-                }
-            }
-        } else {
-            uint16_t *d16 = (uint16_t *)dst;
-            for (int c = tid; c < rowlen; c += 256) d16[c] = E::bits((float)src[c]);
-        }
-    }
-    // per-lane offsets of its 8 im2col entries inside a window
-    int koff[8];
-#pragma unroll
-    for (int t = 0; t < 8; ++t) {
-        const int k = 8 * (lane >> 4) + t;
-        int off = 0;
-        if (k < p.K) {
-            const int tap = k / p.C, ci = k - tap * p.C;
-            const int ky = tap / p.KW, kx = tap - ky * p.KW;
-            off = ky * p.dh * rs + kx * p.dw * p.C + ci;
-        }
-        koff[t] = off;
-    }
+    // weights and bias first, then the input rows of the band (all of the
+    // workgroup's loads in flight together)
     h8 a[NB];
     f4 c0[NB];                                   // accumulators start from the bias
 #pragma unroll
@@ -610,35 +562,61 @@ __global__ __launch_bounds__(256) void stem_kernel(StemParams p, int th, int rs,
         a[i] = p.w[(size_t)i * 64 + lane];
         c0[i] = bias_frag(p.bias, i, p.nb16, lane);
     }
+    stage_input_band<E, TIN, 256, 4>(band, (const TIN *)p.x, n, p.H, p.W, p.C, iy0, nrows, rs, p.pl * p.C, tid);
+    // offsets of the lane's 8 im2col entries inside a window
+    int koff[8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t) koff[t] = p.koff[8 * (lane >> 4) + t];
     __syncthreads();
 
+    // each wave parks a fragment's act1(acc) in its own LDS tile [2*NB
+    // slices][16 pixels][8] fp32 behind the band, then re-reads it so that
+    // consecutive lanes own consecutive pixels of one slice: residual reads
+    // and output writes are whole 16-byte elements (a lane's 4 channels alone
+    // would make half-masked writes)
+    constexpr int NSL = 2 * NB;
+    float *stg = (float *)(band + nrows * rs) + wave * (NSL * 16 * 8);
     const int fpr = (p.OW + 15) >> 4;            // 16-pixel fragments per output row
     const int nfr = min(th, p.OH - oy0) * fpr;
-    for (int f = wave; f < nfr; f += 4) {
-        const int oyl = f / fpr;
-        const int ox = (f - oyl * fpr) * 16 + (lane & 15);
+    int oyl = wave / fpr, fx = wave - oyl * fpr;  // fragment f = oyl * fpr + fx, stepped below
+    for (int f = wave; f < nfr; f += 4, fx += 4) {
+        while (fx >= fpr) {
+            fx -= fpr;
+            ++oyl;
+        }
+        const int ox0 = fx * 16;
+        const int ox = ox0 + (lane & 15);
         const int base = oyl * p.sh * rs + min(ox, p.OW - 1) * p.sw * p.C;
         h8 b;
 #pragma unroll
         for (int t = 0; t < 8; ++t) b[t] = band[base + koff[t]];
-        const int m = (n * p.OH + oy0 + oyl) * p.OW + ox;
 #pragma unroll
         for (int i = 0; i < NB; ++i) {
             const f4 acc = E::mma(a[i], b, c0[i]);
-            const int nbase = i * 16 + 4 * (lane >> 4);
-            const int os = nbase >> 3, hoff = nbase & 7;
-            if (ox >= p.OW || os >= p.ns) continue;
-            const size_t off = ((size_t)os * p.M + m) * 8 + hoff;
-            float v[4];
+            f4 v;
 #pragma unroll
             for (int r = 0; r < 4; ++r) v[r] = act_apply(acc[r], p.act1);
-            if (p.res) {
-                const h4 rv = *(const h4 *)((const _Float16 *)p.res + off);
-#pragma unroll
-                for (int r = 0; r < 4; ++r) v[r] = act_apply(v[r] + E::get4(rv, r), p.act2);
-            }
-            *(h4 *)((_Float16 *)p.y + off) = E::pack4(v);
+            const int sl = 2 * i + (lane >> 5), half = 4 * ((lane >> 4) & 1);
+            *(f4 *)(stg + (sl * 16 + (lane & 15)) * 8 + half) = v;
         }
+        __builtin_amdgcn_wave_barrier();
+        const size_t m0 = (size_t)(n * p.OH + oy0 + oyl) * p.OW + ox0;
+#pragma unroll
+        for (int t = 0; t < (NSL * 16 + 63) / 64; ++t) {
+            const int e = lane + 64 * t;
+            const int sl = e >> 4, px = e & 15;
+            if (e >= NSL * 16 || sl >= p.ns || ox0 + px >= p.OW) continue;
+            const f4 lo = *(const f4 *)(stg + e * 8), hi = *(const f4 *)(stg + e * 8 + 4);
+            float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+            const size_t off = (size_t)sl * p.M + m0 + px;
+            if (p.res) {
+                const h8 rv = p.res[off];
+#pragma unroll
+                for (int r = 0; r < 8; ++r) v[r] = act_apply(v[r] + E::get(rv, r), p.act2);
+            }
+            p.y[off] = E::pack(v);
+        }
+        __builtin_amdgcn_wave_barrier();
     }
 }
 
@@ -654,27 +632,47 @@ size_t stem_band_bytes(int th, int kh, int kw, int c, int w, int ow, int sh, int
     return (size_t)nrows * stem_row_stride(c, w, ow, sw, kw, dw, pl) * 2;
 }
 
+#ifndef MGI_STEM_ROWS
+#define MGI_STEM_ROWS 4
+#endif
+constexpr int kStemRows = MGI_STEM_ROWS;
+
 template <typename E, typename TIN>
 static hipError_t launch_stem_t(const StemParams &p, hipStream_t st) {
     // band of th output rows: enough workgroups to fill the chip when possible
     // and a band that fits 64 KiB of LDS
-    int th = 4;
+    int th = kStemRows;
     while (th > 1 && (size_t)p.N * ((p.OH + th - 1) / th) < 1024) th >>= 1;
-    while (th > 1 && stem_band_bytes(th, p.KH, p.KW, p.C, p.W, p.OW, p.sh, p.sw, p.dh, p.dw, p.pl) > 65536)
+    while (th > 1 && stem_band_bytes(th, p.KH, p.KW, p.C, p.W, p.OW, p.sh, p.sw, p.dh, p.dw, p.pl) +
+                             kStemStageBytes > 65536)
         th >>= 1;
     const int nrows = (th - 1) * p.sh + (p.KH - 1) * p.dh + 1;
     const int rs = stem_row_stride(p.C, p.W, p.OW, p.sw, p.KW, p.dw, p.pl);
-    const size_t lds = (size_t)nrows * rs * 2;
-    if (lds > 65536) return hipErrorInvalidValue;
+    const size_t lds = (size_t)nrows * rs * 2 + (size_t)4 * p.nb16 * 1024;   // band + per-wave staging
+    if (lds > 65536 || p.K > 32) return hipErrorInvalidValue;
+    StemParams q = p;
+    im2col_offsets(q.koff, p.K, p.C, p.KW, p.dh, p.dw, rs);
     const dim3 grid(p.N * ((p.OH + th - 1) / th)), block(256);
     switch (p.nb16) {
-        case 1: launch((stem_kernel<E, TIN, 1>), grid, block, lds, st, p, th, rs, nrows); break;
-        case 2: launch((stem_kernel<E, TIN, 2>), grid, block, lds, st, p, th, rs, nrows); break;
-        case 3: launch((stem_kernel<E, TIN, 3>), grid, block, lds, st, p, th, rs, nrows); break;
-        case 4: launch((stem_kernel<E, TIN, 4>), grid, block, lds, st, p, th, rs, nrows); break;
+        case 1: launch((stem_kernel<E, TIN, 1>), grid, block, lds, st, q, th, rs, nrows); break;
+        case 2: launch((stem_kernel<E, TIN, 2>), grid, block, lds, st, q, th, rs, nrows); break;
+        case 3: launch((stem_kernel<E, TIN, 3>), grid, block, lds, st, q, th, rs, nrows); break;
+        case 4: launch((stem_kernel<E, TIN, 4>), grid, block, lds, st, q, th, rs, nrows); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
+}
+
+void im2col_offsets(int *koff, int K, int C, int KW, int dh, int dw, int rs) {
+    for (int k = 0; k < 32; ++k) {
+        int off = 0;
+        if (k < K) {
+            const int tap = k / C, ci = k - tap * C;
+            const int ky = tap / KW, kx = tap - ky * KW;
+            off = ky * dh * rs + kx * dw * C + ci;
+        }
+        koff[k] = off;
+    }
 }
 
 hipError_t launch_stem(const StemParams &p, bool fp16_in, hipStream_t st) {

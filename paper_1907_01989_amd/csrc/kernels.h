@@ -96,9 +96,12 @@ struct StemParams {
     int KH, KW, K, sh, sw, dh, dw, pt, pl;
     int nb16, ns, act1, act2;
     int bf16;            // storage type: 0 fp16, 1 bf16
+    int koff[32];        // set by launch_stem: offset of im2col entry k in the LDS band
 };
 hipError_t launch_stem(const StemParams &p, bool fp16_in, hipStream_t st);
-// LDS bytes the stem kernel stages for a band of th output rows
+// LDS bytes the stem kernel stages for a band of th output rows, and at most
+// for its output staging (4 waves x 4 channel blocks x 1 KiB)
+constexpr size_t kStemStageBytes = 16384;
 size_t stem_band_bytes(int th, int kh, int kw, int c, int w, int ow, int sh, int sw, int dh, int dw,
                        int pl);
 
@@ -117,7 +120,11 @@ struct StemDwParams {
     int OH, OW, S, dpt, dpl, ns, act2;
     int nbands, rs, pstride, band_h8; // set by launch_stemdw from the configuration
     int bf16;            // storage type: 0 fp16, 1 bf16
+    int koff[32];        // set by launch_stemdw: offset of im2col entry k in the LDS band
 };
+// offsets of im2col entries k < 32 of a kh x kw window (k = (ky*kw + kx)*c +
+// ci) inside an input band of row stride rs; 0 past K (zero weights there)
+void im2col_offsets(int *koff, int K, int C, int KW, int dh, int dw, int rs);
 struct StemDwGeom {
     int rows, nbands, rs, pstride, band_h8;
     size_t lds;

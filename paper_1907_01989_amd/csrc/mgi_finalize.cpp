@@ -639,7 +639,7 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
                 const int rs = std::max(((ow - 1) * d.stride_w + (d.kw - 1) * d.dil_w + 1) * x.c,
                                         (x.w + d.pad_l) * x.c);
                 const size_t band1 = (size_t)((d.kh - 1) * d.dil_h + 1) * (rs + 7) * 2;
-                if (from_input && d.kh * d.kw * x.c <= 32 && d.cout <= 64 && band1 <= 65536) {
+                if (from_input && d.kh * d.kw * x.c <= 32 && d.cout <= 64 && band1 + kern::kStemStageBytes <= 65536) {
                     nd.kind = NodeKind::Stem;
                     nd.kname = "conv_stem";
                     nd.in = {in_buf[op.in[0]]};

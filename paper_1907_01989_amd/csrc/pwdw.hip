@@ -188,7 +188,7 @@ __global__ __launch_bounds__(NW * 64, 2) void pwdw_kernel(PwDwParams p) {   // >
             }
     };
     step(0, xq[0], true);
-    xload(min(PF, nk - 1), xq[0]);
+    if (PF < nk) xload(PF, xq[0]);                // (a single K-step has nothing to prefetch)
     for (int c = 0; c < nchunks; ++c) {
 #pragma unroll
         for (int u = 0; u < CK; ++u) {
@@ -241,8 +241,15 @@ __global__ __launch_bounds__(NW * 64, 2) void pwdw_kernel(PwDwParams p) {   // >
         const int g = pass * GPI + tid / LPR;
         const bool gv = g < ngroups;
         const int gg = gv ? g : 0;
-        const int strip = gg % nstrips, rest = gg / nstrips;
-        const int sl = rest % nsl, t = rest / nsl;
+        // group gg = (t * nsl + sl) * nstrips + strip; a row band has one
+        // image and one strip, so its groups are the slices (no division)
+        int strip = 0, sl = gg, t = 0;
+        if (nstrips != 1 || nimg != 1) {
+            strip = gg % nstrips;
+            const int rest = gg / nstrips;
+            sl = rest % nsl;
+            t = rest / nsl;
+        }
         const int oy0 = oy_lo + strip * R, iy0 = oy0 * S_ - p.pt;
         const h8 *plane = lds + sl * PMAX + t * thw;
         h8 w[9];

@@ -52,64 +52,8 @@ __global__ __launch_bounds__(NT) void stemdw_kernel(StemDwParams p) {
     float *dwb = (float *)(taps + NSL * 9);
     h8 *zslot = (h8 *)(dwb + NSL * 8);
 
-    // 1. the input rows of the band, taps, biases and stem weights: every
-    // global load of the workgroup is issued before any of them is waited
-    // for (each thread holds up to NV 16-byte vectors, or NV elements when
-    // rows are not 16-byte aligned); meanwhile only the padding cells of the
-    // band (rows outside the image, columns before and after the data) are
-    // zeroed, so that no barrier separates the two
-    const TIN *x = (const TIN *)p.x;
-    const int rowlen = p.W * p.C;
-    const int lead = p.pl * p.C;
-    constexpr int VEC = 16 / sizeof(TIN);
-    constexpr int NV = 4;
-    typedef TIN tv __attribute__((ext_vector_type(VEC)));
-    const int r_lo = max(0, -iy0), r_hi = min(nrows, p.H - iy0);   // band rows inside the image
-    const TIN *src0 = x + ((size_t)n * p.H + iy0) * rowlen;
-    const bool vec = (rowlen % 8) == 0 && (lead % 8) == 0 && (rs % 8) == 0;
-    const int vpr = vec ? rowlen / VEC : rowlen;                  // load units per row
-    const int total = (r_hi - r_lo) * vpr;
-    auto load_batch = [&](int b0, tv *bv, TIN *bs) {
-#pragma unroll
-        for (int u = 0; u < NV; ++u) {
-            const int idx = b0 + u * NT + tid;
-            if (idx < total) {
-                const int r = r_lo + idx / vpr, c = idx % vpr;
-                if (vec) bv[u] = *(const tv *)(src0 + (size_t)r * rowlen + c * VEC);
-                else bs[u] = src0[(size_t)r * rowlen + c];
-            }
-        }
-    };
-    auto store_batch = [&](int b0, const tv *bv, const TIN *bs) {
-#pragma unroll
-        for (int u = 0; u < NV; ++u) {
-            const int idx = b0 + u * NT + tid;
-            if (idx < total) {
-                const int r = r_lo + idx / vpr, c = idx % vpr;
-                if (vec) {
-                    _Float16 *dst = band + r * rs + lead + c * VEC;
-                    if (VEC == 8 && !E::bf) {
-                        *(h8 *)dst = *(const h8 *)&bv[u];
-                    } else if (VEC == 8) {
-                        float f[8];
-#pragma unroll
-                        for (int i = 0; i < 8; ++i) f[i] = (float)bv[u][i % VEC];
-                        *(h8 *)dst = E::pack(f);
-                    } else {
-                        float f[4];
-#pragma unroll
-                        for (int i = 0; i < 4; ++i) f[i] = (float)bv[u][i % VEC];
-                        *(h4 *)dst = E::pack4(f);
-                    }
-                } else {
-                    ((uint16_t *)band)[r * rs + lead + c] = E::bits((float)bs[u]);
-                }
-            }
-        }
-    };
-    tv bv[NV];
-    TIN bs[NV];
-    load_batch(0, bv, bs);
+    // 1. taps, biases and stem weights (loads issued first), then the input
+    // rows of the band (all of the workgroup's loads in flight together)
     h8 tq = p.dw_w[min(tid, NSL * 9 - 1)];
     float bq = p.dw_b[min(tid, NSL * 8 - 1)];
     h8 a[NB];
@@ -119,38 +63,14 @@ __global__ __launch_bounds__(NT) void stemdw_kernel(StemDwParams p) {
         a[i] = p.w[(size_t)i * 64 + lane];
         c0[i] = bias_frag(p.bias, i, p.nb16, lane);
     }
-    {
-        uint16_t *b16 = (uint16_t *)band;
-        const int tail = rs - lead - rowlen;                       // zero columns after the data
-        for (int r = 0; r < nrows; ++r) {
-            if (r >= r_lo && r < r_hi) {
-                for (int c = tid; c < lead + tail; c += NT) b16[r * rs + (c < lead ? c : rowlen + c)] = 0;
-            } else {
-                for (int c = tid; c < rs; c += NT) b16[r * rs + c] = 0;
-            }
-        }
-    }
+    stage_input_band<E, TIN, NT, 4>(band, (const TIN *)p.x, n, p.H, p.W, p.C, iy0, nrows, rs, p.pl * p.C, tid);
     if (tid < NSL * 9) taps[tid] = tq;
     if (tid < NSL * 8) dwb[tid] = bq;
     if (tid == 0) *zslot = zero_h8();
-    store_batch(0, bv, bs);
-    for (int b0 = NT * NV; b0 < total; b0 += NT * NV) {          // rows wider than one batch
-        load_batch(b0, bv, bs);
-        store_batch(b0, bv, bs);
-    }
-    // per-lane offsets of its 8 im2col entries inside a window
+    // offsets of the lane's 8 im2col entries inside a window
     int koff[8];
 #pragma unroll
-    for (int t = 0; t < 8; ++t) {
-        const int k = 8 * (lane >> 4) + t;
-        int off = 0;
-        if (k < p.K) {
-            const int tap = k / p.C, ci = k - tap * p.C;
-            const int ky = tap / p.KW, kx = tap - ky * p.KW;
-            off = ky * p.dh * rs + kx * p.dw * p.C + ci;
-        }
-        koff[t] = off;
-    }
+    for (int t = 0; t < 8; ++t) koff[t] = p.koff[8 * (lane >> 4) + t];
     __syncthreads();
 
     // 2. stem outputs of rows [sr0, sr1) into the planes: one 16-pixel
@@ -158,9 +78,13 @@ __global__ __launch_bounds__(NT) void stemdw_kernel(StemDwParams p) {
     const int fpr = (p.SW + 15) >> 4;
     const int nfr = nsr * fpr;
     const int sub = 4 * ((lane >> 4) & 1);        // half of a sliced element
-    for (int f = wave; f < nfr; f += NWV) {
-        const int syl = f / fpr;
-        const int sx = (f - syl * fpr) * 16 + (lane & 15);
+    int syl = wave / fpr, fx = wave - syl * fpr;  // fragment f = syl * fpr + fx, stepped below
+    for (int f = wave; f < nfr; f += NWV, fx += NWV) {
+        while (fx >= fpr) {
+            fx -= fpr;
+            ++syl;
+        }
+        const int sx = fx * 16 + (lane & 15);
         const int base = syl * p.sh * rs + min(sx, p.SW - 1) * p.sw * p.C;
         h8 b;
 #pragma unroll
@@ -295,6 +219,7 @@ hipError_t launch_stemdw(const StemDwParams &p, int cfg, bool fp16_in, hipStream
     if (cfg < 0 || cfg >= stemdw_configs(p, -1, nullptr, nullptr) || !stemdw_configs(p, cfg, &g, nullptr))
         return hipErrorInvalidValue;
     StemDwParams q = p;
+    im2col_offsets(q.koff, p.K, p.C, p.KW, p.dh, p.dw, g.rs);
     q.nbands = g.nbands;
     q.rs = g.rs;
     q.pstride = g.pstride;
