@@ -27,6 +27,21 @@ __device__ __forceinline__ h8 zero_h8() {
     return z;
 }
 
+// q = x / d, r = x % d for 0 <= x < 2^31, 1 <= d, from a host-computed
+// reciprocal inv = 1.0 / d: the double product is within one of the
+// quotient, and one correction step makes it exact.
+__device__ __forceinline__ void divmod_fast(int x, int d, double inv, int &q, int &r) {
+    q = (int)((double)x * inv);
+    r = x - q * d;
+    if (r < 0) {
+        --q;
+        r += d;
+    } else if (r >= d) {
+        ++q;
+        r -= d;
+    }
+}
+
 // Workgroups are dispatched to the 8 XCDs round-robin (block b -> XCD b % 8).
 // Give every XCD a contiguous range of tiles so that tiles sharing input rows
 // (same pixel block, neighbouring channel blocks) meet in the same L2.

@@ -134,6 +134,11 @@ struct StemDwGeom {
 int stemdw_configs(const StemDwParams &p, int cfg, StemDwGeom *g, const char **name);
 hipError_t launch_stemdw(const StemDwParams &p, int cfg, bool fp16_in, hipStream_t st);
 
+// reciprocals of a kernel's index divisors (see divmod_fast)
+struct DivConsts {
+    double inv_ow, inv_nstrips, inv_n;
+};
+
 struct DwParams {
     const h8 *x;
     const h8 *w;         // fp16 taps [S][kh*kw][8]

@@ -33,18 +33,20 @@ LaunchEvents &launch_events() {
 // contiguous run of one row.  Taps outside the input read a zeroed 16-byte
 // element instead of branching, so all loads are issued unconditionally.
 // Launch: 1-D, thread g -> column g % OW, strip (g / OW) % nstrips, plane
-// g / (OW * nstrips) (plane = slice * N + image).
+// g / (OW * nstrips) (plane = slice * N + image); the divisions are
+// reciprocal products with one correction step (divmod_fast), a few
+// instructions instead of an integer division sequence each.
 // ---------------------------------------------------------------------------
 template <typename E, int S_, int D_, int R>
-__global__ __launch_bounds__(256) void dw3_kernel(DwParams p, int nstrips) {
+__global__ __launch_bounds__(256) void dw3_kernel(DwParams p, int nstrips, DivConsts dc) {
     constexpr int NR = (R - 1) * S_ + 2 * D_ + 1;
     const int g = blockIdx.x * 256 + threadIdx.x;
-    const int ox = g % p.OW;
-    const int rest = g / p.OW;
-    const int strip = rest % nstrips;
-    const int plane = rest / nstrips;
+    int rest, ox, plane, strip, s, img;
+    divmod_fast(g, p.OW, dc.inv_ow, rest, ox);
+    divmod_fast(rest, nstrips, dc.inv_nstrips, plane, strip);
     if (plane >= p.S * p.N) return;
-    const int s = plane / p.N;
+    divmod_fast(plane, p.N, dc.inv_n, s, img);
+    (void)img;
     const int oy0 = strip * R;
     const h8 *xin = p.x + (size_t)plane * p.H * p.W;
     const h8 *wp = p.w + (size_t)s * 9;
@@ -134,8 +136,9 @@ static hipError_t launch_dw3(const DwParams &p, hipStream_t st) {
     const int nstrips = (p.OH + R - 1) / R;
     const size_t threads = (size_t)p.OW * nstrips * p.S * p.N;
     if (threads > 0x7fffffffull) return hipErrorInvalidValue;
+    const DivConsts dc{1.0 / p.OW, 1.0 / nstrips, 1.0 / p.N};
     launch((dw3_kernel<E, S_, D_, R>), dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, st,
-                       p, nstrips);
+           p, nstrips, dc);
     return hipGetLastError();
 }
 
