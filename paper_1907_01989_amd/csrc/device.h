@@ -65,6 +65,20 @@ __device__ __forceinline__ void fma_mix(float &acc, uint32_t a, uint32_t b) {
                      : "+v"(acc) : "v"(a), "v"(b));
 }
 
+// the same with a separate addend: out = a * b + c (the first tap of an
+// output takes its bias this way, so no register copy initialises it)
+template <int HI>
+__device__ __forceinline__ float fma_mix_from(uint32_t a, uint32_t b, float c) {
+    float out;
+    if (HI)
+        asm volatile("v_fma_mix_f32 %0, %1, %2, %3 op_sel:[1,1,0] op_sel_hi:[1,1,0]"
+                     : "=v"(out) : "v"(a), "v"(b), "v"(c));
+    else
+        asm volatile("v_fma_mix_f32 %0, %1, %2, %3 op_sel:[0,0,0] op_sel_hi:[1,1,0]"
+                     : "=v"(out) : "v"(a), "v"(b), "v"(c));
+    return out;
+}
+
 typedef uint32_t u4x __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ u4x as_u4(h8 v) { return __builtin_bit_cast(u4x, v); }
@@ -75,6 +89,15 @@ __device__ __forceinline__ void fma8(float *acc, u4x w, u4x v) {
     for (int d = 0; d < 4; ++d) {
         fma_mix<0>(acc[2 * d], w[d], v[d]);
         fma_mix<1>(acc[2 * d + 1], w[d], v[d]);
+    }
+}
+
+// acc[0..7] = w * v + c0 channel-wise
+__device__ __forceinline__ void fma8_from(float *acc, const float *c0, u4x w, u4x v) {
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+        acc[2 * d] = fma_mix_from<0>(w[d], v[d], c0[2 * d]);
+        acc[2 * d + 1] = fma_mix_from<1>(w[d], v[d], c0[2 * d + 1]);
     }
 }
 
@@ -98,6 +121,9 @@ struct F16 {
     }
     __device__ static f4 mma(h8 a, h8 b, f4 c) { return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0); }
     __device__ static void fma8(float *acc, h8 w, h8 v) { kern::fma8(acc, as_u4(w), as_u4(v)); }
+    __device__ static void fma8_from(float *acc, const float *c0, h8 w, h8 v) {
+        kern::fma8_from(acc, c0, as_u4(w), as_u4(v));
+    }
     __device__ static float get4(h4 v, int i) { return (float)v[i]; }
     __device__ static h4 pack4(const float *v) {
         h4 o;
@@ -126,6 +152,10 @@ struct BF16 {
     __device__ static void fma8(float *acc, h8 w, h8 v) {
 #pragma unroll
         for (int i = 0; i < 8; ++i) acc[i] = fmaf(get(w, i), get(v, i), acc[i]);
+    }
+    __device__ static void fma8_from(float *acc, const float *c0, h8 w, h8 v) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[i] = fmaf(get(w, i), get(v, i), c0[i]);
     }
     __device__ static float get4(h4 v, int i) {
         return __uint_as_float((uint32_t)__builtin_bit_cast(u16x4, v)[i] << 16);

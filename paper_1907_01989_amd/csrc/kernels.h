@@ -126,7 +126,7 @@ struct StemDwParams {
 // ci) inside an input band of row stride rs; 0 past K (zero weights there)
 void im2col_offsets(int *koff, int K, int C, int KW, int dh, int dw, int rs);
 struct StemDwGeom {
-    int rows, nbands, rs, pstride, band_h8;
+    int rows, group, threads, nbands, rs, pstride, band_h8;
     size_t lds;
 };
 // Number of fused configurations (band heights) that fit a shape (0: none);

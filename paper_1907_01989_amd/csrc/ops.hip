@@ -70,11 +70,12 @@ __global__ __launch_bounds__(256) void dw3_kernel(DwParams p, int nstrips, DivCo
         for (int k = 0; k < 3; ++k)
             v[r][k] = *((rv && cv[k]) ? xin + (size_t)iy * p.W + cx[k] : p.zero);
     }
+    // accumulation per output: bias, then taps ky = 0..2, kx = 0..2 (the
+    // first tap takes the bias as its addend)
+    float bias[8];
+#pragma unroll
+    for (int c = 0; c < 8; ++c) bias[c] = p.bias[s * 8 + c];
     float acc[R][8];
-#pragma unroll
-    for (int o = 0; o < R; ++o)
-#pragma unroll
-        for (int c = 0; c < 8; ++c) acc[o][c] = p.bias[s * 8 + c];
 #pragma unroll
     for (int r = 0; r < NR; ++r)
 #pragma unroll
@@ -82,7 +83,10 @@ __global__ __launch_bounds__(256) void dw3_kernel(DwParams p, int nstrips, DivCo
             const int t = r - ky * D_;
             if (t >= 0 && t % S_ == 0 && t / S_ < R) {
 #pragma unroll
-                for (int k = 0; k < 3; ++k) E::fma8(acc[t / S_], w[ky * 3 + k], v[r][k]);
+                for (int k = 0; k < 3; ++k) {
+                    if (ky == 0 && k == 0) E::fma8_from(acc[t / S_], bias, w[0], v[r][0]);
+                    else E::fma8(acc[t / S_], w[ky * 3 + k], v[r][k]);
+                }
             }
         }
     // activation as one clamp: [lo, hi] = (-inf, inf), (0, inf) or (0, 6)

@@ -262,11 +262,10 @@ __global__ __launch_bounds__(NW * 64, 2) void pwdw_kernel(PwDwParams p) {   // >
             cx[k] = ox * S_ + cx0 + k;
             cv[k] = gv && cx[k] >= 0 && cx[k] < p.W;
         }
+        float bias2[8];
+#pragma unroll
+        for (int c = 0; c < 8; ++c) bias2[c] = dwb[sl * 8 + c];
         float acc2[R][8];
-#pragma unroll
-        for (int o = 0; o < R; ++o)
-#pragma unroll
-            for (int c = 0; c < 8; ++c) acc2[o][c] = dwb[sl * 8 + c];
 #pragma unroll
         for (int r = 0; r < NR; ++r) {
             const int iy = iy0 + r;
@@ -289,7 +288,10 @@ __global__ __launch_bounds__(NW * 64, 2) void pwdw_kernel(PwDwParams p) {   // >
                 const int tt = r - ky;
                 if (tt >= 0 && tt % S_ == 0 && tt / S_ < R) {
 #pragma unroll
-                    for (int k = 0; k < 3; ++k) E::fma8(acc2[tt / S_], w[ky * 3 + k], t3[k]);
+                    for (int k = 0; k < 3; ++k) {      // (the first tap takes the bias as its addend)
+                        if (ky == 0 && k == 0) E::fma8_from(acc2[tt / S_], bias2, w[0], t3[0]);
+                        else E::fma8(acc2[tt / S_], w[ky * 3 + k], t3[k]);
+                    }
                 }
             }
         }
