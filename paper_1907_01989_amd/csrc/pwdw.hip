@@ -342,6 +342,13 @@ const Inst kInsts[] = {
     // small, this pays for reading the activations twice as often; measured
     // slower on the deeper band layers, as were 16-channel tiles)
     {true, 4, 9, 2, 2, 2, 64, 1, "band2x32w4"},  {true, 4, 4, 2, 1, 2, 64, 2, "band2x32w4"},   // 112 -> 56, 56 x 56
+    // 48- and 96-channel tiles: MobileNet-v2's expansions (96, 144, 192, 576,
+    // 960 channels) are multiples of 48, so these leave no partial tile
+    {true, 4, 9, 3, 2, 2, 64, 1, "band2x48w4"},  {true, 4, 4, 3, 1, 2, 64, 2, "band2x48w4"},   // 112 -> 56, 56 x 56
+    {true, 4, 5, 3, 2, 2, 32, 2, "band2x48w4"},  {true, 4, 3, 3, 1, 4, 32, 4, "band4x48w4"},   // 56 -> 28, 28 x 28
+    {true, 4, 3, 4, 2, 2, 16, 4, "band2x64w4"},  {true, 4, 3, 4, 1, 4, 32, 4, "band4x64w4"},   // 28 -> 14, 28 x 28
+    {false, 8, 2, 6, 1, 7, 16, 4, "img96"},      {false, 8, 2, 6, 1, 7, 8, 4, "img96"},        // 14 x 14, 7 x 7
+    {false, 8, 2, 6, 2, 7, 8, 4, "img96"},                                                     // 14 -> 7
 };
 constexpr int kNumInsts = sizeof(kInsts) / sizeof(kInsts[0]);
 
@@ -414,6 +421,11 @@ hipError_t launch_inst(int k, const PwDwParams &p, size_t lds, hipStream_t st) {
         MGI_PWDW(16, 8, 8, 4, 2, 4, 64, 2) MGI_PWDW(17, 4, 9, 4, 2, 2, 64, 1)
         MGI_PWDW(18, 8, 4, 4, 1, 4, 64, 2) MGI_PWDW(19, 4, 4, 4, 1, 2, 64, 2)
         MGI_PWDW(20, 4, 9, 2, 2, 2, 64, 1) MGI_PWDW(21, 4, 4, 2, 1, 2, 64, 2)
+        MGI_PWDW(22, 4, 9, 3, 2, 2, 64, 1) MGI_PWDW(23, 4, 4, 3, 1, 2, 64, 2)
+        MGI_PWDW(24, 4, 5, 3, 2, 2, 32, 2) MGI_PWDW(25, 4, 3, 3, 1, 4, 32, 4)
+        MGI_PWDW(26, 4, 3, 4, 2, 2, 16, 4) MGI_PWDW(27, 4, 3, 4, 1, 4, 32, 4)
+        MGI_PWDW(28, 8, 2, 6, 1, 7, 16, 4) MGI_PWDW(29, 8, 2, 6, 1, 7, 8, 4)
+        MGI_PWDW(30, 8, 2, 6, 2, 7, 8, 4)
 #undef MGI_PWDW
     }
     return hipErrorInvalidValue;
