@@ -349,6 +349,7 @@ const Inst kInsts[] = {
     {true, 4, 3, 4, 2, 2, 16, 4, "band2x64w4"},  {true, 4, 3, 4, 1, 4, 32, 4, "band4x64w4"},   // 28 -> 14, 28 x 28
     {false, 8, 2, 6, 1, 7, 16, 4, "img96"},      {false, 8, 2, 6, 1, 7, 8, 4, "img96"},        // 14 x 14, 7 x 7
     {false, 8, 2, 6, 2, 7, 8, 4, "img96"},                                                     // 14 -> 7
+    {true, 4, 5, 4, 2, 2, 32, 2, "band2x64w4"},  {true, 8, 4, 4, 2, 4, 32, 2, "band4x64"},     // 56 -> 28
 };
 constexpr int kNumInsts = sizeof(kInsts) / sizeof(kInsts[0]);
 
@@ -426,6 +427,7 @@ hipError_t launch_inst(int k, const PwDwParams &p, size_t lds, hipStream_t st) {
         MGI_PWDW(26, 4, 3, 4, 2, 2, 16, 4) MGI_PWDW(27, 4, 3, 4, 1, 4, 32, 4)
         MGI_PWDW(28, 8, 2, 6, 1, 7, 16, 4) MGI_PWDW(29, 8, 2, 6, 1, 7, 8, 4)
         MGI_PWDW(30, 8, 2, 6, 2, 7, 8, 4)
+        MGI_PWDW(31, 4, 5, 4, 2, 2, 32, 2) MGI_PWDW(32, 8, 4, 4, 2, 4, 32, 2)
 #undef MGI_PWDW
     }
     return hipErrorInvalidValue;
