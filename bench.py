@@ -225,6 +225,10 @@ def measured_traffic(kernel, layer, config):
     return None
 
 
+# the dominant kernel is timestamped in every DOM_EVERY-th step of the timed region
+DOM_EVERY = 5
+
+
 def roofline_entry(flops, byts, bound, seconds):
     if bound == "mfma":
         ach = flops / seconds / 1e12
@@ -280,28 +284,38 @@ def run_workload(key, steps, warmup, hip, profile_steps=20, detail=True, tune=Tr
                 hip.destroy(e)
     dom = max(range(nn), key=lambda i: per_node[i])
 
+    # device time per step, from events between steps of an untimed pass
+    marks = [hip.event() for _ in range(21)]
+    for k in range(20):
+        hip.record(marks[k], sh)
+        B.mgi_plan_run(plan.handle, ins, ops_ptrs, sh)
+    hip.record(marks[20], sh)
+    torch.cuda.synchronize()
+    step_ms = percentiles([hip.elapsed_ms(marks[k], marks[k + 1]) for k in range(20)])
+    for e in marks:
+        hip.destroy(e)
+
     # timed region: K steps; the dominant node's kernel is timestamped at its
-    # start and end in every step
-    dev = [(hip.event(), hip.event()) for _ in range(steps)]
-    arrays = []
-    for a, b in dev:
+    # start and end in every DOM_EVERY-th step (a timestamped launch costs a
+    # few microseconds of its own, so sampling keeps that out of most steps)
+    sampled = list(range(0, steps, DOM_EVERY))
+    dev = {k: (hip.event(), hip.event()) for k in sampled}
+    arrays = {}
+    for k, (a, b) in dev.items():
         e0, e1 = [None] * nn, [None] * nn
         e0[dom], e1[dom] = a, b
-        arrays.append((e0, e1))
-    marks = [hip.event() for _ in range(steps + 1)]
+        arrays[k] = (e0, e1)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(steps):
-        hip.record(marks[k], sh)
-        B.mgi_plan_run_timed(plan.handle, ins, ops_ptrs, arrays[k][0], arrays[k][1], sh)
-    hip.record(marks[steps], sh)
+        if k in arrays:
+            B.mgi_plan_run_timed(plan.handle, ins, ops_ptrs, arrays[k][0], arrays[k][1], sh)
+        else:
+            B.mgi_plan_run(plan.handle, ins, ops_ptrs, sh)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    dom_ms = sum(hip.elapsed_ms(a, b) for a, b in dev) / steps
-    step_ms = percentiles([hip.elapsed_ms(marks[k], marks[k + 1]) for k in range(steps)])
-    for e in marks:
-        hip.destroy(e)
-    for a, b in dev:
+    dom_ms = sum(hip.elapsed_ms(a, b) for a, b in dev.values()) / len(dev)
+    for a, b in dev.values():
         hip.destroy(a)
         hip.destroy(b)
 
@@ -320,6 +334,7 @@ def run_workload(key, steps, warmup, hip, profile_steps=20, detail=True, tune=Tr
     roof = roofline_entry(fl, by, bound, dom_ms * 1e-3)
     dom_layer = desc["ops"][nodes[dom]["tensor"]]["name"]
     roof.update({"kernel": nodes[dom]["kind"], "layer": dom_layer, "config": configs[dom],
+                 "timed_launches": len(dev),
                  "algorithmic_bytes": int(by), "algorithmic_flops": int(fl),
                  "avg_launch_us": round(dom_ms * 1e3, 3),
                  "traffic": measured_traffic(nodes[dom]["kind"], dom_layer, configs[dom])})
@@ -387,18 +402,21 @@ def run_graph_replay(key, steps, warmup, hip, tune=True):
     plan.capture(xs)
     for _ in range(warmup):
         plan.replay(sh)
-    marks = [hip.event() for _ in range(steps + 1)]
+    marks = [hip.event() for _ in range(21)]     # per-step device time: untimed pass
+    for k in range(20):
+        hip.record(marks[k], sh)
+        plan.replay(sh)
+    hip.record(marks[20], sh)
+    torch.cuda.synchronize()
+    step_ms = percentiles([hip.elapsed_ms(marks[k], marks[k + 1]) for k in range(20)])
+    for e in marks:
+        hip.destroy(e)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(steps):
-        hip.record(marks[k], sh)
         plan.replay(sh)
-    hip.record(marks[steps], sh)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    step_ms = percentiles([hip.elapsed_ms(marks[k], marks[k + 1]) for k in range(steps)])
-    for e in marks:
-        hip.destroy(e)
     plan.close()
     total_s = t1 - t0
     return {"images_per_s": batch * steps / total_s, "ms_per_step": total_s / steps * 1e3,
