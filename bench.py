@@ -162,6 +162,14 @@ def node_work(desc, nodes, shapes, i):
         flops = 2.0 * n * h_ * w_ * cin * cmid + 2.0 * elems(t) * op["kh"] * op["kw"]
         byts = (elems(pop["in"]) * 2 + out_b + pop["w"].size * 2 + pop["b"].size * 4 +
                 op["w"].size * 2 + op["b"].size * 4)
+    elif kind == "pw_pool":
+        # pointwise input in, pooled means out; the pointwise output never
+        # reaches memory
+        cop = ops[head_of(op["in"])]
+        n, h_, w_, cin = shapes[cop["in"]]
+        cmid = cop["cout"]
+        flops = 2.0 * n * h_ * w_ * cin * cmid + float(n * h_ * w_ * cmid)
+        byts = elems(cop["in"]) * 2 + out_b + cop["w"].size * 2 + cop["b"].size * 4
     elif kind == "stem_dw":
         # graph input in, depthwise output out; the stem output never
         # reaches memory

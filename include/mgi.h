@@ -120,6 +120,11 @@ typedef struct {
                             kh*kw*c <= 32 and at most 64 output channels) and a 3x3 depthwise
                             convolution at stride 1 that alone reads its output: 0, 1
                             (default) or 2 as for fuse_pwdw.  Needs fuse = 1. */
+    int fuse_pool;       /* the same for a pointwise convolution (no residual) and a global
+                            average pool over planes of at most 64 pixels that alone reads
+                            its output: the means are written directly, bit-identical to the
+                            two operators.  0, 1 (default) or 2 as for fuse_pwdw.  Needs
+                            fuse = 1. */
 } mgi_options;
 
 /* ---------------------------------------------------------------------------

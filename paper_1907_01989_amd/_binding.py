@@ -35,7 +35,8 @@ class Options(ctypes.Structure):
                 ("materialize_all", ctypes.c_int), ("dtype", ctypes.c_int),
                 ("fuse_dwpw", ctypes.c_int),
                 ("fuse_pwdw", ctypes.c_int),
-                ("fuse_stemdw", ctypes.c_int)]
+                ("fuse_stemdw", ctypes.c_int),
+                ("fuse_pool", ctypes.c_int)]
 
 
 _lib = None

@@ -382,19 +382,85 @@ __device__ __forceinline__ void pipe_issue(const GemmParams &p, int kk, h8 *st, 
     }
 }
 
-template <typename E, int BM, int BN>
+// Global average pool of a pipelined-GEMM tile that holds whole images:
+// every output value is rounded to the storage type as a stored tensor would
+// be (act1, then round) and staged in LDS as fp32, pixel-major [BM][BN] with
+// the channel index XOR-swizzled by the pixel (4 * (px % 8)) so that both the
+// accumulator-layout writes and the per-channel reads are free of bank
+// conflicts.  A thread then owns one (image, channel) and sums its pixels in
+// the global-pool kernel's order (8 partial sums over pixels j, j + 8, ...,
+// then pairs (0,4), (2,6), (1,5), (3,7) and their sums, times 1/hw), so the
+// fused node equals the GEMM followed by the pool bit for bit; the lane of
+// each 8 channels gathers the other seven by shuffles and stores the
+// element.  Output: sliced pooled means [ns][nimg].
+template <typename E, int BM, int BN, int FM, int FN>
+__device__ __forceinline__ void pool_epilogue(const GemmParams &p, const f4 (&acc)[FN][FM], int mt, int nb0,
+                                              int wm, int wn, float *T, int tid, int lane) {
+    constexpr int WMP = BM / 2;
+    static_assert(BN % 32 == 0, "swizzle spans 32 channels");
+    auto at = [](int px, int ch) { return px * BN + (ch ^ (4 * (px & 7))); };
+#pragma unroll
+    for (int i = 0; i < FN; ++i) {
+        const int ch = (wn * FN + i) * 16 + 4 * (lane >> 4);
+#pragma unroll
+        for (int j = 0; j < FM; ++j) {
+            const int px = wm * WMP + j * 16 + (lane & 15);
+            float v[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) v[r] = act_apply(acc[i][j][r], p.act1);
+            const h4 h = E::pack4(v);
+            f4 f;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) f[r] = E::get4(h, r);
+            *(f4 *)(T + at(px, ch)) = f;          // 4 channels stay contiguous under the swizzle
+        }
+    }
+    __syncthreads();
+    const float inv = 1.0f / (float)p.hw;
+    for (int t0 = 0; t0 < p.ipt * BN; t0 += 256) {    // same trip count in every lane (shuffles)
+        const int t = t0 + tid;
+        const int k = t / BN, ch = t - k * BN;
+        const bool live = t < p.ipt * BN;
+        const int kk = live ? k : 0;
+        float a[8];
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) {
+            float sum = 0.0f;
+#pragma unroll
+            for (int ii = 0; ii < 8; ++ii) {
+                const int px = jj + 8 * ii;
+                sum += px < p.hw ? T[at(kk * p.hw + min(px, p.hw - 1), ch)] : 0.0f;
+            }
+            a[jj] = sum;
+        }
+        const float q = (((a[0] + a[4]) + (a[2] + a[6])) + ((a[1] + a[5]) + (a[3] + a[7]))) * inv;
+        float o[8];
+#pragma unroll
+        for (int c = 0; c < 8; ++c) o[c] = __shfl(q, (lane & ~7) + c);
+        const int img = mt * p.ipt + k, os = nb0 * 2 + ch / 8;
+        if (live && (ch & 7) == 0 && img < p.nimg && os < p.ns) ((h8 *)p.y)[(size_t)os * p.nimg + img] = E::pack(o);
+    }
+}
+
+// POOL: the output feeds only a global average pool over planes of p.hw <=
+// BM pixels; an M-tile then holds p.ipt whole images (rows mt * ipt * hw
+// on), and the epilogue writes the pooled means instead of the tile (see
+// pool_epilogue).
+template <typename E, int BM, int BN, bool POOL>
 __global__ __launch_bounds__(256) void gemm_pipe_kernel(GemmParams p) {
     using T = PipeTile<BM, BN>;
     constexpr int WMP = BM / 2, WNC = BN / 2, FM = WMP / 16, FN = WNC / 16;
     static_assert(WMP * WNC * 4 <= (T::XE + T::WE) * 16, "epilogue tile must fit one stage");
-    __shared__ h8 st0[T::XE + T::WE], st1[T::XE + T::WE], st2[T::XE + T::WE], st3[T::XE + T::WE];
+    static_assert(!POOL || BM * BN * 4 <= 4 * (T::XE + T::WE) * 16, "pool tile must fit the ring");
+    __shared__ h8 ring[4][T::XE + T::WE];
+    h8 *st0 = ring[0], *st1 = ring[1], *st2 = ring[2], *st3 = ring[3];
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave & 1, wn = wave >> 1;
     const int tile = xcd_tile(blockIdx.x, gridDim.x);
     const int mt = tile / p.ntiles, nt = tile - mt * p.ntiles;
-    const int m0 = mt * BM, nb0 = nt * (BN / 16);
+    const int m0 = POOL ? mt * p.ipt * p.hw : mt * BM, nb0 = nt * (BN / 16);
     const int nk = p.ksp / T::KS;
 
     f4 acc[FN][FM];
@@ -438,6 +504,10 @@ __global__ __launch_bounds__(256) void gemm_pipe_kernel(GemmParams p) {
     }
 
     __syncthreads();
+    if (POOL) {
+        pool_epilogue<E, BM, BN, FM, FN>(p, acc, mt, nb0, wm, wn, (float *)&ring[0][0], tid, lane);
+        return;
+    }
     h8 *stage = wave == 0 ? st0 : wave == 1 ? st1 : wave == 2 ? st2 : st3;
     store_tile_c8<E, FM, FN>(p, acc, m0 + wm * WMP, nb0 + wn * FN, (float *)stage, lane);
 }
@@ -447,8 +517,29 @@ static hipError_t launch_pipe_t(const GemmParams &p, hipStream_t st) {
     GemmParams q = p;
     q.mtiles = (p.M + BM - 1) / BM;
     q.ntiles = (p.nb16 * 16 + BN - 1) / BN;
-    launch((gemm_pipe_kernel<E, BM, BN>), dim3(q.mtiles * q.ntiles), dim3(256), 0, st, q);
+    launch((gemm_pipe_kernel<E, BM, BN, false>), dim3(q.mtiles * q.ntiles), dim3(256), 0, st, q);
     return hipGetLastError();
+}
+
+template <typename E, int BM, int BN>
+static hipError_t launch_pipe_pool_t(const GemmParams &p, hipStream_t st) {
+    GemmParams q = p;
+    q.ipt = BM / p.hw;
+    q.mtiles = (p.nimg + q.ipt - 1) / q.ipt;
+    q.ntiles = (p.nb16 * 16 + BN - 1) / BN;
+    launch((gemm_pipe_kernel<E, BM, BN, true>), dim3(q.mtiles * q.ntiles), dim3(256), 0, st, q);
+    return hipGetLastError();
+}
+
+hipError_t launch_gemm_pool(const GemmParams &p, int bm, int bn, hipStream_t st) {
+    if (p.nimg <= 0) return hipSuccess;
+    if (p.ksp % 4 != 0 || p.Min != p.M || p.hw < 1 || p.hw > bm || p.hw > 64 || p.M != p.nimg * p.hw)
+        return hipErrorInvalidValue;
+    if (bm == 64 && bn == 64) return p.bf16 ? launch_pipe_pool_t<BF16, 64, 64>(p, st) : launch_pipe_pool_t<F16, 64, 64>(p, st);
+    if (bm == 64 && bn == 128) return p.bf16 ? launch_pipe_pool_t<BF16, 64, 128>(p, st) : launch_pipe_pool_t<F16, 64, 128>(p, st);
+    if (bm == 128 && bn == 64) return p.bf16 ? launch_pipe_pool_t<BF16, 128, 64>(p, st) : launch_pipe_pool_t<F16, 128, 64>(p, st);
+    if (bm == 128 && bn == 128) return p.bf16 ? launch_pipe_pool_t<BF16, 128, 128>(p, st) : launch_pipe_pool_t<F16, 128, 128>(p, st);
+    return hipErrorInvalidValue;
 }
 
 hipError_t launch_gemm_pipe(const GemmParams &p, int bm, int bn, hipStream_t st) {

@@ -45,6 +45,8 @@ struct GemmParams {
     int bf16;            // storage type: 0 fp16, 1 bf16
     // implicit-GEMM window geometry
     int H, W, OH, OW, sin, kw, sh, sw, dh, dw, pt, pl;
+    // pooled GEMM: pixels per image, images, images per M-tile (set by the launcher)
+    int hw, nimg, ipt;
 };
 hipError_t launch_gemm(const GemmParams &p, int bm, int bn, bool taps, bool f32out,
                        hipStream_t st);
@@ -56,6 +58,11 @@ hipError_t launch_gemm_xs(const GemmParams &p, int wm, int bn, int pf, hipStream
 // pointwise GEMM with both operands in a 4-stage LDS ring fed by direct
 // global->LDS loads; tile bm pixels x bn channels, bm, bn in {64, 128}
 hipError_t launch_gemm_pipe(const GemmParams &p, int bm, int bn, hipStream_t st);
+// pointwise GEMM whose output feeds only a global average pool: M-tiles of
+// bm rows hold bm / hw whole images (hw <= 64 pixels each, M = nimg * hw),
+// and the pooled means are written, sliced [ns][nimg], bit-identical to the
+// GEMM followed by the pool kernel
+hipError_t launch_gemm_pool(const GemmParams &p, int bm, int bn, hipStream_t st);
 // fully-connected layer, fp32 (M x cout) output; K split over the waves
 hipError_t launch_fc(const GemmParams &p, hipStream_t st);
 size_t gemm_xs_lds_bytes(int ksp, int wm, int bn);

@@ -184,6 +184,25 @@ void add_configs(const mgi_plan &p, Node &nd, size_t M) {
         const Node::Config split{GemmTile{}, 4, "split", true, 0};
         nd.cfgs.insert(nd.fused_default ? nd.cfgs.end() : nd.cfgs.begin(), Node::Config(split));
         nd.apply(0);
+    } else if (nd.kind == NodeKind::GemmPool) {
+        // tiles of the pooled GEMM (M-tiles of whole images), and the GEMM
+        // then the pool kernel through the scratch tensor (first when the
+        // fused kernel would not fill the GPU)
+        const int hw = nd.dw_in.h * nd.dw_in.w, npad = nd.nb16 * 16;
+        const int tiles[4][2] = {{128, 64}, {128, 128}, {64, 128}, {64, 64}};
+        for (auto &tb : tiles) {
+            if (hw > tb[0] || (tb[1] > 64 && npad <= 64)) continue;
+            GemmTile t;
+            t.pipe = true;
+            t.bm = tb[0];
+            t.bn = tb[1];
+            nd.cfgs.push_back({t, 0, "pool" + std::to_string(tb[0]) + "x" + std::to_string(tb[1])});
+        }
+        GemmTile t;
+        pick_pipe_tile(t, nd.dw_in.pixels(), npad);
+        const Node::Config split{t, 0, "split_" + tile_name(t), true, 0};
+        nd.cfgs.insert(nd.fused_default ? nd.cfgs.end() : nd.cfgs.begin(), Node::Config(split));
+        nd.apply(0);
     } else if (nd.kind == NodeKind::DwPw) {
         // band heights for the fused depthwise + pointwise kernel: up to 128
         // or up to 64 pixels per workgroup
@@ -352,6 +371,49 @@ void fuse_stem_into_dw(mgi_plan &p, bool always) {
     p.nodes.swap(kept);
 }
 
+// A pointwise GEMM whose output only a global average pool reads (planes of
+// at most 64 pixels) becomes one node (GemmPool): the pooled GEMM kernel
+// (gemm.hip, pool_epilogue) writes the means directly; the GEMM output stays
+// a planned scratch tensor for the split configuration (GEMM, then pool).
+void fuse_pool_into_pw(mgi_plan &p, bool always) {
+    std::vector<int> readers(p.bufs.size(), 0), producer(p.bufs.size(), -1);
+    for (size_t i = 0; i < p.nodes.size(); ++i) {
+        const Node &nd = p.nodes[i];
+        for (int b : nd.in) readers[b]++;
+        if (nd.residual >= 0) readers[nd.residual]++;
+        producer[nd.out] = (int)i;
+    }
+    std::vector<char> drop(p.nodes.size(), 0);
+    for (size_t i = 0; i < p.nodes.size(); ++i) {
+        const Node &gp = p.nodes[i];
+        if (gp.kind != NodeKind::Gap || gp.in.size() != 1) continue;
+        const int mid = gp.in[0];
+        if (readers[mid] != 1 || p.bufs[mid].loc != Loc::Arena || producer[mid] < 0) continue;
+        Node &pw = p.nodes[producer[mid]];
+        if (pw.kind != NodeKind::Gemm || pw.taps || pw.residual >= 0 || pw.in.size() != 1 ||
+            pw.act2 != MGI_ACT_NONE || gp.act1 != MGI_ACT_NONE)
+            continue;
+        const Shape in = p.bufs[mid].shape;
+        if (in.h * in.w > 64 || pw.ksp % 4 != 0) continue;
+        const int hw = in.h * in.w, ipt = 128 / hw;
+        pw.fused_default = always || (size_t)((in.n + ipt - 1) / ipt) * ((pw.nb16 * 16 + 63) / 64) >= 128;
+        pw.kind = NodeKind::GemmPool;
+        pw.kname = "pw_pool";
+        pw.dw_in = in;
+        pw.dw_out = p.bufs[gp.out].shape;
+        pw.out = gp.out;
+        pw.out_tensor = gp.out_tensor;
+        pw.n_fused += gp.n_fused;
+        pw.tile = GemmTile{};
+        pw.scratch = mid;
+        drop[i] = 1;
+    }
+    std::vector<Node> kept;
+    for (size_t i = 0; i < p.nodes.size(); ++i)
+        if (!drop[i]) kept.push_back(std::move(p.nodes[i]));
+    p.nodes.swap(kept);
+}
+
 void pick_pipe_tile(GemmTile &t, size_t M, int npad) {
     const int cand[3][2] = {{128, 128}, {128, 64}, {64, 64}};
     size_t best_tiles = 0;
@@ -467,6 +529,8 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
         return fail(MGI_ERR_INVALID_ARG, "mgi_graph_finalize: fuse_pwdw is 0, 1 or 2");
     if (o.fuse_stemdw < 0 || o.fuse_stemdw > 2)
         return fail(MGI_ERR_INVALID_ARG, "mgi_graph_finalize: fuse_stemdw is 0, 1 or 2");
+    if (o.fuse_pool < 0 || o.fuse_pool > 2)
+        return fail(MGI_ERR_INVALID_ARG, "mgi_graph_finalize: fuse_pool is 0, 1 or 2");
     auto to_bits = o.dtype == MGI_DTYPE_BF16 ? f32_to_bf16_bits : f32_to_f16_bits;
 
     const std::vector<char> live = live_ops(g);
@@ -864,6 +928,7 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
 
     if (o.fuse && o.fuse_pwdw) fuse_pw_into_dw(p, o.fuse_pwdw == 2);
     if (o.fuse && o.fuse_stemdw) fuse_stem_into_dw(p, o.fuse_stemdw == 2);
+    if (o.fuse && o.fuse_pool) fuse_pool_into_pw(p, o.fuse_pool == 2);
     if (o.fuse && o.fuse_dwpw) fuse_dw_into_pw(p);
     for (Node &nd : p.nodes) add_configs(p, nd, p.bufs[nd.out].shape.pixels());
 
@@ -951,7 +1016,8 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
             for (int ch = 0; ch < c; ++ch) bp[ch] = dop.b[ch];
         }
         if (nd.kind == NodeKind::Gemm || nd.kind == NodeKind::Stem || nd.kind == NodeKind::FC ||
-            nd.kind == NodeKind::DwPw || nd.kind == NodeKind::PwDw || nd.kind == NodeKind::StemDw) {
+            nd.kind == NodeKind::DwPw || nd.kind == NodeKind::PwDw || nd.kind == NodeKind::StemDw ||
+            nd.kind == NodeKind::GemmPool) {
             const Shape x = g.ops[op.in[0]].out;
             const int cin = x.c;
             const int cout = nd.kind == NodeKind::FC ? op.cout : op.conv.cout;

@@ -329,4 +329,5 @@ extern "C" void mgi_options_default(mgi_options *o) {
     o->fuse_dwpw = 0;
     o->fuse_pwdw = 1;
     o->fuse_stemdw = 1;
+    o->fuse_pool = 1;
 }

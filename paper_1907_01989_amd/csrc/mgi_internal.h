@@ -74,7 +74,7 @@ struct Buf {
 
 enum class NodeKind {
     Ingest, Stem, Gemm, Depthwise, Add, Act, Gap, FC, Softmax, Concat, Resize, Argmax,
-    ResizeArgmax, Export, Pad, DwPw, PwDw, StemDw
+    ResizeArgmax, Export, Pad, DwPw, PwDw, StemDw, GemmPool
 };
 
 // Tile shape of the MFMA GEMM (pointwise, implicit-GEMM convolution, FC).
@@ -117,10 +117,11 @@ struct Node {
     mgi_conv_desc dw_conv{};
     int dw_act = MGI_ACT_NONE;
     size_t dw_w_off = 0, dw_b_off = 0;
-    Shape dw_in, dw_out;    // PwDw / StemDw: shapes of the depthwise input (the first op's output) and output
+    Shape dw_in, dw_out;    // PwDw / StemDw / GemmPool: shapes of the intermediate tensor (the first
+                            // op's output) and of the node's output
     // kernel configurations the autotuner may choose from (index 0 = the
     // finalize-time choice); `cfg` is the one in use
-    // PwDw / StemDw: the first op's output kept as a planned scratch tensor,
+    // PwDw / StemDw / GemmPool: the first op's output kept as a planned scratch tensor,
     // so that the node can also run as the two separate kernels (split);
     // whether the fused kernel is the default configuration
     int scratch = -1;

@@ -187,6 +187,39 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
             q.act2 = nd.dw_act;
             return launch_pwdw(q, nd.pwdw_cfg, st);
         }
+        case NodeKind::GemmPool: {
+            // pointwise GEMM + global average pool: the pooled GEMM kernel,
+            // or (split) the GEMM into the scratch tensor and the pool kernel
+            const Shape mid = nd.dw_in;
+            GemmParams g{};
+            g.bf16 = bf;
+            g.x = (const h8 *)buf_ptr(p, nd.in[0], B);
+            g.w = (const h8 *)(wbase + nd.w_off);
+            g.bias = (const float *)(wbase + nd.b_off);
+            g.M = g.Min = (int)mid.pixels();
+            g.ksl = nd.ksl; g.ksp = nd.ksp;
+            g.nb16 = nd.nb16; g.ns = slices(mid.c); g.cout = mid.c;
+            g.act1 = nd.act1; g.act2 = MGI_ACT_NONE;
+            if (!nd.split) {
+                g.y = y;
+                g.hw = mid.h * mid.w;
+                g.nimg = mid.n;
+                return launch_gemm_pool(g, nd.tile.bm, nd.tile.bn, st);
+            }
+            LaunchEvents &ev = launch_events();
+            const LaunchEvents saved = ev;
+            void *sp = buf_ptr(p, nd.scratch, B);
+            g.y = sp;
+            ev.stop = nullptr;
+            hipError_t e = launch_gemm_pipe(g, nd.tile.bm, nd.tile.bn, st);
+            ev.start = nullptr;
+            ev.stop = saved.stop;
+            if (e == hipSuccess)
+                e = launch_gap((const h8 *)sp, (h8 *)y, (const h8 *)(wbase + p.zero_off), mid.n, mid.h * mid.w,
+                               slices(mid.c), bf, st);
+            ev = saved;
+            return e;
+        }
         case NodeKind::StemDw: {
             const Buf &ib = p.bufs[nd.in[0]];
             const bool fp16_in = ib.in_dtype == MGI_DTYPE_FP16;

@@ -110,12 +110,12 @@ def test_finalize_state_errors_and_run_before_bind():
 
 
 def test_fusion_structure():
-    v1 = engine.Plan(workloads.mobilenet_v1(1), bind=False, fuse_pwdw=False, fuse_stemdw=False)
+    v1 = engine.Plan(workloads.mobilenet_v1(1), bind=False, fuse_pwdw=False, fuse_stemdw=False, fuse_pool=False)
     kinds = [n["kind"] for n in v1.nodes()]
     assert kinds[0] == "conv_stem" and kinds.count("dw_conv") == 13 and kinds.count("pw_gemm") == 13
     assert kinds[-3:] == ["global_avgpool", "fc_gemm", "softmax"]
     assert len(kinds) == 30
-    v2 = engine.Plan(workloads.mobilenet_v2(1), bind=False, fuse_pwdw=False, fuse_stemdw=False)
+    v2 = engine.Plan(workloads.mobilenet_v2(1), bind=False, fuse_pwdw=False, fuse_stemdw=False, fuse_pool=False)
     nodes = v2.nodes()
     assert sum(1 for n in nodes if n["n_fused"] == 2) == 10      # residual adds absorbed
     assert not any(n["kind"] == "add" for n in nodes)
@@ -132,11 +132,13 @@ def test_pointwise_depthwise_fusion_structure():
     v1 = engine.Plan(workloads.mobilenet_v1(64), bind=False)
     nodes = v1.nodes()
     kinds = [n["kind"] for n in nodes]
-    assert kinds.count("pw_dw") == 12 and kinds.count("stem_dw") == 1 and kinds.count("pw_gemm") == 1
+    assert kinds.count("pw_dw") == 12 and kinds.count("stem_dw") == 1 and kinds.count("pw_pool") == 1
     assert kinds[0] == "stem_dw" and "dw_conv" not in kinds and "conv_stem" not in kinds
-    assert len(kinds) == 17
+    assert kinds[-3:] == ["pw_pool", "fc_gemm", "softmax"] and len(kinds) == 16
     k_nostem = [n["kind"] for n in engine.Plan(workloads.mobilenet_v1(64), bind=False, fuse_stemdw=False).nodes()]
-    assert k_nostem[:2] == ["conv_stem", "dw_conv"] and len(k_nostem) == 18
+    assert k_nostem[:2] == ["conv_stem", "dw_conv"] and len(k_nostem) == 17
+    k_nopool = [n["kind"] for n in engine.Plan(workloads.mobilenet_v1(64), bind=False, fuse_pool=False).nodes()]
+    assert k_nopool[-4:] == ["pw_gemm", "global_avgpool", "fc_gemm", "softmax"] and len(k_nopool) == 17
     for n in nodes:
         if n["kind"] == "pw_dw":
             assert n["n_fused"] == 2
@@ -158,7 +160,8 @@ def test_pointwise_depthwise_fusion_structure():
     b1f = engine.Plan(workloads.mobilenet_v1(1), bind=False, fuse_pwdw=2)
     b1fc = [c for n, c in zip(b1f.nodes(), b1f.node_configs()) if n["kind"] == "pw_dw"]
     assert len(b1fc) == 12 and all(name.startswith(("img", "band")) for _, _, name in b1fc)
-    for o in (engine.options(fuse_pwdw=3), engine.options(fuse_stemdw=3), engine.options(fuse_stemdw=-1)):
+    for o in (engine.options(fuse_pwdw=3), engine.options(fuse_stemdw=3), engine.options(fuse_stemdw=-1),
+              engine.options(fuse_pool=3)):
         g = engine.build_graph(workloads.mobilenet_v1(1))
         try:
             assert err(B.mgi_graph_finalize, g, o) == 1
@@ -233,7 +236,8 @@ def test_identity_removal_and_pad_merge():
     assert "pad" not in fused and "concat" not in fused
     assert fused.count("activation") == 1                          # only the one on the graph input
     assert "resize_bilinear" not in fused
-    assert fused.count("global_avgpool") == 3                      # the dead pool has no node
+    # the dead pool has no node (the pool of the 1x1 convolution is fused into it)
+    assert fused.count("global_avgpool") == 2 and fused.count("pw_pool") == 1
     assert fused.count("conv_igemm") == 1 and fused.count("dw_conv") == 1
     unfused = _kinds(desc, fuse=False)
     assert unfused.count("pad") == 2 and "concat" in unfused and "resize_bilinear" in unfused
@@ -274,6 +278,8 @@ def test_node_configuration_candidates():
             assert 2 <= k <= 8 and name.startswith(("img", "band", "split"))
         elif n["kind"] == "stem_dw":
             assert k == 3 and name.startswith(("band", "split"))
+        elif n["kind"] == "pw_pool":
+            assert k == 5 and name.startswith(("pool", "split"))
         else:
             assert k == 1
     i = next(j for j, n in enumerate(nodes) if n["kind"] == "pw_gemm")
@@ -299,9 +305,10 @@ def test_pad_that_cannot_merge_runs_as_a_node():
 def test_library_memory_report_reproduces_table3(net, key, fuse):
     t3 = {"MobileNet": (9.6, 2.3), "MobileNetV2": (13.2, 4.0)}[key]
     d = workloads.WORKLOADS[net](1, logits_output=False)
-    # Algorithm 1 on the model graph: the pointwise -> depthwise fusion (which keeps
-    # the pointwise output as a node scratch tensor) is left out
-    naive, planned, nobj = engine.Plan(d, fuse=fuse, bind=False, fuse_pwdw=False).memory_report()
+    # Algorithm 1 on the model graph: the fusions of two convolution-like ops
+    # (which keep the first op's output as a node scratch tensor) are left out
+    naive, planned, nobj = engine.Plan(d, fuse=fuse, bind=False, fuse_pwdw=False, fuse_stemdw=False,
+                                       fuse_pool=False).memory_report()
     ops, sizes, inter = oplan.graph_problem(d, oracle.tensor_shapes(d))
     _, ref = oplan.greedy(ops, sizes, inter)
     assert planned == oplan.total(ref)
@@ -364,7 +371,8 @@ def test_library_mcfp_reproduces_table3(net, key, mib):
     _, ref, _ = oplan.mcfp(ops, sizes, inter)
     assert round(planned / 2 ** 20, 1) == mib
     assert planned == oplan.total(ref) and nobj == len(ref)
-    fused = engine.Plan(d, planner=B.PLANNER_MCFP, fuse=True, bind=False, fuse_pwdw=False).memory_report()
+    fused = engine.Plan(d, planner=B.PLANNER_MCFP, fuse=True, bind=False, fuse_pwdw=False,
+                        fuse_stemdw=False, fuse_pool=False).memory_report()
     assert fused[1] <= planned
 
 
