@@ -608,21 +608,22 @@ __global__ __launch_bounds__(256) void fc_kernel(GemmParams p) {
     }
 }
 
-hipError_t launch_fc(const GemmParams &p, hipStream_t st) {
+hipError_t launch_fc(const GemmParams &p, int fm, int kb, hipStream_t st) {
     if (p.M <= 0) return hipSuccess;
-    const int fm = p.M <= 16 ? 1 : (p.M <= 32 ? 2 : 4);
+    if (fm <= 0) fm = p.M <= 16 ? 1 : (p.M <= 32 ? 2 : 4);
+    if (kb <= 0) kb = 4;
     const int mtiles = (p.M + 16 * fm - 1) / (16 * fm);
     const dim3 grid(mtiles * p.nb16), block(256);
-    if (p.bf16) {
-        if (fm == 1) launch((fc_kernel<BF16, 1, 4>), grid, block, 0, st, p);
-        else if (fm == 2) launch((fc_kernel<BF16, 2, 4>), grid, block, 0, st, p);
-        else launch((fc_kernel<BF16, 4, 4>), grid, block, 0, st, p);
-    } else {
-        if (fm == 1) launch((fc_kernel<F16, 1, 4>), grid, block, 0, st, p);
-        else if (fm == 2) launch((fc_kernel<F16, 2, 4>), grid, block, 0, st, p);
-        else launch((fc_kernel<F16, 4, 4>), grid, block, 0, st, p);
+#define MGI_FC_CASE(FM_, KB_)                                                        \
+    if (fm == FM_ && kb == KB_) {                                                     \
+        if (p.bf16) launch((fc_kernel<BF16, FM_, KB_>), grid, block, 0, st, p);       \
+        else launch((fc_kernel<F16, FM_, KB_>), grid, block, 0, st, p);               \
+        return hipGetLastError();                                                     \
     }
-    return hipGetLastError();
+    MGI_FC_CASE(1, 4) MGI_FC_CASE(2, 4) MGI_FC_CASE(4, 4)
+    MGI_FC_CASE(1, 8) MGI_FC_CASE(2, 8) MGI_FC_CASE(4, 8)
+#undef MGI_FC_CASE
+    return hipErrorInvalidValue;
 }
 
 // ---------------------------------------------------------------------------

@@ -63,8 +63,10 @@ hipError_t launch_gemm_pipe(const GemmParams &p, int bm, int bn, hipStream_t st)
 // and the pooled means are written, sliced [ns][nimg], bit-identical to the
 // GEMM followed by the pool kernel
 hipError_t launch_gemm_pool(const GemmParams &p, int bm, int bn, hipStream_t st);
-// fully-connected layer, fp32 (M x cout) output; K split over the waves
-hipError_t launch_fc(const GemmParams &p, hipStream_t st);
+// fully-connected layer, fp32 (M x cout) output; K split over the waves; a
+// workgroup takes 16 * fm images (1, 2 or 4; 0 = by M) and loads kb K-steps
+// (4 or 8; 0 = 4) at once.  Results do not depend on fm or kb.
+hipError_t launch_fc(const GemmParams &p, int fm, int kb, hipStream_t st);
 size_t gemm_xs_lds_bytes(int ksp, int wm, int bn);
 
 // Depthwise 3x3 (stride 1 or 2, dilation 1) fused into the pointwise GEMM

@@ -114,7 +114,7 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
             q.sh = nd.conv.stride_h; q.sw = nd.conv.stride_w;
             q.dh = nd.conv.dil_h; q.dw = nd.conv.dil_w;
             q.pt = nd.conv.pad_t; q.pl = nd.conv.pad_l;
-            if (nd.kind == NodeKind::FC) return launch_fc(q, st);
+            if (nd.kind == NodeKind::FC) return launch_fc(q, nd.tile.wm, nd.tile.pf, st);
             if (nd.tile.pipe) return launch_gemm_pipe(q, nd.tile.bm, nd.tile.bn, st);
             if (nd.tile.slab) return launch_gemm_xs(q, nd.tile.wm, nd.tile.bn, nd.tile.pf, st);
             return launch_gemm(q, nd.tile.bm, nd.tile.bn, nd.taps, nd.kind == NodeKind::FC, st);

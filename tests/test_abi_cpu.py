@@ -280,6 +280,8 @@ def test_node_configuration_candidates():
             assert k == 3 and name.startswith(("band", "split"))
         elif n["kind"] == "pw_pool":
             assert k == 5 and name.startswith(("pool", "split"))
+        elif n["kind"] == "fc_gemm":
+            assert k >= 1 and name.startswith("fc")
         else:
             assert k == 1
     i = next(j for j, n in enumerate(nodes) if n["kind"] == "pw_gemm")
