@@ -352,19 +352,20 @@ hipError_t launch_gemm_xs(const GemmParams &p, int wm, int bn, int pf, hipStream
 // ahead into the slot freed by the previous iteration, and runs its MFMAs.
 // The loop is unrolled by NST so every slot is a compile-time choice.
 // ---------------------------------------------------------------------------
-template <int BM, int BN>
+template <int BM, int BN, int KS_ = 4>
 struct PipeTile {
-    static constexpr int KS = 4, NST = 4;
+    static constexpr int KS = KS_, NST = 4;       // K slices per stage (4 or 8: one or two MFMA K-steps)
+    static constexpr int SUB = KS / 4;
     static constexpr int XE = BM * KS, WE = BN * KS;    // 16-byte elements per stage
     static constexpr int XL = XE / 256, WL = WE / 256;  // wave loads per wave per stage
     static constexpr int LPW = XL + WL;
     static_assert(XE % 256 == 0 && WE % 256 == 0, "tile must be a multiple of 64 both ways");
 };
 
-template <int BM, int BN>
+template <int BM, int BN, int KS>
 __device__ __forceinline__ void pipe_issue(const GemmParams &p, int kk, h8 *st, int m0, int nb0,
                                            int wave, int lane) {
-    using T = PipeTile<BM, BN>;
+    using T = PipeTile<BM, BN, KS>;
     const int k0 = kk * T::KS;
 #pragma unroll
     for (int i = 0; i < T::XL; ++i) {
@@ -376,9 +377,10 @@ __device__ __forceinline__ void pipe_issue(const GemmParams &p, int kk, h8 *st, 
     }
 #pragma unroll
     for (int i = 0; i < T::WL; ++i) {
-        const int q = wave * T::WL + i;                  // output block within the tile
+        const int L = wave * T::WL + i;                  // (output block, K-step) of the stage
+        const int q = L / T::SUB, sub = L - q * T::SUB;
         const int nb = min(nb0 + q, p.nb16 - 1);
-        load_lds16(p.w + ((size_t)nb * p.ksp + k0) * 16 + lane, st + T::XE + q * 64);
+        load_lds16(p.w + ((size_t)nb * p.ksp + k0 + 4 * sub) * 16 + lane, st + T::XE + L * 64);
     }
 }
 
@@ -446,9 +448,9 @@ __device__ __forceinline__ void pool_epilogue(const GemmParams &p, const f4 (&ac
 // BM pixels; an M-tile then holds p.ipt whole images (rows mt * ipt * hw
 // on), and the epilogue writes the pooled means instead of the tile (see
 // pool_epilogue).
-template <typename E, int BM, int BN, bool POOL>
+template <typename E, int BM, int BN, bool POOL, int KS = 4>
 __global__ __launch_bounds__(256) void gemm_pipe_kernel(GemmParams p) {
-    using T = PipeTile<BM, BN>;
+    using T = PipeTile<BM, BN, KS>;
     constexpr int WMP = BM / 2, WNC = BN / 2, FM = WMP / 16, FN = WNC / 16;
     static_assert(WMP * WNC * 4 <= (T::XE + T::WE) * 16, "epilogue tile must fit one stage");
     static_assert(!POOL || BM * BN * 4 <= 4 * (T::XE + T::WE) * 16, "pool tile must fit the ring");
@@ -471,9 +473,9 @@ __global__ __launch_bounds__(256) void gemm_pipe_kernel(GemmParams p) {
         for (int j = 0; j < FM; ++j) acc[i][j] = b0;
     }
 
-    pipe_issue<BM, BN>(p, 0, st0, m0, nb0, wave, lane);
-    if (nk > 1) pipe_issue<BM, BN>(p, 1, st1, m0, nb0, wave, lane);
-    if (nk > 2) pipe_issue<BM, BN>(p, 2, st2, m0, nb0, wave, lane);
+    pipe_issue<BM, BN, KS>(p, 0, st0, m0, nb0, wave, lane);
+    if (nk > 1) pipe_issue<BM, BN, KS>(p, 1, st1, m0, nb0, wave, lane);
+    if (nk > 2) pipe_issue<BM, BN, KS>(p, 2, st2, m0, nb0, wave, lane);
 
     auto body = [&](int kk, const h8 *cur, h8 *nxt) {
         // stage kk has landed once at most min(2, nk-1-kk) newer stages are
@@ -484,17 +486,21 @@ __global__ __launch_bounds__(256) void gemm_pipe_kernel(GemmParams p) {
         else if (newer == 1) wait_vm_lds<T::LPW>();
         else wait_vm_lds<0>();
         __builtin_amdgcn_s_barrier();
-        if (kk + 3 < nk) pipe_issue<BM, BN>(p, kk + 3, nxt, m0, nb0, wave, lane);
-        h8 a[FN], b[FM];
+        if (kk + 3 < nk) pipe_issue<BM, BN, KS>(p, kk + 3, nxt, m0, nb0, wave, lane);
 #pragma unroll
-        for (int i = 0; i < FN; ++i) a[i] = cur[T::XE + (wn * FN + i) * 64 + lane];
+        for (int sub = 0; sub < T::SUB; ++sub) {      // MFMA K-steps of the stage, in K order
+            h8 a[FN], b[FM];
 #pragma unroll
-        for (int j = 0; j < FM; ++j) b[j] = cur[(lane >> 4) * BM + wm * WMP + j * 16 + (lane & 15)];
-#pragma unroll
-        for (int i = 0; i < FN; ++i)
+            for (int i = 0; i < FN; ++i) a[i] = cur[T::XE + ((wn * FN + i) * T::SUB + sub) * 64 + lane];
 #pragma unroll
             for (int j = 0; j < FM; ++j)
-                acc[i][j] = E::mma(a[i], b[j], acc[i][j]);
+                b[j] = cur[(4 * sub + (lane >> 4)) * BM + wm * WMP + j * 16 + (lane & 15)];
+#pragma unroll
+            for (int i = 0; i < FN; ++i)
+#pragma unroll
+                for (int j = 0; j < FM; ++j)
+                    acc[i][j] = E::mma(a[i], b[j], acc[i][j]);
+        }
     };
     for (int kk = 0; kk < nk; kk += 4) {
         body(kk, st0, st3);
@@ -540,6 +546,30 @@ hipError_t launch_gemm_pool(const GemmParams &p, int bm, int bn, hipStream_t st)
     if (bm == 128 && bn == 64) return p.bf16 ? launch_pipe_pool_t<BF16, 128, 64>(p, st) : launch_pipe_pool_t<F16, 128, 64>(p, st);
     if (bm == 128 && bn == 128) return p.bf16 ? launch_pipe_pool_t<BF16, 128, 128>(p, st) : launch_pipe_pool_t<F16, 128, 128>(p, st);
     return hipErrorInvalidValue;
+}
+
+template <typename E>
+static hipError_t launch_pipe_k8_t(const GemmParams &p, bool pool, hipStream_t st) {
+    GemmParams q = p;
+    q.ntiles = (p.nb16 * 16 + 63) / 64;
+    if (pool) {
+        q.ipt = 64 / p.hw;
+        q.mtiles = (p.nimg + q.ipt - 1) / q.ipt;
+        launch((gemm_pipe_kernel<E, 64, 64, true, 8>), dim3(q.mtiles * q.ntiles), dim3(256), 0, st, q);
+    } else {
+        q.mtiles = (p.M + 63) / 64;
+        launch((gemm_pipe_kernel<E, 64, 64, false, 8>), dim3(q.mtiles * q.ntiles), dim3(256), 0, st, q);
+    }
+    return hipGetLastError();
+}
+
+// 64x64 tiles with 8 K slices (two MFMA K-steps) per ring stage: twice the
+// bytes in flight per workgroup, for long-K GEMMs with few tiles
+hipError_t launch_gemm_pipe_k8(const GemmParams &p, bool pool, hipStream_t st) {
+    if (p.M <= 0) return hipSuccess;
+    if (p.ksp % 8 != 0 || p.Min != p.M) return hipErrorInvalidValue;
+    if (pool && (p.hw < 1 || p.hw > 64 || p.M != p.nimg * p.hw)) return hipErrorInvalidValue;
+    return p.bf16 ? launch_pipe_k8_t<BF16>(p, pool, st) : launch_pipe_k8_t<F16>(p, pool, st);
 }
 
 hipError_t launch_gemm_pipe(const GemmParams &p, int bm, int bn, hipStream_t st) {

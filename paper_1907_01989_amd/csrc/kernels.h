@@ -58,6 +58,10 @@ hipError_t launch_gemm_xs(const GemmParams &p, int wm, int bn, int pf, hipStream
 // pointwise GEMM with both operands in a 4-stage LDS ring fed by direct
 // global->LDS loads; tile bm pixels x bn channels, bm, bn in {64, 128}
 hipError_t launch_gemm_pipe(const GemmParams &p, int bm, int bn, hipStream_t st);
+// the pipelined GEMM with 64x64 tiles and 8 K slices per ring stage (two
+// MFMA K-steps; needs ksp % 8 == 0), plain or pooled (as launch_gemm_pool);
+// same accumulation order as the 4-slice stages
+hipError_t launch_gemm_pipe_k8(const GemmParams &p, bool pool, hipStream_t st);
 // pointwise GEMM whose output feeds only a global average pool: M-tiles of
 // bm rows hold bm / hw whole images (hw <= 64 pixels each, M = nimg * hw),
 // and the pooled means are written, sliced [ns][nimg], bit-identical to the

@@ -98,7 +98,7 @@ GemmTile pick_tile(size_t M, int cout) {
 // in the same order (K ascending in steps of 32 for the GEMMs, taps in window
 // order for depthwise), so they differ in speed only.
 std::string tile_name(const GemmTile &t) {
-    if (t.pipe) return "pipe" + std::to_string(t.bm) + "x" + std::to_string(t.bn);
+    if (t.pipe) return "pipe" + std::to_string(t.bm) + "x" + std::to_string(t.bn) + (t.ks == 8 ? "k8" : "");
     if (t.slab)
         return "slab" + std::to_string(4 * t.wm) + "x" + std::to_string(t.bn) + "p" + std::to_string(t.pf);
     return "lds" + std::to_string(t.bm) + "x" + std::to_string(t.bn);
@@ -109,7 +109,7 @@ void pick_pipe_tile(GemmTile &t, size_t M, int npad);
 void add_configs(const mgi_plan &p, Node &nd, size_t M) {
     auto push = [&](const GemmTile &t) {
         for (const Node::Config &c : nd.cfgs)
-            if (c.tile.pipe == t.pipe && c.tile.slab == t.slab && c.tile.bm == t.bm &&
+            if (c.tile.pipe == t.pipe && c.tile.slab == t.slab && c.tile.bm == t.bm && c.tile.ks == t.ks &&
                 c.tile.bn == t.bn && c.tile.wm == t.wm && c.tile.pf == t.pf)
                 return;
         nd.cfgs.push_back({t, 0, tile_name(t)});
@@ -125,6 +125,12 @@ void add_configs(const mgi_plan &p, Node &nd, size_t M) {
                 t.pipe = true;
                 t.bm = pb[0];
                 t.bn = pb[1];
+                push(t);
+            }
+            if (nd.ksp % 8 == 0) {            // two K-steps per ring stage
+                GemmTile t;
+                t.pipe = true;
+                t.ks = 8;
                 push(t);
             }
             const int slabs[4][2] = {{32, 32}, {16, 32}, {32, 64}, {16, 64}};
@@ -214,6 +220,12 @@ void add_configs(const mgi_plan &p, Node &nd, size_t M) {
             t.bm = tb[0];
             t.bn = tb[1];
             nd.cfgs.push_back({t, 0, "pool" + std::to_string(tb[0]) + "x" + std::to_string(tb[1])});
+        }
+        if (nd.ksp % 8 == 0) {
+            GemmTile t;
+            t.pipe = true;
+            t.ks = 8;
+            nd.cfgs.push_back({t, 0, "pool64x64k8"});
         }
         GemmTile t;
         pick_pipe_tile(t, nd.dw_in.pixels(), npad);

@@ -87,6 +87,7 @@ struct GemmTile {
     bool pipe = false;
     bool slab = false;
     int wm = 32, pf = 1;
+    int ks = 4;             // pipe: K slices per ring stage (4, or 8 for 64 x 64 tiles)
 };
 
 struct Node {

@@ -115,6 +115,7 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
             q.dh = nd.conv.dil_h; q.dw = nd.conv.dil_w;
             q.pt = nd.conv.pad_t; q.pl = nd.conv.pad_l;
             if (nd.kind == NodeKind::FC) return launch_fc(q, nd.tile.wm, nd.tile.pf, st);
+            if (nd.tile.pipe && nd.tile.ks == 8) return launch_gemm_pipe_k8(q, false, st);
             if (nd.tile.pipe) return launch_gemm_pipe(q, nd.tile.bm, nd.tile.bn, st);
             if (nd.tile.slab) return launch_gemm_xs(q, nd.tile.wm, nd.tile.bn, nd.tile.pf, st);
             return launch_gemm(q, nd.tile.bm, nd.tile.bn, nd.taps, nd.kind == NodeKind::FC, st);
@@ -204,6 +205,7 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
                 g.y = y;
                 g.hw = mid.h * mid.w;
                 g.nimg = mid.n;
+                if (nd.tile.ks == 8) return launch_gemm_pipe_k8(g, true, st);
                 return launch_gemm_pool(g, nd.tile.bm, nd.tile.bn, st);
             }
             LaunchEvents &ev = launch_events();
