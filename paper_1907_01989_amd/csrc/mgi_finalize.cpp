@@ -172,8 +172,15 @@ void add_configs(const mgi_plan &p, Node &nd, size_t M) {
         }
         GemmTile t;
         pick_pipe_tile(t, nd.dw_in.pixels(), nd.nb16 * 16);
-        const Node::Config split{t, nd.dw_conv.stride_h == 1 ? 4 : 2, "split_" + tile_name(t), true, 0};
+        const int dwr = nd.dw_conv.stride_h == 1 ? 4 : 2;
+        const Node::Config split{t, dwr, "split_" + tile_name(t), true, 0};
         nd.cfgs.insert(nd.fused_default ? nd.cfgs.end() : nd.cfgs.begin(), Node::Config(split));
+        if (nd.ksp % 8 == 0) {                // the GEMM with two K-steps per ring stage
+            GemmTile t8;
+            t8.pipe = true;
+            t8.ks = 8;
+            nd.cfgs.push_back(Node::Config{t8, dwr, "split_" + tile_name(t8), true, 0});
+        }
         nd.apply(0);
     } else if (nd.kind == NodeKind::StemDw) {
         // band heights of the fused stem + depthwise kernel, and the two

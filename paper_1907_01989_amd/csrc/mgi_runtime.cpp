@@ -166,7 +166,8 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
                 g.nb16 = nd.nb16; g.ns = slices(mid.c); g.cout = mid.c;
                 g.act1 = nd.act1; g.act2 = MGI_ACT_NONE;
                 ev.stop = nullptr;
-                hipError_t e = launch_gemm_pipe(g, nd.tile.bm, nd.tile.bn, st);
+                hipError_t e = nd.tile.ks == 8 ? launch_gemm_pipe_k8(g, false, st)
+                                               : launch_gemm_pipe(g, nd.tile.bm, nd.tile.bn, st);
                 ev.start = nullptr;
                 ev.stop = saved.stop;
                 if (e == hipSuccess) e = launch_split_dw(p, nd, sp, y, bf, st);

@@ -78,7 +78,7 @@ def test_fused_pair(n, h, w, K, C, s, pads, act):
         names.append(plan.node_configs()[idx[0]][2])
     fused_outs = [o for o, n in zip(outs, names) if n.startswith(("img", "band"))]
     split_outs = [o for o, n in zip(outs, names) if n.startswith("split")]
-    assert len(fused_outs) >= 1 and len(split_outs) == 1, names
+    assert len(fused_outs) >= 1 and len(split_outs) >= 1, names
     _, plain, _ = run_gpu(desc, materialize_all=False, fuse_pwdw=False)
     for o in fused_outs + split_outs:
         np.testing.assert_array_equal(o, plain[0])
