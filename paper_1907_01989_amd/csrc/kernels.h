@@ -173,9 +173,10 @@ struct PwDwParams {
     const h8 *w;         // packed pointwise weights [nb16][ksp][16][8]
     const float *bias;   // [nb16 * 16]
     int M, ksl, ksp, nb16, act1;
-    const h8 *dw_w;      // depthwise taps [2 * nb16][9][8]
+    const h8 *dw_w;      // depthwise taps [2 * nb16][9][8] (zero past the channels)
     const float *dw_b;   // [16 * nb16]
-    h8 *y;               // depthwise output, sliced [2 * nb16][N * OH * OW]
+    h8 *y;               // depthwise output, sliced [ns][N * OH * OW]
+    int ns;              // output slices: 2 * nb16, or one fewer (channels = 8 mod 16)
     int N, H, W, OH, OW, S, pt, pl, act2;
     int ipt, nbands, ntiles;   // set by launch_pwdw from the configuration
     int pstride;         // ... pixel stride of the LDS output tile

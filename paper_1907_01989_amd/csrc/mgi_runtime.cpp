@@ -187,6 +187,7 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
             q.N = nd.dw_in.n; q.H = nd.dw_in.h; q.W = nd.dw_in.w; q.OH = os.h; q.OW = os.w;
             q.S = nd.dw_conv.stride_h; q.pt = nd.dw_conv.pad_t; q.pl = nd.dw_conv.pad_l;
             q.act2 = nd.dw_act;
+            q.ns = slices(os.c);
             return launch_pwdw(q, nd.pwdw_cfg, st);
         }
         case NodeKind::GemmPool: {

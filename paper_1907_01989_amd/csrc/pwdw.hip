@@ -72,6 +72,7 @@ __global__ __launch_bounds__(NW * 64, 2) void pwdw_kernel(PwDwParams p) {   // >
     const int grp = tile / p.ntiles, ct = tile - grp * p.ntiles;
     const int nb0 = ct * NBT;
     const int nbv = min(NBT, p.nb16 - nb0);       // channel blocks of this tile
+    const int nsv = min(NSL, p.ns - 2 * nb0);     // ... and output slices (odd when channels = 8 mod 16)
     // pixels of the tile: whole images img0 .. img0+nimg-1, or the input rows
     // [ir0, ir1) of image img0 that output rows [oy_lo, oy_hi) read
     int img0, nimg, oy_lo, oy_hi, ir0, ir1;
@@ -116,14 +117,14 @@ __global__ __launch_bounds__(NW * 64, 2) void pwdw_kernel(PwDwParams p) {   // >
         }
         const h8 *tsrc = p.dw_w + (size_t)nb0 * 2 * 9;
         const h8 *bsrc = (const h8 *)(p.dw_b + nb0 * 16), *psrc = (const h8 *)(p.bias + nb0 * 16);
-        const int tn = nbv * 2 * 9, bn = nbv * 4;
+        const int tn = nsv * 9, dbn = nsv * 2, bn = nbv * 4;
         for (int q = wave; q < kTapQ + 2 * kBiasQ; q += NW) {
             if (q < kTapQ) {
                 const int e = q * 64 + lane;
                 load_lds16(tsrc + min(e, tn - 1), lds + main_h8 + e);
             } else if (q < kTapQ + kBiasQ) {
                 const int e = (q - kTapQ) * 64 + lane;
-                load_lds16(bsrc + min(e, bn - 1), lds + main_h8 + kTapH8 + e);
+                load_lds16(bsrc + min(e, dbn - 1), lds + main_h8 + kTapH8 + e);
             } else {
                 const int e = (q - kTapQ - kBiasQ) * 64 + lane;
                 load_lds16(psrc + min(e, bn - 1), lds + main_h8 + kTapH8 + 64 * kBiasQ + e);
@@ -230,7 +231,7 @@ __global__ __launch_bounds__(NW * 64, 2) void pwdw_kernel(PwDwParams p) {   // >
     // stride 2: lane ox loads columns 2*ox - pl and 2*ox - pl + 1; its third
     // tap column is its right neighbour's first
     const int cx0 = S_ == 2 ? -p.pl : 0;
-    const int nsl = 2 * nbv;
+    const int nsl = nsv;
     const int nstrips = p.nbands ? 1 : (p.OH + R - 1) / R;
     const int ngroups = nimg * nsl * nstrips;
     const int ox = tid % LPR;
@@ -350,6 +351,15 @@ const Inst kInsts[] = {
     {false, 8, 2, 6, 1, 7, 16, 4, "img96"},      {false, 8, 2, 6, 1, 7, 8, 4, "img96"},        // 14 x 14, 7 x 7
     {false, 8, 2, 6, 2, 7, 8, 4, "img96"},                                                     // 14 -> 7
     {true, 4, 5, 4, 2, 2, 32, 2, "band2x64w4"},  {true, 8, 4, 4, 2, 4, 32, 2, "band4x64"},     // 56 -> 28
+    // 16- and 32-channel image tiles with 2-row depthwise strips, for small
+    // batches: more workgroups, and the depthwise step spread over more lanes
+    {false, 8, 2, 1, 1, 2, 16, 4, "img16"},      {false, 8, 2, 2, 1, 2, 16, 4, "img32"},       // 14 x 14
+    {false, 8, 2, 1, 1, 2, 8, 4, "img16"},       {false, 8, 2, 2, 1, 2, 8, 4, "img32"},        // 7 x 7
+    {false, 8, 2, 1, 2, 2, 8, 4, "img16"},       {false, 8, 2, 2, 2, 2, 8, 4, "img32"},        // 14 -> 7
+    // ... with activations prefetched 8 K-steps ahead (at a batch of one the
+    // K loop waits on the memory latency, not on the matrix cores)
+    {false, 8, 2, 1, 1, 2, 16, 8, "img16p8"},    {false, 8, 2, 1, 1, 2, 8, 8, "img16p8"},      // 14 x 14, 7 x 7
+    {false, 8, 2, 1, 2, 2, 8, 8, "img16p8"},                                                   // 14 -> 7
 };
 constexpr int kNumInsts = sizeof(kInsts) / sizeof(kInsts[0]);
 
@@ -368,7 +378,7 @@ size_t lds_bytes(const Inst &in, int ksp, int pstride) {
 }
 
 // geometry of instance `in` for a shape, or false if it does not apply
-bool fits(const Inst &in, int N, int H, int W, int OH, int OW, int S, int pt, int pl, int ksp,
+bool fits(const Inst &in, int N, int H, int W, int OH, int OW, int S, int pt, int pl, int ksp, int nb16,
           PwDwGeom *g) {
     if (S != in.s || lanes_for(OW) != in.lpr || pt < 0) return false;
     // every input column a lane needs from a neighbour is held by a lane of the
@@ -381,6 +391,10 @@ bool fits(const Inst &in, int N, int H, int W, int OH, int OW, int S, int pt, in
         g->nbands = 0;
         g->groups = (N + g->ipt - 1) / g->ipt;
         g->pstride = g->ipt * H * W;
+        // 16- and 32-channel image tiles read the activations 4x and 2x as
+        // often as the 64-channel ones; they are for shapes whose 64-channel
+        // tiles leave most compute units idle (a batch of one or a few)
+        if (in.nbt < 4 && g->groups * ((nb16 + 3) / 4) >= 128) return false;
     } else {
         // a band's input rows: (R - 1) * S + 3 at most
         const int rows = std::min((in.r - 1) * S + 3, H);
@@ -428,18 +442,23 @@ hipError_t launch_inst(int k, const PwDwParams &p, size_t lds, hipStream_t st) {
         MGI_PWDW(28, 8, 2, 6, 1, 7, 16, 4) MGI_PWDW(29, 8, 2, 6, 1, 7, 8, 4)
         MGI_PWDW(30, 8, 2, 6, 2, 7, 8, 4)
         MGI_PWDW(31, 4, 5, 4, 2, 2, 32, 2) MGI_PWDW(32, 8, 4, 4, 2, 4, 32, 2)
+        MGI_PWDW(33, 8, 2, 1, 1, 2, 16, 4) MGI_PWDW(34, 8, 2, 2, 1, 2, 16, 4)
+        MGI_PWDW(35, 8, 2, 1, 1, 2, 8, 4) MGI_PWDW(36, 8, 2, 2, 1, 2, 8, 4)
+        MGI_PWDW(37, 8, 2, 1, 2, 2, 8, 4) MGI_PWDW(38, 8, 2, 2, 2, 2, 8, 4)
+        MGI_PWDW(39, 8, 2, 1, 1, 2, 16, 8) MGI_PWDW(40, 8, 2, 1, 1, 2, 8, 8)
+        MGI_PWDW(41, 8, 2, 1, 2, 2, 8, 8)
 #undef MGI_PWDW
     }
     return hipErrorInvalidValue;
 }
 
 // the applicable instances of a shape, in table order
-int applicable(int N, int H, int W, int OH, int OW, int S, int pt, int pl, int ksp, int *idx,
+int applicable(int N, int H, int W, int OH, int OW, int S, int pt, int pl, int ksp, int nb16, int *idx,
                PwDwGeom *geo) {
     int n = 0;
     for (int k = 0; k < kNumInsts; ++k) {
         PwDwGeom g{};
-        if (!fits(kInsts[k], N, H, W, OH, OW, S, pt, pl, ksp, &g)) continue;
+        if (!fits(kInsts[k], N, H, W, OH, OW, S, pt, pl, ksp, nb16, &g)) continue;
         if (idx) idx[n] = k;
         if (geo) geo[n] = g;
         ++n;
@@ -450,10 +469,9 @@ int applicable(int N, int H, int W, int OH, int OW, int S, int pt, int pl, int k
 
 int pwdw_configs(int N, int H, int W, int OH, int OW, int S, int pt, int pl, int ksp, int nb16, int cfg,
                  PwDwGeom *g, const char **name) {
-    (void)nb16;
     int idx[kNumInsts];
     PwDwGeom geo[kNumInsts];
-    const int n = applicable(N, H, W, OH, OW, S, pt, pl, ksp, idx, geo);
+    const int n = applicable(N, H, W, OH, OW, S, pt, pl, ksp, nb16, idx, geo);
     if (cfg >= 0 && cfg < n) {
         if (g) *g = geo[cfg];
         if (name) *name = kInsts[idx[cfg]].name;
@@ -464,7 +482,7 @@ int pwdw_configs(int N, int H, int W, int OH, int OW, int S, int pt, int pl, int
 hipError_t launch_pwdw(const PwDwParams &p, int cfg, hipStream_t st) {
     int idx[kNumInsts];
     PwDwGeom geo[kNumInsts];
-    const int n = applicable(p.N, p.H, p.W, p.OH, p.OW, p.S, p.pt, p.pl, p.ksp, idx, geo);
+    const int n = applicable(p.N, p.H, p.W, p.OH, p.OW, p.S, p.pt, p.pl, p.ksp, p.nb16, idx, geo);
     if (cfg < 0 || cfg >= n || p.M != p.N * p.H * p.W || p.ksp % 4 != 0 || p.nb16 <= 0) return hipErrorInvalidValue;
     const PwDwGeom &g = geo[cfg];
     PwDwParams q = p;

@@ -9,8 +9,8 @@ the unfused plan must agree bit for bit.  Every case is also held to the
 oracle at the chained-layer bound.  Shapes cover both strides, TF-SAME and
 symmetric padding, whole-image tiles (several images per tile, ragged last
 tile) and row bands (every v1 band shape, odd planes with a short last band),
-partial channel tiles (v2's 96 and 144 channels), K tails and single
-slices, and batch 1.
+partial channel tiles (v2's 96 and 144 channels), channel counts that end in
+half a 16-channel block, K tails and single slices, and batch 1.
 """
 import numpy as np
 import pytest
@@ -33,6 +33,11 @@ CASES = [
     (2, 16, 16, 64, 64, 2, (1, 1, 1, 1), ACT_RELU6),  # symmetric padding at stride 2
     (1, 15, 15, 8, 64, 1, None, ACT_RELU6),         # 15 x 15 (widest row at stride 1), one K slice, batch 1
     (7, 4, 4, 32, 192, 1, None, ACT_RELU6),         # 16 images per tile
+    # batch 1 at v1's 14 x 14 and 7 x 7 layers (16- and 32-channel image tiles)
+    (1, 14, 14, 512, 512, 1, None, ACT_RELU6),      # v1 pw7 -> dw8
+    (1, 14, 14, 512, 512, 2, None, ACT_RELU6),      # v1 pw11 -> dw12
+    (1, 7, 7, 512, 1024, 1, None, ACT_RELU6),       # v1 pw12 -> dw13
+    (1, 14, 14, 160, 120, 1, None, ACT_NONE),       # 15 slices: last tile one slice short, K tail
     # row bands (a halo row computed by both neighbouring bands)
     (3, 112, 112, 32, 64, 2, None, ACT_RELU6),      # v1 pw1 -> dw2
     (2, 56, 56, 64, 128, 1, None, ACT_RELU6),       # v1 pw2 -> dw3
@@ -43,6 +48,7 @@ CASES = [
     (2, 112, 112, 16, 96, 2, None, ACT_RELU6),      # v2 expansion at 112, 6 blocks
     (2, 27, 29, 40, 80, 1, None, ACT_NONE),         # odd plane, last band short, K tail
     (2, 55, 53, 24, 64, 2, (1, 1, 1, 1), ACT_RELU6),  # odd plane at stride 2, symmetric padding
+    (2, 28, 28, 40, 72, 1, None, ACT_RELU6),        # 9 output slices in bands (channels = 8 mod 16)
 ]
 
 
