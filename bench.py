@@ -196,6 +196,13 @@ def node_work(desc, nodes, shapes, i):
     elif kind == "softmax":
         flops = 3.0 * elems(t)
         byts = elems(t) * 8
+    elif kind == "fc_softmax":
+        # FC input and weights in, probabilities out (the logits pass between
+        # the FC and the softmax inside one launch)
+        fop = ops[head_of(op["in"])]
+        n = shapes[t][0]
+        flops = 2.0 * fop["w"].size * n + 3.0 * elems(t)
+        byts = elems(fop["in"]) * 2 + fop["w"].size * 2 + fop["b"].size * 4 + elems(t) * 4
     else:
         ins = op_inputs(op)
         flops = float(elems(t))

@@ -125,6 +125,14 @@ typedef struct {
                             its output: the means are written directly, bit-identical to the
                             two operators.  0, 1 (default) or 2 as for fuse_pwdw.  Needs
                             fuse = 1. */
+    int fuse_softmax;    /* the same for a fully connected layer and the softmax that alone
+                            reads its logits: the workgroup that completes a tile of rows
+                            last runs their softmax, bit-identical to the two operators.  Its
+                            arrival counters live in the workspace past the arena, zeroed by
+                            mgi_plan_bind and left at zero by every run.  The fused kernel is
+                            the default configuration for at most 16 rows (the two kernels
+                            above that), the other one an autotune candidate.  0 or 1
+                            (default).  Needs fuse = 1. */
 } mgi_options;
 
 /* ---------------------------------------------------------------------------

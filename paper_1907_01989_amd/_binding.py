@@ -36,7 +36,8 @@ class Options(ctypes.Structure):
                 ("fuse_dwpw", ctypes.c_int),
                 ("fuse_pwdw", ctypes.c_int),
                 ("fuse_stemdw", ctypes.c_int),
-                ("fuse_pool", ctypes.c_int)]
+                ("fuse_pool", ctypes.c_int),
+                ("fuse_softmax", ctypes.c_int)]
 
 
 _lib = None

@@ -1,6 +1,7 @@
 // Device-side helpers shared by the HIP kernels (gfx950).
 #pragma once
 
+#include <cfloat>
 #include <cmath>
 #include <cstdint>
 
@@ -329,6 +330,62 @@ __device__ __forceinline__ void store_tile_c8(const GemmParams &p, const f4 (&ac
         }
         ((h8 *)p.y)[off] = E::pack(v);
     }
+}
+
+// Softmax of one fp32 row of `cols` values by one wave: up to 1024 columns
+// are held in registers (16 per lane, all loads issued at once; columns past
+// the end repeat the last one, which leaves the max unchanged and is kept out
+// of the sum), longer rows take a looped path; max and sum reduce by a fixed
+// butterfly.  The standalone softmax kernel and the FC kernel's fused softmax
+// both use it, so the two forms round alike.  softmax_load / softmax_finish
+// are its two halves for rows of at most kSoftmaxRegCols columns (a caller
+// may load several rows before finishing any).
+constexpr int kSoftmaxPer = 16, kSoftmaxRegCols = 64 * kSoftmaxPer;
+__device__ inline void softmax_load(const float *zr, int cols, int lane, float (&v)[kSoftmaxPer]) {
+#pragma unroll
+    for (int i = 0; i < kSoftmaxPer; ++i) v[i] = zr[min(lane + 64 * i, cols - 1)];
+}
+__device__ inline void softmax_finish(float (&v)[kSoftmaxPer], float *yr, int cols, int lane) {
+    constexpr int PER = kSoftmaxPer;
+    float m = -FLT_MAX;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) m = fmaxf(m, v[i]);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, 64));
+    float s = 0.0f;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+        v[i] = expf(v[i] - m);
+        s += lane + 64 * i < cols ? v[i] : 0.0f;
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
+    const float inv = 1.0f / s;
+#pragma unroll
+    for (int i = 0; i < PER; ++i)
+        if (lane + 64 * i < cols) yr[lane + 64 * i] = v[i] * inv;
+}
+__device__ inline void softmax_row(const float *zr, float *yr, int cols, int lane) {
+    if (cols <= kSoftmaxRegCols) {
+        float v[kSoftmaxPer];
+        softmax_load(zr, cols, lane, v);
+        softmax_finish(v, yr, cols, lane);
+        return;
+    }
+    float m = -FLT_MAX;
+    for (int j = lane; j < cols; j += 64) m = fmaxf(m, zr[j]);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, 64));
+    float s = 0.0f;
+    for (int j = lane; j < cols; j += 64) {
+        const float e = expf(zr[j] - m);
+        yr[j] = e;
+        s += e;
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
+    const float inv = 1.0f / s;
+    for (int j = lane; j < cols; j += 64) yr[j] *= inv;
 }
 
 }  // namespace kern

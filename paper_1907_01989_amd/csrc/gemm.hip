@@ -588,8 +588,19 @@ hipError_t launch_gemm_pipe(const GemmParams &p, int bm, int bn, hipStream_t st)
 // images and splits K over its 4 waves; each wave loads B K-steps of weight
 // and activation fragments at once, straight from global memory, and the four
 // fp32 partial tiles are summed through LDS in a fixed wave order.
+// With SM, the softmax of the rows follows in the same launch: every
+// workgroup publishes its logits (device-scope release fences) and counts
+// itself in on its row tile's counter; the one that arrives last (the
+// p.nb16-th) takes the acquire fence -- only it, so the others keep their
+// cached weights -- puts the counter back to zero for the next launch and
+// runs the softmax of the tile's rows with the standalone kernel's row
+// routine.  No workgroup waits for another.
 // ---------------------------------------------------------------------------
-template <typename E, int FM, int B>
+// s_waitcnt immediate that waits for every outstanding vector memory
+// operation of the wave (vmcnt 0; expcnt and lgkmcnt left at their maxima)
+constexpr int kWaitVmcnt0 = 0x0F70;
+
+template <typename E, int FM, int B, bool SM>
 __global__ __launch_bounds__(256) void fc_kernel(GemmParams p) {
     __shared__ f4 red[4][FM][64];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -636,6 +647,42 @@ __global__ __launch_bounds__(256) void fc_kernel(GemmParams p) {
         for (int r = 0; r < 4; ++r)
             if (nbase + r < p.cout) y[nbase + r] = act_apply(v[r] + p.bias[nbase + r], p.act1);
     }
+    if constexpr (SM) {
+        __shared__ int last;
+        // each wave waits for its logit stores to complete in the L2 (a
+        // workgroup barrier alone does not wait for them); after the barrier
+        // one release fence writes the L2 back for the whole workgroup, then
+        // one arrival per workgroup
+        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+            last = atomicAdd(p.sm_cnt + mt, 1) == p.nb16 - 1;
+        }
+        __syncthreads();
+        if (!last) return;
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");         // every logit of the tile is visible
+        if (threadIdx.x == 0) atomicExch(p.sm_cnt + mt, 0);        // (every access to a counter is atomic)
+        const float *z = (const float *)p.y + (size_t)m0 * p.cout;
+        float *prob = p.sm_y + (size_t)m0 * p.cout;
+        const int rows = min(16 * FM, p.M - m0);
+        if (p.cout <= kSoftmaxRegCols) {
+            // rows wave, wave + 4, ...: a wave loads up to four rows before
+            // finishing any (one memory round trip per four rows)
+            for (int r0 = wave; r0 < rows; r0 += 16) {
+                float v[4][kSoftmaxPer];
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+                    if (r0 + 4 * u < rows) softmax_load(z + (size_t)(r0 + 4 * u) * p.cout, p.cout, lane, v[u]);
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+                    if (r0 + 4 * u < rows) softmax_finish(v[u], prob + (size_t)(r0 + 4 * u) * p.cout, p.cout, lane);
+            }
+        } else {
+            for (int r = wave; r < rows; r += 4)
+                softmax_row(z + (size_t)r * p.cout, prob + (size_t)r * p.cout, p.cout, lane);
+        }
+    }
 }
 
 hipError_t launch_fc(const GemmParams &p, int fm, int kb, hipStream_t st) {
@@ -644,11 +691,15 @@ hipError_t launch_fc(const GemmParams &p, int fm, int kb, hipStream_t st) {
     if (kb <= 0) kb = 4;
     const int mtiles = (p.M + 16 * fm - 1) / (16 * fm);
     const dim3 grid(mtiles * p.nb16), block(256);
-#define MGI_FC_CASE(FM_, KB_)                                                        \
-    if (fm == FM_ && kb == KB_) {                                                     \
-        if (p.bf16) launch((fc_kernel<BF16, FM_, KB_>), grid, block, 0, st, p);       \
-        else launch((fc_kernel<F16, FM_, KB_>), grid, block, 0, st, p);               \
-        return hipGetLastError();                                                     \
+    const bool sm = p.sm_y != nullptr;
+    if (sm && !p.sm_cnt) return hipErrorInvalidValue;
+#define MGI_FC_CASE(FM_, KB_)                                                              \
+    if (fm == FM_ && kb == KB_) {                                                           \
+        if (p.bf16 && sm) launch((fc_kernel<BF16, FM_, KB_, true>), grid, block, 0, st, p);  \
+        else if (p.bf16) launch((fc_kernel<BF16, FM_, KB_, false>), grid, block, 0, st, p);  \
+        else if (sm) launch((fc_kernel<F16, FM_, KB_, true>), grid, block, 0, st, p);        \
+        else launch((fc_kernel<F16, FM_, KB_, false>), grid, block, 0, st, p);               \
+        return hipGetLastError();                                                           \
     }
     MGI_FC_CASE(1, 4) MGI_FC_CASE(2, 4) MGI_FC_CASE(4, 4)
     MGI_FC_CASE(1, 8) MGI_FC_CASE(2, 8) MGI_FC_CASE(4, 8)

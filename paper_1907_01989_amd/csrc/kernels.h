@@ -47,6 +47,11 @@ struct GemmParams {
     int H, W, OH, OW, sin, kw, sh, sw, dh, dw, pt, pl;
     // pooled GEMM: pixels per image, images, images per M-tile (set by the launcher)
     int hw, nimg, ipt;
+    // FC with the softmax of its rows (sm_y non-null): probabilities (M x cout)
+    // and one arrival counter per tile of 16 * fm rows (zero before the launch,
+    // zero after it)
+    float *sm_y;
+    int *sm_cnt;
 };
 hipError_t launch_gemm(const GemmParams &p, int bm, int bn, bool taps, bool f32out,
                        hipStream_t st);
@@ -69,7 +74,9 @@ hipError_t launch_gemm_pipe_k8(const GemmParams &p, bool pool, hipStream_t st);
 hipError_t launch_gemm_pool(const GemmParams &p, int bm, int bn, hipStream_t st);
 // fully-connected layer, fp32 (M x cout) output; K split over the waves; a
 // workgroup takes 16 * fm images (1, 2 or 4; 0 = by M) and loads kb K-steps
-// (4 or 8; 0 = 4) at once.  Results do not depend on fm or kb.
+// (4 or 8; 0 = 4) at once.  Results do not depend on fm or kb.  With
+// p.sm_y set, the softmax of every row follows in the same launch (p.sm_cnt:
+// ceil(M / (16 * fm)) counters, zero on entry and left at zero).
 hipError_t launch_fc(const GemmParams &p, int fm, int kb, hipStream_t st);
 size_t gemm_xs_lds_bytes(int ksp, int wm, int bn);
 

@@ -197,7 +197,7 @@ void add_configs(const mgi_plan &p, Node &nd, size_t M) {
         const Node::Config split{GemmTile{}, 4, "split", true, 0};
         nd.cfgs.insert(nd.fused_default ? nd.cfgs.end() : nd.cfgs.begin(), Node::Config(split));
         nd.apply(0);
-    } else if (nd.kind == NodeKind::FC) {
+    } else if (nd.kind == NodeKind::FC || nd.kind == NodeKind::FcSoftmax) {
         // images per workgroup (16 * fm) and K-steps per load batch; 16 images
         // and 8 steps first (the most workgroups, one load latency per wave:
         // fastest on v1 b64, 5.6 us against 8.2 us for 64 images and 4 steps)
@@ -212,6 +212,18 @@ void add_configs(const mgi_plan &p, Node &nd, size_t M) {
             t.wm = o[0];
             t.pf = o[1];
             nd.cfgs.push_back({t, 0, "fc" + std::to_string(16 * o[0]) + "k" + std::to_string(o[1])});
+        }
+        if (nd.kind == NodeKind::FcSoftmax) {
+            // FC into the logits, then the softmax kernel: first when there
+            // is more than one tile of 16 rows (each arriving workgroup's L2
+            // write-back costs more than the softmax launch it saves once
+            // the grid has a few hundred workgroups: 16.1 us fused against
+            // 10.6 us split for 64 rows of 1000 classes, 7.2 against 9.6 us
+            // for one row)
+            Node::Config split = nd.cfgs[0];
+            split.name = "split_" + split.name;
+            split.split = true;
+            nd.cfgs.insert(M > 16 ? nd.cfgs.begin() : nd.cfgs.end(), split);
         }
         nd.apply(0);
     } else if (nd.kind == NodeKind::GemmPool) {
@@ -450,6 +462,43 @@ void fuse_pool_into_pw(mgi_plan &p, bool always) {
     p.nodes.swap(kept);
 }
 
+// FC -> softmax fusion: a softmax whose input is the logits of an FC node and
+// nothing else reads them joins that node; the FC kernel's workgroups count
+// themselves in per row tile and the last one runs the tile's softmax.  The
+// logits stay planned as the node's scratch (written, then read by the last
+// workgroup; the split form runs the softmax kernel over them), or stay in
+// the caller's buffer when they are a graph output themselves.
+void fuse_softmax_into_fc(mgi_plan &p) {
+    std::vector<int> readers(p.bufs.size(), 0), producer(p.bufs.size(), -1);
+    for (size_t i = 0; i < p.nodes.size(); ++i) {
+        const Node &nd = p.nodes[i];
+        for (int b : nd.in) readers[b]++;
+        if (nd.residual >= 0) readers[nd.residual]++;
+        producer[nd.out] = (int)i;
+    }
+    std::vector<char> drop(p.nodes.size(), 0);
+    for (size_t i = 0; i < p.nodes.size(); ++i) {
+        const Node &sm = p.nodes[i];
+        if (sm.kind != NodeKind::Softmax || sm.in.size() != 1) continue;
+        const int mid = sm.in[0];
+        const Loc loc = p.bufs[mid].loc;
+        if (readers[mid] != 1 || (loc != Loc::Arena && loc != Loc::Output) || producer[mid] < 0) continue;
+        Node &fc = p.nodes[producer[mid]];
+        if (fc.kind != NodeKind::FC) continue;
+        fc.kind = NodeKind::FcSoftmax;
+        fc.kname = "fc_softmax";
+        fc.out = sm.out;
+        fc.out_tensor = sm.out_tensor;
+        fc.n_fused += sm.n_fused;
+        fc.scratch = mid;
+        drop[i] = 1;
+    }
+    std::vector<Node> kept;
+    for (size_t i = 0; i < p.nodes.size(); ++i)
+        if (!drop[i]) kept.push_back(std::move(p.nodes[i]));
+    p.nodes.swap(kept);
+}
+
 void pick_pipe_tile(GemmTile &t, size_t M, int npad) {
     const int cand[3][2] = {{128, 128}, {128, 64}, {64, 64}};
     size_t best_tiles = 0;
@@ -567,6 +616,8 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
         return fail(MGI_ERR_INVALID_ARG, "mgi_graph_finalize: fuse_stemdw is 0, 1 or 2");
     if (o.fuse_pool < 0 || o.fuse_pool > 2)
         return fail(MGI_ERR_INVALID_ARG, "mgi_graph_finalize: fuse_pool is 0, 1 or 2");
+    if (o.fuse_softmax < 0 || o.fuse_softmax > 1)
+        return fail(MGI_ERR_INVALID_ARG, "mgi_graph_finalize: fuse_softmax is 0 or 1");
     auto to_bits = o.dtype == MGI_DTYPE_BF16 ? f32_to_bf16_bits : f32_to_f16_bits;
 
     const std::vector<char> live = live_ops(g);
@@ -965,6 +1016,7 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
     if (o.fuse && o.fuse_pwdw) fuse_pw_into_dw(p, o.fuse_pwdw == 2);
     if (o.fuse && o.fuse_stemdw) fuse_stem_into_dw(p, o.fuse_stemdw == 2);
     if (o.fuse && o.fuse_pool) fuse_pool_into_pw(p, o.fuse_pool == 2);
+    if (o.fuse && o.fuse_softmax) fuse_softmax_into_fc(p);
     if (o.fuse && o.fuse_dwpw) fuse_dw_into_pw(p);
     for (Node &nd : p.nodes) add_configs(p, nd, p.bufs[nd.out].shape.pixels());
 
@@ -1004,8 +1056,18 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
         off = align256(off + pr.object_size[k]);
     }
     p.n_objects = (int)pr.object_size.size();
-    p.workspace_bytes = std::max<size_t>(off, 256);
     for (size_t i = 0; i < arena.size(); ++i) p.bufs[arena[i]].offset = obj_off[pr.object_of[i]];
+    // state region: arrival counters of fused FC -> softmax nodes, one per
+    // tile of 16 rows (the finest row tiling of the FC kernel)
+    p.state_off = off;
+    size_t state = 0;
+    for (Node &nd : p.nodes) {
+        if (nd.kind != NodeKind::FcSoftmax) continue;
+        nd.cnt_off = p.state_off + state;
+        state = align256(state + ((p.bufs[nd.out].shape.pixels() + 15) / 16) * sizeof(int));
+    }
+    p.state_bytes = state;
+    p.workspace_bytes = std::max<size_t>(p.state_off + state, 256);
 
     // --------------------------------------------------------------- packing
     // GEMM weights (A operand of v_mfma_f32_16x16x32_f16): for output block nb
@@ -1053,12 +1115,13 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
         }
         if (nd.kind == NodeKind::Gemm || nd.kind == NodeKind::Stem || nd.kind == NodeKind::FC ||
             nd.kind == NodeKind::DwPw || nd.kind == NodeKind::PwDw || nd.kind == NodeKind::StemDw ||
-            nd.kind == NodeKind::GemmPool) {
+            nd.kind == NodeKind::GemmPool || nd.kind == NodeKind::FcSoftmax) {
             const Shape x = g.ops[op.in[0]].out;
             const int cin = x.c;
-            const int cout = nd.kind == NodeKind::FC ? op.cout : op.conv.cout;
-            const int kh = nd.kind == NodeKind::FC ? 1 : op.conv.kh;
-            const int kw = nd.kind == NodeKind::FC ? 1 : op.conv.kw;
+            const bool fc = nd.kind == NodeKind::FC || nd.kind == NodeKind::FcSoftmax;
+            const int cout = fc ? op.cout : op.conv.cout;
+            const int kh = fc ? 1 : op.conv.kh;
+            const int kw = fc ? 1 : op.conv.kw;
             const int sin = slices(cin);
             nd.w_bytes = (size_t)nd.nb16 * nd.ksp * 16 * 8 * 2;
             nd.w_off = reserve(nd.w_bytes);

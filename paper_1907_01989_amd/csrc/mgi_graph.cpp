@@ -330,4 +330,5 @@ extern "C" void mgi_options_default(mgi_options *o) {
     o->fuse_pwdw = 1;
     o->fuse_stemdw = 1;
     o->fuse_pool = 1;
+    o->fuse_softmax = 1;
 }

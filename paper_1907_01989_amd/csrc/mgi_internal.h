@@ -74,7 +74,7 @@ struct Buf {
 
 enum class NodeKind {
     Ingest, Stem, Gemm, Depthwise, Add, Act, Gap, FC, Softmax, Concat, Resize, Argmax,
-    ResizeArgmax, Export, Pad, DwPw, PwDw, StemDw, GemmPool
+    ResizeArgmax, Export, Pad, DwPw, PwDw, StemDw, GemmPool, FcSoftmax
 };
 
 // Tile shape of the MFMA GEMM (pointwise, implicit-GEMM convolution, FC).
@@ -130,6 +130,8 @@ struct Node {
     bool fused_default = true;
     int pwdw_cfg = 0;       // PwDw / StemDw: configuration of the fused kernel (pwdw_configs,
                             // stemdw_configs)
+    size_t cnt_off = 0;     // FcSoftmax: its row-tile arrival counters in the workspace's
+                            // state region
     struct Config {
         GemmTile tile;
         int dw_rows = 0;
@@ -162,6 +164,10 @@ struct mgi_plan {
     size_t weight_bytes = 0;
     size_t zero_off = 0;           // offset of a zeroed 256-byte block in the weight blob
     size_t workspace_bytes = 0;
+    // state region of the workspace, past the arena (never shared by the
+    // planner): zeroed by mgi_plan_bind; kernels that keep counters there leave
+    // them at zero when they finish
+    size_t state_off = 0, state_bytes = 0;
     size_t mem_naive = 0, mem_planned = 0;
     int n_objects = 0;
     mgi_options opt{};

@@ -94,6 +94,38 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
             q.act1 = nd.act1; q.act2 = nd.act2;
             return launch_stem(q, ib.in_dtype == MGI_DTYPE_FP16, st);
         }
+        case NodeKind::FcSoftmax: {
+            // FC + softmax: one FC launch whose last workgroup per row tile
+            // runs the softmax, or (split) the FC into the logits scratch and
+            // the softmax kernel
+            const Shape lg = p.bufs[nd.scratch].shape;
+            float *logits = (float *)buf_ptr(p, nd.scratch, B);
+            GemmParams q{};
+            q.bf16 = bf;
+            q.x = (const h8 *)buf_ptr(p, nd.in[0], B);
+            q.w = (const h8 *)(wbase + nd.w_off);
+            q.bias = (const float *)(wbase + nd.b_off);
+            q.y = logits;
+            q.M = (int)lg.pixels();
+            q.Min = (int)p.bufs[nd.in[0]].shape.pixels();
+            q.ksl = nd.ksl; q.ksp = nd.ksp;
+            q.nb16 = nd.nb16; q.ns = slices(lg.c); q.cout = lg.c;
+            q.act1 = nd.act1; q.act2 = nd.act2;
+            if (!nd.split) {
+                q.sm_y = (float *)y;
+                q.sm_cnt = (int *)(B.ws + nd.cnt_off);
+                return launch_fc(q, nd.tile.wm, nd.tile.pf, st);
+            }
+            LaunchEvents &ev = launch_events();
+            const LaunchEvents saved = ev;
+            ev.stop = nullptr;
+            hipError_t e = launch_fc(q, nd.tile.wm, nd.tile.pf, st);
+            ev.start = nullptr;
+            ev.stop = saved.stop;
+            if (e == hipSuccess) e = launch_softmax(logits, (float *)y, q.M, q.cout, st);
+            ev = saved;
+            return e;
+        }
         case NodeKind::Gemm:
         case NodeKind::FC: {
             const Buf &ib = p.bufs[nd.in[0]];
@@ -384,6 +416,12 @@ extern "C" mgi_status mgi_plan_bind(mgi_plan *p, void *dev_workspace, void *dev_
         if (e != hipSuccess) return hip_fail(e, "mgi_plan_bind: weight upload");
         e = hipStreamSynchronize(st);
         if (e != hipSuccess) return hip_fail(e, "mgi_plan_bind: weight upload");
+    }
+    if (p->state_bytes) {   // counters start at zero; runs leave them at zero
+        hipError_t e = hipMemsetAsync(static_cast<char *>(dev_workspace) + p->state_off, 0,
+                                      p->state_bytes, st);
+        if (e == hipSuccess) e = hipStreamSynchronize(st);
+        if (e != hipSuccess) return hip_fail(e, "mgi_plan_bind: state region");
     }
     std::vector<uint8_t>().swap(p->weights);
     p->dev_ws = dev_workspace;

@@ -327,55 +327,13 @@ hipError_t launch_gap(const h8 *x, h8 *y, const h8 *zero, int N, int HW, int S, 
 }
 
 // ---------------------------------------------------------------------------
-// softmax over rows of an fp32 (rows x cols) array; one wave per row.  The
-// row is held in registers (up to 16 values per lane, all loads issued at
-// once; columns past the end repeat the last column, which leaves the max
-// unchanged and is masked out of the sum); max and sum use a fixed butterfly.
-// Longer rows take a looped path.
+// softmax over rows of an fp32 (rows x cols) array; one wave per row
+// (softmax_row)
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void softmax_kernel(const float *z, float *y, int rows, int cols) {
-    constexpr int PER = 16;
-    const int lane = threadIdx.x & 63;
     const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
     if (row >= rows) return;  // whole wave
-    const float *zr = z + (size_t)row * cols;
-    float *yr = y + (size_t)row * cols;
-    float m = -FLT_MAX;
-    if (cols <= 64 * PER) {
-        float v[PER];
-#pragma unroll
-        for (int i = 0; i < PER; ++i) v[i] = zr[min(lane + 64 * i, cols - 1)];
-#pragma unroll
-        for (int i = 0; i < PER; ++i) m = fmaxf(m, v[i]);
-#pragma unroll
-        for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, 64));
-        float s = 0.0f;
-#pragma unroll
-        for (int i = 0; i < PER; ++i) {
-            v[i] = expf(v[i] - m);
-            s += lane + 64 * i < cols ? v[i] : 0.0f;
-        }
-#pragma unroll
-        for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
-        const float inv = 1.0f / s;
-#pragma unroll
-        for (int i = 0; i < PER; ++i)
-            if (lane + 64 * i < cols) yr[lane + 64 * i] = v[i] * inv;
-        return;
-    }
-    for (int j = lane; j < cols; j += 64) m = fmaxf(m, zr[j]);
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, 64));
-    float s = 0.0f;
-    for (int j = lane; j < cols; j += 64) {
-        const float e = expf(zr[j] - m);
-        yr[j] = e;
-        s += e;
-    }
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
-    const float inv = 1.0f / s;
-    for (int j = lane; j < cols; j += 64) yr[j] *= inv;
+    softmax_row(z + (size_t)row * cols, y + (size_t)row * cols, cols, threadIdx.x & 63);
 }
 
 hipError_t launch_softmax(const float *z, float *y, int rows, int cols, hipStream_t st) {

@@ -69,7 +69,7 @@ def build_graph(desc):
 
 
 def options(planner=B.PLANNER_GREEDY, fuse=True, materialize_all=False, fuse_dwpw=False,
-            dtype=B.DTYPE_FP16, fuse_pwdw=True, fuse_stemdw=True, fuse_pool=True):
+            dtype=B.DTYPE_FP16, fuse_pwdw=True, fuse_stemdw=True, fuse_pool=True, fuse_softmax=True):
     o = B.mgi_options_default()
     o.dtype = dtype
     o.planner = planner
@@ -79,6 +79,7 @@ def options(planner=B.PLANNER_GREEDY, fuse=True, materialize_all=False, fuse_dwp
     o.fuse_pwdw = int(fuse_pwdw)     # False/True or 2 (fuse regardless of workgroup count)
     o.fuse_stemdw = int(fuse_stemdw)  # likewise
     o.fuse_pool = int(fuse_pool)      # likewise
+    o.fuse_softmax = int(fuse_softmax)
     return o
 
 
@@ -87,13 +88,13 @@ class Plan:
 
     def __init__(self, desc, planner=B.PLANNER_GREEDY, fuse=True, materialize_all=False,
                  device="cuda:0", bind=True, fuse_dwpw=False, dtype=B.DTYPE_FP16, fuse_pwdw=True,
-                 fuse_stemdw=True, fuse_pool=True):
+                 fuse_stemdw=True, fuse_pool=True, fuse_softmax=True):
         self.desc = desc
         g = build_graph(desc)
         try:
             self.handle = B.mgi_graph_finalize(
                 g, options(planner, fuse, materialize_all, fuse_dwpw, dtype, fuse_pwdw, fuse_stemdw,
-                           fuse_pool))
+                           fuse_pool, fuse_softmax))
         finally:
             B.mgi_graph_destroy(g)
         self.device = device

@@ -110,12 +110,14 @@ def test_finalize_state_errors_and_run_before_bind():
 
 
 def test_fusion_structure():
-    v1 = engine.Plan(workloads.mobilenet_v1(1), bind=False, fuse_pwdw=False, fuse_stemdw=False, fuse_pool=False)
+    v1 = engine.Plan(workloads.mobilenet_v1(1), bind=False, fuse_pwdw=False, fuse_stemdw=False, fuse_pool=False,
+                     fuse_softmax=False)
     kinds = [n["kind"] for n in v1.nodes()]
     assert kinds[0] == "conv_stem" and kinds.count("dw_conv") == 13 and kinds.count("pw_gemm") == 13
     assert kinds[-3:] == ["global_avgpool", "fc_gemm", "softmax"]
     assert len(kinds) == 30
-    v2 = engine.Plan(workloads.mobilenet_v2(1), bind=False, fuse_pwdw=False, fuse_stemdw=False, fuse_pool=False)
+    v2 = engine.Plan(workloads.mobilenet_v2(1), bind=False, fuse_pwdw=False, fuse_stemdw=False, fuse_pool=False,
+                     fuse_softmax=False)
     nodes = v2.nodes()
     assert sum(1 for n in nodes if n["n_fused"] == 2) == 10      # residual adds absorbed
     assert not any(n["kind"] == "add" for n in nodes)
@@ -128,17 +130,23 @@ def test_fusion_structure():
 def test_pointwise_depthwise_fusion_structure():
     # v1: pw1..pw12 each feed one depthwise convolution (whole-image tiles on
     # 14x14 and 7x7 planes, row bands on 112..28); dw1 reads the stem (fused
-    # with it), pw13 feeds the pooling
+    # with it), pw13 feeds the pooling (fused with it), the FC feeds the
+    # softmax (fused with it; the logits are a graph output as well)
     v1 = engine.Plan(workloads.mobilenet_v1(64), bind=False)
     nodes = v1.nodes()
     kinds = [n["kind"] for n in nodes]
     assert kinds.count("pw_dw") == 12 and kinds.count("stem_dw") == 1 and kinds.count("pw_pool") == 1
     assert kinds[0] == "stem_dw" and "dw_conv" not in kinds and "conv_stem" not in kinds
-    assert kinds[-3:] == ["pw_pool", "fc_gemm", "softmax"] and len(kinds) == 16
+    assert kinds[-2:] == ["pw_pool", "fc_softmax"] and len(kinds) == 15
     k_nostem = [n["kind"] for n in engine.Plan(workloads.mobilenet_v1(64), bind=False, fuse_stemdw=False).nodes()]
-    assert k_nostem[:2] == ["conv_stem", "dw_conv"] and len(k_nostem) == 17
+    assert k_nostem[:2] == ["conv_stem", "dw_conv"] and len(k_nostem) == 16
     k_nopool = [n["kind"] for n in engine.Plan(workloads.mobilenet_v1(64), bind=False, fuse_pool=False).nodes()]
-    assert k_nopool[-4:] == ["pw_gemm", "global_avgpool", "fc_gemm", "softmax"] and len(k_nopool) == 17
+    assert k_nopool[-3:] == ["pw_gemm", "global_avgpool", "fc_softmax"] and len(k_nopool) == 16
+    k_nosm = [n["kind"] for n in engine.Plan(workloads.mobilenet_v1(64), bind=False, fuse_softmax=False).nodes()]
+    assert k_nosm[-3:] == ["pw_pool", "fc_gemm", "softmax"] and len(k_nosm) == 16
+    # the fused node produces the probabilities; the logits output keeps its buffer
+    k_nologits = engine.Plan(workloads.mobilenet_v1(64, logits_output=False), bind=False)
+    assert [n["kind"] for n in k_nologits.nodes()][-1] == "fc_softmax" and k_nologits.n_outputs == 1
     for n in nodes:
         if n["kind"] == "pw_dw":
             assert n["n_fused"] == 2
@@ -161,7 +169,7 @@ def test_pointwise_depthwise_fusion_structure():
     b1fc = [c for n, c in zip(b1f.nodes(), b1f.node_configs()) if n["kind"] == "pw_dw"]
     assert len(b1fc) == 12 and all(name.startswith(("img", "band")) for _, _, name in b1fc)
     for o in (engine.options(fuse_pwdw=3), engine.options(fuse_stemdw=3), engine.options(fuse_stemdw=-1),
-              engine.options(fuse_pool=3)):
+              engine.options(fuse_pool=3), engine.options(fuse_softmax=2)):
         g = engine.build_graph(workloads.mobilenet_v1(1))
         try:
             assert err(B.mgi_graph_finalize, g, o) == 1
@@ -282,6 +290,8 @@ def test_node_configuration_candidates():
             assert 5 <= k <= 6 and name.startswith(("pool", "split"))
         elif n["kind"] == "fc_gemm":
             assert k >= 1 and name.startswith("fc")
+        elif n["kind"] == "fc_softmax":
+            assert k >= 2 and name.startswith("fc")
         else:
             assert k == 1
     i = next(j for j, n in enumerate(nodes) if n["kind"] == "pw_gemm")
