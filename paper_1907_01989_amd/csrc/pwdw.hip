@@ -360,6 +360,10 @@ const Inst kInsts[] = {
     // K loop waits on the memory latency, not on the matrix cores)
     {false, 8, 2, 1, 1, 2, 16, 8, "img16p8"},    {false, 8, 2, 1, 1, 2, 8, 8, "img16p8"},      // 14 x 14, 7 x 7
     {false, 8, 2, 1, 2, 2, 8, 8, "img16p8"},                                                   // 14 -> 7
+    // 16-channel bands for small batches
+    {true, 4, 9, 1, 2, 2, 64, 1, "band2x16w4"},  {true, 4, 4, 1, 1, 2, 64, 2, "band2x16w4"},   // 112 -> 56, 56 x 56
+    {true, 4, 5, 1, 2, 2, 32, 2, "band2x16w4"},  {true, 4, 3, 1, 1, 4, 32, 4, "band4x16w4"},   // 56 -> 28, 28 x 28
+    {true, 4, 3, 1, 2, 2, 16, 4, "band2x16w4"},                                                // 28 -> 14
 };
 constexpr int kNumInsts = sizeof(kInsts) / sizeof(kInsts[0]);
 
@@ -403,6 +407,9 @@ bool fits(const Inst &in, int N, int H, int W, int OH, int OW, int S, int pt, in
         g->nbands = (OH + in.r - 1) / in.r;
         g->groups = N * g->nbands;
         g->pstride = rows * W;
+        // 16-channel bands: for shapes whose 64-channel bands leave most
+        // compute units idle, as the small image tiles
+        if (in.nbt == 1 && g->groups * ((nb16 + 3) / 4) >= 128) return false;
     }
     g->nbt = in.nbt;
     g->lds = lds_bytes(in, ksp, g->pstride);
@@ -447,6 +454,9 @@ hipError_t launch_inst(int k, const PwDwParams &p, size_t lds, hipStream_t st) {
         MGI_PWDW(37, 8, 2, 1, 2, 2, 8, 4) MGI_PWDW(38, 8, 2, 2, 2, 2, 8, 4)
         MGI_PWDW(39, 8, 2, 1, 1, 2, 16, 8) MGI_PWDW(40, 8, 2, 1, 1, 2, 8, 8)
         MGI_PWDW(41, 8, 2, 1, 2, 2, 8, 8)
+        MGI_PWDW(42, 4, 9, 1, 2, 2, 64, 1) MGI_PWDW(43, 4, 4, 1, 1, 2, 64, 2)
+        MGI_PWDW(44, 4, 5, 1, 2, 2, 32, 2) MGI_PWDW(45, 4, 3, 1, 1, 4, 32, 4)
+        MGI_PWDW(46, 4, 3, 1, 2, 2, 16, 4)
 #undef MGI_PWDW
     }
     return hipErrorInvalidValue;
