@@ -203,6 +203,14 @@ def node_work(desc, nodes, shapes, i):
         n = shapes[t][0]
         flops = 2.0 * fop["w"].size * n + 3.0 * elems(t)
         byts = elems(fop["in"]) * 2 + fop["w"].size * 2 + fop["b"].size * 4 + elems(t) * 4
+    elif kind == "resize_argmax":
+        # the logits in (fp16), int32 labels out; the upsampled logits never
+        # reach memory
+        src = ops[op["in"]]["in"]
+        n, h_, w_, _ = shapes[t]
+        c = shapes[src][3]
+        flops = float(n * h_ * w_) * c * 8.0
+        byts = elems(src) * 2 + n * h_ * w_ * 4
     else:
         ins = op_inputs(op)
         flops = float(elems(t))
