@@ -241,33 +241,46 @@ hipError_t launch_act(const h8 *x, h8 *y, size_t count, int act, bool bf16, hipS
 }
 
 // ---------------------------------------------------------------------------
-// global average pool: one wave per (slice, image); lanes stride over the
-// pixels, then a fixed butterfly reduction (deterministic).  Output is the
-// sliced (n, 1, 1, c) tensor in fp16.
+// global average pool: one 256-thread workgroup per (slice, image); thread t
+// sums pixels t, t + 256, ... four loads at a time (all issued before any
+// add; pixels past the end read the zero element), then a fixed butterfly in
+// each wave and the four wave sums in a fixed order (deterministic).  Output
+// is the sliced (n, 1, 1, c) tensor in the storage type.
 // ---------------------------------------------------------------------------
 template <typename E>
-__global__ __launch_bounds__(256) void gap_kernel(const h8 *x, h8 *y, int N, int HW, int S) {
-    const int lane = threadIdx.x & 63;
-    const int idx = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (idx >= S * N) return;  // whole wave exits together
-    const h8 *xin = x + (size_t)idx * HW;
+__global__ __launch_bounds__(256) void gap_kernel(const h8 *x, h8 *y, const h8 *zero, int HW) {
+    __shared__ float part[4][8];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const h8 *xin = x + (size_t)blockIdx.x * HW;
     float acc[8];
 #pragma unroll
     for (int c = 0; c < 8; ++c) acc[c] = 0.0f;
-    for (int p = lane; p < HW; p += 64) {
-        const h8 v = xin[p];
+    for (int p0 = 0; p0 < HW; p0 += 4 * 256) {
+        h8 v[4];
 #pragma unroll
-        for (int c = 0; c < 8; ++c) acc[c] += E::get(v, c);
+        for (int u = 0; u < 4; ++u) {
+            const int px = p0 + u * 256 + tid;
+            v[u] = *(px < HW ? xin + px : zero);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+            for (int c = 0; c < 8; ++c) acc[c] += E::get(v[u], c);
     }
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1)
 #pragma unroll
         for (int c = 0; c < 8; ++c) acc[c] += __shfl_xor(acc[c], off, 64);
-    if (lane == 0) {
-        const float inv = 1.0f / (float)HW;
+    if (lane == 0)
 #pragma unroll
-        for (int c = 0; c < 8; ++c) acc[c] *= inv;
-        y[idx] = E::pack(acc);
+        for (int c = 0; c < 8; ++c) part[wave][c] = acc[c];
+    __syncthreads();
+    if (tid == 0) {
+        const float inv = 1.0f / (float)HW;
+        float m[8];
+#pragma unroll
+        for (int c = 0; c < 8; ++c) m[c] = ((part[0][c] + part[1][c]) + (part[2][c] + part[3][c])) * inv;
+        y[blockIdx.x] = E::pack(m);
     }
 }
 
@@ -320,8 +333,8 @@ hipError_t launch_gap(const h8 *x, h8 *y, const h8 *zero, int N, int HW, int S, 
             launch(gap_small_kernel<F16>, dim3(blocks_for(planes * 8, 256)), dim3(256), 0, st, x, y, zero,
                    (int)planes, HW);
     } else {
-        if (bf16) launch(gap_kernel<BF16>, dim3(blocks_for(planes, 4)), dim3(256), 0, st, x, y, N, HW, S);
-        else launch(gap_kernel<F16>, dim3(blocks_for(planes, 4)), dim3(256), 0, st, x, y, N, HW, S);
+        if (bf16) launch(gap_kernel<BF16>, dim3((unsigned)planes), dim3(256), 0, st, x, y, zero, HW);
+        else launch(gap_kernel<F16>, dim3((unsigned)planes), dim3(256), 0, st, x, y, zero, HW);
     }
     return hipGetLastError();
 }

@@ -140,7 +140,8 @@ def test_depthwise_activations():
         check_isolated("dw", nodes[y], ref[y])
 
 
-@pytest.mark.parametrize("n,h,w,c", [(2, 7, 7, 40), (1, 33, 33, 320), (1, 1, 1, 8), (64, 7, 7, 1024)])
+@pytest.mark.parametrize("n,h,w,c", [(2, 7, 7, 40), (1, 33, 33, 320), (1, 1, 1, 8), (64, 7, 7, 1024),
+                                      (2, 9, 9, 16), (3, 40, 40, 24)])
 def test_global_avgpool(n, h, w, c):
     g = NetBuilder(seed=1)
     x = sliced(g, g.input(n, h, w, c, -1, 1))
