@@ -227,9 +227,10 @@ void mgi_options_default(mgi_options *o);
 mgi_status mgi_graph_finalize(const mgi_graph *g, const mgi_options *o, mgi_plan **p);
 mgi_status mgi_plan_destroy(mgi_plan *p); /* NULL is accepted */
 
-/* Bytes of device workspace (the arena holding every intermediate tensor)
- * and of packed weights that the caller must allocate for mgi_plan_bind.
- * Both buffers must be 256-byte aligned. */
+/* Bytes of device workspace (the arena holding every intermediate tensor,
+ * then a small state region: the arrival counters of fused FC + softmax
+ * nodes) and of packed weights that the caller must allocate for
+ * mgi_plan_bind.  Both buffers must be 256-byte aligned. */
 mgi_status mgi_plan_workspace_bytes(const mgi_plan *p, size_t *bytes);
 mgi_status mgi_plan_weight_bytes(const mgi_plan *p, size_t *bytes);
 
@@ -246,9 +247,10 @@ mgi_status mgi_plan_num_io(const mgi_plan *p, int *n_inputs, int *n_outputs);
 mgi_status mgi_plan_io_info(const mgi_plan *p, int is_output, int index, int *n, int *h, int *w,
                             int *c, int *dtype, size_t *bytes);
 
-/* Upload packed weights into dev_weights and adopt dev_workspace as the arena.
- * Asynchronous on `stream`; host copies are released once the copy is done
- * with (the call waits for the upload before returning). */
+/* Upload packed weights into dev_weights, adopt dev_workspace as the arena
+ * and zero the workspace's state region (every run leaves it at zero again;
+ * the caller must not write it).  The call waits for both before returning;
+ * host copies of the weights are released once the upload is done with. */
 mgi_status mgi_plan_bind(mgi_plan *p, void *dev_workspace, void *dev_weights, void *stream);
 
 /* ---------------------------------------------------------------------------

@@ -424,3 +424,14 @@ def test_planner_assign_rejects_bad_lifetimes():
     assert err(B.mgi_planner_assign, B.PLANNER_GREEDY, [4, 4], [0, 3], [2, 1]) == 1
     assert err(B.mgi_planner_assign, 7, [4], [0], [1]) == 3
     assert B.mgi_planner_assign(B.PLANNER_GREEDY, [], [], []) == ([], [])
+
+
+def test_softmax_fusion_state_region():
+    # the fused FC + softmax node keeps one arrival counter per 16 rows in a
+    # state region past the arena: the workspace grows by that region (one
+    # 256-byte block for up to 1024 rows), the arena is unchanged
+    for d in (workloads.mobilenet_v1(64), workloads.mobilenet_v1(100, logits_output=False)):
+        fused = engine.Plan(d, bind=False)
+        split = engine.Plan(d, bind=False, fuse_softmax=False)
+        assert fused.nodes()[-1]["kind"] == "fc_softmax" and fused.nodes()[-1]["n_fused"] == 2
+        assert B.mgi_plan_workspace_bytes(fused.handle) == B.mgi_plan_workspace_bytes(split.handle) + 256
