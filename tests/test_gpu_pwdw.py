@@ -94,16 +94,23 @@ def test_fused_pair(n, h, w, K, C, s, pads, act):
     assert ok, msg
 
 
-def test_fused_pair_bf16():
-    from paper_1907_01989_amd import _binding as B
-    desc, y = pair_graph(16, 14, 14, 128, 256, 1, None, ACT_RELU6)
-    log(f"[case] {desc['name']} bf16")
+@pytest.mark.parametrize("n,h,w,K,C,s", [(16, 14, 14, 128, 256, 1),   # image tiles of 16..128 channels
+                                         (1, 56, 56, 64, 128, 1),     # 16..128-channel row bands
+                                         (1, 7, 7, 512, 1024, 1)])    # batch-1 7x7 tiles
+def test_fused_pair_bf16(n, h, w, K, C, s):
+    from paper_1907_01989_amd import engine, _binding as B
+    desc, y = pair_graph(n, h, w, K, C, s, None, ACT_RELU6)
     bdesc = workloads.as_bf16_graph(desc)
-    _, fused, _ = run_gpu(bdesc, materialize_all=False, dtype=B.DTYPE_BF16, fuse_pwdw=2)
+    plan = engine.Plan(bdesc, bind=False, fuse_pwdw=2, dtype=B.DTYPE_BF16)
+    idx = fused_nodes(plan)
+    ncfg = plan.node_configs()[idx[0]][1]
+    log(f"[case] {desc['name']} bf16 ({ncfg} configurations)")
     _, plain, _ = run_gpu(bdesc, materialize_all=False, dtype=B.DTYPE_BF16, fuse_pwdw=False)
-    np.testing.assert_array_equal(fused[0], plain[0])
+    for c in range(ncfg):
+        _, fused, _ = run_gpu(bdesc, materialize_all=False, dtype=B.DTYPE_BF16, fuse_pwdw=2, configs={idx[0]: c})
+        np.testing.assert_array_equal(fused[0], plain[0], err_msg=f"configuration {c}")
     ref = oracle.run_graph(bdesc, keep=[y], store_bf16=True)[y]
-    ok, msg = check_layer("fused bf16 output", fused[0], ref.reshape(fused[0].shape))
+    ok, msg = check_layer("fused bf16 output", plain[0], ref.reshape(plain[0].shape))
     assert ok, msg
 
 
