@@ -94,15 +94,19 @@ def test_counters_return_to_zero():
 
 
 def test_fused_fc_softmax_bf16():
-    from paper_1907_01989_amd import _binding as B
+    from paper_1907_01989_amd import engine, _binding as B
     desc, y = head_graph(20, 1280, 1000)
-    log(f"[case] {desc['name']} bf16")
     bdesc = workloads.as_bf16_graph(desc)
-    _, fused, _ = run_gpu(bdesc, materialize_all=False, dtype=B.DTYPE_BF16)
+    plan = engine.Plan(bdesc, bind=False, dtype=B.DTYPE_BF16)
+    idx = fused_index(plan)
+    ncfg = plan.node_configs()[idx][1]
+    log(f"[case] {desc['name']} bf16 ({ncfg} configurations)")
     _, plain, _ = run_gpu(bdesc, materialize_all=False, dtype=B.DTYPE_BF16, fuse_softmax=False)
-    np.testing.assert_array_equal(fused[0], plain[0])
+    for cf in range(ncfg):
+        _, fused, _ = run_gpu(bdesc, materialize_all=False, dtype=B.DTYPE_BF16, configs={idx: cf})
+        np.testing.assert_array_equal(fused[0], plain[0], err_msg=f"configuration {cf}")
     ref = oracle.run_graph(bdesc, keep=[y], store_bf16=True)[y]
-    ok, msg = check_layer("bf16 probabilities", fused[0], ref.reshape(fused[0].shape))
+    ok, msg = check_layer("bf16 probabilities", plain[0], ref.reshape(plain[0].shape))
     assert ok, msg
 
 
