@@ -69,15 +69,20 @@ def test_fused_pool_pair(n, h, w, K, C, act):
 
 
 def test_fused_pool_pair_bf16():
-    from paper_1907_01989_amd import _binding as B
+    from paper_1907_01989_amd import engine, _binding as B
     desc, y = pair_graph(16, 7, 7, 256, 320, ACT_RELU6)
-    log(f"[case] {desc['name']} bf16")
     bdesc = workloads.as_bf16_graph(desc)
-    _, fused, _ = run_gpu(bdesc, materialize_all=False, dtype=B.DTYPE_BF16, fuse_pool=2)
+    plan = engine.Plan(bdesc, bind=False, fuse_pool=2, dtype=B.DTYPE_BF16)
+    idx = [i for i, k in enumerate(plan.nodes()) if k["kind"] == "pw_pool"]
+    assert len(idx) == 1
+    ncfg = plan.node_configs()[idx[0]][1]
+    log(f"[case] {desc['name']} bf16 ({ncfg} configurations)")
     _, plain, _ = run_gpu(bdesc, materialize_all=False, dtype=B.DTYPE_BF16, fuse_pool=False)
-    np.testing.assert_array_equal(fused[0], plain[0])
+    for c in range(ncfg):
+        _, fused, _ = run_gpu(bdesc, materialize_all=False, dtype=B.DTYPE_BF16, fuse_pool=2, configs={idx[0]: c})
+        np.testing.assert_array_equal(fused[0], plain[0], err_msg=f"configuration {c}")
     ref = oracle.run_graph(bdesc, keep=[y], store_bf16=True)[y]
-    ok, msg = check_layer("fused bf16 output", fused[0], ref.reshape(fused[0].shape))
+    ok, msg = check_layer("fused bf16 output", plain[0], ref.reshape(plain[0].shape))
     assert ok, msg
 
 

@@ -78,15 +78,20 @@ def test_fused_stem_pair(n, h, w, c, spads, dpads, act, dtype):
 
 
 def test_fused_stem_pair_bf16():
-    from paper_1907_01989_amd import _binding as B
+    from paper_1907_01989_amd import engine, _binding as B
     desc, y = pair_graph(2, 224, 224, 32, None, None, ACT_RELU6, DTYPE_FP16)
-    log(f"[case] {desc['name']} bf16")
     bdesc = workloads.as_bf16_graph(desc)
-    _, fused, _ = run_gpu(bdesc, materialize_all=False, dtype=B.DTYPE_BF16, fuse_stemdw=2)
+    plan = engine.Plan(bdesc, bind=False, fuse_stemdw=2, dtype=B.DTYPE_BF16)
+    idx = [i for i, k in enumerate(plan.nodes()) if k["kind"] == "stem_dw"]
+    assert len(idx) == 1
+    ncfg = plan.node_configs()[idx[0]][1]
+    log(f"[case] {desc['name']} bf16 ({ncfg} configurations)")
     _, plain, _ = run_gpu(bdesc, materialize_all=False, dtype=B.DTYPE_BF16, fuse_stemdw=False)
-    np.testing.assert_array_equal(fused[0], plain[0])
+    for c in range(ncfg):
+        _, fused, _ = run_gpu(bdesc, materialize_all=False, dtype=B.DTYPE_BF16, fuse_stemdw=2, configs={idx[0]: c})
+        np.testing.assert_array_equal(fused[0], plain[0], err_msg=f"configuration {c}")
     ref = oracle.run_graph(bdesc, keep=[y], store_bf16=True)[y]
-    ok, msg = check_layer("fused bf16 output", fused[0], ref.reshape(fused[0].shape))
+    ok, msg = check_layer("fused bf16 output", plain[0], ref.reshape(plain[0].shape))
     assert ok, msg
 
 
