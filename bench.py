@@ -446,25 +446,103 @@ def run_graph_replay(key, steps, warmup, hip, tune=True):
             "step_ms_device": {k: round(v, 5) for k, v in step_ms.items()}}
 
 
-def cpu_baseline(net, budget_s=10.0):
-    """The oracle, as it stands, on a bounded sample of the same workload:
-    whole forward passes of single images until about budget_s has elapsed."""
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(net, batch):
+    """The oracle, as it stands, timed on this host on bounded samples of the
+    workload (about 10-20 s of CPU work in all):
+      threads_all  the whole batch in one oracle run with all the process's
+                   cores (the reported value, in images/s);
+      threads_1    a 4-image slice of the same batch on one thread;
+      b1           single-image passes of the network with all cores."""
     import oracle
     import workloads
-    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
-    desc = workloads.WORKLOADS[net](1)
+    cores = len(os.sched_getaffinity(0))
+    desc = workloads.WORKLOADS[net](batch)
     oracle.lib()
-    n = 0
-    t0 = time.perf_counter()
-    while True:
-        oracle.run_graph(desc, keep=desc["outputs"])
-        n += 1
+    prev = oracle.set_threads(cores)
+
+    def timed(d, n_images, threads):
+        oracle.set_threads(threads)
+        t0 = time.perf_counter()
+        oracle.run_graph(d, keep=d["outputs"])
         el = time.perf_counter() - t0
-        if el >= budget_s or n >= 512:
-            break
-    return {"value": round(n / el, 4), "unit": "images/sec", "cores": threads, "kind": "oracle",
-            "sample": f"{n} single-image forward passes of {desc['name']} (float64, plain loops), "
-                      f"{el:.1f} s"}
+        return n_images / el, el
+
+    try:
+        # the batch itself, all cores (a batch of 1 repeats until ~3 s)
+        if batch > 1:
+            v_all, el_all = timed(desc, batch, cores)
+            what = f"the {batch}-image batch of {desc['name']} in one oracle run"
+        else:
+            n, t0 = 0, time.perf_counter()
+            while time.perf_counter() - t0 < 3.0:
+                oracle.run_graph(desc, keep=desc["outputs"])
+                n += 1
+            el_all = time.perf_counter() - t0
+            v_all = n / el_all
+            what = f"{n} single-image passes of {desc['name']}"
+        sub = workloads.subset_batch(desc, list(range(min(4, batch))))
+        v_1, el_1 = timed(sub, min(4, batch), 1)
+        d1 = workloads.WORKLOADS[net](1)
+        n, t0 = 0, time.perf_counter()
+        oracle.set_threads(cores)
+        while time.perf_counter() - t0 < 2.0:
+            oracle.run_graph(d1, keep=d1["outputs"])
+            n += 1
+        v_b1 = n / (time.perf_counter() - t0)
+    finally:
+        oracle.set_threads(prev)
+    return {"value": round(v_all, 4), "unit": "images/sec", "cores": cores, "kind": "oracle",
+            "sample": f"{what} (float64, plain loops, {cores} threads, {el_all:.1f} s); "
+                      f"1 thread: 4 images of the same batch, {el_1:.1f} s",
+            "threads_all": round(v_all, 4), "threads_1": round(v_1, 4),
+            "b1_threads_all": round(v_b1, 4), "cpu_model": cpu_model()}
+
+
+def run_with_h2d(key, steps, warmup, hip):
+    """Secondary figure: each step first copies the batch's input from pinned
+    host memory to the device input buffer, on the run's stream, then runs the
+    plan (Sec. 6 measures with device-resident I/O; this adds the host side)."""
+    import torch
+    import workloads
+    from paper_1907_01989_amd import engine
+
+    net, batch = WORKLOADS[key]
+    desc = workloads.WORKLOADS[net](batch)
+    plan = engine.Plan(desc)
+    xs = plan.input_tensors()
+    outs = plan.alloc_outputs()
+    host = [x.cpu().pin_memory() for x in xs]
+    sh = torch.cuda.current_stream().cuda_stream
+    plan.autotune(xs, outs, reps=10, stream=sh)
+
+    def step():
+        for h, x in zip(host, xs):
+            x.copy_(h, non_blocking=True)
+        plan.run(xs, outs, stream=sh)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    total_s = time.perf_counter() - t0
+    nbytes = sum(h.numel() * h.element_size() for h in host)
+    plan.close()
+    return {"images_per_s": round(batch * steps / total_s, 1), "ms_per_step": round(total_s / steps * 1e3, 4),
+            "h2d_bytes_per_step": nbytes}
 
 
 def main():
@@ -540,9 +618,14 @@ def main():
                                     "ms_per_step": round(r["ms_per_step"], 4),
                                     "step_ms_device": r["step_ms_device"]}
             eprint(f"[bench] {key} graph replay: {r['images_per_s']:.1f} images/s")
+        r = run_with_h2d(args.workload, 50, 5, hip)
+        also[args.workload + "_with_h2d"] = r
+        eprint(f"[bench] {args.workload} with the input copied from pinned host memory each step: "
+               f"{r['images_per_s']:.1f} images/s")
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(main_res["net"])
+        net0, batch0 = WORKLOADS[args.workload]
+        cpu = cpu_baseline(main_res["net"], batch0)
         eprint(f"[bench] cpu oracle: {cpu}")
     net, batch = WORKLOADS[args.workload]
     out = {

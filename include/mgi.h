@@ -54,7 +54,10 @@ typedef enum {
     MGI_ERR_STATE = 4,       /* call out of order (e.g. run before bind) */
     MGI_ERR_WORKSPACE = 5,   /* a device buffer is missing or misaligned */
     MGI_ERR_HIP = 6,         /* the HIP runtime reported an error */
-    MGI_ERR_OOM_HOST = 7     /* host allocation failed */
+    MGI_ERR_OOM_HOST = 7,    /* host allocation failed */
+    MGI_ERR_INTERNAL = 8     /* any other failure inside the library (a C++
+                                exception stopped at the boundary); the
+                                message is in mgi_last_error() */
 } mgi_status;
 
 typedef enum { MGI_ACT_NONE = 0, MGI_ACT_RELU = 1, MGI_ACT_RELU6 = 2 } mgi_act;

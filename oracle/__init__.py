@@ -51,11 +51,24 @@ def lib():
         L.orc_concat2.argtypes = [D, I, D, I, S, D]
         L.orc_resize_bilinear.argtypes = [D, I, I, I, I, D, I, I, I]
         L.orc_argmax.argtypes = [D, S, I, ctypes.POINTER(ctypes.c_int)]
+        L.orc_set_threads.argtypes = [I]
+        L.orc_set_threads.restype = None
+        L.orc_max_threads.argtypes = []
+        L.orc_max_threads.restype = I
         for f in ("orc_conv2d", "orc_depthwise", "orc_activation", "orc_add", "orc_global_avgpool",
                   "orc_fc", "orc_softmax", "orc_concat2", "orc_resize_bilinear", "orc_argmax"):
             getattr(L, f).restype = None
         _lib = L
     return _lib
+
+
+def set_threads(n: int) -> int:
+    """Set the thread count of the oracle's OpenMP loops; returns the previous
+    one.  Results do not depend on it (each output element is one sequential
+    sum)."""
+    prev = lib().orc_max_threads()
+    lib().orc_set_threads(int(n))
+    return prev
 
 
 def _d(a):

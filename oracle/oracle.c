@@ -24,7 +24,13 @@
  *     classification / segmentation heads of the networks of Sec. 6).
  */
 #include <math.h>
+#include <omp.h>
 #include <stddef.h>
+
+/* Thread count of the OpenMP loops below (timing only; results do not depend
+ * on it). */
+void orc_set_threads(int n) { omp_set_num_threads(n > 0 ? n : 1); }
+int orc_max_threads(void) { return omp_get_max_threads(); }
 
 #define IDX4(n, y, x, c, H, W, C) ((((size_t)(n) * (H) + (y)) * (W) + (x)) * (C) + (c))
 

@@ -40,49 +40,54 @@ def naive(ops, sizes, intermediate):
 
 
 def greedy(ops, sizes, intermediate):
-    """Greedy shared-object assignment (Algorithm 1), written as a plain list scan.
+    """Greedy shared-object assignment (Sec. 5, Algorithm 1), as a sweep over
+    produce and release events.
 
-    Operators are visited in execution order.  Each intermediate output takes
-    a new shared object when the pool of free objects is empty, otherwise the
-    free object whose size is closest to the tensor's size (absolute
-    difference; equal distances go to the lowest object index), which leaves
-    the pool and grows to the tensor's size if smaller.  Only after all outputs
-    of the operator are placed are its intermediate inputs whose last consumer
-    it is handed back to the pool, so an output never shares memory with an
-    input of the same operator.  A tensor that nothing consumes is never
-    returned to the pool.
+    Each intermediate tensor lives from the operator that writes it to the
+    last operator that reads it.  Those lifetimes are computed first; they give
+    one "produce" event per tensor and one "release" event per tensor that
+    something reads.  The events are swept in execution order, and within one
+    operator all of its produce events come before its release events, so an
+    output never takes the memory of an input of the same operator.  A produce
+    event opens a new shared object when no object is free; otherwise it takes
+    the free object whose size is nearest the tensor's (absolute difference,
+    lowest object index on a tie) and enlarges it to the tensor's size if it is
+    smaller.  A release event returns the tensor's object to the free set.  A
+    tensor that nothing reads has no release event and keeps its object.
     """
-    consumers_left = {}
-    for outs, ins in ops:
-        for t in ins:
-            if t in intermediate:
-                consumers_left[t] = consumers_left.get(t, 0) + 1
-    last = {}
-    for i, (_, ins) in enumerate(ops):
-        for t in ins:
-            if t in intermediate:
-                last[t] = i
-    objects: list[int] = []
-    free: list[int] = []          # object indices
-    assign: dict[int, int] = {}
+    produced_at = {}
+    read_last = {}
     for i, (outs, ins) in enumerate(ops):
         for t in outs:
-            if t not in intermediate:
-                continue
-            if not free:
-                k = len(objects)
-                objects.append(sizes[t])
-            else:
-                k = min(free, key=lambda j: (abs(objects[j] - sizes[t]), j))
-                free.remove(k)
-                if sizes[t] > objects[k]:
-                    objects[k] = sizes[t]
-            assign[t] = k
-        released = set()
+            if t in intermediate and t not in produced_at:
+                produced_at[t] = i
         for t in ins:
-            if t in intermediate and last.get(t) == i and t not in released:
-                released.add(t)
-                free.append(assign[t])
+            if t in intermediate:
+                read_last[t] = i
+    # (operator, 0 = produce / 1 = release, position within the operator, tensor)
+    events = []
+    for i, (outs, _) in enumerate(ops):
+        for pos, t in enumerate(outs):
+            if produced_at.get(t) == i:
+                events.append((i, 0, pos, t))
+    for t, i in read_last.items():
+        events.append((i, 1, 0, t))
+    events.sort()
+    objects: list[int] = []
+    free_set: set[int] = set()
+    assign: dict[int, int] = {}
+    for _, kind, _, t in events:
+        if kind == 1:
+            free_set.add(assign[t])
+            continue
+        if free_set:
+            k = sorted(free_set, key=lambda j: (abs(objects[j] - sizes[t]), j))[0]
+            free_set.discard(k)
+            objects[k] = max(objects[k], sizes[t])
+        else:
+            k = len(objects)
+            objects.append(sizes[t])
+        assign[t] = k
     return assign, objects
 
 

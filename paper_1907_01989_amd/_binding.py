@@ -13,7 +13,8 @@ LIB_PATH = os.path.join(_HERE, "libmgi.so")
 
 MGI_OK = 0
 STATUS = {0: "MGI_OK", 1: "MGI_ERR_INVALID_ARG", 2: "MGI_ERR_SHAPE", 3: "MGI_ERR_UNSUPPORTED",
-          4: "MGI_ERR_STATE", 5: "MGI_ERR_WORKSPACE", 6: "MGI_ERR_HIP", 7: "MGI_ERR_OOM_HOST"}
+          4: "MGI_ERR_STATE", 5: "MGI_ERR_WORKSPACE", 6: "MGI_ERR_HIP", 7: "MGI_ERR_OOM_HOST",
+          8: "MGI_ERR_INTERNAL"}
 ACT_NONE, ACT_RELU, ACT_RELU6 = 0, 1, 2
 DTYPE_FP16, DTYPE_BF16, DTYPE_FP32, DTYPE_INT32 = 0, 1, 2, 3
 PLANNER_NAIVE, PLANNER_GREEDY, PLANNER_MCFP = 0, 1, 2
@@ -273,29 +274,40 @@ def mgi_plan_bind(p, dev_ws, dev_w, stream=None):
     _check(lib().mgi_plan_bind(p, P(dev_ws), P(dev_w), P(stream or 0)))
 
 
+def _io_arrays(p, in_ptrs, out_ptrs):
+    """ctypes pointer arrays for a plan's inputs and outputs.  The C calls take
+    arrays with no length, so the counts are checked against the plan here."""
+    n_in, n_out = mgi_plan_num_io(p)
+    if len(in_ptrs) != n_in or len(out_ptrs) != n_out:
+        raise ValueError(f"plan takes {n_in} inputs and {n_out} outputs, "
+                         f"got {len(in_ptrs)} and {len(out_ptrs)}")
+    ins = (P * max(1, n_in))(*in_ptrs)
+    outs = (P * max(1, n_out))(*out_ptrs)
+    return ins, outs
+
+
 def mgi_plan_run(p, in_ptrs, out_ptrs, stream=None):
-    ins = (P * max(1, len(in_ptrs)))(*in_ptrs)
-    outs = (P * max(1, len(out_ptrs)))(*out_ptrs)
+    ins, outs = _io_arrays(p, in_ptrs, out_ptrs)
     _check(lib().mgi_plan_run(p, ins, outs, P(stream or 0)))
 
 
 def mgi_plan_run_timed(p, in_ptrs, out_ptrs, start_events, stop_events, stream=None):
-    ins = (P * max(1, len(in_ptrs)))(*in_ptrs)
-    outs = (P * max(1, len(out_ptrs)))(*out_ptrs)
-    ev0 = (P * max(1, len(start_events)))(*[e or None for e in start_events])
-    ev1 = (P * max(1, len(stop_events)))(*[e or None for e in stop_events])
+    ins, outs = _io_arrays(p, in_ptrs, out_ptrs)
+    n = mgi_plan_node_count(p)
+    if len(start_events) != n or len(stop_events) != n:
+        raise ValueError(f"plan has {n} nodes: one start and one stop event slot each")
+    ev0 = (P * max(1, n))(*[e or None for e in start_events])
+    ev1 = (P * max(1, n))(*[e or None for e in stop_events])
     _check(lib().mgi_plan_run_timed(p, ins, outs, P(stream or 0), ev0, ev1))
 
 
 def mgi_plan_capture(p, in_ptrs, out_ptrs):
-    ins = (P * max(1, len(in_ptrs)))(*in_ptrs)
-    outs = (P * max(1, len(out_ptrs)))(*out_ptrs)
+    ins, outs = _io_arrays(p, in_ptrs, out_ptrs)
     _check(lib().mgi_plan_capture(p, ins, outs))
 
 
 def mgi_plan_autotune(p, in_ptrs, out_ptrs, stream=None, reps=5):
-    ins = (P * max(1, len(in_ptrs)))(*in_ptrs)
-    outs = (P * max(1, len(out_ptrs)))(*out_ptrs)
+    ins, outs = _io_arrays(p, in_ptrs, out_ptrs)
     _check(lib().mgi_plan_autotune(p, ins, outs, P(stream or 0), reps))
 
 

@@ -1176,6 +1176,7 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
 using namespace mgi;
 
 extern "C" mgi_status mgi_graph_finalize(const mgi_graph *g, const mgi_options *o, mgi_plan **p) {
+    MGI_ABI_TRY
     if (!g || !o || !p) return fail(MGI_ERR_INVALID_ARG, "mgi_graph_finalize: null pointer");
     *p = nullptr;
     mgi_plan *plan = new (std::nothrow) mgi_plan();
@@ -1192,38 +1193,48 @@ extern "C" mgi_status mgi_graph_finalize(const mgi_graph *g, const mgi_options *
     }
     *p = plan;
     return MGI_OK;
+    MGI_ABI_CATCH("mgi_graph_finalize")
 }
 
 extern "C" mgi_status mgi_plan_workspace_bytes(const mgi_plan *p, size_t *bytes) {
+    MGI_ABI_TRY
     if (!p || !bytes) return fail(MGI_ERR_INVALID_ARG, "mgi_plan_workspace_bytes: null pointer");
     *bytes = p->workspace_bytes;
     return MGI_OK;
+    MGI_ABI_CATCH("mgi_plan_workspace_bytes")
 }
 
 extern "C" mgi_status mgi_plan_weight_bytes(const mgi_plan *p, size_t *bytes) {
+    MGI_ABI_TRY
     if (!p || !bytes) return fail(MGI_ERR_INVALID_ARG, "mgi_plan_weight_bytes: null pointer");
     *bytes = p->weight_bytes;
     return MGI_OK;
+    MGI_ABI_CATCH("mgi_plan_weight_bytes")
 }
 
 extern "C" mgi_status mgi_plan_memory_report(const mgi_plan *p, size_t *naive, size_t *planned,
                                              int *n_objects) {
+    MGI_ABI_TRY
     if (!p) return fail(MGI_ERR_INVALID_ARG, "mgi_plan_memory_report: null plan");
     if (naive) *naive = p->mem_naive;
     if (planned) *planned = p->mem_planned;
     if (n_objects) *n_objects = p->n_objects;
     return MGI_OK;
+    MGI_ABI_CATCH("mgi_plan_memory_report")
 }
 
 extern "C" mgi_status mgi_plan_num_io(const mgi_plan *p, int *n_inputs, int *n_outputs) {
+    MGI_ABI_TRY
     if (!p) return fail(MGI_ERR_INVALID_ARG, "mgi_plan_num_io: null plan");
     if (n_inputs) *n_inputs = (int)p->input_bufs.size();
     if (n_outputs) *n_outputs = (int)p->output_bufs.size();
     return MGI_OK;
+    MGI_ABI_CATCH("mgi_plan_num_io")
 }
 
 extern "C" mgi_status mgi_plan_io_info(const mgi_plan *p, int is_output, int index, int *n, int *h,
                                        int *w, int *c, int *dtype, size_t *bytes) {
+    MGI_ABI_TRY
     if (!p) return fail(MGI_ERR_INVALID_ARG, "mgi_plan_io_info: null plan");
     const auto &shapes = is_output ? p->output_shapes : p->input_shapes;
     const auto &types = is_output ? p->output_dtypes : p->input_dtypes;
@@ -1237,17 +1248,21 @@ extern "C" mgi_status mgi_plan_io_info(const mgi_plan *p, int is_output, int ind
     if (dtype) *dtype = types[index];
     if (bytes) *bytes = s.elems() * (types[index] == MGI_DTYPE_FP16 ? 2 : 4);
     return MGI_OK;
+    MGI_ABI_CATCH("mgi_plan_io_info")
 }
 
 extern "C" mgi_status mgi_plan_node_count(const mgi_plan *p, int *count) {
+    MGI_ABI_TRY
     if (!p || !count) return fail(MGI_ERR_INVALID_ARG, "mgi_plan_node_count: null pointer");
     *count = (int)p->nodes.size();
     return MGI_OK;
+    MGI_ABI_CATCH("mgi_plan_node_count")
 }
 
 extern "C" mgi_status mgi_plan_node_info(const mgi_plan *p, int i, const char **kind,
                                          int *tensor_id, int *n, int *h, int *w, int *c,
                                          int *n_fused) {
+    MGI_ABI_TRY
     if (!p) return fail(MGI_ERR_INVALID_ARG, "mgi_plan_node_info: null plan");
     if (i < 0 || i >= (int)p->nodes.size())
         return fail(MGI_ERR_INVALID_ARG, "mgi_plan_node_info: node index out of range");
@@ -1261,4 +1276,5 @@ extern "C" mgi_status mgi_plan_node_info(const mgi_plan *p, int i, const char **
     if (c) *c = s.c;
     if (n_fused) *n_fused = nd.n_fused;
     return MGI_OK;
+    MGI_ABI_CATCH("mgi_plan_node_info")
 }

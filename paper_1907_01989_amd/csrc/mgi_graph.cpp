@@ -32,6 +32,7 @@ extern "C" const char *mgi_status_str(mgi_status s) {
         case MGI_ERR_WORKSPACE: return "MGI_ERR_WORKSPACE";
         case MGI_ERR_HIP: return "MGI_ERR_HIP";
         case MGI_ERR_OOM_HOST: return "MGI_ERR_OOM_HOST";
+        case MGI_ERR_INTERNAL: return "MGI_ERR_INTERNAL";
     }
     return "MGI_ERR_UNKNOWN";
 }
@@ -39,15 +40,19 @@ extern "C" const char *mgi_status_str(mgi_status s) {
 extern "C" const char *mgi_last_error(void) { return g_last_error.c_str(); }
 
 extern "C" mgi_status mgi_graph_create(mgi_graph **g) {
+    MGI_ABI_TRY
     if (!g) return fail(MGI_ERR_INVALID_ARG, "mgi_graph_create: null out pointer");
     *g = new (std::nothrow) mgi_graph();
     if (!*g) return fail(MGI_ERR_OOM_HOST, "mgi_graph_create: out of host memory");
     return MGI_OK;
+    MGI_ABI_CATCH("mgi_graph_create")
 }
 
 extern "C" mgi_status mgi_graph_destroy(mgi_graph *g) {
+    MGI_ABI_TRY
     delete g;
     return MGI_OK;
+    MGI_ABI_CATCH("mgi_graph_destroy")
 }
 
 namespace {
@@ -94,6 +99,7 @@ mgi_status conv_geometry(const Shape &x, const mgi_conv_desc *d, const char *who
 
 extern "C" mgi_status mgi_graph_add_input(mgi_graph *g, int n, int h, int w, int c, int dtype,
                                           int *out) {
+    MGI_ABI_TRY
     if (!g || !out) return fail(MGI_ERR_INVALID_ARG, "mgi_graph_add_input: null pointer");
     if (n <= 0 || h <= 0 || w <= 0 || c <= 0)
         return fail(MGI_ERR_INVALID_ARG, "mgi_graph_add_input: sizes must be positive");
@@ -106,10 +112,12 @@ extern "C" mgi_status mgi_graph_add_input(mgi_graph *g, int n, int h, int w, int
     mgi_status s = push(g, std::move(op), out);
     if (s == MGI_OK) g->inputs.push_back(*out);
     return s;
+    MGI_ABI_CATCH("mgi_graph_add_input")
 }
 
 extern "C" mgi_status mgi_graph_add_conv2d(mgi_graph *g, int in, const mgi_conv_desc *d,
                                            const float *w, const float *bias, int *out) {
+    MGI_ABI_TRY
     mgi_status s = check_tensor(g, in, "mgi_graph_add_conv2d");
     if (s) return s;
     if (!out || !w) return fail(MGI_ERR_INVALID_ARG, "mgi_graph_add_conv2d: null pointer");
@@ -131,10 +139,12 @@ extern "C" mgi_status mgi_graph_add_conv2d(mgi_graph *g, int in, const mgi_conv_
         return fail(MGI_ERR_OOM_HOST, "mgi_graph_add_conv2d: out of host memory");
     }
     return push(g, std::move(op), out);
+    MGI_ABI_CATCH("mgi_graph_add_conv2d")
 }
 
 extern "C" mgi_status mgi_graph_add_depthwise(mgi_graph *g, int in, const mgi_conv_desc *d,
                                               const float *w, const float *bias, int *out) {
+    MGI_ABI_TRY
     mgi_status s = check_tensor(g, in, "mgi_graph_add_depthwise");
     if (s) return s;
     if (!out || !w) return fail(MGI_ERR_INVALID_ARG, "mgi_graph_add_depthwise: null pointer");
@@ -156,6 +166,7 @@ extern "C" mgi_status mgi_graph_add_depthwise(mgi_graph *g, int in, const mgi_co
         return fail(MGI_ERR_OOM_HOST, "mgi_graph_add_depthwise: out of host memory");
     }
     return push(g, std::move(op), out);
+    MGI_ABI_CATCH("mgi_graph_add_depthwise")
 }
 
 static bool same_shape(const Shape &a, const Shape &b) {
@@ -163,6 +174,7 @@ static bool same_shape(const Shape &a, const Shape &b) {
 }
 
 extern "C" mgi_status mgi_graph_add_add(mgi_graph *g, int a, int b, int act, int *out) {
+    MGI_ABI_TRY
     mgi_status s;
     if ((s = check_tensor(g, a, "mgi_graph_add_add")) || (s = check_tensor(g, b, "mgi_graph_add_add")))
         return s;
@@ -176,9 +188,11 @@ extern "C" mgi_status mgi_graph_add_add(mgi_graph *g, int a, int b, int act, int
     op.act = act;
     op.out = g->ops[a].out;
     return push(g, std::move(op), out);
+    MGI_ABI_CATCH("mgi_graph_add_add")
 }
 
 extern "C" mgi_status mgi_graph_add_activation(mgi_graph *g, int in, int act, int *out) {
+    MGI_ABI_TRY
     mgi_status s = check_tensor(g, in, "mgi_graph_add_activation");
     if (s) return s;
     if (!out) return fail(MGI_ERR_INVALID_ARG, "mgi_graph_add_activation: null pointer");
@@ -189,10 +203,12 @@ extern "C" mgi_status mgi_graph_add_activation(mgi_graph *g, int in, int act, in
     op.act = act;
     op.out = g->ops[in].out;
     return push(g, std::move(op), out);
+    MGI_ABI_CATCH("mgi_graph_add_activation")
 }
 
 extern "C" mgi_status mgi_graph_add_pad(mgi_graph *g, int in, int pad_t, int pad_b, int pad_l,
                                         int pad_r, int *out) {
+    MGI_ABI_TRY
     mgi_status s = check_tensor(g, in, "mgi_graph_add_pad");
     if (s) return s;
     if (!out) return fail(MGI_ERR_INVALID_ARG, "mgi_graph_add_pad: null pointer");
@@ -209,9 +225,11 @@ extern "C" mgi_status mgi_graph_add_pad(mgi_graph *g, int in, int pad_t, int pad
     op.out.h += pad_t + pad_b;
     op.out.w += pad_l + pad_r;
     return push(g, std::move(op), out);
+    MGI_ABI_CATCH("mgi_graph_add_pad")
 }
 
 extern "C" mgi_status mgi_graph_add_global_avgpool(mgi_graph *g, int in, int *out) {
+    MGI_ABI_TRY
     mgi_status s = check_tensor(g, in, "mgi_graph_add_global_avgpool");
     if (s) return s;
     if (!out) return fail(MGI_ERR_INVALID_ARG, "mgi_graph_add_global_avgpool: null pointer");
@@ -221,10 +239,12 @@ extern "C" mgi_status mgi_graph_add_global_avgpool(mgi_graph *g, int in, int *ou
     const Shape x = g->ops[in].out;
     op.out = {x.n, 1, 1, x.c};
     return push(g, std::move(op), out);
+    MGI_ABI_CATCH("mgi_graph_add_global_avgpool")
 }
 
 extern "C" mgi_status mgi_graph_add_fc(mgi_graph *g, int in, int cout, const float *w,
                                        const float *bias, int *out) {
+    MGI_ABI_TRY
     mgi_status s = check_tensor(g, in, "mgi_graph_add_fc");
     if (s) return s;
     if (!out || !w) return fail(MGI_ERR_INVALID_ARG, "mgi_graph_add_fc: null pointer");
@@ -244,9 +264,11 @@ extern "C" mgi_status mgi_graph_add_fc(mgi_graph *g, int in, int cout, const flo
         return fail(MGI_ERR_OOM_HOST, "mgi_graph_add_fc: out of host memory");
     }
     return push(g, std::move(op), out);
+    MGI_ABI_CATCH("mgi_graph_add_fc")
 }
 
 extern "C" mgi_status mgi_graph_add_softmax(mgi_graph *g, int in, int *out) {
+    MGI_ABI_TRY
     mgi_status s = check_tensor(g, in, "mgi_graph_add_softmax");
     if (s) return s;
     if (!out) return fail(MGI_ERR_INVALID_ARG, "mgi_graph_add_softmax: null pointer");
@@ -255,9 +277,11 @@ extern "C" mgi_status mgi_graph_add_softmax(mgi_graph *g, int in, int *out) {
     op.in = {in};
     op.out = g->ops[in].out;
     return push(g, std::move(op), out);
+    MGI_ABI_CATCH("mgi_graph_add_softmax")
 }
 
 extern "C" mgi_status mgi_graph_add_concat(mgi_graph *g, const int *ins, int count, int *out) {
+    MGI_ABI_TRY
     if (!g || !ins || !out) return fail(MGI_ERR_INVALID_ARG, "mgi_graph_add_concat: null pointer");
     if (count < 1 || count > 8)
         return fail(count < 1 ? MGI_ERR_INVALID_ARG : MGI_ERR_UNSUPPORTED,
@@ -277,10 +301,12 @@ extern "C" mgi_status mgi_graph_add_concat(mgi_graph *g, const int *ins, int cou
     op.in.assign(ins, ins + count);
     op.out = o;
     return push(g, std::move(op), out);
+    MGI_ABI_CATCH("mgi_graph_add_concat")
 }
 
 extern "C" mgi_status mgi_graph_add_resize_bilinear(mgi_graph *g, int in, int oh, int ow,
                                                     int align_corners, int *out) {
+    MGI_ABI_TRY
     mgi_status s = check_tensor(g, in, "mgi_graph_add_resize_bilinear");
     if (s) return s;
     if (!out) return fail(MGI_ERR_INVALID_ARG, "mgi_graph_add_resize_bilinear: null pointer");
@@ -295,9 +321,11 @@ extern "C" mgi_status mgi_graph_add_resize_bilinear(mgi_graph *g, int in, int oh
     const Shape x = g->ops[in].out;
     op.out = {x.n, oh, ow, x.c};
     return push(g, std::move(op), out);
+    MGI_ABI_CATCH("mgi_graph_add_resize_bilinear")
 }
 
 extern "C" mgi_status mgi_graph_add_argmax(mgi_graph *g, int in, int *out) {
+    MGI_ABI_TRY
     mgi_status s = check_tensor(g, in, "mgi_graph_add_argmax");
     if (s) return s;
     if (!out) return fail(MGI_ERR_INVALID_ARG, "mgi_graph_add_argmax: null pointer");
@@ -307,9 +335,11 @@ extern "C" mgi_status mgi_graph_add_argmax(mgi_graph *g, int in, int *out) {
     const Shape x = g->ops[in].out;
     op.out = {x.n, x.h, x.w, 1};
     return push(g, std::move(op), out);
+    MGI_ABI_CATCH("mgi_graph_add_argmax")
 }
 
 extern "C" mgi_status mgi_graph_mark_output(mgi_graph *g, int id) {
+    MGI_ABI_TRY
     mgi_status s = check_tensor(g, id, "mgi_graph_mark_output");
     if (s) return s;
     if (g->ops[id].kind == OpKind::Input)
@@ -318,6 +348,7 @@ extern "C" mgi_status mgi_graph_mark_output(mgi_graph *g, int id) {
         if (t == id) return fail(MGI_ERR_INVALID_ARG, "mgi_graph_mark_output: already an output");
     g->outputs.push_back(id);
     return MGI_OK;
+    MGI_ABI_CATCH("mgi_graph_mark_output")
 }
 
 extern "C" void mgi_options_default(mgi_options *o) {

@@ -12,10 +12,29 @@
 
 #include <cstddef>
 #include <cstdint>
+#include <exception>
+#include <new>
 #include <string>
 #include <vector>
 
 #include "../../include/mgi.h"
+
+// Every extern "C" entry point runs its body inside MGI_ABI_TRY /
+// MGI_ABI_CATCH(name): no C++ exception crosses the C boundary; an allocation
+// failure becomes MGI_ERR_OOM_HOST and anything else MGI_ERR_INTERNAL, with
+// the message left in mgi_last_error().
+#define MGI_ABI_TRY try {
+#define MGI_ABI_CATCH(name)                                                               \
+    }                                                                                     \
+    catch (const std::bad_alloc &) {                                                      \
+        return ::mgi::fail(MGI_ERR_OOM_HOST, std::string(name) + ": out of host memory"); \
+    }                                                                                     \
+    catch (const std::exception &e) {                                                     \
+        return ::mgi::fail(MGI_ERR_INTERNAL, std::string(name) + ": " + e.what());        \
+    }                                                                                     \
+    catch (...) {                                                                         \
+        return ::mgi::fail(MGI_ERR_INTERNAL, std::string(name) + ": unknown exception");  \
+    }
 
 namespace mgi {
 
@@ -175,6 +194,7 @@ struct mgi_plan {
     void *dev_w = nullptr;
     bool bound = false;
     std::vector<void *> last_outputs;  // output pointers of the latest run
+    void *last_ws = nullptr;           // workspace base of the latest run
     void *graph = nullptr;             // hipGraph_t of the captured launch list
     void *graph_exec = nullptr;        // hipGraphExec_t
     std::vector<void *> graph_outputs; // output pointers baked into the graph

@@ -204,6 +204,7 @@ using namespace mgi;
 extern "C" mgi_status mgi_planner_assign(int planner, int n_tensors, const size_t *sizes,
                                          const int *first_op, const int *last_op, int *object_of,
                                          size_t *object_sizes, int *n_objects) {
+    MGI_ABI_TRY
     if (n_tensors < 0) return fail(MGI_ERR_INVALID_ARG, "mgi_planner_assign: n_tensors < 0");
     if (n_tensors > 0 && (!sizes || !first_op || !last_op || !object_of || !object_sizes))
         return fail(MGI_ERR_INVALID_ARG, "mgi_planner_assign: null pointer");
@@ -224,4 +225,5 @@ extern "C" mgi_status mgi_planner_assign(int planner, int n_tensors, const size_
     for (size_t k = 0; k < r.object_size.size(); ++k) object_sizes[k] = r.object_size[k];
     *n_objects = (int)r.object_size.size();
     return MGI_OK;
+    MGI_ABI_CATCH("mgi_planner_assign")
 }

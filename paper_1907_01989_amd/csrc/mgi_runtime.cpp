@@ -11,6 +11,8 @@
 #include <cstring>
 
 #include <algorithm>
+#include <mutex>
+#include <string>
 
 #include "kernels.h"
 #include "mgi_internal.h"
@@ -384,8 +386,8 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
 namespace {
 
 void release_graph(mgi_plan &p) {
-    if (p.graph_exec) hipGraphExecDestroy(static_cast<hipGraphExec_t>(p.graph_exec));
-    if (p.graph) hipGraphDestroy(static_cast<hipGraph_t>(p.graph));
+    if (p.graph_exec) (void)hipGraphExecDestroy(static_cast<hipGraphExec_t>(p.graph_exec));
+    if (p.graph) (void)hipGraphDestroy(static_cast<hipGraph_t>(p.graph));
     p.graph_exec = nullptr;
     p.graph = nullptr;
     p.graph_outputs.clear();
@@ -396,12 +398,15 @@ void release_graph(mgi_plan &p) {
 mgi_plan::~mgi_plan() { release_graph(*this); }
 
 extern "C" mgi_status mgi_plan_destroy(mgi_plan *p) {
+    MGI_ABI_TRY
     delete p;
     return MGI_OK;
+    MGI_ABI_CATCH("mgi_plan_destroy")
 }
 
 extern "C" mgi_status mgi_plan_bind(mgi_plan *p, void *dev_workspace, void *dev_weights,
                                     void *stream) {
+    MGI_ABI_TRY
     if (!p) return fail(MGI_ERR_INVALID_ARG, "mgi_plan_bind: null plan");
     if (!dev_workspace || !dev_weights)
         return fail(MGI_ERR_WORKSPACE, "mgi_plan_bind: workspace and weight buffers are required");
@@ -428,12 +433,16 @@ extern "C" mgi_status mgi_plan_bind(mgi_plan *p, void *dev_workspace, void *dev_
     p->dev_w = dev_weights;
     p->bound = true;
     return MGI_OK;
+    MGI_ABI_CATCH("mgi_plan_bind")
 }
 
 namespace {
 
+// Enqueues every node of a bound plan on `stream`, with the arena and state
+// region at `ws` (the bound workspace when null).
 mgi_status run_plan(mgi_plan *p, const void *const *dev_inputs, void *const *dev_outputs,
-                    void *stream, void *const *start_ev, void *const *stop_ev, const char *who) {
+                    void *stream, void *const *start_ev, void *const *stop_ev, const char *who,
+                    char *ws = nullptr) {
     if (!p) return fail(MGI_ERR_INVALID_ARG, std::string(who) + ": null plan");
     if (!p->bound) return fail(MGI_ERR_STATE, std::string(who) + ": plan is not bound");
     if (!p->input_bufs.empty() && !dev_inputs)
@@ -444,7 +453,8 @@ mgi_status run_plan(mgi_plan *p, const void *const *dev_inputs, void *const *dev
     for (size_t i = 0; i < p->output_bufs.size(); ++i)
         if (!dev_outputs[i]) return fail(MGI_ERR_INVALID_ARG, std::string(who) + ": null output pointer");
     hipStream_t st = static_cast<hipStream_t>(stream);
-    Bases B{static_cast<char *>(p->dev_ws), dev_inputs, dev_outputs};
+    if (!ws) ws = static_cast<char *>(p->dev_ws);
+    Bases B{ws, dev_inputs, dev_outputs};
     LaunchEvents &ev = launch_events();
     for (size_t i = 0; i < p->nodes.size(); ++i) {
         ev.start = start_ev ? static_cast<hipEvent_t>(start_ev[i]) : nullptr;
@@ -456,6 +466,7 @@ mgi_status run_plan(mgi_plan *p, const void *const *dev_inputs, void *const *dev
                                 p->nodes[i].kname + ")").c_str());
     }
     p->last_outputs.assign(dev_outputs, dev_outputs + p->output_bufs.size());
+    p->last_ws = ws;
     return MGI_OK;
 }
 
@@ -463,16 +474,20 @@ mgi_status run_plan(mgi_plan *p, const void *const *dev_inputs, void *const *dev
 
 extern "C" mgi_status mgi_plan_run(mgi_plan *p, const void *const *dev_inputs,
                                    void *const *dev_outputs, void *stream) {
+    MGI_ABI_TRY
     return run_plan(p, dev_inputs, dev_outputs, stream, nullptr, nullptr, "mgi_plan_run");
+    MGI_ABI_CATCH("mgi_plan_run")
 }
 
 extern "C" mgi_status mgi_plan_run_timed(mgi_plan *p, const void *const *dev_inputs,
                                          void *const *dev_outputs, void *stream,
                                          void *const *start_events, void *const *stop_events) {
+    MGI_ABI_TRY
     if (!start_events || !stop_events)
         return fail(MGI_ERR_INVALID_ARG, "mgi_plan_run_timed: null event array");
     return run_plan(p, dev_inputs, dev_outputs, stream, start_events, stop_events,
                     "mgi_plan_run_timed");
+    MGI_ABI_CATCH("mgi_plan_run_timed")
 }
 
 // The launch list of one run is recorded once through stream capture on a
@@ -483,6 +498,7 @@ extern "C" mgi_status mgi_plan_run_timed(mgi_plan *p, const void *const *dev_inp
 // the graph holds kernel nodes only.
 extern "C" mgi_status mgi_plan_capture(mgi_plan *p, const void *const *dev_inputs,
                                        void *const *dev_outputs) {
+    MGI_ABI_TRY
     if (!p) return fail(MGI_ERR_INVALID_ARG, "mgi_plan_capture: null plan");
     if (!p->bound) return fail(MGI_ERR_STATE, "mgi_plan_capture: plan is not bound");
     release_graph(*p);
@@ -491,49 +507,54 @@ extern "C" mgi_status mgi_plan_capture(mgi_plan *p, const void *const *dev_input
     if (e != hipSuccess) return hip_fail(e, "mgi_plan_capture: stream");
     e = hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal);
     if (e != hipSuccess) {
-        hipStreamDestroy(cs);
+        (void)hipStreamDestroy(cs);
         return hip_fail(e, "mgi_plan_capture: begin capture");
     }
     const mgi_status st = run_plan(p, dev_inputs, dev_outputs, cs, nullptr, nullptr, "mgi_plan_capture");
     hipGraph_t g = nullptr;
     e = hipStreamEndCapture(cs, &g);
-    hipStreamDestroy(cs);
+    (void)hipStreamDestroy(cs);
     if (st != MGI_OK) {
-        if (g) hipGraphDestroy(g);
+        if (g) (void)hipGraphDestroy(g);
         return st;
     }
     if (e != hipSuccess) return hip_fail(e, "mgi_plan_capture: end capture");
     hipGraphExec_t ge = nullptr;
     e = hipGraphInstantiate(&ge, g, nullptr, nullptr, 0);
     if (e != hipSuccess) {
-        hipGraphDestroy(g);
+        (void)hipGraphDestroy(g);
         return hip_fail(e, "mgi_plan_capture: instantiate");
     }
     p->graph = g;
     p->graph_exec = ge;
     p->graph_outputs.assign(dev_outputs, dev_outputs + p->output_bufs.size());
     return MGI_OK;
+    MGI_ABI_CATCH("mgi_plan_capture")
 }
 
 extern "C" mgi_status mgi_plan_replay(mgi_plan *p, void *stream) {
+    MGI_ABI_TRY
     if (!p) return fail(MGI_ERR_INVALID_ARG, "mgi_plan_replay: null plan");
     if (!p->graph_exec) return fail(MGI_ERR_STATE, "mgi_plan_replay: nothing captured");
     hipError_t e = hipGraphLaunch(static_cast<hipGraphExec_t>(p->graph_exec),
                                   static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "mgi_plan_replay");
     p->last_outputs = p->graph_outputs;
+    p->last_ws = p->dev_ws;
     return MGI_OK;
+    MGI_ABI_CATCH("mgi_plan_replay")
 }
 
 // Plan-time tuning, the counterpart of choosing work-group sizes by
 // measurement (Sec. 4.2): every node with more than one candidate
 // configuration is launched reps + 1 times per candidate on the plan's own
 // buffers (after one full run has filled them), each launch timestamped on the
-// device; the fastest (minimum over the timed launches, the first launch being
-// a warm-up) is kept.  Candidates compute identical results, so tuning changes
+// device; the one with the lowest median over the timed launches (the first
+// launch being a warm-up) is kept.  Candidates compute identical results, so tuning changes
 // speed only.  A captured graph holds the old configurations and is released.
 extern "C" mgi_status mgi_plan_autotune(mgi_plan *p, const void *const *dev_inputs,
                                         void *const *dev_outputs, void *stream, int reps) {
+    MGI_ABI_TRY
     if (!p) return fail(MGI_ERR_INVALID_ARG, "mgi_plan_autotune: null plan");
     if (reps < 1 || reps > 1000) return fail(MGI_ERR_INVALID_ARG, "mgi_plan_autotune: reps in 1..1000");
     mgi_status s = run_plan(p, dev_inputs, dev_outputs, stream, nullptr, nullptr, "mgi_plan_autotune");
@@ -547,7 +568,7 @@ extern "C" mgi_status mgi_plan_autotune(mgi_plan *p, const void *const *dev_inpu
     for (size_t k = 0; k < evs.size() && e == hipSuccess; ++k) e = hipEventCreate(&evs[k]);
     auto destroy = [&]() {
         for (hipEvent_t x : evs)
-            if (x) hipEventDestroy(x);
+            if (x) (void)hipEventDestroy(x);
     };
     if (e != hipSuccess) {
         destroy();
@@ -611,10 +632,12 @@ extern "C" mgi_status mgi_plan_autotune(mgi_plan *p, const void *const *dev_inpu
     }
     destroy();
     return result;
+    MGI_ABI_CATCH("mgi_plan_autotune")
 }
 
 extern "C" mgi_status mgi_plan_node_config(const mgi_plan *p, int i, int *config, int *n_configs,
                                            const char **name) {
+    MGI_ABI_TRY
     if (!p) return fail(MGI_ERR_INVALID_ARG, "mgi_plan_node_config: null plan");
     if (i < 0 || i >= (int)p->nodes.size())
         return fail(MGI_ERR_INVALID_ARG, "mgi_plan_node_config: node index out of range");
@@ -623,9 +646,11 @@ extern "C" mgi_status mgi_plan_node_config(const mgi_plan *p, int i, int *config
     if (n_configs) *n_configs = nd.cfgs.empty() ? 1 : (int)nd.cfgs.size();
     if (name) *name = nd.cfgs.empty() ? nd.kname : nd.cfgs[nd.cfg].name.c_str();
     return MGI_OK;
+    MGI_ABI_CATCH("mgi_plan_node_config")
 }
 
 extern "C" mgi_status mgi_plan_set_node_config(mgi_plan *p, int i, int config) {
+    MGI_ABI_TRY
     if (!p) return fail(MGI_ERR_INVALID_ARG, "mgi_plan_set_node_config: null plan");
     if (i < 0 || i >= (int)p->nodes.size())
         return fail(MGI_ERR_INVALID_ARG, "mgi_plan_set_node_config: node index out of range");
@@ -636,9 +661,11 @@ extern "C" mgi_status mgi_plan_set_node_config(mgi_plan *p, int i, int config) {
     if (!nd.cfgs.empty()) nd.apply(config);
     release_graph(*p);
     return MGI_OK;
+    MGI_ABI_CATCH("mgi_plan_set_node_config")
 }
 
 extern "C" mgi_status mgi_plan_read_node(mgi_plan *p, int i, void *dev_dst, void *stream) {
+    MGI_ABI_TRY
     if (!p || !dev_dst) return fail(MGI_ERR_INVALID_ARG, "mgi_plan_read_node: null pointer");
     if (i < 0 || i >= (int)p->nodes.size())
         return fail(MGI_ERR_INVALID_ARG, "mgi_plan_read_node: node index out of range");
@@ -649,7 +676,7 @@ extern "C" mgi_status mgi_plan_read_node(mgi_plan *p, int i, void *dev_dst, void
     hipStream_t st = static_cast<hipStream_t>(stream);
     const Node &nd = p->nodes[i];
     const Buf &b = p->bufs[nd.out];
-    Bases B{static_cast<char *>(p->dev_ws), nullptr, p->last_outputs.data()};
+    Bases B{static_cast<char *>(p->last_ws ? p->last_ws : p->dev_ws), nullptr, p->last_outputs.data()};
     if (b.loc == Loc::Input) return fail(MGI_ERR_STATE, "mgi_plan_read_node: input buffer");
     void *src = buf_ptr(*p, nd.out, B);
     hipError_t e;
@@ -661,4 +688,5 @@ extern "C" mgi_status mgi_plan_read_node(mgi_plan *p, int i, void *dev_dst, void
     }
     if (e != hipSuccess) return hip_fail(e, "mgi_plan_read_node");
     return MGI_OK;
+    MGI_ABI_CATCH("mgi_plan_read_node")
 }

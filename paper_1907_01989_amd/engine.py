@@ -131,13 +131,42 @@ class Plan:
                 outs.append(torch.empty((n, h, w, c), dtype=tdt, device=self.device))
         return outs
 
+    def check_io(self, inputs, outputs):
+        """Raise ValueError unless ``inputs`` and ``outputs`` match the plan:
+        as many tensors as it has graph inputs and outputs, each a contiguous
+        tensor on this plan's device with the element type and byte size the
+        plan reads or writes.  The library receives raw device pointers, so a
+        tensor that fails any of these would make its kernels read or write
+        outside the buffer."""
+        import torch
+        inputs, outputs = list(inputs), list(outputs)
+        if len(inputs) != self.n_inputs or len(outputs) != self.n_outputs:
+            raise ValueError(f"plan takes {self.n_inputs} inputs and {self.n_outputs} outputs, "
+                             f"got {len(inputs)} and {len(outputs)}")
+        dev = torch.device(self.device)
+        in_types = {B.DTYPE_FP16: torch.float16, B.DTYPE_FP32: torch.float32}
+        out_types = {B.DTYPE_INT32: torch.int32, B.DTYPE_FP32: torch.float32}
+        for role, ts, info, types in (("input", inputs, self.inputs_info, in_types),
+                                      ("output", outputs, self.outputs_info, out_types)):
+            for i, (x, (shape, dt, nbytes)) in enumerate(zip(ts, info)):
+                if not isinstance(x, torch.Tensor):
+                    raise ValueError(f"{role} {i}: expected a torch tensor, got {type(x).__name__}")
+                if not x.is_cuda or x.device.index != (dev.index if dev.index is not None else
+                                                       torch.cuda.current_device()):
+                    raise ValueError(f"{role} {i}: tensor on {x.device}, plan on {self.device}")
+                if x.dtype != types.get(dt):
+                    raise ValueError(f"{role} {i}: dtype {x.dtype}, plan expects {types.get(dt)}")
+                if not x.is_contiguous() or x.numel() * x.element_size() != nbytes:
+                    raise ValueError(f"{role} {i}: must be a contiguous tensor of {nbytes} bytes "
+                                     f"(NHWC {shape}), got {tuple(x.shape)}")
+
     def run(self, inputs, outputs=None, stream=None):
         """Enqueue one forward pass; returns the output tensors (not synchronised)."""
+        if not self.bound:
+            raise RuntimeError("plan is not bound to device memory (call bind())")
         if outputs is None:
             outputs = self.alloc_outputs()
-        for x, (shape, dt, nbytes) in zip(inputs, self.inputs_info):
-            if x.numel() * x.element_size() != nbytes or not x.is_contiguous():
-                raise ValueError(f"input must be a contiguous NHWC tensor of {nbytes} bytes")
+        self.check_io(inputs, outputs)
         B.mgi_plan_run(self.handle, [x.data_ptr() for x in inputs],
                        [y.data_ptr() for y in outputs], _stream_handle(stream))
         return outputs
@@ -147,6 +176,7 @@ class Plan:
         and keep the fastest (see mgi_plan_autotune); synchronises."""
         if outputs is None:
             outputs = self.alloc_outputs()
+        self.check_io(inputs, outputs)
         B.mgi_plan_autotune(self.handle, [x.data_ptr() for x in inputs], [y.data_ptr() for y in outputs],
                             _stream_handle(stream), reps)
         self._graph_io = None
@@ -159,9 +189,7 @@ class Plan:
         tensors stay referenced by the plan so that their memory outlives it."""
         if outputs is None:
             outputs = self.alloc_outputs()
-        for x, (shape, dt, nbytes) in zip(inputs, self.inputs_info):
-            if x.numel() * x.element_size() != nbytes or not x.is_contiguous():
-                raise ValueError(f"input must be a contiguous NHWC tensor of {nbytes} bytes")
+        self.check_io(inputs, outputs)
         B.mgi_plan_capture(self.handle, [x.data_ptr() for x in inputs], [y.data_ptr() for y in outputs])
         self._graph_io = (list(inputs), list(outputs))
         return outputs

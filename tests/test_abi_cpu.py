@@ -40,6 +40,7 @@ def test_library_exports_every_declared_symbol():
 def test_status_strings():
     assert B.mgi_status_str(0) == "MGI_OK"
     assert B.mgi_status_str(3) == "MGI_ERR_UNSUPPORTED"
+    assert B.mgi_status_str(8) == "MGI_ERR_INTERNAL"
     assert B.mgi_status_str(99) == "MGI_ERR_UNKNOWN"
 
 
@@ -435,3 +436,44 @@ def test_softmax_fusion_state_region():
         split = engine.Plan(d, bind=False, fuse_softmax=False)
         assert fused.nodes()[-1]["kind"] == "fc_softmax" and fused.nodes()[-1]["n_fused"] == 2
         assert B.mgi_plan_workspace_bytes(fused.handle) == B.mgi_plan_workspace_bytes(split.handle) + 256
+
+
+def test_io_counts_and_tensor_checks_before_any_pointer_is_passed():
+    """The C calls take pointer arrays with no length: the binding checks the
+    counts against the plan, and the engine checks every tensor's device,
+    dtype, contiguity and byte size, before the library sees a pointer."""
+    import torch
+
+    import workloads
+    from paper_1907_01989_amd import engine
+    g = workloads.NetBuilder(seed=0)
+    x = g.input(1, 8, 8, 3, 0.0, 1.0)
+    t = g.conv(x, 16, 3, 2, name="stem")
+    p = g.gap(t, name="pool")
+    z = g.fc(p, 10, name="fc")
+    g.mark_output(z)
+    plan = engine.Plan(g.graph("io_checks"), bind=False)
+    try:
+        assert (plan.n_inputs, plan.n_outputs) == (1, 1)
+        with pytest.raises(ValueError, match="1 inputs and 1 outputs"):
+            B.mgi_plan_run(plan.handle, [], [1])
+        with pytest.raises(ValueError, match="1 inputs and 1 outputs"):
+            B.mgi_plan_capture(plan.handle, [1, 2], [1])
+        with pytest.raises(ValueError, match="1 inputs and 1 outputs"):
+            B.mgi_plan_autotune(plan.handle, [1], [], None, 3)
+        with pytest.raises(ValueError, match="node"):
+            B.mgi_plan_run_timed(plan.handle, [1], [1], [None], [None])
+        with pytest.raises(RuntimeError, match="not bound"):
+            plan.run([torch.zeros(1)])
+        xin = torch.zeros((1, 8, 8, 3), dtype=torch.float16)
+        out = torch.zeros((1, 10), dtype=torch.float32)
+        with pytest.raises(ValueError, match="inputs"):
+            plan.check_io([], [out])
+        with pytest.raises(ValueError, match="inputs"):
+            plan.check_io([xin], [out, out])
+        with pytest.raises(ValueError, match="input 0: tensor on cpu"):
+            plan.check_io([xin], [out])           # host memory is not a device pointer
+        with pytest.raises(ValueError, match="expected a torch tensor"):
+            plan.check_io([0x1000], [out])
+    finally:
+        plan.close()

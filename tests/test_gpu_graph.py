@@ -50,3 +50,32 @@ def test_graph_replay_matches_eager(net, batch):
         np.testing.assert_array_equal(g_.cpu().numpy(), r)
     assert any(not np.array_equal(a, b) for a, b in zip(ref, ref2))
     plan.close()
+
+
+def test_run_rejects_mismatched_device_tensors():
+    """Wrong element type, byte size or layout of a device tensor is refused
+    on the host, before any kernel is launched."""
+    import torch
+    from paper_1907_01989_amd import engine
+
+    g = workloads.NetBuilder(seed=0)
+    x = g.input(1, 16, 16, 3, 0.0, 1.0)
+    t = g.conv(x, 16, 3, 2, name="stem")
+    p = g.gap(t, name="pool")
+    z = g.fc(p, 10, name="fc")
+    g.mark_output(z)
+    plan = engine.Plan(g.graph("io_checks_gpu"))
+    log("[case] run argument checks")
+    xs = plan.input_tensors()
+    good = plan.alloc_outputs()
+    with pytest.raises(ValueError, match="dtype"):
+        plan.run([xs[0].float()], good)
+    with pytest.raises(ValueError, match="bytes"):
+        plan.run(xs, [torch.empty((1, 9), dtype=torch.float32, device="cuda:0")])
+    with pytest.raises(ValueError, match="contiguous"):
+        plan.run([xs[0].transpose(1, 2)], good)
+    with pytest.raises(ValueError, match="dtype"):
+        plan.run(xs, [torch.empty((1, 10), dtype=torch.int32, device="cuda:0")])
+    out = plan.run(xs, good)[0]
+    torch.cuda.synchronize()
+    assert torch.isfinite(out).all()

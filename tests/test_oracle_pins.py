@@ -268,6 +268,36 @@ def test_bilinear_midpoint_weights():
     np.testing.assert_array_equal(y, [0, 2, 4, 6, 8])
 
 
+def test_bilinear_half_scale_branch_by_hand():
+    """align_corners = 0: output sample d reads source coordinate d * in / out
+    (no half-pixel offset), the upper neighbour clamped to the last sample.
+    Worked by hand:
+      2 -> 4: src = 0, 0.5, 1, 1.5  ->  [a, (a+b)/2, b, b]  (1.5 clamps to b)
+      3 -> 2: src = 0, 1.5          ->  [x0, (x1+x2)/2]
+      4 -> 3: src = 0, 4/3, 8/3     ->  [x0, x1 + (x2-x1)/3, x2 + 2(x3-x2)/3]
+    A half-pixel-centre reading (src = (d+0.5)*in/out - 0.5) would give
+    [a, a + (b-a)/4, a + 3(b-a)/4, b] for the first case instead."""
+    a, b = 2.0, 10.0
+    x = np.array([a, b]).reshape(1, 1, 2, 1)
+    np.testing.assert_array_equal(oracle.resize_bilinear(x, 1, 4, False)[0, 0, :, 0],
+                                  [2.0, 6.0, 10.0, 10.0])
+    np.testing.assert_array_equal(oracle.resize_bilinear(x.reshape(1, 2, 1, 1), 4, 1, False)[0, :, 0, 0],
+                                  [2.0, 6.0, 10.0, 10.0])
+    x3 = np.array([1.0, 4.0, 10.0]).reshape(1, 1, 3, 1)
+    np.testing.assert_array_equal(oracle.resize_bilinear(x3, 1, 2, False)[0, 0, :, 0], [1.0, 7.0])
+    x4 = np.array([0.0, 3.0, 9.0, 12.0]).reshape(1, 4, 1, 1)
+    np.testing.assert_allclose(oracle.resize_bilinear(x4, 3, 1, False)[0, :, 0, 0],
+                               [0.0, 3.0 + 6.0 / 3.0, 9.0 + 2.0 * 3.0 / 3.0], rtol=0, atol=1e-14)
+    # 2-D: 2x2 -> 4x4 is the separable product of the 1-D weights above
+    q = np.array([[1.0, 3.0], [5.0, 11.0]]).reshape(1, 2, 2, 1)
+    row_w = np.array([[1, 0], [0.5, 0.5], [0, 1], [0, 1]])   # 2 -> 4, by hand
+    expect = row_w @ q[0, :, :, 0] @ row_w.T
+    np.testing.assert_array_equal(oracle.resize_bilinear(q, 4, 4, False)[0, :, :, 0], expect)
+    # 2x downscale 4 -> 2 takes samples 0 and 2 exactly (integer sources)
+    r = rnd((1, 4, 4, 3), 33)
+    np.testing.assert_array_equal(oracle.resize_bilinear(r, 2, 2, False), r[:, ::2, ::2, :])
+
+
 def test_argmax_ties_lowest_index():
     x = np.array([[1.0, 3.0, 3.0, 2.0], [5.0, 5.0, 5.0, 5.0], [-1.0, -2.0, -0.5, -0.5]]).reshape(1, 1, 3, 4)
     np.testing.assert_array_equal(oracle.argmax(x).ravel(), [1, 0, 2])
