@@ -264,6 +264,30 @@ mgi_status mgi_plan_bind(mgi_plan *p, void *dev_workspace, void *dev_weights, vo
 mgi_status mgi_plan_run(mgi_plan *p, const void *const *dev_inputs, void *const *dev_outputs,
                         void *stream);
 
+/* For callers that cannot allocate device memory while they run (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * as mgi_plan_run, but the plan's workspace (arena and state region) is the
+ * library's own no-allocation workspace, a static device array of
+ * MGI_NOALLOC_WORKSPACE_BYTES on each device, instead of the buffer given to
+ * mgi_plan_bind (which this call does not touch; weights still come from the
+ * bound weight buffer).  The array is placed when the library's kernels are
+ * loaded on a device and held until the process ends; the call allocates and
+ * frees nothing, on the device or through any library.  Its device address is
+ * looked up on the first call on each device (the device current at the
+ * call), so the first call is not capturable; later ones are (the state
+ * region is cleared with a kernel, not a memset).
+ *   Every call on one device shares that device's array: calls that overlap
+ * on a device (two streams, two threads, two plans) race and give undefined
+ * results; serialise them.  The array keeps the last call's contents, so
+ * mgi_plan_read_node after this call reads it and is valid only until the
+ * next call that uses it.
+ *   Errors: as mgi_plan_run; MGI_ERR_WORKSPACE, before anything is enqueued,
+ * when mgi_plan_workspace_bytes exceeds MGI_NOALLOC_WORKSPACE_BYTES (run such
+ * a plan with mgi_plan_run); MGI_ERR_HIP if the address lookup fails. */
+#define MGI_NOALLOC_WORKSPACE_BYTES (64u << 20)
+mgi_status mgi_plan_run_noalloc(mgi_plan *p, const void *const *dev_inputs, void *const *dev_outputs,
+                                void *stream);
+
 /* As mgi_plan_run, and timestamps node kernels: node i's kernel is launched
  * so that start_events[i] is recorded when it begins executing on the device
  * and stop_events[i] when it ends (hipEvent_t values; NULL entries are not

@@ -76,6 +76,7 @@ _SIGS = {
     "mgi_plan_io_info": ([P, I, I, IP, IP, IP, IP, IP, SP], I),
     "mgi_plan_bind": ([P, P, P, P], I),
     "mgi_plan_run": ([P, ctypes.POINTER(P), ctypes.POINTER(P), P], I),
+    "mgi_plan_run_noalloc": ([P, ctypes.POINTER(P), ctypes.POINTER(P), P], I),
     "mgi_plan_run_timed": ([P, ctypes.POINTER(P), ctypes.POINTER(P), P, ctypes.POINTER(P),
                             ctypes.POINTER(P)], I),
     "mgi_plan_capture": ([P, ctypes.POINTER(P), ctypes.POINTER(P)], I),
@@ -289,6 +290,14 @@ def _io_arrays(p, in_ptrs, out_ptrs):
 def mgi_plan_run(p, in_ptrs, out_ptrs, stream=None):
     ins, outs = _io_arrays(p, in_ptrs, out_ptrs)
     _check(lib().mgi_plan_run(p, ins, outs, P(stream or 0)))
+
+
+def mgi_plan_run_noalloc(p, in_ptrs, out_ptrs, stream=None):
+    ins, outs = _io_arrays(p, in_ptrs, out_ptrs)
+    _check(lib().mgi_plan_run_noalloc(p, ins, outs, P(stream or 0)))
+
+
+NOALLOC_WORKSPACE_BYTES = 64 << 20
 
 
 def mgi_plan_run_timed(p, in_ptrs, out_ptrs, start_events, stop_events, stream=None):

@@ -231,6 +231,9 @@ hipError_t launch_resize(const ResizeParams &p, bool argmax, hipStream_t st);
 hipError_t launch_argmax(const h8 *x, int *y, int M, int S, int C, bool bf16, hipStream_t st);
 
 hipError_t launch_ingest(const void *x, bool fp16_in, h8 *y, int M, int C, bool bf16, hipStream_t st);
+// sets `words` 32-bit words at dst to zero with a kernel (no memset node in a
+// captured graph)
+hipError_t launch_zero_words(unsigned *dst, size_t words, hipStream_t st);
 hipError_t launch_export(const h8 *x, float *y, int M, int C, bool bf16, hipStream_t st);
 
 }  // namespace kern

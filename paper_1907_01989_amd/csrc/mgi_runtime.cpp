@@ -439,7 +439,7 @@ extern "C" mgi_status mgi_plan_bind(mgi_plan *p, void *dev_workspace, void *dev_
 namespace {
 
 // Enqueues every node of a bound plan on `stream`, with the arena and state
-// region at `ws` (the bound workspace when null).
+// region at `ws` (the bound workspace, or the no-allocation workspace).
 mgi_status run_plan(mgi_plan *p, const void *const *dev_inputs, void *const *dev_outputs,
                     void *stream, void *const *start_ev, void *const *stop_ev, const char *who,
                     char *ws = nullptr) {
@@ -470,6 +470,41 @@ mgi_status run_plan(mgi_plan *p, const void *const *dev_inputs, void *const *dev
     return MGI_OK;
 }
 
+// ---------------------------------------------------------------------------
+// the no-allocation workspace: one array per device, placed by the code
+// object loader when the library's kernels are loaded on that device, never
+// allocated or freed by the library.  Host code must not use the array's name
+// as a device address (on the host it names a stand-in): the address is
+// looked up once per device with hipGetSymbolAddress and kept here.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) unsigned char scratch[MGI_NOALLOC_WORKSPACE_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's array, looked up on the first call
+// on that device.
+mgi_status noalloc_workspace(char **out, const char *who) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, who);
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(MGI_ERR_UNSUPPORTED, std::string(who) + ": device index " + std::to_string(dev) +
+                                             " beyond the " + std::to_string(kMaxDevices) + " supported");
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *ptr = nullptr;
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_fail(e, (std::string(who) + ": workspace address").c_str());
+        if (!ptr || ((uintptr_t)ptr & 255))
+            return fail(MGI_ERR_WORKSPACE, std::string(who) + ": workspace address not 256-byte aligned");
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = static_cast<char *>(g_scratch_ptr[dev]);
+    return MGI_OK;
+}
+
 }  // namespace
 
 extern "C" mgi_status mgi_plan_run(mgi_plan *p, const void *const *dev_inputs,
@@ -477,6 +512,31 @@ extern "C" mgi_status mgi_plan_run(mgi_plan *p, const void *const *dev_inputs,
     MGI_ABI_TRY
     return run_plan(p, dev_inputs, dev_outputs, stream, nullptr, nullptr, "mgi_plan_run");
     MGI_ABI_CATCH("mgi_plan_run")
+}
+
+extern "C" mgi_status mgi_plan_run_noalloc(mgi_plan *p, const void *const *dev_inputs,
+                                           void *const *dev_outputs, void *stream) {
+    MGI_ABI_TRY
+    const char *who = "mgi_plan_run_noalloc";
+    if (!p) return fail(MGI_ERR_INVALID_ARG, std::string(who) + ": null plan");
+    if (!p->bound) return fail(MGI_ERR_STATE, std::string(who) + ": plan is not bound");
+    if (p->workspace_bytes > (size_t)MGI_NOALLOC_WORKSPACE_BYTES)
+        return fail(MGI_ERR_WORKSPACE,
+                    std::string(who) + ": the plan needs a workspace of " + std::to_string(p->workspace_bytes) +
+                        " bytes, more than the " + std::to_string((size_t)MGI_NOALLOC_WORKSPACE_BYTES) +
+                        " bytes of the no-allocation workspace; run it with mgi_plan_run");
+    char *ws = nullptr;
+    mgi_status s = noalloc_workspace(&ws, who);
+    if (s != MGI_OK) return s;
+    // the array holds whatever the previous call on this device left there:
+    // the state region (arrival counters) must start at zero
+    if (p->state_bytes) {
+        hipError_t e = launch_zero_words(reinterpret_cast<unsigned *>(ws + p->state_off),
+                                         p->state_bytes / sizeof(unsigned), static_cast<hipStream_t>(stream));
+        if (e != hipSuccess) return hip_fail(e, (std::string(who) + ": state region").c_str());
+    }
+    return run_plan(p, dev_inputs, dev_outputs, stream, nullptr, nullptr, who, ws);
+    MGI_ABI_CATCH("mgi_plan_run_noalloc")
 }
 
 extern "C" mgi_status mgi_plan_run_timed(mgi_plan *p, const void *const *dev_inputs,

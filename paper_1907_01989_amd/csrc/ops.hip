@@ -240,6 +240,17 @@ hipError_t launch_act(const h8 *x, h8 *y, size_t count, int act, bool bf16, hipS
     return hipGetLastError();
 }
 
+__global__ __launch_bounds__(256) void zero_words_kernel(unsigned *p, size_t n) {
+    const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+    if (i < n) p[i] = 0u;
+}
+
+hipError_t launch_zero_words(unsigned *dst, size_t words, hipStream_t st) {
+    if (!words) return hipSuccess;
+    launch(zero_words_kernel, dim3(blocks_for(words, 256)), dim3(256), 0, st, dst, words);
+    return hipGetLastError();
+}
+
 // ---------------------------------------------------------------------------
 // global average pool: one 256-thread workgroup per (slice, image); thread t
 // sums pixels t, t + 256, ... four loads at a time (all issued before any
