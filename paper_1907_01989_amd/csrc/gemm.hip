@@ -19,6 +19,7 @@
 // Weight and activation tiles for four K slices (32 channels) per step are
 // staged through LDS, double-buffered with one barrier per step, the next
 // step's global loads issued before the current step's MFMAs.
+#include <algorithm>
 #include <cmath>
 
 #include "device.h"
@@ -793,16 +794,17 @@ __global__ __launch_bounds__(256) void stem_kernel(StemParams p, int th, int rs,
     }
 }
 
-static int stem_row_stride(int c, int w, int ow, int sw, int kw, int dw, int pl) {
+int stem_row_stride(int c, int w, int ow, int sw, int kh, int kw, int dw, int pl) {
     int rs = ((ow - 1) * sw + (kw - 1) * dw + 1) * c;
     rs = rs > (w + pl) * c ? rs : (w + pl) * c;
+    if (stem_row_aligned(kh, kw, c, dw) && rs < (ow - 1) * sw * c + 10) rs = (ow - 1) * sw * c + 10;
     return (rs + 7) & ~7;
 }
 
 size_t stem_band_bytes(int th, int kh, int kw, int c, int w, int ow, int sh, int sw, int dh, int dw,
                        int pl) {
     const int nrows = (th - 1) * sh + (kh - 1) * dh + 1;
-    return (size_t)nrows * stem_row_stride(c, w, ow, sw, kw, dw, pl) * 2;
+    return (size_t)nrows * stem_row_stride(c, w, ow, sw, kh, kw, dw, pl) * 2;
 }
 
 #ifndef MGI_STEM_ROWS
@@ -820,11 +822,11 @@ static hipError_t launch_stem_t(const StemParams &p, hipStream_t st) {
                              kStemStageBytes > 65536)
         th >>= 1;
     const int nrows = (th - 1) * p.sh + (p.KH - 1) * p.dh + 1;
-    const int rs = stem_row_stride(p.C, p.W, p.OW, p.sw, p.KW, p.dw, p.pl);
+    const int rs = stem_row_stride(p.C, p.W, p.OW, p.sw, p.KH, p.KW, p.dw, p.pl);
     const size_t lds = (size_t)nrows * rs * 2 + (size_t)4 * p.nb16 * 1024;   // band + per-wave staging
     if (lds > 65536 || p.K > 32) return hipErrorInvalidValue;
     StemParams q = p;
-    im2col_offsets(q.koff, p.K, p.C, p.KW, p.dh, p.dw, rs);
+    im2col_offsets(q.koff, p.K, p.KH, p.C, p.KW, p.dh, p.dw, rs);
     const dim3 grid(p.N * ((p.OH + th - 1) / th)), block(256);
     switch (p.nb16) {
         case 1: launch((stem_kernel<E, TIN, 1>), grid, block, lds, st, q, th, rs, nrows); break;
@@ -836,10 +838,25 @@ static hipError_t launch_stem_t(const StemParams &p, hipStream_t st) {
     return hipGetLastError();
 }
 
-void im2col_offsets(int *koff, int K, int C, int KW, int dh, int dw, int rs) {
+bool stem_row_aligned(int KH, int KW, int C, int dw) { return KH == 3 && KW * C == 9 && dw == 1; }
+
+int stem_kpos(int ky, int kx, int ci, int KH, int KW, int C, int dw) {
+    const int e = kx * C + ci;                   // entry within the window row
+    if (!stem_row_aligned(KH, KW, C, dw)) return ky * KW * C + e;
+    return e < 8 ? 8 * ky + e : 24 + 2 * ky;
+}
+
+void im2col_offsets(int *koff, int K, int KH, int C, int KW, int dh, int dw, int rs) {
+    const bool ra = stem_row_aligned(KH, KW, C, dw);
     for (int k = 0; k < 32; ++k) {
         int off = 0;
-        if (k < K) {
+        if (ra) {
+            // 8 values of row k / 8, or (from 24) the 9th and 10th value of
+            // rows 0, 1, 2, 2
+            const int ky = k < 24 ? k / 8 : std::min((k - 24) / 2, 2);
+            const int e = k < 24 ? k % 8 : 8 + (k - 24) % 2;
+            off = ky * dh * rs + e;
+        } else if (k < K) {
             const int tap = k / C, ci = k - tap * C;
             const int ky = tap / KW, kx = tap - ky * KW;
             off = ky * dh * rs + kx * dw * C + ci;

@@ -139,14 +139,31 @@ struct StemDwParams {
     h8 *y;               // depthwise output, sliced [ns][N * OH * OW]
     int OH, OW, S, dpt, dpl, ns, act2;
     int nbands, rs, pstride, band_h8; // set by launch_stemdw from the configuration
+    int srows, qi, vec;  // rolling strips: output rows per strip, input-ring slots, 16-byte input loads
+    int fp16_in;         // the graph input is fp16 (else fp32)
     int bf16;            // storage type: 0 fp16, 1 bf16
     int koff[32];        // set by launch_stemdw: offset of im2col entry k in the LDS band
 };
-// offsets of im2col entries k < 32 of a kh x kw window (k = (ky*kw + kx)*c +
-// ci) inside an input band of row stride rs; 0 past K (zero weights there)
-void im2col_offsets(int *koff, int K, int C, int KW, int dh, int dw, int rs);
+// A stem window (kh*kw*c <= 32 entries) is one MFMA K step of 32 positions.
+// Entry (ky, kx, ci) sits at position (ky*kw + kx)*c + ci, except in
+// row-aligned windows -- 3 rows of 9 entries (kw*c = 9, no horizontal
+// dilation: the 3x3 stem over RGB) -- where row ky's first 8 entries take
+// positions 8*ky .. 8*ky+7 and its 9th takes 24 + 2*ky (positions 25, 27,
+// 29, 30, 31 hold zero weights): 8 consecutive positions are then 8
+// consecutive values of one staged input row.
+bool stem_row_aligned(int KH, int KW, int C, int dw);
+int stem_kpos(int ky, int kx, int ci, int KH, int KW, int C, int dw);
+// offset of the value that im2col position k < 32 reads inside an input band
+// of row stride rs (positions with zero weights read values that are staged
+// anyway: the next value of the same row, or the band's first)
+void im2col_offsets(int *koff, int K, int KH, int C, int KW, int dh, int dw, int rs);
+// row stride, in 16-bit values (a multiple of 8), of a staged input band for
+// output width ow: every window value, and for row-aligned windows the value
+// after each row's 9th, lies inside the row
+int stem_row_stride(int c, int w, int ow, int sw, int kh, int kw, int dw, int pl);
 struct StemDwGeom {
     int rows, group, threads, nbands, rs, pstride, band_h8;
+    int roll, srows, qi, vec, prod;
     size_t lds;
 };
 // Number of fused configurations (band heights) that fit a shape (0: none);

@@ -39,6 +39,7 @@ void stemdw_shape(const mgi_plan &p, const Node &nd, kern::StemDwParams &q) {
     q.OH = nd.dw_out.h; q.OW = nd.dw_out.w; q.S = d.stride_h;
     q.dpt = d.pad_t; q.dpl = d.pad_l;
     q.ns = (nd.dw_out.c + 7) / 8; q.act2 = nd.dw_act;
+    q.fp16_in = p.bufs[nd.in[0]].in_dtype == MGI_DTYPE_FP16;
 }
 
 namespace {
@@ -1133,7 +1134,7 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
                         for (int ci = 0; ci < cin; ++ci) {
                             int ks, j;
                             if (nd.kind == NodeKind::Stem || nd.kind == NodeKind::StemDw) {
-                                int k = (ky * kw + kx) * cin + ci;
+                                const int k = kern::stem_kpos(ky, kx, ci, kh, kw, cin, op.conv.dil_w);
                                 ks = k / 8;
                                 j = k % 8;
                             } else {

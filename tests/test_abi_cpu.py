@@ -180,19 +180,20 @@ def test_pointwise_depthwise_fusion_structure():
 
 def test_stem_depthwise_fusion_structure():
     # the stem node absorbs dw1: at batch 64 the fused kernel (4- or 2-row
-    # bands) is the default and the split pair a candidate; at batch 1 (28
-    # bands) the split pair is the default unless asked for (fuse_stemdw = 2)
+    # bands, or rolling strips of 14, 16 or 28 rows) is the default and the
+    # split pair a candidate; at batch 1 (28 bands) the split pair is the
+    # default unless asked for (fuse_stemdw = 2)
     for net in (workloads.mobilenet_v1, workloads.mobilenet_v2):
         p = engine.Plan(net(64), bind=False)
         n0 = p.nodes()[0]
         assert n0["kind"] == "stem_dw" and n0["n_fused"] == 2 and tuple(n0["shape"]) == (64, 112, 112, 32)
         cfg, k, name = p.node_configs()[0]
-        assert name == "band4" and k == 3
+        assert name == "band4" and k == 6
         names = []
         for c in range(k):
             B.mgi_plan_set_node_config(p.handle, 0, c)
             names.append(p.node_configs()[0][2])
-        assert names == ["band4", "band2", "split"]
+        assert names == ["band4", "band2", "roll14", "roll16r4", "roll28", "split"]
     assert engine.Plan(workloads.mobilenet_v1(1), bind=False).node_configs()[0][2] == "split"
     assert engine.Plan(workloads.mobilenet_v1(1), bind=False, fuse_stemdw=2).node_configs()[0][2] == "band4"
     # a stride-2 depthwise after the stem is not fused
@@ -286,7 +287,7 @@ def test_node_configuration_candidates():
         elif n["kind"] == "pw_dw":
             assert 2 <= k <= 8 and name.startswith(("img", "band", "split"))
         elif n["kind"] == "stem_dw":
-            assert k == 3 and name.startswith(("band", "split"))
+            assert k == 6 and name.startswith(("band", "split"))
         elif n["kind"] == "pw_pool":
             assert 5 <= k <= 6 and name.startswith(("pool", "split"))
         elif n["kind"] == "fc_gemm":
