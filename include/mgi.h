@@ -322,10 +322,12 @@ mgi_status mgi_plan_read_node(mgi_plan *p, int i, void *dev_dst, void *stream);
  * (pointwise / implicit-GEMM, depthwise, fused pointwise -> depthwise) inside
  * `reps` whole runs of the plan, queued back to back (plus one warm-up run;
  * only the node's kernels are timestamped, so it meets its input as in a
- * run), and keeps the one with the lowest median time.  All candidates
- * produce bit-identical results.  Synchronises `stream` once per candidate;
- * releases a captured graph (capture again afterwards).  The output buffers hold no defined result afterwards: run the
- * plan again.  Errors: MGI_ERR_INVALID_ARG for reps outside 1..1000; run
+ * run), and keeps the one with the lowest median time (a candidate listed
+ * later replaces an earlier one only when more than 2% faster; fused forms
+ * are listed before split ones).  All candidates produce bit-identical
+ * results.  Synchronises `stream` once per candidate; releases a captured
+ * graph (capture again afterwards).  The output buffers hold no defined
+ * result afterwards: run the plan again.  Errors: MGI_ERR_INVALID_ARG for reps outside 1..1000; run
  * errors; MGI_ERR_HIP if timing fails. */
 mgi_status mgi_plan_autotune(mgi_plan *p, const void *const *dev_inputs, void *const *dev_outputs,
                              void *stream, int reps);

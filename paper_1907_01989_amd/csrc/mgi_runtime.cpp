@@ -610,7 +610,8 @@ extern "C" mgi_status mgi_plan_replay(mgi_plan *p, void *stream) {
 // configuration is launched reps + 1 times per candidate on the plan's own
 // buffers (after one full run has filled them), each launch timestamped on the
 // device; the one with the lowest median over the timed launches (the first
-// launch being a warm-up) is kept.  Candidates compute identical results, so tuning changes
+// launch being a warm-up) is kept, a later candidate replacing an earlier one
+// only when more than 2% faster.  Candidates compute identical results, so tuning changes
 // speed only.  A captured graph holds the old configurations and is released.
 extern "C" mgi_status mgi_plan_autotune(mgi_plan *p, const void *const *dev_inputs,
                                         void *const *dev_outputs, void *stream, int reps) {
@@ -680,10 +681,14 @@ extern "C" mgi_status mgi_plan_autotune(mgi_plan *p, const void *const *dev_inpu
                 result = hip_fail(e, "mgi_plan_autotune: timing");
                 break;
             }
-            // median of the runs after the first (which meets cold caches)
+            // median of the runs after the first (which meets cold caches);
+            // a later candidate must be more than 2% faster to replace an
+            // earlier one, so that run-to-run noise does not flip the choice
+            // (candidates are listed fused forms first, the split form of a
+            // fused node, which moves more bytes, last)
             std::sort(times.begin(), times.end());
             const float med = times[times.size() / 2];
-            if (med < best_ms) {
+            if (med < best_ms * 0.98f) {
                 best_ms = med;
                 best = (int)c;
             }

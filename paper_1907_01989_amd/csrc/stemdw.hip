@@ -410,12 +410,13 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) void st
         }
     };
 
-    // prologue: input rows of stem step 0, stem step 0, input rows of step 1
+    // prologue: input rows of stem step 0; stem step 0 while the input rows
+    // of step 1 load; those rows into the ring
     stage_issue(ib(0), ie(0));
     stage_store(ib(0), ie(0));
+    if (nsteps > 1) stage_issue(ie(0), ie(1));
     __syncthreads();
     stem_step(ub(0), ue(0));
-    if (nsteps > 1) stage_issue(ie(0), ie(1));
     __syncthreads();
     if (nsteps > 1) stage_store(ie(0), ie(1));
     __syncthreads();
@@ -441,7 +442,7 @@ struct Cfg {
 // unit, measured no faster on the 224 -> 112 stem: the node is bound by
 // vector-ALU work, not latency)
 constexpr Cfg kCfgs[] = {{4, 0, 512, 0, 0, 0, "band4"}, {2, 0, 512, 0, 0, 0, "band2"},
-                         {14, 0, 512, 1, 2, 0, "roll14"}, {16, 0, 512, 1, 4, 0, "roll16r4"},
+                         {14, 0, 512, 1, 2, 0, "roll14"}, {15, 0, 512, 1, 3, 0, "roll15r3"},
                          {28, 0, 512, 1, 2, 0, "roll28"}};
 constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
 constexpr int kRollUnits = 2;      // input load units per thread held across a phase
@@ -516,7 +517,7 @@ hipError_t launch_t(const StemDwParams &p, const StemDwGeom &g, hipStream_t st) 
         return hipGetLastError();                                                               \
     }
 #define MGI_STEMDW_NB(NB_) MGI_STEMDW(NB_, 4, NB_, 512) MGI_STEMDW(NB_, 2, NB_, 512) \
-    MGI_STEMDW_ROLL(NB_, 512, 2) MGI_STEMDW_ROLL(NB_, 512, 4)
+    MGI_STEMDW_ROLL(NB_, 512, 2) MGI_STEMDW_ROLL(NB_, 512, 3)
     MGI_STEMDW_NB(1) MGI_STEMDW_NB(2) MGI_STEMDW_NB(3) MGI_STEMDW_NB(4)
 #undef MGI_STEMDW_NB
 #undef MGI_STEMDW_ROLL
