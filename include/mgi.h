@@ -141,8 +141,9 @@ typedef struct {
 /* ---------------------------------------------------------------------------
  * errors
  * ------------------------------------------------------------------------- */
-/* Static text naming a status code.  Never NULL. */
-const char *mgi_status_str(mgi_status s);
+/* Static text naming a status code (an mgi_status value; any other int gives
+ * "MGI_ERR_UNKNOWN").  Never NULL. */
+const char *mgi_status_str(int status);
 /* Message of the most recent failed call on this thread ("" if none).  The
  * pointer stays valid until the next failing call on the same thread. */
 const char *mgi_last_error(void);
@@ -314,6 +315,16 @@ mgi_status mgi_plan_node_info(const mgi_plan *p, int i, const char **kind, int *
  * dev_dst on `stream`.  Requires materialize_all (MGI_ERR_STATE otherwise)
  * and a completed or stream-ordered run. */
 mgi_status mgi_plan_read_node(mgi_plan *p, int i, void *dev_dst, void *stream);
+
+/* Copy node i's output as stored: the channel-sliced 16-bit tensor (Sec. 4's
+ * slices, 8 channels each), [ceil(c/8)][n*h*w][8] values including the
+ * padding lanes of the last slice, raw fp16 (or bf16) bits, to dev_dst
+ * (ceil(c/8) * n*h*w * 16 bytes) on `stream`; *bytes receives that size (it
+ * may be queried with dev_dst NULL).  For checking that padding lanes hold
+ * zeros.  Requires materialize_all and an enqueued run (MGI_ERR_STATE), and a
+ * node whose output is stored sliced (MGI_ERR_UNSUPPORTED for fp32 logits,
+ * probabilities and labels). */
+mgi_status mgi_plan_read_node_raw(mgi_plan *p, int i, void *dev_dst, size_t *bytes, void *stream);
 
 /* Plan-time tuning (after Sec. 4.2, where work-group sizes are chosen by
  * measurement): runs the plan once with these device buffers (same

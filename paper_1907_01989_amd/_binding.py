@@ -9,7 +9,9 @@ import ctypes
 import os
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libmgi.so")
+# the engine library; MGI_LIB_PATH selects another build of it (e.g. the
+# sanitizer build of build_lib --sanitize)
+LIB_PATH = os.environ.get("MGI_LIB_PATH") or os.path.join(_HERE, "libmgi.so")
 
 MGI_OK = 0
 STATUS = {0: "MGI_OK", 1: "MGI_ERR_INVALID_ARG", 2: "MGI_ERR_SHAPE", 3: "MGI_ERR_UNSUPPORTED",
@@ -77,6 +79,7 @@ _SIGS = {
     "mgi_plan_bind": ([P, P, P, P], I),
     "mgi_plan_run": ([P, ctypes.POINTER(P), ctypes.POINTER(P), P], I),
     "mgi_plan_run_noalloc": ([P, ctypes.POINTER(P), ctypes.POINTER(P), P], I),
+    "mgi_plan_read_node_raw": ([P, I, P, SP, P], I),
     "mgi_plan_run_timed": ([P, ctypes.POINTER(P), ctypes.POINTER(P), P, ctypes.POINTER(P),
                             ctypes.POINTER(P)], I),
     "mgi_plan_capture": ([P, ctypes.POINTER(P), ctypes.POINTER(P)], I),
@@ -318,6 +321,13 @@ def mgi_plan_capture(p, in_ptrs, out_ptrs):
 def mgi_plan_autotune(p, in_ptrs, out_ptrs, stream=None, reps=5):
     ins, outs = _io_arrays(p, in_ptrs, out_ptrs)
     _check(lib().mgi_plan_autotune(p, ins, outs, P(stream or 0), reps))
+
+
+def mgi_plan_read_node_raw(p, i, dev_dst=None, stream=None):
+    """Bytes of node i's stored sliced output; copies them to dev_dst if given."""
+    nb = ctypes.c_size_t()
+    _check(lib().mgi_plan_read_node_raw(p, i, P(dev_dst or 0), ctypes.byref(nb), P(stream or 0)))
+    return nb.value
 
 
 def mgi_plan_node_config(p, i):

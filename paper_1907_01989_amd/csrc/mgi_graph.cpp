@@ -22,7 +22,7 @@ mgi_status fail(mgi_status s, const std::string &msg) {
 
 using namespace mgi;
 
-extern "C" const char *mgi_status_str(mgi_status s) {
+extern "C" const char *mgi_status_str(int s) {
     switch (s) {
         case MGI_OK: return "MGI_OK";
         case MGI_ERR_INVALID_ARG: return "MGI_ERR_INVALID_ARG";

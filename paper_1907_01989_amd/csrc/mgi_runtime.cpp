@@ -755,3 +755,25 @@ extern "C" mgi_status mgi_plan_read_node(mgi_plan *p, int i, void *dev_dst, void
     return MGI_OK;
     MGI_ABI_CATCH("mgi_plan_read_node")
 }
+
+extern "C" mgi_status mgi_plan_read_node_raw(mgi_plan *p, int i, void *dev_dst, size_t *bytes, void *stream) {
+    MGI_ABI_TRY
+    if (!p || !bytes) return fail(MGI_ERR_INVALID_ARG, "mgi_plan_read_node_raw: null pointer");
+    if (i < 0 || i >= (int)p->nodes.size())
+        return fail(MGI_ERR_INVALID_ARG, "mgi_plan_read_node_raw: node index out of range");
+    const Node &nd = p->nodes[i];
+    const Buf &b = p->bufs[nd.out];
+    if (b.layout != Layout::C8 || b.loc != Loc::Arena)
+        return fail(MGI_ERR_UNSUPPORTED, "mgi_plan_read_node_raw: node output is not stored sliced");
+    *bytes = b.bytes;
+    if (!dev_dst) return MGI_OK;
+    if (!p->opt.materialize_all)
+        return fail(MGI_ERR_STATE, "mgi_plan_read_node_raw: plan was finalized without materialize_all");
+    if (!p->bound || p->last_outputs.size() != p->output_bufs.size())
+        return fail(MGI_ERR_STATE, "mgi_plan_read_node_raw: no run has been enqueued");
+    const char *src = static_cast<const char *>(p->last_ws ? p->last_ws : p->dev_ws) + b.offset;
+    hipError_t e = hipMemcpyAsync(dev_dst, src, b.bytes, hipMemcpyDeviceToDevice, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "mgi_plan_read_node_raw");
+    return MGI_OK;
+    MGI_ABI_CATCH("mgi_plan_read_node_raw")
+}

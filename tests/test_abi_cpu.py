@@ -478,3 +478,34 @@ def test_io_counts_and_tensor_checks_before_any_pointer_is_passed():
             plan.check_io([0x1000], [out])
     finally:
         plan.close()
+
+
+def test_read_node_raw_sizes_and_errors():
+    """mgi_plan_read_node_raw: the stored size of a sliced node output can be
+    queried without a run; fp32 outputs are refused; a copy needs
+    materialize_all and an enqueued run."""
+    g = workloads.NetBuilder(seed=0)
+    x = g.input(2, 9, 9, 3, 0.0, 1.0)
+    t = g.conv(x, 13, 3, 2, name="stem")
+    p = g.gap(t, name="pool")
+    z = g.fc(p, 10, name="fc")
+    g.mark_output(z)
+    desc = g.graph("raw")
+    plan = engine.Plan(desc, bind=False, materialize_all=True)
+    try:
+        kinds = [n["kind"] for n in plan.nodes()]
+        i_stem = kinds.index("conv_stem")
+        n, h, w, c = plan.nodes()[i_stem]["shape"]
+        assert B.mgi_plan_read_node_raw(plan.handle, i_stem) == 2 * n * h * w * 16     # 13 -> 2 slices
+        i_fc = len(kinds) - 1
+        assert err(B.mgi_plan_read_node_raw, plan.handle, i_fc) == 3
+        assert err(B.mgi_plan_read_node_raw, plan.handle, 99) == 1
+        assert err(B.mgi_plan_read_node_raw, plan.handle, i_stem, 0x1000) == 4       # no run yet
+    finally:
+        plan.close()
+    plan = engine.Plan(desc, bind=False)
+    try:
+        kinds = [n["kind"] for n in plan.nodes()]
+        assert err(B.mgi_plan_read_node_raw, plan.handle, kinds.index("conv_stem"), 0x1000) == 4
+    finally:
+        plan.close()
