@@ -107,7 +107,9 @@ std::string tile_name(const GemmTile &t) {
 
 void pick_pipe_tile(GemmTile &t, size_t M, int npad);
 
-void add_configs(const mgi_plan &p, Node &nd, size_t M) {
+// Candidate tiles of a pointwise or implicit-GEMM node: the finalize-time
+// tile first, then pipelined, two-K-step and weight-slab tiles that fit.
+void add_gemm_configs(Node &nd, size_t M) {
     auto push = [&](const GemmTile &t) {
         for (const Node::Config &c : nd.cfgs)
             if (c.tile.pipe == t.pipe && c.tile.slab == t.slab && c.tile.bm == t.bm && c.tile.ks == t.ks &&
@@ -115,47 +117,51 @@ void add_configs(const mgi_plan &p, Node &nd, size_t M) {
                 return;
         nd.cfgs.push_back({t, 0, tile_name(t)});
     };
-    if (nd.kind == NodeKind::Gemm) {
-        push(nd.tile);
-        const int npad = nd.nb16 * 16;
-        if (!nd.taps) {
-            const int pipes[4][2] = {{128, 128}, {128, 64}, {64, 128}, {64, 64}};
-            for (auto &pb : pipes) {
-                if (pb[1] > 64 && npad <= 64) continue;
-                GemmTile t;
-                t.pipe = true;
-                t.bm = pb[0];
-                t.bn = pb[1];
-                push(t);
-            }
-            if (nd.ksp % 8 == 0) {            // two K-steps per ring stage
-                GemmTile t;
-                t.pipe = true;
-                t.ks = 8;
-                push(t);
-            }
-            const int slabs[4][2] = {{32, 32}, {16, 32}, {32, 64}, {16, 64}};
-            for (auto &sb : slabs) {
-                if (sb[1] > 32 && npad <= 32) continue;
-                const size_t lds = (size_t)(sb[1] / 16) * nd.ksp * 256 +
-                                   (size_t)4 * (sb[0] / 16) * (sb[1] / 16) * 1024;
-                if (lds > 65536) continue;
-                GemmTile t;
-                t.slab = true;
-                t.wm = sb[0];
-                t.bn = sb[1];
-                t.pf = nd.ksp >= 8 ? 2 : 1;
-                push(t);
-            }
-        }
-        const int ldss[5][2] = {{128, 128}, {64, 128}, {32, 128}, {64, 64}, {128, 64}};
-        for (auto &lb : ldss) {
-            if (lb[1] > 64 && npad <= 64) continue;
+    push(nd.tile);
+    const int npad = nd.nb16 * 16;
+    if (!nd.taps) {
+        const int pipes[4][2] = {{128, 128}, {128, 64}, {64, 128}, {64, 64}};
+        for (auto &pb : pipes) {
+            if (pb[1] > 64 && npad <= 64) continue;
             GemmTile t;
-            t.bm = lb[0];
-            t.bn = lb[1];
+            t.pipe = true;
+            t.bm = pb[0];
+            t.bn = pb[1];
             push(t);
         }
+        if (nd.ksp % 8 == 0) {            // two K-steps per ring stage
+            GemmTile t;
+            t.pipe = true;
+            t.ks = 8;
+            push(t);
+        }
+        const int slabs[4][2] = {{32, 32}, {16, 32}, {32, 64}, {16, 64}};
+        for (auto &sb : slabs) {
+            if (sb[1] > 32 && npad <= 32) continue;
+            const size_t lds = (size_t)(sb[1] / 16) * nd.ksp * 256 +
+                               (size_t)4 * (sb[0] / 16) * (sb[1] / 16) * 1024;
+            if (lds > 65536) continue;
+            GemmTile t;
+            t.slab = true;
+            t.wm = sb[0];
+            t.bn = sb[1];
+            t.pf = nd.ksp >= 8 ? 2 : 1;
+            push(t);
+        }
+    }
+    const int ldss[5][2] = {{128, 128}, {64, 128}, {32, 128}, {64, 64}, {128, 64}};
+    for (auto &lb : ldss) {
+        if (lb[1] > 64 && npad <= 64) continue;
+        GemmTile t;
+        t.bm = lb[0];
+        t.bn = lb[1];
+        push(t);
+    }
+}
+
+void add_configs(const mgi_plan &p, Node &nd, size_t M) {
+    if (nd.kind == NodeKind::Gemm) {
+        add_gemm_configs(nd, M);
     } else if (nd.kind == NodeKind::PwDw) {
         // channels per workgroup of the fused pointwise + depthwise kernel, and
         // the two separate kernels through the scratch tensor (pipelined GEMM
@@ -604,9 +610,7 @@ mgi_status build_plan(const mgi_graph &g, const mgi_options &o, mgi_plan &p) {
 
 namespace {
 
-mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p) {
-    const int nops = (int)g.ops.size();
-    if (g.outputs.empty()) return fail(MGI_ERR_STATE, "mgi_graph_finalize: no output marked");
+mgi_status check_options(const mgi_options &o) {
     if (o.planner != MGI_PLANNER_NAIVE && o.planner != MGI_PLANNER_GREEDY && o.planner != MGI_PLANNER_MCFP)
         return fail(MGI_ERR_UNSUPPORTED, "mgi_graph_finalize: unknown planner");
     if (o.dtype != MGI_DTYPE_FP16 && o.dtype != MGI_DTYPE_BF16)
@@ -619,17 +623,22 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
         return fail(MGI_ERR_INVALID_ARG, "mgi_graph_finalize: fuse_pool is 0, 1 or 2");
     if (o.fuse_softmax < 0 || o.fuse_softmax > 1)
         return fail(MGI_ERR_INVALID_ARG, "mgi_graph_finalize: fuse_softmax is 0 or 1");
-    auto to_bits = o.dtype == MGI_DTYPE_BF16 ? f32_to_bf16_bits : f32_to_f16_bits;
+    return MGI_OK;
+}
 
-    const std::vector<char> live = live_ops(g);
+// Element-wise operator fusion (Sec. 3.2): an activation or an add whose
+// operand is the private output of a convolution (or of another fusible
+// group), and an argmax of a resize, join that group; every other live
+// operator starts its own.  Groups come back in execution order (the
+// position of the last absorbed operator).
+std::vector<Group> group_operators(const mgi_graph &g, const mgi_options &o, const std::vector<char> &live) {
+    const int nops = (int)g.ops.size();
     std::vector<char> is_output(nops, 0);
     for (int t : g.outputs) is_output[t] = 1;
     std::vector<std::vector<int>> consumers(nops);
     for (int i = 0; i < nops; ++i)
         if (live[i])
             for (int t : g.ops[i].in) consumers[t].push_back(i);
-
-    // ---------------------------------------------------------------- fusion
     std::vector<int> group_of(nops, -1);
     std::vector<Group> groups;
     auto single_private_use = [&](int t) {
@@ -696,21 +705,41 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
         group_of[i] = (int)groups.size();
         groups.push_back(G);
     }
-    // execution order: position of the last absorbed op
-    std::vector<int> order(groups.size());
-    for (size_t k = 0; k < groups.size(); ++k) order[k] = (int)k;
-    std::stable_sort(order.begin(), order.end(),
-                     [&](int a, int b) { return groups[a].last < groups[b].last; });
+    std::stable_sort(groups.begin(), groups.end(), [](const Group &a, const Group &b) { return a.last < b.last; });
+    return groups;
+}
 
-    // ------------------------------------------------------- buffers, nodes
-    p.bufs.clear();
-    p.nodes.clear();
-    std::vector<int> c8_buf(nops, -1);   // graph tensor -> C8 (or other) buffer holding it
-    std::vector<int> flat_buf(nops, -1); // graph tensor -> F32 / I32 buffer
-    std::vector<int> in_buf(nops, -1);   // graph input tensor -> NHWC_IN buffer
-    std::vector<int> out_index(nops, -1);
-    for (size_t k = 0; k < g.outputs.size(); ++k) out_index[g.outputs[k]] = (int)k;
 
+// Buffers and nodes for the operator groups: every graph input gets a buffer
+// read in place, every group one node (lower), graph outputs an fp32 / int32
+// buffer of the caller.
+struct Lowering {
+    const mgi_graph &g;
+    mgi_plan &p;
+    std::vector<int> c8_buf;     // graph tensor -> C8 (or other) buffer holding it
+    std::vector<int> flat_buf;   // graph tensor -> F32 / I32 buffer
+    std::vector<int> in_buf;     // graph input tensor -> NHWC_IN buffer
+    std::vector<int> out_index;  // graph tensor -> graph output index
+
+    Lowering(const mgi_graph &g_, mgi_plan &p_)
+        : g(g_), p(p_), c8_buf(g_.ops.size(), -1), flat_buf(g_.ops.size(), -1), in_buf(g_.ops.size(), -1),
+          out_index(g_.ops.size(), -1) {
+        for (size_t k = 0; k < g.outputs.size(); ++k) out_index[g.outputs[k]] = (int)k;
+    }
+    void add_inputs();
+    int new_buf(Layout L, const Shape &s, int tensor);
+    int add_node(Node &&nd) {
+        p.nodes.push_back(std::move(nd));
+        return (int)p.nodes.size() - 1;
+    }
+    int need_c8(int t);
+    mgi_status lower_conv(const Group &G, const GOp &op, const Shape &out_shape, Node &nd);
+    mgi_status lower_other(const Group &G, const GOp &op, const Shape &out_shape, Node &nd);
+    mgi_status lower(const Group &G);
+    mgi_status bind_outputs();
+};
+
+void Lowering::add_inputs() {
     p.input_bufs.clear();
     p.input_shapes.clear();
     p.input_dtypes.clear();
@@ -731,272 +760,304 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
         p.bufs.push_back(b);
     }
 
-    auto new_buf = [&](Layout L, const Shape &s, int tensor) {
-        Buf b;
-        b.layout = L;
-        b.shape = s;
-        if (L == Layout::C8) b.bytes = (size_t)slices(s.c) * 8 * s.pixels() * 2;
-        else b.bytes = s.elems() * 4;
-        b.graph_tensor = tensor;
-        if (tensor >= 0 && out_index[tensor] >= 0 && L != Layout::C8) {
-            b.loc = Loc::Output;
-            b.index = out_index[tensor];
-        }
-        p.bufs.push_back(b);
-        return (int)p.bufs.size() - 1;
-    };
-    auto add_node = [&](Node &&nd) {
-        p.nodes.push_back(std::move(nd));
-        return (int)p.nodes.size() - 1;
-    };
-    // a C8 view of graph tensor t, converting a graph input on first use
-    auto need_c8 = [&](int t) -> int {
-        if (c8_buf[t] >= 0) return c8_buf[t];
-        if (g.ops[t].kind == OpKind::Input) {
-            Node nd;
-            nd.kind = NodeKind::Ingest;
-            nd.kname = "ingest";
-            nd.op = t;
-            nd.out_tensor = -1;
-            nd.n_fused = 0;
-            nd.in = {in_buf[t]};
-            nd.out = new_buf(Layout::C8, g.ops[t].out, -1);
-            const int ob = nd.out;
-            add_node(std::move(nd));
-            c8_buf[t] = ob;
-            return ob;
-        }
-        return -1;
-    };
+}
 
-    for (int gk : order) {
-        const Group &G = groups[gk];
-        const GOp &op = g.ops[G.head];
-        const Shape out_shape = g.ops[G.last].out;
+int Lowering::new_buf(Layout L, const Shape &s, int tensor) {
+    Buf b;
+    b.layout = L;
+    b.shape = s;
+    if (L == Layout::C8) b.bytes = (size_t)slices(s.c) * 8 * s.pixels() * 2;
+    else b.bytes = s.elems() * 4;
+    b.graph_tensor = tensor;
+    if (tensor >= 0 && out_index[tensor] >= 0 && L != Layout::C8) {
+        b.loc = Loc::Output;
+        b.index = out_index[tensor];
+    }
+    p.bufs.push_back(b);
+    return (int)p.bufs.size() - 1;
+}
+
+// a C8 view of graph tensor t, converting a graph input on first use
+int Lowering::need_c8(int t) {
+    if (c8_buf[t] >= 0) return c8_buf[t];
+    if (g.ops[t].kind == OpKind::Input) {
         Node nd;
-        nd.op = G.head;
-        nd.out_tensor = G.last;
-        nd.n_fused = G.n;
-        nd.act1 = G.act1;
-        nd.act2 = G.act2;
-        switch (op.kind) {
-            case OpKind::Conv2d: {
-                const Shape x = g.ops[op.in[0]].out;
-                const mgi_conv_desc &d = op.conv;
-                nd.conv = d;
-                const bool from_input = g.ops[op.in[0]].kind == OpKind::Input;
-                // LDS for a one-row band of the stem kernel (graph inputs up to a few
-                // thousand pixels wide); wider inputs take the sliced path
-                const int ow = out_shape.w;
-                const int rs = std::max(((ow - 1) * d.stride_w + (d.kw - 1) * d.dil_w + 1) * x.c,
-                                        (x.w + d.pad_l) * x.c);
-                const size_t band1 = (size_t)((d.kh - 1) * d.dil_h + 1) * (rs + 7) * 2;
-                if (from_input && d.kh * d.kw * x.c <= 32 && d.cout <= 64 && band1 + kern::kStemStageBytes <= 65536) {
-                    nd.kind = NodeKind::Stem;
-                    nd.kname = "conv_stem";
-                    nd.in = {in_buf[op.in[0]]};
-                    nd.ksl = 4;
-                    nd.ksp = 4;
-                } else {
-                    int xb = need_c8(op.in[0]);
-                    if (xb < 0) return fail(MGI_ERR_UNSUPPORTED, "conv2d input has no sliced form");
-                    nd.kind = NodeKind::Gemm;
-                    nd.in = {xb};
-                    nd.taps = !(d.kh == 1 && d.kw == 1 && d.stride_h == 1 && d.stride_w == 1 &&
-                                d.pad_t == 0 && d.pad_b == 0 && d.pad_l == 0 && d.pad_r == 0);
-                    nd.kname = nd.taps ? "conv_igemm" : "pw_gemm";
-                    nd.ksl = d.kh * d.kw * slices(x.c);
-                    nd.ksp = (nd.ksl + 3) / 4 * 4;
-                }
-                nd.nb16 = (d.cout + 15) / 16;
-                nd.tile = pick_tile(out_shape.pixels(), d.cout);
-                if (nd.kind == NodeKind::Gemm && !nd.taps && nd.ksl >= 8 && nd.nb16 * 16 >= 64) {
-                    pick_pipe_tile(nd.tile, out_shape.pixels(), nd.nb16 * 16);
-                } else if (nd.kind == NodeKind::Gemm && !nd.taps) {
-                    // weight-slab kernel: 128 x 32 tiles, two K steps of
-                    // prefetch when there are at least two; the slab (32
-                    // channels x all K) plus the epilogue tiles fit 64 KiB
-                    // up to K = 768
-                    const size_t slab = (size_t)2 * nd.ksp * 256 + 16384;
-                    if (slab <= 65536) {
-                        nd.tile.slab = true;
-                        nd.tile.wm = 32;
-                        nd.tile.bn = 32;
-                        nd.tile.pf = nd.ksp >= 8 ? 2 : 1;
-                    }
-                }
-                if (G.residual_tensor >= 0) {
-                    int rb = need_c8(G.residual_tensor);
-                    if (rb < 0) rb = c8_buf[G.residual_tensor];
-                    if (rb < 0) return fail(MGI_ERR_UNSUPPORTED, "residual operand has no sliced form");
-                    nd.residual = rb;
-                }
-                nd.out = new_buf(Layout::C8, out_shape, G.last);
-                c8_buf[G.last] = nd.out;
-                break;
-            }
-            case OpKind::Depthwise: {
-                int xb = need_c8(op.in[0]);
-                if (xb < 0) return fail(MGI_ERR_UNSUPPORTED, "depthwise input has no sliced form");
-                nd.kind = NodeKind::Depthwise;
-                nd.kname = "dw_conv";
-                nd.conv = op.conv;
-                nd.in = {xb};
-                nd.out = new_buf(Layout::C8, out_shape, G.last);
-                c8_buf[G.last] = nd.out;
-                break;
-            }
-            case OpKind::Add:
-            case OpKind::Activation: {
-                nd.kind = op.kind == OpKind::Add ? NodeKind::Add : NodeKind::Act;
-                nd.kname = op.kind == OpKind::Add ? "add" : "activation";
-                for (int t : op.in) {
-                    int b = need_c8(t);
-                    if (b < 0) b = c8_buf[t];
-                    if (b < 0) return fail(MGI_ERR_UNSUPPORTED, "element-wise operand is not sliced");
-                    nd.in.push_back(b);
-                }
-                nd.out = new_buf(Layout::C8, out_shape, G.last);
-                c8_buf[G.last] = nd.out;
-                break;
-            }
-            case OpKind::GlobalAvgPool: {
-                int xb = need_c8(op.in[0]);
-                if (xb < 0) xb = c8_buf[op.in[0]];
-                if (xb < 0) return fail(MGI_ERR_UNSUPPORTED, "pool input is not sliced");
-                nd.kind = NodeKind::Gap;
-                nd.kname = "global_avgpool";
-                nd.in = {xb};
-                nd.out = new_buf(Layout::C8, out_shape, G.last);
-                c8_buf[G.last] = nd.out;
-                break;
-            }
-            case OpKind::FC: {
-                int xb = need_c8(op.in[0]);
-                if (xb < 0) xb = c8_buf[op.in[0]];
-                if (xb < 0)
-                    return fail(MGI_ERR_UNSUPPORTED, "fc input must come from a sliced tensor");
-                const Shape x = g.ops[op.in[0]].out;
-                nd.kind = NodeKind::FC;
-                nd.kname = "fc_gemm";
-                nd.in = {xb};
-                nd.ksl = slices(x.c);
-                nd.ksp = (nd.ksl + 3) / 4 * 4;
-                nd.nb16 = (op.cout + 15) / 16;
-                nd.conv.cout = op.cout;
-                nd.tile = pick_tile(out_shape.pixels(), op.cout);
-                nd.out = new_buf(Layout::F32, out_shape, G.last);
-                flat_buf[G.last] = nd.out;
-                break;
-            }
-            case OpKind::Softmax: {
-                int t = op.in[0];
-                int xb = flat_buf[t];
-                if (xb < 0) {
-                    int cb = need_c8(t);
-                    if (cb < 0) cb = c8_buf[t];
-                    if (cb < 0) return fail(MGI_ERR_UNSUPPORTED, "softmax input unavailable");
-                    Node ex;
-                    ex.kind = NodeKind::Export;
-                    ex.kname = "export";
-                    ex.out_tensor = -1;
-                    ex.n_fused = 0;
-                    ex.in = {cb};
-                    ex.out = new_buf(Layout::F32, g.ops[t].out, -1);
-                    xb = ex.out;
-                    add_node(std::move(ex));
-                }
-                nd.kind = NodeKind::Softmax;
-                nd.kname = "softmax";
-                nd.in = {xb};
-                nd.out = new_buf(Layout::F32, out_shape, G.last);
-                flat_buf[G.last] = nd.out;
-                break;
-            }
-            case OpKind::Concat: {
-                nd.kind = NodeKind::Concat;
-                nd.kname = "concat";
-                for (int t : op.in) {
-                    int b = need_c8(t);
-                    if (b < 0) b = c8_buf[t];
-                    if (b < 0) return fail(MGI_ERR_UNSUPPORTED, "concat operand is not sliced");
-                    nd.in.push_back(b);
-                }
-                nd.out = new_buf(Layout::C8, out_shape, G.last);
-                c8_buf[G.last] = nd.out;
-                break;
-            }
-            case OpKind::ResizeBilinear: {
-                int xb = need_c8(op.in[0]);
-                if (xb < 0) xb = c8_buf[op.in[0]];
-                if (xb < 0) return fail(MGI_ERR_UNSUPPORTED, "resize input is not sliced");
-                nd.in = {xb};
-                nd.align_corners = op.align_corners;
-                if (G.resize_argmax) {
-                    nd.kind = NodeKind::ResizeArgmax;
-                    nd.kname = "resize_argmax";
-                    nd.out = new_buf(Layout::I32, out_shape, G.last);
-                    flat_buf[G.last] = nd.out;
-                } else {
-                    nd.kind = NodeKind::Resize;
-                    nd.kname = "resize_bilinear";
-                    nd.out = new_buf(Layout::C8, out_shape, G.last);
-                    c8_buf[G.last] = nd.out;
-                }
-                break;
-            }
-            case OpKind::Argmax: {
-                int xb = need_c8(op.in[0]);
-                if (xb < 0) xb = c8_buf[op.in[0]];
-                if (xb < 0) return fail(MGI_ERR_UNSUPPORTED, "argmax input is not sliced");
-                nd.kind = NodeKind::Argmax;
-                nd.kname = "argmax";
-                nd.in = {xb};
-                nd.out = new_buf(Layout::I32, out_shape, G.last);
-                flat_buf[G.last] = nd.out;
-                break;
-            }
-            case OpKind::Pad: {
-                int xb = need_c8(op.in[0]);
-                if (xb < 0) xb = c8_buf[op.in[0]];
-                if (xb < 0) return fail(MGI_ERR_UNSUPPORTED, "pad input is not sliced");
-                nd.kind = NodeKind::Pad;
-                nd.kname = "pad";
-                nd.in = {xb};
-                nd.conv.pad_t = op.pads[0];
-                nd.conv.pad_l = op.pads[2];
-                nd.out = new_buf(Layout::C8, out_shape, G.last);
-                c8_buf[G.last] = nd.out;
-                break;
-            }
-            case OpKind::Input:
-                break;
-        }
+        nd.kind = NodeKind::Ingest;
+        nd.kname = "ingest";
+        nd.op = t;
+        nd.out_tensor = -1;
+        nd.n_fused = 0;
+        nd.in = {in_buf[t]};
+        nd.out = new_buf(Layout::C8, g.ops[t].out, -1);
+        const int ob = nd.out;
         add_node(std::move(nd));
-        // a sliced tensor that is a graph output is exported right away
-        const int t = G.last;
-        if (out_index[t] >= 0 && c8_buf[t] >= 0 && p.bufs[c8_buf[t]].layout == Layout::C8 &&
-            flat_buf[t] < 0) {
-            Node ex;
-            ex.kind = NodeKind::Export;
-            ex.kname = "export";
-            ex.out_tensor = -1;
-            ex.n_fused = 0;
-            ex.in = {c8_buf[t]};
-            Buf b;
-            b.layout = Layout::F32;
-            b.shape = g.ops[t].out;
-            b.bytes = b.shape.elems() * 4;
-            b.loc = Loc::Output;
-            b.index = out_index[t];
-            b.graph_tensor = t;
-            p.bufs.push_back(b);
-            ex.out = (int)p.bufs.size() - 1;
-            flat_buf[t] = ex.out;
-            add_node(std::move(ex));
+        c8_buf[t] = ob;
+        return ob;
+    }
+    return -1;
+}
+
+// A convolution group: the stem kernel when it reads a graph input through a
+// window of at most 32 values, otherwise a GEMM (pointwise) or implicit GEMM
+// over the sliced input, with the residual operand of a fused add.
+mgi_status Lowering::lower_conv(const Group &G, const GOp &op, const Shape &out_shape, Node &nd) {
+    const Shape x = g.ops[op.in[0]].out;
+    const mgi_conv_desc &d = op.conv;
+    nd.conv = d;
+    const bool from_input = g.ops[op.in[0]].kind == OpKind::Input;
+    // LDS for a one-row band of the stem kernel (graph inputs up to a few
+    // thousand pixels wide); wider inputs take the sliced path
+    const int ow = out_shape.w;
+    const int rs = std::max(((ow - 1) * d.stride_w + (d.kw - 1) * d.dil_w + 1) * x.c,
+                            (x.w + d.pad_l) * x.c);
+    const size_t band1 = (size_t)((d.kh - 1) * d.dil_h + 1) * (rs + 7) * 2;
+    if (from_input && d.kh * d.kw * x.c <= 32 && d.cout <= 64 && band1 + kern::kStemStageBytes <= 65536) {
+        nd.kind = NodeKind::Stem;
+        nd.kname = "conv_stem";
+        nd.in = {in_buf[op.in[0]]};
+        nd.ksl = 4;
+        nd.ksp = 4;
+    } else {
+        int xb = need_c8(op.in[0]);
+        if (xb < 0) return fail(MGI_ERR_UNSUPPORTED, "conv2d input has no sliced form");
+        nd.kind = NodeKind::Gemm;
+        nd.in = {xb};
+        nd.taps = !(d.kh == 1 && d.kw == 1 && d.stride_h == 1 && d.stride_w == 1 &&
+                    d.pad_t == 0 && d.pad_b == 0 && d.pad_l == 0 && d.pad_r == 0);
+        nd.kname = nd.taps ? "conv_igemm" : "pw_gemm";
+        nd.ksl = d.kh * d.kw * slices(x.c);
+        nd.ksp = (nd.ksl + 3) / 4 * 4;
+    }
+    nd.nb16 = (d.cout + 15) / 16;
+    nd.tile = pick_tile(out_shape.pixels(), d.cout);
+    if (nd.kind == NodeKind::Gemm && !nd.taps && nd.ksl >= 8 && nd.nb16 * 16 >= 64) {
+        pick_pipe_tile(nd.tile, out_shape.pixels(), nd.nb16 * 16);
+    } else if (nd.kind == NodeKind::Gemm && !nd.taps) {
+        // weight-slab kernel: 128 x 32 tiles, two K steps of
+        // prefetch when there are at least two; the slab (32
+        // channels x all K) plus the epilogue tiles fit 64 KiB
+        // up to K = 768
+        const size_t slab = (size_t)2 * nd.ksp * 256 + 16384;
+        if (slab <= 65536) {
+            nd.tile.slab = true;
+            nd.tile.wm = 32;
+            nd.tile.bn = 32;
+            nd.tile.pf = nd.ksp >= 8 ? 2 : 1;
         }
     }
+    if (G.residual_tensor >= 0) {
+        int rb = need_c8(G.residual_tensor);
+        if (rb < 0) rb = c8_buf[G.residual_tensor];
+        if (rb < 0) return fail(MGI_ERR_UNSUPPORTED, "residual operand has no sliced form");
+        nd.residual = rb;
+    }
+    nd.out = new_buf(Layout::C8, out_shape, G.last);
+    c8_buf[G.last] = nd.out;
+    return MGI_OK;
+}
 
+// One node for an operator group (Sec. 3.2: the element-wise operators a
+// group absorbed run in the head operator's epilogue), plus an export node
+// when the group's output is a graph output kept in sliced form.
+// Groups headed by a fully-connected layer, softmax, concatenation, resize,
+// argmax or padding.
+mgi_status Lowering::lower_other(const Group &G, const GOp &op, const Shape &out_shape, Node &nd) {
+    switch (op.kind) {
+        case OpKind::FC: {
+            int xb = need_c8(op.in[0]);
+            if (xb < 0) xb = c8_buf[op.in[0]];
+            if (xb < 0)
+                return fail(MGI_ERR_UNSUPPORTED, "fc input must come from a sliced tensor");
+            const Shape x = g.ops[op.in[0]].out;
+            nd.kind = NodeKind::FC;
+            nd.kname = "fc_gemm";
+            nd.in = {xb};
+            nd.ksl = slices(x.c);
+            nd.ksp = (nd.ksl + 3) / 4 * 4;
+            nd.nb16 = (op.cout + 15) / 16;
+            nd.conv.cout = op.cout;
+            nd.tile = pick_tile(out_shape.pixels(), op.cout);
+            nd.out = new_buf(Layout::F32, out_shape, G.last);
+            flat_buf[G.last] = nd.out;
+            return MGI_OK;
+        }
+        case OpKind::Softmax: {
+            int t = op.in[0];
+            int xb = flat_buf[t];
+            if (xb < 0) {
+                int cb = need_c8(t);
+                if (cb < 0) cb = c8_buf[t];
+                if (cb < 0) return fail(MGI_ERR_UNSUPPORTED, "softmax input unavailable");
+                Node ex;
+                ex.kind = NodeKind::Export;
+                ex.kname = "export";
+                ex.out_tensor = -1;
+                ex.n_fused = 0;
+                ex.in = {cb};
+                ex.out = new_buf(Layout::F32, g.ops[t].out, -1);
+                xb = ex.out;
+                add_node(std::move(ex));
+            }
+            nd.kind = NodeKind::Softmax;
+            nd.kname = "softmax";
+            nd.in = {xb};
+            nd.out = new_buf(Layout::F32, out_shape, G.last);
+            flat_buf[G.last] = nd.out;
+            return MGI_OK;
+        }
+        case OpKind::Concat: {
+            nd.kind = NodeKind::Concat;
+            nd.kname = "concat";
+            for (int t : op.in) {
+                int b = need_c8(t);
+                if (b < 0) b = c8_buf[t];
+                if (b < 0) return fail(MGI_ERR_UNSUPPORTED, "concat operand is not sliced");
+                nd.in.push_back(b);
+            }
+            nd.out = new_buf(Layout::C8, out_shape, G.last);
+            c8_buf[G.last] = nd.out;
+            return MGI_OK;
+        }
+        case OpKind::ResizeBilinear: {
+            int xb = need_c8(op.in[0]);
+            if (xb < 0) xb = c8_buf[op.in[0]];
+            if (xb < 0) return fail(MGI_ERR_UNSUPPORTED, "resize input is not sliced");
+            nd.in = {xb};
+            nd.align_corners = op.align_corners;
+            if (G.resize_argmax) {
+                nd.kind = NodeKind::ResizeArgmax;
+                nd.kname = "resize_argmax";
+                nd.out = new_buf(Layout::I32, out_shape, G.last);
+                flat_buf[G.last] = nd.out;
+            } else {
+                nd.kind = NodeKind::Resize;
+                nd.kname = "resize_bilinear";
+                nd.out = new_buf(Layout::C8, out_shape, G.last);
+                c8_buf[G.last] = nd.out;
+            }
+            return MGI_OK;
+        }
+        case OpKind::Argmax: {
+            int xb = need_c8(op.in[0]);
+            if (xb < 0) xb = c8_buf[op.in[0]];
+            if (xb < 0) return fail(MGI_ERR_UNSUPPORTED, "argmax input is not sliced");
+            nd.kind = NodeKind::Argmax;
+            nd.kname = "argmax";
+            nd.in = {xb};
+            nd.out = new_buf(Layout::I32, out_shape, G.last);
+            flat_buf[G.last] = nd.out;
+            return MGI_OK;
+        }
+        case OpKind::Pad: {
+            int xb = need_c8(op.in[0]);
+            if (xb < 0) xb = c8_buf[op.in[0]];
+            if (xb < 0) return fail(MGI_ERR_UNSUPPORTED, "pad input is not sliced");
+            nd.kind = NodeKind::Pad;
+            nd.kname = "pad";
+            nd.in = {xb};
+            nd.conv.pad_t = op.pads[0];
+            nd.conv.pad_l = op.pads[2];
+            nd.out = new_buf(Layout::C8, out_shape, G.last);
+            c8_buf[G.last] = nd.out;
+            return MGI_OK;
+        }
+        default:
+            break;
+    }
+    return MGI_OK;
+}
+
+mgi_status Lowering::lower(const Group &G) {
+    const GOp &op = g.ops[G.head];
+    const Shape out_shape = g.ops[G.last].out;
+    Node nd;
+    nd.op = G.head;
+    nd.out_tensor = G.last;
+    nd.n_fused = G.n;
+    nd.act1 = G.act1;
+    nd.act2 = G.act2;
+    switch (op.kind) {
+        case OpKind::Conv2d: {
+            const mgi_status st = lower_conv(G, op, out_shape, nd);
+            if (st != MGI_OK) return st;
+            break;
+        }
+        case OpKind::Depthwise: {
+            int xb = need_c8(op.in[0]);
+            if (xb < 0) return fail(MGI_ERR_UNSUPPORTED, "depthwise input has no sliced form");
+            nd.kind = NodeKind::Depthwise;
+            nd.kname = "dw_conv";
+            nd.conv = op.conv;
+            nd.in = {xb};
+            nd.out = new_buf(Layout::C8, out_shape, G.last);
+            c8_buf[G.last] = nd.out;
+            break;
+        }
+        case OpKind::Add:
+        case OpKind::Activation: {
+            nd.kind = op.kind == OpKind::Add ? NodeKind::Add : NodeKind::Act;
+            nd.kname = op.kind == OpKind::Add ? "add" : "activation";
+            for (int t : op.in) {
+                int b = need_c8(t);
+                if (b < 0) b = c8_buf[t];
+                if (b < 0) return fail(MGI_ERR_UNSUPPORTED, "element-wise operand is not sliced");
+                nd.in.push_back(b);
+            }
+            nd.out = new_buf(Layout::C8, out_shape, G.last);
+            c8_buf[G.last] = nd.out;
+            break;
+        }
+        case OpKind::GlobalAvgPool: {
+            int xb = need_c8(op.in[0]);
+            if (xb < 0) xb = c8_buf[op.in[0]];
+            if (xb < 0) return fail(MGI_ERR_UNSUPPORTED, "pool input is not sliced");
+            nd.kind = NodeKind::Gap;
+            nd.kname = "global_avgpool";
+            nd.in = {xb};
+            nd.out = new_buf(Layout::C8, out_shape, G.last);
+            c8_buf[G.last] = nd.out;
+            break;
+        }
+        case OpKind::FC:
+        case OpKind::Softmax:
+        case OpKind::Concat:
+        case OpKind::ResizeBilinear:
+        case OpKind::Argmax:
+        case OpKind::Pad: {
+            const mgi_status st = lower_other(G, op, out_shape, nd);
+            if (st != MGI_OK) return st;
+            break;
+        }
+        case OpKind::Input:
+            break;
+    }
+    add_node(std::move(nd));
+    // a sliced tensor that is a graph output is exported right away
+    const int t = G.last;
+    if (out_index[t] >= 0 && c8_buf[t] >= 0 && p.bufs[c8_buf[t]].layout == Layout::C8 &&
+        flat_buf[t] < 0) {
+        Node ex;
+        ex.kind = NodeKind::Export;
+        ex.kname = "export";
+        ex.out_tensor = -1;
+        ex.n_fused = 0;
+        ex.in = {c8_buf[t]};
+        Buf b;
+        b.layout = Layout::F32;
+        b.shape = g.ops[t].out;
+        b.bytes = b.shape.elems() * 4;
+        b.loc = Loc::Output;
+        b.index = out_index[t];
+        b.graph_tensor = t;
+        p.bufs.push_back(b);
+        ex.out = (int)p.bufs.size() - 1;
+        flat_buf[t] = ex.out;
+        add_node(std::move(ex));
+    }
+    return MGI_OK;
+}
+
+mgi_status Lowering::bind_outputs() {
     // outputs
     p.output_bufs.assign(g.outputs.size(), -1);
     p.output_tensor = g.outputs;
@@ -1014,14 +1075,12 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
         p.output_dtypes.push_back(p.bufs[b].layout == Layout::I32 ? MGI_DTYPE_INT32 : MGI_DTYPE_FP32);
     }
 
-    if (o.fuse && o.fuse_pwdw) fuse_pw_into_dw(p, o.fuse_pwdw == 2);
-    if (o.fuse && o.fuse_stemdw) fuse_stem_into_dw(p, o.fuse_stemdw == 2);
-    if (o.fuse && o.fuse_pool) fuse_pool_into_pw(p, o.fuse_pool == 2);
-    if (o.fuse && o.fuse_softmax) fuse_softmax_into_fc(p);
-    if (o.fuse && o.fuse_dwpw) fuse_dw_into_pw(p);
-    for (Node &nd : p.nodes) add_configs(p, nd, p.bufs[nd.out].shape.pixels());
+    return MGI_OK;
+}
 
-    // ------------------------------------------------------------ lifetimes
+// First and last node of every buffer (the lifetimes the planner shares
+// memory by, Sec. 5).
+void compute_lifetimes(mgi_plan &p) {
     for (size_t i = 0; i < p.nodes.size(); ++i) {
         Node &nd = p.nodes[i];
         p.bufs[nd.out].producer = (int)i;
@@ -1030,7 +1089,11 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
         if (nd.scratch >= 0) p.bufs[nd.scratch].producer = p.bufs[nd.scratch].last_use = (int)i;
     }
 
-    // -------------------------------------------------------------- planning
+}
+
+// Offsets of the arena buffers (the planner the options name, Sec. 5), then
+// the state region behind the arena.
+void plan_memory(mgi_plan &p, const mgi_options &o) {
     std::vector<int> arena;
     std::vector<size_t> sizes;
     std::vector<int> first, last;
@@ -1070,7 +1133,11 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
     p.state_bytes = state;
     p.workspace_bytes = std::max<size_t>(p.state_off + state, 256);
 
-    // --------------------------------------------------------------- packing
+}
+
+// The packed weight blob, uploaded by mgi_plan_bind.
+void pack_weights(const mgi_graph &g, mgi_plan &p, const mgi_options &o) {
+    auto to_bits = o.dtype == MGI_DTYPE_BF16 ? f32_to_bf16_bits : f32_to_f16_bits;
     // GEMM weights (A operand of v_mfma_f32_16x16x32_f16): for output block nb
     // (16 channels) and K slice ks (8 inputs), 16 rows x 8 halves, contiguous:
     //   packed[((nb * ksp + ks) * 16 + row) * 8 + j] = W[nb*16 + row][k(ks, j)]
@@ -1166,6 +1233,30 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
         }
     }
     p.weight_bytes = std::max<size_t>(blob.size(), 256);
+}
+
+mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p) {
+    if (g.outputs.empty()) return fail(MGI_ERR_STATE, "mgi_graph_finalize: no output marked");
+    mgi_status st = check_options(o);
+    if (st != MGI_OK) return st;
+    const std::vector<Group> groups = group_operators(g, o, live_ops(g));
+    p.bufs.clear();
+    p.nodes.clear();
+    Lowering L(g, p);
+    L.add_inputs();
+    for (const Group &G : groups)
+        if ((st = L.lower(G)) != MGI_OK) return st;
+    if ((st = L.bind_outputs()) != MGI_OK) return st;
+    // node-level fusion passes, then each node's kernel configurations
+    if (o.fuse && o.fuse_pwdw) fuse_pw_into_dw(p, o.fuse_pwdw == 2);
+    if (o.fuse && o.fuse_stemdw) fuse_stem_into_dw(p, o.fuse_stemdw == 2);
+    if (o.fuse && o.fuse_pool) fuse_pool_into_pw(p, o.fuse_pool == 2);
+    if (o.fuse && o.fuse_softmax) fuse_softmax_into_fc(p);
+    if (o.fuse && o.fuse_dwpw) fuse_dw_into_pw(p);
+    for (Node &nd : p.nodes) add_configs(p, nd, p.bufs[nd.out].shape.pixels());
+    compute_lifetimes(p);
+    plan_memory(p, o);
+    pack_weights(g, p, o);
     p.opt = o;
     return MGI_OK;
 }
