@@ -31,6 +31,7 @@
 // separate GEMM and depthwise kernels, so the result is bit-identical to the
 // unfused pair (and to the node's split form, which runs those kernels).
 #include <algorithm>
+#include <utility>
 
 #include "device.h"
 
@@ -52,7 +53,7 @@ __device__ __forceinline__ h8 wave_shift(h8 v) {
 
 constexpr int kPwDwLds = 160 * 1024;
 
-template <typename E, int NW, int FMW, int NBT, int S_, int R, int LPR, int PF>
+template <typename E, int NW, int FMW, int NBT, int S_, int R, int LPR, int PF, bool DEEP>
 __global__ __launch_bounds__(NW * 64, 2) void pwdw_kernel(PwDwParams p) {   // >= 2 waves per SIMD: <= 256 VGPRs
     const int PMAX = p.pstride;                   // pixel stride of the LDS output tile (>= a tile's pixels)
     constexpr int NCH = 16 * NBT;                 // output channels of a tile
@@ -133,8 +134,14 @@ __global__ __launch_bounds__(NW * 64, 2) void pwdw_kernel(PwDwParams p) {   // >
     }
 
     // 2. this wave's pixel fragments: wave, wave + NW, ... (a fragment with no
-    // valid pixel is skipped; rows past the tile read its last pixel and are
-    // never stored)
+    // valid pixel computes nothing; rows past the tile read its last pixel and
+    // are never stored).  When K has more steps than the PF prefetch slots
+    // (DEEP, chosen at launch), every K-step loads every fragment, valid or
+    // not (an invalid one reads the tile's last pixel again), and the loop
+    // issues the same loads whichever steps it computes: with no load under a
+    // condition the compiler can count the loads in flight and wait only for
+    // the one a step consumes, so the loads for the next PF-1 steps stay in
+    // flight.  Otherwise the slots take all of K at once, each step once.
     int mj[FMW];
     bool fj[FMW];
 #pragma unroll
@@ -145,16 +152,22 @@ __global__ __launch_bounds__(NW * 64, 2) void pwdw_kernel(PwDwParams p) {   // >
     }
     const int xsl = lane >> 4;
     h8 xq[PF][FMW];
+    // (byte offsets from the tensor's base fit 32 bits: the host offers this
+    // kernel only for inputs of at most 4 GiB)
     auto xload = [&](int kk, h8 *dst) {
-        const int ks = min(kk * 4 + xsl, p.ksl - 1);   // K tail meets zero weights
-        const h8 *src = p.x + (size_t)ks * p.M;
+        const uint32_t ks = min(kk * 4 + xsl, p.ksl - 1);   // K tail meets zero weights
+        const uint32_t off = ks * (uint32_t)p.M;
 #pragma unroll
-        for (int j = 0; j < FMW; ++j)
-            if (fj[j]) dst[j] = src[mj[j]];
+        for (int j = 0; j < FMW; ++j) dst[j] = *(const h8 *)((const char *)p.x + (off + (uint32_t)mj[j]) * 16u);
     };
+    if constexpr (DEEP) {
 #pragma unroll
-    for (int u = 0; u < PF; ++u)
-        if (u < nk) xload(u, xq[u]);
+        for (int u = 0; u < PF; ++u) xload(u, xq[u]);
+    } else {
+#pragma unroll
+        for (int u = 0; u < PF; ++u)
+            if (u < nk) xload(u, xq[u]);
+    }
     if (tid == 0) *zslot = zero_h8();
     wait_vm_lds<0>();                 // this wave's share of the weights has landed
     __builtin_amdgcn_s_barrier();     // ... and every other wave's
@@ -163,8 +176,8 @@ __global__ __launch_bounds__(NW * 64, 2) void pwdw_kernel(PwDwParams p) {   // >
     // the first K-step takes it from LDS as an operand, one channel block at
     // a time, so nothing is initialised and few registers hold it).  The
     // weight fragments are read right before their MFMAs: reading the next
-    // step's ahead costs registers, and past 128 (or 168) registers a compute
-    // unit holds fewer waves, which cost more than the overlap gained.
+    // step's ahead costs NBT*4 registers, and measured no faster, also where
+    // the LDS already limits a compute unit to one workgroup.
     f4 acc[NBT][FMW];
     auto step = [&](int kk, const h8 *b, bool first) {
         const h8 *buf = lds + (kk / CK) * SQ * 64 + (kk % CK) * 64 + lane;
@@ -189,16 +202,19 @@ __global__ __launch_bounds__(NW * 64, 2) void pwdw_kernel(PwDwParams p) {   // >
             }
     };
     step(0, xq[0], true);
-    if (PF < nk) xload(PF, xq[0]);                // (a single K-step has nothing to prefetch)
-    for (int c = 0; c < nchunks; ++c) {
+    if constexpr (DEEP) {
+        for (int c = 0; c < nchunks; ++c) {
 #pragma unroll
-        for (int u = 0; u < CK; ++u) {
-            const int kk = c * CK + u;
-            if (kk > 0 && kk < nk) {
-                step(kk, xq[u], false);
-                xload(min(kk + PF, nk - 1), xq[u]);
+            for (int u = 0; u < CK; ++u) {
+                const int kk = c * CK + u;
+                if (kk > 0 && kk < nk) step(kk, xq[u], false);
+                xload(min(kk + PF, nk - 1), xq[u]);   // (past the last step: a repeat of it, never used)
             }
         }
+    } else {
+#pragma unroll
+        for (int u = 1; u < PF; ++u)
+            if (u < nk) step(u, xq[u], false);
     }
 
     // 3. pointwise epilogue into LDS: tile [NSL][PMAX] of sliced elements
@@ -325,7 +341,7 @@ struct Inst {
 };
 
 // the candidates, in preference order for a shape
-const Inst kInsts[] = {
+constexpr Inst kInsts[] = {
     {false, 8, 2, 4, 1, 7, 16, 4, "img64"},   {false, 8, 2, 8, 1, 7, 16, 4, "img128"},
     {false, 8, 2, 4, 1, 7, 8, 4, "img64"},    {false, 8, 2, 8, 1, 7, 8, 4, "img128"},
     {false, 8, 2, 4, 2, 7, 16, 4, "img64"},   {false, 8, 2, 8, 2, 7, 16, 4, "img128"},
@@ -385,6 +401,8 @@ size_t lds_bytes(const Inst &in, int ksp, int pstride) {
 bool fits(const Inst &in, int N, int H, int W, int OH, int OW, int S, int pt, int pl, int ksp, int nb16,
           PwDwGeom *g) {
     if (S != in.s || lanes_for(OW) != in.lpr || pt < 0) return false;
+    // the kernel addresses its input with 32-bit byte offsets
+    if ((uint64_t)ksp * (uint64_t)N * (uint64_t)H * (uint64_t)W * 16u > 0xffffffffull) return false;
     // every input column a lane needs from a neighbour is held by a lane of the
     // same row, or is padding (the neighbour past the row's end holds zeros)
     if (S == 1 ? (pl != 1 || W >= in.lpr) : ((pl != 0 && pl != 1) || W > 2 * in.lpr - 1)) return false;
@@ -416,50 +434,37 @@ bool fits(const Inst &in, int N, int H, int W, int OH, int OW, int S, int pt, in
     return g->lds <= (size_t)kPwDwLds;
 }
 
-template <typename E, int NW, int FMW, int NBT, int S_, int R, int LPR, int PF>
+template <typename E, int K>
 hipError_t launch_t(const PwDwParams &p, size_t lds, hipStream_t st) {
-    auto kern = pwdw_kernel<E, NW, FMW, NBT, S_, R, LPR, PF>;
-    static const hipError_t attr =
-        hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, kPwDwLds);
+    constexpr Inst in = kInsts[K];
+    constexpr int NW = in.nw;
+    auto deep = pwdw_kernel<E, NW, in.fmw, in.nbt, in.s, in.r, in.lpr, in.pf, true>;
+    auto shallow = pwdw_kernel<E, NW, in.fmw, in.nbt, in.s, in.r, in.lpr, in.pf, false>;
+    static const hipError_t attr = [&] {
+        const hipError_t e =
+            hipFuncSetAttribute((const void *)deep, hipFuncAttributeMaxDynamicSharedMemorySize, kPwDwLds);
+        return e != hipSuccess
+                   ? e
+                   : hipFuncSetAttribute((const void *)shallow, hipFuncAttributeMaxDynamicSharedMemorySize, kPwDwLds);
+    }();
     if (attr != hipSuccess) return attr;
+    auto kern = (p.ksp >> 2) > in.pf ? deep : shallow;   // more K-steps than prefetch slots
     const int groups = p.nbands ? p.N * p.nbands : (p.N + p.ipt - 1) / p.ipt;
     launch(kern, dim3(groups * p.ntiles), dim3(NW * 64), (unsigned)lds, st, p);
     return hipGetLastError();
 }
 
+// instance k of the table (every entry is instantiated for both types)
+template <typename E, size_t... K>
+hipError_t launch_any(int k, const PwDwParams &p, size_t lds, hipStream_t st, std::index_sequence<K...>) {
+    hipError_t r = hipErrorInvalidValue;
+    (void)((k == (int)K && ((r = launch_t<E, (int)K>(p, lds, st)), true)) || ...);
+    return r;
+}
+
 template <typename E>
 hipError_t launch_inst(int k, const PwDwParams &p, size_t lds, hipStream_t st) {
-    switch (k) {
-#define MGI_PWDW(K_, NW_, FMW_, NBT_, S_, R_, LPR_, PF_) \
-    case K_: return launch_t<E, NW_, FMW_, NBT_, S_, R_, LPR_, PF_>(p, lds, st);
-        MGI_PWDW(0, 8, 2, 4, 1, 7, 16, 4) MGI_PWDW(1, 8, 2, 8, 1, 7, 16, 4)
-        MGI_PWDW(2, 8, 2, 4, 1, 7, 8, 4) MGI_PWDW(3, 8, 2, 8, 1, 7, 8, 4)
-        MGI_PWDW(4, 8, 2, 4, 2, 7, 16, 4) MGI_PWDW(5, 8, 2, 8, 2, 7, 16, 4)
-        MGI_PWDW(6, 8, 2, 4, 2, 7, 8, 4) MGI_PWDW(7, 8, 2, 8, 2, 7, 8, 4)
-        MGI_PWDW(8, 8, 2, 8, 2, 4, 16, 4) MGI_PWDW(9, 4, 3, 8, 2, 2, 16, 4)
-        MGI_PWDW(10, 8, 2, 8, 1, 4, 32, 4) MGI_PWDW(11, 4, 3, 8, 1, 4, 32, 4)
-        MGI_PWDW(12, 8, 4, 8, 2, 4, 32, 4) MGI_PWDW(13, 4, 5, 8, 2, 2, 32, 2)
-        MGI_PWDW(14, 8, 3, 8, 1, 4, 64, 2) MGI_PWDW(15, 4, 4, 8, 1, 2, 64, 2)
-        MGI_PWDW(16, 8, 8, 4, 2, 4, 64, 2) MGI_PWDW(17, 4, 9, 4, 2, 2, 64, 1)
-        MGI_PWDW(18, 8, 4, 4, 1, 4, 64, 2) MGI_PWDW(19, 4, 4, 4, 1, 2, 64, 2)
-        MGI_PWDW(20, 4, 9, 2, 2, 2, 64, 1) MGI_PWDW(21, 4, 4, 2, 1, 2, 64, 2)
-        MGI_PWDW(22, 4, 9, 3, 2, 2, 64, 1) MGI_PWDW(23, 4, 4, 3, 1, 2, 64, 2)
-        MGI_PWDW(24, 4, 5, 3, 2, 2, 32, 2) MGI_PWDW(25, 4, 3, 3, 1, 4, 32, 4)
-        MGI_PWDW(26, 4, 3, 4, 2, 2, 16, 4) MGI_PWDW(27, 4, 3, 4, 1, 4, 32, 4)
-        MGI_PWDW(28, 8, 2, 6, 1, 7, 16, 4) MGI_PWDW(29, 8, 2, 6, 1, 7, 8, 4)
-        MGI_PWDW(30, 8, 2, 6, 2, 7, 8, 4)
-        MGI_PWDW(31, 4, 5, 4, 2, 2, 32, 2) MGI_PWDW(32, 8, 4, 4, 2, 4, 32, 2)
-        MGI_PWDW(33, 8, 2, 1, 1, 2, 16, 4) MGI_PWDW(34, 8, 2, 2, 1, 2, 16, 4)
-        MGI_PWDW(35, 8, 2, 1, 1, 2, 8, 4) MGI_PWDW(36, 8, 2, 2, 1, 2, 8, 4)
-        MGI_PWDW(37, 8, 2, 1, 2, 2, 8, 4) MGI_PWDW(38, 8, 2, 2, 2, 2, 8, 4)
-        MGI_PWDW(39, 8, 2, 1, 1, 2, 16, 8) MGI_PWDW(40, 8, 2, 1, 1, 2, 8, 8)
-        MGI_PWDW(41, 8, 2, 1, 2, 2, 8, 8)
-        MGI_PWDW(42, 4, 9, 1, 2, 2, 64, 1) MGI_PWDW(43, 4, 4, 1, 1, 2, 64, 2)
-        MGI_PWDW(44, 4, 5, 1, 2, 2, 32, 2) MGI_PWDW(45, 4, 3, 1, 1, 4, 32, 4)
-        MGI_PWDW(46, 4, 3, 1, 2, 2, 16, 4)
-#undef MGI_PWDW
-    }
-    return hipErrorInvalidValue;
+    return launch_any<E>(k, p, lds, st, std::make_index_sequence<kNumInsts>{});
 }
 
 // the applicable instances of a shape, in table order
