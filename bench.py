@@ -162,6 +162,20 @@ def node_work(desc, nodes, shapes, i):
         flops = 2.0 * n * h_ * w_ * cin * cmid + 2.0 * elems(t) * op["kh"] * op["kw"]
         byts = (elems(pop["in"]) * 2 + out_b + pop["w"].size * 2 + pop["b"].size * 4 +
                 op["w"].size * 2 + op["b"].size * 4)
+    elif kind == "irb":
+        # inverted residual block: block input in (and the residual), block
+        # output out; the expanded and depthwise tensors never reach memory
+        dop = ops[head_of(op["in"])]
+        pop = ops[head_of(dop["in"])]
+        n, h_, w_, cin = shapes[pop["in"]]        # 1x1 stride 1: same plane
+        cmid = pop["cout"]
+        no, oh, ow, cout = shapes[t]                # 1x1 stride-1 projection: the depthwise plane
+        flops = (2.0 * n * h_ * w_ * cin * cmid + 2.0 * no * oh * ow * cmid * dop["kh"] * dop["kw"] +
+                 2.0 * no * oh * ow * cmid * cout)
+        byts = (elems(pop["in"]) * 2 + out_b + pop["w"].size * 2 + pop["b"].size * 4 +
+                dop["w"].size * 2 + dop["b"].size * 4 + op["w"].size * 2 + op["b"].size * 4)
+        if h != t:
+            byts += out_b          # fused residual operand
     elif kind == "pw_pool":
         # pointwise input in, pooled means out; the pointwise output never
         # reaches memory
@@ -224,7 +238,7 @@ def kernel_sources_hash():
     while the kernels it was measured on are unchanged."""
     import hashlib
     h = hashlib.sha1()
-    for f in ("gemm.hip", "ops.hip", "dwpw.hip", "pwdw.hip", "stemdw.hip", "device.h", "kernels.h"):
+    for f in ("gemm.hip", "ops.hip", "dwpw.hip", "pwdw.hip", "stemdw.hip", "irb.hip", "device.h", "kernels.h"):
         with open(os.path.join(ROOT, "paper_1907_01989_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]

@@ -136,6 +136,17 @@ typedef struct {
                             the default configuration for at most 16 rows (the two kernels
                             above that), the other one an autotune candidate.  0 or 1
                             (default).  Needs fuse = 1. */
+    int fuse_irb;        /* run a 1x1 projection convolution (stride 1, at most 320 output
+                            channels, optional residual add) inside a fused pointwise ->
+                            depthwise node (fuse_pwdw) whose output only it reads: MobileNet-v2's
+                            inverted residual block as one kernel, the expanded and depthwise
+                            tensors kept on chip; bit-identical to the separate operators,
+                            which stay autotune candidates.  0 (default): never; 1: the block
+                            kernel is the default configuration when it gets at least 256
+                            workgroups; 2: whenever the shapes allow.  Needs fuse_pwdw.  Off by
+                            default: measured on MI355X it is not faster than the separate
+                            kernels on most MobileNet-v2 blocks (they are bound by depthwise
+                            vector-ALU work, not by the memory traffic it removes). */
 } mgi_options;
 
 /* ---------------------------------------------------------------------------

@@ -40,7 +40,8 @@ class Options(ctypes.Structure):
                 ("fuse_pwdw", ctypes.c_int),
                 ("fuse_stemdw", ctypes.c_int),
                 ("fuse_pool", ctypes.c_int),
-                ("fuse_softmax", ctypes.c_int)]
+                ("fuse_softmax", ctypes.c_int),
+                ("fuse_irb", ctypes.c_int)]
 
 
 _lib = None

@@ -28,7 +28,7 @@ LIB_ASAN = os.path.join(HERE, "libmgi_asan.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 SOURCES = ["mgi_graph.cpp", "mgi_planner.cpp", "mgi_finalize.cpp", "mgi_runtime.cpp",
-           "gemm.hip", "ops.hip", "dwpw.hip", "pwdw.hip", "stemdw.hip"]
+           "gemm.hip", "ops.hip", "dwpw.hip", "pwdw.hip", "stemdw.hip", "irb.hip"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950", "-Wall",
           # packed fp32 instructions are kept out of every device code object

@@ -84,6 +84,19 @@ typedef uint32_t u4x __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ u4x as_u4(h8 v) { return __builtin_bit_cast(u4x, v); }
 
+// whole-wave lane shift of a 16-byte value: kWaveShr1 gives lane l the value
+// of lane l-1, kWaveShl1 that of lane l+1; the lane with no source gets zero
+// (DPP bound control)
+constexpr int kWaveShl1 = 0x130, kWaveShr1 = 0x138;
+template <int CTRL>
+__device__ __forceinline__ h8 wave_shift(h8 v) {
+    const u4x u = as_u4(v);
+    u4x r;
+#pragma unroll
+    for (int d = 0; d < 4; ++d) r[d] = (uint32_t)__builtin_amdgcn_mov_dpp((int)u[d], CTRL, 0xf, 0xf, true);
+    return __builtin_bit_cast(h8, r);
+}
+
 // acc[0..7] += w * v channel-wise, w and v fp16 x 8
 __device__ __forceinline__ void fma8(float *acc, u4x w, u4x v) {
 #pragma unroll

@@ -218,6 +218,38 @@ int pwdw_configs(int N, int H, int W, int OH, int OW, int S, int pt, int pl, int
                  PwDwGeom *g, const char **name);
 hipError_t launch_pwdw(const PwDwParams &p, int cfg, hipStream_t st);
 
+// MobileNet-v2 inverted residual block in one kernel: pointwise expansion
+// (+ bias, act1), depthwise 3x3 (+ bias, act2) and pointwise projection
+// (+ bias, pact1, + residual, pact2).  A workgroup owns a band of output rows
+// of one image, or whole images, and walks all expansion channels in chunks;
+// the expanded and depthwise tensors stay in LDS.
+struct IrbParams {
+    const h8 *x;         // block input, sliced [ksl][M]
+    const h8 *w;         // packed expansion weights [nb16][ksp][16][8]
+    const float *bias;   // [nb16 * 16]
+    int M, ksl, ksp, nb16, act1;
+    const h8 *dw_w;      // depthwise taps [2 * nb16][9][8]
+    const float *dw_b;   // [16 * nb16]
+    int ns, act2;        // expansion slices (2 * nb16, or one fewer), depthwise activation
+    const h8 *pw;        // packed projection weights [pnb16][pksp][16][8], K = expansion channels
+    const float *pbias;  // [pnb16 * 16]
+    int pksp, pnb16, pact1, pact2;
+    const h8 *res;       // residual, sliced like the output, or null
+    h8 *y;               // output, sliced [ps][MO]
+    int ps, MO;          // output slices and pixels
+    int N, H, W, OH, OW, S, pt, pl;
+    int ipt, nbands;     // set by launch_irb from the configuration
+    int pstride;         // ... pixel stride of the LDS expansion tile
+    int opstride;        // ... and of the LDS depthwise tile
+    int bf16;            // storage type: 0 fp16, 1 bf16
+};
+// Number of configurations of the block kernel that cover a shape (0: none);
+// for 0 <= cfg < that number, its name and workgroup count.  pnb16: output
+// channel blocks of the projection.
+int irb_configs(int N, int H, int W, int OH, int OW, int S, int pt, int pl, int ksp, int nb16, int pnb16, int cfg,
+                const char **name, int *groups);
+hipError_t launch_irb(const IrbParams &p, int cfg, hipStream_t st);
+
 hipError_t launch_add(const h8 *a, const h8 *b, h8 *y, size_t count, int act, bool bf16, hipStream_t st);
 // zero padding of a sliced tensor: (N, H, W) planes of S slices -> (N, OH, OW),
 // input placed at row pt, column pl

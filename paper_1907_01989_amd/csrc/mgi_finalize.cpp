@@ -189,6 +189,60 @@ void add_configs(const mgi_plan &p, Node &nd, size_t M) {
             nd.cfgs.push_back(Node::Config{t8, dwr, "split_" + tile_name(t8), true, 0});
         }
         nd.apply(0);
+    } else if (nd.kind == NodeKind::Irb) {
+        // the block kernel's configurations; the fused pointwise -> depthwise
+        // kernel's configurations, each followed by the projection GEMM; the
+        // three separate kernels.  The block kernel first when it fills the
+        // GPU, else the form the pointwise -> depthwise node would have taken.
+        // The projection GEMM of the split forms: the weight-slab tile for at
+        // most 32 output channels (it streams the wide input once), else the
+        // pipelined tile by the pointwise rule.
+        const Shape &s = nd.dw_in, &d = nd.dw_out;
+        {
+            const int npad = nd.pj_nb16 * 16;
+            const size_t slab_lds = (size_t)2 * nd.pj_ksp * 256 + (size_t)4 * 2 * 2 * 1024;
+            GemmTile t;
+            if (npad <= 32 && slab_lds <= 65536) {
+                t.slab = true;
+                t.wm = 32;
+                t.bn = 32;
+                t.pf = nd.pj_ksp >= 8 ? 2 : 1;
+            } else if (npad >= 64) {
+                pick_pipe_tile(t, d.pixels(), npad);
+            } else {
+                t = pick_tile(d.pixels(), npad);
+            }
+            nd.pj_tile = t;
+        }
+        const int st = nd.dw_conv.stride_h, pt = nd.dw_conv.pad_t, pl = nd.dw_conv.pad_l;
+        std::vector<Node::Config> blk, two, three;
+        const int nb = kern::irb_configs(s.n, s.h, s.w, d.h, d.w, st, pt, pl, nd.ksp, nd.nb16, nd.pj_nb16, -1,
+                                         nullptr, nullptr);
+        for (int c = 0; c < nb; ++c) {
+            const char *name = "";
+            kern::irb_configs(s.n, s.h, s.w, d.h, d.w, st, pt, pl, nd.ksp, nd.nb16, nd.pj_nb16, c, &name, nullptr);
+            blk.push_back(Node::Config{GemmTile{}, 0, name, false, c, 0});
+        }
+        const int nf = kern::pwdw_configs(s.n, s.h, s.w, d.h, d.w, st, pt, pl, nd.ksp, nd.nb16, -1, nullptr, nullptr);
+        for (int c = 0; c < nf; ++c) {
+            const char *name = "";
+            kern::pwdw_configs(s.n, s.h, s.w, d.h, d.w, st, pt, pl, nd.ksp, nd.nb16, c, nullptr, &name);
+            two.push_back(Node::Config{GemmTile{}, 0, std::string(name) + "+" + tile_name(nd.pj_tile), true, c, 1});
+        }
+        GemmTile t;
+        pick_pipe_tile(t, s.pixels(), nd.nb16 * 16);
+        three.push_back(Node::Config{t, st == 1 ? 4 : 2, "split3_" + tile_name(t), true, 0, 2});
+        std::vector<Node::Config> order;
+        auto add = [&](const std::vector<Node::Config> &v) { order.insert(order.end(), v.begin(), v.end()); };
+        if (nd.irb_default) {
+            add(blk); add(two); add(three);
+        } else if (nd.fused_default) {
+            add(two); add(blk); add(three);
+        } else {
+            add(three); add(two); add(blk);
+        }
+        nd.cfgs = order;
+        nd.apply(0);
     } else if (nd.kind == NodeKind::StemDw) {
         // band heights of the fused stem + depthwise kernel, and the two
         // separate kernels through the scratch tensor (first when the fused
@@ -370,6 +424,66 @@ void fuse_pw_into_dw(mgi_plan &p, bool always) {
         pw.tile = GemmTile{};
         pw.scratch = mid;
         drop[i] = 1;
+    }
+    std::vector<Node> kept;
+    for (size_t i = 0; i < p.nodes.size(); ++i)
+        if (!drop[i]) kept.push_back(std::move(p.nodes[i]));
+    p.nodes.swap(kept);
+}
+
+// Projection fusion (MobileNet-v2's inverted residual block as one node): a
+// 1x1 stride-1 GEMM node that alone reads the output of a fused pointwise ->
+// depthwise node joins it, when its residual (if any) is produced before that
+// node, it has at most 320 output channels and the block kernel (irb.hip)
+// covers the shapes.  The depthwise output stays planned as the node's second
+// scratch tensor, so the node can also run as the fused pointwise ->
+// depthwise kernel plus the projection GEMM, or as three kernels; the block
+// kernel is the default configuration when it gets at least 256 workgroups
+// (or `always`).
+void fuse_proj_into_pwdw(mgi_plan &p, bool always) {
+    std::vector<int> readers(p.bufs.size(), 0), producer(p.bufs.size(), -1), reader(p.bufs.size(), -1);
+    for (size_t i = 0; i < p.nodes.size(); ++i) {
+        const Node &nd = p.nodes[i];
+        for (int b : nd.in) {
+            readers[b]++;
+            reader[b] = (int)i;
+        }
+        if (nd.residual >= 0) readers[nd.residual]++;
+        producer[nd.out] = (int)i;
+    }
+    std::vector<char> drop(p.nodes.size(), 0);
+    for (size_t i = 0; i < p.nodes.size(); ++i) {
+        Node &b = p.nodes[i];
+        if (b.kind != NodeKind::PwDw) continue;
+        const int mid = b.out;
+        if (readers[mid] != 1 || p.bufs[mid].loc != Loc::Arena || reader[mid] < 0) continue;
+        const Node &pj = p.nodes[reader[mid]];
+        const mgi_conv_desc &c = pj.conv;
+        if (pj.kind != NodeKind::Gemm || pj.taps || pj.in.size() != 1 || c.kh != 1 || c.kw != 1 || c.stride_h != 1 ||
+            c.stride_w != 1 || pj.nb16 > 20)
+            continue;
+        if (pj.residual >= 0 && producer[pj.residual] >= (int)i) continue;
+        const Shape &s = b.dw_in, &d = b.dw_out;
+        if (pj.ksl != (d.c + 7) / 8) continue;
+        int groups = 0;
+        if (kern::irb_configs(s.n, s.h, s.w, d.h, d.w, b.dw_conv.stride_h, b.dw_conv.pad_t, b.dw_conv.pad_l, b.ksp,
+                              b.nb16, pj.nb16, 0, nullptr, &groups) == 0)
+            continue;
+        b.irb_default = always || groups >= 256;
+        b.kind = NodeKind::Irb;
+        b.kname = "irb";
+        b.pj_op = pj.op;
+        b.pj_ksl = pj.ksl;
+        b.pj_ksp = pj.ksp;
+        b.pj_nb16 = pj.nb16;
+        b.pj_act1 = pj.act1;
+        b.pj_act2 = pj.act2;
+        b.residual = pj.residual;
+        b.scratch2 = mid;
+        b.out = pj.out;
+        b.out_tensor = pj.out_tensor;
+        b.n_fused += pj.n_fused;
+        drop[reader[mid]] = 1;
     }
     std::vector<Node> kept;
     for (size_t i = 0; i < p.nodes.size(); ++i)
@@ -623,6 +737,8 @@ mgi_status check_options(const mgi_options &o) {
         return fail(MGI_ERR_INVALID_ARG, "mgi_graph_finalize: fuse_pool is 0, 1 or 2");
     if (o.fuse_softmax < 0 || o.fuse_softmax > 1)
         return fail(MGI_ERR_INVALID_ARG, "mgi_graph_finalize: fuse_softmax is 0 or 1");
+    if (o.fuse_irb < 0 || o.fuse_irb > 2)
+        return fail(MGI_ERR_INVALID_ARG, "mgi_graph_finalize: fuse_irb is 0, 1 or 2");
     return MGI_OK;
 }
 
@@ -1087,6 +1203,7 @@ void compute_lifetimes(mgi_plan &p) {
         for (int b : nd.in) p.bufs[b].last_use = (int)i;
         if (nd.residual >= 0) p.bufs[nd.residual].last_use = (int)i;
         if (nd.scratch >= 0) p.bufs[nd.scratch].producer = p.bufs[nd.scratch].last_use = (int)i;
+        if (nd.scratch2 >= 0) p.bufs[nd.scratch2].producer = p.bufs[nd.scratch2].last_use = (int)i;
     }
 
 }
@@ -1167,7 +1284,7 @@ void pack_weights(const mgi_graph &g, mgi_plan &p, const mgi_options &o) {
             float *bp = reinterpret_cast<float *>(blob.data() + nd.dw_b_off);
             for (int ch = 0; ch < c; ++ch) bp[ch] = dop.b[ch];
         }
-        if (nd.kind == NodeKind::PwDw || nd.kind == NodeKind::StemDw) {
+        if (nd.kind == NodeKind::PwDw || nd.kind == NodeKind::StemDw || nd.kind == NodeKind::Irb) {
             // depthwise taps of the absorbed op laid out as for a depthwise
             // node, [S][9][8], biases fp32; channels past c are zero
             const GOp &dop = g.ops[nd.dw_op];
@@ -1183,7 +1300,7 @@ void pack_weights(const mgi_graph &g, mgi_plan &p, const mgi_options &o) {
         }
         if (nd.kind == NodeKind::Gemm || nd.kind == NodeKind::Stem || nd.kind == NodeKind::FC ||
             nd.kind == NodeKind::DwPw || nd.kind == NodeKind::PwDw || nd.kind == NodeKind::StemDw ||
-            nd.kind == NodeKind::GemmPool || nd.kind == NodeKind::FcSoftmax) {
+            nd.kind == NodeKind::GemmPool || nd.kind == NodeKind::FcSoftmax || nd.kind == NodeKind::Irb) {
             const Shape x = g.ops[op.in[0]].out;
             const int cin = x.c;
             const bool fc = nd.kind == NodeKind::FC || nd.kind == NodeKind::FcSoftmax;
@@ -1216,6 +1333,20 @@ void pack_weights(const mgi_graph &g, mgi_plan &p, const mgi_options &o) {
             nd.b_off = reserve(nd.b_bytes);
             float *bp = reinterpret_cast<float *>(blob.data() + nd.b_off);
             for (int co = 0; co < cout; ++co) bp[co] = op.b[co];
+            if (nd.kind == NodeKind::Irb) {
+                // the projection: a 1x1 GEMM over the depthwise output, same layout
+                const GOp &pop = g.ops[nd.pj_op];
+                const int pin = g.ops[pop.in[0]].out.c, pco = pop.conv.cout;
+                nd.pj_w_off = reserve((size_t)nd.pj_nb16 * nd.pj_ksp * 16 * 8 * 2);
+                uint16_t *qp = reinterpret_cast<uint16_t *>(blob.data() + nd.pj_w_off);
+                for (int co = 0; co < pco; ++co)
+                    for (int ci = 0; ci < pin; ++ci)
+                        qp[(((size_t)(co / 16) * nd.pj_ksp + ci / 8) * 16 + co % 16) * 8 + ci % 8] =
+                            to_bits(pop.w[(size_t)co * pin + ci]);
+                nd.pj_b_off = reserve((size_t)nd.pj_nb16 * 16 * 4);
+                float *pb = reinterpret_cast<float *>(blob.data() + nd.pj_b_off);
+                for (int co = 0; co < pco; ++co) pb[co] = pop.b[co];
+            }
         } else if (nd.kind == NodeKind::Depthwise) {
             // fp16 taps per slice: [S][kh*kw][8], bias fp32 [S*8]; padded channels 0
             const int c = op.out.c, S = slices(c), taps = op.conv.kh * op.conv.kw;
@@ -1249,6 +1380,7 @@ mgi_status build_plan_impl(const mgi_graph &g, const mgi_options &o, mgi_plan &p
     if ((st = L.bind_outputs()) != MGI_OK) return st;
     // node-level fusion passes, then each node's kernel configurations
     if (o.fuse && o.fuse_pwdw) fuse_pw_into_dw(p, o.fuse_pwdw == 2);
+    if (o.fuse && o.fuse_pwdw && o.fuse_irb) fuse_proj_into_pwdw(p, o.fuse_irb == 2);
     if (o.fuse && o.fuse_stemdw) fuse_stem_into_dw(p, o.fuse_stemdw == 2);
     if (o.fuse && o.fuse_pool) fuse_pool_into_pw(p, o.fuse_pool == 2);
     if (o.fuse && o.fuse_softmax) fuse_softmax_into_fc(p);

@@ -362,4 +362,5 @@ extern "C" void mgi_options_default(mgi_options *o) {
     o->fuse_stemdw = 1;
     o->fuse_pool = 1;
     o->fuse_softmax = 1;
+    o->fuse_irb = 0;
 }

@@ -93,7 +93,7 @@ struct Buf {
 
 enum class NodeKind {
     Ingest, Stem, Gemm, Depthwise, Add, Act, Gap, FC, Softmax, Concat, Resize, Argmax,
-    ResizeArgmax, Export, Pad, DwPw, PwDw, StemDw, GemmPool, FcSoftmax
+    ResizeArgmax, Export, Pad, DwPw, PwDw, StemDw, GemmPool, FcSoftmax, Irb
 };
 
 // Tile shape of the MFMA GEMM (pointwise, implicit-GEMM convolution, FC).
@@ -147,16 +147,32 @@ struct Node {
     int scratch = -1;
     bool split = false;
     bool fused_default = true;
+    bool irb_default = false;   // Irb: the block kernel is the default configuration
     int pwdw_cfg = 0;       // PwDw / StemDw: configuration of the fused kernel (pwdw_configs,
                             // stemdw_configs)
     size_t cnt_off = 0;     // FcSoftmax: its row-tile arrival counters in the workspace's
                             // state region
+    // Irb (a PwDw node that also runs the pointwise projection reading its
+    // output): the projection's graph op, packed weights, GEMM geometry and
+    // epilogue (residual in `residual`), the depthwise output kept as a
+    // second planned scratch tensor (`scratch2`) for the split forms, and the
+    // projection's GEMM tile in those forms
+    int pj_op = -1;
+    size_t pj_w_off = 0, pj_b_off = 0;
+    int pj_ksl = 0, pj_ksp = 0, pj_nb16 = 0;
+    int pj_act1 = MGI_ACT_NONE, pj_act2 = MGI_ACT_NONE;
+    int scratch2 = -1;
+    GemmTile pj_tile;
+    int mode = 0;           // Irb: 0 the block kernel (pwdw_cfg: its configuration), 1 the fused
+                            // pointwise -> depthwise kernel (pwdw_cfg) then the projection GEMM,
+                            // 2 three kernels (expansion GEMM `tile`, depthwise, projection GEMM)
     struct Config {
         GemmTile tile;
         int dw_rows = 0;
         std::string name;
         bool split = false;
         int pwdw_cfg = 0;
+        int mode = 0;
     };
     std::vector<Config> cfgs;
     int cfg = 0;
@@ -166,6 +182,7 @@ struct Node {
         dw_rows = cfgs[c].dw_rows;
         split = cfgs[c].split;
         pwdw_cfg = cfgs[c].pwdw_cfg;
+        mode = cfgs[c].mode;
     }
 };
 

@@ -65,6 +65,54 @@ hipError_t launch_split_dw(const mgi_plan &p, const Node &nd, const void *sp, vo
     return launch_depthwise(q, nd.dw_rows, st);
 }
 
+// A pointwise GEMM (no window) with the kernel a tile names.
+hipError_t launch_gemm_tile(const GemmParams &q, const GemmTile &t, hipStream_t st) {
+    if (t.pipe && t.ks == 8) return launch_gemm_pipe_k8(q, false, st);
+    if (t.pipe) return launch_gemm_pipe(q, t.bm, t.bn, st);
+    if (t.slab) return launch_gemm_xs(q, t.wm, t.bn, t.pf, st);
+    return launch_gemm(q, t.bm, t.bn, false, false, st);
+}
+
+// The fused pointwise -> depthwise kernel of a PwDw or Irb node from its
+// input to `y` (the node's output, or an Irb node's depthwise scratch).
+hipError_t launch_node_pwdw(const mgi_plan &p, const Node &nd, const Bases &B, void *y, int ns, bool bf,
+                            hipStream_t st) {
+    const char *wbase = static_cast<const char *>(p.dev_w);
+    PwDwParams q{};
+    q.bf16 = bf;
+    q.x = (const h8 *)buf_ptr(p, nd.in[0], B);
+    q.w = (const h8 *)(wbase + nd.w_off);
+    q.bias = (const float *)(wbase + nd.b_off);
+    q.M = (int)nd.dw_in.pixels();
+    q.ksl = nd.ksl; q.ksp = nd.ksp; q.nb16 = nd.nb16; q.act1 = nd.act1;
+    q.dw_w = (const h8 *)(wbase + nd.dw_w_off);
+    q.dw_b = (const float *)(wbase + nd.dw_b_off);
+    q.y = (h8 *)y;
+    q.N = nd.dw_in.n; q.H = nd.dw_in.h; q.W = nd.dw_in.w; q.OH = nd.dw_out.h; q.OW = nd.dw_out.w;
+    q.S = nd.dw_conv.stride_h; q.pt = nd.dw_conv.pad_t; q.pl = nd.dw_conv.pad_l;
+    q.act2 = nd.dw_act;
+    q.ns = ns;
+    return launch_pwdw(q, nd.pwdw_cfg, st);
+}
+
+// The pointwise GEMM of a PwDw or Irb node's expansion into its scratch
+// tensor (the split forms).
+hipError_t launch_node_expand(const mgi_plan &p, const Node &nd, const Bases &B, bool bf, hipStream_t st) {
+    const char *wbase = static_cast<const char *>(p.dev_w);
+    const Shape mid = nd.dw_in;
+    GemmParams g{};
+    g.bf16 = bf;
+    g.x = (const h8 *)buf_ptr(p, nd.in[0], B);
+    g.w = (const h8 *)(wbase + nd.w_off);
+    g.bias = (const float *)(wbase + nd.b_off);
+    g.y = buf_ptr(p, nd.scratch, B);
+    g.M = g.Min = (int)mid.pixels();
+    g.ksl = nd.ksl; g.ksp = nd.ksp;
+    g.nb16 = nd.nb16; g.ns = slices(mid.c); g.cout = mid.c;
+    g.act1 = nd.act1; g.act2 = MGI_ACT_NONE;
+    return nd.tile.ks == 8 ? launch_gemm_pipe_k8(g, false, st) : launch_gemm_pipe(g, nd.tile.bm, nd.tile.bn, st);
+}
+
 hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStream_t st) {
     const char *wbase = static_cast<const char *>(p.dev_w);
     const Buf &ob = p.bufs[nd.out];
@@ -179,6 +227,64 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
             if (!dwpw_tile(os.h, os.w, q.sh, os.n, t, nd.tile.bm > 0 ? nd.tile.bm : 128))
                 return hipErrorInvalidValue;
             return launch_dwpw(q, t, st);
+        }
+        case NodeKind::Irb: {
+            const Shape d = nd.dw_out;
+            if (nd.mode == 0) {
+                IrbParams q{};
+                q.bf16 = bf;
+                q.x = (const h8 *)buf_ptr(p, nd.in[0], B);
+                q.w = (const h8 *)(wbase + nd.w_off);
+                q.bias = (const float *)(wbase + nd.b_off);
+                q.M = (int)nd.dw_in.pixels();
+                q.ksl = nd.ksl; q.ksp = nd.ksp; q.nb16 = nd.nb16; q.act1 = nd.act1;
+                q.dw_w = (const h8 *)(wbase + nd.dw_w_off);
+                q.dw_b = (const float *)(wbase + nd.dw_b_off);
+                q.ns = slices(d.c); q.act2 = nd.dw_act;
+                q.pw = (const h8 *)(wbase + nd.pj_w_off);
+                q.pbias = (const float *)(wbase + nd.pj_b_off);
+                q.pksp = nd.pj_ksp; q.pnb16 = nd.pj_nb16; q.pact1 = nd.pj_act1; q.pact2 = nd.pj_act2;
+                q.res = nd.residual >= 0 ? (const h8 *)buf_ptr(p, nd.residual, B) : nullptr;
+                q.y = (h8 *)y;
+                q.ps = slices(os.c); q.MO = (int)os.pixels();
+                q.N = nd.dw_in.n; q.H = nd.dw_in.h; q.W = nd.dw_in.w; q.OH = d.h; q.OW = d.w;
+                q.S = nd.dw_conv.stride_h; q.pt = nd.dw_conv.pad_t; q.pl = nd.dw_conv.pad_l;
+                return launch_irb(q, nd.pwdw_cfg, st);
+            }
+            // split forms: the expansion and depthwise into the depthwise
+            // scratch (one fused kernel, or the GEMM and the depthwise kernel),
+            // then the projection GEMM; a timed run stamps the first kernel's
+            // start and the last one's end
+            LaunchEvents &ev = launch_events();
+            const LaunchEvents saved = ev;
+            void *d2 = buf_ptr(p, nd.scratch2, B);
+            hipError_t e;
+            ev.stop = nullptr;
+            if (nd.mode == 1) {
+                e = launch_node_pwdw(p, nd, B, d2, slices(d.c), bf, st);
+            } else {
+                e = launch_node_expand(p, nd, B, bf, st);
+                ev.start = nullptr;
+                if (e == hipSuccess) e = launch_split_dw(p, nd, buf_ptr(p, nd.scratch, B), d2, bf, st);
+            }
+            ev.start = nullptr;
+            ev.stop = saved.stop;
+            if (e == hipSuccess) {
+                GemmParams g{};
+                g.bf16 = bf;
+                g.x = (const h8 *)d2;
+                g.w = (const h8 *)(wbase + nd.pj_w_off);
+                g.bias = (const float *)(wbase + nd.pj_b_off);
+                g.res = nd.residual >= 0 ? (const h8 *)buf_ptr(p, nd.residual, B) : nullptr;
+                g.y = y;
+                g.M = g.Min = (int)os.pixels();
+                g.ksl = nd.pj_ksl; g.ksp = nd.pj_ksp;
+                g.nb16 = nd.pj_nb16; g.ns = slices(os.c); g.cout = os.c;
+                g.act1 = nd.pj_act1; g.act2 = nd.pj_act2;
+                e = launch_gemm_tile(g, nd.pj_tile, st);
+            }
+            ev = saved;
+            return e;
         }
         case NodeKind::PwDw: {
             if (nd.split) {

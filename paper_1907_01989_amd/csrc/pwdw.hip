@@ -38,19 +38,6 @@
 namespace mgi {
 namespace kern {
 
-// whole-wave lane shift of a 16-byte value: kWaveShr1 gives lane l the value
-// of lane l-1, kWaveShl1 that of lane l+1; the lane with no source gets zero
-// (DPP bound control)
-constexpr int kWaveShl1 = 0x130, kWaveShr1 = 0x138;
-template <int CTRL>
-__device__ __forceinline__ h8 wave_shift(h8 v) {
-    const u4x u = as_u4(v);
-    u4x r;
-#pragma unroll
-    for (int d = 0; d < 4; ++d) r[d] = (uint32_t)__builtin_amdgcn_mov_dpp((int)u[d], CTRL, 0xf, 0xf, true);
-    return __builtin_bit_cast(h8, r);
-}
-
 constexpr int kPwDwLds = 160 * 1024;
 
 template <typename E, int NW, int FMW, int NBT, int S_, int R, int LPR, int PF, bool DEEP>

@@ -69,7 +69,8 @@ def build_graph(desc):
 
 
 def options(planner=B.PLANNER_GREEDY, fuse=True, materialize_all=False, fuse_dwpw=False,
-            dtype=B.DTYPE_FP16, fuse_pwdw=True, fuse_stemdw=True, fuse_pool=True, fuse_softmax=True):
+            dtype=B.DTYPE_FP16, fuse_pwdw=True, fuse_stemdw=True, fuse_pool=True, fuse_softmax=True,
+            fuse_irb=False):
     o = B.mgi_options_default()
     o.dtype = dtype
     o.planner = planner
@@ -80,6 +81,7 @@ def options(planner=B.PLANNER_GREEDY, fuse=True, materialize_all=False, fuse_dwp
     o.fuse_stemdw = int(fuse_stemdw)  # likewise
     o.fuse_pool = int(fuse_pool)      # likewise
     o.fuse_softmax = int(fuse_softmax)
+    o.fuse_irb = int(fuse_irb)        # False/True or 2
     return o
 
 
@@ -88,13 +90,13 @@ class Plan:
 
     def __init__(self, desc, planner=B.PLANNER_GREEDY, fuse=True, materialize_all=False,
                  device="cuda:0", bind=True, fuse_dwpw=False, dtype=B.DTYPE_FP16, fuse_pwdw=True,
-                 fuse_stemdw=True, fuse_pool=True, fuse_softmax=True):
+                 fuse_stemdw=True, fuse_pool=True, fuse_softmax=True, fuse_irb=False):
         self.desc = desc
         g = build_graph(desc)
         try:
             self.handle = B.mgi_graph_finalize(
                 g, options(planner, fuse, materialize_all, fuse_dwpw, dtype, fuse_pwdw, fuse_stemdw,
-                           fuse_pool, fuse_softmax))
+                           fuse_pool, fuse_softmax, fuse_irb))
         finally:
             B.mgi_graph_destroy(g)
         self.device = device

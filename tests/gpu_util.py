@@ -30,13 +30,13 @@ def to_numpy(t):
 
 
 def run_gpu(desc, materialize_all=True, fuse=True, planner=None, fuse_dwpw=False, dtype=0,
-            fuse_pwdw=True, configs=None, fuse_stemdw=True, fuse_pool=True, fuse_softmax=True):
+            fuse_pwdw=True, configs=None, fuse_stemdw=True, fuse_pool=True, fuse_softmax=True, fuse_irb=False):
     """Run ``desc`` once; returns (plan, outputs as numpy, {tensor id: node output}).
     ``configs``: {node index: kernel configuration} set before the run."""
     import torch
     from paper_1907_01989_amd import engine, _binding as B
     kw = {"fuse_dwpw": fuse_dwpw, "dtype": dtype, "fuse_pwdw": fuse_pwdw, "fuse_stemdw": fuse_stemdw,
-          "fuse_pool": fuse_pool, "fuse_softmax": fuse_softmax}
+          "fuse_pool": fuse_pool, "fuse_softmax": fuse_softmax, "fuse_irb": fuse_irb}
     if planner is not None:
         kw["planner"] = planner
     plan = engine.Plan(desc, fuse=fuse, materialize_all=materialize_all, **kw)

@@ -156,7 +156,7 @@ def test_pointwise_depthwise_fusion_structure():
     fused_tensors = [n["tensor"] for n in nodes if n["kind"] == "pw_dw"]
     assert all(desc["ops"][t]["op"] == "depthwise" for t in fused_tensors)
     # v2: every expansion feeds the block's depthwise convolution (16 blocks)
-    v2 = engine.Plan(workloads.mobilenet_v2(64), bind=False)
+    v2 = engine.Plan(workloads.mobilenet_v2(64), bind=False, fuse_irb=False)
     k2 = [n["kind"] for n in v2.nodes()]
     assert k2.count("pw_dw") == 16
     cf = [c for n, c in zip(nodes, v1.node_configs()) if n["kind"] == "pw_dw"]
@@ -170,7 +170,7 @@ def test_pointwise_depthwise_fusion_structure():
     b1fc = [c for n, c in zip(b1f.nodes(), b1f.node_configs()) if n["kind"] == "pw_dw"]
     assert len(b1fc) == 12 and all(name.startswith(("img", "band")) for _, _, name in b1fc)
     for o in (engine.options(fuse_pwdw=3), engine.options(fuse_stemdw=3), engine.options(fuse_stemdw=-1),
-              engine.options(fuse_pool=3), engine.options(fuse_softmax=2)):
+              engine.options(fuse_pool=3), engine.options(fuse_softmax=2), engine.options(fuse_irb=3)):
         g = engine.build_graph(workloads.mobilenet_v1(1))
         try:
             assert err(B.mgi_graph_finalize, g, o) == 1
@@ -290,6 +290,8 @@ def test_node_configuration_candidates():
             assert k == 6 and name.startswith(("band", "split"))
         elif n["kind"] == "pw_pool":
             assert 5 <= k <= 6 and name.startswith(("pool", "split"))
+        elif n["kind"] == "irb":
+            assert k >= 3 and name.startswith(("irb", "img", "band", "split3"))
         elif n["kind"] == "fc_gemm":
             assert k >= 1 and name.startswith("fc")
         elif n["kind"] == "fc_softmax":
@@ -426,6 +428,39 @@ def test_planner_assign_rejects_bad_lifetimes():
     assert err(B.mgi_planner_assign, B.PLANNER_GREEDY, [4, 4], [0, 3], [2, 1]) == 1
     assert err(B.mgi_planner_assign, 7, [4], [0], [1]) == 3
     assert B.mgi_planner_assign(B.PLANNER_GREEDY, [], [], []) == ([], [])
+
+
+def test_inverted_residual_block_fusion_structure():
+    """MobileNet-v2: each of the 16 expansion -> depthwise -> projection blocks
+    (with its residual add where there is one) becomes one node; its output
+    is the block's output tensor (the add, else the projection), its
+    configurations are the block kernel's, the fused pointwise -> depthwise
+    kernel's followed by the projection GEMM, and three separate kernels."""
+    desc = workloads.mobilenet_v2(64)
+    plan = engine.Plan(desc, bind=False, fuse_irb=True)
+    nodes, cfgs = plan.nodes(), plan.node_configs()
+    kinds = [n["kind"] for n in nodes]
+    assert kinds.count("irb") == 16 and "pw_dw" not in kinds and len(kinds) == 20
+    ops = desc["ops"]
+    adds = 0
+    for n, (cur, k, name) in zip(nodes, cfgs):
+        if n["kind"] != "irb":
+            continue
+        t = n["tensor"]
+        assert ops[t]["op"] in ("conv2d", "add")
+        adds += ops[t]["op"] == "add"
+        assert n["n_fused"] >= (4 if ops[t]["op"] == "add" else 3)
+        assert k >= 3 and name.startswith("irb")     # batch 64: the block kernel fills the GPU
+    assert adds == 10
+    # the unfused plan (the default) keeps the separate projections; batch 1
+    # defaults to a split form
+    assert len(engine.Plan(desc, bind=False).nodes()) == 36
+    b1 = engine.Plan(workloads.mobilenet_v2(1), bind=False, fuse_irb=True)
+    for n, (_, k, name) in zip(b1.nodes(), b1.node_configs()):
+        if n["kind"] == "irb":
+            assert not name.startswith("irb")
+    # MobileNet-v1 has no projection after a depthwise convolution's pointwise pair
+    assert "irb" not in [n["kind"] for n in engine.Plan(workloads.mobilenet_v1(64), bind=False, fuse_irb=True).nodes()]
 
 
 def test_softmax_fusion_state_region():
