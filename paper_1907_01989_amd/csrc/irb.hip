@@ -326,13 +326,19 @@ __global__ __launch_bounds__(NW * 64, 1) void irb_kernel(IrbParams p) {
 #pragma unroll
                 for (int c = 0; c < 8; ++c) bias2[c] = dwb[tsl * 8 + c];
                 float acc2[R][8];
+                const h8 *rowp[NC];      // advanced by one plane row per input row
+#pragma unroll
+                for (int k = 0; k < NC; ++k) rowp[k] = plane + (iy0 - ir0) * p.W + cx[k];
 #pragma unroll
                 for (int r = 0; r < NR; ++r) {
                     const int iy = iy0 + r;
                     const bool rv = iy >= ir0 && iy < ir1;
                     h8 v[NC];
 #pragma unroll
-                    for (int k = 0; k < NC; ++k) v[k] = *((rv && cv[k]) ? plane + (iy - ir0) * p.W + cx[k] : zslot);
+                    for (int k = 0; k < NC; ++k) {
+                        v[k] = *((rv && cv[k]) ? rowp[k] : zslot);
+                        rowp[k] += p.W;
+                    }
                     h8 t3[3];
                     if (S_ == 1) {
                         t3[0] = wave_shift<kWaveShr1>(v[0]);
@@ -363,7 +369,8 @@ __global__ __launch_bounds__(NW * 64, 1) void irb_kernel(IrbParams p) {
                         float q[8];
 #pragma unroll
                         for (int c = 0; c < 8; ++c) q[c] = __builtin_amdgcn_fmed3f(acc2[o][c], lo2, hi2);
-                        dout[o * p.OW] = E::pack(q);
+                        *dout = E::pack(q);
+                        dout += p.OW;
                     }
                 }
             }

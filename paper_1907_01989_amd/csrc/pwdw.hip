@@ -270,13 +270,21 @@ __global__ __launch_bounds__(NW * 64, 2) void pwdw_kernel(PwDwParams p) {   // >
 #pragma unroll
         for (int c = 0; c < 8; ++c) bias2[c] = dwb[sl * 8 + c];
         float acc2[R][8];
+        // row pointers advance by one plane row per input row (adds, not
+        // per-row multiplies)
+        const h8 *rowp[NC];
+#pragma unroll
+        for (int k = 0; k < NC; ++k) rowp[k] = plane + (iy0 - ir0) * p.W + cx[k];
 #pragma unroll
         for (int r = 0; r < NR; ++r) {
             const int iy = iy0 + r;
             const bool rv = iy >= ir0 && iy < ir1;
             h8 v[NC];
 #pragma unroll
-            for (int k = 0; k < NC; ++k) v[k] = *((rv && cv[k]) ? plane + (iy - ir0) * p.W + cx[k] : zslot);
+            for (int k = 0; k < NC; ++k) {
+                v[k] = *((rv && cv[k]) ? rowp[k] : zslot);
+                rowp[k] += p.W;
+            }
             h8 t3[3];
             if (S_ == 1) {          // columns ox-1, ox, ox+1 (left padding 1)
                 t3[0] = wave_shift<kWaveShr1>(v[0]);
@@ -301,14 +309,15 @@ __global__ __launch_bounds__(NW * 64, 2) void pwdw_kernel(PwDwParams p) {   // >
         }
         if (gv && ox < p.OW) {
             const int gs = nb0 * 2 + sl;                 // global slice
-            h8 *yout = p.y + ((size_t)gs * p.N + img0 + t) * p.OH * p.OW + ox;
+            h8 *yout = p.y + (((size_t)gs * p.N + img0 + t) * p.OH + oy0) * p.OW + ox;
 #pragma unroll
             for (int o = 0; o < R; ++o) {
                 if (oy0 + o >= oy_hi) break;
                 float q[8];
 #pragma unroll
                 for (int c = 0; c < 8; ++c) q[c] = __builtin_amdgcn_fmed3f(acc2[o][c], lo, hi);
-                yout[(size_t)(oy0 + o) * p.OW] = E::pack(q);
+                *yout = E::pack(q);
+                yout += p.OW;
             }
         }
     }
