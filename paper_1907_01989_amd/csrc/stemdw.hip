@@ -17,6 +17,7 @@
 // ky = 0..2, columns kx = 0..2, fp16 x fp16 + fp32 products), so the fused
 // node is bit-identical to the two kernels run separately.
 #include <cmath>
+#include <type_traits>
 
 #include "device.h"
 
@@ -205,7 +206,8 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) void st
     _Float16 *inr = (_Float16 *)(lds + NSL * Q * RW);        // [QI][rs]
     h8 *taps = (h8 *)(inr + (size_t)QI * rs);                // [NSL][9]
     float *dwb = (float *)(taps + NSL * 9);                  // [NSL * 8]
-    h8 *zslot = (h8 *)(dwb + NSL * 8);
+    float *sbias = dwb + NSL * 8;                            // stem bias [NB * 16]
+    h8 *zslot = (h8 *)(sbias + NB * 16);
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -227,16 +229,15 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) void st
     const int upr = vec ? rowlen / VN : rowlen;              // load units per input row
     const TIN *xin = (const TIN *)p.x + (size_t)n * p.H * rowlen;
 
-    // weights, taps and biases; zero columns of every input-ring slot
+    // weights (held in registers), taps and biases (in LDS: the stem bias
+    // fragments are read again per fragment, which keeps the register count
+    // at the 4-wave limit); zero columns of every input-ring slot
     h8 a[NB];
-    f4 c0[NB];
 #pragma unroll
-    for (int i = 0; i < NB; ++i) {
-        a[i] = p.w[(size_t)i * 64 + lane];
-        c0[i] = bias_frag(p.bias, i, p.nb16, lane);
-    }
+    for (int i = 0; i < NB; ++i) a[i] = p.w[(size_t)i * 64 + lane];
     if (tid < NSL * 9) taps[tid] = p.dw_w[tid];
     if (tid < NSL * 8) dwb[tid] = p.dw_b[tid];
+    if (tid < NB * 16) sbias[tid] = p.bias[tid];
     if (tid == 0) *zslot = zero_h8();
     for (int e = tid; e < NSL * Q * 2; e += NT) {
         const int r = e >> 1, c = (e & 1) ? SW + p.dpl : 0;   // zero columns of ring row r
@@ -267,10 +268,16 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) void st
     auto src_of = [&](int r, int c) {
         return xin + (size_t)min(max(r, 0), p.H - 1) * rowlen + (vec ? c * VN : c);
     };
+    // fp16 input into fp16 planes: the conversion through fp32 is the identity
+    // on finite values, so the 16 bytes are copied as they are
+    constexpr bool raw = std::is_same<E, F16>::value && std::is_same<TIN, _Float16>::value;
     auto put = [&](int r, int c, const tv &v) {
         const bool inside = r >= 0 && r < p.H;
-        _Float16 *dst = inr + ((r - i_org) % QI) * rs + lead;
-        if (vec) {
+        _Float16 *dst = inr + ((unsigned)(r - i_org) % QI) * rs + lead;   // r >= i_org
+        if (raw && vec) {
+            const tv z = {};
+            *(tv *)(dst + c * VN) = inside ? v : z;
+        } else if (vec) {
             float f[VN];
 #pragma unroll
             for (int i = 0; i < VN; ++i) f[i] = inside ? (float)v[i] : 0.0f;
@@ -350,7 +357,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) void st
             const h8 b = __builtin_bit_cast(h8, w4);
 #pragma unroll
             for (int i = 0; i < NB; ++i) {
-                const f4 acc = E::mma(a[i], b, c0[i]);
+                const f4 acc = E::mma(a[i], b, *(const f4 *)(sbias + i * 16 + 4 * q));
                 float v[4];
 #pragma unroll
                 for (int r = 0; r < 4; ++r) v[r] = act_apply(acc[r], p.act1);
@@ -477,7 +484,7 @@ bool geometry(const StemDwParams &p, int cfg, bool fp16_in, StemDwGeom &g) {
         g.vec = rowlen % vn == 0 && lead % (fp16_in ? 8 : 4) == 0;
         g.pstride = 0;
         g.band_h8 = 0;
-        g.lds = ((size_t)nsl * Q * (p.SW + 2) + nsl * 9) * 16 + (size_t)g.qi * rs * 2 + (size_t)nsl * 8 * 4 + 16;
+        g.lds = ((size_t)nsl * Q * (p.SW + 2) + nsl * 9) * 16 + (size_t)g.qi * rs * 2 + (size_t)nsl * 8 * 4 * 2 + 16;
         return g.lds <= 160 * 1024;
     }
     const int R = c.rows;
