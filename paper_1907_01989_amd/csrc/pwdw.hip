@@ -334,6 +334,7 @@ struct Inst {
     bool band;
     int nw, fmw, nbt, s, r, lpr, pf;
     const char *name;
+    int ipt = 0;   // image tiles: images per workgroup (0: as many as fit)
 };
 
 // the candidates, in preference order for a shape
@@ -362,6 +363,11 @@ constexpr Inst kInsts[] = {
     {true, 4, 3, 4, 2, 2, 16, 4, "band2x64w4"},  {true, 4, 3, 4, 1, 4, 32, 4, "band4x64w4"},   // 28 -> 14, 28 x 28
     {false, 8, 2, 6, 1, 7, 16, 4, "img96"},      {false, 8, 2, 6, 1, 7, 8, 4, "img96"},        // 14 x 14, 7 x 7
     {false, 8, 2, 6, 2, 7, 8, 4, "img96"},                                                     // 14 -> 7
+    // four 7 x 7 images per workgroup instead of the five that fit: a batch
+    // of 64 then makes 16 image groups, so 64-channel tiles of 960-1024
+    // channels fill the 256 compute units in one round with fewer pixels per
+    // workgroup (two images with 96- or 128-channel tiles measured slower)
+    {false, 8, 2, 4, 1, 7, 8, 4, "img64i4", 4},
     {true, 4, 5, 4, 2, 2, 32, 2, "band2x64w4"},  {true, 8, 4, 4, 2, 4, 32, 2, "band4x64"},     // 56 -> 28
     // 16- and 32-channel image tiles with 2-row depthwise strips, for small
     // batches: more workgroups, and the depthwise step spread over more lanes
@@ -406,6 +412,11 @@ bool fits(const Inst &in, int N, int H, int W, int OH, int OW, int S, int pt, in
     if (!in.band) {
         if (H * W > pmax) return false;
         g->ipt = pmax / (H * W);
+        if (in.ipt) {
+            // (not where it gives the same groups as the instance without a cap)
+            if (in.ipt >= g->ipt || (N + in.ipt - 1) / in.ipt == (N + g->ipt - 1) / g->ipt) return false;
+            g->ipt = in.ipt;
+        }
         g->nbands = 0;
         g->groups = (N + g->ipt - 1) / g->ipt;
         g->pstride = g->ipt * H * W;
