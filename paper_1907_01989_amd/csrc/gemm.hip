@@ -261,14 +261,16 @@ __global__ __launch_bounds__(256) void gemm_xs_kernel(GemmParams p) {
     }
 
     // weight slab: FN blocks x ksp slices x 16 rows (blocks past the end are
-    // clamped; their accumulators are never stored)
-    const int slab = FN * p.ksp * 16;
-    for (int e = tid; e < slab; e += 256) {
-        const int f = e / (p.ksp * 16);
-        const int r = e - f * p.ksp * 16;
+    // clamped; their accumulators are never stored), 1 KiB per wave load by
+    // direct global->LDS loads, all in flight together with the activation
+    // prefetch; one wait and one barrier
+    const int kq = p.ksp >> 2;                   // KiB loads per block
+    for (int q = wave; q < FN * kq; q += 4) {
+        const int f = q / kq, r = q - f * kq;
         const int nb = min(nb0 + f, p.nb16 - 1);
-        wsm[e] = p.w[(size_t)nb * p.ksp * 16 + r];
+        load_lds16(p.w + ((size_t)nb * p.ksp + r * 4) * 16 + lane, wsm + q * 64);
     }
+    wait_vm_lds<0>();
     __syncthreads();
 
     auto step = [&](int kk, const h8 *b) {
@@ -321,10 +323,12 @@ static hipError_t launch_xs(const GemmParams &p, hipStream_t st) {
 
 hipError_t launch_gemm_xs(const GemmParams &p, int wm, int bn, int pf, hipStream_t st) {
     if (p.M <= 0) return hipSuccess;
+    if (p.ksp % 4 != 0) return hipErrorInvalidValue;
 #define MGI_XS_CASE(WM_, BN_, PF_) \
     if (wm == WM_ && bn == BN_ && pf == PF_) \
         return p.bf16 ? launch_xs<BF16, WM_, BN_, PF_>(p, st) : launch_xs<F16, WM_, BN_, PF_>(p, st);
-#define MGI_XS_PF(WM_, BN_) MGI_XS_CASE(WM_, BN_, 1) MGI_XS_CASE(WM_, BN_, 2) MGI_XS_CASE(WM_, BN_, 4)
+#define MGI_XS_PF(WM_, BN_) MGI_XS_CASE(WM_, BN_, 1) MGI_XS_CASE(WM_, BN_, 2) MGI_XS_CASE(WM_, BN_, 4) \
+    MGI_XS_CASE(WM_, BN_, 8)
     MGI_XS_PF(16, 32)
     MGI_XS_PF(16, 64)
     MGI_XS_PF(16, 128)

@@ -112,8 +112,8 @@ void pick_pipe_tile(GemmTile &t, size_t M, int npad);
 void add_gemm_configs(Node &nd, size_t M) {
     auto push = [&](const GemmTile &t) {
         for (const Node::Config &c : nd.cfgs)
-            if (c.tile.pipe == t.pipe && c.tile.slab == t.slab && c.tile.bm == t.bm && c.tile.ks == t.ks &&
-                c.tile.bn == t.bn && c.tile.wm == t.wm && c.tile.pf == t.pf)
+            if (c.tile.pipe == t.pipe && c.tile.slab == t.slab && (t.slab || c.tile.bm == t.bm) &&
+                c.tile.ks == t.ks && c.tile.bn == t.bn && c.tile.wm == t.wm && c.tile.pf == t.pf)
                 return;
         nd.cfgs.push_back({t, 0, tile_name(t)});
     };
@@ -147,6 +147,13 @@ void add_gemm_configs(Node &nd, size_t M) {
             t.bn = sb[1];
             t.pf = nd.ksp >= 8 ? 2 : 1;
             push(t);
+            // activations 8 K-steps ahead where the grid leaves most compute
+            // units idle (a batch of one: the K loop waits on memory latency)
+            const size_t tiles = (M + 4 * sb[0] - 1) / (4 * sb[0]) * (size_t)((npad + sb[1] - 1) / sb[1]);
+            if (nd.ksp >= 32 && tiles < 128) {
+                t.pf = 8;
+                push(t);
+            }
         }
     }
     const int ldss[5][2] = {{128, 128}, {64, 128}, {32, 128}, {64, 64}, {128, 64}};
