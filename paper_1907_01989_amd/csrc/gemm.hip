@@ -207,6 +207,69 @@ hipError_t launch_gemm(const GemmParams &p, int bm, int bn, bool taps, bool f32o
     return hipErrorInvalidValue;
 }
 
+// Global average pool of a GEMM tile (pipelined or weight-slab) that holds
+// whole images: every output value is rounded to the storage type as a stored
+// tensor would be (act1, then round) and staged in LDS as fp32, pixel-major
+// [BM][BN] with the channel index XOR-swizzled by the pixel (4 * (px % 8); 4 *
+// (px % 4) in a 16-channel tile) so that both the
+// accumulator-layout writes and the per-channel reads are free of bank
+// conflicts.  A thread then owns one (image, channel) and sums its pixels in
+// the global-pool kernel's order (8 partial sums over pixels j, j + 8, ...,
+// then pairs (0,4), (2,6), (1,5), (3,7) and their sums, times 1/hw), so the
+// fused node equals the GEMM followed by the pool bit for bit; the lane of
+// each 8 channels gathers the other seven by shuffles and stores the
+// element.  Output: sliced pooled means [ns][nimg].
+template <typename E, int BM, int BN, int FM, int FN>
+__device__ __forceinline__ void pool_epilogue(const GemmParams &p, const f4 (&acc)[FN][FM], int mt, int nb0,
+                                              int px0, int cb0, float *T, int tid, int lane) {
+    static_assert(BN % 16 == 0, "whole channel blocks");
+    // (the swizzle moves whole 4-channel groups inside their 32 channels, or
+    // inside the tile's 16 channels when BN is 16)
+    constexpr int PXM = BN >= 32 ? 7 : 3;
+    auto at = [](int px, int ch) { return px * BN + (ch ^ (4 * (px & PXM))); };
+#pragma unroll
+    for (int i = 0; i < FN; ++i) {
+        const int ch = (cb0 + i) * 16 + 4 * (lane >> 4);
+#pragma unroll
+        for (int j = 0; j < FM; ++j) {
+            const int px = px0 + j * 16 + (lane & 15);
+            float v[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) v[r] = act_apply(acc[i][j][r], p.act1);
+            const h4 h = E::pack4(v);
+            f4 f;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) f[r] = E::get4(h, r);
+            *(f4 *)(T + at(px, ch)) = f;          // 4 channels stay contiguous under the swizzle
+        }
+    }
+    __syncthreads();
+    const float inv = 1.0f / (float)p.hw;
+    for (int t0 = 0; t0 < p.ipt * BN; t0 += 256) {    // same trip count in every lane (shuffles)
+        const int t = t0 + tid;
+        const int k = t / BN, ch = t - k * BN;
+        const bool live = t < p.ipt * BN;
+        const int kk = live ? k : 0;
+        float a[8];
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) {
+            float sum = 0.0f;
+#pragma unroll
+            for (int ii = 0; ii < 8; ++ii) {
+                const int px = jj + 8 * ii;
+                sum += px < p.hw ? T[at(kk * p.hw + min(px, p.hw - 1), ch)] : 0.0f;
+            }
+            a[jj] = sum;
+        }
+        const float q = (((a[0] + a[4]) + (a[2] + a[6])) + ((a[1] + a[5]) + (a[3] + a[7]))) * inv;
+        float o[8];
+#pragma unroll
+        for (int c = 0; c < 8; ++c) o[c] = __shfl(q, (lane & ~7) + c);
+        const int img = mt * p.ipt + k, os = nb0 * 2 + ch / 8;
+        if (live && (ch & 7) == 0 && img < p.nimg && os < p.ns) ((h8 *)p.y)[(size_t)os * p.nimg + img] = E::pack(o);
+    }
+}
+
 // ---------------------------------------------------------------------------
 // Pointwise GEMM, weight-slab variant.  The tile's whole weight slab
 // (BN channels x all K, at most 64 KiB) is loaded into LDS once, behind one
@@ -217,14 +280,17 @@ hipError_t launch_gemm(const GemmParams &p, int bm, int bn, bool taps, bool f32o
 // load other than the activation stream, so the in-order load counter lets
 // PF steps of loads stay in flight.
 // ---------------------------------------------------------------------------
-template <typename E, int WM, int BN, int PF>
+// POOL: the output feeds only a global average pool over planes of p.hw <=
+// BM pixels; an M-tile then holds p.ipt whole images and the epilogue writes
+// the pooled means (pool_epilogue), as in the pipelined kernel.
+template <typename E, int WM, int BN, int PF, bool POOL>
 __global__ __launch_bounds__(256) void gemm_xs_kernel(GemmParams p) {
     constexpr int FM = WM / 16, FN = BN / 16, BM = 4 * WM;
     extern __shared__ h8 wsm[];                  // [FN][ksp][16]
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int tile = xcd_tile(blockIdx.x, gridDim.x);
     const int mt = tile / p.ntiles, nt = tile - mt * p.ntiles;
-    const int m0 = mt * BM + wave * WM, nb0 = nt * FN;
+    const int m0 = (POOL ? mt * p.ipt * p.hw : mt * BM) + wave * WM, nb0 = nt * FN;
     const int ksteps = p.ksp >> 2;
 
     // Loads are branch-free (a load under a lane condition becomes an
@@ -298,37 +364,67 @@ __global__ __launch_bounds__(256) void gemm_xs_kernel(GemmParams p) {
     for (int u = 0; u < PF - 1; ++u)
         if (kk0 + u < ksteps) step(kk0 + u, xq[u]);
 
-    // per-wave epilogue tile after the weight slab
-    float *stage = (float *)(wsm + FN * p.ksp * 16) + wave * (FN * FM * 256);
-    store_tile_c8<E, FM, FN>(p, acc, m0, nb0, stage, lane);
+    // epilogue tile after the weight slab: per wave, or the pooled tile
+    float *stage = (float *)(wsm + FN * p.ksp * 16);
+    if constexpr (POOL) {
+        pool_epilogue<E, BM, BN, FM, FN>(p, acc, mt, nb0, wave * WM, 0, stage, tid, lane);
+        return;
+    }
+    store_tile_c8<E, FM, FN>(p, acc, m0, nb0, stage + wave * (FN * FM * 256), lane);
 }
 
-// LDS bytes of the weight slab for a bn-wide tile
+// LDS bytes of the weight slab for a bn-wide tile (slab plus epilogue tile)
 static size_t xs_stage_bytes(int wm, int bn) { return (size_t)4 * (wm / 16) * (bn / 16) * 256 * 4; }
 size_t gemm_xs_lds_bytes(int ksp, int wm, int bn) {
     return (size_t)(bn / 16) * ksp * 256 + xs_stage_bytes(wm, bn);
 }
 
-template <typename E, int WM, int BN, int PF>
+constexpr size_t kXsMaxLds = 160 * 1024;
+
+template <typename E, int WM, int BN, int PF, bool POOL>
 static hipError_t launch_xs(const GemmParams &p, hipStream_t st) {
     GemmParams q = p;
     constexpr int BM = 4 * WM, FN = BN / 16;
-    q.mtiles = (p.M + BM - 1) / BM;
+    if (POOL) {
+        q.ipt = BM / p.hw;
+        q.mtiles = (p.nimg + q.ipt - 1) / q.ipt;
+    } else {
+        q.mtiles = (p.M + BM - 1) / BM;
+    }
     q.ntiles = (p.nb16 + FN - 1) / FN;
     const size_t lds = gemm_xs_lds_bytes(p.ksp, WM, BN);
-    if (lds > 65536) return hipErrorInvalidValue;
-    launch((gemm_xs_kernel<E, WM, BN, PF>), dim3(q.mtiles * q.ntiles), dim3(256), lds, st, q);
+    if (lds > kXsMaxLds) return hipErrorInvalidValue;
+    auto kern = gemm_xs_kernel<E, WM, BN, PF, POOL>;
+    if (lds > 65536) {
+        static const hipError_t attr =
+            hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kXsMaxLds);
+        if (attr != hipSuccess) return attr;
+    }
+    launch(kern, dim3(q.mtiles * q.ntiles), dim3(256), lds, st, q);
     return hipGetLastError();
 }
 
-hipError_t launch_gemm_xs(const GemmParams &p, int wm, int bn, int pf, hipStream_t st) {
+hipError_t launch_gemm_xs(const GemmParams &p, int wm, int bn, int pf, bool pool, hipStream_t st) {
     if (p.M <= 0) return hipSuccess;
     if (p.ksp % 4 != 0) return hipErrorInvalidValue;
+    if (pool) {
+        // pooled tiles: one image group of planes of at most 64 pixels per
+        // 64-row tile (16 pixels per wave)
+        if (p.hw < 1 || p.hw > 64 || p.M != p.nimg * p.hw || wm != 16) return hipErrorInvalidValue;
+#define MGI_XSP_CASE(BN_, PF_) \
+        if (bn == BN_ && pf == PF_) \
+            return p.bf16 ? launch_xs<BF16, 16, BN_, PF_, true>(p, st) : launch_xs<F16, 16, BN_, PF_, true>(p, st);
+        MGI_XSP_CASE(16, 2) MGI_XSP_CASE(16, 8) MGI_XSP_CASE(32, 2) MGI_XSP_CASE(32, 8)
+        MGI_XSP_CASE(64, 2) MGI_XSP_CASE(64, 8)
+#undef MGI_XSP_CASE
+        return hipErrorInvalidValue;
+    }
 #define MGI_XS_CASE(WM_, BN_, PF_) \
     if (wm == WM_ && bn == BN_ && pf == PF_) \
-        return p.bf16 ? launch_xs<BF16, WM_, BN_, PF_>(p, st) : launch_xs<F16, WM_, BN_, PF_>(p, st);
+        return p.bf16 ? launch_xs<BF16, WM_, BN_, PF_, false>(p, st) : launch_xs<F16, WM_, BN_, PF_, false>(p, st);
 #define MGI_XS_PF(WM_, BN_) MGI_XS_CASE(WM_, BN_, 1) MGI_XS_CASE(WM_, BN_, 2) MGI_XS_CASE(WM_, BN_, 4) \
     MGI_XS_CASE(WM_, BN_, 8)
+    MGI_XS_CASE(16, 16, 8)
     MGI_XS_PF(16, 32)
     MGI_XS_PF(16, 64)
     MGI_XS_PF(16, 128)
@@ -386,66 +482,6 @@ __device__ __forceinline__ void pipe_issue(const GemmParams &p, int kk, h8 *st, 
         const int q = L / T::SUB, sub = L - q * T::SUB;
         const int nb = min(nb0 + q, p.nb16 - 1);
         load_lds16(p.w + ((size_t)nb * p.ksp + k0 + 4 * sub) * 16 + lane, st + T::XE + L * 64);
-    }
-}
-
-// Global average pool of a pipelined-GEMM tile that holds whole images:
-// every output value is rounded to the storage type as a stored tensor would
-// be (act1, then round) and staged in LDS as fp32, pixel-major [BM][BN] with
-// the channel index XOR-swizzled by the pixel (4 * (px % 8)) so that both the
-// accumulator-layout writes and the per-channel reads are free of bank
-// conflicts.  A thread then owns one (image, channel) and sums its pixels in
-// the global-pool kernel's order (8 partial sums over pixels j, j + 8, ...,
-// then pairs (0,4), (2,6), (1,5), (3,7) and their sums, times 1/hw), so the
-// fused node equals the GEMM followed by the pool bit for bit; the lane of
-// each 8 channels gathers the other seven by shuffles and stores the
-// element.  Output: sliced pooled means [ns][nimg].
-template <typename E, int BM, int BN, int FM, int FN>
-__device__ __forceinline__ void pool_epilogue(const GemmParams &p, const f4 (&acc)[FN][FM], int mt, int nb0,
-                                              int wm, int wn, float *T, int tid, int lane) {
-    constexpr int WMP = BM / 2;
-    static_assert(BN % 32 == 0, "swizzle spans 32 channels");
-    auto at = [](int px, int ch) { return px * BN + (ch ^ (4 * (px & 7))); };
-#pragma unroll
-    for (int i = 0; i < FN; ++i) {
-        const int ch = (wn * FN + i) * 16 + 4 * (lane >> 4);
-#pragma unroll
-        for (int j = 0; j < FM; ++j) {
-            const int px = wm * WMP + j * 16 + (lane & 15);
-            float v[4];
-#pragma unroll
-            for (int r = 0; r < 4; ++r) v[r] = act_apply(acc[i][j][r], p.act1);
-            const h4 h = E::pack4(v);
-            f4 f;
-#pragma unroll
-            for (int r = 0; r < 4; ++r) f[r] = E::get4(h, r);
-            *(f4 *)(T + at(px, ch)) = f;          // 4 channels stay contiguous under the swizzle
-        }
-    }
-    __syncthreads();
-    const float inv = 1.0f / (float)p.hw;
-    for (int t0 = 0; t0 < p.ipt * BN; t0 += 256) {    // same trip count in every lane (shuffles)
-        const int t = t0 + tid;
-        const int k = t / BN, ch = t - k * BN;
-        const bool live = t < p.ipt * BN;
-        const int kk = live ? k : 0;
-        float a[8];
-#pragma unroll
-        for (int jj = 0; jj < 8; ++jj) {
-            float sum = 0.0f;
-#pragma unroll
-            for (int ii = 0; ii < 8; ++ii) {
-                const int px = jj + 8 * ii;
-                sum += px < p.hw ? T[at(kk * p.hw + min(px, p.hw - 1), ch)] : 0.0f;
-            }
-            a[jj] = sum;
-        }
-        const float q = (((a[0] + a[4]) + (a[2] + a[6])) + ((a[1] + a[5]) + (a[3] + a[7]))) * inv;
-        float o[8];
-#pragma unroll
-        for (int c = 0; c < 8; ++c) o[c] = __shfl(q, (lane & ~7) + c);
-        const int img = mt * p.ipt + k, os = nb0 * 2 + ch / 8;
-        if (live && (ch & 7) == 0 && img < p.nimg && os < p.ns) ((h8 *)p.y)[(size_t)os * p.nimg + img] = E::pack(o);
     }
 }
 
@@ -516,7 +552,7 @@ __global__ __launch_bounds__(256) void gemm_pipe_kernel(GemmParams p) {
 
     __syncthreads();
     if (POOL) {
-        pool_epilogue<E, BM, BN, FM, FN>(p, acc, mt, nb0, wm, wn, (float *)&ring[0][0], tid, lane);
+        pool_epilogue<E, BM, BN, FM, FN>(p, acc, mt, nb0, wm * WMP, wn * FN, (float *)&ring[0][0], tid, lane);
         return;
     }
     h8 *stage = wave == 0 ? st0 : wave == 1 ? st1 : wave == 2 ? st2 : st3;

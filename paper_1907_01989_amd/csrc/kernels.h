@@ -58,8 +58,11 @@ hipError_t launch_gemm(const GemmParams &p, int bm, int bn, bool taps, bool f32o
 // pointwise (1x1, stride 1) GEMM with fp16 sliced output: the tile's weight
 // slab in LDS, activations streamed to registers; tile (4 * wm) pixels x bn
 // channels, pf K steps of activation prefetch.  Needs
-// gemm_xs_lds_bytes(ksp, wm, bn) <= 64 KiB and zero weights for padded K.
-hipError_t launch_gemm_xs(const GemmParams &p, int wm, int bn, int pf, hipStream_t st);
+// gemm_xs_lds_bytes(ksp, wm, bn) <= 160 KiB and zero weights for padded K.
+// pool: the output feeds only a global average pool (as launch_gemm_pool:
+// hw, nimg set, M = nimg * hw, hw <= 64; wm 16, bn 16/32/64, pf 2/8); y
+// receives the pooled means.
+hipError_t launch_gemm_xs(const GemmParams &p, int wm, int bn, int pf, bool pool, hipStream_t st);
 // pointwise GEMM with both operands in a 4-stage LDS ring fed by direct
 // global->LDS loads; tile bm pixels x bn channels, bm, bn in {64, 128}
 hipError_t launch_gemm_pipe(const GemmParams &p, int bm, int bn, hipStream_t st);

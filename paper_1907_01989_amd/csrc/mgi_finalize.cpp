@@ -135,22 +135,26 @@ void add_gemm_configs(Node &nd, size_t M) {
             t.ks = 8;
             push(t);
         }
-        const int slabs[4][2] = {{32, 32}, {16, 32}, {32, 64}, {16, 64}};
+        const int slabs[5][2] = {{32, 32}, {16, 32}, {32, 64}, {16, 64}, {16, 16}};
         for (auto &sb : slabs) {
             if (sb[1] > 32 && npad <= 32) continue;
-            const size_t lds = (size_t)(sb[1] / 16) * nd.ksp * 256 +
-                               (size_t)4 * (sb[0] / 16) * (sb[1] / 16) * 1024;
-            if (lds > 65536) continue;
+            const size_t lds = kern::gemm_xs_lds_bytes(nd.ksp, sb[0], sb[1]);
+            // where the grid leaves most compute units idle (a batch of one),
+            // activations 8 K-steps ahead (the K loop waits on memory
+            // latency) and slabs up to the whole LDS (one workgroup per
+            // compute unit costs nothing there)
+            const size_t tiles = (M + 4 * sb[0] - 1) / (4 * sb[0]) * (size_t)((npad + sb[1] - 1) / sb[1]);
+            const bool few = nd.ksp >= 32 && tiles < 128;
+            if (lds > (few ? 160 * 1024 : 65536) || (sb[1] == 16 && !few)) continue;   // 16 channels: p8 only
             GemmTile t;
             t.slab = true;
             t.wm = sb[0];
             t.bn = sb[1];
-            t.pf = nd.ksp >= 8 ? 2 : 1;
-            push(t);
-            // activations 8 K-steps ahead where the grid leaves most compute
-            // units idle (a batch of one: the K loop waits on memory latency)
-            const size_t tiles = (M + 4 * sb[0] - 1) / (4 * sb[0]) * (size_t)((npad + sb[1] - 1) / sb[1]);
-            if (nd.ksp >= 32 && tiles < 128) {
+            if (lds <= 65536 && sb[1] > 16) {
+                t.pf = nd.ksp >= 8 ? 2 : 1;
+                push(t);
+            }
+            if (few) {
                 t.pf = 8;
                 push(t);
             }
@@ -313,6 +317,20 @@ void add_configs(const mgi_plan &p, Node &nd, size_t M) {
             t.pipe = true;
             t.ks = 8;
             nd.cfgs.push_back({t, 0, "pool64x64k8"});
+        }
+        // weight-slab tiles of one 64-row image group (planes of at most 64
+        // pixels) for grids of few workgroups: the slab loads in one round and
+        // the activations stream 8 K-steps ahead
+        const size_t per = (size_t)(64 / hw), groups = ((size_t)nd.dw_in.n + per - 1) / per;
+        for (int bn : {16, 32, 64}) {
+            const size_t lds = kern::gemm_xs_lds_bytes(nd.ksp, 16, bn);
+            if (groups * (size_t)((npad + bn - 1) / bn) >= 128 || nd.ksp < 32 || lds > 160 * 1024) continue;
+            GemmTile ts;
+            ts.slab = true;
+            ts.wm = 16;
+            ts.bn = bn;
+            ts.pf = 8;
+            nd.cfgs.push_back({ts, 0, "poolslab64x" + std::to_string(bn) + "p8"});
         }
         GemmTile t;
         pick_pipe_tile(t, nd.dw_in.pixels(), npad);

@@ -69,7 +69,7 @@ hipError_t launch_split_dw(const mgi_plan &p, const Node &nd, const void *sp, vo
 hipError_t launch_gemm_tile(const GemmParams &q, const GemmTile &t, hipStream_t st) {
     if (t.pipe && t.ks == 8) return launch_gemm_pipe_k8(q, false, st);
     if (t.pipe) return launch_gemm_pipe(q, t.bm, t.bn, st);
-    if (t.slab) return launch_gemm_xs(q, t.wm, t.bn, t.pf, st);
+    if (t.slab) return launch_gemm_xs(q, t.wm, t.bn, t.pf, false, st);
     return launch_gemm(q, t.bm, t.bn, false, false, st);
 }
 
@@ -199,7 +199,7 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
             if (nd.kind == NodeKind::FC) return launch_fc(q, nd.tile.wm, nd.tile.pf, st);
             if (nd.tile.pipe && nd.tile.ks == 8) return launch_gemm_pipe_k8(q, false, st);
             if (nd.tile.pipe) return launch_gemm_pipe(q, nd.tile.bm, nd.tile.bn, st);
-            if (nd.tile.slab) return launch_gemm_xs(q, nd.tile.wm, nd.tile.bn, nd.tile.pf, st);
+            if (nd.tile.slab) return launch_gemm_xs(q, nd.tile.wm, nd.tile.bn, nd.tile.pf, false, st);
             return launch_gemm(q, nd.tile.bm, nd.tile.bn, nd.taps, nd.kind == NodeKind::FC, st);
         }
         case NodeKind::DwPw: {
@@ -347,6 +347,7 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
                 g.y = y;
                 g.hw = mid.h * mid.w;
                 g.nimg = mid.n;
+                if (nd.tile.slab) return launch_gemm_xs(g, nd.tile.wm, nd.tile.bn, nd.tile.pf, true, st);
                 if (nd.tile.ks == 8) return launch_gemm_pipe_k8(g, true, st);
                 return launch_gemm_pool(g, nd.tile.bm, nd.tile.bn, st);
             }

@@ -289,7 +289,7 @@ def test_node_configuration_candidates():
         elif n["kind"] == "stem_dw":
             assert k == 6 and name.startswith(("band", "split"))
         elif n["kind"] == "pw_pool":
-            assert 5 <= k <= 6 and name.startswith(("pool", "split"))
+            assert 5 <= k <= 9 and name.startswith(("pool", "split"))
         elif n["kind"] == "irb":
             assert k >= 3 and name.startswith(("irb", "img", "band", "split3"))
         elif n["kind"] == "fc_gemm":
