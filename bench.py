@@ -618,7 +618,9 @@ def main():
     eprint(f"[bench] {main_res['images_per_s']:.1f} images/s, {main_res['ms_per_step']:.4f} ms/step")
     also = {}
     if not args.no_extra:
-        for key in ("v1_b1", "v2_b1", "v1_b64", "v2_b64"):
+        # every configuration of the metric: the single depthwise-separable
+        # block, both networks at batch 1 and 64, and the 513x513 dense net
+        for key in ("dw_block", "v1_b1", "v2_b1", "v1_b64", "v2_b64", "deeplab"):
             if key == args.workload:
                 continue
             r = run_workload(key, 100, 10, hip, detail=False, tune=tune)
