@@ -368,6 +368,12 @@ constexpr Inst kInsts[] = {
     // channels fill the 256 compute units in one round with fewer pixels per
     // workgroup (two images with 96- or 128-channel tiles measured slower)
     {false, 8, 2, 4, 1, 7, 8, 4, "img64i4", 4},
+    // 64-channel image tiles of four pixel fragments per wave (two 14 x 14
+    // images per workgroup): each weight fragment read from LDS serves four
+    // pixel fragments instead of two, and the weight slab is half that of the
+    // 128-channel tile (measured 1-3% faster than the 128-channel tile on
+    // v1's 14 x 14 nodes; an 8-step activation prefetch was slower)
+    {false, 8, 4, 4, 1, 7, 16, 4, "img64f4"},   {false, 8, 4, 4, 2, 7, 8, 4, "img64f4"},       // 14 x 14, 14 -> 7
     {true, 4, 5, 4, 2, 2, 32, 2, "band2x64w4"},  {true, 8, 4, 4, 2, 4, 32, 2, "band4x64"},     // 56 -> 28
     // 16- and 32-channel image tiles with 2-row depthwise strips, for small
     // batches: more workgroups, and the depthwise step spread over more lanes
