@@ -139,12 +139,13 @@ void add_gemm_configs(Node &nd, size_t M) {
         for (auto &sb : slabs) {
             if (sb[1] > 32 && npad <= 32) continue;
             const size_t lds = kern::gemm_xs_lds_bytes(nd.ksp, sb[0], sb[1]);
-            // where the grid leaves most compute units idle (a batch of one),
-            // activations 8 K-steps ahead (the K loop waits on memory
-            // latency) and slabs up to the whole LDS (one workgroup per
-            // compute unit costs nothing there)
+            // where the grid is less than one workgroup per compute unit (a
+            // batch of one; v2's 7x7 projections at batch 64), activations 8
+            // K-steps ahead (the K loop waits on memory latency) and slabs up
+            // to the whole LDS (one workgroup per compute unit costs nothing
+            // there)
             const size_t tiles = (M + 4 * sb[0] - 1) / (4 * sb[0]) * (size_t)((npad + sb[1] - 1) / sb[1]);
-            const bool few = nd.ksp >= 32 && tiles < 128;
+            const bool few = nd.ksp >= 32 && tiles < 256;
             if (lds > (few ? 160 * 1024 : 65536) || (sb[1] == 16 && !few)) continue;   // 16 channels: p8 only
             GemmTile t;
             t.slab = true;
