@@ -544,3 +544,46 @@ def test_read_node_raw_sizes_and_errors():
         assert err(B.mgi_plan_read_node_raw, plan.handle, kinds.index("conv_stem"), 0x1000) == 4
     finally:
         plan.close()
+
+
+def _config_names(plan, i):
+    names = []
+    for k in range(plan.node_configs()[i][1]):
+        B.mgi_plan_set_node_config(plan.handle, i, k)
+        names.append(plan.node_configs()[i][2])
+    B.mgi_plan_set_node_config(plan.handle, i, 0)
+    return names
+
+
+def test_grid_dependent_candidates():
+    # candidates that exist for some grid sizes only: the four-image 7x7 tile
+    # where it changes the number of image groups (batch 64, not batch 1);
+    # the four-fragment 14x14 tile; weight-slab tiles with the 8-step
+    # prefetch, 16-channel slabs and pooled slab tiles only for grids of less
+    # than one workgroup per compute unit
+    v1 = engine.Plan(workloads.mobilenet_v1(64), bind=False)
+    kinds = [n["kind"] for n in v1.nodes()]
+    shapes = [n["shape"] for n in v1.nodes()]
+    n7 = [i for i, (k, s) in enumerate(zip(kinds, shapes)) if k == "pw_dw" and s[1] == 7 and s[3] == 1024][0]
+    assert "img64i4" in _config_names(v1, n7)
+    n14 = [i for i, (k, s) in enumerate(zip(kinds, shapes)) if k == "pw_dw" and s[1] == 14 and s[3] == 512][0]
+    assert "img64f4" in _config_names(v1, n14)
+    pool64 = _config_names(v1, kinds.index("pw_pool"))
+    assert not any(n.startswith("poolslab") for n in pool64)
+    v1b1 = engine.Plan(workloads.mobilenet_v1(1), bind=False)
+    kinds1 = [n["kind"] for n in v1b1.nodes()]
+    assert not any(n == "img64i4" for i, k in enumerate(kinds1) if k == "pw_dw" for n in _config_names(v1b1, i))
+    pool1 = _config_names(v1b1, kinds1.index("pw_pool"))
+    assert {"poolslab64x16p8", "poolslab64x32p8", "poolslab64x64p8"} <= set(pool1)
+    v2b1 = engine.Plan(workloads.mobilenet_v2(1), bind=False)
+    v2b64 = engine.Plan(workloads.mobilenet_v2(64), bind=False)
+    for plan, few in ((v2b1, True), (v2b64, False)):
+        for i, n in enumerate(plan.nodes()):
+            if n["kind"] != "pw_gemm":
+                continue
+            names = _config_names(plan, i)
+            slabs = [x for x in names if x.startswith("slab")]
+            # 16-channel slabs only with the 8-step prefetch, and only for few workgroups
+            assert all(x.endswith("p8") for x in slabs if "x16" in x)
+            if not few and n["shape"][1] >= 28:
+                assert not any(x.endswith("p8") for x in slabs)
