@@ -272,8 +272,10 @@ __device__ __forceinline__ void pool_epilogue(const GemmParams &p, const f4 (&ac
 
 // ---------------------------------------------------------------------------
 // Pointwise GEMM, weight-slab variant.  The tile's whole weight slab
-// (BN channels x all K, at most 64 KiB) is loaded into LDS once, behind one
-// barrier; each of the 4 waves then owns WM pixels and all BN channels, and
+// (BN channels x all K, up to 64 KiB where several workgroups share a
+// compute unit, up to the whole LDS for grids under one round) is loaded into
+// LDS once, behind one barrier; each of the 4 waves then owns WM pixels and
+// all BN channels, and
 // streams its activation fragments straight from the sliced layout into
 // registers, PF K-steps ahead of their use (a ring of PF register sets indexed
 // statically by unrolling the K loop by PF).  The K loop has no barrier and no
