@@ -275,16 +275,22 @@ __global__ __launch_bounds__(NW * 64, 2) void pwdw_kernel(PwDwParams p) {   // >
         const h8 *rowp[NC];
 #pragma unroll
         for (int k = 0; k < NC; ++k) rowp[k] = plane + (iy0 - ir0) * p.W + cx[k];
+        // every input row of the strip is read before the first FMA, so the
+        // LDS latency of the later rows overlaps the arithmetic of the earlier
+        h8 vr[NR][NC];
 #pragma unroll
         for (int r = 0; r < NR; ++r) {
             const int iy = iy0 + r;
             const bool rv = iy >= ir0 && iy < ir1;
-            h8 v[NC];
 #pragma unroll
             for (int k = 0; k < NC; ++k) {
-                v[k] = *((rv && cv[k]) ? rowp[k] : zslot);
+                vr[r][k] = *((rv && cv[k]) ? rowp[k] : zslot);
                 rowp[k] += p.W;
             }
+        }
+#pragma unroll
+        for (int r = 0; r < NR; ++r) {
+            const h8 *v = vr[r];
             h8 t3[3];
             if (S_ == 1) {          // columns ox-1, ox, ox+1 (left padding 1)
                 t3[0] = wave_shift<kWaveShr1>(v[0]);
