@@ -29,6 +29,7 @@ CASES = [
     (7, 4, 4, 64, 24, ACT_RELU6),        # 8 images per 128-row tile
     (3, 1, 1, 48, 16, ACT_RELU6),        # 1x1 planes
     (1, 7, 7, 256, 128, ACT_RELU6),      # batch 1
+    (2, 8, 8, 264, 40, ACT_NONE),        # weight-slab pooled tiles: K tail, partial block, 64-pixel planes
 ]
 
 
@@ -68,9 +69,10 @@ def test_fused_pool_pair(n, h, w, K, C, act):
     assert ok, msg
 
 
-def test_fused_pool_pair_bf16():
+@pytest.mark.parametrize("n,c", [(16, 320), (1, 64)])
+def test_fused_pool_pair_bf16(n, c):
     from paper_1907_01989_amd import engine, _binding as B
-    desc, y = pair_graph(16, 7, 7, 256, 320, ACT_RELU6)
+    desc, y = pair_graph(n, 7, 7, 256, c, ACT_RELU6)
     bdesc = workloads.as_bf16_graph(desc)
     plan = engine.Plan(bdesc, bind=False, fuse_pool=2, dtype=B.DTYPE_BF16)
     idx = [i for i, k in enumerate(plan.nodes()) if k["kind"] == "pw_pool"]
