@@ -47,6 +47,35 @@ def test_bf16_pointwise(n, h, w, cin, cout, res):
     check_node(desc, nodes, y)
 
 
+@pytest.mark.parametrize("n,h,w,cin,cout", [(1, 14, 14, 512, 160), (1, 7, 7, 960, 320)])
+def test_bf16_pointwise_every_configuration(n, h, w, cin, cout):
+    # every candidate kernel configuration of a small-grid pointwise GEMM
+    # (pipelined tiles, weight-slab tiles with the 8-step prefetch, 16-channel
+    # and up-to-160 KiB slabs) gives the default's bits in bf16 too
+    from paper_1907_01989_amd import engine, _binding as B
+    g = NetBuilder(seed=cin + cout)
+    x = sliced(g, g.input(n, h, w, cin, -1, 1))
+    y = g.conv(x, cout, 1, act=ACT_NONE)
+    g.mark_output(y)
+    desc = workloads.as_bf16_graph(g.graph(f"pwcfg{cin}x{cout}"))
+    plan = engine.Plan(desc, bind=False, dtype=BF16)
+    idx = [i for i, k in enumerate(plan.nodes()) if k["kind"] == "pw_gemm"]
+    assert len(idx) == 1
+    ncfg = plan.node_configs()[idx[0]][1]
+    names = []
+    for c in range(ncfg):
+        B.mgi_plan_set_node_config(plan.handle, idx[0], c)
+        names.append(plan.node_configs()[idx[0]][2])
+    log(f"[case] bf16 {desc['name']} configurations {names}")
+    assert any(nm.endswith("p8") for nm in names)
+    _, base, _ = run_gpu(desc, materialize_all=False, dtype=BF16)
+    for c, nm in enumerate(names):
+        _, o, _ = run_gpu(desc, materialize_all=False, dtype=BF16, configs={idx[0]: c})
+        np.testing.assert_array_equal(o[0], base[0], err_msg=nm)
+    ref = oracle.run_graph(desc, keep=[y], store_bf16=True)[y]
+    check_isolated(desc["name"], base[0], ref.reshape(base[0].shape), rtol=ISO_RTOL_BF16)
+
+
 @pytest.mark.parametrize("k,s,d", [(3, 1, 1), (3, 2, 1), (3, 1, 2), (5, 1, 1)])
 def test_bf16_depthwise_and_conv(k, s, d):
     g = NetBuilder(seed=k + s + d)
