@@ -96,7 +96,9 @@ def test_fused_pair(n, h, w, K, C, s, pads, act):
 
 @pytest.mark.parametrize("n,h,w,K,C,s", [(16, 14, 14, 128, 256, 1),   # image tiles of 16..128 channels
                                          (1, 56, 56, 64, 128, 1),     # 16..128-channel row bands
-                                         (1, 7, 7, 512, 1024, 1)])    # batch-1 7x7 tiles
+                                         (1, 7, 7, 512, 1024, 1),     # batch-1 7x7 tiles
+                                         (9, 7, 7, 256, 256, 1),      # 7x7 tiles capped at four images
+                                         (16, 14, 14, 128, 256, 2)])  # four fragments per wave at stride 2
 def test_fused_pair_bf16(n, h, w, K, C, s):
     from paper_1907_01989_amd import engine, _binding as B
     desc, y = pair_graph(n, h, w, K, C, s, None, ACT_RELU6)
