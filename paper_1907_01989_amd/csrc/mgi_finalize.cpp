@@ -322,8 +322,9 @@ void add_configs(const mgi_plan &p, Node &nd, size_t M) {
         // weight-slab tiles of one 64-row image group (planes of at most 64
         // pixels) for grids of few workgroups: the slab loads in one round and
         // the activations stream 8 K-steps ahead
-        const size_t per = (size_t)(64 / hw), groups = ((size_t)nd.dw_in.n + per - 1) / per;
+        const size_t per = (size_t)std::max(1, 64 / hw), groups = ((size_t)nd.dw_in.n + per - 1) / per;
         for (int bn : {16, 32, 64}) {
+            if (hw > 64) break;   // (a pooled node's planes have at most 64 pixels)
             const size_t lds = kern::gemm_xs_lds_bytes(nd.ksp, 16, bn);
             if (groups * (size_t)((npad + bn - 1) / bn) >= 128 || nd.ksp < 32 || lds > 160 * 1024) continue;
             GemmTile ts;
