@@ -171,190 +171,216 @@ void add_gemm_configs(Node &nd, size_t M) {
     }
 }
 
-void add_configs(const mgi_plan &p, Node &nd, size_t M) {
-    if (nd.kind == NodeKind::Gemm) {
-        add_gemm_configs(nd, M);
-    } else if (nd.kind == NodeKind::PwDw) {
-        // channels per workgroup of the fused pointwise + depthwise kernel, and
-        // the two separate kernels through the scratch tensor (pipelined GEMM
-        // tile by the pointwise rule, depthwise rows by the depthwise rule);
-        // the split form first when the fused kernel would not fill the GPU
-        const Shape &s = nd.dw_in;
-        const int nf = kern::pwdw_configs(s.n, s.h, s.w, nd.dw_out.h, nd.dw_out.w, nd.dw_conv.stride_h,
-                                          nd.dw_conv.pad_t, nd.dw_conv.pad_l, nd.ksp, nd.nb16, -1, nullptr, nullptr);
-        for (int c = 0; c < nf; ++c) {
-            const char *name = "";
-            kern::pwdw_configs(s.n, s.h, s.w, nd.dw_out.h, nd.dw_out.w, nd.dw_conv.stride_h, nd.dw_conv.pad_t,
-                               nd.dw_conv.pad_l, nd.ksp, nd.nb16, c, nullptr, &name);
-            Node::Config fc{GemmTile{}, 0, name, false, c};
-            nd.cfgs.push_back(fc);
-        }
-        GemmTile t;
-        pick_pipe_tile(t, nd.dw_in.pixels(), nd.nb16 * 16);
-        const int dwr = nd.dw_conv.stride_h == 1 ? 4 : 2;
-        const Node::Config split{t, dwr, "split_" + tile_name(t), true, 0};
-        nd.cfgs.insert(nd.fused_default ? nd.cfgs.end() : nd.cfgs.begin(), Node::Config(split));
-        if (nd.ksp % 8 == 0) {                // the GEMM with two K-steps per ring stage
-            GemmTile t8;
-            t8.pipe = true;
-            t8.ks = 8;
-            nd.cfgs.push_back(Node::Config{t8, dwr, "split_" + tile_name(t8), true, 0});
-        }
-        nd.apply(0);
-    } else if (nd.kind == NodeKind::Irb) {
-        // the block kernel's configurations; the fused pointwise -> depthwise
-        // kernel's configurations, each followed by the projection GEMM; the
-        // three separate kernels.  The block kernel first when it fills the
-        // GPU, else the form the pointwise -> depthwise node would have taken.
-        // The projection GEMM of the split forms: the weight-slab tile for at
-        // most 32 output channels (it streams the wide input once), else the
-        // pipelined tile by the pointwise rule.
-        const Shape &s = nd.dw_in, &d = nd.dw_out;
-        {
-            const int npad = nd.pj_nb16 * 16;
-            const size_t slab_lds = (size_t)2 * nd.pj_ksp * 256 + (size_t)4 * 2 * 2 * 1024;
-            GemmTile t;
-            if (npad <= 32 && slab_lds <= 65536) {
-                t.slab = true;
-                t.wm = 32;
-                t.bn = 32;
-                t.pf = nd.pj_ksp >= 8 ? 2 : 1;
-            } else if (npad >= 64) {
-                pick_pipe_tile(t, d.pixels(), npad);
-            } else {
-                t = pick_tile(d.pixels(), npad);
-            }
-            nd.pj_tile = t;
-        }
-        const int st = nd.dw_conv.stride_h, pt = nd.dw_conv.pad_t, pl = nd.dw_conv.pad_l;
-        std::vector<Node::Config> blk, two, three;
-        const int nb = kern::irb_configs(s.n, s.h, s.w, d.h, d.w, st, pt, pl, nd.ksp, nd.nb16, nd.pj_nb16, -1,
-                                         nullptr, nullptr);
-        for (int c = 0; c < nb; ++c) {
-            const char *name = "";
-            kern::irb_configs(s.n, s.h, s.w, d.h, d.w, st, pt, pl, nd.ksp, nd.nb16, nd.pj_nb16, c, &name, nullptr);
-            blk.push_back(Node::Config{GemmTile{}, 0, name, false, c, 0});
-        }
-        const int nf = kern::pwdw_configs(s.n, s.h, s.w, d.h, d.w, st, pt, pl, nd.ksp, nd.nb16, -1, nullptr, nullptr);
-        for (int c = 0; c < nf; ++c) {
-            const char *name = "";
-            kern::pwdw_configs(s.n, s.h, s.w, d.h, d.w, st, pt, pl, nd.ksp, nd.nb16, c, nullptr, &name);
-            two.push_back(Node::Config{GemmTile{}, 0, std::string(name) + "+" + tile_name(nd.pj_tile), true, c, 1});
-        }
-        GemmTile t;
-        pick_pipe_tile(t, s.pixels(), nd.nb16 * 16);
-        three.push_back(Node::Config{t, st == 1 ? 4 : 2, "split3_" + tile_name(t), true, 0, 2});
-        std::vector<Node::Config> order;
-        auto add = [&](const std::vector<Node::Config> &v) { order.insert(order.end(), v.begin(), v.end()); };
-        if (nd.irb_default) {
-            add(blk); add(two); add(three);
-        } else if (nd.fused_default) {
-            add(two); add(blk); add(three);
-        } else {
-            add(three); add(two); add(blk);
-        }
-        nd.cfgs = order;
-        nd.apply(0);
-    } else if (nd.kind == NodeKind::StemDw) {
-        // band heights of the fused stem + depthwise kernel, and the two
-        // separate kernels through the scratch tensor (first when the fused
-        // kernel would not fill the GPU)
-        kern::StemDwParams q{};
-        stemdw_shape(p, nd, q);
-        const int nf = kern::stemdw_configs(q, -1, nullptr, nullptr);
-        for (int c = 0; c < nf; ++c) {
-            const char *name = "";
-            kern::stemdw_configs(q, c, nullptr, &name);
-            nd.cfgs.push_back(Node::Config{GemmTile{}, 0, name, false, c});
-        }
-        const Node::Config split{GemmTile{}, 4, "split", true, 0};
-        nd.cfgs.insert(nd.fused_default ? nd.cfgs.end() : nd.cfgs.begin(), Node::Config(split));
-        nd.apply(0);
-    } else if (nd.kind == NodeKind::FC || nd.kind == NodeKind::FcSoftmax) {
-        // images per workgroup (16 * fm) and K-steps per load batch; 16 images
-        // and 8 steps first (the most workgroups, one load latency per wave:
-        // fastest on v1 b64, 5.6 us against 8.2 us for 64 images and 4 steps)
-        const int fm0 = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
-        const int opts[6][2] = {{1, 8}, {2, 8}, {4, 8}, {1, 4}, {2, 4}, {4, 4}};
-        for (auto &o : opts) {
-            if (o[0] > fm0) continue;
-            bool dup = false;
-            for (const Node::Config &c : nd.cfgs) dup = dup || (c.tile.wm == o[0] && c.tile.pf == o[1]);
-            if (dup) continue;
-            GemmTile t;
-            t.wm = o[0];
-            t.pf = o[1];
-            nd.cfgs.push_back({t, 0, "fc" + std::to_string(16 * o[0]) + "k" + std::to_string(o[1])});
-        }
-        if (nd.kind == NodeKind::FcSoftmax) {
-            // FC into the logits, then the softmax kernel: first when there
-            // is more than one tile of 16 rows (each arriving workgroup's L2
-            // write-back costs more than the softmax launch it saves once
-            // the grid has a few hundred workgroups: 16.1 us fused against
-            // 10.6 us split for 64 rows of 1000 classes, 7.2 against 9.6 us
-            // for one row)
-            Node::Config split = nd.cfgs[0];
-            split.name = "split_" + split.name;
-            split.split = true;
-            nd.cfgs.insert(M > 16 ? nd.cfgs.begin() : nd.cfgs.end(), split);
-        }
-        nd.apply(0);
-    } else if (nd.kind == NodeKind::GemmPool) {
-        // tiles of the pooled GEMM (M-tiles of whole images), and the GEMM
-        // then the pool kernel through the scratch tensor (first when the
-        // fused kernel would not fill the GPU)
-        const int hw = nd.dw_in.h * nd.dw_in.w, npad = nd.nb16 * 16;
-        const int tiles[4][2] = {{128, 64}, {128, 128}, {64, 128}, {64, 64}};
-        for (auto &tb : tiles) {
-            if (hw > tb[0] || (tb[1] > 64 && npad <= 64)) continue;
-            GemmTile t;
-            t.pipe = true;
-            t.bm = tb[0];
-            t.bn = tb[1];
-            nd.cfgs.push_back({t, 0, "pool" + std::to_string(tb[0]) + "x" + std::to_string(tb[1])});
-        }
-        if (nd.ksp % 8 == 0) {
-            GemmTile t;
-            t.pipe = true;
-            t.ks = 8;
-            nd.cfgs.push_back({t, 0, "pool64x64k8"});
-        }
-        // weight-slab tiles of one 64-row image group (planes of at most 64
-        // pixels) for grids of few workgroups: the slab loads in one round and
-        // the activations stream 8 K-steps ahead
-        const size_t per = (size_t)std::max(1, 64 / hw), groups = ((size_t)nd.dw_in.n + per - 1) / per;
-        for (int bn : {16, 32, 64}) {
-            if (hw > 64) break;   // (a pooled node's planes have at most 64 pixels)
-            const size_t lds = kern::gemm_xs_lds_bytes(nd.ksp, 16, bn);
-            if (groups * (size_t)((npad + bn - 1) / bn) >= 128 || nd.ksp < 32 || lds > 160 * 1024) continue;
-            GemmTile ts;
-            ts.slab = true;
-            ts.wm = 16;
-            ts.bn = bn;
-            ts.pf = 8;
-            nd.cfgs.push_back({ts, 0, "poolslab64x" + std::to_string(bn) + "p8"});
-        }
-        GemmTile t;
-        pick_pipe_tile(t, nd.dw_in.pixels(), npad);
-        const Node::Config split{t, 0, "split_" + tile_name(t), true, 0};
-        nd.cfgs.insert(nd.fused_default ? nd.cfgs.end() : nd.cfgs.begin(), Node::Config(split));
-        nd.apply(0);
-    } else if (nd.kind == NodeKind::DwPw) {
-        // band heights for the fused depthwise + pointwise kernel: up to 128
-        // or up to 64 pixels per workgroup
-        for (int px : {128, 64}) {
-            GemmTile t;
-            t.bm = px;
-            nd.cfgs.push_back({t, 0, "band" + std::to_string(px)});
-        }
-    } else if (nd.kind == NodeKind::Depthwise && nd.conv.kh == 3 && nd.conv.kw == 3 &&
-               nd.conv.stride_h == nd.conv.stride_w && nd.conv.dil_h == nd.conv.dil_w &&
-               nd.conv.stride_h <= 2 && nd.conv.dil_h <= 2) {
-        const int rows[2][3] = {{4, 2, 8}, {2, 1, 4}};
-        for (int r : rows[nd.conv.stride_h - 1]) nd.cfgs.push_back({GemmTile{}, r, "rows" + std::to_string(r)});
-        nd.dw_rows = nd.cfgs[0].dw_rows;
+void add_pwdw_configs(Node &nd) {
+    // channels per workgroup of the fused pointwise + depthwise kernel, and
+    // the two separate kernels through the scratch tensor (pipelined GEMM
+    // tile by the pointwise rule, depthwise rows by the depthwise rule);
+    // the split form first when the fused kernel would not fill the GPU
+    const Shape &s = nd.dw_in;
+    const int nf = kern::pwdw_configs(s.n, s.h, s.w, nd.dw_out.h, nd.dw_out.w, nd.dw_conv.stride_h,
+                                      nd.dw_conv.pad_t, nd.dw_conv.pad_l, nd.ksp, nd.nb16, -1, nullptr, nullptr);
+    for (int c = 0; c < nf; ++c) {
+        const char *name = "";
+        kern::pwdw_configs(s.n, s.h, s.w, nd.dw_out.h, nd.dw_out.w, nd.dw_conv.stride_h, nd.dw_conv.pad_t,
+                           nd.dw_conv.pad_l, nd.ksp, nd.nb16, c, nullptr, &name);
+        Node::Config fc{GemmTile{}, 0, name, false, c};
+        nd.cfgs.push_back(fc);
     }
-    (void)M;
+    GemmTile t;
+    pick_pipe_tile(t, nd.dw_in.pixels(), nd.nb16 * 16);
+    const int dwr = nd.dw_conv.stride_h == 1 ? 4 : 2;
+    const Node::Config split{t, dwr, "split_" + tile_name(t), true, 0};
+    nd.cfgs.insert(nd.fused_default ? nd.cfgs.end() : nd.cfgs.begin(), Node::Config(split));
+    if (nd.ksp % 8 == 0) {                // the GEMM with two K-steps per ring stage
+        GemmTile t8;
+        t8.pipe = true;
+        t8.ks = 8;
+        nd.cfgs.push_back(Node::Config{t8, dwr, "split_" + tile_name(t8), true, 0});
+    }
+    nd.apply(0);
+}
+
+void add_irb_configs(Node &nd) {
+    // the block kernel's configurations; the fused pointwise -> depthwise
+    // kernel's configurations, each followed by the projection GEMM; the
+    // three separate kernels.  The block kernel first when it fills the
+    // GPU, else the form the pointwise -> depthwise node would have taken.
+    // The projection GEMM of the split forms: the weight-slab tile for at
+    // most 32 output channels (it streams the wide input once), else the
+    // pipelined tile by the pointwise rule.
+    const Shape &s = nd.dw_in, &d = nd.dw_out;
+    {
+        const int npad = nd.pj_nb16 * 16;
+        const size_t slab_lds = (size_t)2 * nd.pj_ksp * 256 + (size_t)4 * 2 * 2 * 1024;
+        GemmTile t;
+        if (npad <= 32 && slab_lds <= 65536) {
+            t.slab = true;
+            t.wm = 32;
+            t.bn = 32;
+            t.pf = nd.pj_ksp >= 8 ? 2 : 1;
+        } else if (npad >= 64) {
+            pick_pipe_tile(t, d.pixels(), npad);
+        } else {
+            t = pick_tile(d.pixels(), npad);
+        }
+        nd.pj_tile = t;
+    }
+    const int st = nd.dw_conv.stride_h, pt = nd.dw_conv.pad_t, pl = nd.dw_conv.pad_l;
+    std::vector<Node::Config> blk, two, three;
+    const int nb = kern::irb_configs(s.n, s.h, s.w, d.h, d.w, st, pt, pl, nd.ksp, nd.nb16, nd.pj_nb16, -1,
+                                     nullptr, nullptr);
+    for (int c = 0; c < nb; ++c) {
+        const char *name = "";
+        kern::irb_configs(s.n, s.h, s.w, d.h, d.w, st, pt, pl, nd.ksp, nd.nb16, nd.pj_nb16, c, &name, nullptr);
+        blk.push_back(Node::Config{GemmTile{}, 0, name, false, c, 0});
+    }
+    const int nf = kern::pwdw_configs(s.n, s.h, s.w, d.h, d.w, st, pt, pl, nd.ksp, nd.nb16, -1, nullptr, nullptr);
+    for (int c = 0; c < nf; ++c) {
+        const char *name = "";
+        kern::pwdw_configs(s.n, s.h, s.w, d.h, d.w, st, pt, pl, nd.ksp, nd.nb16, c, nullptr, &name);
+        two.push_back(Node::Config{GemmTile{}, 0, std::string(name) + "+" + tile_name(nd.pj_tile), true, c, 1});
+    }
+    GemmTile t;
+    pick_pipe_tile(t, s.pixels(), nd.nb16 * 16);
+    three.push_back(Node::Config{t, st == 1 ? 4 : 2, "split3_" + tile_name(t), true, 0, 2});
+    std::vector<Node::Config> order;
+    auto add = [&](const std::vector<Node::Config> &v) { order.insert(order.end(), v.begin(), v.end()); };
+    if (nd.irb_default) {
+        add(blk); add(two); add(three);
+    } else if (nd.fused_default) {
+        add(two); add(blk); add(three);
+    } else {
+        add(three); add(two); add(blk);
+    }
+    nd.cfgs = order;
+    nd.apply(0);
+}
+
+void add_stemdw_configs(const mgi_plan &p, Node &nd) {
+    // band heights of the fused stem + depthwise kernel, and the two
+    // separate kernels through the scratch tensor (first when the fused
+    // kernel would not fill the GPU)
+    kern::StemDwParams q{};
+    stemdw_shape(p, nd, q);
+    const int nf = kern::stemdw_configs(q, -1, nullptr, nullptr);
+    for (int c = 0; c < nf; ++c) {
+        const char *name = "";
+        kern::stemdw_configs(q, c, nullptr, &name);
+        nd.cfgs.push_back(Node::Config{GemmTile{}, 0, name, false, c});
+    }
+    const Node::Config split{GemmTile{}, 4, "split", true, 0};
+    nd.cfgs.insert(nd.fused_default ? nd.cfgs.end() : nd.cfgs.begin(), Node::Config(split));
+    nd.apply(0);
+}
+
+void add_fc_configs(Node &nd, size_t M) {
+    // images per workgroup (16 * fm) and K-steps per load batch; 16 images
+    // and 8 steps first (the most workgroups, one load latency per wave:
+    // fastest on v1 b64, 5.6 us against 8.2 us for 64 images and 4 steps)
+    const int fm0 = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
+    const int opts[6][2] = {{1, 8}, {2, 8}, {4, 8}, {1, 4}, {2, 4}, {4, 4}};
+    for (auto &o : opts) {
+        if (o[0] > fm0) continue;
+        bool dup = false;
+        for (const Node::Config &c : nd.cfgs) dup = dup || (c.tile.wm == o[0] && c.tile.pf == o[1]);
+        if (dup) continue;
+        GemmTile t;
+        t.wm = o[0];
+        t.pf = o[1];
+        nd.cfgs.push_back({t, 0, "fc" + std::to_string(16 * o[0]) + "k" + std::to_string(o[1])});
+    }
+    if (nd.kind == NodeKind::FcSoftmax) {
+        // FC into the logits, then the softmax kernel: first when there
+        // is more than one tile of 16 rows (each arriving workgroup's L2
+        // write-back costs more than the softmax launch it saves once
+        // the grid has a few hundred workgroups: 16.1 us fused against
+        // 10.6 us split for 64 rows of 1000 classes, 7.2 against 9.6 us
+        // for one row)
+        Node::Config split = nd.cfgs[0];
+        split.name = "split_" + split.name;
+        split.split = true;
+        nd.cfgs.insert(M > 16 ? nd.cfgs.begin() : nd.cfgs.end(), split);
+    }
+    nd.apply(0);
+}
+
+void add_pool_configs(Node &nd) {
+    // tiles of the pooled GEMM (M-tiles of whole images), and the GEMM
+    // then the pool kernel through the scratch tensor (first when the
+    // fused kernel would not fill the GPU)
+    const int hw = nd.dw_in.h * nd.dw_in.w, npad = nd.nb16 * 16;
+    const int tiles[4][2] = {{128, 64}, {128, 128}, {64, 128}, {64, 64}};
+    for (auto &tb : tiles) {
+        if (hw > tb[0] || (tb[1] > 64 && npad <= 64)) continue;
+        GemmTile t;
+        t.pipe = true;
+        t.bm = tb[0];
+        t.bn = tb[1];
+        nd.cfgs.push_back({t, 0, "pool" + std::to_string(tb[0]) + "x" + std::to_string(tb[1])});
+    }
+    if (nd.ksp % 8 == 0) {
+        GemmTile t;
+        t.pipe = true;
+        t.ks = 8;
+        nd.cfgs.push_back({t, 0, "pool64x64k8"});
+    }
+    // weight-slab tiles of one 64-row image group (planes of at most 64
+    // pixels) for grids of few workgroups: the slab loads in one round and
+    // the activations stream 8 K-steps ahead
+    const size_t per = (size_t)std::max(1, 64 / hw), groups = ((size_t)nd.dw_in.n + per - 1) / per;
+    for (int bn : {16, 32, 64}) {
+        if (hw > 64) break;   // (a pooled node's planes have at most 64 pixels)
+        const size_t lds = kern::gemm_xs_lds_bytes(nd.ksp, 16, bn);
+        if (groups * (size_t)((npad + bn - 1) / bn) >= 128 || nd.ksp < 32 || lds > 160 * 1024) continue;
+        GemmTile ts;
+        ts.slab = true;
+        ts.wm = 16;
+        ts.bn = bn;
+        ts.pf = 8;
+        nd.cfgs.push_back({ts, 0, "poolslab64x" + std::to_string(bn) + "p8"});
+    }
+    GemmTile t;
+    pick_pipe_tile(t, nd.dw_in.pixels(), npad);
+    const Node::Config split{t, 0, "split_" + tile_name(t), true, 0};
+    nd.cfgs.insert(nd.fused_default ? nd.cfgs.end() : nd.cfgs.begin(), Node::Config(split));
+    nd.apply(0);
+}
+
+void add_dwpw_configs(Node &nd) {
+    // band heights for the fused depthwise + pointwise kernel: up to 128
+    // or up to 64 pixels per workgroup
+    for (int px : {128, 64}) {
+        GemmTile t;
+        t.bm = px;
+        nd.cfgs.push_back({t, 0, "band" + std::to_string(px)});
+    }
+}
+
+// rows per thread of the 3x3 depthwise kernel (stride 1 or 2, dilation 1 or 2)
+void add_depthwise_configs(Node &nd) {
+    if (nd.conv.kh != 3 || nd.conv.kw != 3 || nd.conv.stride_h != nd.conv.stride_w ||
+        nd.conv.dil_h != nd.conv.dil_w || nd.conv.stride_h > 2 || nd.conv.dil_h > 2)
+        return;
+    const int rows[2][3] = {{4, 2, 8}, {2, 1, 4}};
+    for (int r : rows[nd.conv.stride_h - 1]) nd.cfgs.push_back({GemmTile{}, r, "rows" + std::to_string(r)});
+    nd.dw_rows = nd.cfgs[0].dw_rows;
+}
+
+// the node's candidate configurations, in preference order (the first is
+// the one a plan runs before any autotuning)
+void add_configs(const mgi_plan &p, Node &nd, size_t M) {
+    switch (nd.kind) {
+        case NodeKind::Gemm: add_gemm_configs(nd, M); break;
+        case NodeKind::PwDw: add_pwdw_configs(nd); break;
+        case NodeKind::Irb: add_irb_configs(nd); break;
+        case NodeKind::StemDw: add_stemdw_configs(p, nd); break;
+        case NodeKind::FC:
+        case NodeKind::FcSoftmax: add_fc_configs(nd, M); break;
+        case NodeKind::GemmPool: add_pool_configs(nd); break;
+        case NodeKind::DwPw: add_dwpw_configs(nd); break;
+        case NodeKind::Depthwise: add_depthwise_configs(nd); break;
+        default: break;
+    }
 }
 
 // Depthwise -> pointwise fusion (Sec. 3.2's fusion extended to the
@@ -1437,6 +1463,9 @@ extern "C" mgi_status mgi_graph_finalize(const mgi_graph *g, const mgi_options *
         s = build_plan(*g, *o, *plan);
     } catch (const std::bad_alloc &) {
         s = fail(MGI_ERR_OOM_HOST, "mgi_graph_finalize: out of host memory");
+    } catch (...) {
+        delete plan;   // (the wrapper below turns the exception into a status)
+        throw;
     }
     if (s != MGI_OK) {
         delete plan;

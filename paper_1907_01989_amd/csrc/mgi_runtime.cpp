@@ -113,6 +113,266 @@ hipError_t launch_node_expand(const mgi_plan &p, const Node &nd, const Bases &B,
     return nd.tile.ks == 8 ? launch_gemm_pipe_k8(g, false, st) : launch_gemm_pipe(g, nd.tile.bm, nd.tile.bn, st);
 }
 
+hipError_t launch_fcsoftmax_node(const mgi_plan &p, const Node &nd, const Bases &B, void *y, hipStream_t st) {
+    const char *wbase = static_cast<const char *>(p.dev_w);
+    const bool bf = p.opt.dtype == MGI_DTYPE_BF16;
+    // FC + softmax: one FC launch whose last workgroup per row tile
+    // runs the softmax, or (split) the FC into the logits scratch and
+    // the softmax kernel
+    const Shape lg = p.bufs[nd.scratch].shape;
+    float *logits = (float *)buf_ptr(p, nd.scratch, B);
+    GemmParams q{};
+    q.bf16 = bf;
+    q.x = (const h8 *)buf_ptr(p, nd.in[0], B);
+    q.w = (const h8 *)(wbase + nd.w_off);
+    q.bias = (const float *)(wbase + nd.b_off);
+    q.y = logits;
+    q.M = (int)lg.pixels();
+    q.Min = (int)p.bufs[nd.in[0]].shape.pixels();
+    q.ksl = nd.ksl; q.ksp = nd.ksp;
+    q.nb16 = nd.nb16; q.ns = slices(lg.c); q.cout = lg.c;
+    q.act1 = nd.act1; q.act2 = nd.act2;
+    if (!nd.split) {
+        q.sm_y = (float *)y;
+        q.sm_cnt = (int *)(B.ws + nd.cnt_off);
+        return launch_fc(q, nd.tile.wm, nd.tile.pf, st);
+    }
+    LaunchEvents &ev = launch_events();
+    const LaunchEvents saved = ev;
+    ev.stop = nullptr;
+    hipError_t e = launch_fc(q, nd.tile.wm, nd.tile.pf, st);
+    ev.start = nullptr;
+    ev.stop = saved.stop;
+    if (e == hipSuccess) e = launch_softmax(logits, (float *)y, q.M, q.cout, st);
+    ev = saved;
+    return e;
+}
+
+hipError_t launch_irb_node(const mgi_plan &p, const Node &nd, const Bases &B, void *y, hipStream_t st) {
+    const char *wbase = static_cast<const char *>(p.dev_w);
+    const Shape os = p.bufs[nd.out].shape;
+    const bool bf = p.opt.dtype == MGI_DTYPE_BF16;
+    const Shape d = nd.dw_out;
+    if (nd.mode == 0) {
+        IrbParams q{};
+        q.bf16 = bf;
+        q.x = (const h8 *)buf_ptr(p, nd.in[0], B);
+        q.w = (const h8 *)(wbase + nd.w_off);
+        q.bias = (const float *)(wbase + nd.b_off);
+        q.M = (int)nd.dw_in.pixels();
+        q.ksl = nd.ksl; q.ksp = nd.ksp; q.nb16 = nd.nb16; q.act1 = nd.act1;
+        q.dw_w = (const h8 *)(wbase + nd.dw_w_off);
+        q.dw_b = (const float *)(wbase + nd.dw_b_off);
+        q.ns = slices(d.c); q.act2 = nd.dw_act;
+        q.pw = (const h8 *)(wbase + nd.pj_w_off);
+        q.pbias = (const float *)(wbase + nd.pj_b_off);
+        q.pksp = nd.pj_ksp; q.pnb16 = nd.pj_nb16; q.pact1 = nd.pj_act1; q.pact2 = nd.pj_act2;
+        q.res = nd.residual >= 0 ? (const h8 *)buf_ptr(p, nd.residual, B) : nullptr;
+        q.y = (h8 *)y;
+        q.ps = slices(os.c); q.MO = (int)os.pixels();
+        q.N = nd.dw_in.n; q.H = nd.dw_in.h; q.W = nd.dw_in.w; q.OH = d.h; q.OW = d.w;
+        q.S = nd.dw_conv.stride_h; q.pt = nd.dw_conv.pad_t; q.pl = nd.dw_conv.pad_l;
+        return launch_irb(q, nd.pwdw_cfg, st);
+    }
+    // split forms: the expansion and depthwise into the depthwise
+    // scratch (one fused kernel, or the GEMM and the depthwise kernel),
+    // then the projection GEMM; a timed run stamps the first kernel's
+    // start and the last one's end
+    LaunchEvents &ev = launch_events();
+    const LaunchEvents saved = ev;
+    void *d2 = buf_ptr(p, nd.scratch2, B);
+    hipError_t e;
+    ev.stop = nullptr;
+    if (nd.mode == 1) {
+        e = launch_node_pwdw(p, nd, B, d2, slices(d.c), bf, st);
+    } else {
+        e = launch_node_expand(p, nd, B, bf, st);
+        ev.start = nullptr;
+        if (e == hipSuccess) e = launch_split_dw(p, nd, buf_ptr(p, nd.scratch, B), d2, bf, st);
+    }
+    ev.start = nullptr;
+    ev.stop = saved.stop;
+    if (e == hipSuccess) {
+        GemmParams g{};
+        g.bf16 = bf;
+        g.x = (const h8 *)d2;
+        g.w = (const h8 *)(wbase + nd.pj_w_off);
+        g.bias = (const float *)(wbase + nd.pj_b_off);
+        g.res = nd.residual >= 0 ? (const h8 *)buf_ptr(p, nd.residual, B) : nullptr;
+        g.y = y;
+        g.M = g.Min = (int)os.pixels();
+        g.ksl = nd.pj_ksl; g.ksp = nd.pj_ksp;
+        g.nb16 = nd.pj_nb16; g.ns = slices(os.c); g.cout = os.c;
+        g.act1 = nd.pj_act1; g.act2 = nd.pj_act2;
+        e = launch_gemm_tile(g, nd.pj_tile, st);
+    }
+    ev = saved;
+    return e;
+}
+
+hipError_t launch_pwdw_node(const mgi_plan &p, const Node &nd, const Bases &B, void *y, hipStream_t st) {
+    const char *wbase = static_cast<const char *>(p.dev_w);
+    const Shape os = p.bufs[nd.out].shape;
+    const bool bf = p.opt.dtype == MGI_DTYPE_BF16;
+    if (nd.split) {
+        // the pointwise GEMM into the scratch tensor, then the depthwise
+        // kernel; a timed run stamps the first kernel's start and the
+        // second one's end
+        LaunchEvents &ev = launch_events();
+        const LaunchEvents saved = ev;
+        const Shape mid = nd.dw_in;
+        void *sp = buf_ptr(p, nd.scratch, B);
+        GemmParams g{};
+        g.bf16 = bf;
+        g.x = (const h8 *)buf_ptr(p, nd.in[0], B);
+        g.w = (const h8 *)(wbase + nd.w_off);
+        g.bias = (const float *)(wbase + nd.b_off);
+        g.y = sp;
+        g.M = g.Min = (int)mid.pixels();
+        g.ksl = nd.ksl; g.ksp = nd.ksp;
+        g.nb16 = nd.nb16; g.ns = slices(mid.c); g.cout = mid.c;
+        g.act1 = nd.act1; g.act2 = MGI_ACT_NONE;
+        ev.stop = nullptr;
+        hipError_t e = nd.tile.ks == 8 ? launch_gemm_pipe_k8(g, false, st)
+                                       : launch_gemm_pipe(g, nd.tile.bm, nd.tile.bn, st);
+        ev.start = nullptr;
+        ev.stop = saved.stop;
+        if (e == hipSuccess) e = launch_split_dw(p, nd, sp, y, bf, st);
+        ev = saved;
+        return e;
+    }
+    PwDwParams q{};
+    q.bf16 = bf;
+    q.x = (const h8 *)buf_ptr(p, nd.in[0], B);
+    q.w = (const h8 *)(wbase + nd.w_off);
+    q.bias = (const float *)(wbase + nd.b_off);
+    q.M = (int)nd.dw_in.pixels();
+    q.ksl = nd.ksl; q.ksp = nd.ksp; q.nb16 = nd.nb16; q.act1 = nd.act1;
+    q.dw_w = (const h8 *)(wbase + nd.dw_w_off);
+    q.dw_b = (const float *)(wbase + nd.dw_b_off);
+    q.y = (h8 *)y;
+    q.N = nd.dw_in.n; q.H = nd.dw_in.h; q.W = nd.dw_in.w; q.OH = os.h; q.OW = os.w;
+    q.S = nd.dw_conv.stride_h; q.pt = nd.dw_conv.pad_t; q.pl = nd.dw_conv.pad_l;
+    q.act2 = nd.dw_act;
+    q.ns = slices(os.c);
+    return launch_pwdw(q, nd.pwdw_cfg, st);
+}
+
+hipError_t launch_gemmpool_node(const mgi_plan &p, const Node &nd, const Bases &B, void *y, hipStream_t st) {
+    const char *wbase = static_cast<const char *>(p.dev_w);
+    const bool bf = p.opt.dtype == MGI_DTYPE_BF16;
+    // pointwise GEMM + global average pool: the pooled GEMM kernel,
+    // or (split) the GEMM into the scratch tensor and the pool kernel
+    const Shape mid = nd.dw_in;
+    GemmParams g{};
+    g.bf16 = bf;
+    g.x = (const h8 *)buf_ptr(p, nd.in[0], B);
+    g.w = (const h8 *)(wbase + nd.w_off);
+    g.bias = (const float *)(wbase + nd.b_off);
+    g.M = g.Min = (int)mid.pixels();
+    g.ksl = nd.ksl; g.ksp = nd.ksp;
+    g.nb16 = nd.nb16; g.ns = slices(mid.c); g.cout = mid.c;
+    g.act1 = nd.act1; g.act2 = MGI_ACT_NONE;
+    if (!nd.split) {
+        g.y = y;
+        g.hw = mid.h * mid.w;
+        g.nimg = mid.n;
+        if (nd.tile.slab) return launch_gemm_xs(g, nd.tile.wm, nd.tile.bn, nd.tile.pf, true, st);
+        if (nd.tile.ks == 8) return launch_gemm_pipe_k8(g, true, st);
+        return launch_gemm_pool(g, nd.tile.bm, nd.tile.bn, st);
+    }
+    LaunchEvents &ev = launch_events();
+    const LaunchEvents saved = ev;
+    void *sp = buf_ptr(p, nd.scratch, B);
+    g.y = sp;
+    ev.stop = nullptr;
+    hipError_t e = launch_gemm_pipe(g, nd.tile.bm, nd.tile.bn, st);
+    ev.start = nullptr;
+    ev.stop = saved.stop;
+    if (e == hipSuccess)
+        e = launch_gap((const h8 *)sp, (h8 *)y, (const h8 *)(wbase + p.zero_off), mid.n, mid.h * mid.w,
+                       slices(mid.c), bf, st);
+    ev = saved;
+    return e;
+}
+
+hipError_t launch_stemdw_node(const mgi_plan &p, const Node &nd, const Bases &B, void *y, hipStream_t st) {
+    const char *wbase = static_cast<const char *>(p.dev_w);
+    const bool bf = p.opt.dtype == MGI_DTYPE_BF16;
+    const Buf &ib = p.bufs[nd.in[0]];
+    const bool fp16_in = ib.in_dtype == MGI_DTYPE_FP16;
+    if (nd.split) {
+        // the stem kernel into the scratch tensor, then the depthwise
+        // kernel (timed as one: first kernel's start, second's end)
+        LaunchEvents &ev = launch_events();
+        const LaunchEvents saved = ev;
+        const Shape mid = nd.dw_in;
+        void *sp = buf_ptr(p, nd.scratch, B);
+        StemParams q{};
+        q.bf16 = bf;
+        q.x = buf_ptr(p, nd.in[0], B);
+        q.w = (const h8 *)(wbase + nd.w_off);
+        q.bias = (const float *)(wbase + nd.b_off);
+        q.res = nullptr;
+        q.y = (h8 *)sp;
+        q.N = ib.shape.n; q.H = ib.shape.h; q.W = ib.shape.w; q.C = ib.shape.c;
+        q.OH = mid.h; q.OW = mid.w; q.M = (int)mid.pixels();
+        q.KH = nd.conv.kh; q.KW = nd.conv.kw; q.K = nd.conv.kh * nd.conv.kw * ib.shape.c;
+        q.sh = nd.conv.stride_h; q.sw = nd.conv.stride_w;
+        q.dh = nd.conv.dil_h; q.dw = nd.conv.dil_w;
+        q.pt = nd.conv.pad_t; q.pl = nd.conv.pad_l;
+        q.nb16 = nd.nb16; q.ns = slices(mid.c);
+        q.act1 = nd.act1; q.act2 = MGI_ACT_NONE;
+        ev.stop = nullptr;
+        hipError_t e = launch_stem(q, fp16_in, st);
+        ev.start = nullptr;
+        ev.stop = saved.stop;
+        if (e == hipSuccess) e = launch_split_dw(p, nd, sp, y, bf, st);
+        ev = saved;
+        return e;
+    }
+    StemDwParams q{};
+    stemdw_shape(p, nd, q);
+    q.bf16 = bf;
+    q.x = buf_ptr(p, nd.in[0], B);
+    q.w = (const h8 *)(wbase + nd.w_off);
+    q.bias = (const float *)(wbase + nd.b_off);
+    q.dw_w = (const h8 *)(wbase + nd.dw_w_off);
+    q.dw_b = (const float *)(wbase + nd.dw_b_off);
+    q.y = (h8 *)y;
+    return launch_stemdw(q, nd.pwdw_cfg, fp16_in, st);
+}
+
+hipError_t launch_dwpw_node(const mgi_plan &p, const Node &nd, const Bases &B, void *y, hipStream_t st) {
+    const char *wbase = static_cast<const char *>(p.dev_w);
+    const Shape os = p.bufs[nd.out].shape;
+    const bool bf = p.opt.dtype == MGI_DTYPE_BF16;
+    const Buf &ib = p.bufs[nd.in[0]];
+    DwPwParams q{};
+    q.x = (const h8 *)buf_ptr(p, nd.in[0], B);
+    q.dww = (const h8 *)(wbase + nd.dw_w_off);
+    q.dwb = (const float *)(wbase + nd.dw_b_off);
+    q.zero = (const h8 *)(wbase + p.zero_off);
+    q.N = ib.shape.n; q.H = ib.shape.h; q.W = ib.shape.w; q.OH = os.h; q.OW = os.w;
+    q.sh = nd.dw_conv.stride_h; q.sw = nd.dw_conv.stride_w;
+    q.pt = nd.dw_conv.pad_t; q.pl = nd.dw_conv.pad_l; q.act = nd.dw_act;
+    GemmParams &g = q.g;
+    g.bf16 = bf;
+    g.w = (const h8 *)(wbase + nd.w_off);
+    g.bias = (const float *)(wbase + nd.b_off);
+    g.res = nd.residual >= 0 ? (const h8 *)buf_ptr(p, nd.residual, B) : nullptr;
+    g.y = y;
+    g.M = (int)os.pixels();
+    g.Min = g.M;
+    g.ksl = nd.ksl; g.ksp = nd.ksp;
+    g.nb16 = nd.nb16; g.ns = slices(os.c); g.cout = os.c;
+    g.act1 = nd.act1; g.act2 = nd.act2;
+    DwPwTile t;
+    if (!dwpw_tile(os.h, os.w, q.sh, os.n, t, nd.tile.bm > 0 ? nd.tile.bm : 128))
+        return hipErrorInvalidValue;
+    return launch_dwpw(q, t, st);
+}
+
 hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStream_t st) {
     const char *wbase = static_cast<const char *>(p.dev_w);
     const Buf &ob = p.bufs[nd.out];
@@ -144,38 +404,8 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
             q.act1 = nd.act1; q.act2 = nd.act2;
             return launch_stem(q, ib.in_dtype == MGI_DTYPE_FP16, st);
         }
-        case NodeKind::FcSoftmax: {
-            // FC + softmax: one FC launch whose last workgroup per row tile
-            // runs the softmax, or (split) the FC into the logits scratch and
-            // the softmax kernel
-            const Shape lg = p.bufs[nd.scratch].shape;
-            float *logits = (float *)buf_ptr(p, nd.scratch, B);
-            GemmParams q{};
-            q.bf16 = bf;
-            q.x = (const h8 *)buf_ptr(p, nd.in[0], B);
-            q.w = (const h8 *)(wbase + nd.w_off);
-            q.bias = (const float *)(wbase + nd.b_off);
-            q.y = logits;
-            q.M = (int)lg.pixels();
-            q.Min = (int)p.bufs[nd.in[0]].shape.pixels();
-            q.ksl = nd.ksl; q.ksp = nd.ksp;
-            q.nb16 = nd.nb16; q.ns = slices(lg.c); q.cout = lg.c;
-            q.act1 = nd.act1; q.act2 = nd.act2;
-            if (!nd.split) {
-                q.sm_y = (float *)y;
-                q.sm_cnt = (int *)(B.ws + nd.cnt_off);
-                return launch_fc(q, nd.tile.wm, nd.tile.pf, st);
-            }
-            LaunchEvents &ev = launch_events();
-            const LaunchEvents saved = ev;
-            ev.stop = nullptr;
-            hipError_t e = launch_fc(q, nd.tile.wm, nd.tile.pf, st);
-            ev.start = nullptr;
-            ev.stop = saved.stop;
-            if (e == hipSuccess) e = launch_softmax(logits, (float *)y, q.M, q.cout, st);
-            ev = saved;
-            return e;
-        }
+        case NodeKind::FcSoftmax:
+            return launch_fcsoftmax_node(p, nd, B, y, st);
         case NodeKind::Gemm:
         case NodeKind::FC: {
             const Buf &ib = p.bufs[nd.in[0]];
@@ -202,213 +432,16 @@ hipError_t launch_node(const mgi_plan &p, const Node &nd, const Bases &B, hipStr
             if (nd.tile.slab) return launch_gemm_xs(q, nd.tile.wm, nd.tile.bn, nd.tile.pf, false, st);
             return launch_gemm(q, nd.tile.bm, nd.tile.bn, nd.taps, nd.kind == NodeKind::FC, st);
         }
-        case NodeKind::DwPw: {
-            const Buf &ib = p.bufs[nd.in[0]];
-            DwPwParams q{};
-            q.x = (const h8 *)buf_ptr(p, nd.in[0], B);
-            q.dww = (const h8 *)(wbase + nd.dw_w_off);
-            q.dwb = (const float *)(wbase + nd.dw_b_off);
-            q.zero = (const h8 *)(wbase + p.zero_off);
-            q.N = ib.shape.n; q.H = ib.shape.h; q.W = ib.shape.w; q.OH = os.h; q.OW = os.w;
-            q.sh = nd.dw_conv.stride_h; q.sw = nd.dw_conv.stride_w;
-            q.pt = nd.dw_conv.pad_t; q.pl = nd.dw_conv.pad_l; q.act = nd.dw_act;
-            GemmParams &g = q.g;
-            g.bf16 = bf;
-            g.w = (const h8 *)(wbase + nd.w_off);
-            g.bias = (const float *)(wbase + nd.b_off);
-            g.res = nd.residual >= 0 ? (const h8 *)buf_ptr(p, nd.residual, B) : nullptr;
-            g.y = y;
-            g.M = (int)os.pixels();
-            g.Min = g.M;
-            g.ksl = nd.ksl; g.ksp = nd.ksp;
-            g.nb16 = nd.nb16; g.ns = slices(os.c); g.cout = os.c;
-            g.act1 = nd.act1; g.act2 = nd.act2;
-            DwPwTile t;
-            if (!dwpw_tile(os.h, os.w, q.sh, os.n, t, nd.tile.bm > 0 ? nd.tile.bm : 128))
-                return hipErrorInvalidValue;
-            return launch_dwpw(q, t, st);
-        }
-        case NodeKind::Irb: {
-            const Shape d = nd.dw_out;
-            if (nd.mode == 0) {
-                IrbParams q{};
-                q.bf16 = bf;
-                q.x = (const h8 *)buf_ptr(p, nd.in[0], B);
-                q.w = (const h8 *)(wbase + nd.w_off);
-                q.bias = (const float *)(wbase + nd.b_off);
-                q.M = (int)nd.dw_in.pixels();
-                q.ksl = nd.ksl; q.ksp = nd.ksp; q.nb16 = nd.nb16; q.act1 = nd.act1;
-                q.dw_w = (const h8 *)(wbase + nd.dw_w_off);
-                q.dw_b = (const float *)(wbase + nd.dw_b_off);
-                q.ns = slices(d.c); q.act2 = nd.dw_act;
-                q.pw = (const h8 *)(wbase + nd.pj_w_off);
-                q.pbias = (const float *)(wbase + nd.pj_b_off);
-                q.pksp = nd.pj_ksp; q.pnb16 = nd.pj_nb16; q.pact1 = nd.pj_act1; q.pact2 = nd.pj_act2;
-                q.res = nd.residual >= 0 ? (const h8 *)buf_ptr(p, nd.residual, B) : nullptr;
-                q.y = (h8 *)y;
-                q.ps = slices(os.c); q.MO = (int)os.pixels();
-                q.N = nd.dw_in.n; q.H = nd.dw_in.h; q.W = nd.dw_in.w; q.OH = d.h; q.OW = d.w;
-                q.S = nd.dw_conv.stride_h; q.pt = nd.dw_conv.pad_t; q.pl = nd.dw_conv.pad_l;
-                return launch_irb(q, nd.pwdw_cfg, st);
-            }
-            // split forms: the expansion and depthwise into the depthwise
-            // scratch (one fused kernel, or the GEMM and the depthwise kernel),
-            // then the projection GEMM; a timed run stamps the first kernel's
-            // start and the last one's end
-            LaunchEvents &ev = launch_events();
-            const LaunchEvents saved = ev;
-            void *d2 = buf_ptr(p, nd.scratch2, B);
-            hipError_t e;
-            ev.stop = nullptr;
-            if (nd.mode == 1) {
-                e = launch_node_pwdw(p, nd, B, d2, slices(d.c), bf, st);
-            } else {
-                e = launch_node_expand(p, nd, B, bf, st);
-                ev.start = nullptr;
-                if (e == hipSuccess) e = launch_split_dw(p, nd, buf_ptr(p, nd.scratch, B), d2, bf, st);
-            }
-            ev.start = nullptr;
-            ev.stop = saved.stop;
-            if (e == hipSuccess) {
-                GemmParams g{};
-                g.bf16 = bf;
-                g.x = (const h8 *)d2;
-                g.w = (const h8 *)(wbase + nd.pj_w_off);
-                g.bias = (const float *)(wbase + nd.pj_b_off);
-                g.res = nd.residual >= 0 ? (const h8 *)buf_ptr(p, nd.residual, B) : nullptr;
-                g.y = y;
-                g.M = g.Min = (int)os.pixels();
-                g.ksl = nd.pj_ksl; g.ksp = nd.pj_ksp;
-                g.nb16 = nd.pj_nb16; g.ns = slices(os.c); g.cout = os.c;
-                g.act1 = nd.pj_act1; g.act2 = nd.pj_act2;
-                e = launch_gemm_tile(g, nd.pj_tile, st);
-            }
-            ev = saved;
-            return e;
-        }
-        case NodeKind::PwDw: {
-            if (nd.split) {
-                // the pointwise GEMM into the scratch tensor, then the depthwise
-                // kernel; a timed run stamps the first kernel's start and the
-                // second one's end
-                LaunchEvents &ev = launch_events();
-                const LaunchEvents saved = ev;
-                const Shape mid = nd.dw_in;
-                void *sp = buf_ptr(p, nd.scratch, B);
-                GemmParams g{};
-                g.bf16 = bf;
-                g.x = (const h8 *)buf_ptr(p, nd.in[0], B);
-                g.w = (const h8 *)(wbase + nd.w_off);
-                g.bias = (const float *)(wbase + nd.b_off);
-                g.y = sp;
-                g.M = g.Min = (int)mid.pixels();
-                g.ksl = nd.ksl; g.ksp = nd.ksp;
-                g.nb16 = nd.nb16; g.ns = slices(mid.c); g.cout = mid.c;
-                g.act1 = nd.act1; g.act2 = MGI_ACT_NONE;
-                ev.stop = nullptr;
-                hipError_t e = nd.tile.ks == 8 ? launch_gemm_pipe_k8(g, false, st)
-                                               : launch_gemm_pipe(g, nd.tile.bm, nd.tile.bn, st);
-                ev.start = nullptr;
-                ev.stop = saved.stop;
-                if (e == hipSuccess) e = launch_split_dw(p, nd, sp, y, bf, st);
-                ev = saved;
-                return e;
-            }
-            PwDwParams q{};
-            q.bf16 = bf;
-            q.x = (const h8 *)buf_ptr(p, nd.in[0], B);
-            q.w = (const h8 *)(wbase + nd.w_off);
-            q.bias = (const float *)(wbase + nd.b_off);
-            q.M = (int)nd.dw_in.pixels();
-            q.ksl = nd.ksl; q.ksp = nd.ksp; q.nb16 = nd.nb16; q.act1 = nd.act1;
-            q.dw_w = (const h8 *)(wbase + nd.dw_w_off);
-            q.dw_b = (const float *)(wbase + nd.dw_b_off);
-            q.y = (h8 *)y;
-            q.N = nd.dw_in.n; q.H = nd.dw_in.h; q.W = nd.dw_in.w; q.OH = os.h; q.OW = os.w;
-            q.S = nd.dw_conv.stride_h; q.pt = nd.dw_conv.pad_t; q.pl = nd.dw_conv.pad_l;
-            q.act2 = nd.dw_act;
-            q.ns = slices(os.c);
-            return launch_pwdw(q, nd.pwdw_cfg, st);
-        }
-        case NodeKind::GemmPool: {
-            // pointwise GEMM + global average pool: the pooled GEMM kernel,
-            // or (split) the GEMM into the scratch tensor and the pool kernel
-            const Shape mid = nd.dw_in;
-            GemmParams g{};
-            g.bf16 = bf;
-            g.x = (const h8 *)buf_ptr(p, nd.in[0], B);
-            g.w = (const h8 *)(wbase + nd.w_off);
-            g.bias = (const float *)(wbase + nd.b_off);
-            g.M = g.Min = (int)mid.pixels();
-            g.ksl = nd.ksl; g.ksp = nd.ksp;
-            g.nb16 = nd.nb16; g.ns = slices(mid.c); g.cout = mid.c;
-            g.act1 = nd.act1; g.act2 = MGI_ACT_NONE;
-            if (!nd.split) {
-                g.y = y;
-                g.hw = mid.h * mid.w;
-                g.nimg = mid.n;
-                if (nd.tile.slab) return launch_gemm_xs(g, nd.tile.wm, nd.tile.bn, nd.tile.pf, true, st);
-                if (nd.tile.ks == 8) return launch_gemm_pipe_k8(g, true, st);
-                return launch_gemm_pool(g, nd.tile.bm, nd.tile.bn, st);
-            }
-            LaunchEvents &ev = launch_events();
-            const LaunchEvents saved = ev;
-            void *sp = buf_ptr(p, nd.scratch, B);
-            g.y = sp;
-            ev.stop = nullptr;
-            hipError_t e = launch_gemm_pipe(g, nd.tile.bm, nd.tile.bn, st);
-            ev.start = nullptr;
-            ev.stop = saved.stop;
-            if (e == hipSuccess)
-                e = launch_gap((const h8 *)sp, (h8 *)y, (const h8 *)(wbase + p.zero_off), mid.n, mid.h * mid.w,
-                               slices(mid.c), bf, st);
-            ev = saved;
-            return e;
-        }
-        case NodeKind::StemDw: {
-            const Buf &ib = p.bufs[nd.in[0]];
-            const bool fp16_in = ib.in_dtype == MGI_DTYPE_FP16;
-            if (nd.split) {
-                // the stem kernel into the scratch tensor, then the depthwise
-                // kernel (timed as one: first kernel's start, second's end)
-                LaunchEvents &ev = launch_events();
-                const LaunchEvents saved = ev;
-                const Shape mid = nd.dw_in;
-                void *sp = buf_ptr(p, nd.scratch, B);
-                StemParams q{};
-                q.bf16 = bf;
-                q.x = buf_ptr(p, nd.in[0], B);
-                q.w = (const h8 *)(wbase + nd.w_off);
-                q.bias = (const float *)(wbase + nd.b_off);
-                q.res = nullptr;
-                q.y = (h8 *)sp;
-                q.N = ib.shape.n; q.H = ib.shape.h; q.W = ib.shape.w; q.C = ib.shape.c;
-                q.OH = mid.h; q.OW = mid.w; q.M = (int)mid.pixels();
-                q.KH = nd.conv.kh; q.KW = nd.conv.kw; q.K = nd.conv.kh * nd.conv.kw * ib.shape.c;
-                q.sh = nd.conv.stride_h; q.sw = nd.conv.stride_w;
-                q.dh = nd.conv.dil_h; q.dw = nd.conv.dil_w;
-                q.pt = nd.conv.pad_t; q.pl = nd.conv.pad_l;
-                q.nb16 = nd.nb16; q.ns = slices(mid.c);
-                q.act1 = nd.act1; q.act2 = MGI_ACT_NONE;
-                ev.stop = nullptr;
-                hipError_t e = launch_stem(q, fp16_in, st);
-                ev.start = nullptr;
-                ev.stop = saved.stop;
-                if (e == hipSuccess) e = launch_split_dw(p, nd, sp, y, bf, st);
-                ev = saved;
-                return e;
-            }
-            StemDwParams q{};
-            stemdw_shape(p, nd, q);
-            q.bf16 = bf;
-            q.x = buf_ptr(p, nd.in[0], B);
-            q.w = (const h8 *)(wbase + nd.w_off);
-            q.bias = (const float *)(wbase + nd.b_off);
-            q.dw_w = (const h8 *)(wbase + nd.dw_w_off);
-            q.dw_b = (const float *)(wbase + nd.dw_b_off);
-            q.y = (h8 *)y;
-            return launch_stemdw(q, nd.pwdw_cfg, fp16_in, st);
-        }
+        case NodeKind::DwPw:
+            return launch_dwpw_node(p, nd, B, y, st);
+        case NodeKind::Irb:
+            return launch_irb_node(p, nd, B, y, st);
+        case NodeKind::PwDw:
+            return launch_pwdw_node(p, nd, B, y, st);
+        case NodeKind::GemmPool:
+            return launch_gemmpool_node(p, nd, B, y, st);
+        case NodeKind::StemDw:
+            return launch_stemdw_node(p, nd, B, y, st);
         case NodeKind::Depthwise: {
             const Buf &ib = p.bufs[nd.in[0]];
             DwParams q{};
