@@ -256,7 +256,8 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) void st
     // = value group e % upr of row r0 + e / upr (a thread's units are e = tid
     // + u * NT, their row and column offsets computed once); rows outside the
     // image are zeros.  The first UMAX * NT units go through registers
-    // (stage_issue, then stage_store); any rest is copied in stage_store.
+    // (stage_issue, then stage_store) when they are 16-byte vectors; any rest,
+    // and every single-value unit, is copied in stage_store.
     typedef TIN tv __attribute__((ext_vector_type(VN)));
     tv reg[UMAX];
     int urow[UMAX], ucol[UMAX];
@@ -287,21 +288,23 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) void st
             ((uint16_t *)dst)[c] = E::bits(inside ? (float)v[0] : 0.0f);
         }
     };
+    // (only 16-byte units go through registers: a load whose destination
+    // depends on a run-time choice of unit size would be merged by register
+    // copies right after it, which wait for the load to return)
     auto stage_issue = [&](int r0, int r1) {
+        if (!vec) return;
 #pragma unroll
         for (int u = 0; u < UMAX; ++u)
-            if (urow[u] < r1 - r0) {
-                const TIN *src = src_of(r0 + urow[u], ucol[u]);
-                if (vec) reg[u] = *(const tv *)src;
-                else reg[u][0] = *src;
-            }
+            if (urow[u] < r1 - r0) reg[u] = *(const tv *)src_of(r0 + urow[u], ucol[u]);
     };
     auto stage_store = [&](int r0, int r1) {
+        if (vec) {
 #pragma unroll
-        for (int u = 0; u < UMAX; ++u)
-            if (urow[u] < r1 - r0) put(r0 + urow[u], ucol[u], reg[u]);
+            for (int u = 0; u < UMAX; ++u)
+                if (urow[u] < r1 - r0) put(r0 + urow[u], ucol[u], reg[u]);
+        }
         const int total = (r1 - r0) * upr;
-        for (int e = tid + UMAX * NT; e < total; e += NT) {
+        for (int e = tid + (vec ? UMAX * NT : 0); e < total; e += NT) {
             const int rr = e / upr, c = e - rr * upr;
             const TIN *src = src_of(r0 + rr, c);
             tv v;
@@ -426,6 +429,11 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) void st
     stem_step(ub(0), ue(0));
     __syncthreads();
     if (nsteps > 1) stage_store(ie(0), ie(1));
+    // (every load of the prologue has returned here; waiting for them in so
+    // many words keeps the loop's waits to the loads the loop issues, instead
+    // of waits for the weight, tap and bias registers that the compiler
+    // cannot prove loaded and so places after each step's row loads)
+    wait_vm_lds<0>();
     __syncthreads();
     for (int j = 0; j < nsteps; ++j) {
         const bool more = j + 2 < nsteps;
@@ -433,6 +441,10 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) void st
         if (j + 1 < nsteps) stem_step(ub(j + 1), ue(j + 1));
         dw_step(j);
         if (more) stage_store(ie(j + 1), ie(j + 2));
+        // (the staging registers count as read on every path, so that the
+        // next step's loads into them wait for nothing)
+#pragma unroll
+        for (int u = 0; u < UMAX; ++u) asm volatile("" ::"v"(reg[u]));
         __syncthreads();
     }
 }
