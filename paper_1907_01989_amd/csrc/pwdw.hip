@@ -394,6 +394,15 @@ constexpr Inst kInsts[] = {
     {true, 4, 9, 1, 2, 2, 64, 1, "band2x16w4"},  {true, 4, 4, 1, 1, 2, 64, 2, "band2x16w4"},   // 112 -> 56, 56 x 56
     {true, 4, 5, 1, 2, 2, 32, 2, "band2x16w4"},  {true, 4, 3, 1, 1, 4, 32, 4, "band4x16w4"},   // 56 -> 28, 28 x 28
     {true, 4, 3, 1, 2, 2, 16, 4, "band2x16w4"},                                                // 28 -> 14
+    // taller bands with 4 waves: less halo recomputation than 2- and 4-row
+    // bands (a 7-row band computes 9 input rows of the pointwise output per
+    // 7 output rows, a 2-row band 4 per 2), and 7 rows divide the 56 and 28
+    // planes (measured on those planes at a batch of 64: 56 x 56 x 128 21.4
+    // against 26.0 us for the best shorter band, 56 x 56 x 144 23.8 against
+    // 30.4, 28 x 28 x 192 12.0 against 13.5; 6- and 8-row bands, 48-channel
+    // tiles and 7-row bands of 14 x 14 planes measured slower)
+    {true, 4, 6, 2, 1, 4, 64, 2, "band4x32w4"},  {true, 4, 8, 2, 1, 7, 64, 2, "band7x32w4"},   // 56 x 56
+    {true, 4, 4, 4, 1, 7, 32, 4, "band7x64w4"},                                                // 28 x 28
 };
 constexpr int kNumInsts = sizeof(kInsts) / sizeof(kInsts[0]);
 

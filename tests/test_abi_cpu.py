@@ -285,7 +285,7 @@ def test_node_configuration_candidates():
         elif n["kind"] == "dw_conv":
             assert k == 3 and name.startswith("rows")
         elif n["kind"] == "pw_dw":
-            assert 2 <= k <= 10 and name.startswith(("img", "band", "split"))
+            assert 2 <= k <= 12 and name.startswith(("img", "band", "split"))
         elif n["kind"] == "stem_dw":
             assert k == 6 and name.startswith(("band", "split"))
         elif n["kind"] == "pw_pool":

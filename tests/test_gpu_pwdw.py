@@ -8,7 +8,8 @@ the split form (the two separate kernels through a scratch tensor) -- and
 the unfused plan must agree bit for bit.  Every case is also held to the
 oracle at the chained-layer bound.  Shapes cover both strides, TF-SAME and
 symmetric padding, whole-image tiles (several images per tile, ragged last
-tile) and row bands (every v1 band shape, odd planes with a short last band),
+tile) and row bands (every v1 band shape, 2- to 7-row bands, odd planes with a
+short last band),
 partial channel tiles (v2's 96 and 144 channels), channel counts that end in
 half a 16-channel block, K tails and single slices, and batch 1.
 """
@@ -49,6 +50,7 @@ CASES = [
     (2, 27, 29, 40, 80, 1, None, ACT_NONE),         # odd plane, last band short, K tail
     (2, 55, 53, 24, 64, 2, (1, 1, 1, 1), ACT_RELU6),  # odd plane at stride 2, symmetric padding
     (2, 28, 28, 40, 72, 1, None, ACT_RELU6),        # 9 output slices in bands (channels = 8 mod 16)
+    (2, 45, 45, 40, 96, 1, None, ACT_RELU6),        # 7-row bands with a 3-row last band, K tail
 ]
 
 
