@@ -647,7 +647,10 @@ template <typename E, int FM, int B, bool SM>
 __global__ __launch_bounds__(256) void fc_kernel(GemmParams p) {
     __shared__ f4 red[4][FM][64];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int nb = blockIdx.x % p.nb16, mt = blockIdx.x / p.nb16;
+    // the row tiles of one 16-channel weight block are neighbouring tiles,
+    // which xcd_tile puts on one XCD: each weight block is read into one L2
+    const int mtiles = gridDim.x / p.nb16, t = xcd_tile(blockIdx.x, gridDim.x);
+    const int nb = t / mtiles, mt = t - nb * mtiles;
     const int m0 = mt * 16 * FM;
     const int ksteps = p.ksp >> 2;
     const int per = (ksteps + 3) >> 2;
